@@ -1,0 +1,214 @@
+/*
+ * moe_stage.h -- C ABI of the MI355X (gfx950) MoE expert stage.
+ *
+ * One expert-parallel rank's expert stage with the return all-to-all
+ * overlapped by tile-level signaling (paper Section 3: "Fine-grained
+ * Computation-Communication Overlap via Tile-level Signaling and Scheduling
+ * for Mixture-of-Experts").
+ *
+ * Problem (paper Section 2.1, steps 3-4, and Section 3.1): the rank owns
+ * num_local_experts experts.  After the dispatch all-to-all it holds `rows`
+ * routed token copies, expert-contiguous in `dispatched_x`.  For every row i
+ * of local expert e it computes the SiLU-gated FFN
+ *     y_i = W2_e * bf16( silu(W1_e x_i) (.) (W3_e x_i) ),  silu(g) = g/(1+e^-g)
+ * and returns y_i to the rank the token came from, at the slot that rank
+ * reserved for it:
+ *     return_bufs[row_src_rank[i]][row_slot[i], :] = bf16_rne(y_i)
+ * No other byte of the return buffers is written.  The outputs are not
+ * gate-weighted (the weighted reduction happens on the owner, Section 2.1
+ * step 5).  On one GPU, `return_bufs[r]` stands in for source rank r's receive
+ * buffer; the transfer is a device copy inside local HBM.
+ *
+ * Layouts (all bf16 tensors row-major, 2-byte elements):
+ *   dispatched_x  device  [rows, hidden]
+ *   w1, w3        device  [num_local_experts, ffn, hidden]   (row f = output feature f)
+ *   w2            device  [num_local_experts, hidden, ffn]
+ *   return_bufs   host array of num_ranks device pointers; buffer r is
+ *                 [return_rows[r], hidden]
+ *   expert_offsets, row_src_rank, row_slot, return_rows: host arrays.
+ *
+ * Ownership: the caller owns every tensor and keeps it alive until the work
+ * enqueued on `stream` has completed.  Host arrays may be freed as soon as a
+ * call returns.  The handle owns its workspaces (intermediate activation,
+ * staged output, flags, counters, plan buffers), the CU-masked streams and
+ * events it creates; no device memory is allocated per run.  A handle is not
+ * thread-safe and runs one stage at a time (a run waits for the previous
+ * run's plan upload before reusing its staging memory).
+ *
+ * Errors: every call returns MOE_OK (0) or a negative code.  Validation runs
+ * before anything is enqueued, so a failed call leaves the stream untouched.
+ * moe_stage_last_error() describes the most recent failure of a handle.
+ */
+#ifndef MOE_STAGE_H
+#define MOE_STAGE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_OK 0
+#define MOE_EINVAL (-1)       /* null pointer, non-positive dimension, bad config value        */
+#define MOE_EROUTING (-2)     /* offsets not 0..rows monotone, rank out of range, slot outside  */
+                              /* its receive buffer, or two rows with the same (rank, slot)     */
+#define MOE_ECAPACITY (-3)    /* rows > max_rows, or the plan exceeds the handle's workspaces   */
+#define MOE_EHIP (-4)         /* a HIP runtime call failed (message names it)                  */
+#define MOE_ETIMEOUT (-5)     /* a bounded device wait expired; sticky until the next query   */
+#define MOE_EUNSUPPORTED (-6) /* hidden/ffn not multiples of 64, cu_split out of range         */
+
+/* Config flags */
+#define MOE_LOCAL_DIRECT (1u << 0) /* overlapped run: rows whose source is self_rank are written
+                                      by the producer epilogue straight into return_bufs[self];
+                                      local tiles need no transfer (paper Section 3.2.3)       */
+#define MOE_KERNEL_TIMING (1u << 1) /* record HIP events around each kernel of every run       */
+#define MOE_POISON (1u << 2)        /* fill the staged output with NaN before each run, so a
+                                       copy that races ahead of its data is detectable          */
+
+typedef struct moe_stage_s* moe_stage_t;
+
+typedef struct {
+  int32_t hidden;            /* H, multiple of 64                                             */
+  int32_t ffn;               /* F, multiple of 64                                             */
+  int32_t num_local_experts; /* E_l >= 1                                                      */
+  int32_t num_ranks;         /* R >= 1 source ranks                                           */
+  int32_t self_rank;         /* 0 <= self_rank < R; rows from it are local (Section 3.2.1)    */
+  int32_t max_rows;          /* capacity of one run; sizes the workspaces                     */
+  int32_t band_rows;         /* tb_M of the remote-owner-aligned layout (Section 3.2.1): each
+                                remote owner group is padded to a multiple of it, so every
+                                band of band_rows rows has one destination.  Power of two in
+                                [1, 256]; 0 picks a default.                                  */
+  int32_t mid_segment_bands; /* x of Section 3.3.2 (mgb in the evaluation): bands per middle
+                                transfer segment; first and last segments of a group are one
+                                band.  >= 1; 0 means 1.                                       */
+  uint32_t flags;            /* MOE_* flags above                                            */
+  int32_t watchdog_ms;       /* bound on every device spin-wait; 0 = 2000 ms                  */
+} moe_stage_config_t;
+
+/* Statistics of the most recent run (moe_stage_query). */
+typedef struct {
+  int64_t n_valid;          /* routed rows                                                   */
+  int64_t n_logical_rows;   /* rows of the padded layout, incl. band and tile padding        */
+  int64_t n_band_padding;   /* zero rows inserted at owner-group boundaries (Section 4.5)    */
+  int64_t n_remote_rows;    /* rows whose source rank is not self_rank                      */
+  int32_t n_tile_rows;      /* 256-row GEMM tile rows                                        */
+  int32_t n_bands;
+  int32_t n_gu_items;       /* gate/up tiles                                                */
+  int32_t n_down_items;     /* down-projection tiles (each raises one ready flag)           */
+  int32_t n_segments;       /* transfer segments issued by the consumer                      */
+  int32_t producer_grid;    /* persistent producer workgroups launched                      */
+  int32_t consumer_grid;    /* persistent consumer workgroups launched                      */
+  int32_t consumer_cus;     /* compute units reserved for the consumer (cu_split rounded up
+                               to a multiple of the XCD count; 0 for serial runs)            */
+  int32_t timeout;          /* 1 if a device wait hit the watchdog                           */
+  double plan_us;           /* host time to validate and build the plan                      */
+  uint64_t poll_iters;      /* consumer flag-poll iterations summed over segments            */
+  uint64_t wait_ticks;      /* consumer time spent waiting for flags (100 MHz ticks)         */
+  uint64_t producer_wait_ticks; /* producer time spent waiting on gate/up dependencies       */
+} moe_stage_stats_t;
+
+/* Accumulated kernel times (MOE_KERNEL_TIMING), milliseconds, over runs since the last reset. */
+typedef struct {
+  int32_t runs;
+  double stage_ms;     /* fork to join of each run (overlapped) or first to last kernel (serial) */
+  double producer_ms;  /* producer kernel                                                */
+  double consumer_ms;  /* consumer kernel (overlapped runs)                              */
+  double scatter_ms;   /* scatter kernel (serial runs)                                   */
+} moe_stage_times_t;
+
+/* Creates a handle and its device workspaces on the current HIP device. */
+int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out);
+
+/*
+ * Overlapped stage (paper Section 3.3): builds the remote-owner-aligned row
+ * layout, remote-first tile schedule and combine plan (Section 3.2, Algorithm
+ * 1) on the host, then launches a persistent consumer on `cu_split` compute
+ * units and the persistent rank-wide producer on the remaining ones.  The
+ * producer raises a ready flag per finished down-projection tile; the
+ * consumer copies each ready segment into return_bufs[destination].  The
+ * work is ordered after prior work on `stream` (a hipStream_t; NULL = null
+ * stream) and later work on `stream` sees the results.
+ *
+ * cu_split: compute units for the consumer, 1 <= cu_split <= CUs - XCDs.  Workgroups
+ * are dealt round-robin over the XCDs (8 on MI355X) and a CU-masked queue must own
+ * CUs on each of them, so the split is rounded up to a multiple of the XCD count
+ * (the stats report the effective value); the producer gets every other CU.
+ */
+int moe_stage_run(moe_stage_t h, const void* dispatched_x, const int32_t* expert_offsets,
+                  const int32_t* row_src_rank, const int32_t* row_slot, const void* w1,
+                  const void* w3, const void* w2, void* const* return_bufs,
+                  const int64_t* return_rows, int32_t cu_split, void* stream);
+
+/*
+ * Non-overlapped baseline (paper Section 4.1.3: expert compute, then the
+ * whole return transfer): the same producer on all compute units with no
+ * signaling, then one scatter kernel that copies every routed row to its slot.
+ */
+int moe_stage_run_serial(moe_stage_t h, const void* dispatched_x, const int32_t* expert_offsets,
+                         const int32_t* row_src_rank, const int32_t* row_slot, const void* w1,
+                         const void* w3, const void* w2, void* const* return_bufs,
+                         const int64_t* return_rows, void* stream);
+
+/* Statistics of the last run; synchronizes with it.  Returns MOE_ETIMEOUT once after a timeout. */
+int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out);
+
+/* Kernel times accumulated since the last reset (needs MOE_KERNEL_TIMING); synchronizes. */
+int moe_stage_times(moe_stage_t h, int32_t reset, moe_stage_times_t* out);
+
+/* Human-readable description of the handle's last error ("" if none).  Valid until the next call. */
+const char* moe_stage_last_error(moe_stage_t h);
+
+/* Waits for outstanding work, then frees the handle and everything it owns. */
+int moe_stage_destroy(moe_stage_t h);
+
+/* ---------------------------------------------------------------------------
+ * Host-only plan inspection (no GPU needed).  Builds exactly the plan that
+ * moe_stage_run would use for these arguments and lets the caller read its
+ * tables, so the layout, schedule and combine plan can be checked on a CPU.
+ * ------------------------------------------------------------------------- */
+typedef struct moe_plan_s* moe_plan_t;
+
+typedef struct {
+  int32_t n_tile_rows, n_items, n_gu_items, n_down_items, n_segments, n_bands;
+  int32_t gu_tiles_per_row;   /* gate/up tiles per tile row (ffn / 128, rounded up)          */
+  int32_t down_tiles_per_row; /* down tiles per tile row (hidden / 256, rounded up)          */
+  int32_t tile_m, band_rows;
+  int64_t n_logical_rows, n_valid, n_band_padding, n_remote_rows;
+} moe_plan_info_t;
+
+/* Tables readable with moe_plan_copy:
+ *   MOE_PLAN_TILE_ROWS  int32 [n_tile_rows][4]: expert, first logical row, valid rows, has_remote
+ *   MOE_PLAN_ITEMS      uint32 [n_items]: bit 31 = down tile, bits 30..12 tile row, 11..0 column tile
+ *   MOE_PLAN_ROW_X      int32 [n_logical_rows]: dispatched_x row feeding each logical row
+ *                       (padding rows repeat a valid row of the same expert)
+ *   MOE_PLAN_ROW_RANK   int32 [n_logical_rows]: source rank, -1 for padding
+ *   MOE_PLAN_ROW_SLOT   int32 [n_logical_rows]: receive slot, -1 for padding
+ *   MOE_PLAN_SEGMENTS   int32 [n_segments][8]: dst rank, rows, first logical row, first slot,
+ *                       first flag, flag count, last schedule position it waits for, band count
+ *   MOE_PLAN_BANDS      int32 [n_bands][4]: expert, first logical row, valid rows, dst rank (-1 pad)
+ */
+#define MOE_PLAN_TILE_ROWS 0
+#define MOE_PLAN_ITEMS 1
+#define MOE_PLAN_ROW_X 2
+#define MOE_PLAN_ROW_RANK 3
+#define MOE_PLAN_ROW_SLOT 4
+#define MOE_PLAN_SEGMENTS 5
+#define MOE_PLAN_BANDS 6
+
+/* `producer_grid` models the number of persistent producer workgroups (it sets how far the
+ * down tiles of a tile row lag behind its gate/up tiles); `overlapped` selects the plan of
+ * moe_stage_run (1) or moe_stage_run_serial (0). */
+int moe_plan_build(const moe_stage_config_t* cfg, int64_t rows, const int32_t* expert_offsets,
+                   const int32_t* row_src_rank, const int32_t* row_slot,
+                   const int64_t* return_rows, int32_t producer_grid, int32_t overlapped,
+                   moe_plan_t* out);
+int moe_plan_info(moe_plan_t p, moe_plan_info_t* out);
+/* Copies table `which` into `dst` (host memory of at least `bytes`); returns bytes needed if
+ * dst is NULL, else MOE_OK or MOE_EINVAL when bytes is too small. */
+int64_t moe_plan_copy(moe_plan_t p, int32_t which, void* dst, int64_t bytes);
+void moe_plan_free(moe_plan_t p);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_STAGE_H */

@@ -1,0 +1,285 @@
+"""Thin ctypes binding of ``include/moe_stage.h``.
+
+Argument marshalling only: every step of the expert stage runs in the HIP
+library ``_lib/libmoe_stage.so``.  Functions keep the C names; ``MoeStage`` is a
+small convenience wrapper that accepts torch tensors (device memory) and numpy
+or CPU arrays (routing).  There is no fallback: if the library is missing or no
+GPU is present, calls fail loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "_lib", "libmoe_stage.so")
+
+MOE_OK, MOE_EINVAL, MOE_EROUTING, MOE_ECAPACITY, MOE_EHIP, MOE_ETIMEOUT, MOE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
+MOE_LOCAL_DIRECT, MOE_KERNEL_TIMING, MOE_POISON = 1, 2, 4
+MOE_PLAN_TILE_ROWS, MOE_PLAN_ITEMS, MOE_PLAN_ROW_X, MOE_PLAN_ROW_RANK, MOE_PLAN_ROW_SLOT, MOE_PLAN_SEGMENTS, MOE_PLAN_BANDS = range(7)
+ERROR_NAMES = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EROUTING", -3: "MOE_ECAPACITY", -4: "MOE_EHIP",
+               -5: "MOE_ETIMEOUT", -6: "MOE_EUNSUPPORTED"}
+
+EXPORTED = ["moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query", "moe_stage_times",
+            "moe_stage_last_error", "moe_stage_destroy", "moe_plan_build", "moe_plan_info", "moe_plan_copy",
+            "moe_plan_free"]
+
+
+class moe_stage_config_t(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("ffn", ctypes.c_int32), ("num_local_experts", ctypes.c_int32),
+                ("num_ranks", ctypes.c_int32), ("self_rank", ctypes.c_int32), ("max_rows", ctypes.c_int32),
+                ("band_rows", ctypes.c_int32), ("mid_segment_bands", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("watchdog_ms", ctypes.c_int32)]
+
+
+class moe_stage_stats_t(ctypes.Structure):
+    _fields_ = [("n_valid", ctypes.c_int64), ("n_logical_rows", ctypes.c_int64), ("n_band_padding", ctypes.c_int64),
+                ("n_remote_rows", ctypes.c_int64), ("n_tile_rows", ctypes.c_int32), ("n_bands", ctypes.c_int32),
+                ("n_gu_items", ctypes.c_int32), ("n_down_items", ctypes.c_int32), ("n_segments", ctypes.c_int32),
+                ("producer_grid", ctypes.c_int32), ("consumer_grid", ctypes.c_int32), ("consumer_cus", ctypes.c_int32),
+                ("timeout", ctypes.c_int32),
+                ("plan_us", ctypes.c_double), ("poll_iters", ctypes.c_uint64), ("wait_ticks", ctypes.c_uint64),
+                ("producer_wait_ticks", ctypes.c_uint64)]
+
+
+class moe_stage_times_t(ctypes.Structure):
+    _fields_ = [("runs", ctypes.c_int32), ("stage_ms", ctypes.c_double), ("producer_ms", ctypes.c_double),
+                ("consumer_ms", ctypes.c_double), ("scatter_ms", ctypes.c_double)]
+
+
+class moe_plan_info_t(ctypes.Structure):
+    _fields_ = [("n_tile_rows", ctypes.c_int32), ("n_items", ctypes.c_int32), ("n_gu_items", ctypes.c_int32),
+                ("n_down_items", ctypes.c_int32), ("n_segments", ctypes.c_int32), ("n_bands", ctypes.c_int32),
+                ("gu_tiles_per_row", ctypes.c_int32), ("down_tiles_per_row", ctypes.c_int32),
+                ("tile_m", ctypes.c_int32), ("band_rows", ctypes.c_int32), ("n_logical_rows", ctypes.c_int64),
+                ("n_valid", ctypes.c_int64), ("n_band_padding", ctypes.c_int64), ("n_remote_rows", ctypes.c_int64)]
+
+
+def _struct_dict(s) -> dict:
+    return {name: getattr(s, name) for name, _ in s._fields_}
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"HIP library not built: {path} (run `python -m paper_2607_19539_amd.build`)")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.moe_stage_create.argtypes = [ctypes.POINTER(moe_stage_config_t), ctypes.POINTER(vp)]
+    lib.moe_stage_run.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp]
+    lib.moe_stage_run_serial.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.moe_stage_query.argtypes = [vp, ctypes.POINTER(moe_stage_stats_t)]
+    lib.moe_stage_times.argtypes = [vp, i32, ctypes.POINTER(moe_stage_times_t)]
+    lib.moe_stage_last_error.argtypes = [vp]
+    lib.moe_stage_last_error.restype = ctypes.c_char_p
+    lib.moe_stage_destroy.argtypes = [vp]
+    lib.moe_plan_build.argtypes = [ctypes.POINTER(moe_stage_config_t), i64, vp, vp, vp, vp, i32, i32,
+                                   ctypes.POINTER(vp)]
+    lib.moe_plan_info.argtypes = [vp, ctypes.POINTER(moe_plan_info_t)]
+    lib.moe_plan_copy.argtypes = [vp, i32, vp, i64]
+    lib.moe_plan_copy.restype = ctypes.c_int64
+    lib.moe_plan_free.argtypes = [vp]
+    lib.moe_plan_free.restype = None
+    for name in ("moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query",
+                 "moe_stage_times", "moe_stage_destroy", "moe_plan_build", "moe_plan_info"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+class MoeError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERROR_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+def _host_i32(a) -> np.ndarray:
+    if hasattr(a, "detach"):
+        a = a.detach().cpu().numpy()
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _host_i64(a) -> np.ndarray:
+    if hasattr(a, "detach"):
+        a = a.detach().cpu().numpy()
+    return np.ascontiguousarray(a, dtype=np.int64)
+
+
+def _np_ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dev_ptr(t) -> int:
+    """Device pointer of a contiguous torch tensor (or a raw integer address)."""
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous device tensor")
+    return t.data_ptr()
+
+
+# ----------------------------------------------------------------------------- C-named functions
+
+def make_config(hidden, ffn, num_local_experts, num_ranks, self_rank, max_rows, band_rows=0,
+                mid_segment_bands=1, flags=MOE_LOCAL_DIRECT, watchdog_ms=0) -> moe_stage_config_t:
+    return moe_stage_config_t(hidden, ffn, num_local_experts, num_ranks, self_rank, max_rows, band_rows,
+                              mid_segment_bands, flags, watchdog_ms)
+
+
+def moe_stage_last_error(h=None) -> str:
+    s = load().moe_stage_last_error(h)
+    return s.decode() if s else ""
+
+
+def _check(rc: int, h=None) -> int:
+    if rc != MOE_OK:
+        raise MoeError(rc, moe_stage_last_error(h))
+    return rc
+
+
+def moe_stage_create(cfg: moe_stage_config_t) -> int:
+    h = ctypes.c_void_p()
+    _check(load().moe_stage_create(ctypes.byref(cfg), ctypes.byref(h)))
+    return h.value
+
+
+def _run_args(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows):
+    off, src, slot = _host_i32(expert_offsets), _host_i32(row_src_rank), _host_i32(row_slot)
+    rr = _host_i64(return_rows if return_rows is not None else [b.shape[0] for b in return_bufs])
+    ptrs = (ctypes.c_void_p * len(return_bufs))(*[_dev_ptr(b) for b in return_bufs])
+    keep = (off, src, slot, rr, ptrs)
+    args = [_dev_ptr(x) if x is not None else None, _np_ptr(off), _np_ptr(src), _np_ptr(slot),
+            _dev_ptr(w1) if w1 is not None else None, _dev_ptr(w3) if w3 is not None else None,
+            _dev_ptr(w2) if w2 is not None else None, ctypes.cast(ptrs, ctypes.c_void_p), _np_ptr(rr)]
+    return args, keep
+
+
+def _stream_ptr(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def moe_stage_run(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs: Sequence,
+                  return_rows=None, cu_split: int = 8, stream=None) -> int:
+    args, keep = _run_args(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows)
+    rc = load().moe_stage_run(h, *args, int(cu_split), _stream_ptr(stream))
+    del keep
+    return _check(rc, h)
+
+
+def moe_stage_run_serial(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs: Sequence,
+                         return_rows=None, stream=None) -> int:
+    args, keep = _run_args(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows)
+    rc = load().moe_stage_run_serial(h, *args, _stream_ptr(stream))
+    del keep
+    return _check(rc, h)
+
+
+def moe_stage_query(h, check: bool = True) -> dict:
+    st = moe_stage_stats_t()
+    rc = load().moe_stage_query(h, ctypes.byref(st))
+    d = _struct_dict(st)
+    d["rc"] = rc
+    if check:
+        _check(rc, h)
+    return d
+
+
+def moe_stage_times(h, reset: bool = False) -> dict:
+    t = moe_stage_times_t()
+    _check(load().moe_stage_times(h, int(reset), ctypes.byref(t)), h)
+    return _struct_dict(t)
+
+
+def moe_stage_destroy(h) -> int:
+    return _check(load().moe_stage_destroy(h))
+
+
+def moe_plan_build(cfg: moe_stage_config_t, expert_offsets, row_src_rank, row_slot, return_rows,
+                   producer_grid: int = 256, overlapped: bool = True) -> dict:
+    """Build the plan on the host and return its tables as numpy arrays (no GPU needed)."""
+    lib = load()
+    off, src, slot, rr = _host_i32(expert_offsets), _host_i32(row_src_rank), _host_i32(row_slot), _host_i64(return_rows)
+    p = ctypes.c_void_p()
+    rows = int(off[-1]) if off.size else 0
+    _check(lib.moe_plan_build(ctypes.byref(cfg), rows, _np_ptr(off), _np_ptr(src), _np_ptr(slot), _np_ptr(rr),
+                              int(producer_grid), int(bool(overlapped)), ctypes.byref(p)))
+    try:
+        info = moe_plan_info_t()
+        _check(lib.moe_plan_info(p, ctypes.byref(info)))
+        out = {"info": _struct_dict(info)}
+        for key, which, dt, width in (("tile_rows", MOE_PLAN_TILE_ROWS, np.int32, 4),
+                                      ("items", MOE_PLAN_ITEMS, np.uint32, 1),
+                                      ("row_x", MOE_PLAN_ROW_X, np.int32, 1),
+                                      ("row_rank", MOE_PLAN_ROW_RANK, np.int32, 1),
+                                      ("row_slot", MOE_PLAN_ROW_SLOT, np.int32, 1),
+                                      ("segments", MOE_PLAN_SEGMENTS, np.int32, 8),
+                                      ("bands", MOE_PLAN_BANDS, np.int32, 4)):
+            need = lib.moe_plan_copy(p, which, None, 0)
+            arr = np.empty(need // np.dtype(dt).itemsize, dt)
+            if need:
+                _check(lib.moe_plan_copy(p, which, _np_ptr(arr), need))
+            out[key] = arr.reshape(-1, width) if width > 1 else arr
+        return out
+    finally:
+        lib.moe_plan_free(p)
+
+
+# ----------------------------------------------------------------------------- convenience wrapper
+
+class MoeStage:
+    """Owns one library handle.  Tensors are torch device tensors holding bf16 (or int16 bit patterns)."""
+
+    def __init__(self, hidden, ffn, num_local_experts, num_ranks, self_rank, max_rows, band_rows=0,
+                 mid_segment_bands=1, flags=MOE_LOCAL_DIRECT, watchdog_ms=0):
+        self.cfg = make_config(hidden, ffn, num_local_experts, num_ranks, self_rank, max_rows, band_rows,
+                               mid_segment_bands, flags, watchdog_ms)
+        self.h = moe_stage_create(self.cfg)
+
+    def run(self, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows=None,
+            cu_split=8, stream=None):
+        return moe_stage_run(self.h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs,
+                             return_rows, cu_split, stream)
+
+    def run_serial(self, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows=None,
+                   stream=None):
+        return moe_stage_run_serial(self.h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs,
+                                    return_rows, stream)
+
+    def query(self, check=True) -> dict:
+        return moe_stage_query(self.h, check)
+
+    def times(self, reset=False) -> dict:
+        return moe_stage_times(self.h, reset)
+
+    def close(self):
+        if self.h:
+            moe_stage_destroy(self.h)
+            self.h = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

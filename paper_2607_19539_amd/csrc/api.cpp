@@ -1,0 +1,628 @@
+// api.cpp -- the C ABI of include/moe_stage.h: handle, validation, plan upload,
+// CU-masked stream pair and the fork/join of producer and consumer.
+//
+// Co-scheduling (paper Section 3.3.3): the consumer and the producer are two
+// persistent kernels on two streams whose compute-unit masks are disjoint, so
+// each keeps a stable CU budget; they coordinate only through device memory.
+// The consumer is enqueued first so its workgroups are resident before the
+// producer fills the remaining compute units.  Stream priorities are left at
+// the default: with disjoint CU masks there is nothing left for a priority to
+// arbitrate.
+#include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+#include <chrono>
+#include <string>
+#include <vector>
+
+#include "../../include/moe_stage.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+using namespace moe;
+
+namespace {
+
+thread_local std::string g_create_error;
+
+constexpr int kTimingRing = 512;
+
+struct TimingRec {
+  hipEvent_t ev[6];  // 0 stage start, 1 producer start, 2 producer end, 3 consumer start,
+                     // 4 consumer end / scatter start, 5 stage end / scatter end
+  int kind = -1;     // 0 overlapped, 1 serial
+};
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+}  // namespace
+
+struct moe_stage_s {
+  moe_stage_config_t cfg{};
+  int device = 0;
+  int num_cus = 0;
+  int n_xcd = 1;
+  int producer_bpc = 1;
+  int64_t max_lrows = 0;
+  int32_t max_tile_rows = 0;
+  int32_t down_per_row = 0;
+
+  uint16_t* hws = nullptr;
+  uint16_t* y = nullptr;
+  uint32_t* flags = nullptr;
+  uint32_t* gu_done = nullptr;
+  RunCounters* ctr = nullptr;
+  uint8_t* d_plan = nullptr;
+  size_t plan_cap = 0;
+  uint8_t* h_stage[2] = {nullptr, nullptr};
+  hipEvent_t stage_free[2] = {nullptr, nullptr};
+  int stage_idx = 0;
+  uint32_t epoch = 0;
+
+  int cached_split = -1;
+  hipStream_t s_cons = nullptr, s_prod = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join_c = nullptr, ev_join_p = nullptr, ev_done = nullptr;
+  bool ran = false;
+
+  std::vector<TimingRec> ring;
+  int ring_next = 0, ring_count = 0;
+
+  Plan plan;
+  std::string err;
+  moe_stage_stats_t last{};
+};
+
+namespace {
+
+int set_err(moe_stage_s* h, int code, const std::string& msg) {
+  if (h)
+    h->err = msg;
+  else
+    g_create_error = msg;
+  return code;
+}
+
+#define HIP_TRY(h, call)                                                                   \
+  do {                                                                                     \
+    hipError_t e__ = (call);                                                               \
+    if (e__ != hipSuccess)                                                                 \
+      return set_err((h), MOE_EHIP, std::string(#call) + ": " + hipGetErrorString(e__));   \
+  } while (0)
+
+PlanParams params_of(const moe_stage_config_t& c, bool overlapped, int producer_grid) {
+  PlanParams p;
+  p.H = c.hidden;
+  p.F = c.ffn;
+  p.E_l = c.num_local_experts;
+  p.R = c.num_ranks;
+  p.self = c.self_rank;
+  p.band_rows = c.band_rows;
+  p.mid_bands = std::max(c.mid_segment_bands, 1);
+  p.local_direct = (c.flags & MOE_LOCAL_DIRECT) != 0;
+  p.overlapped = overlapped;
+  p.producer_grid = producer_grid;
+  return p;
+}
+
+int check_config(const moe_stage_config_t* c) {
+  if (!c) return MOE_EINVAL;
+  if (c->hidden <= 0 || c->ffn <= 0 || c->num_local_experts <= 0 || c->num_ranks <= 0 ||
+      c->self_rank < 0 || c->self_rank >= c->num_ranks || c->max_rows < 0 ||
+      c->mid_segment_bands < 0 || c->watchdog_ms < 0)
+    return MOE_EINVAL;
+  if (c->band_rows < 0 || c->band_rows > 256 || (c->band_rows & (c->band_rows - 1)) != 0)
+    return MOE_EINVAL;
+  if (c->hidden % 64 != 0 || c->ffn % 64 != 0) return MOE_EUNSUPPORTED;
+  return MOE_OK;
+}
+
+// Byte layout of the device plan blob.
+struct BlobLayout {
+  size_t tile_rows, items, row_x, row_rank, row_slot, segs, ret, total;
+};
+
+BlobLayout blob_layout(int64_t n_tr, int64_t n_items, int64_t n_lrows, int64_t n_segs, int32_t R) {
+  BlobLayout b{};
+  size_t o = 0;
+  b.tile_rows = o; o = align256(o + sizeof(TileRow) * (size_t)n_tr);
+  b.items = o;     o = align256(o + sizeof(uint32_t) * (size_t)n_items);
+  b.row_x = o;     o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
+  b.row_rank = o;  o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
+  b.row_slot = o;  o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
+  b.segs = o;      o = align256(o + sizeof(Segment) * (size_t)n_segs);
+  b.ret = o;       o = align256(o + sizeof(void*) * (size_t)R);
+  b.total = o;
+  return b;
+}
+
+uint64_t watchdog_ticks(const moe_stage_s* h) {
+  const int ms = h->cfg.watchdog_ms > 0 ? h->cfg.watchdog_ms : 2000;
+  return (uint64_t)ms * 100000ull;  // wall clock runs at 100 MHz
+}
+
+// Validates and builds the plan, uploads it and resets the run counters, all on `stream`.
+int prepare(moe_stage_s* h, bool overlapped, int producer_grid, const void* x,
+            const int32_t* off, const int32_t* src, const int32_t* slot, const void* w1,
+            const void* w3, const void* w2, void* const* ret, const int64_t* return_rows,
+            hipStream_t stream, BlobLayout* lay) {
+  const auto t0 = std::chrono::steady_clock::now();
+  const moe_stage_config_t& c = h->cfg;
+  if (!off || !return_rows || !ret) return set_err(h, MOE_EINVAL, "null routing or buffer array");
+  const int64_t rows = off[c.num_local_experts];
+  if (rows < 0) return set_err(h, MOE_EROUTING, "expert_offsets[E_l] < 0");
+  if (rows > c.max_rows)
+    return set_err(h, MOE_ECAPACITY, "rows " + std::to_string(rows) + " > max_rows " +
+                                         std::to_string(c.max_rows));
+  if (rows > 0 && (!x || !w1 || !w3 || !w2)) return set_err(h, MOE_EINVAL, "null tensor pointer");
+  for (int r = 0; r < c.num_ranks; ++r)
+    if (!ret[r] && return_rows[r] > 0) return set_err(h, MOE_EINVAL, "null return buffer");
+
+  std::string msg;
+  int rc = build_plan(params_of(c, overlapped, producer_grid), rows, off, src, slot, return_rows,
+                      &h->plan, &msg);
+  if (rc) return set_err(h, rc, msg);
+  const Plan& P = h->plan;
+  if (P.n_lrows() > h->max_lrows || (int64_t)P.tile_rows.size() > h->max_tile_rows)
+    return set_err(h, MOE_ECAPACITY, "plan exceeds the handle's workspaces");
+  *lay = blob_layout((int64_t)P.tile_rows.size(), (int64_t)P.items.size(), P.n_lrows(),
+                     (int64_t)P.segs.size(), c.num_ranks);
+  if (lay->total > h->plan_cap) return set_err(h, MOE_ECAPACITY, "plan exceeds the plan buffer");
+
+  // Stage into pinned memory (wait until the copy that last used this half finished).
+  const int si = h->stage_idx;
+  h->stage_idx ^= 1;
+  HIP_TRY(h, hipEventSynchronize(h->stage_free[si]));
+  uint8_t* hs = h->h_stage[si];
+  memcpy(hs + lay->tile_rows, P.tile_rows.data(), sizeof(TileRow) * P.tile_rows.size());
+  memcpy(hs + lay->items, P.items.data(), sizeof(uint32_t) * P.items.size());
+  memcpy(hs + lay->row_x, P.row_x.data(), sizeof(int32_t) * P.row_x.size());
+  memcpy(hs + lay->row_rank, P.row_rank.data(), sizeof(int32_t) * P.row_rank.size());
+  memcpy(hs + lay->row_slot, P.row_slot.data(), sizeof(int32_t) * P.row_slot.size());
+  memcpy(hs + lay->segs, P.segs.data(), sizeof(Segment) * P.segs.size());
+  memcpy(hs + lay->ret, ret, sizeof(void*) * (size_t)c.num_ranks);
+  h->last.plan_us =
+      std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+
+  HIP_TRY(h, hipMemcpyAsync(h->d_plan, hs, lay->total, hipMemcpyHostToDevice, stream));
+  HIP_TRY(h, hipEventRecord(h->stage_free[si], stream));
+
+  InitArgs ia{};
+  ia.ctr = h->ctr;
+  ia.gu_done = h->gu_done;
+  ia.n_tile_rows = (int32_t)P.tile_rows.size();
+  if (c.flags & MOE_POISON) {
+    ia.poison = h->y;
+    ia.poison_elems = P.n_lrows() * c.hidden;
+  }
+  HIP_TRY(h, launch_init(ia, stream));
+
+  h->epoch = h->epoch + 1 == 0 ? 1 : h->epoch + 1;  // flags hold the epoch of the run that set them
+  moe_stage_stats_t& st = h->last;
+  st.n_valid = P.n_valid;
+  st.n_logical_rows = P.n_lrows();
+  st.n_band_padding = P.n_band_pad;
+  st.n_remote_rows = P.n_remote;
+  st.n_tile_rows = (int32_t)P.tile_rows.size();
+  st.n_bands = (int32_t)P.bands.size();
+  st.n_gu_items = P.n_gu;
+  st.n_down_items = P.n_down;
+  st.n_segments = (int32_t)P.segs.size();
+  return MOE_OK;
+}
+
+ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x, const void* w1,
+                           const void* w3, const void* w2, uint32_t mode) {
+  const Plan& P = h->plan;
+  ProducerArgs a{};
+  a.x = (const uint16_t*)x;
+  a.w1 = (const uint16_t*)w1;
+  a.w3 = (const uint16_t*)w3;
+  a.w2 = (const uint16_t*)w2;
+  a.hws = h->hws;
+  a.y = h->y;
+  a.tile_rows = (const TileRow*)(h->d_plan + lay.tile_rows);
+  a.items = (const uint32_t*)(h->d_plan + lay.items);
+  a.n_items = (int32_t)P.items.size();
+  a.row_x = (const int32_t*)(h->d_plan + lay.row_x);
+  a.row_rank = (const int32_t*)(h->d_plan + lay.row_rank);
+  a.row_slot = (const int32_t*)(h->d_plan + lay.row_slot);
+  a.ret = (uint16_t* const*)(h->d_plan + lay.ret);
+  a.ctr = h->ctr;
+  a.gu_done = h->gu_done;
+  a.flags = h->flags;
+  a.epoch = h->epoch;
+  a.H = h->cfg.hidden;
+  a.F = h->cfg.ffn;
+  a.self_rank = h->cfg.self_rank;
+  a.gu_per_row = P.gu_per_row;
+  a.down_per_row = P.down_per_row;
+  a.mode = mode;
+  a.watchdog_ticks = watchdog_ticks(h);
+  return a;
+}
+
+TimingRec* timing_slot(moe_stage_s* h) {
+  if (!(h->cfg.flags & MOE_KERNEL_TIMING)) return nullptr;
+  TimingRec* r = &h->ring[h->ring_next];
+  h->ring_next = (h->ring_next + 1) % kTimingRing;
+  h->ring_count = std::min(h->ring_count + 1, kTimingRing);
+  return r;
+}
+
+// CU masks for the consumer/producer partition.  Workgroups of a launch are dealt
+// round-robin to the XCDs, so a queue must own CUs on every XCD, and an even split keeps
+// the per-XCD share symmetric: the consumer gets m = c / n_xcd CUs on each XCD.  The mask
+// bit b = i * (cus_per_xcd + 1) + j (XCD i, j < m) lands on XCD i whether the driver maps
+// bit b to XCD (b mod n_xcd) or to XCD (b / cus_per_xcd).  The producer gets the complement.
+void make_masks(int num_cus, int n_xcd, int c, std::vector<uint32_t>* mc, std::vector<uint32_t>* mp) {
+  const int words = (num_cus + 31) / 32;
+  mc->assign(words, 0);
+  mp->assign(words, 0);
+  std::vector<char> is_c(num_cus, 0);
+  const int per = num_cus / n_xcd, m = c / n_xcd;
+  if (per % n_xcd == 0 && m <= per - n_xcd + 1) {
+    for (int i = 0; i < n_xcd; ++i)
+      for (int j = 0; j < m; ++j) is_c[i * (per + 1) + j] = 1;
+  } else {
+    for (int b = 0; b < c; ++b) is_c[b] = 1;  // interleaved numbering: bits 0..c-1 cover every XCD
+  }
+  for (int cu = 0; cu < num_cus; ++cu) ((is_c[cu] ? *mc : *mp))[cu / 32] |= 1u << (cu % 32);
+}
+
+// Consumer CUs actually reserved for a requested split: a multiple of the XCD count.
+int effective_split(const moe_stage_s* h, int c) {
+  const int n = h->n_xcd;
+  return std::min((c + n - 1) / n * n, h->num_cus - n);
+}
+
+int ensure_streams(moe_stage_s* h, int c) {
+  if (h->cached_split == c) return MOE_OK;
+  if (h->s_cons) {
+    HIP_TRY(h, hipStreamSynchronize(h->s_cons));
+    HIP_TRY(h, hipStreamSynchronize(h->s_prod));
+    HIP_TRY(h, hipStreamDestroy(h->s_cons));
+    HIP_TRY(h, hipStreamDestroy(h->s_prod));
+    h->s_cons = h->s_prod = nullptr;
+    h->cached_split = -1;
+  }
+  std::vector<uint32_t> mc, mp;
+  make_masks(h->num_cus, h->n_xcd, c, &mc, &mp);
+  HIP_TRY(h, hipExtStreamCreateWithCUMask(&h->s_cons, (uint32_t)mc.size(), mc.data()));
+  HIP_TRY(h, hipExtStreamCreateWithCUMask(&h->s_prod, (uint32_t)mp.size(), mp.data()));
+  h->cached_split = c;
+  return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
+  if (!out) return set_err(nullptr, MOE_EINVAL, "out is null");
+  *out = nullptr;
+  int rc = check_config(cfg);
+  if (rc) return set_err(nullptr, rc, "invalid configuration");
+  auto* h = new moe_stage_s();
+  h->cfg = *cfg;
+  if (h->cfg.mid_segment_bands == 0) h->cfg.mid_segment_bands = 1;
+  if (h->cfg.band_rows == 0)
+    h->cfg.band_rows = default_band_rows(cfg->max_rows, cfg->num_local_experts, cfg->num_ranks);
+  auto bail = [&](int code) {
+    moe_stage_destroy(h);
+    return code;
+  };
+  hipError_t e = hipGetDevice(&h->device);
+  hipDeviceProp_t prop{};
+  if (e == hipSuccess) e = hipGetDeviceProperties(&prop, h->device);
+  if (e != hipSuccess) {
+    set_err(nullptr, MOE_EHIP, std::string("no HIP device: ") + hipGetErrorString(e));
+    delete h;
+    return MOE_EHIP;
+  }
+  h->num_cus = prop.multiProcessorCount;
+  if (hipDeviceGetAttribute(&h->n_xcd, hipDeviceAttributeNumberOfXccs, h->device) != hipSuccess ||
+      h->n_xcd < 1 || h->num_cus % h->n_xcd != 0)
+    h->n_xcd = 1;
+  h->producer_bpc = producer_blocks_per_cu();
+  h->max_lrows = max_logical_rows(cfg->max_rows, cfg->num_local_experts, cfg->num_ranks,
+                                  h->cfg.band_rows);
+  h->max_tile_rows = (int32_t)((h->max_lrows + kTileM - 1) / kTileM) + cfg->num_local_experts;
+  h->max_lrows = (int64_t)h->max_tile_rows * kTileM;
+  h->down_per_row = (cfg->hidden + kDownTileN - 1) / kDownTileN;
+  const int gu_per_row = (cfg->ffn + kGuTileF - 1) / kGuTileF;
+  const int64_t max_items = (int64_t)h->max_tile_rows * (gu_per_row + h->down_per_row);
+  const BlobLayout lay =
+      blob_layout(h->max_tile_rows, max_items, h->max_lrows, h->max_lrows, cfg->num_ranks);
+  h->plan_cap = lay.total;
+
+  auto try_hip = [&](hipError_t err, const char* what) {
+    if (err != hipSuccess) {
+      set_err(nullptr, MOE_EHIP, std::string(what) + ": " + hipGetErrorString(err));
+      return false;
+    }
+    return true;
+  };
+  const size_t hws_bytes = (size_t)h->max_lrows * cfg->ffn * 2;
+  const size_t y_bytes = (size_t)h->max_lrows * cfg->hidden * 2;
+  const size_t flag_bytes = (size_t)h->max_tile_rows * h->down_per_row * 4;
+  if (!try_hip(hipMalloc(&h->hws, hws_bytes), "hipMalloc(hws)") ||
+      !try_hip(hipMalloc(&h->y, y_bytes), "hipMalloc(y)") ||
+      !try_hip(hipMalloc(&h->flags, flag_bytes), "hipMalloc(flags)") ||
+      !try_hip(hipMalloc(&h->gu_done, (size_t)h->max_tile_rows * 4), "hipMalloc(gu_done)") ||
+      !try_hip(hipMalloc(&h->ctr, sizeof(RunCounters)), "hipMalloc(counters)") ||
+      !try_hip(hipMalloc(&h->d_plan, h->plan_cap), "hipMalloc(plan)") ||
+      !try_hip(hipHostMalloc(&h->h_stage[0], h->plan_cap, hipHostMallocDefault), "hipHostMalloc") ||
+      !try_hip(hipHostMalloc(&h->h_stage[1], h->plan_cap, hipHostMallocDefault), "hipHostMalloc") ||
+      !try_hip(hipMemset(h->hws, 0, hws_bytes), "hipMemset(hws)") ||
+      !try_hip(hipMemset(h->y, 0, y_bytes), "hipMemset(y)") ||
+      !try_hip(hipMemset(h->flags, 0, flag_bytes), "hipMemset(flags)") ||
+      !try_hip(hipMemset(h->ctr, 0, sizeof(RunCounters)), "hipMemset(counters)"))
+    return bail(MOE_EHIP);
+  for (int i = 0; i < 2; ++i)
+    if (!try_hip(hipEventCreateWithFlags(&h->stage_free[i], hipEventDisableTiming), "hipEventCreate") ||
+        !try_hip(hipEventRecord(h->stage_free[i], nullptr), "hipEventRecord"))
+      return bail(MOE_EHIP);
+  if (!try_hip(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming), "hipEventCreate") ||
+      !try_hip(hipEventCreateWithFlags(&h->ev_join_c, hipEventDisableTiming), "hipEventCreate") ||
+      !try_hip(hipEventCreateWithFlags(&h->ev_join_p, hipEventDisableTiming), "hipEventCreate") ||
+      !try_hip(hipEventCreateWithFlags(&h->ev_done, hipEventDisableTiming), "hipEventCreate"))
+    return bail(MOE_EHIP);
+  if (h->cfg.flags & MOE_KERNEL_TIMING) {
+    h->ring.resize(kTimingRing);
+    for (auto& r : h->ring)
+      for (auto& ev : r.ev)
+        if (!try_hip(hipEventCreate(&ev), "hipEventCreate")) return bail(MOE_EHIP);
+  }
+  if (!try_hip(hipDeviceSynchronize(), "hipDeviceSynchronize")) return bail(MOE_EHIP);
+  *out = h;
+  return MOE_OK;
+}
+
+int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_t* src,
+                  const int32_t* slot, const void* w1, const void* w3, const void* w2,
+                  void* const* ret, const int64_t* return_rows, int32_t cu_split, void* stream_) {
+  if (!h) return MOE_EINVAL;
+  hipStream_t stream = (hipStream_t)stream_;
+  if (cu_split < 1 || cu_split > h->num_cus - h->n_xcd)
+    return set_err(h, MOE_EUNSUPPORTED, "cu_split must be in [1, compute units - XCDs]");
+  const int c_eff = effective_split(h, cu_split);
+  const int pgrid = (h->num_cus - c_eff) * h->producer_bpc;
+  const int cgrid = c_eff * 2;
+  int rc = ensure_streams(h, c_eff);
+  if (rc) return rc;
+  BlobLayout lay{};
+  TimingRec* tr = timing_slot(h);
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[0], stream));
+  rc = prepare(h, true, pgrid, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
+  if (rc) {
+    if (tr) h->ring_next = (h->ring_next + kTimingRing - 1) % kTimingRing, --h->ring_count;
+    return rc;
+  }
+  h->last.producer_grid = pgrid;
+  h->last.consumer_grid = cgrid;
+  h->last.consumer_cus = c_eff;
+  uint32_t mode = kModeSignal;
+  if (h->cfg.flags & MOE_LOCAL_DIRECT) mode |= kModeLocalDirect;
+  const ProducerArgs pa = producer_args(h, lay, x, w1, w3, w2, mode);
+  ConsumerArgs ca{};
+  ca.y = h->y;
+  ca.ret = pa.ret;
+  ca.segs = (const Segment*)(h->d_plan + lay.segs);
+  ca.n_segs = (int32_t)h->plan.segs.size();
+  ca.flags = h->flags;
+  ca.epoch = h->epoch;
+  ca.H = h->cfg.hidden;
+  ca.ctr = h->ctr;
+  ca.watchdog_ticks = watchdog_ticks(h);
+
+  HIP_TRY(h, hipEventRecord(h->ev_fork, stream));
+  HIP_TRY(h, hipStreamWaitEvent(h->s_cons, h->ev_fork, 0));
+  HIP_TRY(h, hipStreamWaitEvent(h->s_prod, h->ev_fork, 0));
+  if (ca.n_segs > 0) {
+    if (tr) HIP_TRY(h, hipEventRecord(tr->ev[3], h->s_cons));
+    HIP_TRY(h, launch_consumer(ca, cgrid, h->s_cons));
+    if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
+  } else if (tr) {
+    HIP_TRY(h, hipEventRecord(tr->ev[3], h->s_cons));
+    HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
+  }
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], h->s_prod));
+  if (pa.n_items > 0) HIP_TRY(h, launch_producer(pa, pgrid, h->s_prod));
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], h->s_prod));
+  HIP_TRY(h, hipEventRecord(h->ev_join_c, h->s_cons));
+  HIP_TRY(h, hipEventRecord(h->ev_join_p, h->s_prod));
+  HIP_TRY(h, hipStreamWaitEvent(stream, h->ev_join_c, 0));
+  HIP_TRY(h, hipStreamWaitEvent(stream, h->ev_join_p, 0));
+  if (tr) {
+    HIP_TRY(h, hipEventRecord(tr->ev[5], stream));
+    tr->kind = 0;
+  }
+  HIP_TRY(h, hipEventRecord(h->ev_done, stream));
+  h->ran = true;
+  return MOE_OK;
+}
+
+int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const int32_t* src,
+                         const int32_t* slot, const void* w1, const void* w3, const void* w2,
+                         void* const* ret, const int64_t* return_rows, void* stream_) {
+  if (!h) return MOE_EINVAL;
+  hipStream_t stream = (hipStream_t)stream_;
+  const int pgrid = h->num_cus * h->producer_bpc;
+  BlobLayout lay{};
+  TimingRec* tr = timing_slot(h);
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[0], stream));
+  int rc = prepare(h, false, pgrid, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
+  if (rc) {
+    if (tr) h->ring_next = (h->ring_next + kTimingRing - 1) % kTimingRing, --h->ring_count;
+    return rc;
+  }
+  h->last.producer_grid = pgrid;
+  h->last.consumer_grid = 0;
+  h->last.consumer_cus = 0;
+  const ProducerArgs pa = producer_args(h, lay, x, w1, w3, w2, 0u);
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], stream));
+  if (pa.n_items > 0) HIP_TRY(h, launch_producer(pa, pgrid, stream));
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], stream));
+  ScatterArgs sa{};
+  sa.y = h->y;
+  sa.ret = pa.ret;
+  sa.row_rank = pa.row_rank;
+  sa.row_slot = pa.row_slot;
+  sa.n_lrows = h->plan.n_lrows();
+  sa.H = h->cfg.hidden;
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], stream));
+  if (sa.n_lrows > 0)
+    HIP_TRY(h, launch_scatter(sa, (int)std::min<int64_t>(sa.n_lrows, (int64_t)h->num_cus * 8), stream));
+  if (tr) {
+    HIP_TRY(h, hipEventRecord(tr->ev[5], stream));
+    tr->kind = 1;
+  }
+  HIP_TRY(h, hipEventRecord(h->ev_done, stream));
+  h->ran = true;
+  return MOE_OK;
+}
+
+int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
+  if (!h || !out) return MOE_EINVAL;
+  if (h->ran) {
+    HIP_TRY(h, hipEventSynchronize(h->ev_done));
+    RunCounters c{};
+    HIP_TRY(h, hipMemcpy(&c, h->ctr, sizeof c, hipMemcpyDeviceToHost));
+    h->last.poll_iters = c.poll_iters;
+    h->last.wait_ticks = c.wait_ticks;
+    h->last.producer_wait_ticks = c.producer_wait_ticks;
+    h->last.timeout = (int32_t)c.timeout;
+  }
+  *out = h->last;
+  if (h->last.timeout) {
+    h->last.timeout = 0;
+    return set_err(h, MOE_ETIMEOUT,
+                   "a device wait hit the watchdog (1 = consumer flag wait, 2 = producer dependency)");
+  }
+  return MOE_OK;
+}
+
+int moe_stage_times(moe_stage_t h, int32_t reset, moe_stage_times_t* out) {
+  if (!h || !out) return MOE_EINVAL;
+  *out = moe_stage_times_t{};
+  if (!(h->cfg.flags & MOE_KERNEL_TIMING)) return set_err(h, MOE_EINVAL, "MOE_KERNEL_TIMING not set");
+  if (h->ran) HIP_TRY(h, hipEventSynchronize(h->ev_done));
+  for (int k = 0; k < h->ring_count; ++k) {
+    TimingRec& r = h->ring[(h->ring_next - 1 - k + 2 * kTimingRing) % kTimingRing];
+    float ms = 0;
+    HIP_TRY(h, hipEventElapsedTime(&ms, r.ev[0], r.ev[5]));
+    out->stage_ms += ms;
+    HIP_TRY(h, hipEventElapsedTime(&ms, r.ev[1], r.ev[2]));
+    out->producer_ms += ms;
+    if (r.kind == 0) {
+      HIP_TRY(h, hipEventElapsedTime(&ms, r.ev[3], r.ev[4]));
+      out->consumer_ms += ms;
+    } else {
+      HIP_TRY(h, hipEventElapsedTime(&ms, r.ev[4], r.ev[5]));
+      out->scatter_ms += ms;
+    }
+    ++out->runs;
+  }
+  if (reset) h->ring_count = 0;
+  return MOE_OK;
+}
+
+const char* moe_stage_last_error(moe_stage_t h) { return h ? h->err.c_str() : g_create_error.c_str(); }
+
+int moe_stage_destroy(moe_stage_t h) {
+  if (!h) return MOE_EINVAL;
+  (void)hipDeviceSynchronize();
+  for (auto& r : h->ring)
+    for (auto& ev : r.ev)
+      if (ev) (void)hipEventDestroy(ev);
+  for (hipEvent_t ev : {h->stage_free[0], h->stage_free[1], h->ev_fork, h->ev_join_c, h->ev_join_p, h->ev_done})
+    if (ev) (void)hipEventDestroy(ev);
+  if (h->s_cons) (void)hipStreamDestroy(h->s_cons);
+  if (h->s_prod) (void)hipStreamDestroy(h->s_prod);
+  for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->gu_done, (void*)h->ctr,
+                  (void*)h->d_plan})
+    if (p) (void)hipFree(p);
+  for (uint8_t* p : h->h_stage)
+    if (p) (void)hipHostFree(p);
+  delete h;
+  return MOE_OK;
+}
+
+// ----------------------------------------------------------------- plan inspection
+struct moe_plan_s {
+  Plan plan;
+  int32_t band_rows = 0;
+};
+
+int moe_plan_build(const moe_stage_config_t* cfg, int64_t rows, const int32_t* off,
+                   const int32_t* src, const int32_t* slot, const int64_t* return_rows,
+                   int32_t producer_grid, int32_t overlapped, moe_plan_t* out) {
+  if (!out) return MOE_EINVAL;
+  *out = nullptr;
+  int rc = check_config(cfg);
+  if (rc) return set_err(nullptr, rc, "invalid configuration");
+  if (rows > cfg->max_rows) return set_err(nullptr, MOE_ECAPACITY, "rows > max_rows");
+  moe_stage_config_t c = *cfg;
+  if (c.band_rows == 0) c.band_rows = default_band_rows(c.max_rows, c.num_local_experts, c.num_ranks);
+  if (off && off[c.num_local_experts] != rows)
+    return set_err(nullptr, MOE_EROUTING, "expert_offsets[E_l] must equal rows");
+  auto* p = new moe_plan_s();
+  std::string msg;
+  rc = build_plan(params_of(c, overlapped != 0, std::max(producer_grid, 1)), rows, off, src, slot,
+                  return_rows, &p->plan, &msg);
+  if (rc) {
+    delete p;
+    return set_err(nullptr, rc, msg);
+  }
+  p->band_rows = overlapped ? c.band_rows : 1;
+  *out = p;
+  return MOE_OK;
+}
+
+int moe_plan_info(moe_plan_t p, moe_plan_info_t* o) {
+  if (!p || !o) return MOE_EINVAL;
+  const Plan& P = p->plan;
+  o->n_tile_rows = (int32_t)P.tile_rows.size();
+  o->n_items = (int32_t)P.items.size();
+  o->n_gu_items = P.n_gu;
+  o->n_down_items = P.n_down;
+  o->n_segments = (int32_t)P.segs.size();
+  o->n_bands = (int32_t)P.bands.size();
+  o->gu_tiles_per_row = P.gu_per_row;
+  o->down_tiles_per_row = P.down_per_row;
+  o->tile_m = kTileM;
+  o->band_rows = p->band_rows;
+  o->n_logical_rows = P.n_lrows();
+  o->n_valid = P.n_valid;
+  o->n_band_padding = P.n_band_pad;
+  o->n_remote_rows = P.n_remote;
+  return MOE_OK;
+}
+
+int64_t moe_plan_copy(moe_plan_t p, int32_t which, void* dst, int64_t bytes) {
+  if (!p) return MOE_EINVAL;
+  const Plan& P = p->plan;
+  const void* src = nullptr;
+  int64_t need = 0;
+  switch (which) {
+    case MOE_PLAN_TILE_ROWS: src = P.tile_rows.data(); need = sizeof(TileRow) * P.tile_rows.size(); break;
+    case MOE_PLAN_ITEMS: src = P.items.data(); need = sizeof(uint32_t) * P.items.size(); break;
+    case MOE_PLAN_ROW_X: src = P.row_x.data(); need = sizeof(int32_t) * P.row_x.size(); break;
+    case MOE_PLAN_ROW_RANK: src = P.row_rank.data(); need = sizeof(int32_t) * P.row_rank.size(); break;
+    case MOE_PLAN_ROW_SLOT: src = P.row_slot.data(); need = sizeof(int32_t) * P.row_slot.size(); break;
+    case MOE_PLAN_SEGMENTS: src = P.segs.data(); need = sizeof(Segment) * P.segs.size(); break;
+    case MOE_PLAN_BANDS: src = P.bands.data(); need = sizeof(Band) * P.bands.size(); break;
+    default: return MOE_EINVAL;
+  }
+  if (!dst) return need;
+  if (bytes < need) return MOE_EINVAL;
+  if (need) memcpy(dst, src, (size_t)need);
+  return MOE_OK;
+}
+
+void moe_plan_free(moe_plan_t p) { delete p; }
+
+}  // extern "C"

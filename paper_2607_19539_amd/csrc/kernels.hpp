@@ -1,0 +1,75 @@
+// kernels.hpp -- launch interface of the gfx950 kernels (host side).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "plan_types.hpp"
+
+namespace moe {
+
+// Producer mode bits.
+constexpr uint32_t kModeSignal = 1u;       // raise a ready flag per down tile of a transfer tile row
+constexpr uint32_t kModeLocalDirect = 2u;  // local rows go straight to the local receive buffer
+
+struct ProducerArgs {
+  const uint16_t* x;       // [rows, H] dispatched tokens
+  const uint16_t* w1;      // [E_l, F, H]
+  const uint16_t* w3;      // [E_l, F, H]
+  const uint16_t* w2;      // [E_l, H, F]
+  uint16_t* hws;           // [n_lrows, F] gated activation (workspace)
+  uint16_t* y;             // [n_lrows, H] staged output (workspace)
+  const TileRow* tile_rows;
+  const uint32_t* items;
+  int32_t n_items;
+  const int32_t* row_x;    // [n_lrows]
+  const int32_t* row_rank; // [n_lrows], -1 = padding
+  const int32_t* row_slot; // [n_lrows]
+  uint16_t* const* ret;    // [R] receive buffers (device array of device pointers)
+  RunCounters* ctr;
+  uint32_t* gu_done;       // [n_tile_rows] finished gate/up tiles per tile row
+  uint32_t* flags;         // [n_tile_rows * down_per_row] ready flags (value = epoch)
+  uint32_t epoch;
+  int32_t H, F, self_rank, gu_per_row, down_per_row;
+  uint32_t mode;
+  uint64_t watchdog_ticks; // bound on a dependency wait, 100 MHz ticks
+};
+
+struct ConsumerArgs {
+  const uint16_t* y;
+  uint16_t* const* ret;
+  const Segment* segs;
+  int32_t n_segs;
+  const uint32_t* flags;
+  uint32_t epoch;
+  int32_t H;
+  RunCounters* ctr;
+  uint64_t watchdog_ticks;
+};
+
+struct ScatterArgs {
+  const uint16_t* y;
+  uint16_t* const* ret;
+  const int32_t* row_rank;
+  const int32_t* row_slot;
+  int64_t n_lrows;
+  int32_t H;
+};
+
+struct InitArgs {
+  RunCounters* ctr;
+  uint32_t* gu_done;
+  int32_t n_tile_rows;
+  uint16_t* poison;        // optional: filled with bf16 NaN
+  int64_t poison_elems;    // multiple of 8
+};
+
+hipError_t launch_init(const InitArgs& a, hipStream_t s);
+hipError_t launch_producer(const ProducerArgs& a, int grid, hipStream_t s);
+hipError_t launch_consumer(const ConsumerArgs& a, int grid, hipStream_t s);
+hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s);
+// Resident producer workgroups per compute unit.
+int producer_blocks_per_cu();
+constexpr int kProducerThreads = 256;
+constexpr int kConsumerThreads = 256;
+
+}  // namespace moe

@@ -1,0 +1,320 @@
+// plan.cpp -- host construction of the remote-owner-aligned layout, the
+// remote-first tile schedule and the combine plan (paper Section 3.2,
+// Algorithm 1, and the segment composition of Section 3.3.2).
+#include "plan.hpp"
+
+#include <algorithm>
+#include <deque>
+#include <numeric>
+#include <string>
+
+namespace moe {
+
+namespace {
+
+int fail(std::string* err, int code, const std::string& msg) {
+  if (err) *err = msg;
+  return code;
+}
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+uint32_t gu_item(int32_t t, int32_t j) { return ((uint32_t)t << kItemRowShift) | (uint32_t)j; }
+uint32_t down_item(int32_t t, int32_t n) {
+  return kItemDown | ((uint32_t)t << kItemRowShift) | (uint32_t)n;
+}
+
+}  // namespace
+
+int64_t max_logical_rows(int64_t max_rows, int32_t E_l, int32_t R, int32_t band_rows) {
+  const int64_t tb = std::max<int32_t>(band_rows, 1);
+  return max_rows + (int64_t)E_l * ((int64_t)(R - 1) * (tb - 1) + kTileM - 1);
+}
+
+int32_t default_band_rows(int32_t max_rows, int32_t E_l, int32_t R) {
+  // Largest band whose expected group padding (half a band per remote group) stays
+  // within 2 % of the rows; never below 16 rows.
+  for (int32_t tb = 256; tb >= 16; tb /= 2)
+    if ((double)E_l * (R - 1) * (tb - 1) * 0.5 <= 0.02 * (double)max_rows) return tb;
+  return 16;
+}
+
+int validate_routing(const PlanParams& p, int64_t rows, const int32_t* off, const int32_t* src,
+                     const int32_t* slot, const int64_t* return_rows, std::string* err) {
+  if (!off || !return_rows) return fail(err, -1, "expert_offsets and return_rows must not be null");
+  if (rows < 0) return fail(err, -1, "rows must be >= 0");
+  if (rows > 0 && (!src || !slot)) return fail(err, -1, "row_src_rank and row_slot must not be null");
+  for (int r = 0; r < p.R; ++r)
+    if (return_rows[r] < 0) return fail(err, -1, "return_rows[" + std::to_string(r) + "] < 0");
+  if (off[0] != 0) return fail(err, -2, "expert_offsets[0] must be 0");
+  for (int e = 0; e < p.E_l; ++e)
+    if (off[e] > off[e + 1])
+      return fail(err, -2, "expert_offsets not monotone at expert " + std::to_string(e));
+  if (off[p.E_l] != rows) return fail(err, -2, "expert_offsets[E_l] must equal rows");
+
+  std::vector<int64_t> per_rank(p.R, 0);
+  for (int64_t i = 0; i < rows; ++i) {
+    const int32_t r = src[i];
+    if (r < 0 || r >= p.R)
+      return fail(err, -2, "row " + std::to_string(i) + ": source rank out of range");
+    if (slot[i] < 0 || (int64_t)slot[i] >= return_rows[r])
+      return fail(err, -2, "row " + std::to_string(i) + ": slot outside its receive buffer");
+    ++per_rank[r];
+  }
+  // Duplicate (rank, slot): a bitmap per rank when the buffers are modest, else a sort.
+  bool small = true;
+  for (int r = 0; r < p.R; ++r) small &= return_rows[r] <= 64 * (rows + 64);
+  if (small) {
+    std::vector<std::vector<uint64_t>> seen(p.R);
+    for (int r = 0; r < p.R; ++r) seen[r].assign((size_t)(return_rows[r] + 63) / 64, 0);
+    for (int64_t i = 0; i < rows; ++i) {
+      uint64_t& w = seen[src[i]][(size_t)slot[i] >> 6];
+      const uint64_t bit = 1ull << (slot[i] & 63);
+      if (w & bit) return fail(err, -2, "row " + std::to_string(i) + ": duplicate (rank, slot)");
+      w |= bit;
+    }
+  } else {
+    std::vector<uint64_t> keys((size_t)rows);
+    for (int64_t i = 0; i < rows; ++i) keys[i] = ((uint64_t)src[i] << 32) | (uint32_t)slot[i];
+    std::sort(keys.begin(), keys.end());
+    for (size_t i = 1; i < keys.size(); ++i)
+      if (keys[i] == keys[i - 1]) return fail(err, -2, "duplicate (rank, slot)");
+  }
+  return 0;
+}
+
+int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int32_t* src,
+               const int32_t* slot, const int64_t* return_rows, Plan* out, std::string* err) {
+  int rc = validate_routing(p, rows, off, src, slot, return_rows, err);
+  if (rc) return rc;
+  Plan& P = *out;
+  P.p = p;
+  P.tile_rows.clear();
+  P.items.clear();
+  P.row_x.clear();
+  P.row_rank.clear();
+  P.row_slot.clear();
+  P.segs.clear();
+  P.bands.clear();
+  P.n_valid = rows;
+  P.n_band_pad = 0;
+  P.n_remote = 0;
+  P.gu_per_row = (p.F + kGuTileF - 1) / kGuTileF;
+  P.down_per_row = (p.H + kDownTileN - 1) / kDownTileN;
+
+  // The baseline uses the conventional expert-contiguous layout: no alignment padding.
+  const int32_t tb = p.overlapped ? std::max<int32_t>(p.band_rows, 1) : 1;
+
+  // Owner-group order inside an expert (Section 3.2.1, Algorithm 1): remote ranks in
+  // ascending order first, the local rank last.
+  std::vector<int32_t> rank_order;
+  for (int r = 0; r < p.R; ++r)
+    if (!p.overlapped || r != p.self) rank_order.push_back(r);
+  if (p.overlapped) rank_order.push_back(p.self);
+
+  std::vector<int32_t> tr_begin(p.E_l, 0), tr_end(p.E_l, 0), remote_bands(p.E_l, 0);
+  std::vector<int64_t> bucket_start(p.R + 1);
+  std::vector<int32_t> order_buf;
+  for (int e = 0; e < p.E_l; ++e) {
+    const int64_t lo = off[e], hi = off[e + 1];
+    const int64_t base = (int64_t)P.row_x.size();  // multiple of kTileM
+    tr_begin[e] = tr_end[e] = (int32_t)(base / kTileM);
+    if (hi == lo) continue;
+
+    // Bucket the expert's rows by source rank (stable), then order each bucket by slot so
+    // that consecutive rows of a group fill consecutive receive slots when possible.
+    std::fill(bucket_start.begin(), bucket_start.end(), 0);
+    for (int64_t i = lo; i < hi; ++i) ++bucket_start[src[i] + 1];
+    for (int r = 0; r < p.R; ++r) bucket_start[r + 1] += bucket_start[r];
+    order_buf.resize((size_t)(hi - lo));
+    {
+      std::vector<int64_t> fillp(bucket_start.begin(), bucket_start.end() - 1);
+      for (int64_t i = lo; i < hi; ++i) order_buf[(size_t)fillp[src[i]]++] = (int32_t)i;
+    }
+    for (int r = 0; r < p.R; ++r) {
+      auto b = order_buf.begin() + bucket_start[r], en = order_buf.begin() + bucket_start[r + 1];
+      if (!std::is_sorted(b, en, [&](int32_t a, int32_t c) { return slot[a] < slot[c]; }))
+        std::stable_sort(b, en, [&](int32_t a, int32_t c) { return slot[a] < slot[c]; });
+    }
+
+    int64_t pos = base;
+    for (int32_t r : rank_order) {
+      const int64_t n = bucket_start[r + 1] - bucket_start[r];
+      if (n == 0) continue;
+      for (int64_t q = bucket_start[r]; q < bucket_start[r + 1]; ++q) {
+        const int32_t i = order_buf[(size_t)q];
+        P.row_x.push_back(i);
+        P.row_rank.push_back(r);
+        P.row_slot.push_back(slot[i]);
+      }
+      if (r != p.self) P.n_remote += n;
+      if (p.overlapped) {
+        for (int64_t b0 = pos; b0 < pos + n; b0 += tb) {
+          P.bands.push_back(Band{e, (int32_t)b0, (int32_t)std::min<int64_t>(tb, pos + n - b0), r});
+          if (r != p.self) ++remote_bands[e];
+        }
+      }
+      pos += n;
+      if (p.overlapped && r != p.self) {
+        // Zero-row padding up to the next band boundary (Algorithm 1): the next group then
+        // starts band-aligned and every band has a single destination.  Padding rows repeat
+        // the expert's first row as input; their outputs are never stored or transferred.
+        const int64_t pad = round_up(pos - base, tb) - (pos - base);
+        for (int64_t q = 0; q < pad; ++q) {
+          P.row_x.push_back((int32_t)lo);
+          P.row_rank.push_back(-1);
+          P.row_slot.push_back(-1);
+        }
+        P.n_band_pad += pad;
+        pos += pad;
+      }
+    }
+    const int64_t end = base + round_up(pos - base, kTileM);
+    while ((int64_t)P.row_x.size() < end) {
+      P.row_x.push_back((int32_t)lo);
+      P.row_rank.push_back(-1);
+      P.row_slot.push_back(-1);
+    }
+    for (int64_t t0 = base; t0 < end; t0 += kTileM) {
+      TileRow tr{e, (int32_t)t0, 0, 0};
+      for (int64_t q = t0; q < t0 + kTileM; ++q) {
+        if (P.row_rank[q] >= 0) ++tr.nvalid;
+        if (P.row_rank[q] >= 0 && P.row_rank[q] != p.self) tr.has_remote = 1;
+      }
+      P.tile_rows.push_back(tr);
+    }
+    tr_end[e] = (int32_t)(end / kTileM);
+  }
+  const int32_t n_tr = (int32_t)P.tile_rows.size();
+  if (n_tr >= kMaxTileRows) return fail(err, -3, "too many tile rows");
+  if (P.gu_per_row >= kMaxColTiles || P.down_per_row >= kMaxColTiles)
+    return fail(err, -6, "hidden or ffn too large for the work-item encoding");
+
+  // Remote-first tile schedule (Section 3.2.2): rule (ii) experts by remote band count,
+  // descending (ties by expert id); rule (i) every tile row holding remote rows before
+  // any tile row that holds only local rows.
+  std::vector<int32_t> order;
+  order.reserve(n_tr);
+  if (p.overlapped) {
+    std::vector<int32_t> experts(p.E_l);
+    std::iota(experts.begin(), experts.end(), 0);
+    std::stable_sort(experts.begin(), experts.end(),
+                     [&](int32_t a, int32_t b) { return remote_bands[a] > remote_bands[b]; });
+    for (int32_t e : experts)
+      for (int32_t t = tr_begin[e]; t < tr_end[e]; ++t)
+        if (P.tile_rows[t].has_remote) order.push_back(t);
+    for (int32_t e = 0; e < p.E_l; ++e)
+      for (int32_t t = tr_begin[e]; t < tr_end[e]; ++t)
+        if (!P.tile_rows[t].has_remote) order.push_back(t);
+  } else {
+    for (int32_t t = 0; t < n_tr; ++t) order.push_back(t);
+  }
+
+  // Band groups: up to band_group consecutive tile rows of one expert (and of one class,
+  // remote or local) sweep the gate/up columns together, so each weight slice is fetched
+  // once per group rather than once per tile row.
+  std::vector<std::pair<int32_t, int32_t>> groups;  // [begin, end) into `order`
+  const int32_t G = std::max<int32_t>(p.band_group, 1);
+  for (int32_t a = 0; a < n_tr;) {
+    int32_t b = a + 1;
+    while (b < n_tr && b - a < G && P.tile_rows[order[b]].expert == P.tile_rows[order[a]].expert &&
+           P.tile_rows[order[b]].has_remote == P.tile_rows[order[a]].has_remote)
+      ++b;
+    groups.emplace_back(a, b);
+    a = b;
+  }
+
+  // Work items.  A down tile of tile row t depends on all gate/up tiles of t, so every
+  // gate/up tile of a group precedes its down tiles; the down tiles trail by about one
+  // producer grid of gate/up tiles so their dependencies have usually finished when a
+  // workgroup picks them up.
+  std::vector<int32_t> pos_of_down((size_t)n_tr * P.down_per_row, -1);
+  auto emit_down = [&](int32_t g) {
+    for (int32_t n = 0; n < P.down_per_row; ++n)
+      for (int32_t q = groups[g].first; q < groups[g].second; ++q) {
+        const int32_t t = order[q];
+        pos_of_down[(size_t)t * P.down_per_row + n] = (int32_t)P.items.size();
+        P.items.push_back(down_item(t, n));
+      }
+  };
+  const int64_t lag = std::max<int32_t>(p.producer_grid, 1);
+  std::deque<std::pair<int32_t, int64_t>> pending;  // (group, gate/up count at its end)
+  int64_t gu_count = 0;
+  for (int32_t g = 0; g < (int32_t)groups.size(); ++g) {
+    for (int32_t j = 0; j < P.gu_per_row; ++j)
+      for (int32_t q = groups[g].first; q < groups[g].second; ++q) {
+        P.items.push_back(gu_item(order[q], j));
+        ++gu_count;
+        while (!pending.empty() && gu_count - pending.front().second >= lag) {
+          emit_down(pending.front().first);
+          pending.pop_front();
+        }
+      }
+    pending.emplace_back(g, gu_count);
+  }
+  while (!pending.empty()) {
+    emit_down(pending.front().first);
+    pending.pop_front();
+  }
+  P.n_gu = (int32_t)gu_count;
+  P.n_down = (int32_t)(P.items.size() - gu_count);
+
+  // Combine plan (Section 3.2.3) and segment composition (Section 3.3.2): per owner group,
+  // the first and last segments are one band, middle segments coalesce x bands.  Rows of a
+  // segment are contiguous in the staged output and in the receive buffer; a slot gap splits
+  // a segment.  Local groups need no transfer when the producer writes them directly.
+  if (p.overlapped) {
+    const int32_t x = std::max<int32_t>(p.mid_bands, 1);
+    const size_t nb = P.bands.size();
+    for (size_t g0 = 0; g0 < nb;) {
+      size_t g1 = g0 + 1;
+      while (g1 < nb && P.bands[g1].expert == P.bands[g0].expert &&
+             P.bands[g1].dst_rank == P.bands[g0].dst_rank)
+        ++g1;
+      const int32_t dst = P.bands[g0].dst_rank;
+      if (dst != p.self || !p.local_direct) {
+        const int32_t k = (int32_t)(g1 - g0);
+        std::vector<std::pair<int32_t, int32_t>> chunks;  // band ranges
+        if (k <= 2) {
+          for (int32_t b = 0; b < k; ++b) chunks.emplace_back(b, b + 1);
+        } else {
+          chunks.emplace_back(0, 1);
+          for (int32_t b = 1; b < k - 1; b += x) chunks.emplace_back(b, std::min(b + x, k - 1));
+          chunks.emplace_back(k - 1, k);
+        }
+        for (auto& c : chunks) {
+          const Band& first = P.bands[g0 + c.first];
+          const Band& last = P.bands[g0 + c.second - 1];
+          const int32_t r0 = first.lrow0, r1 = last.lrow0 + last.nvalid;
+          int32_t s = r0;
+          while (s < r1) {
+            int32_t e_ = s + 1;
+            while (e_ < r1 && P.row_slot[e_] == P.row_slot[e_ - 1] + 1) ++e_;
+            Segment sg{};
+            sg.dst_rank = dst;
+            sg.rows = e_ - s;
+            sg.y_row0 = s;
+            sg.slot0 = P.row_slot[s];
+            const int32_t t0 = s / kTileM, t1 = (e_ - 1) / kTileM;
+            sg.flag_begin = t0 * P.down_per_row;
+            sg.flag_count = (t1 - t0 + 1) * P.down_per_row;
+            int32_t rp = 0;
+            for (int32_t f = sg.flag_begin; f < sg.flag_begin + sg.flag_count; ++f)
+              rp = std::max(rp, pos_of_down[f]);
+            sg.ready_pos = rp;
+            sg.nbands = c.second - c.first;
+            P.segs.push_back(sg);
+            s = e_;
+          }
+        }
+      }
+      g0 = g1;
+    }
+    // The consumer claims segments in the order their data becomes ready.
+    std::stable_sort(P.segs.begin(), P.segs.end(),
+                     [](const Segment& a, const Segment& b) { return a.ready_pos < b.ready_pos; });
+  }
+  return 0;
+}
+
+}  // namespace moe

@@ -1,0 +1,64 @@
+// plan_types.hpp -- plain structs shared by the host plan builder and the gfx950 kernels.
+//
+// The plan is a set of flat tables the host builds per run and uploads once
+// (paper Section 3.2.3: routing is resolved up front into per-tile device
+// arrays so no kernel inspects individual rows' owners at transfer time).
+#pragma once
+#include <stdint.h>
+
+namespace moe {
+
+// GEMM tiling of the producer.  A tile row is kTileM consecutive rows of one
+// expert's padded layout; a gate/up tile covers kGuTileF ffn features (and
+// computes both the gate and the up projection for them); a down tile covers
+// kDownTileN hidden columns.  K advances kTileK elements per step.
+constexpr int kTileM = 256;
+constexpr int kGuTileF = 128;
+constexpr int kDownTileN = 256;
+constexpr int kTileK = 64;
+
+// Work-item encoding: bit 31 = down tile, bits 30..12 = tile row, bits 11..0 = column tile.
+constexpr uint32_t kItemDown = 0x80000000u;
+constexpr int kItemRowShift = 12;
+constexpr uint32_t kItemColMask = 0xFFFu;
+constexpr int32_t kMaxTileRows = 1 << 19;
+constexpr int32_t kMaxColTiles = 1 << 12;
+
+struct TileRow {
+  int32_t expert;      // local expert index
+  int32_t lrow0;       // first logical row (multiple of kTileM)
+  int32_t nvalid;      // routed (non-padding) rows in this tile row
+  int32_t has_remote;  // 1 if any row returns to another rank
+};
+
+struct Segment {
+  int32_t dst_rank;    // receive buffer the rows go to
+  int32_t rows;        // rows in the segment (all valid, slot-contiguous)
+  int32_t y_row0;      // first logical row in the staged output
+  int32_t slot0;       // slot of the first row in the receive buffer
+  int32_t flag_begin;  // first ready flag the segment waits for
+  int32_t flag_count;  // consecutive flags it waits for
+  int32_t ready_pos;   // schedule position of the last down tile it needs
+  int32_t nbands;      // bands it covers (1 for first/last segments)
+};
+
+struct Band {
+  int32_t expert;
+  int32_t lrow0;
+  int32_t nvalid;
+  int32_t dst_rank;    // -1 for a band of padding only
+};
+
+// Device-side counters of one run, zeroed by the init kernel.
+struct RunCounters {
+  uint32_t work_next;       // producer work queue head
+  uint32_t seg_next;        // consumer segment queue head
+  uint32_t timeout;         // set to 1 when a bounded wait expires
+  uint32_t timeout_where;   // 1 = consumer flag wait, 2 = producer dependency wait
+  uint64_t poll_iters;      // consumer poll iterations
+  uint64_t wait_ticks;      // consumer wait time, 100 MHz ticks
+  uint64_t producer_wait_ticks;
+  uint64_t pad[3];
+};
+
+}  // namespace moe

@@ -1,0 +1,249 @@
+"""Host plan builder through the C ABI (no GPU): row layout, tile schedule, combine plan.
+
+Checks the properties the paper states for the remote-owner-aligned layout
+(Section 3.2.1, Algorithm 1), the remote-first schedule (Section 3.2.2), the
+combine plan (Section 3.2.3), the segment composition (Section 3.3.2) and the
+padding bound (Section 4.5, per-expert reading), plus the worked example of
+Section 3.2.2 stored in tests/golden/schedule_example.json.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from paper_2607_19539_amd import binding as B
+from paper_2607_19539_amd.workload import make_workload
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+TILE_M = 256
+
+
+def cfg_for(H, F, E_l, R, self_rank, max_rows, band_rows=32, mgb=1, flags=B.MOE_LOCAL_DIRECT):
+    return B.make_config(H, F, E_l, R, self_rank, max_rows, band_rows, mgb, flags)
+
+
+def routing_from_groups(groups, E_l, R):
+    """groups[e][r] = rows of local expert e from rank r; slots follow (expert, row) per rank."""
+    src, slot, off = [], [], [0]
+    next_slot = [0] * R
+    for e in range(E_l):
+        for r in range(R):
+            for _ in range(groups[e].get(r, 0)):
+                src.append(r)
+                slot.append(next_slot[r])
+                next_slot[r] += 1
+        off.append(len(src))
+    return (np.array(off, np.int32), np.array(src, np.int32), np.array(slot, np.int32),
+            np.array([max(n, 1) for n in next_slot], np.int64))
+
+
+def decode(items):
+    down = (items >> 31) & 1
+    t = (items >> 12) & ((1 << 19) - 1)
+    col = items & 0xFFF
+    return down.astype(int), t.astype(int), col.astype(int)
+
+
+def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True, local_direct=True):
+    info = p["info"]
+    rows = int(off[-1])
+    rank, lslot, rx = p["row_rank"], p["row_slot"], p["row_x"]
+    valid = rank >= 0
+    # every routed row appears exactly once, with its own rank and slot
+    assert valid.sum() == rows
+    assert np.array_equal(np.sort(rx[valid]), np.arange(rows))
+    assert np.array_equal(rank[valid], src[rx[valid]])
+    assert np.array_equal(lslot[valid], slot[rx[valid]])
+    # padding rows feed from a row of the same expert (finite input) and are never stored
+    e_of_row = np.searchsorted(off, np.arange(rows), side="right") - 1
+    tr = p["tile_rows"]
+    assert np.all(tr[:, 1] % TILE_M == 0)
+    for t, (e, l0, nvalid, has_remote) in enumerate(tr):
+        seg = slice(l0, l0 + TILE_M)
+        assert np.all(e_of_row[rx[seg]] == e)
+        assert nvalid == valid[seg].sum()
+        assert has_remote == int(np.any(valid[seg] & (rank[seg] != self_rank)))
+    # items: each gate/up and down tile exactly once; down tiles after all gate/up of their row
+    down, t, col = decode(p["items"])
+    n_tr = len(tr)
+    gu_pos = {}
+    for pos, (d, ti, c) in enumerate(zip(down, t, col)):
+        key = (d, ti, c)
+        assert key not in gu_pos
+        gu_pos[key] = pos
+    assert len(gu_pos) == n_tr * (info["gu_tiles_per_row"] + info["down_tiles_per_row"])
+    last_gu = {ti: max(gu_pos[(0, ti, j)] for j in range(info["gu_tiles_per_row"])) for ti in range(n_tr)}
+    for ti in range(n_tr):
+        first_down = min(gu_pos[(1, ti, n)] for n in range(info["down_tiles_per_row"]))
+        assert first_down > last_gu[ti]
+    if not overlapped:
+        assert info["n_band_padding"] == 0 and info["n_segments"] == 0
+        return
+    # bands: single destination, remote groups band-aligned and first, local group last
+    bands = p["bands"]
+    for e, l0, nvalid, dst in bands:
+        seg = slice(l0, l0 + nvalid)
+        assert np.all(rank[seg] == dst)
+    E_l = len(off) - 1
+    for e in range(E_l):
+        te = tr[tr[:, 0] == e]
+        if len(te) == 0:
+            continue
+        base, end = te[0, 1], te[-1, 1] + TILE_M
+        r_seq = rank[base:end]
+        starts, order_seen = {}, []
+        for i, r in enumerate(r_seq):
+            if r >= 0 and r not in starts:
+                starts[r] = i
+                order_seen.append(r)
+        remote = [r for r in order_seen if r != self_rank]
+        assert remote == sorted(remote)
+        if self_rank in order_seen:
+            assert order_seen[-1] == self_rank
+        for r in remote:
+            assert starts[r] % band_rows == 0
+        # padding bound: (R - 1)(tb_M - 1) band padding per expert (Section 4.5, per expert)
+        n_pad_band = sum((-int(np.sum(r_seq == r))) % band_rows for r in remote)
+        assert n_pad_band <= (R - 1) * (band_rows - 1)
+    # segments cover every row that needs a transfer exactly once
+    segs = p["segments"]
+    covered = np.zeros(len(rank), int)
+    for dst, nrows, y0, s0, fb, fc, rp, nb in segs:
+        assert nrows > 0
+        assert np.all(rank[y0:y0 + nrows] == dst)
+        assert np.array_equal(lslot[y0:y0 + nrows], s0 + np.arange(nrows))
+        covered[y0:y0 + nrows] += 1
+        t0, t1 = y0 // TILE_M, (y0 + nrows - 1) // TILE_M
+        dpr = info["down_tiles_per_row"]
+        assert fb == t0 * dpr and fc == (t1 - t0 + 1) * dpr
+        assert rp == max(gu_pos[(1, ti, n)] for ti in range(t0, t1 + 1) for n in range(dpr))
+        assert 1 <= nb <= max(mgb, 1)
+    need = valid & ((rank != self_rank) | (not local_direct))
+    assert np.array_equal(covered, need.astype(int))
+    assert np.all(np.diff(segs[:, 6]) >= 0) if len(segs) else True
+    # first and last segments of every (expert, destination) group are a single band
+    group_of = {}
+    for s_idx, (dst, nrows, y0, *_rest) in enumerate(segs):
+        e = int(tr[y0 // TILE_M, 0])
+        group_of.setdefault((e, int(dst)), []).append((y0, s_idx))
+    for (e, dst), lst in group_of.items():
+        lst.sort()
+        assert segs[lst[0][1], 7] == 1 and segs[lst[-1][1], 7] == 1
+
+
+def test_golden_schedule_example():
+    g = json.load(open(os.path.join(GOLDEN, "schedule_example.json")))
+    R, E_l, me, tb = g["num_ranks"], g["experts_per_rank"], g["self_rank"], g["band_rows"]
+    glob = [me * E_l + i for i in range(E_l)]
+    groups = [{int(r): n for r, n in g["rows_per_group"][str(e)].items()} for e in glob]
+    off, src, slot, rr = routing_from_groups(groups, E_l, R)
+    cfg = cfg_for(g["hidden"], g["ffn"], E_l, R, me, int(off[-1]), tb)
+    p = B.moe_plan_build(cfg, off, src, slot, rr, producer_grid=8)
+    check_plan(p, off, src, slot, me, R, tb, 1)
+    assert p["tile_rows"][:, 0].tolist() == g["expected_tile_row_experts"]
+    down, t, col = decode(p["items"])
+    order = []
+    for ti in t[down == 0]:
+        if ti not in order:
+            order.append(int(ti))
+    assert order == g["expected_tile_row_order"]
+    bands = p["bands"]
+    for e_glob, want in g["expected_remote_bands"].items():
+        e = glob.index(int(e_glob))
+        assert int(np.sum((bands[:, 0] == e) & (bands[:, 3] != me))) == want
+    # the group from rank 3 is padded up to the band height
+    for e_glob, want in g["expected_padding_from_rank3"].items():
+        e = glob.index(int(e_glob))
+        n3 = groups[e][3]
+        assert (-n3) % tb == want
+
+
+@pytest.mark.parametrize("name,band_rows,mgb", [("tiny", 16, 1), ("tiny", 32, 2), ("fine", 32, 2),
+                                                ("large_fine", 16, 1), ("mixtral_zipf", 64, 2)])
+def test_plan_properties_generated(name, band_rows, mgb):
+    ov = {"T_r": 512} if name != "tiny" else None
+    wl = make_workload(name, weights=None, overrides=ov)
+    cfg = cfg_for(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, band_rows, mgb)
+    p = B.moe_plan_build(cfg, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.return_rows)
+    check_plan(p, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.self_rank, wl.R, band_rows, mgb)
+    ps = B.moe_plan_build(cfg, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.return_rows, overlapped=False)
+    check_plan(ps, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.self_rank, wl.R, 1, 1, overlapped=False)
+
+
+@pytest.mark.parametrize("groups", [
+    [{0: 0, 1: 0, 2: 0}, {0: 5, 1: 0, 2: 0}],          # empty expert, remote-only expert
+    [{0: 300, 1: 0, 2: 0}, {0: 0, 1: 0, 2: 0}],         # all local, one empty expert
+    [{0: 0, 1: 64, 2: 64}, {0: 1, 1: 1, 2: 1}],         # exact band multiples; single rows
+    [{0: 31, 1: 33, 2: 257}, {0: 700, 1: 2, 2: 0}],     # groups smaller/larger than bands and tiles
+])
+def test_plan_edge_cases(groups):
+    R, E_l, me, tb = 3, 2, 0, 32
+    off, src, slot, rr = routing_from_groups(groups, E_l, R)
+    cfg = cfg_for(128, 192, E_l, R, me, max(int(off[-1]), 1), tb, 2)
+    for ld in (True, False):
+        flags = B.MOE_LOCAL_DIRECT if ld else 0
+        cfg.flags = flags
+        p = B.moe_plan_build(cfg, off, src, slot, rr)
+        check_plan(p, off, src, slot, me, R, tb, 2, local_direct=ld)
+
+
+def test_empty_routing():
+    cfg = cfg_for(128, 128, 2, 2, 0, 16)
+    p = B.moe_plan_build(cfg, np.zeros(3, np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32),
+                         np.array([4, 4], np.int64))
+    assert p["info"]["n_items"] == 0 and p["info"]["n_segments"] == 0 and p["info"]["n_logical_rows"] == 0
+
+
+def test_slot_gaps_split_segments():
+    """Rows of one group whose slots are not consecutive go out as separate contiguous segments."""
+    R, E_l, me = 2, 1, 0
+    off = np.array([0, 40], np.int32)
+    src = np.ones(40, np.int32)
+    slot = np.concatenate([np.arange(20), 30 + np.arange(20)]).astype(np.int32)[::-1].copy()
+    rr = np.array([1, 64], np.int64)
+    cfg = cfg_for(64, 64, E_l, R, me, 40, 16, 4)
+    p = B.moe_plan_build(cfg, off, src, slot, rr)
+    check_plan(p, off, src, slot, me, R, 16, 4)
+    segs = p["segments"]
+    starts = sorted(int(s) for s in segs[:, 3])
+    assert 0 in starts and 30 in starts
+
+
+def test_validation_codes_via_plan():
+    wl = make_workload("tiny", weights=None)
+    cfg = cfg_for(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows)
+
+    def code(off=wl.expert_offsets, src=wl.row_src_rank, slot=wl.row_slot, rr=wl.return_rows, c=cfg):
+        try:
+            B.moe_plan_build(c, off, src, slot, rr)
+            return 0
+        except B.MoeError as e:
+            return e.code
+
+    assert code() == 0
+    off = wl.expert_offsets.copy(); off[1] = off[2] + 1
+    assert code(off=off) == B.MOE_EROUTING
+    src = wl.row_src_rank.copy(); src[0] = -1
+    assert code(src=src) == B.MOE_EROUTING
+    slot = wl.row_slot.copy(); slot[2] = wl.return_rows[wl.row_src_rank[2]]
+    assert code(slot=slot) == B.MOE_EROUTING
+    slot = wl.row_slot.copy(); src = wl.row_src_rank.copy(); src[4], slot[4] = src[9], slot[9]
+    assert code(src=src, slot=slot) == B.MOE_EROUTING
+    small = cfg_for(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows - 1)
+    assert code(c=small) == B.MOE_ECAPACITY
+    assert code(c=cfg_for(wl.H + 32, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows)) == B.MOE_EUNSUPPORTED
+    assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, wl.R, wl.rows)) == B.MOE_EINVAL
+    assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, 0, wl.rows, band_rows=48)) == B.MOE_EINVAL
+
+
+def test_band_group_rasterisation_reuses_weights():
+    """Gate/up tiles sweep the ffn columns for a group of tile rows before moving on."""
+    wl = make_workload("mixtral", weights=None, overrides={"T_r": 2048})
+    cfg = cfg_for(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, 32)
+    p = B.moe_plan_build(cfg, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.return_rows)
+    down, t, col = decode(p["items"])
+    gu_t, gu_c = t[down == 0], col[down == 0]
+    # consecutive gate/up tiles share the weight column tile far more often than they change it
+    same_col = np.mean(gu_c[1:] == gu_c[:-1])
+    assert same_col > 0.5
