@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Benchmark of the MI355X MoE expert stage (one expert-parallel rank, one GPU).
+
+A step is one overlapped expert-stage run (moe_stage_run): host plan build and
+upload, the persistent gated-FFN producer with tile-level ready flags and the
+CU-masked consumer copying finished segments into the per-source-rank receive
+buffers.  Inputs (activations, weights, receive buffers) are resident in HBM
+before the timed region; the routing arrays are host inputs by design of the C
+ABI, so each step re-validates and re-uploads the plan.
+
+Prints one JSON line.  ``value`` is the stage's algorithmic bf16 throughput
+(6*H*F flops per routed row, padding excluded) in TFLOP/s; ``ms_per_step`` is
+the expert-stage time; ``overlap_speedup`` is serial time / overlapped time.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "MoE expert-stage µs + bf16 MFMA TFLOP/s vs peak; overlap speedup vs serial"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA peak
+PEAK_HBM_GBS = 8000.0
+
+DESCRIPTIONS = {
+    "tiny": "tiny: H256 F512, SiLU-gated FFN, 8 experts top-2, 4 source ranks x 64 tokens, 2 local experts",
+    "mixtral": "mixtral: H4096 F14336, SiLU-gated FFN, 8 experts top-2, 4 source ranks x 4096 tokens, "
+               "2 local experts, uniform router",
+    "mixtral_zipf": "mixtral_zipf: mixtral shapes, Zipf(1.2) expert popularity (this rank owns the two hottest)",
+    "fine": "fine: H2048 F1408, 64 experts top-6, 4 source ranks x 8192 tokens, 16 local experts",
+    "large_fine": "large_fine: H7168 F2048, 256 experts top-8, 8 source ranks x 4096 tokens, 32 local experts",
+}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="mixtral", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cu-split", type=int, default=8, help="consumer compute units")
+    ap.add_argument("--band-rows", type=int, default=0, help="tb_M of the row layout (0 = library default)")
+    ap.add_argument("--mgb", type=int, default=1, help="bands per middle transfer segment")
+    ap.add_argument("--sweep", default="8,16,32", help="CU splits for the overlap-speedup sweep ('' = none)")
+    ap.add_argument("--only", choices=["all", "serial", "overlapped"], default="all",
+                    help="run only one path (counter collection serialises kernels, so use 'serial' there)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    return ap.parse_args()
+
+
+def cpu_baseline(wl, target_s):
+    """Time the CPU oracle on a bounded sample of the workload's routed rows."""
+    from oracle import oracle as orc
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    o = orc.get()
+
+    def run(n):
+        sub = wl.sample(n)
+        bufs = [np.zeros((int(r), wl.H), np.uint16) for r in wl.return_rows]
+        t0 = time.perf_counter()
+        rc = o.run_workload(sub, bufs, threads)
+        dt = time.perf_counter() - t0
+        assert rc == 0, rc
+        return sub.rows, dt
+
+    n0, t_probe = run(max(threads, 4))
+    rate = n0 / max(t_probe, 1e-6)                         # rows per second
+    n = int(min(wl.rows, max(n0, rate * target_s)))
+    n, dt = run(n)
+    flops = 6.0 * wl.H * wl.F * n
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} of {wl.rows} routed rows ({n / wl.rows:.1%}), {dt:.1f} s wall; full stage "
+                      f"would take ~{dt * wl.rows / n:.0f} s on these cores"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only: the return all-to-all is modelled by "
+                                   "copies into per-source-rank buffers in local HBM; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+    from paper_2607_19539_amd import binding as B
+    from paper_2607_19539_amd.workload import make_workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    log(f"generating workload {args.workload} seed {args.seed}")
+    wl = make_workload(args.workload, seed=args.seed)
+    log(f"rows={wl.rows} H={wl.H} F={wl.F} E_l={wl.E_l} R={wl.R}")
+
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to("cuda")
+
+    x, w1, w3, w2 = dev(wl.dispatched_x), dev(wl.w1), dev(wl.w3), dev(wl.w2)
+    bufs = [torch.zeros((int(n), wl.H), dtype=torch.int16, device="cuda") for n in wl.return_rows]
+    run_args = (x, wl.expert_offsets, wl.row_src_rank, wl.row_slot, w1, w3, w2, bufs, wl.return_rows)
+    flops = wl.flops()
+    stage = B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, args.mgb,
+                       B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, steps, warmup):
+        for _ in range(warmup):
+            fn()
+        stage.query()
+        stage.times(reset=True)
+        torch.cuda.synchronize()
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for _ in range(steps):
+            fn()
+        end.record(stream)
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(end) / steps
+        st = stage.query()
+        tm = stage.times(reset=True)
+        return ms, st, tm
+
+    out = {"metric": METRIC, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded generator, random-init weights N(0,0.02^2), activations N(0,1))"}
+    res = {}
+    if args.only in ("all", "serial"):
+        log("timing serial baseline")
+        ms_s, st_s, tm_s = timed(lambda: stage.run_serial(*run_args, stream=stream), args.steps, args.warmup)
+        res["serial"] = dict(ms=ms_s, producer_ms=tm_s["producer_ms"] / tm_s["runs"],
+                             scatter_ms=tm_s["scatter_ms"] / tm_s["runs"], stats=st_s)
+        log(f"serial: {ms_s * 1e3:.1f} us/step, producer {res['serial']['producer_ms'] * 1e3:.1f} us, "
+            f"scatter {res['serial']['scatter_ms'] * 1e3:.1f} us")
+    if args.only in ("all", "overlapped"):
+        log(f"timing overlapped stage, cu_split={args.cu_split}")
+        ms_o, st_o, tm_o = timed(lambda: stage.run(*run_args, cu_split=args.cu_split, stream=stream),
+                                 args.steps, args.warmup)
+        res["overlapped"] = dict(ms=ms_o, producer_ms=tm_o["producer_ms"] / tm_o["runs"],
+                                 consumer_ms=tm_o["consumer_ms"] / tm_o["runs"], stats=st_o)
+        log(f"overlapped: {ms_o * 1e3:.1f} us/step, producer {res['overlapped']['producer_ms'] * 1e3:.1f} us, "
+            f"consumer {res['overlapped']['consumer_ms'] * 1e3:.1f} us, segments {st_o['n_segments']}, "
+            f"consumer wait {st_o['wait_ticks'] / 100:.0f} us (summed), polls {st_o['poll_iters']}")
+
+    main_path = "overlapped" if "overlapped" in res else "serial"
+    r = res[main_path]
+    out["value"] = flops / (r["ms"] * 1e-3) / 1e12
+    out["ms_per_step"] = r["ms"]
+    out["expert_stage_us"] = r["ms"] * 1e3
+    if "serial" in res:
+        out["serial_stage_us"] = res["serial"]["ms"] * 1e3
+    if "serial" in res and "overlapped" in res:
+        out["overlap_speedup"] = res["serial"]["ms"] / res["overlapped"]["ms"]
+    st = r["stats"]
+    out["config"] = {"workload": DESCRIPTIONS[args.workload], "routed_rows": wl.rows, "path": main_path,
+                     "cu_split": args.cu_split, "consumer_cus": st.get("consumer_cus", 0),
+                     "band_rows": stage.cfg.band_rows or "default", "mid_segment_bands": args.mgb,
+                     "padding_rows": int(st["n_logical_rows"] - st["n_valid"]),
+                     "band_padding_rows": int(st["n_band_padding"]), "plan_us": round(st["plan_us"], 1),
+                     "seed": args.seed}
+    # Dominant kernel: the producer (all MFMA work).  Its duration comes from HIP events the library
+    # records on the producer's own stream around every launch in the timed region.
+    prod_ms = r["producer_ms"]
+    achieved = flops / (prod_ms * 1e-3) / 1e12
+    out["producer_us"] = prod_ms * 1e3
+    out["roofline"] = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                       "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                       "kernel": "moe::producer_kernel", "flops_per_launch": flops}
+    if "overlapped" in res:
+        cons_bytes = 4.0 * wl.H * st["n_remote_rows"]
+        out["consumer"] = {"us": res["overlapped"]["consumer_ms"] * 1e3, "bytes": cons_bytes,
+                           "busy_GBps_lower_bound": cons_bytes / (res["overlapped"]["consumer_ms"] * 1e-3) / 1e9,
+                           "flag_wait_us_summed": st["wait_ticks"] / 100.0, "poll_iters": int(st["poll_iters"]),
+                           "segments": int(st["n_segments"])}
+    if args.sweep and "serial" in res and args.only == "all":
+        sweep = []
+        for c in [int(v) for v in args.sweep.split(",") if v]:
+            for mgb in (1, 2):
+                s2 = B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, mgb,
+                                B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING)
+                old, stage = stage, s2
+                ms_c, st_c, _ = timed(lambda: stage.run(*run_args, cu_split=c, stream=stream),
+                                      max(args.steps // 2, 5), max(args.warmup // 2, 2))
+                stage = old
+                s2.close()
+                sweep.append({"cu_split": c, "consumer_cus": st_c["consumer_cus"], "mgb": mgb,
+                              "stage_us": ms_c * 1e3, "speedup_vs_serial": res["serial"]["ms"] / ms_c})
+                log(f"sweep c={c} mgb={mgb}: {ms_c * 1e3:.1f} us, speedup {res['serial']['ms'] / ms_c:.3f}")
+        out["cu_split_sweep"] = sweep
+    stage.close()
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -64,6 +64,9 @@ extern "C" {
 #define MOE_KERNEL_TIMING (1u << 1) /* record HIP events around each kernel of every run       */
 #define MOE_POISON (1u << 2)        /* fill the staged output with NaN before each run, so a
                                        copy that races ahead of its data is detectable          */
+#define MOE_TEST_NO_SIGNAL (1u << 3) /* testing aid: the producer raises no ready flags, so every
+                                       consumer wait runs into watchdog_ms and the run reports
+                                       MOE_ETIMEOUT; the kernels still exit normally            */
 
 typedef struct moe_stage_s* moe_stage_t;
 

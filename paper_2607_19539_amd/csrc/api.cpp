@@ -66,6 +66,7 @@ struct moe_stage_s {
   hipStream_t s_cons = nullptr, s_prod = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join_c = nullptr, ev_join_p = nullptr, ev_done = nullptr;
   bool ran = false;
+  bool counters_pending = false;  // the last run's device counters have not been read yet
 
   std::vector<TimingRec> ring;
   int ring_next = 0, ring_count = 0;
@@ -404,7 +405,7 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   h->last.producer_grid = pgrid;
   h->last.consumer_grid = cgrid;
   h->last.consumer_cus = c_eff;
-  uint32_t mode = kModeSignal;
+  uint32_t mode = (h->cfg.flags & MOE_TEST_NO_SIGNAL) ? 0u : kModeSignal;
   if (h->cfg.flags & MOE_LOCAL_DIRECT) mode |= kModeLocalDirect;
   const ProducerArgs pa = producer_args(h, lay, x, w1, w3, w2, mode);
   ConsumerArgs ca{};
@@ -442,6 +443,7 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   }
   HIP_TRY(h, hipEventRecord(h->ev_done, stream));
   h->ran = true;
+  h->counters_pending = true;
   return MOE_OK;
 }
 
@@ -482,13 +484,15 @@ int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const
   }
   HIP_TRY(h, hipEventRecord(h->ev_done, stream));
   h->ran = true;
+  h->counters_pending = true;
   return MOE_OK;
 }
 
 int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
   if (!h || !out) return MOE_EINVAL;
-  if (h->ran) {
-    HIP_TRY(h, hipEventSynchronize(h->ev_done));
+  if (h->ran) HIP_TRY(h, hipEventSynchronize(h->ev_done));
+  if (h->counters_pending) {
+    h->counters_pending = false;
     RunCounters c{};
     HIP_TRY(h, hipMemcpy(&c, h->ctr, sizeof c, hipMemcpyDeviceToHost));
     h->last.poll_iters = c.poll_iters;

@@ -118,6 +118,29 @@ class Workload:
         """Algorithmic flops of the stage: 6*H*F per routed row (gate + up + down)."""
         return 6.0 * self.H * self.F * self.rows
 
+    def subset(self, rows_idx) -> "Workload":
+        """The same stage restricted to some routed rows (weights and receive buffers unchanged)."""
+        import copy
+        idx = np.sort(np.asarray(rows_idx, dtype=np.int64))
+        e_of = np.searchsorted(self.expert_offsets, idx, side="right") - 1
+        s = copy.copy(self)
+        s.dispatched_x = self.dispatched_x[idx]
+        s.row_src_rank = self.row_src_rank[idx]
+        s.row_slot = self.row_slot[idx]
+        s.row_token = self.row_token[idx]
+        s.row_j = self.row_j[idx]
+        off = np.zeros(self.E_l + 1, np.int32)
+        off[1:] = np.cumsum(np.bincount(e_of, minlength=self.E_l))
+        s.expert_offsets = off
+        return s
+
+    def sample(self, n: int, seed: int = 12345) -> "Workload":
+        """A seeded uniform sample of n routed rows (all rows if n >= rows)."""
+        if n >= self.rows:
+            return self
+        g = np.random.default_rng(np.random.SeedSequence([seed, 7]))
+        return self.subset(g.choice(self.rows, size=n, replace=False))
+
 
 def _router_logits(name: str, cfg: dict, seed: int) -> np.ndarray:
     R, T, E = cfg["R"], cfg["T_r"], cfg["E_t"]

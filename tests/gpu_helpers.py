@@ -88,16 +88,4 @@ def compare(gpu, ref, rel_l2=8e-3):
 
 def sub_workload(wl, rows_idx):
     """The same stage restricted to a subset of routed rows (for sampled full-size checks)."""
-    import copy
-    rows_idx = np.sort(np.asarray(rows_idx))
-    e_of = np.searchsorted(wl.expert_offsets, rows_idx, side="right") - 1
-    s = copy.copy(wl)
-    s.dispatched_x = wl.dispatched_x[rows_idx]
-    s.row_src_rank = wl.row_src_rank[rows_idx]
-    s.row_slot = wl.row_slot[rows_idx]
-    s.row_token = wl.row_token[rows_idx]
-    s.row_j = wl.row_j[rows_idx]
-    off = np.zeros(wl.E_l + 1, np.int32)
-    off[1:] = np.cumsum(np.bincount(e_of, minlength=wl.E_l))
-    s.expert_offsets = off
-    return s
+    return wl.subset(rows_idx)
