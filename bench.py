@@ -113,6 +113,7 @@ def main():
     stage = B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, args.mgb,
                        B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING)
     stream = torch.cuda.current_stream()
+    timeouts = []
 
     def timed(fn, steps, warmup):
         for _ in range(warmup):
@@ -127,7 +128,10 @@ def main():
         end.record(stream)
         torch.cuda.synchronize()
         ms = start.elapsed_time(end) / steps
-        st = stage.query()
+        st = stage.query(check=False)
+        if st["rc"] != 0:
+            log(f"ERROR: {B.moe_stage_last_error(stage.h)} -- timing invalid")
+            timeouts.append(B.moe_stage_last_error(stage.h))
         tm = stage.times(reset=True)
         return ms, st, tm
 
@@ -198,6 +202,7 @@ def main():
                 log(f"sweep c={c} mgb={mgb}: {ms_c * 1e3:.1f} us, speedup {res['serial']['ms'] / ms_c:.3f}")
         out["cu_split_sweep"] = sweep
     stage.close()
+    out["watchdog_timeouts"] = timeouts
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)

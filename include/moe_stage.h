@@ -103,7 +103,8 @@ typedef struct {
   int32_t consumer_grid;    /* persistent consumer workgroups launched                      */
   int32_t consumer_cus;     /* compute units reserved for the consumer (cu_split rounded up
                                to a multiple of the XCD count; 0 for serial runs)            */
-  int32_t timeout;          /* 1 if a device wait hit the watchdog                           */
+  int32_t timeout;          /* 1 if a device wait hit the watchdog in any run since the last
+                               query (sticky across runs)                                    */
   double plan_us;           /* host time to validate and build the plan                      */
   uint64_t poll_iters;      /* consumer flag-poll iterations summed over segments            */
   uint64_t wait_ticks;      /* consumer time spent waiting for flags (100 MHz ticks)         */
@@ -152,7 +153,8 @@ int moe_stage_run_serial(moe_stage_t h, const void* dispatched_x, const int32_t*
                          const void* w3, const void* w2, void* const* return_bufs,
                          const int64_t* return_rows, void* stream);
 
-/* Statistics of the last run; synchronizes with it.  Returns MOE_ETIMEOUT once after a timeout. */
+/* Statistics of the last run; synchronizes with it.  Returns MOE_ETIMEOUT (once) if any run
+ * since the previous query had a device wait expire; its outputs are then incomplete. */
 int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out);
 
 /* Kernel times accumulated since the last reset (needs MOE_KERNEL_TIMING); synchronizes. */

@@ -67,6 +67,7 @@ struct moe_stage_s {
   hipEvent_t ev_fork = nullptr, ev_join_c = nullptr, ev_join_p = nullptr, ev_done = nullptr;
   bool ran = false;
   bool counters_pending = false;  // the last run's device counters have not been read yet
+  uint32_t last_timeouts = 0, last_timeout_where = 0;
 
   std::vector<TimingRec> ring;
   int ring_next = 0, ring_count = 0;
@@ -172,6 +173,8 @@ int prepare(moe_stage_s* h, bool overlapped, int producer_grid, const void* x,
                      (int64_t)P.segs.size(), c.num_ranks);
   if (lay->total > h->plan_cap) return set_err(h, MOE_ECAPACITY, "plan exceeds the plan buffer");
 
+  h->last.plan_us =
+      std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
   // Stage into pinned memory (wait until the copy that last used this half finished).
   const int si = h->stage_idx;
   h->stage_idx ^= 1;
@@ -184,8 +187,6 @@ int prepare(moe_stage_s* h, bool overlapped, int producer_grid, const void* x,
   memcpy(hs + lay->row_slot, P.row_slot.data(), sizeof(int32_t) * P.row_slot.size());
   memcpy(hs + lay->segs, P.segs.data(), sizeof(Segment) * P.segs.size());
   memcpy(hs + lay->ret, ret, sizeof(void*) * (size_t)c.num_ranks);
-  h->last.plan_us =
-      std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
 
   HIP_TRY(h, hipMemcpyAsync(h->d_plan, hs, lay->total, hipMemcpyHostToDevice, stream));
   HIP_TRY(h, hipEventRecord(h->stage_free[si], stream));
@@ -498,13 +499,21 @@ int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
     h->last.poll_iters = c.poll_iters;
     h->last.wait_ticks = c.wait_ticks;
     h->last.producer_wait_ticks = c.producer_wait_ticks;
-    h->last.timeout = (int32_t)c.timeout;
+    h->last.timeout = c.timeouts ? 1 : 0;
+    h->last_timeouts = c.timeouts;
+    h->last_timeout_where = c.timeout_where;
+    if (c.timeouts) {  // sticky across runs until reported here
+      const uint32_t zero[2] = {0, 0};
+      HIP_TRY(h, hipMemcpy(&h->ctr->timeouts, zero, sizeof zero, hipMemcpyHostToDevice));
+    }
   }
   *out = h->last;
   if (h->last.timeout) {
     h->last.timeout = 0;
     return set_err(h, MOE_ETIMEOUT,
-                   "a device wait hit the watchdog (1 = consumer flag wait, 2 = producer dependency)");
+                   std::to_string(h->last_timeouts) + " device wait(s) hit the watchdog since the last query (" +
+                       ((h->last_timeout_where & 1) ? "consumer flag wait " : "") +
+                       ((h->last_timeout_where & 2) ? "producer dependency wait" : "") + ")");
   }
   return MOE_OK;
 }

@@ -174,8 +174,8 @@ __device__ void producer_item(const ProducerArgs& a, uint32_t item, uint8_t* lds
     __syncthreads();
     if (s_timeout) {
       if (tid == 0) {
-        __hip_atomic_store(&a.ctr->timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&a.ctr->timeout_where, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(&a.ctr->timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_or(&a.ctr->timeout_where, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       return;
     }
@@ -307,8 +307,8 @@ __global__ __launch_bounds__(kConsumerThreads) void consumer_kernel(ConsumerArgs
     __syncthreads();
     if (s_abort) {
       if (tid == 0) {
-        __hip_atomic_store(&a.ctr->timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&a.ctr->timeout_where, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(&a.ctr->timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_or(&a.ctr->timeout_where, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       break;
     }
@@ -353,8 +353,6 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
   if (i == 0) {
     a.ctr->work_next = 0;
     a.ctr->seg_next = 0;
-    a.ctr->timeout = 0;
-    a.ctr->timeout_where = 0;
     a.ctr->poll_iters = 0;
     a.ctr->wait_ticks = 0;
     a.ctr->producer_wait_ticks = 0;

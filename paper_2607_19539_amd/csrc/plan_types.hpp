@@ -53,8 +53,8 @@ struct Band {
 struct RunCounters {
   uint32_t work_next;       // producer work queue head
   uint32_t seg_next;        // consumer segment queue head
-  uint32_t timeout;         // set to 1 when a bounded wait expires
-  uint32_t timeout_where;   // 1 = consumer flag wait, 2 = producer dependency wait
+  uint32_t timeouts;        // bounded waits that expired; NOT reset per run (cleared by a query)
+  uint32_t timeout_where;   // bit 0 = consumer flag wait, bit 1 = producer dependency wait
   uint64_t poll_iters;      // consumer poll iterations
   uint64_t wait_ticks;      // consumer wait time, 100 MHz ticks
   uint64_t producer_wait_ticks;
