@@ -143,16 +143,19 @@ def main():
         log("timing serial baseline")
         ms_s, st_s, tm_s = timed(lambda: stage.run_serial(*run_args, stream=stream), args.steps, args.warmup)
         res["serial"] = dict(ms=ms_s, producer_ms=tm_s["producer_ms"] / tm_s["runs"],
+                             gate_up_ms=tm_s["gate_up_ms"] / tm_s["runs"],
                              scatter_ms=tm_s["scatter_ms"] / tm_s["runs"], stats=st_s)
-        log(f"serial: {ms_s * 1e3:.1f} us/step, producer {res['serial']['producer_ms'] * 1e3:.1f} us, "
-            f"scatter {res['serial']['scatter_ms'] * 1e3:.1f} us")
+        log(f"serial: {ms_s * 1e3:.1f} us/step, producer {res['serial']['producer_ms'] * 1e3:.1f} us "
+            f"(gate/up {res['serial']['gate_up_ms'] * 1e3:.1f} us), scatter {res['serial']['scatter_ms'] * 1e3:.1f} us")
     if args.only in ("all", "overlapped"):
         log(f"timing overlapped stage, cu_split={args.cu_split}")
         ms_o, st_o, tm_o = timed(lambda: stage.run(*run_args, cu_split=args.cu_split, stream=stream),
                                  args.steps, args.warmup)
         res["overlapped"] = dict(ms=ms_o, producer_ms=tm_o["producer_ms"] / tm_o["runs"],
+                                 gate_up_ms=tm_o["gate_up_ms"] / tm_o["runs"],
                                  consumer_ms=tm_o["consumer_ms"] / tm_o["runs"], stats=st_o)
-        log(f"overlapped: {ms_o * 1e3:.1f} us/step, producer {res['overlapped']['producer_ms'] * 1e3:.1f} us, "
+        log(f"overlapped: {ms_o * 1e3:.1f} us/step, producer {res['overlapped']['producer_ms'] * 1e3:.1f} us "
+            f"(gate/up {res['overlapped']['gate_up_ms'] * 1e3:.1f} us), "
             f"consumer {res['overlapped']['consumer_ms'] * 1e3:.1f} us, segments {st_o['n_segments']}, "
             f"consumer wait {st_o['wait_ticks'] / 100:.0f} us (summed), polls {st_o['poll_iters']}")
 
@@ -177,9 +180,12 @@ def main():
     prod_ms = r["producer_ms"]
     achieved = flops / (prod_ms * 1e-3) / 1e12
     out["producer_us"] = prod_ms * 1e3
+    out["producer_gate_up_us"] = r["gate_up_ms"] * 1e3
+    out["producer_down_us"] = (prod_ms - r["gate_up_ms"]) * 1e3
     out["roofline"] = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                        "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                       "kernel": "moe::producer_kernel", "flops_per_launch": flops}
+                       "kernel": "moe::producer_kernel (gate/up launch + down launch)",
+                       "flops_per_launch": flops}
     if "overlapped" in res:
         cons_bytes = 4.0 * wl.H * st["n_remote_rows"]
         out["consumer"] = {"us": res["overlapped"]["consumer_ms"] * 1e3, "bytes": cons_bytes,

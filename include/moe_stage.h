@@ -108,14 +108,14 @@ typedef struct {
   double plan_us;           /* host time to validate and build the plan                      */
   uint64_t poll_iters;      /* consumer flag-poll iterations summed over segments            */
   uint64_t wait_ticks;      /* consumer time spent waiting for flags (100 MHz ticks)         */
-  uint64_t producer_wait_ticks; /* producer time spent waiting on gate/up dependencies       */
 } moe_stage_stats_t;
 
 /* Accumulated kernel times (MOE_KERNEL_TIMING), milliseconds, over runs since the last reset. */
 typedef struct {
   int32_t runs;
   double stage_ms;     /* fork to join of each run (overlapped) or first to last kernel (serial) */
-  double producer_ms;  /* producer kernel                                                */
+  double producer_ms;  /* producer: gate/up launch start to down launch end              */
+  double gate_up_ms;   /* gate/up launch                                                 */
   double consumer_ms;  /* consumer kernel (overlapped runs)                              */
   double scatter_ms;   /* scatter kernel (serial runs)                                   */
 } moe_stage_times_t;
@@ -126,10 +126,11 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out);
 /*
  * Overlapped stage (paper Section 3.3): builds the remote-owner-aligned row
  * layout, remote-first tile schedule and combine plan (Section 3.2, Algorithm
- * 1) on the host, then launches a persistent consumer on `cu_split` compute
- * units and the persistent rank-wide producer on the remaining ones.  The
- * producer raises a ready flag per finished down-projection tile; the
- * consumer copies each ready segment into return_bufs[destination].  The
+ * 1) on the host, then runs the persistent rank-wide producer (a gate/up launch,
+ * then the down-projection launch) on all but `cu_split` compute units and a
+ * persistent consumer on the others.  The down launch raises a ready flag per
+ * finished tile; the consumer, released when the gate/up launch completes,
+ * copies each ready segment into return_bufs[destination].  The
  * work is ordered after prior work on `stream` (a hipStream_t; NULL = null
  * stream) and later work on `stream` sees the results.
  *
@@ -183,7 +184,8 @@ typedef struct {
 
 /* Tables readable with moe_plan_copy:
  *   MOE_PLAN_TILE_ROWS  int32 [n_tile_rows][4]: expert, first logical row, valid rows, has_remote
- *   MOE_PLAN_ITEMS      uint32 [n_items]: bit 31 = down tile, bits 30..12 tile row, 11..0 column tile
+ *   MOE_PLAN_ITEMS      uint32 [n_items]: bit 31 = down tile, bits 30..12 tile row, 11..0 column
+ *                       tile; all gate/up tiles (first launch) precede all down tiles
  *   MOE_PLAN_ROW_X      int32 [n_logical_rows]: dispatched_x row feeding each logical row
  *                       (padding rows repeat a valid row of the same expert)
  *   MOE_PLAN_ROW_RANK   int32 [n_logical_rows]: source rank, -1 for padding
@@ -200,13 +202,10 @@ typedef struct {
 #define MOE_PLAN_SEGMENTS 5
 #define MOE_PLAN_BANDS 6
 
-/* `producer_grid` models the number of persistent producer workgroups (it sets how far the
- * down tiles of a tile row lag behind its gate/up tiles); `overlapped` selects the plan of
- * moe_stage_run (1) or moe_stage_run_serial (0). */
+/* `overlapped` selects the plan of moe_stage_run (1) or moe_stage_run_serial (0). */
 int moe_plan_build(const moe_stage_config_t* cfg, int64_t rows, const int32_t* expert_offsets,
                    const int32_t* row_src_rank, const int32_t* row_slot,
-                   const int64_t* return_rows, int32_t producer_grid, int32_t overlapped,
-                   moe_plan_t* out);
+                   const int64_t* return_rows, int32_t overlapped, moe_plan_t* out);
 int moe_plan_info(moe_plan_t p, moe_plan_info_t* out);
 /* Copies table `which` into `dst` (host memory of at least `bytes`); returns bytes needed if
  * dst is NULL, else MOE_OK or MOE_EINVAL when bytes is too small. */

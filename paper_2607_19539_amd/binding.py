@@ -41,13 +41,12 @@ class moe_stage_stats_t(ctypes.Structure):
                 ("n_gu_items", ctypes.c_int32), ("n_down_items", ctypes.c_int32), ("n_segments", ctypes.c_int32),
                 ("producer_grid", ctypes.c_int32), ("consumer_grid", ctypes.c_int32), ("consumer_cus", ctypes.c_int32),
                 ("timeout", ctypes.c_int32),
-                ("plan_us", ctypes.c_double), ("poll_iters", ctypes.c_uint64), ("wait_ticks", ctypes.c_uint64),
-                ("producer_wait_ticks", ctypes.c_uint64)]
+                ("plan_us", ctypes.c_double), ("poll_iters", ctypes.c_uint64), ("wait_ticks", ctypes.c_uint64)]
 
 
 class moe_stage_times_t(ctypes.Structure):
     _fields_ = [("runs", ctypes.c_int32), ("stage_ms", ctypes.c_double), ("producer_ms", ctypes.c_double),
-                ("consumer_ms", ctypes.c_double), ("scatter_ms", ctypes.c_double)]
+                ("gate_up_ms", ctypes.c_double), ("consumer_ms", ctypes.c_double), ("scatter_ms", ctypes.c_double)]
 
 
 class moe_plan_info_t(ctypes.Structure):
@@ -82,7 +81,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.moe_stage_last_error.argtypes = [vp]
     lib.moe_stage_last_error.restype = ctypes.c_char_p
     lib.moe_stage_destroy.argtypes = [vp]
-    lib.moe_plan_build.argtypes = [ctypes.POINTER(moe_stage_config_t), i64, vp, vp, vp, vp, i32, i32,
+    lib.moe_plan_build.argtypes = [ctypes.POINTER(moe_stage_config_t), i64, vp, vp, vp, vp, i32,
                                    ctypes.POINTER(vp)]
     lib.moe_plan_info.argtypes = [vp, ctypes.POINTER(moe_plan_info_t)]
     lib.moe_plan_copy.argtypes = [vp, i32, vp, i64]
@@ -211,14 +210,14 @@ def moe_stage_destroy(h) -> int:
 
 
 def moe_plan_build(cfg: moe_stage_config_t, expert_offsets, row_src_rank, row_slot, return_rows,
-                   producer_grid: int = 256, overlapped: bool = True) -> dict:
+                   overlapped: bool = True) -> dict:
     """Build the plan on the host and return its tables as numpy arrays (no GPU needed)."""
     lib = load()
     off, src, slot, rr = _host_i32(expert_offsets), _host_i32(row_src_rank), _host_i32(row_slot), _host_i64(return_rows)
     p = ctypes.c_void_p()
     rows = int(off[-1]) if off.size else 0
     _check(lib.moe_plan_build(ctypes.byref(cfg), rows, _np_ptr(off), _np_ptr(src), _np_ptr(slot), _np_ptr(rr),
-                              int(producer_grid), int(bool(overlapped)), ctypes.byref(p)))
+                              int(bool(overlapped)), ctypes.byref(p)))
     try:
         info = moe_plan_info_t()
         _check(lib.moe_plan_info(p, ctypes.byref(info)))

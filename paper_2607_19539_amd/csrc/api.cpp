@@ -31,8 +31,8 @@ thread_local std::string g_create_error;
 constexpr int kTimingRing = 512;
 
 struct TimingRec {
-  hipEvent_t ev[6];  // 0 stage start, 1 producer start, 2 producer end, 3 consumer start,
-                     // 4 consumer end / scatter start, 5 stage end / scatter end
+  hipEvent_t ev[7];  // 0 stage start, 1 producer start, 2 producer end, 3 consumer start,
+                     // 4 consumer end / scatter start, 5 stage end / scatter end, 6 gate/up end
   int kind = -1;     // 0 overlapped, 1 serial
 };
 
@@ -53,7 +53,6 @@ struct moe_stage_s {
   uint16_t* hws = nullptr;
   uint16_t* y = nullptr;
   uint32_t* flags = nullptr;
-  uint32_t* gu_done = nullptr;
   RunCounters* ctr = nullptr;
   uint8_t* d_plan = nullptr;
   size_t plan_cap = 0;
@@ -64,7 +63,7 @@ struct moe_stage_s {
 
   int cached_split = -1;
   hipStream_t s_cons = nullptr, s_prod = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join_c = nullptr, ev_join_p = nullptr, ev_done = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_gu = nullptr, ev_join_c = nullptr, ev_join_p = nullptr, ev_done = nullptr;
   bool ran = false;
   bool counters_pending = false;  // the last run's device counters have not been read yet
   uint32_t last_timeouts = 0, last_timeout_where = 0;
@@ -94,7 +93,7 @@ int set_err(moe_stage_s* h, int code, const std::string& msg) {
       return set_err((h), MOE_EHIP, std::string(#call) + ": " + hipGetErrorString(e__));   \
   } while (0)
 
-PlanParams params_of(const moe_stage_config_t& c, bool overlapped, int producer_grid) {
+PlanParams params_of(const moe_stage_config_t& c, bool overlapped) {
   PlanParams p;
   p.H = c.hidden;
   p.F = c.ffn;
@@ -105,7 +104,6 @@ PlanParams params_of(const moe_stage_config_t& c, bool overlapped, int producer_
   p.mid_bands = std::max(c.mid_segment_bands, 1);
   p.local_direct = (c.flags & MOE_LOCAL_DIRECT) != 0;
   p.overlapped = overlapped;
-  p.producer_grid = producer_grid;
   return p;
 }
 
@@ -146,7 +144,7 @@ uint64_t watchdog_ticks(const moe_stage_s* h) {
 }
 
 // Validates and builds the plan, uploads it and resets the run counters, all on `stream`.
-int prepare(moe_stage_s* h, bool overlapped, int producer_grid, const void* x,
+int prepare(moe_stage_s* h, bool overlapped, const void* x,
             const int32_t* off, const int32_t* src, const int32_t* slot, const void* w1,
             const void* w3, const void* w2, void* const* ret, const int64_t* return_rows,
             hipStream_t stream, BlobLayout* lay) {
@@ -163,8 +161,7 @@ int prepare(moe_stage_s* h, bool overlapped, int producer_grid, const void* x,
     if (!ret[r] && return_rows[r] > 0) return set_err(h, MOE_EINVAL, "null return buffer");
 
   std::string msg;
-  int rc = build_plan(params_of(c, overlapped, producer_grid), rows, off, src, slot, return_rows,
-                      &h->plan, &msg);
+  int rc = build_plan(params_of(c, overlapped), rows, off, src, slot, return_rows, &h->plan, &msg);
   if (rc) return set_err(h, rc, msg);
   const Plan& P = h->plan;
   if (P.n_lrows() > h->max_lrows || (int64_t)P.tile_rows.size() > h->max_tile_rows)
@@ -193,8 +190,6 @@ int prepare(moe_stage_s* h, bool overlapped, int producer_grid, const void* x,
 
   InitArgs ia{};
   ia.ctr = h->ctr;
-  ia.gu_done = h->gu_done;
-  ia.n_tile_rows = (int32_t)P.tile_rows.size();
   if (c.flags & MOE_POISON) {
     ia.poison = h->y;
     ia.poison_elems = P.n_lrows() * c.hidden;
@@ -216,7 +211,7 @@ int prepare(moe_stage_s* h, bool overlapped, int producer_grid, const void* x,
 }
 
 ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x, const void* w1,
-                           const void* w3, const void* w2, uint32_t mode) {
+                           const void* w3, const void* w2, uint32_t mode, bool down) {
   const Plan& P = h->plan;
   ProducerArgs a{};
   a.x = (const uint16_t*)x;
@@ -226,23 +221,20 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
   a.hws = h->hws;
   a.y = h->y;
   a.tile_rows = (const TileRow*)(h->d_plan + lay.tile_rows);
-  a.items = (const uint32_t*)(h->d_plan + lay.items);
-  a.n_items = (int32_t)P.items.size();
+  a.items = (const uint32_t*)(h->d_plan + lay.items) + (down ? P.n_gu : 0);
+  a.n_items = down ? P.n_down : P.n_gu;
+  a.claim = down ? &h->ctr->down_next : &h->ctr->gu_next;
   a.row_x = (const int32_t*)(h->d_plan + lay.row_x);
   a.row_rank = (const int32_t*)(h->d_plan + lay.row_rank);
   a.row_slot = (const int32_t*)(h->d_plan + lay.row_slot);
   a.ret = (uint16_t* const*)(h->d_plan + lay.ret);
-  a.ctr = h->ctr;
-  a.gu_done = h->gu_done;
   a.flags = h->flags;
   a.epoch = h->epoch;
   a.H = h->cfg.hidden;
   a.F = h->cfg.ffn;
   a.self_rank = h->cfg.self_rank;
-  a.gu_per_row = P.gu_per_row;
   a.down_per_row = P.down_per_row;
   a.mode = mode;
-  a.watchdog_ticks = watchdog_ticks(h);
   return a;
 }
 
@@ -353,7 +345,6 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   if (!try_hip(hipMalloc(&h->hws, hws_bytes), "hipMalloc(hws)") ||
       !try_hip(hipMalloc(&h->y, y_bytes), "hipMalloc(y)") ||
       !try_hip(hipMalloc(&h->flags, flag_bytes), "hipMalloc(flags)") ||
-      !try_hip(hipMalloc(&h->gu_done, (size_t)h->max_tile_rows * 4), "hipMalloc(gu_done)") ||
       !try_hip(hipMalloc(&h->ctr, sizeof(RunCounters)), "hipMalloc(counters)") ||
       !try_hip(hipMalloc(&h->d_plan, h->plan_cap), "hipMalloc(plan)") ||
       !try_hip(hipHostMalloc(&h->h_stage[0], h->plan_cap, hipHostMallocDefault), "hipHostMalloc") ||
@@ -368,6 +359,7 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
         !try_hip(hipEventRecord(h->stage_free[i], nullptr), "hipEventRecord"))
       return bail(MOE_EHIP);
   if (!try_hip(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming), "hipEventCreate") ||
+      !try_hip(hipEventCreateWithFlags(&h->ev_gu, hipEventDisableTiming), "hipEventCreate") ||
       !try_hip(hipEventCreateWithFlags(&h->ev_join_c, hipEventDisableTiming), "hipEventCreate") ||
       !try_hip(hipEventCreateWithFlags(&h->ev_join_p, hipEventDisableTiming), "hipEventCreate") ||
       !try_hip(hipEventCreateWithFlags(&h->ev_done, hipEventDisableTiming), "hipEventCreate"))
@@ -398,7 +390,7 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   BlobLayout lay{};
   TimingRec* tr = timing_slot(h);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[0], stream));
-  rc = prepare(h, true, pgrid, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
+  rc = prepare(h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
   if (rc) {
     if (tr) h->ring_next = (h->ring_next + kTimingRing - 1) % kTimingRing, --h->ring_count;
     return rc;
@@ -408,10 +400,11 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   h->last.consumer_cus = c_eff;
   uint32_t mode = (h->cfg.flags & MOE_TEST_NO_SIGNAL) ? 0u : kModeSignal;
   if (h->cfg.flags & MOE_LOCAL_DIRECT) mode |= kModeLocalDirect;
-  const ProducerArgs pa = producer_args(h, lay, x, w1, w3, w2, mode);
+  const ProducerArgs pgu = producer_args(h, lay, x, w1, w3, w2, mode, false);
+  const ProducerArgs pdn = producer_args(h, lay, x, w1, w3, w2, mode, true);
   ConsumerArgs ca{};
   ca.y = h->y;
-  ca.ret = pa.ret;
+  ca.ret = pgu.ret;
   ca.segs = (const Segment*)(h->d_plan + lay.segs);
   ca.n_segs = (int32_t)h->plan.segs.size();
   ca.flags = h->flags;
@@ -420,19 +413,20 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   ca.ctr = h->ctr;
   ca.watchdog_ticks = watchdog_ticks(h);
 
+  // Producer stream: gate/up GEMM, then the signaling down GEMM.  The consumer is released
+  // when the gate/up launch completes (down tiles, the only transfer sources, start then),
+  // and is enqueued before the down launch so its workgroups are resident first.
   HIP_TRY(h, hipEventRecord(h->ev_fork, stream));
-  HIP_TRY(h, hipStreamWaitEvent(h->s_cons, h->ev_fork, 0));
   HIP_TRY(h, hipStreamWaitEvent(h->s_prod, h->ev_fork, 0));
-  if (ca.n_segs > 0) {
-    if (tr) HIP_TRY(h, hipEventRecord(tr->ev[3], h->s_cons));
-    HIP_TRY(h, launch_consumer(ca, cgrid, h->s_cons));
-    if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
-  } else if (tr) {
-    HIP_TRY(h, hipEventRecord(tr->ev[3], h->s_cons));
-    HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
-  }
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], h->s_prod));
-  if (pa.n_items > 0) HIP_TRY(h, launch_producer(pa, pgrid, h->s_prod));
+  if (pgu.n_items > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, h->s_prod));
+  HIP_TRY(h, hipEventRecord(h->ev_gu, h->s_prod));
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], h->s_prod));
+  HIP_TRY(h, hipStreamWaitEvent(h->s_cons, h->ev_gu, 0));
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[3], h->s_cons));
+  if (ca.n_segs > 0) HIP_TRY(h, launch_consumer(ca, cgrid, h->s_cons));
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
+  if (pdn.n_items > 0) HIP_TRY(h, launch_producer(pdn, true, pgrid, h->s_prod));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], h->s_prod));
   HIP_TRY(h, hipEventRecord(h->ev_join_c, h->s_cons));
   HIP_TRY(h, hipEventRecord(h->ev_join_p, h->s_prod));
@@ -457,7 +451,7 @@ int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const
   BlobLayout lay{};
   TimingRec* tr = timing_slot(h);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[0], stream));
-  int rc = prepare(h, false, pgrid, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
+  int rc = prepare(h, false, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
   if (rc) {
     if (tr) h->ring_next = (h->ring_next + kTimingRing - 1) % kTimingRing, --h->ring_count;
     return rc;
@@ -465,9 +459,12 @@ int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const
   h->last.producer_grid = pgrid;
   h->last.consumer_grid = 0;
   h->last.consumer_cus = 0;
-  const ProducerArgs pa = producer_args(h, lay, x, w1, w3, w2, 0u);
+  const ProducerArgs pgu = producer_args(h, lay, x, w1, w3, w2, 0u, false);
+  const ProducerArgs pa = producer_args(h, lay, x, w1, w3, w2, 0u, true);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], stream));
-  if (pa.n_items > 0) HIP_TRY(h, launch_producer(pa, pgrid, stream));
+  if (pgu.n_items > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, stream));
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], stream));
+  if (pa.n_items > 0) HIP_TRY(h, launch_producer(pa, true, pgrid, stream));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], stream));
   ScatterArgs sa{};
   sa.y = h->y;
@@ -498,7 +495,6 @@ int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
     HIP_TRY(h, hipMemcpy(&c, h->ctr, sizeof c, hipMemcpyDeviceToHost));
     h->last.poll_iters = c.poll_iters;
     h->last.wait_ticks = c.wait_ticks;
-    h->last.producer_wait_ticks = c.producer_wait_ticks;
     h->last.timeout = c.timeouts ? 1 : 0;
     h->last_timeouts = c.timeouts;
     h->last_timeout_where = c.timeout_where;
@@ -512,8 +508,7 @@ int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
     h->last.timeout = 0;
     return set_err(h, MOE_ETIMEOUT,
                    std::to_string(h->last_timeouts) + " device wait(s) hit the watchdog since the last query (" +
-                       ((h->last_timeout_where & 1) ? "consumer flag wait " : "") +
-                       ((h->last_timeout_where & 2) ? "producer dependency wait" : "") + ")");
+                       ((h->last_timeout_where & 1) ? "consumer flag wait" : "") + ")");
   }
   return MOE_OK;
 }
@@ -530,6 +525,8 @@ int moe_stage_times(moe_stage_t h, int32_t reset, moe_stage_times_t* out) {
     out->stage_ms += ms;
     HIP_TRY(h, hipEventElapsedTime(&ms, r.ev[1], r.ev[2]));
     out->producer_ms += ms;
+    HIP_TRY(h, hipEventElapsedTime(&ms, r.ev[1], r.ev[6]));
+    out->gate_up_ms += ms;
     if (r.kind == 0) {
       HIP_TRY(h, hipEventElapsedTime(&ms, r.ev[3], r.ev[4]));
       out->consumer_ms += ms;
@@ -551,12 +548,12 @@ int moe_stage_destroy(moe_stage_t h) {
   for (auto& r : h->ring)
     for (auto& ev : r.ev)
       if (ev) (void)hipEventDestroy(ev);
-  for (hipEvent_t ev : {h->stage_free[0], h->stage_free[1], h->ev_fork, h->ev_join_c, h->ev_join_p, h->ev_done})
+  for (hipEvent_t ev : {h->stage_free[0], h->stage_free[1], h->ev_fork, h->ev_gu, h->ev_join_c, h->ev_join_p,
+                        h->ev_done})
     if (ev) (void)hipEventDestroy(ev);
   if (h->s_cons) (void)hipStreamDestroy(h->s_cons);
   if (h->s_prod) (void)hipStreamDestroy(h->s_prod);
-  for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->gu_done, (void*)h->ctr,
-                  (void*)h->d_plan})
+  for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->ctr, (void*)h->d_plan})
     if (p) (void)hipFree(p);
   for (uint8_t* p : h->h_stage)
     if (p) (void)hipHostFree(p);
@@ -572,7 +569,7 @@ struct moe_plan_s {
 
 int moe_plan_build(const moe_stage_config_t* cfg, int64_t rows, const int32_t* off,
                    const int32_t* src, const int32_t* slot, const int64_t* return_rows,
-                   int32_t producer_grid, int32_t overlapped, moe_plan_t* out) {
+                   int32_t overlapped, moe_plan_t* out) {
   if (!out) return MOE_EINVAL;
   *out = nullptr;
   int rc = check_config(cfg);
@@ -584,8 +581,7 @@ int moe_plan_build(const moe_stage_config_t* cfg, int64_t rows, const int32_t* o
     return set_err(nullptr, MOE_EROUTING, "expert_offsets[E_l] must equal rows");
   auto* p = new moe_plan_s();
   std::string msg;
-  rc = build_plan(params_of(c, overlapped != 0, std::max(producer_grid, 1)), rows, off, src, slot,
-                  return_rows, &p->plan, &msg);
+  rc = build_plan(params_of(c, overlapped != 0), rows, off, src, slot, return_rows, &p->plan, &msg);
   if (rc) {
     delete p;
     return set_err(nullptr, rc, msg);

@@ -1,12 +1,12 @@
 // kernels.hip -- gfx950 (MI355X, CDNA4) kernels of the MoE expert stage.
 //
-//  * producer: persistent rank-wide grouped gated-FFN GEMM (paper Section
-//    3.3.1).  One work queue covers every local expert; an item is one
-//    256x256 output tile of either the fused gate/up projection (128 ffn
-//    features, both projections, SiLU-gated in the epilogue) or the down
-//    projection.  Each finished down tile of a tile row that needs a transfer
-//    publishes a ready flag with an agent-scope release (the epilogue signal
-//    of Section 3.3.1).
+//  * producer: persistent rank-wide grouped GEMMs (paper Section 3.3.1), one
+//    launch for the fused gate/up projection (an item = 256 rows x 128 ffn
+//    features, both projections, SiLU-gated in the epilogue) and one for the
+//    down projection (an item = 256 rows x 256 hidden columns).  A queue per
+//    launch covers every local expert.  Each finished down tile of a tile row
+//    that needs a transfer publishes a ready flag with an agent-scope release
+//    (the epilogue signal of Section 3.3.1).
 //  * consumer: persistent kernel on its own compute units (Section 3.3.3)
 //    that polls the flags of whole segments (Section 3.3.2) and copies each
 //    ready segment into its destination receive buffer.
@@ -29,213 +29,271 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Operand tile in LDS: 256 rows x 64 k (bf16) = 32 KiB, 128 bytes per row.  The
-// 16-byte chunk index is XOR-swizzled with the row so that the 32 rows read by
-// one MFMA operand load spread over all banks (conflict-free for 8-lane and
-// 16-lane bank phases alike).
-constexpr int kRowBytes = kTileK * 2;
-constexpr int kOperandBytes = kTileM * kRowBytes;   // 32 KiB
-constexpr int kStageBytes = 2 * kOperandBytes;      // weight tile + token tile
-constexpr int kLdsBytes = 2 * kStageBytes;          // double buffered: 128 KiB
+// Operand tiles in LDS: 256 rows x 32 k (bf16) = 16 KiB per operand, 64 bytes per row,
+// weight tile then token tile per stage, four stages in a ring (128 KiB).  Global
+// memory is copied straight into LDS with global_load_lds_dwordx4 (no register
+// staging), three K-steps ahead of the MFMAs.  A DMA instruction writes 64 lanes x 16
+// bytes contiguously, i.e. 16 rows, so each lane fetches the 16-byte chunk that
+// belongs at its slot: chunk c of row r sits at physical chunk c ^ g(r).  g spreads the
+// 32 rows that one MFMA operand read touches over all banks, for 8-lane (32-bank) and
+// 16-lane (64-bank) phases alike.
+constexpr int kRowBytes = kTileK * 2;                  // 64
+constexpr int kOperandBytes = kTileM * kRowBytes;      // 16 KiB
+constexpr int kStageBytes = 2 * kOperandBytes;         // 32 KiB
+constexpr int kStages = 4;
+constexpr int kLdsBytes = kStages * kStageBytes;       // 128 KiB (operand ring)
+constexpr int kRowsPerDma = 64 * 16 / kRowBytes;       // 16 rows per DMA instruction
+// Epilogue staging: the finished tile goes through LDS (free once the pipeline drains) so
+// that global stores are whole 16-byte chunks of contiguous rows.  Rows are padded by 16
+// bytes so the 32 lanes writing one column of 32 rows hit distinct banks.
+constexpr int kDownOutStride = kDownTileN * 2 + 16;    // 528 B per staged output row
+constexpr int kGuOutStride = kGuTileF * 2 + 16;        // 272 B per staged activation row
+constexpr int kLdsAlloc = kTileM * kDownOutStride;     // 135168 B >= the 128 KiB operand ring
+constexpr int kDmaPerThread = kTileM / kRowsPerDma / 4;  // 4 per operand per thread
 
-__device__ __forceinline__ uint32_t swz(uint32_t row) { return (row & 7u) ^ ((row >> 3) & 1u); }
+__device__ __forceinline__ uint32_t swz(uint32_t row) { return ((row >> 1) ^ (row >> 3)) & 3u; }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  __bf16 a = (__bf16)lo, b = (__bf16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
 
 __device__ __forceinline__ uint64_t ticks() { return wall_clock64(); }
 
+#define LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)LDS_PTR(p);
+}
+
+// 16 bytes per lane from global memory (scalar base + 32-bit lane offset) straight into
+// LDS at M0 + 16 * lane.  Issued as inline assembly so that the compiler's wait-count
+// pass does not serialise LDS reads behind every in-flight DMA: the pipeline waits for
+// exactly the stage it needs with an explicit vmcnt.  M0 is written right before the
+// load and is not used by any compiler-generated code in the producer.
+__device__ __forceinline__ void dma16(const uint8_t* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(sbase)
+               : "memory");
+}
+
+// Waits until at most n of this wave's global loads are outstanding and all LDS reads have
+// returned, then joins the workgroup barrier.  The empty asm statements keep the compiler
+// from moving memory operations across the barrier; no fence is emitted, so in-flight
+// LDS-DMA loads of later stages stay in flight.
+template <int n>
+__device__ __forceinline__ void wait_vm_and_barrier() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  // gfx9 s_waitcnt: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14, expcnt 6:4, lgkmcnt 11:8.
+  constexpr int imm = (n & 15) | ((n >> 4) << 14) | (7 << 4) | (0 << 8);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(imm);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // ---------------------------------------------------------------------------
 // One 256x256 output tile: acc[i][j] holds D[n][m] for the wave's 128x128
 // quadrant, n = wn*128 + i*32 + 8*(r/4) + 4*(lane/32) + r%4, m = wm*128 + j*32 + lane%32.
-// wp[i] / xp[i] point at row (tid/8 + 32 i) of the weight / token operand, already
-// offset by this thread's 16-byte chunk (tid%8).
+// wbase / xbase are wave-uniform byte bases of the weight / token operand; woff[i] /
+// xoff[i] are this lane's byte offsets of the row it fetches for DMA instruction i
+// (operand-tile row (wave*4 + i)*16 + lane/4), including its swizzled 16-byte chunk.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const uint16_t* const (&wp)[8],
-                                         const uint16_t* const (&xp)[8], int K, f32x16 (&acc)[4][4]) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+__device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const uint8_t* wbase, const uint8_t* xbase,
+                                         const uint32_t (&woff)[kDmaPerThread],
+                                         const uint32_t (&xoff)[kDmaPerThread], int K, f32x16 (&acc)[4][4]) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave & 1, wm = wave >> 1;
-  const int r0 = tid >> 3, c = tid & 7;
-  const uint32_t st_off = (uint32_t)r0 * kRowBytes + ((c ^ swz(r0)) << 4);
   const int lr = lane & 31, lk = lane >> 5;
   const uint32_t lsw = swz(lr);
   const uint32_t a_row = (uint32_t)(wn * 128 + lr) * kRowBytes;
   const uint32_t b_row = (uint32_t)(wm * 128 + lr) * kRowBytes;
+  const uint32_t dma_off = (uint32_t)wave * kDmaPerThread * 1024;
 
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
 
-  u32x4 rw[8], rx[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    rw[i] = *(const u32x4*)(wp[i]);
-    rx[i] = *(const u32x4*)(xp[i]);
-  }
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    *(u32x4*)(lds + st_off + i * 4096) = rw[i];
-    *(u32x4*)(lds + kOperandBytes + st_off + i * 4096) = rx[i];
-  }
-  __syncthreads();
-
   const int nk = K / kTileK;
+  const uint32_t lds0 = lds_addr(lds) + dma_off;
+  auto issue = [&](int ks) {
+    const uint32_t st = lds0 + (uint32_t)(ks & (kStages - 1)) * kStageBytes;
+    const uint8_t* wb = wbase + ks * kRowBytes;  // wave-uniform: scalar base + 32-bit lane offset
+    const uint8_t* xb = xbase + ks * kRowBytes;
+#pragma unroll
+    for (int i = 0; i < kDmaPerThread; ++i) dma16(wb, woff[i], st + i * 1024);
+#pragma unroll
+    for (int i = 0; i < kDmaPerThread; ++i) dma16(xb, xoff[i], st + kOperandBytes + i * 1024);
+  };
+  issue(0);
+  if (nk > 1) issue(1);
+  if (nk > 2) issue(2);
+
+  constexpr int per_stage = 2 * kDmaPerThread;
   for (int ks = 0; ks < nk; ++ks) {
-    uint8_t* cur = lds + (ks & 1) * kStageBytes;
-    uint8_t* nxt = lds + ((ks + 1) & 1) * kStageBytes;
-    const bool more = ks + 1 < nk;
-    if (more) {
-      const int koff = (ks + 1) * kTileK;
+    // Stage ks has landed once only the stages issued after it are outstanding.
+    if (ks + 2 < nk)
+      wait_vm_and_barrier<2 * per_stage>();
+    else if (ks + 1 < nk)
+      wait_vm_and_barrier<per_stage>();
+    else
+      wait_vm_and_barrier<0>();
+    // Every wave finished reading the slot of stage ks - 1 before the barrier: refill it.
+    if (ks + 3 < nk) issue(ks + 3);
+    const uint8_t* cur = lds + (ks & (kStages - 1)) * kStageBytes;
+    // Read every fragment of the stage up front (16 x 16 B per lane) so that only the
+    // first read's latency is exposed; the MFMAs then consume them in issue order.
+    constexpr int kSub = kTileK / 16;
+    bf16x8 a[kSub][4], b[kSub][4];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        rw[i] = *(const u32x4*)(wp[i] + koff);
-        rx[i] = *(const u32x4*)(xp[i] + koff);
-      }
-    }
-#pragma unroll
-    for (int kk = 0; kk < kTileK / 16; ++kk) {
+    for (int kk = 0; kk < kSub; ++kk) {
       const uint32_t coff = ((uint32_t)(2 * kk + lk) ^ lsw) << 4;
-      bf16x8 a[4], b[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(cur + a_row + i * 32 * kRowBytes + coff);
+      for (int i = 0; i < 4; ++i) a[kk][i] = *(const bf16x8*)(cur + a_row + i * 32 * kRowBytes + coff);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        b[j] = *(const bf16x8*)(cur + kOperandBytes + b_row + j * 32 * kRowBytes + coff);
+        b[kk][j] = *(const bf16x8*)(cur + kOperandBytes + b_row + j * 32 * kRowBytes + coff);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep all reads ahead of the MFMAs
+#pragma unroll
+    for (int kk = 0; kk < kSub; ++kk)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    if (more) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        *(u32x4*)(nxt + st_off + i * 4096) = rw[i];
-        *(u32x4*)(nxt + kOperandBytes + st_off + i * 4096) = rx[i];
-      }
-    }
-    __syncthreads();
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk][i], b[kk][j], acc[i][j], 0, 0, 0);
   }
+  // All waves are done reading LDS before the next tile's prologue overwrites it.
+  wait_vm_and_barrier<0>();
 }
 
-__device__ void producer_item(const ProducerArgs& a, uint32_t item, uint8_t* lds, uint64_t& wait_acc) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// One work item; `down` selects a down-projection tile (otherwise a fused gate/up tile).
+// Each kind is its own instantiation so the register allocator sees one straight path.
+template <bool down>
+__device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t item, uint8_t* lds) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave: keeps bases scalar
   const int wn = wave & 1, wm = wave >> 1;
   const int lr = lane & 31, lk = lane >> 5;
-  const bool down = (item & kItemDown) != 0;
   const int t = (int)((item >> kItemRowShift) & (uint32_t)(kMaxTileRows - 1));
   const int col = (int)(item & kItemColMask);
   const TileRow tr = a.tile_rows[t];
   const int64_t H = a.H, F = a.F;
   const int e = tr.expert, lrow0 = tr.lrow0;
-  const int r0 = tid >> 3, c = tid & 7;
-
-  const uint16_t* wp[8];
-  const uint16_t* xp[8];
+  // Operand rows this lane fetches: row n_i = (wave*4 + i)*16 + lane/4 of each 256-row tile.
+  // Tensors stay below 4 GiB per expert/operand, so per-lane offsets fit in 32 bits and the
+  // bases are wave-uniform (scalar registers).
+  const uint8_t* wbase;
+  const uint8_t* xbase;
+  uint32_t woff[kDmaPerThread], xoff[kDmaPerThread];
+  const uint32_t lrow4 = (uint32_t)lane >> 2;
+  if constexpr (!down) {
+    // Waves 0 and 2 fetch gate rows (W1), waves 1 and 3 the matching up rows (W3): tile rows
+    // 0..63 / 128..191 are gate features, 64..127 / 192..255 the same features' up rows, so
+    // each wave's MFMA quadrant holds gate and up of the same 64 features.
+    wbase = (const uint8_t*)((wave & 1) ? a.w3 : a.w1) + (uint64_t)e * F * H * 2;
+    xbase = (const uint8_t*)a.x;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int n = r0 + 32 * i;  // row of the weight operand tile
-    if (!down) {
-      // Rows 0..63 / 128..191 hold gate features, 64..127 / 192..255 the matching up
-      // features, so each wave's quadrant holds gate and up of the same 64 features.
-      const int half = n >> 7, w = n & 127;
-      const int f = min(col * kGuTileF + half * 64 + (w & 63), (int)F - 1);
-      wp[i] = (w < 64 ? a.w1 : a.w3) + ((int64_t)e * F + f) * H + c * 8;
-      xp[i] = a.x + (int64_t)a.row_x[lrow0 + n] * H + c * 8;
-    } else {
-      const int hcol = min(col * kDownTileN + n, (int)H - 1);
-      wp[i] = a.w2 + ((int64_t)e * H + hcol) * F + c * 8;
-      xp[i] = a.hws + (int64_t)(lrow0 + n) * F + c * 8;
+    for (int i = 0; i < kDmaPerThread; ++i) {
+      const uint32_t n = (uint32_t)(wave * kDmaPerThread + i) * kRowsPerDma + lrow4;
+      const uint32_t ch = ((uint32_t)(lane & 3) ^ swz(n)) * 16;
+      const int f = min(col * kGuTileF + (wave >> 1) * 64 + i * kRowsPerDma + (int)lrow4, (int)F - 1);
+      woff[i] = (uint32_t)f * (uint32_t)H * 2 + ch;
+      xoff[i] = (uint32_t)a.row_x[lrow0 + n] * (uint32_t)H * 2 + ch;
     }
-  }
-
-  if (down) {
-    // Every gate/up tile of this tile row must have published its activation.
-    __shared__ uint32_t s_timeout;
-    if (tid == 0) {
-      s_timeout = 0;
-      const uint64_t t0 = ticks();
-      while (__hip_atomic_load(&a.gu_done[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
-             (uint32_t)a.gu_per_row) {
-        if (ticks() - t0 > a.watchdog_ticks) {
-          s_timeout = 1;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(2);
-      }
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      wait_acc += ticks() - t0;
-    }
-    __syncthreads();
-    if (s_timeout) {
-      if (tid == 0) {
-        __hip_atomic_fetch_add(&a.ctr->timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_fetch_or(&a.ctr->timeout_where, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-      return;
+  } else {
+    wbase = (const uint8_t*)a.w2 + (uint64_t)e * H * F * 2;
+    xbase = (const uint8_t*)a.hws + (uint64_t)lrow0 * F * 2;
+#pragma unroll
+    for (int i = 0; i < kDmaPerThread; ++i) {
+      const uint32_t n = (uint32_t)(wave * kDmaPerThread + i) * kRowsPerDma + lrow4;
+      const uint32_t ch = ((uint32_t)(lane & 3) ^ swz(n)) * 16;
+      const int hcol = min(col * kDownTileN + (int)n, (int)H - 1);
+      woff[i] = (uint32_t)hcol * (uint32_t)F * 2 + ch;
+      xoff[i] = n * (uint32_t)F * 2 + ch;
     }
   }
 
   f32x16 acc[4][4];
-  tile_mma(lds, wp, xp, down ? (int)F : (int)H, acc);
+  tile_mma(lds, wbase, xbase, woff, xoff, down ? (int)F : (int)H, acc);
 
-  if (!down) {
-    const int f_base = col * kGuTileF + wn * 64;
+  if constexpr (!down) {
+    // Gated activation a = bf16(silu(g) * u): lane values -> LDS tile [256 rows][128 features].
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int lrow = lrow0 + wm * 128 + j * 32 + lr;
-      if (a.row_rank[lrow] < 0) continue;  // padding rows are never read back
-      uint16_t* dst = a.hws + (int64_t)lrow * F;
+      const int m = wm * 128 + j * 32 + lr;
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int f = f_base + i * 32 + 8 * q + 4 * lk;
-          if (f < F) {
-            const f32x16& g = acc[i][j];
-            const f32x16& u = acc[i + 2][j];
-            uint2 v;
-            v.x = pack_bf16x2(silu_mul(g[4 * q + 0], u[4 * q + 0]), silu_mul(g[4 * q + 1], u[4 * q + 1]));
-            v.y = pack_bf16x2(silu_mul(g[4 * q + 2], u[4 * q + 2]), silu_mul(g[4 * q + 3], u[4 * q + 3]));
-            *(uint2*)(dst + f) = v;
-          }
+          const int fl = wn * 64 + i * 32 + 8 * q + 4 * lk;
+          const f32x16& g = acc[i][j];
+          const f32x16& u = acc[i + 2][j];
+          uint2 v;
+          v.x = pack_bf16x2(silu_mul(g[4 * q + 0], u[4 * q + 0]), silu_mul(g[4 * q + 1], u[4 * q + 1]));
+          v.y = pack_bf16x2(silu_mul(g[4 * q + 2], u[4 * q + 2]), silu_mul(g[4 * q + 3], u[4 * q + 3]));
+          *(uint2*)(lds + m * kGuOutStride + fl * 2) = v;
+          // Convert block by block: without this the scheduler hoists every accumulator
+          // read ahead of the LDS writes and runs out of VGPRs.
+          __builtin_amdgcn_sched_barrier(0);
         }
     }
     __syncthreads();
-    if (tid == 0)
-      __hip_atomic_fetch_add(&a.gu_done[t], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    // 16 threads store one 256-byte activation row; 16 rows per pass.
+    const int c16 = tid & 15;
+    const int f = col * kGuTileF + c16 * 8;
+#pragma unroll 4
+    for (int p = 0; p < kTileM / 16; ++p) {
+      const int m = p * 16 + (tid >> 4);
+      const int lrow = lrow0 + m;
+      if (a.row_rank[lrow] >= 0 && f < F)  // padding rows are never read back
+        *(u32x4*)(a.hws + (int64_t)lrow * F + f) = *(const u32x4*)(lds + m * kGuOutStride + c16 * 16);
+    }
   } else {
-    const int n_base = col * kDownTileN + wn * 128;
-    const bool direct = (a.mode & kModeLocalDirect) != 0;
+    // Down-projection output: lane values -> LDS tile [256 rows][256 hidden columns].
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int lrow = lrow0 + wm * 128 + j * 32 + lr;
-      const int rank = a.row_rank[lrow];
-      if (rank < 0) continue;
-      uint16_t* dst = (direct && rank == a.self_rank)
-                          ? a.ret[rank] + (int64_t)a.row_slot[lrow] * H
-                          : a.y + (int64_t)lrow * H;
+      const int m = wm * 128 + j * 32 + lr;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int n = n_base + i * 32 + 8 * q + 4 * lk;
-          if (n < H) {
-            const f32x16& d = acc[i][j];
-            uint2 v;
-            v.x = pack_bf16x2(d[4 * q + 0], d[4 * q + 1]);
-            v.y = pack_bf16x2(d[4 * q + 2], d[4 * q + 3]);
-            *(uint2*)(dst + n) = v;
-          }
+          const int nl = wn * 128 + i * 32 + 8 * q + 4 * lk;
+          const f32x16& d = acc[i][j];
+          uint2 v;
+          v.x = pack_bf16x2(d[4 * q + 0], d[4 * q + 1]);
+          v.y = pack_bf16x2(d[4 * q + 2], d[4 * q + 3]);
+          *(uint2*)(lds + m * kDownOutStride + nl * 2) = v;
+          __builtin_amdgcn_sched_barrier(0);  // block by block (see above)
         }
     }
+    __syncthreads();
+    // 32 threads store one 512-byte output row; 8 rows per pass.  Rows returning to another
+    // rank go to the staged output Y (the consumer moves them); local rows go straight to
+    // the local receive buffer when the producer writes local rows directly.
+    const bool direct = (a.mode & kModeLocalDirect) != 0;
+    const int c16 = tid & 31;
+    const int n = col * kDownTileN + c16 * 8;
+#pragma unroll 4
+    for (int p = 0; p < kTileM / 8; ++p) {
+      const int m = p * 8 + (tid >> 5);
+      const int lrow = lrow0 + m;
+      const int rank = a.row_rank[lrow];
+      if (rank >= 0 && n < H) {
+        uint16_t* dst = (direct && rank == a.self_rank) ? a.ret[rank] + (int64_t)a.row_slot[lrow] * H
+                                                        : a.y + (int64_t)lrow * H;
+        *(u32x4*)(dst + n) = *(const u32x4*)(lds + m * kDownOutStride + c16 * 16);
+      }
+    }
+    __syncthreads();
     if ((a.mode & kModeSignal) && (tr.has_remote || !direct)) {
-      __syncthreads();
       if (tid == 0)
         __hip_atomic_store(&a.flags[t * a.down_per_row + col], a.epoch, __ATOMIC_RELEASE,
                            __HIP_MEMORY_SCOPE_AGENT);
@@ -243,24 +301,26 @@ __device__ void producer_item(const ProducerArgs& a, uint32_t item, uint8_t* lds
   }
 }
 
+// Persistent producer: every workgroup claims items from this launch's queue until it is
+// empty.  Nothing inside waits on another workgroup, so progress never depends on which
+// workgroups are resident.
+template <bool down>
 __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerArgs a) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsBytes];
+  static_assert(kLdsAlloc >= kLdsBytes, "staging must fit the LDS allocation");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsAlloc];
   __shared__ uint32_t s_next;
   const int tid = threadIdx.x;
-  uint64_t wait_acc = 0;
-  if (tid == 0) s_next = atomicAdd(&a.ctr->work_next, 1u);
+  if (tid == 0) s_next = atomicAdd(a.claim, 1u);
   __syncthreads();
   uint32_t cur = s_next;
   while (cur < (uint32_t)a.n_items) {
     __syncthreads();
-    // Claim the next item now; its index is read after this one finishes.  Items are
-    // claimed in schedule order, so a tile only ever waits on tiles claimed earlier.
-    if (tid == 0) s_next = atomicAdd(&a.ctr->work_next, 1u);
-    producer_item(a, a.items[cur], lds, wait_acc);
+    // Claim the next item now; its index is read after this one finishes.
+    if (tid == 0) s_next = atomicAdd(a.claim, 1u);
+    producer_item<down>(a, a.items[cur], lds);
     __syncthreads();
     cur = s_next;
   }
-  if (tid == 0 && wait_acc) atomicAdd((unsigned long long*)&a.ctr->producer_wait_ticks, (unsigned long long)wait_acc);
 }
 
 // ---------------------------------------------------------------------------
@@ -351,13 +411,12 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   if (i == 0) {
-    a.ctr->work_next = 0;
+    a.ctr->gu_next = 0;
+    a.ctr->down_next = 0;
     a.ctr->seg_next = 0;
     a.ctr->poll_iters = 0;
     a.ctr->wait_ticks = 0;
-    a.ctr->producer_wait_ticks = 0;
   }
-  for (int64_t j = i; j < a.n_tile_rows; j += stride) a.gu_done[j] = 0;
   if (a.poison) {
     const u32x4 nan = {0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};
     for (int64_t j = i; j < a.poison_elems / 8; j += stride) ((u32x4*)a.poison)[j] = nan;
@@ -371,8 +430,11 @@ hipError_t launch_init(const InitArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_producer(const ProducerArgs& a, int grid, hipStream_t s) {
-  hipLaunchKernelGGL(producer_kernel, dim3(grid), dim3(kProducerThreads), 0, s, a);
+hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream_t s) {
+  if (down)
+    hipLaunchKernelGGL(producer_kernel<true>, dim3(grid), dim3(kProducerThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(producer_kernel<false>, dim3(grid), dim3(kProducerThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -388,7 +450,7 @@ hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s) {
 
 int producer_blocks_per_cu() {
   int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, producer_kernel, kProducerThreads, 0) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, producer_kernel<false>, kProducerThreads, 0) != hipSuccess)
     return 1;
   return n > 0 ? n : 1;
 }

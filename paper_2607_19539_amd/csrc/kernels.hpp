@@ -19,19 +19,17 @@ struct ProducerArgs {
   uint16_t* hws;           // [n_lrows, F] gated activation (workspace)
   uint16_t* y;             // [n_lrows, H] staged output (workspace)
   const TileRow* tile_rows;
-  const uint32_t* items;
+  const uint32_t* items;   // this launch's work items (all gate/up or all down tiles)
   int32_t n_items;
+  uint32_t* claim;         // queue head of this launch
   const int32_t* row_x;    // [n_lrows]
   const int32_t* row_rank; // [n_lrows], -1 = padding
   const int32_t* row_slot; // [n_lrows]
   uint16_t* const* ret;    // [R] receive buffers (device array of device pointers)
-  RunCounters* ctr;
-  uint32_t* gu_done;       // [n_tile_rows] finished gate/up tiles per tile row
   uint32_t* flags;         // [n_tile_rows * down_per_row] ready flags (value = epoch)
   uint32_t epoch;
-  int32_t H, F, self_rank, gu_per_row, down_per_row;
+  int32_t H, F, self_rank, down_per_row;
   uint32_t mode;
-  uint64_t watchdog_ticks; // bound on a dependency wait, 100 MHz ticks
 };
 
 struct ConsumerArgs {
@@ -57,14 +55,13 @@ struct ScatterArgs {
 
 struct InitArgs {
   RunCounters* ctr;
-  uint32_t* gu_done;
-  int32_t n_tile_rows;
   uint16_t* poison;        // optional: filled with bf16 NaN
   int64_t poison_elems;    // multiple of 8
 };
 
 hipError_t launch_init(const InitArgs& a, hipStream_t s);
-hipError_t launch_producer(const ProducerArgs& a, int grid, hipStream_t s);
+// Gate/up tiles (down = false) or down-projection tiles with ready flags (down = true).
+hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream_t s);
 hipError_t launch_consumer(const ConsumerArgs& a, int grid, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s);
 // Resident producer workgroups per compute unit.

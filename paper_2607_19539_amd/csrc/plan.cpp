@@ -4,7 +4,6 @@
 #include "plan.hpp"
 
 #include <algorithm>
-#include <deque>
 #include <numeric>
 #include <string>
 
@@ -213,51 +212,29 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
   // Band groups: up to band_group consecutive tile rows of one expert (and of one class,
   // remote or local) sweep the gate/up columns together, so each weight slice is fetched
   // once per group rather than once per tile row.
-  std::vector<std::pair<int32_t, int32_t>> groups;  // [begin, end) into `order`
   const int32_t G = std::max<int32_t>(p.band_group, 1);
   for (int32_t a = 0; a < n_tr;) {
     int32_t b = a + 1;
     while (b < n_tr && b - a < G && P.tile_rows[order[b]].expert == P.tile_rows[order[a]].expert &&
            P.tile_rows[order[b]].has_remote == P.tile_rows[order[a]].has_remote)
       ++b;
-    groups.emplace_back(a, b);
+    for (int32_t j = 0; j < P.gu_per_row; ++j)
+      for (int32_t q = a; q < b; ++q) P.items.push_back(gu_item(order[q], j));
     a = b;
   }
+  P.n_gu = (int32_t)P.items.size();
 
-  // Work items.  A down tile of tile row t depends on all gate/up tiles of t, so every
-  // gate/up tile of a group precedes its down tiles; the down tiles trail by about one
-  // producer grid of gate/up tiles so their dependencies have usually finished when a
-  // workgroup picks them up.
+  // Down tiles, the signaling GEMM of Section 3.3.1, run after every gate/up tile (a separate
+  // launch on the producer stream).  They follow the remote-first order tile row by tile
+  // row, so the first segments become ready as early as possible.
   std::vector<int32_t> pos_of_down((size_t)n_tr * P.down_per_row, -1);
-  auto emit_down = [&](int32_t g) {
-    for (int32_t n = 0; n < P.down_per_row; ++n)
-      for (int32_t q = groups[g].first; q < groups[g].second; ++q) {
-        const int32_t t = order[q];
-        pos_of_down[(size_t)t * P.down_per_row + n] = (int32_t)P.items.size();
-        P.items.push_back(down_item(t, n));
-      }
-  };
-  const int64_t lag = std::max<int32_t>(p.producer_grid, 1);
-  std::deque<std::pair<int32_t, int64_t>> pending;  // (group, gate/up count at its end)
-  int64_t gu_count = 0;
-  for (int32_t g = 0; g < (int32_t)groups.size(); ++g) {
-    for (int32_t j = 0; j < P.gu_per_row; ++j)
-      for (int32_t q = groups[g].first; q < groups[g].second; ++q) {
-        P.items.push_back(gu_item(order[q], j));
-        ++gu_count;
-        while (!pending.empty() && gu_count - pending.front().second >= lag) {
-          emit_down(pending.front().first);
-          pending.pop_front();
-        }
-      }
-    pending.emplace_back(g, gu_count);
-  }
-  while (!pending.empty()) {
-    emit_down(pending.front().first);
-    pending.pop_front();
-  }
-  P.n_gu = (int32_t)gu_count;
-  P.n_down = (int32_t)(P.items.size() - gu_count);
+  for (int32_t q = 0; q < n_tr; ++q)
+    for (int32_t n = 0; n < P.down_per_row; ++n) {
+      const int32_t t = order[q];
+      pos_of_down[(size_t)t * P.down_per_row + n] = (int32_t)P.items.size();
+      P.items.push_back(down_item(t, n));
+    }
+  P.n_down = (int32_t)P.items.size() - P.n_gu;
 
   // Combine plan (Section 3.2.3) and segment composition (Section 3.3.2): per owner group,
   // the first and last segments are one band, middle segments coalesce x bands.  Rows of a

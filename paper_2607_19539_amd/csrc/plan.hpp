@@ -22,7 +22,6 @@ struct PlanParams {
   int32_t mid_bands = 1;      // x (mgb)
   bool local_direct = true;   // local rows need no transfer
   bool overlapped = true;     // false: plan of the non-overlapped baseline
-  int32_t producer_grid = 256;  // persistent producer workgroups (sets the down-tile lag)
   int32_t band_group = 8;     // tile rows that sweep the weight columns together
 };
 

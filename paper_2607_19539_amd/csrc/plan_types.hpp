@@ -15,7 +15,7 @@ namespace moe {
 constexpr int kTileM = 256;
 constexpr int kGuTileF = 128;
 constexpr int kDownTileN = 256;
-constexpr int kTileK = 64;
+constexpr int kTileK = 32;
 
 // Work-item encoding: bit 31 = down tile, bits 30..12 = tile row, bits 11..0 = column tile.
 constexpr uint32_t kItemDown = 0x80000000u;
@@ -49,15 +49,16 @@ struct Band {
   int32_t dst_rank;    // -1 for a band of padding only
 };
 
-// Device-side counters of one run, zeroed by the init kernel.
+// Device-side counters of one run; the queue heads are zeroed by the init kernel.
 struct RunCounters {
-  uint32_t work_next;       // producer work queue head
+  uint32_t gu_next;         // gate/up work queue head
   uint32_t seg_next;        // consumer segment queue head
   uint32_t timeouts;        // bounded waits that expired; NOT reset per run (cleared by a query)
   uint32_t timeout_where;   // bit 0 = consumer flag wait, bit 1 = producer dependency wait
   uint64_t poll_iters;      // consumer poll iterations
   uint64_t wait_ticks;      // consumer wait time, 100 MHz ticks
-  uint64_t producer_wait_ticks;
+  uint32_t down_next;       // down-projection work queue head
+  uint32_t pad0;
   uint64_t pad[3];
 };
 

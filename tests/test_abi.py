@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
 def test_struct_sizes_match_header_layout():
     # int32 x 9 + uint32 = 40 bytes; stats and plan-info contain int64 fields (8-byte aligned)
     assert ctypes.sizeof(B.moe_stage_config_t) == 40
-    assert ctypes.sizeof(B.moe_stage_stats_t) == 4 * 8 + 9 * 4 + 4 + 8 + 3 * 8  # 9 int32 + pad
+    assert ctypes.sizeof(B.moe_stage_stats_t) == 4 * 8 + 9 * 4 + 4 + 8 + 2 * 8  # 9 int32 + pad
     assert ctypes.sizeof(B.moe_plan_info_t) == 10 * 4 + 4 * 8
 
 
