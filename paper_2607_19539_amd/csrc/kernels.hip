@@ -21,6 +21,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace moe {
@@ -132,45 +134,66 @@ __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const uint8_
 #pragma unroll
     for (int i = 0; i < kDmaPerThread; ++i) dma16(xb, xoff[i], st + kOperandBytes + i * 1024);
   };
-  issue(0);
-  if (nk > 1) issue(1);
-  if (nk > 2) issue(2);
-
-  constexpr int per_stage = 2 * kDmaPerThread;
-  for (int ks = 0; ks < nk; ++ks) {
-    // Stage ks has landed once only the stages issued after it are outstanding.
-    if (ks + 2 < nk)
-      wait_vm_and_barrier<2 * per_stage>();
-    else if (ks + 1 < nk)
-      wait_vm_and_barrier<per_stage>();
-    else
-      wait_vm_and_barrier<0>();
-    // Every wave finished reading the slot of stage ks - 1 before the barrier: refill it.
-    if (ks + 3 < nk) issue(ks + 3);
+  // Fragments of one 16-deep K half of stage ks: 4 weight and 4 token fragments per lane.
+  auto read_half = [&](int ks, int kk, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
     const uint8_t* cur = lds + (ks & (kStages - 1)) * kStageBytes;
-    // Read every fragment of the stage up front (16 x 16 B per lane) so that only the
-    // first read's latency is exposed; the MFMAs then consume them in issue order.
-    constexpr int kSub = kTileK / 16;
-    bf16x8 a[kSub][4], b[kSub][4];
+    const uint32_t coff = ((uint32_t)(2 * kk + lk) ^ lsw) << 4;
 #pragma unroll
-    for (int kk = 0; kk < kSub; ++kk) {
-      const uint32_t coff = ((uint32_t)(2 * kk + lk) ^ lsw) << 4;
+    for (int i = 0; i < 4; ++i) fa[i] = *(const bf16x8*)(cur + a_row + i * 32 * kRowBytes + coff);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[kk][i] = *(const bf16x8*)(cur + a_row + i * 32 * kRowBytes + coff);
+    for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8*)(cur + kOperandBytes + b_row + j * 32 * kRowBytes + coff);
+  };
+  auto mma_half = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        b[kk][j] = *(const bf16x8*)(cur + kOperandBytes + b_row + j * 32 * kRowBytes + coff);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  };
+
+  // Prologue: four stages in flight, stage 0 visible, its first half read.
+#pragma unroll
+  for (int ks = 0; ks < kStages; ++ks)
+    if (ks < nk) issue(ks);
+  constexpr int per_stage = 2 * kDmaPerThread;
+  if (nk >= 4)
+    wait_vm_and_barrier<3 * per_stage>();
+  else if (nk == 3)
+    wait_vm_and_barrier<2 * per_stage>();
+  else if (nk == 2)
+    wait_vm_and_barrier<per_stage>();
+  else
+    wait_vm_and_barrier<0>();
+  bf16x8 a0[4], b0[4], a1[4], b1[4];
+  read_half(0, 0, a0, b0);
+
+  // Steady state.  Each stage: read the second half while the first half's MFMAs issue;
+  // then, with every read of this stage issued and returned, a barrier makes stage ks+1
+  // visible and frees this stage's slot for stage ks+4; the next stage's first half is read
+  // while the second half's MFMAs issue.  Reads stay one half ahead of the MFMAs and the
+  // DMA four stages ahead, so neither LDS nor global latency sits on the MFMA path.  The last
+  // three stages are peeled so each wait count is a constant on a straight path.
+  auto stage = [&](int ks, auto vm_after) {
+    read_half(ks, 1, a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_half(a0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    constexpr int vm = decltype(vm_after)::value;
+    if constexpr (vm >= 0) {
+      wait_vm_and_barrier<vm>();  // stage ks+1 has landed; slot ks % 4 is free
+      if (ks + kStages < nk) issue(ks + kStages);
+      read_half(ks + 1, 0, a0, b0);
     }
-    __builtin_amdgcn_sched_barrier(0);  // keep all reads ahead of the MFMAs
-#pragma unroll
-    for (int kk = 0; kk < kSub; ++kk)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk][i], b[kk][j], acc[i][j], 0, 0, 0);
-  }
-  // All waves are done reading LDS before the next tile's prologue overwrites it.
+    __builtin_amdgcn_sched_barrier(0);
+    mma_half(a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  int ks = 0;
+  for (; ks + 3 < nk; ++ks) stage(ks, std::integral_constant<int, 2 * per_stage>{});
+  if (ks + 2 < nk) stage(ks++, std::integral_constant<int, per_stage>{});
+  if (ks + 1 < nk) stage(ks++, std::integral_constant<int, 0>{});
+  stage(ks, std::integral_constant<int, -1>{});
+  // All waves are done reading LDS before the epilogue or the next tile reuses it.
   wait_vm_and_barrier<0>();
 }
 
