@@ -48,13 +48,18 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", default="mixtral", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cu-split", type=int, default=8, help="consumer compute units")
-    ap.add_argument("--band-rows", type=int, default=0, help="tb_M of the row layout (0 = library default)")
-    ap.add_argument("--mgb", type=int, default=1, help="bands per middle transfer segment")
-    ap.add_argument("--sweep", default="8,16,32", help="CU splits for the overlap-speedup sweep ('' = none)")
+    ap.add_argument("--band-rows", type=int, default=0, help="tb_M of the row layout (0 = 1, no alignment)")
+    ap.add_argument("--split-k", type=int, default=0, help="K parts per down tile (0 = library default)")
+    ap.add_argument("--mgb", type=int, default=1, help="tile-row pieces per middle transfer segment")
+    ap.add_argument("--mode", choices=["shared", "partitioned"], default="shared",
+                    help="shared: the producer keeps every CU and the consumer runs beside it on its "
+                         "cu_split CUs; partitioned: the consumer's CUs are reserved for it")
+    ap.add_argument("--sweep", default="4,8,16,32",
+                    help="CU splits for the overlap-speedup sweep, both modes ('' = none)")
     ap.add_argument("--only", choices=["all", "serial", "overlapped"], default="all",
                     help="run only one path (counter collection serialises kernels, so use 'serial' there)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -110,16 +115,22 @@ def main():
     bufs = [torch.zeros((int(n), wl.H), dtype=torch.int16, device="cuda") for n in wl.return_rows]
     run_args = (x, wl.expert_offsets, wl.row_src_rank, wl.row_slot, w1, w3, w2, bufs, wl.return_rows)
     flops = wl.flops()
-    stage = B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, args.mgb,
-                       B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING)
-    stream = torch.cuda.current_stream()
+    base_flags = B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING
+    stages = {m: B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, args.mgb,
+                            base_flags | (B.MOE_SHARED_CUS if m == "shared" else 0), 0, args.split_k)
+              for m in ("shared", "partitioned")}
+    stage = stages[args.mode]
+    # The stage runs on a stream of its own, as in a serving loop (the legacy null stream would
+    # force the shared-CU producer onto a second queue; see moe_stage_run).
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
     timeouts = []
 
-    def timed(fn, steps, warmup):
+    def timed(stg, fn, steps, warmup):
         for _ in range(warmup):
             fn()
-        stage.query()
-        stage.times(reset=True)
+        stg.query(check=False)
+        stg.times(reset=True)
         torch.cuda.synchronize()
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         start.record(stream)
@@ -128,11 +139,11 @@ def main():
         end.record(stream)
         torch.cuda.synchronize()
         ms = start.elapsed_time(end) / steps
-        st = stage.query(check=False)
+        st = stg.query(check=False)
         if st["rc"] != 0:
-            log(f"ERROR: {B.moe_stage_last_error(stage.h)} -- timing invalid")
-            timeouts.append(B.moe_stage_last_error(stage.h))
-        tm = stage.times(reset=True)
+            log(f"ERROR: {B.moe_stage_last_error(stg.h)} -- timing invalid")
+            timeouts.append(B.moe_stage_last_error(stg.h))
+        tm = stg.times(reset=True)
         return ms, st, tm
 
     out = {"metric": METRIC, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -141,15 +152,16 @@ def main():
     res = {}
     if args.only in ("all", "serial"):
         log("timing serial baseline")
-        ms_s, st_s, tm_s = timed(lambda: stage.run_serial(*run_args, stream=stream), args.steps, args.warmup)
+        ms_s, st_s, tm_s = timed(stage, lambda: stage.run_serial(*run_args, stream=stream), args.steps,
+                                 args.warmup)
         res["serial"] = dict(ms=ms_s, producer_ms=tm_s["producer_ms"] / tm_s["runs"],
                              gate_up_ms=tm_s["gate_up_ms"] / tm_s["runs"],
                              scatter_ms=tm_s["scatter_ms"] / tm_s["runs"], stats=st_s)
         log(f"serial: {ms_s * 1e3:.1f} us/step, producer {res['serial']['producer_ms'] * 1e3:.1f} us "
             f"(gate/up {res['serial']['gate_up_ms'] * 1e3:.1f} us), scatter {res['serial']['scatter_ms'] * 1e3:.1f} us")
     if args.only in ("all", "overlapped"):
-        log(f"timing overlapped stage, cu_split={args.cu_split}")
-        ms_o, st_o, tm_o = timed(lambda: stage.run(*run_args, cu_split=args.cu_split, stream=stream),
+        log(f"timing overlapped stage, {args.mode} CUs, cu_split={args.cu_split}")
+        ms_o, st_o, tm_o = timed(stage, lambda: stage.run(*run_args, cu_split=args.cu_split, stream=stream),
                                  args.steps, args.warmup)
         res["overlapped"] = dict(ms=ms_o, producer_ms=tm_o["producer_ms"] / tm_o["runs"],
                                  gate_up_ms=tm_o["gate_up_ms"] / tm_o["runs"],
@@ -171,7 +183,9 @@ def main():
     st = r["stats"]
     out["config"] = {"workload": DESCRIPTIONS[args.workload], "routed_rows": wl.rows, "path": main_path,
                      "cu_split": args.cu_split, "consumer_cus": st.get("consumer_cus", 0),
-                     "band_rows": stage.cfg.band_rows or "default", "mid_segment_bands": args.mgb,
+                     "cu_mode": args.mode,
+                     "band_rows": stage.cfg.band_rows or 1, "mid_segment_pieces": args.mgb,
+                     "down_split_k": st.get("split_k", 0),
                      "padding_rows": int(st["n_logical_rows"] - st["n_valid"]),
                      "band_padding_rows": int(st["n_band_padding"]), "plan_us": round(st["plan_us"], 1),
                      "seed": args.seed}
@@ -195,19 +209,15 @@ def main():
     if args.sweep and "serial" in res and args.only == "all":
         sweep = []
         for c in [int(v) for v in args.sweep.split(",") if v]:
-            for mgb in (1, 2):
-                s2 = B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, mgb,
-                                B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING)
-                old, stage = stage, s2
-                ms_c, st_c, _ = timed(lambda: stage.run(*run_args, cu_split=c, stream=stream),
+            for mode, stg in stages.items():
+                ms_c, st_c, _ = timed(stg, lambda: stg.run(*run_args, cu_split=c, stream=stream),
                                       max(args.steps // 2, 5), max(args.warmup // 2, 2))
-                stage = old
-                s2.close()
-                sweep.append({"cu_split": c, "consumer_cus": st_c["consumer_cus"], "mgb": mgb,
+                sweep.append({"cu_split": c, "cu_mode": mode, "consumer_cus": st_c["consumer_cus"],
                               "stage_us": ms_c * 1e3, "speedup_vs_serial": res["serial"]["ms"] / ms_c})
-                log(f"sweep c={c} mgb={mgb}: {ms_c * 1e3:.1f} us, speedup {res['serial']['ms'] / ms_c:.3f}")
+                log(f"sweep c={c} {mode}: {ms_c * 1e3:.1f} us, speedup {res['serial']['ms'] / ms_c:.3f}")
         out["cu_split_sweep"] = sweep
-    stage.close()
+    for stg in stages.values():
+        stg.close()
     out["watchdog_timeouts"] = timeouts
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")

@@ -55,7 +55,8 @@ extern "C" {
 #define MOE_ECAPACITY (-3)    /* rows > max_rows, or the plan exceeds the handle's workspaces   */
 #define MOE_EHIP (-4)         /* a HIP runtime call failed (message names it)                  */
 #define MOE_ETIMEOUT (-5)     /* a bounded device wait expired; sticky until the next query   */
-#define MOE_EUNSUPPORTED (-6) /* hidden/ffn not multiples of 64, cu_split out of range         */
+#define MOE_EUNSUPPORTED (-6) /* hidden/ffn not multiples of 64, hidden > 65536, cu_split out
+                                 of range                                                      */
 
 /* Config flags */
 #define MOE_LOCAL_DIRECT (1u << 0) /* overlapped run: rows whose source is self_rank are written
@@ -67,6 +68,11 @@ extern "C" {
 #define MOE_TEST_NO_SIGNAL (1u << 3) /* testing aid: the producer raises no ready flags, so every
                                        consumer wait runs into watchdog_ms and the run reports
                                        MOE_ETIMEOUT; the kernels still exit normally            */
+#define MOE_SHARED_CUS (1u << 4)   /* overlapped run: the producer keeps every compute unit and
+                                      the consumer, still confined to its cu_split units, runs
+                                      beside producer workgroups there (a consumer workgroup's
+                                      registers and LDS fit next to a producer workgroup's), so
+                                      the partition costs the producer issue slots, not CUs    */
 
 typedef struct moe_stage_s* moe_stage_t;
 
@@ -80,12 +86,21 @@ typedef struct {
   int32_t band_rows;         /* tb_M of the remote-owner-aligned layout (Section 3.2.1): each
                                 remote owner group is padded to a multiple of it, so every
                                 band of band_rows rows has one destination.  Power of two in
-                                [1, 256]; 0 picks a default.                                  */
-  int32_t mid_segment_bands; /* x of Section 3.3.2 (mgb in the evaluation): bands per middle
-                                transfer segment; first and last segments of a group are one
-                                band.  >= 1; 0 means 1.                                       */
+                                [1, 256]; 0 means 1, the default: readiness is tracked per
+                                256-row tile row, so alignment would only add padding rows. */
+  int32_t mid_segment_pieces; /* x of Section 3.3.2 (mgb in the evaluation): an owner group is
+                                cut at 256-row tile-row boundaries into pieces; its first and
+                                last pieces are one transfer segment each and middle segments
+                                coalesce x pieces.  >= 1; 0 means 1.                         */
   uint32_t flags;            /* MOE_* flags above                                            */
   int32_t watchdog_ms;       /* bound on every device spin-wait; 0 = 2000 ms                  */
+  int32_t down_split_k;      /* K parts per down-projection tile, 1..16 and <= ffn / 32: each
+                                part accumulates one contiguous K range in fp32 and the part
+                                that finishes last adds the parts in part order and writes the
+                                tile.  Fixed per handle, so results do not depend on the
+                                schedule or the path.  0 picks a default from ffn (long
+                                down-projection tiles are split so their last round fills the
+                                GPU).                                                         */
 } moe_stage_config_t;
 
 /* Statistics of the most recent run (moe_stage_query). */
@@ -95,19 +110,27 @@ typedef struct {
   int64_t n_band_padding;   /* zero rows inserted at owner-group boundaries (Section 4.5)    */
   int64_t n_remote_rows;    /* rows whose source rank is not self_rank                      */
   int32_t n_tile_rows;      /* 256-row GEMM tile rows                                        */
-  int32_t n_bands;
+  int32_t n_groups;         /* owner groups: (local expert, source rank) row groups          */
   int32_t n_gu_items;       /* gate/up tiles                                                */
-  int32_t n_down_items;     /* down-projection tiles (each raises one ready flag)           */
+  int32_t n_down_items;     /* down-projection work items: tiles x split_k parts (each tile
+                               raises one ready flag when its last part is done)             */
   int32_t n_segments;       /* transfer segments issued by the consumer                      */
   int32_t producer_grid;    /* persistent producer workgroups launched                      */
   int32_t consumer_grid;    /* persistent consumer workgroups launched                      */
-  int32_t consumer_cus;     /* compute units reserved for the consumer (cu_split rounded up
-                               to a multiple of the XCD count; 0 for serial runs)            */
+  int32_t consumer_cus;     /* compute units the consumer is confined to (cu_split rounded up
+                               to a multiple of the XCD count; 0 for serial runs); with
+                               MOE_SHARED_CUS the producer runs on them too                  */
   int32_t timeout;          /* 1 if a device wait hit the watchdog in any run since the last
                                query (sticky across runs)                                    */
   double plan_us;           /* host time to validate and build the plan                      */
   uint64_t poll_iters;      /* consumer flag-poll iterations summed over segments            */
   uint64_t wait_ticks;      /* consumer time spent waiting for flags (100 MHz ticks)         */
+  int32_t gu_workgroups;    /* producer workgroups that claimed at least one tile in the last
+                               run's gate/up launch (fewer than producer_grid means some
+                               were not resident while the queue still held work)            */
+  int32_t down_workgroups;  /* the same for the down-projection launch                       */
+  int32_t split_k;          /* K parts per down-projection tile in effect                    */
+  int32_t reserved;
 } moe_stage_stats_t;
 
 /* Accumulated kernel times (MOE_KERNEL_TIMING), milliseconds, over runs since the last reset. */
@@ -129,15 +152,19 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out);
  * 1) on the host, then runs the persistent rank-wide producer (a gate/up launch,
  * then the down-projection launch) on all but `cu_split` compute units and a
  * persistent consumer on the others.  The down launch raises a ready flag per
- * finished tile; the consumer, released when the gate/up launch completes,
+ * finished tile; the consumer, released once the run's queues are reset,
  * copies each ready segment into return_bufs[destination].  The
  * work is ordered after prior work on `stream` (a hipStream_t; NULL = null
- * stream) and later work on `stream` sees the results.
+ * stream) and later work on `stream` sees the results.  The consumer runs on a
+ * CU-masked stream of the handle; the producer runs on another one, or directly
+ * on `stream` under MOE_SHARED_CUS when `stream` is not the legacy null stream
+ * (whose launches would wait for the polling consumer).
  *
  * cu_split: compute units for the consumer, 1 <= cu_split <= CUs - XCDs.  Workgroups
  * are dealt round-robin over the XCDs (8 on MI355X) and a CU-masked queue must own
  * CUs on each of them, so the split is rounded up to a multiple of the XCD count
- * (the stats report the effective value); the producer gets every other CU.
+ * (the stats report the effective value); the producer gets every other CU, or every
+ * CU under MOE_SHARED_CUS.
  */
 int moe_stage_run(moe_stage_t h, const void* dispatched_x, const int32_t* expert_offsets,
                   const int32_t* row_src_rank, const int32_t* row_slot, const void* w1,
@@ -175,24 +202,29 @@ int moe_stage_destroy(moe_stage_t h);
 typedef struct moe_plan_s* moe_plan_t;
 
 typedef struct {
-  int32_t n_tile_rows, n_items, n_gu_items, n_down_items, n_segments, n_bands;
+  int32_t n_tile_rows, n_items, n_gu_items, n_down_items, n_segments, n_groups;
   int32_t gu_tiles_per_row;   /* gate/up tiles per tile row (ffn / 128, rounded up)          */
   int32_t down_tiles_per_row; /* down tiles per tile row (hidden / 256, rounded up)          */
   int32_t tile_m, band_rows;
+  int32_t split_k;            /* K parts per down tile                                        */
+  int32_t reserved;
   int64_t n_logical_rows, n_valid, n_band_padding, n_remote_rows;
 } moe_plan_info_t;
 
 /* Tables readable with moe_plan_copy:
  *   MOE_PLAN_TILE_ROWS  int32 [n_tile_rows][4]: expert, first logical row, valid rows, has_remote
- *   MOE_PLAN_ITEMS      uint32 [n_items]: bit 31 = down tile, bits 30..12 tile row, 11..0 column
- *                       tile; all gate/up tiles (first launch) precede all down tiles
+ *   MOE_PLAN_ITEMS      uint32 [n_items]: bit 31 = down tile, bits 30..12 tile row; gate/up
+ *                       items: bits 11..0 column tile; down items: bits 11..4 column tile,
+ *                       bits 3..0 K part (the parts of a tile are adjacent, in part order);
+ *                       all gate/up tiles (first launch) precede all down items
  *   MOE_PLAN_ROW_X      int32 [n_logical_rows]: dispatched_x row feeding each logical row
  *                       (padding rows repeat a valid row of the same expert)
  *   MOE_PLAN_ROW_RANK   int32 [n_logical_rows]: source rank, -1 for padding
  *   MOE_PLAN_ROW_SLOT   int32 [n_logical_rows]: receive slot, -1 for padding
  *   MOE_PLAN_SEGMENTS   int32 [n_segments][8]: dst rank, rows, first logical row, first slot,
- *                       first flag, flag count, last schedule position it waits for, band count
- *   MOE_PLAN_BANDS      int32 [n_bands][4]: expert, first logical row, valid rows, dst rank (-1 pad)
+ *                       first flag, flag count, last schedule position it waits for, tile-row
+ *                       pieces of its group it covers
+ *   MOE_PLAN_GROUPS     int32 [n_groups][4]: expert, first logical row, rows, source rank
  */
 #define MOE_PLAN_TILE_ROWS 0
 #define MOE_PLAN_ITEMS 1
@@ -200,7 +232,7 @@ typedef struct {
 #define MOE_PLAN_ROW_RANK 3
 #define MOE_PLAN_ROW_SLOT 4
 #define MOE_PLAN_SEGMENTS 5
-#define MOE_PLAN_BANDS 6
+#define MOE_PLAN_GROUPS 6
 
 /* `overlapped` selects the plan of moe_stage_run (1) or moe_stage_run_serial (0). */
 int moe_plan_build(const moe_stage_config_t* cfg, int64_t rows, const int32_t* expert_offsets,

@@ -18,8 +18,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "_lib", "libmoe_stage.so")
 
 MOE_OK, MOE_EINVAL, MOE_EROUTING, MOE_ECAPACITY, MOE_EHIP, MOE_ETIMEOUT, MOE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
-MOE_LOCAL_DIRECT, MOE_KERNEL_TIMING, MOE_POISON, MOE_TEST_NO_SIGNAL = 1, 2, 4, 8
-MOE_PLAN_TILE_ROWS, MOE_PLAN_ITEMS, MOE_PLAN_ROW_X, MOE_PLAN_ROW_RANK, MOE_PLAN_ROW_SLOT, MOE_PLAN_SEGMENTS, MOE_PLAN_BANDS = range(7)
+MOE_LOCAL_DIRECT, MOE_KERNEL_TIMING, MOE_POISON, MOE_TEST_NO_SIGNAL, MOE_SHARED_CUS = 1, 2, 4, 8, 16
+MOE_PLAN_TILE_ROWS, MOE_PLAN_ITEMS, MOE_PLAN_ROW_X, MOE_PLAN_ROW_RANK, MOE_PLAN_ROW_SLOT, MOE_PLAN_SEGMENTS, MOE_PLAN_GROUPS = range(7)
 ERROR_NAMES = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EROUTING", -3: "MOE_ECAPACITY", -4: "MOE_EHIP",
                -5: "MOE_ETIMEOUT", -6: "MOE_EUNSUPPORTED"}
 
@@ -31,17 +31,19 @@ EXPORTED = ["moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_st
 class moe_stage_config_t(ctypes.Structure):
     _fields_ = [("hidden", ctypes.c_int32), ("ffn", ctypes.c_int32), ("num_local_experts", ctypes.c_int32),
                 ("num_ranks", ctypes.c_int32), ("self_rank", ctypes.c_int32), ("max_rows", ctypes.c_int32),
-                ("band_rows", ctypes.c_int32), ("mid_segment_bands", ctypes.c_int32), ("flags", ctypes.c_uint32),
-                ("watchdog_ms", ctypes.c_int32)]
+                ("band_rows", ctypes.c_int32), ("mid_segment_pieces", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("watchdog_ms", ctypes.c_int32), ("down_split_k", ctypes.c_int32)]
 
 
 class moe_stage_stats_t(ctypes.Structure):
     _fields_ = [("n_valid", ctypes.c_int64), ("n_logical_rows", ctypes.c_int64), ("n_band_padding", ctypes.c_int64),
-                ("n_remote_rows", ctypes.c_int64), ("n_tile_rows", ctypes.c_int32), ("n_bands", ctypes.c_int32),
+                ("n_remote_rows", ctypes.c_int64), ("n_tile_rows", ctypes.c_int32), ("n_groups", ctypes.c_int32),
                 ("n_gu_items", ctypes.c_int32), ("n_down_items", ctypes.c_int32), ("n_segments", ctypes.c_int32),
                 ("producer_grid", ctypes.c_int32), ("consumer_grid", ctypes.c_int32), ("consumer_cus", ctypes.c_int32),
                 ("timeout", ctypes.c_int32),
-                ("plan_us", ctypes.c_double), ("poll_iters", ctypes.c_uint64), ("wait_ticks", ctypes.c_uint64)]
+                ("plan_us", ctypes.c_double), ("poll_iters", ctypes.c_uint64), ("wait_ticks", ctypes.c_uint64),
+                ("gu_workgroups", ctypes.c_int32), ("down_workgroups", ctypes.c_int32),
+                ("split_k", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class moe_stage_times_t(ctypes.Structure):
@@ -51,9 +53,10 @@ class moe_stage_times_t(ctypes.Structure):
 
 class moe_plan_info_t(ctypes.Structure):
     _fields_ = [("n_tile_rows", ctypes.c_int32), ("n_items", ctypes.c_int32), ("n_gu_items", ctypes.c_int32),
-                ("n_down_items", ctypes.c_int32), ("n_segments", ctypes.c_int32), ("n_bands", ctypes.c_int32),
+                ("n_down_items", ctypes.c_int32), ("n_segments", ctypes.c_int32), ("n_groups", ctypes.c_int32),
                 ("gu_tiles_per_row", ctypes.c_int32), ("down_tiles_per_row", ctypes.c_int32),
-                ("tile_m", ctypes.c_int32), ("band_rows", ctypes.c_int32), ("n_logical_rows", ctypes.c_int64),
+                ("tile_m", ctypes.c_int32), ("band_rows", ctypes.c_int32), ("split_k", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("n_logical_rows", ctypes.c_int64),
                 ("n_valid", ctypes.c_int64), ("n_band_padding", ctypes.c_int64), ("n_remote_rows", ctypes.c_int64)]
 
 
@@ -131,9 +134,9 @@ def _dev_ptr(t) -> int:
 # ----------------------------------------------------------------------------- C-named functions
 
 def make_config(hidden, ffn, num_local_experts, num_ranks, self_rank, max_rows, band_rows=0,
-                mid_segment_bands=1, flags=MOE_LOCAL_DIRECT, watchdog_ms=0) -> moe_stage_config_t:
+                mid_segment_pieces=1, flags=MOE_LOCAL_DIRECT, watchdog_ms=0, down_split_k=0) -> moe_stage_config_t:
     return moe_stage_config_t(hidden, ffn, num_local_experts, num_ranks, self_rank, max_rows, band_rows,
-                              mid_segment_bands, flags, watchdog_ms)
+                              mid_segment_pieces, flags, watchdog_ms, down_split_k)
 
 
 def moe_stage_last_error(h=None) -> str:
@@ -228,7 +231,7 @@ def moe_plan_build(cfg: moe_stage_config_t, expert_offsets, row_src_rank, row_sl
                                       ("row_rank", MOE_PLAN_ROW_RANK, np.int32, 1),
                                       ("row_slot", MOE_PLAN_ROW_SLOT, np.int32, 1),
                                       ("segments", MOE_PLAN_SEGMENTS, np.int32, 8),
-                                      ("bands", MOE_PLAN_BANDS, np.int32, 4)):
+                                      ("groups", MOE_PLAN_GROUPS, np.int32, 4)):
             need = lib.moe_plan_copy(p, which, None, 0)
             arr = np.empty(need // np.dtype(dt).itemsize, dt)
             if need:
@@ -245,9 +248,9 @@ class MoeStage:
     """Owns one library handle.  Tensors are torch device tensors holding bf16 (or int16 bit patterns)."""
 
     def __init__(self, hidden, ffn, num_local_experts, num_ranks, self_rank, max_rows, band_rows=0,
-                 mid_segment_bands=1, flags=MOE_LOCAL_DIRECT, watchdog_ms=0):
+                 mid_segment_pieces=1, flags=MOE_LOCAL_DIRECT, watchdog_ms=0, down_split_k=0):
         self.cfg = make_config(hidden, ffn, num_local_experts, num_ranks, self_rank, max_rows, band_rows,
-                               mid_segment_bands, flags, watchdog_ms)
+                               mid_segment_pieces, flags, watchdog_ms, down_split_k)
         self.h = moe_stage_create(self.cfg)
 
     def run(self, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows=None,

@@ -53,6 +53,8 @@ struct moe_stage_s {
   uint16_t* hws = nullptr;
   uint16_t* y = nullptr;
   uint32_t* flags = nullptr;
+  float* partials = nullptr;
+  uint32_t* arrivals = nullptr;
   RunCounters* ctr = nullptr;
   uint8_t* d_plan = nullptr;
   size_t plan_cap = 0;
@@ -63,7 +65,7 @@ struct moe_stage_s {
 
   int cached_split = -1;
   hipStream_t s_cons = nullptr, s_prod = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_gu = nullptr, ev_join_c = nullptr, ev_join_p = nullptr, ev_done = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join_c = nullptr, ev_join_p = nullptr, ev_done = nullptr;
   bool ran = false;
   bool counters_pending = false;  // the last run's device counters have not been read yet
   uint32_t last_timeouts = 0, last_timeout_where = 0;
@@ -101,9 +103,10 @@ PlanParams params_of(const moe_stage_config_t& c, bool overlapped) {
   p.R = c.num_ranks;
   p.self = c.self_rank;
   p.band_rows = c.band_rows;
-  p.mid_bands = std::max(c.mid_segment_bands, 1);
+  p.mid_pieces = std::max(c.mid_segment_pieces, 1);
   p.local_direct = (c.flags & MOE_LOCAL_DIRECT) != 0;
   p.overlapped = overlapped;
+  p.split_k = c.down_split_k > 0 ? c.down_split_k : default_split_k(c.ffn);
   return p;
 }
 
@@ -111,11 +114,18 @@ int check_config(const moe_stage_config_t* c) {
   if (!c) return MOE_EINVAL;
   if (c->hidden <= 0 || c->ffn <= 0 || c->num_local_experts <= 0 || c->num_ranks <= 0 ||
       c->self_rank < 0 || c->self_rank >= c->num_ranks || c->max_rows < 0 ||
-      c->mid_segment_bands < 0 || c->watchdog_ms < 0)
+      c->mid_segment_pieces < 0 || c->watchdog_ms < 0)
     return MOE_EINVAL;
+  constexpr uint32_t kKnownFlags = MOE_LOCAL_DIRECT | MOE_KERNEL_TIMING | MOE_POISON |
+                                   MOE_TEST_NO_SIGNAL | MOE_SHARED_CUS;
+  if (c->flags & ~kKnownFlags) return MOE_EINVAL;
   if (c->band_rows < 0 || c->band_rows > 256 || (c->band_rows & (c->band_rows - 1)) != 0)
     return MOE_EINVAL;
-  if (c->hidden % 64 != 0 || c->ffn % 64 != 0) return MOE_EUNSUPPORTED;
+  if (c->down_split_k < 0 || c->down_split_k > kMaxSplitK ||
+      (c->ffn > 0 && c->down_split_k > c->ffn / kTileK))
+    return MOE_EINVAL;
+  if (c->hidden % 64 != 0 || c->ffn % 64 != 0 || c->hidden > kMaxDownColTiles * kDownTileN)
+    return MOE_EUNSUPPORTED;
   return MOE_OK;
 }
 
@@ -190,6 +200,8 @@ int prepare(moe_stage_s* h, bool overlapped, const void* x,
 
   InitArgs ia{};
   ia.ctr = h->ctr;
+  ia.arrivals = h->arrivals;
+  ia.n_arrivals = (int32_t)P.tile_rows.size() * P.down_per_row;
   if (c.flags & MOE_POISON) {
     ia.poison = h->y;
     ia.poison_elems = P.n_lrows() * c.hidden;
@@ -203,10 +215,11 @@ int prepare(moe_stage_s* h, bool overlapped, const void* x,
   st.n_band_padding = P.n_band_pad;
   st.n_remote_rows = P.n_remote;
   st.n_tile_rows = (int32_t)P.tile_rows.size();
-  st.n_bands = (int32_t)P.bands.size();
+  st.n_groups = (int32_t)P.groups.size();
   st.n_gu_items = P.n_gu;
   st.n_down_items = P.n_down;
   st.n_segments = (int32_t)P.segs.size();
+  st.split_k = P.p.split_k;
   return MOE_OK;
 }
 
@@ -224,6 +237,7 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
   a.items = (const uint32_t*)(h->d_plan + lay.items) + (down ? P.n_gu : 0);
   a.n_items = down ? P.n_down : P.n_gu;
   a.claim = down ? &h->ctr->down_next : &h->ctr->gu_next;
+  a.active = down ? &h->ctr->down_active : &h->ctr->gu_active;
   a.row_x = (const int32_t*)(h->d_plan + lay.row_x);
   a.row_rank = (const int32_t*)(h->d_plan + lay.row_rank);
   a.row_slot = (const int32_t*)(h->d_plan + lay.row_slot);
@@ -235,6 +249,9 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
   a.self_rank = h->cfg.self_rank;
   a.down_per_row = P.down_per_row;
   a.mode = mode;
+  a.split_k = P.p.split_k;
+  a.partials = h->partials;
+  a.arrivals = h->arrivals;
   return a;
 }
 
@@ -250,8 +267,10 @@ TimingRec* timing_slot(moe_stage_s* h) {
 // round-robin to the XCDs, so a queue must own CUs on every XCD, and an even split keeps
 // the per-XCD share symmetric: the consumer gets m = c / n_xcd CUs on each XCD.  The mask
 // bit b = i * (cus_per_xcd + 1) + j (XCD i, j < m) lands on XCD i whether the driver maps
-// bit b to XCD (b mod n_xcd) or to XCD (b / cus_per_xcd).  The producer gets the complement.
-void make_masks(int num_cus, int n_xcd, int c, std::vector<uint32_t>* mc, std::vector<uint32_t>* mp) {
+// bit b to XCD (b mod n_xcd) or to XCD (b / cus_per_xcd).  The producer gets the complement,
+// or every CU when `shared`.
+void make_masks(int num_cus, int n_xcd, int c, bool shared, std::vector<uint32_t>* mc,
+                std::vector<uint32_t>* mp) {
   const int words = (num_cus + 31) / 32;
   mc->assign(words, 0);
   mp->assign(words, 0);
@@ -263,7 +282,10 @@ void make_masks(int num_cus, int n_xcd, int c, std::vector<uint32_t>* mc, std::v
   } else {
     for (int b = 0; b < c; ++b) is_c[b] = 1;  // interleaved numbering: bits 0..c-1 cover every XCD
   }
-  for (int cu = 0; cu < num_cus; ++cu) ((is_c[cu] ? *mc : *mp))[cu / 32] |= 1u << (cu % 32);
+  for (int cu = 0; cu < num_cus; ++cu) {
+    if (is_c[cu]) (*mc)[cu / 32] |= 1u << (cu % 32);
+    if (shared || !is_c[cu]) (*mp)[cu / 32] |= 1u << (cu % 32);
+  }
 }
 
 // Consumer CUs actually reserved for a requested split: a multiple of the XCD count.
@@ -283,7 +305,7 @@ int ensure_streams(moe_stage_s* h, int c) {
     h->cached_split = -1;
   }
   std::vector<uint32_t> mc, mp;
-  make_masks(h->num_cus, h->n_xcd, c, &mc, &mp);
+  make_masks(h->num_cus, h->n_xcd, c, (h->cfg.flags & MOE_SHARED_CUS) != 0, &mc, &mp);
   HIP_TRY(h, hipExtStreamCreateWithCUMask(&h->s_cons, (uint32_t)mc.size(), mc.data()));
   HIP_TRY(h, hipExtStreamCreateWithCUMask(&h->s_prod, (uint32_t)mp.size(), mp.data()));
   h->cached_split = c;
@@ -301,9 +323,9 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   if (rc) return set_err(nullptr, rc, "invalid configuration");
   auto* h = new moe_stage_s();
   h->cfg = *cfg;
-  if (h->cfg.mid_segment_bands == 0) h->cfg.mid_segment_bands = 1;
-  if (h->cfg.band_rows == 0)
-    h->cfg.band_rows = default_band_rows(cfg->max_rows, cfg->num_local_experts, cfg->num_ranks);
+  if (h->cfg.mid_segment_pieces == 0) h->cfg.mid_segment_pieces = 1;
+  if (h->cfg.band_rows == 0) h->cfg.band_rows = 1;
+  if (h->cfg.down_split_k == 0) h->cfg.down_split_k = default_split_k(cfg->ffn);
   auto bail = [&](int code) {
     moe_stage_destroy(h);
     return code;
@@ -327,7 +349,8 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   h->max_lrows = (int64_t)h->max_tile_rows * kTileM;
   h->down_per_row = (cfg->hidden + kDownTileN - 1) / kDownTileN;
   const int gu_per_row = (cfg->ffn + kGuTileF - 1) / kGuTileF;
-  const int64_t max_items = (int64_t)h->max_tile_rows * (gu_per_row + h->down_per_row);
+  const int32_t S = h->cfg.down_split_k;
+  const int64_t max_items = (int64_t)h->max_tile_rows * (gu_per_row + (int64_t)h->down_per_row * S);
   const BlobLayout lay =
       blob_layout(h->max_tile_rows, max_items, h->max_lrows, h->max_lrows, cfg->num_ranks);
   h->plan_cap = lay.total;
@@ -342,7 +365,13 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   const size_t hws_bytes = (size_t)h->max_lrows * cfg->ffn * 2;
   const size_t y_bytes = (size_t)h->max_lrows * cfg->hidden * 2;
   const size_t flag_bytes = (size_t)h->max_tile_rows * h->down_per_row * 4;
-  if (!try_hip(hipMalloc(&h->hws, hws_bytes), "hipMalloc(hws)") ||
+  // One fp32 partial tile (256 threads x 256 accumulators) per K part of every down tile.
+  const size_t part_bytes =
+      S > 1 ? (size_t)h->max_tile_rows * h->down_per_row * S * kProducerThreads * 256 * 4 : 0;
+  if ((part_bytes && !try_hip(hipMalloc(&h->partials, part_bytes), "hipMalloc(partials)")) ||
+      !try_hip(hipMalloc(&h->arrivals, flag_bytes), "hipMalloc(arrivals)") ||
+      !try_hip(hipMemset(h->arrivals, 0, flag_bytes), "hipMemset(arrivals)") ||
+      !try_hip(hipMalloc(&h->hws, hws_bytes), "hipMalloc(hws)") ||
       !try_hip(hipMalloc(&h->y, y_bytes), "hipMalloc(y)") ||
       !try_hip(hipMalloc(&h->flags, flag_bytes), "hipMalloc(flags)") ||
       !try_hip(hipMalloc(&h->ctr, sizeof(RunCounters)), "hipMalloc(counters)") ||
@@ -354,21 +383,26 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       !try_hip(hipMemset(h->flags, 0, flag_bytes), "hipMemset(flags)") ||
       !try_hip(hipMemset(h->ctr, 0, sizeof(RunCounters)), "hipMemset(counters)"))
     return bail(MOE_EHIP);
+  // Every event here orders work on this device or marks completion for the host; none
+  // publishes device writes to the host (results are read through the caller's own copies),
+  // so a device-scope release suffices and no system-scope cache writeback sits between
+  // launches.
+  constexpr unsigned kSyncEv = hipEventDisableTiming | hipEventReleaseToDevice;
   for (int i = 0; i < 2; ++i)
-    if (!try_hip(hipEventCreateWithFlags(&h->stage_free[i], hipEventDisableTiming), "hipEventCreate") ||
+    if (!try_hip(hipEventCreateWithFlags(&h->stage_free[i], kSyncEv), "hipEventCreate") ||
         !try_hip(hipEventRecord(h->stage_free[i], nullptr), "hipEventRecord"))
       return bail(MOE_EHIP);
-  if (!try_hip(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming), "hipEventCreate") ||
-      !try_hip(hipEventCreateWithFlags(&h->ev_gu, hipEventDisableTiming), "hipEventCreate") ||
-      !try_hip(hipEventCreateWithFlags(&h->ev_join_c, hipEventDisableTiming), "hipEventCreate") ||
-      !try_hip(hipEventCreateWithFlags(&h->ev_join_p, hipEventDisableTiming), "hipEventCreate") ||
-      !try_hip(hipEventCreateWithFlags(&h->ev_done, hipEventDisableTiming), "hipEventCreate"))
+  if (!try_hip(hipEventCreateWithFlags(&h->ev_fork, kSyncEv), "hipEventCreate") ||
+      !try_hip(hipEventCreateWithFlags(&h->ev_join_c, kSyncEv), "hipEventCreate") ||
+      !try_hip(hipEventCreateWithFlags(&h->ev_join_p, kSyncEv), "hipEventCreate") ||
+      !try_hip(hipEventCreateWithFlags(&h->ev_done, kSyncEv), "hipEventCreate"))
     return bail(MOE_EHIP);
   if (h->cfg.flags & MOE_KERNEL_TIMING) {
     h->ring.resize(kTimingRing);
     for (auto& r : h->ring)
       for (auto& ev : r.ev)
-        if (!try_hip(hipEventCreate(&ev), "hipEventCreate")) return bail(MOE_EHIP);
+        if (!try_hip(hipEventCreateWithFlags(&ev, hipEventReleaseToDevice), "hipEventCreate"))
+          return bail(MOE_EHIP);
   }
   if (!try_hip(hipDeviceSynchronize(), "hipDeviceSynchronize")) return bail(MOE_EHIP);
   *out = h;
@@ -383,7 +417,8 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   if (cu_split < 1 || cu_split > h->num_cus - h->n_xcd)
     return set_err(h, MOE_EUNSUPPORTED, "cu_split must be in [1, compute units - XCDs]");
   const int c_eff = effective_split(h, cu_split);
-  const int pgrid = (h->num_cus - c_eff) * h->producer_bpc;
+  const bool shared = (h->cfg.flags & MOE_SHARED_CUS) != 0;
+  const int pgrid = (shared ? h->num_cus : h->num_cus - c_eff) * h->producer_bpc;
   const int cgrid = c_eff * 2;
   int rc = ensure_streams(h, c_eff);
   if (rc) return rc;
@@ -413,25 +448,33 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   ca.ctr = h->ctr;
   ca.watchdog_ticks = watchdog_ticks(h);
 
-  // Producer stream: gate/up GEMM, then the signaling down GEMM.  The consumer is released
-  // when the gate/up launch completes (down tiles, the only transfer sources, start then),
-  // and is enqueued before the down launch so its workgroups are resident first.
+  // The consumer is released as soon as the init kernel has reset the queue heads: it only
+  // reads segments of the uploaded plan and flags this run's down launch raises, so no event
+  // sits between the producer's two launches.  With shared CUs the producer stays on the
+  // caller's stream and follows the init kernel without a cross-queue hop -- unless that is
+  // the legacy null stream, whose launches wait for all earlier work on blocking streams,
+  // the still-polling consumer included: that would be a cycle, so the producer then forks
+  // to the handle's own stream like the partitioned launch.
+  const bool legacy = stream == nullptr || stream == hipStreamLegacy;
+  const bool on_caller = shared && !legacy;
+  hipStream_t ps = on_caller ? stream : h->s_prod;
   HIP_TRY(h, hipEventRecord(h->ev_fork, stream));
-  HIP_TRY(h, hipStreamWaitEvent(h->s_prod, h->ev_fork, 0));
-  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], h->s_prod));
-  if (pgu.n_items > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, h->s_prod));
-  HIP_TRY(h, hipEventRecord(h->ev_gu, h->s_prod));
-  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], h->s_prod));
-  HIP_TRY(h, hipStreamWaitEvent(h->s_cons, h->ev_gu, 0));
+  HIP_TRY(h, hipStreamWaitEvent(h->s_cons, h->ev_fork, 0));
+  if (!on_caller) HIP_TRY(h, hipStreamWaitEvent(h->s_prod, h->ev_fork, 0));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[3], h->s_cons));
   if (ca.n_segs > 0) HIP_TRY(h, launch_consumer(ca, cgrid, h->s_cons));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
-  if (pdn.n_items > 0) HIP_TRY(h, launch_producer(pdn, true, pgrid, h->s_prod));
-  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], h->s_prod));
   HIP_TRY(h, hipEventRecord(h->ev_join_c, h->s_cons));
-  HIP_TRY(h, hipEventRecord(h->ev_join_p, h->s_prod));
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], ps));
+  if (pgu.n_items > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, ps));
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], ps));
+  if (pdn.n_items > 0) HIP_TRY(h, launch_producer(pdn, true, pgrid, ps));
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], ps));
+  if (!on_caller) {
+    HIP_TRY(h, hipEventRecord(h->ev_join_p, h->s_prod));
+    HIP_TRY(h, hipStreamWaitEvent(stream, h->ev_join_p, 0));
+  }
   HIP_TRY(h, hipStreamWaitEvent(stream, h->ev_join_c, 0));
-  HIP_TRY(h, hipStreamWaitEvent(stream, h->ev_join_p, 0));
   if (tr) {
     HIP_TRY(h, hipEventRecord(tr->ev[5], stream));
     tr->kind = 0;
@@ -495,6 +538,8 @@ int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
     HIP_TRY(h, hipMemcpy(&c, h->ctr, sizeof c, hipMemcpyDeviceToHost));
     h->last.poll_iters = c.poll_iters;
     h->last.wait_ticks = c.wait_ticks;
+    h->last.gu_workgroups = (int32_t)c.gu_active;
+    h->last.down_workgroups = (int32_t)c.down_active;
     h->last.timeout = c.timeouts ? 1 : 0;
     h->last_timeouts = c.timeouts;
     h->last_timeout_where = c.timeout_where;
@@ -548,12 +593,13 @@ int moe_stage_destroy(moe_stage_t h) {
   for (auto& r : h->ring)
     for (auto& ev : r.ev)
       if (ev) (void)hipEventDestroy(ev);
-  for (hipEvent_t ev : {h->stage_free[0], h->stage_free[1], h->ev_fork, h->ev_gu, h->ev_join_c, h->ev_join_p,
+  for (hipEvent_t ev : {h->stage_free[0], h->stage_free[1], h->ev_fork, h->ev_join_c, h->ev_join_p,
                         h->ev_done})
     if (ev) (void)hipEventDestroy(ev);
   if (h->s_cons) (void)hipStreamDestroy(h->s_cons);
   if (h->s_prod) (void)hipStreamDestroy(h->s_prod);
-  for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->ctr, (void*)h->d_plan})
+  for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->ctr, (void*)h->d_plan,
+                  (void*)h->partials, (void*)h->arrivals})
     if (p) (void)hipFree(p);
   for (uint8_t* p : h->h_stage)
     if (p) (void)hipHostFree(p);
@@ -576,7 +622,7 @@ int moe_plan_build(const moe_stage_config_t* cfg, int64_t rows, const int32_t* o
   if (rc) return set_err(nullptr, rc, "invalid configuration");
   if (rows > cfg->max_rows) return set_err(nullptr, MOE_ECAPACITY, "rows > max_rows");
   moe_stage_config_t c = *cfg;
-  if (c.band_rows == 0) c.band_rows = default_band_rows(c.max_rows, c.num_local_experts, c.num_ranks);
+  if (c.band_rows == 0) c.band_rows = 1;
   if (off && off[c.num_local_experts] != rows)
     return set_err(nullptr, MOE_EROUTING, "expert_offsets[E_l] must equal rows");
   auto* p = new moe_plan_s();
@@ -599,11 +645,12 @@ int moe_plan_info(moe_plan_t p, moe_plan_info_t* o) {
   o->n_gu_items = P.n_gu;
   o->n_down_items = P.n_down;
   o->n_segments = (int32_t)P.segs.size();
-  o->n_bands = (int32_t)P.bands.size();
+  o->n_groups = (int32_t)P.groups.size();
   o->gu_tiles_per_row = P.gu_per_row;
   o->down_tiles_per_row = P.down_per_row;
   o->tile_m = kTileM;
   o->band_rows = p->band_rows;
+  o->split_k = P.p.split_k;
   o->n_logical_rows = P.n_lrows();
   o->n_valid = P.n_valid;
   o->n_band_padding = P.n_band_pad;
@@ -623,7 +670,7 @@ int64_t moe_plan_copy(moe_plan_t p, int32_t which, void* dst, int64_t bytes) {
     case MOE_PLAN_ROW_RANK: src = P.row_rank.data(); need = sizeof(int32_t) * P.row_rank.size(); break;
     case MOE_PLAN_ROW_SLOT: src = P.row_slot.data(); need = sizeof(int32_t) * P.row_slot.size(); break;
     case MOE_PLAN_SEGMENTS: src = P.segs.data(); need = sizeof(Segment) * P.segs.size(); break;
-    case MOE_PLAN_BANDS: src = P.bands.data(); need = sizeof(Band) * P.bands.size(); break;
+    case MOE_PLAN_GROUPS: src = P.groups.data(); need = sizeof(Group) * P.groups.size(); break;
     default: return MOE_EINVAL;
   }
   if (!dst) return need;

@@ -199,14 +199,20 @@ __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const uint8_
 
 // One work item; `down` selects a down-projection tile (otherwise a fused gate/up tile).
 // Each kind is its own instantiation so the register allocator sees one straight path.
-template <bool down>
-__device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t item, uint8_t* lds) {
+// One work item.  kSplit (down tiles only) selects the K-part count at compile time: 1 = whole
+// tiles, 2..4 = that many parts, 0 = any count read from the arguments.  A kernel holding
+// both epilogues would keep copies of the accumulators live across the branch, and a fixed
+// count lets the reduction issue the loads of several blocks of every part at once.
+template <bool down, int kSplit>
+__device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t item, uint8_t* lds,
+                                              uint32_t* s_last) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave: keeps bases scalar
   const int wn = wave & 1, wm = wave >> 1;
   const int lr = lane & 31, lk = lane >> 5;
   const int t = (int)((item >> kItemRowShift) & (uint32_t)(kMaxTileRows - 1));
-  const int col = (int)(item & kItemColMask);
+  const int col = down ? (int)((item >> kDownColShift) & kDownColMask) : (int)(item & kItemColMask);
+  const int part = down ? (int)(item & kDownPartMask) : 0;
   const TileRow tr = a.tile_rows[t];
   const int64_t H = a.H, F = a.F;
   const int e = tr.expert, lrow0 = tr.lrow0;
@@ -244,8 +250,18 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     }
   }
 
+  // K range of this item: all of it, or one of split_k near-equal runs of K steps.
+  int kbeg = 0, klen = down ? (int)F : (int)H;
+  constexpr bool split = kSplit != 1;
+  const int S = kSplit == 0 ? a.split_k : kSplit;
+  if (split) {
+    const int nk = (int)F / kTileK;
+    const int s0 = part * nk / S, s1 = (part + 1) * nk / S;
+    kbeg = s0 * kTileK;
+    klen = (s1 - s0) * kTileK;
+  }
   f32x16 acc[4][4];
-  tile_mma(lds, wbase, xbase, woff, xoff, down ? (int)F : (int)H, acc);
+  tile_mma(lds, wbase + kbeg * 2, xbase + kbeg * 2, woff, xoff, klen, acc);
 
   if constexpr (!down) {
     // Gated activation a = bf16(silu(g) * u): lane values -> LDS tile [256 rows][128 features].
@@ -280,22 +296,97 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
         *(u32x4*)(a.hws + (int64_t)lrow * F + f) = *(const u32x4*)(lds + m * kGuOutStride + c16 * 16);
     }
   } else {
-    // Down-projection output: lane values -> LDS tile [256 rows][256 hidden columns].
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = wm * 128 + j * 32 + lr;
+    // Split K: every part stores its fp32 accumulators (in register order, so each thread
+    // reads back exactly the positions it wrote) and counts itself in; the part that arrives
+    // last reads all parts back and adds them in part order -- a fixed order whichever part
+    // that is -- and writes the tile.
+    const int tile = t * a.down_per_row + col;
+    const float4* parts = nullptr;
+    if constexpr (split) {
+      constexpr int kPartF4 = kProducerThreads * 64;  // float4s per part tile
+      parts = (const float4*)a.partials + (size_t)tile * S * kPartF4;
+      float4* mine = (float4*)a.partials + ((size_t)tile * S + part) * kPartF4;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int nl = wn * 128 + i * 32 + 8 * q + 4 * lk;
-          const f32x16& d = acc[i][j];
-          uint2 v;
-          v.x = pack_bf16x2(d[4 * q + 0], d[4 * q + 1]);
-          v.y = pack_bf16x2(d[4 * q + 2], d[4 * q + 3]);
-          *(uint2*)(lds + m * kDownOutStride + nl * 2) = v;
-          __builtin_amdgcn_sched_barrier(0);  // block by block (see above)
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            mine[((i * 4 + j) * 4 + q) * kProducerThreads + tid] =
+                float4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+      wait_vm_and_barrier<0>();  // every wave's part stores have completed
+      if (tid == 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        const uint32_t prev =
+            __hip_atomic_fetch_add(&a.arrivals[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *s_last = (prev + 1 == (uint32_t)S) ? 1u : 0u;
+      }
+      __syncthreads();
+      if (*s_last == 0) return;  // another part finishes the tile
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+    // Down-projection output: lane values -> LDS tile [256 rows][256 hidden columns].
+    auto stage_out = [&](int i, int j, int q, float4 s) {
+      const int m = wm * 128 + j * 32 + lr;
+      const int nl = wn * 128 + i * 32 + 8 * q + 4 * lk;
+      uint2 v;
+      v.x = pack_bf16x2(s.x, s.y);
+      v.y = pack_bf16x2(s.z, s.w);
+      *(uint2*)(lds + m * kDownOutStride + nl * 2) = v;
+    };
+    if constexpr (kSplit == 0) {
+      // Any part count: blocks b = (i*4 + j)*4 + q indexed at run time, every part read back.
+      const float4* src = parts + tid;
+#pragma unroll 1
+      for (int b = 0; b < 64; ++b) {
+        const float4* blk = src + b * kProducerThreads;
+        float4 s = blk[0];
+        for (int p = 1; p < S; ++p) {
+          const float4 v = blk[(size_t)p * kProducerThreads * 64];
+          s.x += v.x;
+          s.y += v.y;
+          s.z += v.z;
+          s.w += v.w;
         }
+        stage_out(b >> 4, (b >> 2) & 3, b & 3, s);
+      }
+    } else if constexpr (split) {
+      // kSplit parts: all parts read back (this part's too: the same values, and no branch
+      // that would serialize the loads), 4 blocks of kSplit loads in flight per step.
+      const float4* src = parts + tid;
+#pragma unroll 1
+      for (int b0 = 0; b0 < 64; b0 += 4) {
+        float4 v[4][kSplit];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int p = 0; p < kSplit; ++p)
+            v[u][p] = src[(size_t)p * kProducerThreads * 64 + (b0 + u) * kProducerThreads];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          float4 s = v[u][0];
+#pragma unroll
+          for (int p = 1; p < kSplit; ++p) {
+            s.x += v[u][p].x;
+            s.y += v[u][p].y;
+            s.z += v[u][p].z;
+            s.w += v[u][p].w;
+          }
+          const int b = b0 + u;
+          stage_out(b >> 4, (b >> 2) & 3, b & 3, s);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x16& d = acc[i][j];
+            stage_out(i, j, q, float4{d[4 * q], d[4 * q + 1], d[4 * q + 2], d[4 * q + 3]});
+            __builtin_amdgcn_sched_barrier(0);  // block by block (see above)
+          }
     }
     __syncthreads();
     // 32 threads store one 512-byte output row; 8 rows per pass.  Rows returning to another
@@ -315,11 +406,12 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
         *(u32x4*)(dst + n) = *(const u32x4*)(lds + m * kDownOutStride + c16 * 16);
       }
     }
-    __syncthreads();
+    // Every wave's output stores have completed before wave 0's agent-scope release
+    // publishes the tile (a plain barrier does not wait for other waves' stores).
+    wait_vm_and_barrier<0>();
     if ((a.mode & kModeSignal) && (tr.has_remote || !direct)) {
       if (tid == 0)
-        __hip_atomic_store(&a.flags[t * a.down_per_row + col], a.epoch, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&a.flags[tile], a.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -327,22 +419,25 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
 // Persistent producer: every workgroup claims items from this launch's queue until it is
 // empty.  Nothing inside waits on another workgroup, so progress never depends on which
 // workgroups are resident.
-template <bool down>
+template <bool down, int kSplit>
 __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerArgs a) {
   static_assert(kLdsAlloc >= kLdsBytes, "staging must fit the LDS allocation");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsAlloc];
-  __shared__ uint32_t s_next;
+  __shared__ uint32_t s_next, s_last;
   const int tid = threadIdx.x;
-  if (tid == 0) s_next = atomicAdd(a.claim, 1u);
+  if (tid == 0) {
+    s_next = atomicAdd(a.claim, 1u);
+    if (s_next < (uint32_t)a.n_items) atomicAdd(a.active, 1u);
+  }
   __syncthreads();
-  uint32_t cur = s_next;
+  uint32_t cur = __builtin_amdgcn_readfirstlane(s_next);  // uniform: item fields stay scalar
   while (cur < (uint32_t)a.n_items) {
     __syncthreads();
     // Claim the next item now; its index is read after this one finishes.
     if (tid == 0) s_next = atomicAdd(a.claim, 1u);
-    producer_item<down>(a, a.items[cur], lds);
+    producer_item<down, kSplit>(a, a.items[cur], lds, &s_last);
     __syncthreads();
-    cur = s_next;
+    cur = __builtin_amdgcn_readfirstlane(s_next);
   }
 }
 
@@ -437,9 +532,12 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
     a.ctr->gu_next = 0;
     a.ctr->down_next = 0;
     a.ctr->seg_next = 0;
+    a.ctr->gu_active = 0;
+    a.ctr->down_active = 0;
     a.ctr->poll_iters = 0;
     a.ctr->wait_ticks = 0;
   }
+  for (int64_t j = i; j < a.n_arrivals; j += stride) a.arrivals[j] = 0;
   if (a.poison) {
     const u32x4 nan = {0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};
     for (int64_t j = i; j < a.poison_elems / 8; j += stride) ((u32x4*)a.poison)[j] = nan;
@@ -454,10 +552,19 @@ hipError_t launch_init(const InitArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream_t s) {
-  if (down)
-    hipLaunchKernelGGL(producer_kernel<true>, dim3(grid), dim3(kProducerThreads), 0, s, a);
+  const dim3 g(grid), b(kProducerThreads);
+  if (!down)
+    hipLaunchKernelGGL((producer_kernel<false, 1>), g, b, 0, s, a);
+  else if (a.split_k == 1)
+    hipLaunchKernelGGL((producer_kernel<true, 1>), g, b, 0, s, a);
+  else if (a.split_k == 2)
+    hipLaunchKernelGGL((producer_kernel<true, 2>), g, b, 0, s, a);
+  else if (a.split_k == 3)
+    hipLaunchKernelGGL((producer_kernel<true, 3>), g, b, 0, s, a);
+  else if (a.split_k == 4)
+    hipLaunchKernelGGL((producer_kernel<true, 4>), g, b, 0, s, a);
   else
-    hipLaunchKernelGGL(producer_kernel<false>, dim3(grid), dim3(kProducerThreads), 0, s, a);
+    hipLaunchKernelGGL((producer_kernel<true, 0>), g, b, 0, s, a);
   return hipGetLastError();
 }
 
@@ -473,7 +580,7 @@ hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s) {
 
 int producer_blocks_per_cu() {
   int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, producer_kernel<false>, kProducerThreads, 0) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, producer_kernel<false, 1>, kProducerThreads, 0) != hipSuccess)
     return 1;
   return n > 0 ? n : 1;
 }

@@ -22,6 +22,7 @@ struct ProducerArgs {
   const uint32_t* items;   // this launch's work items (all gate/up or all down tiles)
   int32_t n_items;
   uint32_t* claim;         // queue head of this launch
+  uint32_t* active;        // count of workgroups that claimed work in this launch
   const int32_t* row_x;    // [n_lrows]
   const int32_t* row_rank; // [n_lrows], -1 = padding
   const int32_t* row_slot; // [n_lrows]
@@ -30,6 +31,9 @@ struct ProducerArgs {
   uint32_t epoch;
   int32_t H, F, self_rank, down_per_row;
   uint32_t mode;
+  int32_t split_k;         // K parts per down tile
+  float* partials;         // [tiles][split_k][256 threads x 256] fp32 part sums (split_k > 1)
+  uint32_t* arrivals;      // [tiles] parts finished this run (zeroed by the init kernel)
 };
 
 struct ConsumerArgs {
@@ -57,6 +61,8 @@ struct InitArgs {
   RunCounters* ctr;
   uint16_t* poison;        // optional: filled with bf16 NaN
   int64_t poison_elems;    // multiple of 8
+  uint32_t* arrivals;      // split-K arrival counters to zero
+  int32_t n_arrivals;
 };
 
 hipError_t launch_init(const InitArgs& a, hipStream_t s);

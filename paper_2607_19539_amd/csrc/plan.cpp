@@ -19,8 +19,8 @@ int fail(std::string* err, int code, const std::string& msg) {
 int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
 uint32_t gu_item(int32_t t, int32_t j) { return ((uint32_t)t << kItemRowShift) | (uint32_t)j; }
-uint32_t down_item(int32_t t, int32_t n) {
-  return kItemDown | ((uint32_t)t << kItemRowShift) | (uint32_t)n;
+uint32_t down_item(int32_t t, int32_t n, int32_t part) {
+  return kItemDown | ((uint32_t)t << kItemRowShift) | ((uint32_t)n << kDownColShift) | (uint32_t)part;
 }
 
 }  // namespace
@@ -30,13 +30,7 @@ int64_t max_logical_rows(int64_t max_rows, int32_t E_l, int32_t R, int32_t band_
   return max_rows + (int64_t)E_l * ((int64_t)(R - 1) * (tb - 1) + kTileM - 1);
 }
 
-int32_t default_band_rows(int32_t max_rows, int32_t E_l, int32_t R) {
-  // Largest band whose expected group padding (half a band per remote group) stays
-  // within 2 % of the rows; never below 16 rows.
-  for (int32_t tb = 256; tb >= 16; tb /= 2)
-    if ((double)E_l * (R - 1) * (tb - 1) * 0.5 <= 0.02 * (double)max_rows) return tb;
-  return 16;
-}
+int32_t default_split_k(int32_t ffn) { return std::max(1, std::min(4, ffn / 3072)); }
 
 int validate_routing(const PlanParams& p, int64_t rows, const int32_t* off, const int32_t* src,
                      const int32_t* slot, const int64_t* return_rows, std::string* err) {
@@ -94,7 +88,7 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
   P.row_rank.clear();
   P.row_slot.clear();
   P.segs.clear();
-  P.bands.clear();
+  P.groups.clear();
   P.n_valid = rows;
   P.n_band_pad = 0;
   P.n_remote = 0;
@@ -148,16 +142,15 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
       }
       if (r != p.self) P.n_remote += n;
       if (p.overlapped) {
-        for (int64_t b0 = pos; b0 < pos + n; b0 += tb) {
-          P.bands.push_back(Band{e, (int32_t)b0, (int32_t)std::min<int64_t>(tb, pos + n - b0), r});
-          if (r != p.self) ++remote_bands[e];
-        }
+        P.groups.push_back(Group{e, (int32_t)pos, (int32_t)n, r});
+        if (r != p.self) remote_bands[e] += (int32_t)((n + tb - 1) / tb);
       }
       pos += n;
       if (p.overlapped && r != p.self) {
         // Zero-row padding up to the next band boundary (Algorithm 1): the next group then
-        // starts band-aligned and every band has a single destination.  Padding rows repeat
-        // the expert's first row as input; their outputs are never stored or transferred.
+        // starts band-aligned and every band of tb_M rows has a single destination (none
+        // with the default tb_M = 1).  Padding rows repeat the expert's first row as input;
+        // their outputs are never stored or transferred.
         const int64_t pad = round_up(pos - base, tb) - (pos - base);
         for (int64_t q = 0; q < pad; ++q) {
           P.row_x.push_back((int32_t)lo);
@@ -186,12 +179,14 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
   }
   const int32_t n_tr = (int32_t)P.tile_rows.size();
   if (n_tr >= kMaxTileRows) return fail(err, -3, "too many tile rows");
-  if (P.gu_per_row >= kMaxColTiles || P.down_per_row >= kMaxColTiles)
+  if (P.gu_per_row >= kMaxColTiles || P.down_per_row > kMaxDownColTiles)
     return fail(err, -6, "hidden or ffn too large for the work-item encoding");
+  if (p.split_k < 1 || p.split_k > kMaxSplitK || p.split_k > p.F / kTileK)
+    return fail(err, -1, "split_k out of range");
 
-  // Remote-first tile schedule (Section 3.2.2): rule (ii) experts by remote band count,
-  // descending (ties by expert id); rule (i) every tile row holding remote rows before
-  // any tile row that holds only local rows.
+  // Remote-first tile schedule (Section 3.2.2): rule (ii) experts by remote band count
+  // (bands of tb_M rows, so remote rows when tb_M = 1), descending, ties by expert id;
+  // rule (i) every tile row holding remote rows before any tile row of only local rows.
   std::vector<int32_t> order;
   order.reserve(n_tr);
   if (p.overlapped) {
@@ -226,66 +221,67 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
 
   // Down tiles, the signaling GEMM of Section 3.3.1, run after every gate/up tile (a separate
   // launch on the producer stream).  They follow the remote-first order tile row by tile
-  // row, so the first segments become ready as early as possible.
+  // row, so the first segments become ready as early as possible; the K parts of one tile
+  // are adjacent, so they run side by side and the tile is ready after 1/split_k of its
+  // sequential time.  A tile is ready once its last part is done.
   std::vector<int32_t> pos_of_down((size_t)n_tr * P.down_per_row, -1);
   for (int32_t q = 0; q < n_tr; ++q)
     for (int32_t n = 0; n < P.down_per_row; ++n) {
       const int32_t t = order[q];
-      pos_of_down[(size_t)t * P.down_per_row + n] = (int32_t)P.items.size();
-      P.items.push_back(down_item(t, n));
+      for (int32_t part = 0; part < p.split_k; ++part) P.items.push_back(down_item(t, n, part));
+      pos_of_down[(size_t)t * P.down_per_row + n] = (int32_t)P.items.size() - 1;
     }
   P.n_down = (int32_t)P.items.size() - P.n_gu;
 
-  // Combine plan (Section 3.2.3) and segment composition (Section 3.3.2): per owner group,
-  // the first and last segments are one band, middle segments coalesce x bands.  Rows of a
-  // segment are contiguous in the staged output and in the receive buffer; a slot gap splits
-  // a segment.  Local groups need no transfer when the producer writes them directly.
+  // Combine plan (Section 3.2.3) and segment composition (Section 3.3.2).  A row is ready
+  // when the down tiles of its 256-row tile row are, so each owner group is cut at tile-row
+  // boundaries into pieces; per group the first and the last piece are one segment each and
+  // middle segments coalesce x pieces.  Rows of a segment are contiguous in the staged output
+  // and in the receive buffer; a slot gap splits a segment.  Local groups need no transfer
+  // when the producer writes them directly.
   if (p.overlapped) {
-    const int32_t x = std::max<int32_t>(p.mid_bands, 1);
-    const size_t nb = P.bands.size();
-    for (size_t g0 = 0; g0 < nb;) {
-      size_t g1 = g0 + 1;
-      while (g1 < nb && P.bands[g1].expert == P.bands[g0].expert &&
-             P.bands[g1].dst_rank == P.bands[g0].dst_rank)
-        ++g1;
-      const int32_t dst = P.bands[g0].dst_rank;
-      if (dst != p.self || !p.local_direct) {
-        const int32_t k = (int32_t)(g1 - g0);
-        std::vector<std::pair<int32_t, int32_t>> chunks;  // band ranges
-        if (k <= 2) {
-          for (int32_t b = 0; b < k; ++b) chunks.emplace_back(b, b + 1);
-        } else {
-          chunks.emplace_back(0, 1);
-          for (int32_t b = 1; b < k - 1; b += x) chunks.emplace_back(b, std::min(b + x, k - 1));
-          chunks.emplace_back(k - 1, k);
-        }
-        for (auto& c : chunks) {
-          const Band& first = P.bands[g0 + c.first];
-          const Band& last = P.bands[g0 + c.second - 1];
-          const int32_t r0 = first.lrow0, r1 = last.lrow0 + last.nvalid;
-          int32_t s = r0;
-          while (s < r1) {
-            int32_t e_ = s + 1;
-            while (e_ < r1 && P.row_slot[e_] == P.row_slot[e_ - 1] + 1) ++e_;
-            Segment sg{};
-            sg.dst_rank = dst;
-            sg.rows = e_ - s;
-            sg.y_row0 = s;
-            sg.slot0 = P.row_slot[s];
-            const int32_t t0 = s / kTileM, t1 = (e_ - 1) / kTileM;
-            sg.flag_begin = t0 * P.down_per_row;
-            sg.flag_count = (t1 - t0 + 1) * P.down_per_row;
-            int32_t rp = 0;
-            for (int32_t f = sg.flag_begin; f < sg.flag_begin + sg.flag_count; ++f)
-              rp = std::max(rp, pos_of_down[f]);
-            sg.ready_pos = rp;
-            sg.nbands = c.second - c.first;
-            P.segs.push_back(sg);
-            s = e_;
-          }
+    const int32_t x = std::max<int32_t>(p.mid_pieces, 1);
+    std::vector<std::pair<int32_t, int32_t>> pieces, chunks;
+    for (const Group& g : P.groups) {
+      if (g.dst_rank == p.self && p.local_direct) continue;
+      pieces.clear();
+      for (int32_t s0 = g.lrow0; s0 < g.lrow0 + g.rows;) {
+        const int32_t s1 = std::min(g.lrow0 + g.rows, (s0 / kTileM + 1) * kTileM);
+        pieces.emplace_back(s0, s1);
+        s0 = s1;
+      }
+      const int32_t k = (int32_t)pieces.size();
+      chunks.clear();
+      if (k <= 2) {
+        for (int32_t b = 0; b < k; ++b) chunks.emplace_back(b, b + 1);
+      } else {
+        chunks.emplace_back(0, 1);
+        for (int32_t b = 1; b < k - 1; b += x) chunks.emplace_back(b, std::min(b + x, k - 1));
+        chunks.emplace_back(k - 1, k);
+      }
+      for (auto& c : chunks) {
+        const int32_t r0 = pieces[c.first].first, r1 = pieces[c.second - 1].second;
+        int32_t s = r0;
+        while (s < r1) {
+          int32_t e_ = s + 1;
+          while (e_ < r1 && P.row_slot[e_] == P.row_slot[e_ - 1] + 1) ++e_;
+          Segment sg{};
+          sg.dst_rank = g.dst_rank;
+          sg.rows = e_ - s;
+          sg.y_row0 = s;
+          sg.slot0 = P.row_slot[s];
+          const int32_t t0 = s / kTileM, t1 = (e_ - 1) / kTileM;
+          sg.flag_begin = t0 * P.down_per_row;
+          sg.flag_count = (t1 - t0 + 1) * P.down_per_row;
+          int32_t rp = 0;
+          for (int32_t f = sg.flag_begin; f < sg.flag_begin + sg.flag_count; ++f)
+            rp = std::max(rp, pos_of_down[f]);
+          sg.ready_pos = rp;
+          sg.npieces = c.second - c.first;
+          P.segs.push_back(sg);
+          s = e_;
         }
       }
-      g0 = g1;
     }
     // The consumer claims segments in the order their data becomes ready.
     std::stable_sort(P.segs.begin(), P.segs.end(),

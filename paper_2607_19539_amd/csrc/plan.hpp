@@ -18,11 +18,12 @@ namespace moe {
 
 struct PlanParams {
   int32_t H = 0, F = 0, E_l = 0, R = 0, self = 0;
-  int32_t band_rows = 0;      // tb_M
-  int32_t mid_bands = 1;      // x (mgb)
+  int32_t band_rows = 1;      // tb_M: remote owner groups start at multiples of it
+  int32_t mid_pieces = 1;     // x (mgb): tile-row pieces per middle segment
   bool local_direct = true;   // local rows need no transfer
   bool overlapped = true;     // false: plan of the non-overlapped baseline
   int32_t band_group = 8;     // tile rows that sweep the weight columns together
+  int32_t split_k = 1;        // K parts per down tile (1..kMaxSplitK)
 };
 
 struct Plan {
@@ -32,7 +33,7 @@ struct Plan {
   std::vector<uint32_t> items;
   std::vector<int32_t> row_x, row_rank, row_slot;
   std::vector<Segment> segs;
-  std::vector<Band> bands;
+  std::vector<Group> groups;
   int64_t n_valid = 0, n_band_pad = 0, n_remote = 0;
   int32_t n_gu = 0, n_down = 0;
   int64_t n_lrows() const { return (int64_t)row_x.size(); }
@@ -52,8 +53,11 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* expert_offsets,
 // Upper bound of logical rows of the padded layout for `max_rows` routed rows.
 int64_t max_logical_rows(int64_t max_rows, int32_t E_l, int32_t R, int32_t band_rows);
 
-// Default band height: the largest power of two (16..256) whose expected owner-group
-// padding stays within 2 % of max_rows.
-int32_t default_band_rows(int32_t max_rows, int32_t E_l, int32_t R);
+
+// Default K parts per down tile: one per 3072 of ffn, at most 4.  A down tile is
+// 2 * 256 * 256 * ffn flops; long tiles make the last, partly filled round of the down launch
+// expensive, and splitting them shrinks that round while the added fp32 partial traffic
+// (about 7/4 x 256 KiB per tile at 4 parts) stays small next to the operand traffic.
+int32_t default_split_k(int32_t ffn);
 
 }  // namespace moe

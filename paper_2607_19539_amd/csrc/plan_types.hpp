@@ -17,12 +17,21 @@ constexpr int kGuTileF = 128;
 constexpr int kDownTileN = 256;
 constexpr int kTileK = 32;
 
-// Work-item encoding: bit 31 = down tile, bits 30..12 = tile row, bits 11..0 = column tile.
+// Work-item encoding: bit 31 = down tile, bits 30..12 = tile row.  A gate/up item keeps its
+// column tile in bits 11..0.  A down item keeps its column tile in bits 11..4 and, in bits
+// 3..0, which of the tile's split_k parts it is: part p accumulates the K steps
+// [p*nk/split_k, (p+1)*nk/split_k) of the nk = F/kTileK steps, and the part that finishes
+// last adds all parts in part order and writes the tile.
 constexpr uint32_t kItemDown = 0x80000000u;
 constexpr int kItemRowShift = 12;
 constexpr uint32_t kItemColMask = 0xFFFu;
+constexpr int kDownColShift = 4;
+constexpr uint32_t kDownColMask = 0xFFu;
+constexpr uint32_t kDownPartMask = 0xFu;
 constexpr int32_t kMaxTileRows = 1 << 19;
 constexpr int32_t kMaxColTiles = 1 << 12;
+constexpr int32_t kMaxDownColTiles = 1 << 8;
+constexpr int32_t kMaxSplitK = 16;
 
 struct TileRow {
   int32_t expert;      // local expert index
@@ -38,15 +47,17 @@ struct Segment {
   int32_t slot0;       // slot of the first row in the receive buffer
   int32_t flag_begin;  // first ready flag the segment waits for
   int32_t flag_count;  // consecutive flags it waits for
-  int32_t ready_pos;   // schedule position of the last down tile it needs
-  int32_t nbands;      // bands it covers (1 for first/last segments)
+  int32_t ready_pos;   // schedule position of the last down item it needs
+  int32_t npieces;     // tile-row pieces of its group it covers (1 for first/last segments)
 };
 
-struct Band {
+// One owner group: the rows of one local expert that came from one source rank, contiguous
+// in the padded layout.
+struct Group {
   int32_t expert;
-  int32_t lrow0;
-  int32_t nvalid;
-  int32_t dst_rank;    // -1 for a band of padding only
+  int32_t lrow0;       // first logical row
+  int32_t rows;
+  int32_t dst_rank;    // the source rank the rows return to
 };
 
 // Device-side counters of one run; the queue heads are zeroed by the init kernel.
@@ -58,8 +69,10 @@ struct RunCounters {
   uint64_t poll_iters;      // consumer poll iterations
   uint64_t wait_ticks;      // consumer wait time, 100 MHz ticks
   uint32_t down_next;       // down-projection work queue head
+  uint32_t gu_active;       // gate/up workgroups that claimed at least one tile
+  uint32_t down_active;     // down workgroups that claimed at least one tile
   uint32_t pad0;
-  uint64_t pad[3];
+  uint64_t pad[2];
 };
 
 }  // namespace moe

@@ -48,9 +48,9 @@ class DeviceWorkload:
         return [b.cpu().numpy().view(np.uint16) for b in self.bufs]
 
 
-def make_stage(wl, band_rows=0, mgb=1, flags=B.MOE_LOCAL_DIRECT, watchdog_ms=0, max_rows=None):
+def make_stage(wl, band_rows=0, mgb=1, flags=B.MOE_LOCAL_DIRECT, watchdog_ms=0, max_rows=None, split_k=0):
     return B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, max_rows or max(wl.rows, 1), band_rows, mgb,
-                      flags, watchdog_ms)
+                      flags, watchdog_ms, split_k)
 
 
 def oracle_bufs(wl, extra_rows: int = 0, threads: int = 0):

@@ -2,6 +2,7 @@
 import ctypes
 import os
 import re
+import subprocess
 
 import pytest
 
@@ -26,11 +27,34 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
 
 
-def test_struct_sizes_match_header_layout():
-    # int32 x 9 + uint32 = 40 bytes; stats and plan-info contain int64 fields (8-byte aligned)
-    assert ctypes.sizeof(B.moe_stage_config_t) == 40
-    assert ctypes.sizeof(B.moe_stage_stats_t) == 4 * 8 + 9 * 4 + 4 + 8 + 2 * 8  # 9 int32 + pad
-    assert ctypes.sizeof(B.moe_plan_info_t) == 10 * 4 + 4 * 8
+def _c_layout(tmp_path, struct, fields):
+    """sizeof and offsetof of `fields` in `struct` as the C compiler lays it out from the header."""
+    src = tmp_path / "layout.c"
+    body = "".join(f'  printf("%zu\\n", offsetof({struct}, {f}));\n' for f in fields)
+    src.write_text(f'#include <stddef.h>\n#include <stdio.h>\n#include "moe_stage.h"\n'
+                   f'int main(void) {{\n  printf("%zu\\n", sizeof({struct}));\n{body}  return 0;\n}}\n')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    vals = [int(v) for v in subprocess.run([str(exe)], check=True, capture_output=True,
+                                           text=True).stdout.split()]
+    return vals[0], vals[1:]
+
+
+@pytest.mark.parametrize("cname, cls", [("moe_stage_config_t", B.moe_stage_config_t),
+                                        ("moe_stage_stats_t", B.moe_stage_stats_t),
+                                        ("moe_stage_times_t", B.moe_stage_times_t),
+                                        ("moe_plan_info_t", B.moe_plan_info_t)])
+def test_struct_layout_matches_header(tmp_path, cname, cls):
+    fields = [f for f, _ in cls._fields_]
+    size, offsets = _c_layout(tmp_path, cname, fields)
+    assert ctypes.sizeof(cls) == size
+    assert [getattr(cls, f).offset for f in fields] == offsets
+
+
+def test_unknown_config_flags_rejected():
+    with pytest.raises(B.MoeError) as ei:
+        B.moe_stage_create(B.make_config(256, 512, 2, 4, 0, 128, flags=1 << 20))
+    assert ei.value.code == B.MOE_EINVAL
 
 
 def test_create_without_gpu_fails_loudly():

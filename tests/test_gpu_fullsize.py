@@ -15,6 +15,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 BENCH_CU_SPLIT = 8
+BENCH_FLAGS = B.MOE_LOCAL_DIRECT | B.MOE_SHARED_CUS   # bench.py's default mode, on its own stream
 SAMPLE_ROWS = 24
 
 
@@ -30,11 +31,15 @@ def test_fullsize_sampled(name):
     wl = make_workload(name)
     log(f"full-size {name}: rows={wl.rows}")
     dw = DeviceWorkload(torch, wl)
-    with make_stage(wl) as st:
+    side = torch.cuda.Stream()
+    with make_stage(wl, flags=BENCH_FLAGS) as st:
         dw.fill()
-        st.run(*dw.args(), cu_split=BENCH_CU_SPLIT)
+        torch.cuda.synchronize()
+        st.run(*dw.args(), cu_split=BENCH_CU_SPLIT, stream=side)
+        torch.cuda.synchronize()
         stats = st.query()
-        log(f"full-size {name}: overlapped done, segments={stats['n_segments']} tiles={stats['n_tile_rows']}")
+        log(f"full-size {name}: overlapped done, segments={stats['n_segments']} tiles={stats['n_tile_rows']} "
+            f"split_k={stats['split_k']} workgroups={stats['gu_workgroups']}/{stats['down_workgroups']}")
         assert stats["timeout"] == 0
         # placement on every row: exactly the routed slots are written
         for r in range(wl.R):
@@ -43,7 +48,9 @@ def test_fullsize_sampled(name):
             assert np.array_equal(written_mask(dw.bufs[r]), want), f"rank {r} placement"
         over = [b.clone() for b in dw.bufs]
         dw.fill()
-        st.run_serial(*dw.args())
+        torch.cuda.synchronize()
+        st.run_serial(*dw.args(), stream=side)
+        torch.cuda.synchronize()
         st.query()
         for a, b in zip(over, dw.bufs):
             assert torch.equal(a, b), "serial and overlapped differ"

@@ -125,6 +125,60 @@ def test_poison_mode_catches_no_early_copy():
             compare(out, ref)
 
 
+@pytest.mark.parametrize("split_k", [2, 3, 5, 16])
+def test_split_k_down_tiles(split_k):
+    """Down tiles split into K parts (18 K steps here, so parts of 1..9 steps, uneven for 5 and 16):
+    within tolerance of the oracle, bitwise equal between the overlapped and the serial path of
+    one handle (the parts are added in part order whichever part finishes last), and poisoned
+    staging shows no tile was published before its last part."""
+    log(f"split_k={split_k}")
+    wl = make_workload("tiny", owner=2, overrides=dict(RAGGED, T_r=1024))
+    dw = DeviceWorkload(torch, wl)
+    ref = oracle_bufs(wl)
+    with make_stage(wl, band_rows=16, flags=B.MOE_LOCAL_DIRECT | B.MOE_POISON, split_k=split_k) as st:
+        out, stats = run_overlapped(dw, st, cu_split=8)
+        assert stats["split_k"] == split_k and stats["timeout"] == 0
+        assert stats["n_down_items"] == stats["n_tile_rows"] * 2 * split_k
+        compare(out, ref)
+        again, _ = run_overlapped(dw, st, cu_split=8)
+        ser = run_serial(dw, st)
+        for a, b, c in zip(out, again, ser):
+            assert np.array_equal(a, b) and np.array_equal(a, c)
+    with make_stage(wl, band_rows=16, split_k=1) as st:
+        whole, _ = run_overlapped(dw, st, cu_split=8)
+    compare(whole, ref)
+
+
+@pytest.mark.parametrize("local_direct", [True, False])
+def test_shared_cus_matches_partitioned(local_direct):
+    """MOE_SHARED_CUS: the producer also runs on the consumer's CUs; results are bitwise those
+    of the partitioned launch, and poisoned staging shows no copy ran ahead of its flag."""
+    log(f"shared cus local_direct={local_direct}")
+    wl = make_workload("tiny", owner=1, overrides=dict(RAGGED, T_r=2048))
+    dw = DeviceWorkload(torch, wl)
+    ref = oracle_bufs(wl)
+    base = B.MOE_LOCAL_DIRECT if local_direct else 0
+    with make_stage(wl, band_rows=16, flags=base) as st:
+        part, _ = run_overlapped(dw, st, cu_split=8)
+    compare(part, ref)
+    side = torch.cuda.Stream()
+    with make_stage(wl, band_rows=16, flags=base | B.MOE_SHARED_CUS | B.MOE_POISON) as st:
+        # Null stream: the producer forks to the handle's stream.  Created stream: the
+        # producer runs on it directly, beside the consumer's CU-masked stream.
+        for stream, split in ((None, 1), (None, 8), (side, 8), (side, 32)):
+            dw.fill()
+            torch.cuda.synchronize()
+            st.run(*dw.args(), cu_split=split, stream=stream)
+            torch.cuda.synchronize()
+            out = dw.host_bufs()
+            stats = st.query()
+            assert stats["timeout"] == 0
+            assert stats["producer_grid"] >= 256 and stats["consumer_cus"] >= 8
+            compare(out, ref)
+            for a, b in zip(out, part):
+                assert np.array_equal(a, b)
+
+
 @pytest.mark.parametrize("kind", ["identity", "zero_w1", "zero_w3", "zero_w2"])
 def test_special_weights(kind):
     wl = make_workload("tiny", owner=0, weights=kind)

@@ -19,8 +19,8 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 TILE_M = 256
 
 
-def cfg_for(H, F, E_l, R, self_rank, max_rows, band_rows=32, mgb=1, flags=B.MOE_LOCAL_DIRECT):
-    return B.make_config(H, F, E_l, R, self_rank, max_rows, band_rows, mgb, flags)
+def cfg_for(H, F, E_l, R, self_rank, max_rows, band_rows=32, mgb=1, flags=B.MOE_LOCAL_DIRECT, split_k=0):
+    return B.make_config(H, F, E_l, R, self_rank, max_rows, band_rows, mgb, flags, down_split_k=split_k)
 
 
 def routing_from_groups(groups, E_l, R):
@@ -39,10 +39,12 @@ def routing_from_groups(groups, E_l, R):
 
 
 def decode(items):
+    """(down, tile row, column tile, K part) of each work item."""
     down = (items >> 31) & 1
     t = (items >> 12) & ((1 << 19) - 1)
-    col = items & 0xFFF
-    return down.astype(int), t.astype(int), col.astype(int)
+    col = np.where(down == 1, (items >> 4) & 0xFF, items & 0xFFF)
+    part = np.where(down == 1, items & 0xF, 0)
+    return down.astype(int), t.astype(int), col.astype(int), part.astype(int)
 
 
 def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True, local_direct=True):
@@ -64,25 +66,34 @@ def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True,
         assert np.all(e_of_row[rx[seg]] == e)
         assert nvalid == valid[seg].sum()
         assert has_remote == int(np.any(valid[seg] & (rank[seg] != self_rank)))
-    # items: each gate/up and down tile exactly once; down tiles after all gate/up of their row
-    down, t, col = decode(p["items"])
+    # items: each gate/up tile and each K part of each down tile exactly once
+    down, t, col, part = decode(p["items"])
+    S = info["split_k"]
     n_tr = len(tr)
     gu_pos = {}
-    for pos, (d, ti, c) in enumerate(zip(down, t, col)):
-        key = (d, ti, c)
+    for pos, (d, ti, c, k) in enumerate(zip(down, t, col, part)):
+        key = (d, ti, c, k)
         assert key not in gu_pos
         gu_pos[key] = pos
-    assert len(gu_pos) == n_tr * (info["gu_tiles_per_row"] + info["down_tiles_per_row"])
-    # two launches: every gate/up tile precedes every down tile
+    assert len(gu_pos) == n_tr * (info["gu_tiles_per_row"] + info["down_tiles_per_row"] * S)
+    assert info["n_down_items"] == n_tr * info["down_tiles_per_row"] * S
+    # two launches: every gate/up tile precedes every down item
     assert np.all(down[:info["n_gu_items"]] == 0) and np.all(down[info["n_gu_items"]:] == 1)
+    # the K parts of a down tile are adjacent and in part order
+    dn = slice(info["n_gu_items"], None)
+    assert np.array_equal(part[dn], np.tile(np.arange(S), len(part[dn]) // S))
+    assert np.all(t[dn][::S, None] == t[dn].reshape(-1, S)) and np.all(col[dn][::S, None] == col[dn].reshape(-1, S))
     if not overlapped:
         assert info["n_band_padding"] == 0 and info["n_segments"] == 0
         return
-    # bands: single destination, remote groups band-aligned and first, local group last
-    bands = p["bands"]
-    for e, l0, nvalid, dst in bands:
-        seg = slice(l0, l0 + nvalid)
-        assert np.all(rank[seg] == dst)
+    # owner groups: one source rank each, every routed row in exactly one group
+    groups = p["groups"]
+    in_group = np.zeros(len(rank), int)
+    for e, l0, nrows, dst in groups:
+        seg = slice(l0, l0 + nrows)
+        assert nrows > 0 and np.all(rank[seg] == dst) and np.all(e_of_row[rx[seg]] == e)
+        in_group[seg] += 1
+    assert np.array_equal(in_group, valid.astype(int))
     E_l = len(off) - 1
     for e in range(E_l):
         te = tr[tr[:, 0] == e]
@@ -110,17 +121,19 @@ def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True,
     for dst, nrows, y0, s0, fb, fc, rp, nb in segs:
         assert nrows > 0
         assert np.all(rank[y0:y0 + nrows] == dst)
+        # a segment spans at most its pieces' tile rows: nb pieces cover at most nb tile rows
+        assert (y0 + nrows - 1) // TILE_M - y0 // TILE_M + 1 <= nb
         assert np.array_equal(lslot[y0:y0 + nrows], s0 + np.arange(nrows))
         covered[y0:y0 + nrows] += 1
         t0, t1 = y0 // TILE_M, (y0 + nrows - 1) // TILE_M
         dpr = info["down_tiles_per_row"]
         assert fb == t0 * dpr and fc == (t1 - t0 + 1) * dpr
-        assert rp == max(gu_pos[(1, ti, n)] for ti in range(t0, t1 + 1) for n in range(dpr))
+        assert rp == max(gu_pos[(1, ti, n, S - 1)] for ti in range(t0, t1 + 1) for n in range(dpr))
         assert 1 <= nb <= max(mgb, 1)
     need = valid & ((rank != self_rank) | (not local_direct))
     assert np.array_equal(covered, need.astype(int))
     assert np.all(np.diff(segs[:, 6]) >= 0) if len(segs) else True
-    # first and last segments of every (expert, destination) group are a single band
+    # first and last segments of every (expert, destination) group are a single tile-row piece
     group_of = {}
     for s_idx, (dst, nrows, y0, *_rest) in enumerate(segs):
         e = int(tr[y0 // TILE_M, 0])
@@ -140,16 +153,17 @@ def test_golden_schedule_example():
     p = B.moe_plan_build(cfg, off, src, slot, rr)
     check_plan(p, off, src, slot, me, R, tb, 1)
     assert p["tile_rows"][:, 0].tolist() == g["expected_tile_row_experts"]
-    down, t, col = decode(p["items"])
+    down, t, col, _ = decode(p["items"])
     order = []
     for ti in t[down == 0]:
         if ti not in order:
             order.append(int(ti))
     assert order == g["expected_tile_row_order"]
-    bands = p["bands"]
+    pg = p["groups"]
     for e_glob, want in g["expected_remote_bands"].items():
         e = glob.index(int(e_glob))
-        assert int(np.sum((bands[:, 0] == e) & (bands[:, 3] != me))) == want
+        remote = pg[(pg[:, 0] == e) & (pg[:, 3] != me)]
+        assert int(np.sum((remote[:, 2] + tb - 1) // tb)) == want
     # the group from rank 3 is padded up to the band height
     for e_glob, want in g["expected_padding_from_rank3"].items():
         e = glob.index(int(e_glob))
@@ -157,12 +171,12 @@ def test_golden_schedule_example():
         assert (-n3) % tb == want
 
 
-@pytest.mark.parametrize("name,band_rows,mgb", [("tiny", 16, 1), ("tiny", 32, 2), ("fine", 32, 2),
-                                                ("large_fine", 16, 1), ("mixtral_zipf", 64, 2)])
-def test_plan_properties_generated(name, band_rows, mgb):
+@pytest.mark.parametrize("name,band_rows,mgb,split_k", [("tiny", 16, 1, 0), ("tiny", 32, 2, 3), ("fine", 32, 2, 0),
+                                                        ("large_fine", 16, 1, 2), ("mixtral_zipf", 64, 2, 0)])
+def test_plan_properties_generated(name, band_rows, mgb, split_k):
     ov = {"T_r": 512} if name != "tiny" else None
     wl = make_workload(name, weights=None, overrides=ov)
-    cfg = cfg_for(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, band_rows, mgb)
+    cfg = cfg_for(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, band_rows, mgb, split_k=split_k)
     p = B.moe_plan_build(cfg, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.return_rows)
     check_plan(p, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.self_rank, wl.R, band_rows, mgb)
     ps = B.moe_plan_build(cfg, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.return_rows, overlapped=False)
@@ -233,6 +247,28 @@ def test_validation_codes_via_plan():
     assert code(c=cfg_for(wl.H + 32, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows)) == B.MOE_EUNSUPPORTED
     assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, wl.R, wl.rows)) == B.MOE_EINVAL
     assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, 0, wl.rows, band_rows=48)) == B.MOE_EINVAL
+    assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, 0, wl.rows, split_k=17)) == B.MOE_EINVAL
+    assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, 0, wl.rows, split_k=wl.F // 32 + 1)) == B.MOE_EINVAL
+    assert code(c=cfg_for(65536 + 64, wl.F, wl.E_l, wl.R, 0, wl.rows)) == B.MOE_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("ffn,want", [(512, 1), (1408, 1), (2048, 1), (6144, 2), (9216, 3), (14336, 4), (32768, 4)])
+def test_default_split_k(ffn, want):
+    """Default K parts per down tile: one per 3072 of ffn, between 1 and 4."""
+    off = np.array([0, 4], np.int32)
+    p = B.moe_plan_build(cfg_for(256, ffn, 1, 1, 0, 4), off, np.zeros(4, np.int32),
+                         np.arange(4, dtype=np.int32), np.array([4], np.int64))
+    assert p["info"]["split_k"] == want
+    assert p["info"]["n_down_items"] == want
+
+
+def test_split_k_part_ranges_cover_k():
+    """The K steps [p*nk/S, (p+1)*nk/S) of the S parts tile [0, nk) with no gap or overlap."""
+    for nk in (2, 3, 16, 18, 44, 448):
+        for S in range(1, min(16, nk) + 1):
+            bounds = [p * nk // S for p in range(S + 1)]
+            assert bounds[0] == 0 and bounds[-1] == nk
+            assert all(b1 > b0 for b0, b1 in zip(bounds, bounds[1:]))
 
 
 def test_band_group_rasterisation_reuses_weights():
@@ -240,8 +276,21 @@ def test_band_group_rasterisation_reuses_weights():
     wl = make_workload("mixtral", weights=None, overrides={"T_r": 2048})
     cfg = cfg_for(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, 32)
     p = B.moe_plan_build(cfg, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.return_rows)
-    down, t, col = decode(p["items"])
+    down, t, col, _ = decode(p["items"])
     gu_t, gu_c = t[down == 0], col[down == 0]
     # consecutive gate/up tiles share the weight column tile far more often than they change it
     same_col = np.mean(gu_c[1:] == gu_c[:-1])
     assert same_col > 0.5
+
+
+@pytest.mark.parametrize("name", ["mixtral", "mixtral_zipf", "fine", "large_fine"])
+def test_default_layout_costs_no_extra_tiles(name):
+    """With the default tb_M = 1 the owner-grouped layout has exactly the tile rows of the
+    expert-contiguous baseline: the overlapped path does no extra MFMA work."""
+    wl = make_workload(name, weights=None)
+    cfg = B.make_config(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows)
+    po = B.moe_plan_build(cfg, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.return_rows)
+    ps = B.moe_plan_build(cfg, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.return_rows, overlapped=False)
+    assert po["info"]["band_rows"] == 1 and po["info"]["n_band_padding"] == 0
+    assert po["info"]["n_tile_rows"] == ps["info"]["n_tile_rows"]
+    check_plan(po, wl.expert_offsets, wl.row_src_rank, wl.row_slot, wl.self_rank, wl.R, 1, 1)
