@@ -2,21 +2,26 @@
 """Benchmark of the MI355X MoE expert stage (one expert-parallel rank, one GPU).
 
 A step is one overlapped expert-stage run (moe_stage_run): host plan build and
-upload, the persistent gated-FFN producer with tile-level ready flags and the
-CU-masked consumer copying finished segments into the per-source-rank receive
-buffers.  Inputs (activations, weights, receive buffers) are resident in HBM
-before the timed region; the routing arrays are host inputs by design of the C
-ABI, so each step re-validates and re-uploads the plan.
+upload, the persistent gated-FFN producer (gate/up launch, then the signaling
+down launch) and the CU-confined consumer copying finished segments into the
+per-source-rank receive buffers.  Inputs (activations, weights, receive
+buffers) are resident in HBM before the timed region; the routing arrays are
+host inputs by design of the C ABI, so each step re-validates and re-uploads
+the plan.
 
 Prints one JSON line.  ``value`` is the stage's algorithmic bf16 throughput
-(6*H*F flops per routed row, padding excluded) in TFLOP/s; ``ms_per_step`` is
-the expert-stage time; ``overlap_speedup`` is serial time / overlapped time.
+(6*H*F flops per routed row, padding excluded) in TFLOP/s on the headline
+workload; ``ms_per_step`` is its expert-stage time; ``overlap_speedup`` is
+serial time / overlapped time.  ``workloads`` holds the same figures and the
+consumer CU-split sweep (both CU modes) for every workload measured.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -29,6 +34,8 @@ if ROOT not in sys.path:
 METRIC = "MoE expert-stage µs + bf16 MFMA TFLOP/s vs peak; overlap speedup vs serial"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA peak
 PEAK_HBM_GBS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_19539_amd", "csrc", "kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "producer_mixtral_traffic.md")
 
 DESCRIPTIONS = {
     "tiny": "tiny: H256 F512, SiLU-gated FFN, 8 experts top-2, 4 source ranks x 64 tokens, 2 local experts",
@@ -49,19 +56,21 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=30)
-    ap.add_argument("--workload", default="mixtral", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--workload", default="mixtral", choices=sorted(DESCRIPTIONS), help="headline workload")
+    ap.add_argument("--extra-workloads", default="mixtral_zipf,fine,large_fine",
+                    help="further workloads measured into 'workloads' ('' = none)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cu-split", type=int, default=8, help="consumer compute units")
-    ap.add_argument("--band-rows", type=int, default=0, help="tb_M of the row layout (0 = 1, no alignment)")
-    ap.add_argument("--split-k", type=int, default=0, help="K parts per down tile (0 = library default)")
-    ap.add_argument("--mgb", type=int, default=1, help="tile-row pieces per middle transfer segment")
+    ap.add_argument("--cu-split", type=int, default=32, help="consumer compute units")
     ap.add_argument("--mode", choices=["shared", "partitioned"], default="shared",
                     help="shared: the producer keeps every CU and the consumer runs beside it on its "
                          "cu_split CUs; partitioned: the consumer's CUs are reserved for it")
+    ap.add_argument("--band-rows", type=int, default=0, help="tb_M of the row layout (0 = 1, no alignment)")
+    ap.add_argument("--split-k", type=int, default=0, help="K parts per down tile (0 = library default)")
+    ap.add_argument("--mgb", type=int, default=1, help="tile-row pieces per middle transfer segment")
     ap.add_argument("--sweep", default="4,8,16,32",
                     help="CU splits for the overlap-speedup sweep, both modes ('' = none)")
     ap.add_argument("--only", choices=["all", "serial", "overlapped"], default="all",
-                    help="run only one path (counter collection serialises kernels, so use 'serial' there)")
+                    help="run only one path of the headline workload (counter collection)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     return ap.parse_args()
@@ -92,6 +101,103 @@ def cpu_baseline(wl, target_s):
                       f"would take ~{dt * wl.rows / n:.0f} s on these cores"}
 
 
+def stored_traffic():
+    """HBM bytes per gate/up launch from the committed counter summary, if it was taken on the
+    current kernel source (its sha256 is recorded next to the figure); else None."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    m_b = re.search(r"^traffic_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
+    m_h = re.search(r"^kernel_sha256:\s*([0-9a-f]{64})", text, re.M)
+    if not m_b or not m_h:
+        return None
+    cur = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    return float(m_b.group(1)) if cur == m_h.group(1) else None
+
+
+class Bench:
+    """One workload resident on the GPU, with a handle per CU mode on a dedicated stream."""
+
+    def __init__(self, torch, B, wl, args):
+        self.torch, self.B, self.wl, self.args = torch, B, wl, args
+
+        def dev(a):
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to("cuda")
+
+        self.x, self.w1, self.w3, self.w2 = dev(wl.dispatched_x), dev(wl.w1), dev(wl.w3), dev(wl.w2)
+        self.bufs = [torch.zeros((int(n), wl.H), dtype=torch.int16, device="cuda") for n in wl.return_rows]
+        self.run_args = (self.x, wl.expert_offsets, wl.row_src_rank, wl.row_slot, self.w1, self.w3, self.w2,
+                         self.bufs, wl.return_rows)
+        base = B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING
+        self.stages = {m: B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, args.mgb,
+                                     base | (B.MOE_SHARED_CUS if m == "shared" else 0), 0, args.split_k)
+                       for m in ("shared", "partitioned")}
+        torch.cuda.synchronize()
+        # The stage runs on a stream of its own, as in a serving loop (on the legacy null stream
+        # the shared-CU producer would have to fork to a second queue; see moe_stage_run).
+        self.stream = torch.cuda.Stream()
+        self.timeouts = []
+
+    def close(self):
+        for s in self.stages.values():
+            s.close()
+        self.torch.cuda.synchronize()
+
+    def timed(self, mode, path, cu_split, steps, warmup):
+        """W untimed steps, then exactly `steps` timed steps bracketed by device synchronisation."""
+        torch, stg = self.torch, self.stages[mode]
+        if path == "serial":
+            fn = lambda: stg.run_serial(*self.run_args, stream=self.stream)
+        else:
+            fn = lambda: stg.run(*self.run_args, cu_split=cu_split, stream=self.stream)
+        for _ in range(warmup):
+            fn()
+        stg.query(check=False)
+        stg.times(reset=True)
+        torch.cuda.synchronize()
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(self.stream)
+        for _ in range(steps):
+            fn()
+        end.record(self.stream)
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(end) / steps
+        st = stg.query(check=False)
+        if st["rc"] != 0:
+            msg = self.B.moe_stage_last_error(stg.h)
+            log(f"ERROR: {msg} -- timing invalid")
+            self.timeouts.append(msg)
+        tm = stg.times(reset=True)
+        runs = max(tm["runs"], 1)
+        return {"ms": ms, "stats": st, "producer_ms": tm["producer_ms"] / runs,
+                "gate_up_ms": tm["gate_up_ms"] / runs, "consumer_ms": tm["consumer_ms"] / runs,
+                "scatter_ms": tm["scatter_ms"] / runs}
+
+
+def summarize(wl, ser, ovl, sweep):
+    """Per-workload figures: stage times, producer launches, throughput against the bf16 peak."""
+    flops = wl.flops()
+    out = {"routed_rows": wl.rows, "gflop": flops / 1e9}
+    for key, r in (("serial", ser), ("overlapped", ovl)):
+        if r is None:
+            continue
+        gu = r["gate_up_ms"]
+        dn = r["producer_ms"] - gu
+        out[key] = {"stage_us": r["ms"] * 1e3, "tflops": flops / (r["ms"] * 1e-3) / 1e12,
+                    "producer_us": r["producer_ms"] * 1e3, "gate_up_us": gu * 1e3, "down_us": dn * 1e3,
+                    "producer_frac_of_peak": flops / (r["producer_ms"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+        if key == "serial":
+            out[key]["scatter_us"] = r["scatter_ms"] * 1e3
+        else:
+            out[key]["consumer_us"] = r["consumer_ms"] * 1e3
+    if ser is not None and ovl is not None:
+        out["overlap_speedup"] = ser["ms"] / ovl["ms"]
+    if sweep:
+        out["cu_split_sweep"] = sweep
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -104,124 +210,95 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    log(f"generating workload {args.workload} seed {args.seed}")
-    wl = make_workload(args.workload, seed=args.seed)
-    log(f"rows={wl.rows} H={wl.H} F={wl.F} E_l={wl.E_l} R={wl.R}")
-
-    def dev(a):
-        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to("cuda")
-
-    x, w1, w3, w2 = dev(wl.dispatched_x), dev(wl.w1), dev(wl.w3), dev(wl.w2)
-    bufs = [torch.zeros((int(n), wl.H), dtype=torch.int16, device="cuda") for n in wl.return_rows]
-    run_args = (x, wl.expert_offsets, wl.row_src_rank, wl.row_slot, w1, w3, w2, bufs, wl.return_rows)
-    flops = wl.flops()
-    base_flags = B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING
-    stages = {m: B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, args.mgb,
-                            base_flags | (B.MOE_SHARED_CUS if m == "shared" else 0), 0, args.split_k)
-              for m in ("shared", "partitioned")}
-    stage = stages[args.mode]
-    # The stage runs on a stream of its own, as in a serving loop (the legacy null stream would
-    # force the shared-CU producer onto a second queue; see moe_stage_run).
-    torch.cuda.synchronize()
-    stream = torch.cuda.Stream()
-    timeouts = []
-
-    def timed(stg, fn, steps, warmup):
-        for _ in range(warmup):
-            fn()
-        stg.query(check=False)
-        stg.times(reset=True)
-        torch.cuda.synchronize()
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        start.record(stream)
-        for _ in range(steps):
-            fn()
-        end.record(stream)
-        torch.cuda.synchronize()
-        ms = start.elapsed_time(end) / steps
-        st = stg.query(check=False)
-        if st["rc"] != 0:
-            log(f"ERROR: {B.moe_stage_last_error(stg.h)} -- timing invalid")
-            timeouts.append(B.moe_stage_last_error(stg.h))
-        tm = stg.times(reset=True)
-        return ms, st, tm
-
+    sweep_cs = [int(v) for v in args.sweep.split(",") if v]
+    names = [args.workload] + [w for w in args.extra_workloads.split(",") if w and w != args.workload]
     out = {"metric": METRIC, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic (seeded generator, random-init weights N(0,0.02^2), activations N(0,1))"}
-    res = {}
-    if args.only in ("all", "serial"):
-        log("timing serial baseline")
-        ms_s, st_s, tm_s = timed(stage, lambda: stage.run_serial(*run_args, stream=stream), args.steps,
-                                 args.warmup)
-        res["serial"] = dict(ms=ms_s, producer_ms=tm_s["producer_ms"] / tm_s["runs"],
-                             gate_up_ms=tm_s["gate_up_ms"] / tm_s["runs"],
-                             scatter_ms=tm_s["scatter_ms"] / tm_s["runs"], stats=st_s)
-        log(f"serial: {ms_s * 1e3:.1f} us/step, producer {res['serial']['producer_ms'] * 1e3:.1f} us "
-            f"(gate/up {res['serial']['gate_up_ms'] * 1e3:.1f} us), scatter {res['serial']['scatter_ms'] * 1e3:.1f} us")
-    if args.only in ("all", "overlapped"):
-        log(f"timing overlapped stage, {args.mode} CUs, cu_split={args.cu_split}")
-        ms_o, st_o, tm_o = timed(stage, lambda: stage.run(*run_args, cu_split=args.cu_split, stream=stream),
-                                 args.steps, args.warmup)
-        res["overlapped"] = dict(ms=ms_o, producer_ms=tm_o["producer_ms"] / tm_o["runs"],
-                                 gate_up_ms=tm_o["gate_up_ms"] / tm_o["runs"],
-                                 consumer_ms=tm_o["consumer_ms"] / tm_o["runs"], stats=st_o)
-        log(f"overlapped: {ms_o * 1e3:.1f} us/step, producer {res['overlapped']['producer_ms'] * 1e3:.1f} us "
-            f"(gate/up {res['overlapped']['gate_up_ms'] * 1e3:.1f} us), "
-            f"consumer {res['overlapped']['consumer_ms'] * 1e3:.1f} us, segments {st_o['n_segments']}, "
-            f"consumer wait {st_o['wait_ticks'] / 100:.0f} us (summed), polls {st_o['poll_iters']}")
-
-    main_path = "overlapped" if "overlapped" in res else "serial"
-    r = res[main_path]
-    out["value"] = flops / (r["ms"] * 1e-3) / 1e12
-    out["ms_per_step"] = r["ms"]
-    out["expert_stage_us"] = r["ms"] * 1e3
-    if "serial" in res:
-        out["serial_stage_us"] = res["serial"]["ms"] * 1e3
-    if "serial" in res and "overlapped" in res:
-        out["overlap_speedup"] = res["serial"]["ms"] / res["overlapped"]["ms"]
-    st = r["stats"]
-    out["config"] = {"workload": DESCRIPTIONS[args.workload], "routed_rows": wl.rows, "path": main_path,
-                     "cu_split": args.cu_split, "consumer_cus": st.get("consumer_cus", 0),
-                     "cu_mode": args.mode,
-                     "band_rows": stage.cfg.band_rows or 1, "mid_segment_pieces": args.mgb,
-                     "down_split_k": st.get("split_k", 0),
-                     "padding_rows": int(st["n_logical_rows"] - st["n_valid"]),
-                     "band_padding_rows": int(st["n_band_padding"]), "plan_us": round(st["plan_us"], 1),
-                     "seed": args.seed}
-    # Dominant kernel: the producer (all MFMA work).  Its duration comes from HIP events the library
-    # records on the producer's own stream around every launch in the timed region.
-    prod_ms = r["producer_ms"]
-    achieved = flops / (prod_ms * 1e-3) / 1e12
-    out["producer_us"] = prod_ms * 1e3
-    out["producer_gate_up_us"] = r["gate_up_ms"] * 1e3
-    out["producer_down_us"] = (prod_ms - r["gate_up_ms"]) * 1e3
-    out["roofline"] = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                       "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                       "kernel": "moe::producer_kernel (gate/up launch + down launch)",
-                       "flops_per_launch": flops}
-    if "overlapped" in res:
-        cons_bytes = 4.0 * wl.H * st["n_remote_rows"]
-        out["consumer"] = {"us": res["overlapped"]["consumer_ms"] * 1e3, "bytes": cons_bytes,
-                           "busy_GBps_lower_bound": cons_bytes / (res["overlapped"]["consumer_ms"] * 1e-3) / 1e9,
-                           "flag_wait_us_summed": st["wait_ticks"] / 100.0, "poll_iters": int(st["poll_iters"]),
-                           "segments": int(st["n_segments"])}
-    if args.sweep and "serial" in res and args.only == "all":
+    per_wl = {}
+    timeouts = []
+    for wi, name in enumerate(names):
+        headline = wi == 0
+        log(f"generating workload {name} seed {args.seed}")
+        wl = make_workload(name, seed=args.seed)
+        log(f"{name}: rows={wl.rows} H={wl.H} F={wl.F} E_l={wl.E_l} R={wl.R}")
+        bench = Bench(torch, B, wl, args)
+        steps, warmup = (args.steps, args.warmup) if headline else (max(args.steps // 2, 10),
+                                                                    max(args.warmup // 2, 5))
+        only = args.only if headline else "all"
+        ser = ovl = None
+        if only in ("all", "serial"):
+            ser = bench.timed(args.mode, "serial", 0, steps, warmup)
+            log(f"{name} serial: {ser['ms'] * 1e3:.1f} us (producer {ser['producer_ms'] * 1e3:.1f}, gate/up "
+                f"{ser['gate_up_ms'] * 1e3:.1f}, scatter {ser['scatter_ms'] * 1e3:.1f})")
+        if only in ("all", "overlapped"):
+            ovl = bench.timed(args.mode, "overlapped", args.cu_split, steps, warmup)
+            st = ovl["stats"]
+            log(f"{name} overlapped ({args.mode}, c={args.cu_split}): {ovl['ms'] * 1e3:.1f} us (producer "
+                f"{ovl['producer_ms'] * 1e3:.1f}, gate/up {ovl['gate_up_ms'] * 1e3:.1f}, consumer "
+                f"{ovl['consumer_ms'] * 1e3:.1f}); segments {st['n_segments']}, workgroups "
+                f"{st['gu_workgroups']}/{st['down_workgroups']}")
         sweep = []
-        for c in [int(v) for v in args.sweep.split(",") if v]:
-            for mode, stg in stages.items():
-                ms_c, st_c, _ = timed(stg, lambda: stg.run(*run_args, cu_split=c, stream=stream),
-                                      max(args.steps // 2, 5), max(args.warmup // 2, 2))
-                sweep.append({"cu_split": c, "cu_mode": mode, "consumer_cus": st_c["consumer_cus"],
-                              "stage_us": ms_c * 1e3, "speedup_vs_serial": res["serial"]["ms"] / ms_c})
-                log(f"sweep c={c} {mode}: {ms_c * 1e3:.1f} us, speedup {res['serial']['ms'] / ms_c:.3f}")
-        out["cu_split_sweep"] = sweep
-    for stg in stages.values():
-        stg.close()
+        if sweep_cs and ser is not None and only == "all":
+            for c in sweep_cs:
+                for mode in ("shared", "partitioned"):
+                    r = bench.timed(mode, "overlapped", c, max(steps // 2, 5), max(warmup // 2, 3))
+                    sweep.append({"cu_split": c, "cu_mode": mode, "consumer_cus": r["stats"]["consumer_cus"],
+                                  "stage_us": r["ms"] * 1e3, "speedup_vs_serial": ser["ms"] / r["ms"]})
+                    log(f"{name} sweep c={c} {mode}: {r['ms'] * 1e3:.1f} us, speedup {ser['ms'] / r['ms']:.3f}")
+        per_wl[name] = summarize(wl, ser, ovl, sweep)
+        timeouts += bench.timeouts
+        if headline:
+            main_r = ovl if ovl is not None else ser
+            st = main_r["stats"]
+            out["value"] = wl.flops() / (main_r["ms"] * 1e-3) / 1e12
+            out["ms_per_step"] = main_r["ms"]
+            out["expert_stage_us"] = main_r["ms"] * 1e3
+            if ser is not None:
+                out["serial_stage_us"] = ser["ms"] * 1e3
+            if ser is not None and ovl is not None:
+                out["overlap_speedup"] = ser["ms"] / ovl["ms"]
+            out["config"] = {"workload": DESCRIPTIONS[name], "routed_rows": wl.rows,
+                             "path": "overlapped" if ovl is not None else "serial",
+                             "cu_split": args.cu_split, "consumer_cus": st.get("consumer_cus", 0),
+                             "cu_mode": args.mode, "band_rows": args.band_rows or 1,
+                             "mid_segment_pieces": args.mgb, "down_split_k": st["split_k"],
+                             "padding_rows": int(st["n_logical_rows"] - st["n_valid"]),
+                             "plan_us": round(st["plan_us"], 1), "seed": args.seed}
+            # Dominant kernel: the gate/up launch of the producer (4*H*F flops per routed row, two
+            # thirds of the stage).  Its duration comes from HIP events the library records on the
+            # producer's own stream around every launch in the timed region.
+            gu_flops = 4.0 * wl.H * wl.F * wl.rows
+            gu_ms = main_r["gate_up_ms"]
+            achieved = gu_flops / (gu_ms * 1e-3) / 1e12
+            out["roofline"] = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                               "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                               "traffic": stored_traffic(),
+                               "kernel": "moe::producer_kernel<false, 1> (gate/up launch)",
+                               "flops_per_launch": gu_flops, "launch_us": gu_ms * 1e3}
+            dn_ms = main_r["producer_ms"] - gu_ms
+            dn_flops = 2.0 * wl.H * wl.F * wl.rows
+            out["roofline_down"] = {"bound": "mfma", "achieved": dn_flops / (dn_ms * 1e-3) / 1e12,
+                                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                                    "frac": dn_flops / (dn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                                    "kernel": f"moe::producer_kernel<true, {st['split_k']}> (down launch)",
+                                    "flops_per_launch": dn_flops, "launch_us": dn_ms * 1e3}
+            prod = wl.flops() / (main_r["producer_ms"] * 1e-3) / 1e12
+            out["producer"] = {"us": main_r["producer_ms"] * 1e3, "tflops": prod, "frac": prod / PEAK_BF16_TFLOPS}
+            if ovl is not None:
+                cons_bytes = 4.0 * wl.H * st["n_remote_rows"]
+                out["consumer"] = {"us": ovl["consumer_ms"] * 1e3, "bytes": cons_bytes,
+                                   "busy_GBps_lower_bound": cons_bytes / (ovl["consumer_ms"] * 1e-3) / 1e9,
+                                   "flag_wait_us_summed": st["wait_ticks"] / 100.0,
+                                   "poll_iters": int(st["poll_iters"]), "segments": int(st["n_segments"])}
+            if not args.no_cpu_baseline:
+                log("timing the CPU oracle on a bounded sample")
+                out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        bench.close()
+        del bench, wl
+        torch.cuda.empty_cache()
+    out["workloads"] = per_wl
     out["watchdog_timeouts"] = timeouts
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 

@@ -419,7 +419,9 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   const int c_eff = effective_split(h, cu_split);
   const bool shared = (h->cfg.flags & MOE_SHARED_CUS) != 0;
   const int pgrid = (shared ? h->num_cus : h->num_cus - c_eff) * h->producer_bpc;
-  const int cgrid = c_eff * 2;
+  // Consumer workgroups per CU: two beside a producer workgroup (their registers fill what a
+  // producer wave leaves free), six when the consumer owns its CUs.
+  const int cgrid = c_eff * (shared ? 2 : 6);
   int rc = ensure_streams(h, c_eff);
   if (rc) return rc;
   BlobLayout lay{};

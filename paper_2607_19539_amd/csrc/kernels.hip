@@ -30,6 +30,9 @@ namespace moe {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// Global-memory view of a pointer that was loaded from memory (the receive-buffer table): the
+// compiler cannot infer its address space and would emit flat accesses.
+typedef __attribute__((address_space(1))) u32x4 g_u32x4;
 
 // Operand tiles in LDS: 256 rows x 32 k (bf16) = 16 KiB per operand, 64 bytes per row,
 // weight tile then token tile per stage, four stages in a ring (128 KiB).  Global
@@ -79,6 +82,19 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // pass does not serialise LDS reads behind every in-flight DMA: the pipeline waits for
 // exactly the stage it needs with an explicit vmcnt.  M0 is written right before the
 // load and is not used by any compiler-generated code in the producer.
+// 8 bytes stored as a relaxed agent-scope atomic store: it completes at the device's coherence
+// point, so once every wave's stores have completed (an explicit vmcnt(0) before a barrier)
+// another XCD can read the data after an agent-scope acquire, and the writer needs no L2
+// writeback to publish it.  A relaxed flag store or arrival count then follows.  Callers lay
+// data out so that the 64 lanes of a wave store 512 contiguous bytes (whole cache lines).
+__device__ __forceinline__ void store8_device(void* p, uint64_t v) {
+  __hip_atomic_store((uint64_t*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint64_t pack_f32x2(float lo, float hi) {
+  return (uint64_t)__float_as_uint(lo) | ((uint64_t)__float_as_uint(hi) << 32);
+}
+
 __device__ __forceinline__ void dma16(const uint8_t* sbase, uint32_t voff, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(sbase)
                : "memory");
@@ -299,24 +315,27 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     // Split K: every part stores its fp32 accumulators (in register order, so each thread
     // reads back exactly the positions it wrote) and counts itself in; the part that arrives
     // last reads all parts back and adds them in part order -- a fixed order whichever part
-    // that is -- and writes the tile.
+    // that is -- and writes the tile.  A part tile is 128 slices of 256 threads x 8 bytes:
+    // slice 2b + h holds half h of accumulator block b = (i*4 + j)*4 + q.
     const int tile = t * a.down_per_row + col;
-    const float4* parts = nullptr;
+    constexpr int kPartU64 = kProducerThreads * 128;  // 8-byte elements per part tile
+    const uint64_t* parts = nullptr;
     if constexpr (split) {
-      constexpr int kPartF4 = kProducerThreads * 64;  // float4s per part tile
-      parts = (const float4*)a.partials + (size_t)tile * S * kPartF4;
-      float4* mine = (float4*)a.partials + ((size_t)tile * S + part) * kPartF4;
+      parts = (const uint64_t*)a.partials + (size_t)tile * S * kPartU64;
+      uint64_t* mine = (uint64_t*)a.partials + ((size_t)tile * S + part) * kPartU64 + tid;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            mine[((i * 4 + j) * 4 + q) * kProducerThreads + tid] =
-                float4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-      wait_vm_and_barrier<0>();  // every wave's part stores have completed
+          for (int q = 0; q < 4; ++q) {
+            const f32x16& d = acc[i][j];
+            const int b = (i * 4 + j) * 4 + q;
+            store8_device(mine + (2 * b) * kProducerThreads, pack_f32x2(d[4 * q], d[4 * q + 1]));
+            store8_device(mine + (2 * b + 1) * kProducerThreads, pack_f32x2(d[4 * q + 2], d[4 * q + 3]));
+          }
+      wait_vm_and_barrier<0>();  // every wave's part stores have reached the coherence point
       if (tid == 0) {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         const uint32_t prev =
             __hip_atomic_fetch_add(&a.arrivals[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         *s_last = (prev + 1 == (uint32_t)S) ? 1u : 0u;
@@ -334,15 +353,21 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
       v.y = pack_bf16x2(s.z, s.w);
       *(uint2*)(lds + m * kDownOutStride + nl * 2) = v;
     };
+    // Accumulator block b of part p: its two 8-byte halves, widened back to four floats.
+    auto part_block = [&](const uint64_t* src, int p, int b) {
+      const uint64_t lo = src[(size_t)p * kPartU64 + (2 * b) * kProducerThreads];
+      const uint64_t hi = src[(size_t)p * kPartU64 + (2 * b + 1) * kProducerThreads];
+      return float4{__uint_as_float((uint32_t)lo), __uint_as_float((uint32_t)(lo >> 32)),
+                    __uint_as_float((uint32_t)hi), __uint_as_float((uint32_t)(hi >> 32))};
+    };
     if constexpr (kSplit == 0) {
       // Any part count: blocks b = (i*4 + j)*4 + q indexed at run time, every part read back.
-      const float4* src = parts + tid;
+      const uint64_t* src = parts + tid;
 #pragma unroll 1
       for (int b = 0; b < 64; ++b) {
-        const float4* blk = src + b * kProducerThreads;
-        float4 s = blk[0];
+        float4 s = part_block(src, 0, b);
         for (int p = 1; p < S; ++p) {
-          const float4 v = blk[(size_t)p * kProducerThreads * 64];
+          const float4 v = part_block(src, p, b);
           s.x += v.x;
           s.y += v.y;
           s.z += v.z;
@@ -352,16 +377,15 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
       }
     } else if constexpr (split) {
       // kSplit parts: all parts read back (this part's too: the same values, and no branch
-      // that would serialize the loads), 4 blocks of kSplit loads in flight per step.
-      const float4* src = parts + tid;
+      // that would serialize the loads), 4 blocks of kSplit parts in flight per step.
+      const uint64_t* src = parts + tid;
 #pragma unroll 1
       for (int b0 = 0; b0 < 64; b0 += 4) {
         float4 v[4][kSplit];
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
-          for (int p = 0; p < kSplit; ++p)
-            v[u][p] = src[(size_t)p * kProducerThreads * 64 + (b0 + u) * kProducerThreads];
+          for (int p = 0; p < kSplit; ++p) v[u][p] = part_block(src, p, b0 + u);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           float4 s = v[u][0];
@@ -389,29 +413,51 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
           }
     }
     __syncthreads();
-    // 32 threads store one 512-byte output row; 8 rows per pass.  Rows returning to another
-    // rank go to the staged output Y (the consumer moves them); local rows go straight to
-    // the local receive buffer when the producer writes local rows directly.
+    // Rows returning to another rank go to the staged output Y (the consumer moves them);
+    // local rows go straight to the local receive buffer when the producer writes them
+    // directly.  In a signalled launch a wave stores one 512-byte row (64 lanes x 8 bytes, 4
+    // rows per pass) and the Y rows at device scope, so publishing the tile needs no L2
+    // writeback.  Without signalling, 32 lanes store a row with ordinary 16-byte stores.
     const bool direct = (a.mode & kModeLocalDirect) != 0;
-    const int c16 = tid & 31;
-    const int n = col * kDownTileN + c16 * 8;
+    const bool signal = (a.mode & kModeSignal) != 0;
+    if (signal) {
+      const int c8 = tid & 63;
+      const int n = col * kDownTileN + c8 * 4;
 #pragma unroll 4
-    for (int p = 0; p < kTileM / 8; ++p) {
-      const int m = p * 8 + (tid >> 5);
-      const int lrow = lrow0 + m;
-      const int rank = a.row_rank[lrow];
-      if (rank >= 0 && n < H) {
-        uint16_t* dst = (direct && rank == a.self_rank) ? a.ret[rank] + (int64_t)a.row_slot[lrow] * H
-                                                        : a.y + (int64_t)lrow * H;
-        *(u32x4*)(dst + n) = *(const u32x4*)(lds + m * kDownOutStride + c16 * 16);
+      for (int p = 0; p < kTileM / 4; ++p) {
+        const int m = p * 4 + (tid >> 6);
+        const int lrow = lrow0 + m;
+        const int rank = a.row_rank[lrow];
+        if (rank >= 0 && n < H) {
+          const uint64_t v = *(const uint64_t*)(lds + m * kDownOutStride + c8 * 8);
+          if (direct && rank == a.self_rank)
+            *(__attribute__((address_space(1))) uint64_t*)(a.ret[rank] + (int64_t)a.row_slot[lrow] * H + n) = v;
+          else
+            store8_device(a.y + (int64_t)lrow * H + n, v);
+        }
+      }
+    } else {
+      const int c16 = tid & 31;
+      const int n = col * kDownTileN + c16 * 8;
+#pragma unroll 4
+      for (int p = 0; p < kTileM / 8; ++p) {
+        const int m = p * 8 + (tid >> 5);
+        const int lrow = lrow0 + m;
+        const int rank = a.row_rank[lrow];
+        if (rank >= 0 && n < H) {
+          const u32x4 v = *(const u32x4*)(lds + m * kDownOutStride + c16 * 16);
+          if (direct && rank == a.self_rank)
+            *(g_u32x4*)(a.ret[rank] + (int64_t)a.row_slot[lrow] * H + n) = v;
+          else
+            *(g_u32x4*)(a.y + (int64_t)lrow * H + n) = v;
+        }
       }
     }
-    // Every wave's output stores have completed before wave 0's agent-scope release
-    // publishes the tile (a plain barrier does not wait for other waves' stores).
+    // Every wave's output stores have completed (the staged rows at the coherence point)
+    // before wave 0 raises the flag; a plain barrier does not wait for other waves' stores.
     wait_vm_and_barrier<0>();
-    if ((a.mode & kModeSignal) && (tr.has_remote || !direct)) {
-      if (tid == 0)
-        __hip_atomic_store(&a.flags[tile], a.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    if (signal && (tr.has_remote || !direct)) {
+      if (tid == 0) __hip_atomic_store(&a.flags[tile], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -446,7 +492,7 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
 // (one flag per lane, all lanes must read the current epoch), then the whole
 // workgroup copies rows * H bf16 with 16-byte loads and stores.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kConsumerThreads) void consumer_kernel(ConsumerArgs a) {
+__global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_kernel(ConsumerArgs a) {
   __shared__ int32_t s_seg;
   __shared__ uint32_t s_abort;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -490,19 +536,33 @@ __global__ __launch_bounds__(kConsumerThreads) void consumer_kernel(ConsumerArgs
       }
       break;
     }
+    // The segment is contiguous on both sides: a flat 16-byte-vector copy in chunks of
+    // kCopyUnroll vectors per thread, double-buffered: the next chunk's loads are in flight
+    // while the current chunk is stored, so neither load nor store latency is exposed per
+    // chunk.  The last chunk re-reads itself as its "next" (in bounds) instead of branching,
+    // which would drain every outstanding access.
     const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H);
-    u32x4* dst = (u32x4*)(a.ret[sg.dst_rank] + (int64_t)sg.slot0 * a.H);
+    g_u32x4* dst = (g_u32x4*)(a.ret[sg.dst_rank] + (int64_t)sg.slot0 * a.H);
     const int64_t n16 = (int64_t)sg.rows * a.H / 8;
-    int64_t i = tid;
-    for (; i + 3 * kConsumerThreads < n16; i += 4 * kConsumerThreads) {
-      const u32x4 v0 = src[i], v1 = src[i + kConsumerThreads], v2 = src[i + 2 * kConsumerThreads],
-                  v3 = src[i + 3 * kConsumerThreads];
-      dst[i] = v0;
-      dst[i + kConsumerThreads] = v1;
-      dst[i + 2 * kConsumerThreads] = v2;
-      dst[i + 3 * kConsumerThreads] = v3;
+    constexpr int kU = kCopyUnroll;
+    constexpr int64_t kStep = (int64_t)kU * kConsumerThreads;
+    const int64_t nfull = n16 / kStep;
+    if (nfull > 0) {
+      u32x4 cur[kU], nxt[kU];
+#pragma unroll
+      for (int u = 0; u < kU; ++u) cur[u] = src[tid + u * kConsumerThreads];
+      for (int64_t c = 0; c < nfull; ++c) {
+        const int64_t base = c * kStep + tid;
+        const int64_t next = (c + 1 < nfull ? c + 1 : c) * kStep + tid;
+#pragma unroll
+        for (int u = 0; u < kU; ++u) nxt[u] = src[next + u * kConsumerThreads];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) dst[base + u * kConsumerThreads] = cur[u];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) cur[u] = nxt[u];
+      }
     }
-    for (; i < n16; i += kConsumerThreads) dst[i] = src[i];
+    for (int64_t i = nfull * kStep + tid; i < n16; i += kConsumerThreads) dst[i] = src[i];
     __syncthreads();
   }
   if (wave == 0 && lane == 0 && (polls || waited)) {
@@ -520,7 +580,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
     const int rank = a.row_rank[r];
     if (rank < 0) continue;
     const u32x4* src = (const u32x4*)(a.y + r * a.H);
-    u32x4* dst = (u32x4*)(a.ret[rank] + (int64_t)a.row_slot[r] * a.H);
+    g_u32x4* dst = (g_u32x4*)(a.ret[rank] + (int64_t)a.row_slot[r] * a.H);
     for (int64_t i = threadIdx.x; i < per_row; i += blockDim.x) dst[i] = src[i];
   }
 }

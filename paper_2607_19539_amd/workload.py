@@ -38,6 +38,8 @@ rank r, ``[seed, 1000 + 3e + {0,1,2}]`` W1/W3/W2 of global expert e.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 from typing import Dict, List, Optional
 
@@ -162,11 +164,34 @@ def _router_logits(name: str, cfg: dict, seed: int) -> np.ndarray:
     raise ValueError(f"unknown router kind {kind!r}")
 
 
+def _normal_bf16_into(dst: np.ndarray, seed: int, stream: int, scale: float, chunk_rows: int = 2048) -> None:
+    """dst[:] = bf16(N(0,1) * scale) from one stream, drawn in row chunks (the same values as a
+    single draw of the whole matrix)."""
+    g = _rng(seed, stream)
+    for r0 in range(0, dst.shape[0], chunk_rows):
+        r1 = min(dst.shape[0], r0 + chunk_rows)
+        v = g.standard_normal((r1 - r0, dst.shape[1]), dtype=np.float32)
+        v *= np.float32(scale)
+        dst[r0:r1] = f32_to_bf16_bits(v)
+
+
+def _normal_weights_into(w1, w3, w2, seed: int, first_expert: int) -> None:
+    """Fill all local experts' weights, one thread per matrix (each has its own stream)."""
+    jobs = []
+    for i in range(w1.shape[0]):
+        e = first_expert + i
+        jobs += [(w1[i], 1000 + 3 * e + 0), (w3[i], 1000 + 3 * e + 1), (w2[i], 1000 + 3 * e + 2)]
+    workers = max(1, min(16, len(jobs), len(os.sched_getaffinity(0))))
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        list(ex.map(lambda j: _normal_bf16_into(j[0], seed, j[1], WEIGHT_STD), jobs))
+
+
 def _expert_weights(seed: int, e: int, H: int, F: int, kind: str, E_l_index: int):
     if kind == "normal":
-        w1 = f32_to_bf16_bits(_rng(seed, 1000 + 3 * e + 0).standard_normal((F, H), dtype=np.float32) * WEIGHT_STD)
-        w3 = f32_to_bf16_bits(_rng(seed, 1000 + 3 * e + 1).standard_normal((F, H), dtype=np.float32) * WEIGHT_STD)
-        w2 = f32_to_bf16_bits(_rng(seed, 1000 + 3 * e + 2).standard_normal((H, F), dtype=np.float32) * WEIGHT_STD)
+        w1, w3, w2 = np.empty((F, H), np.uint16), np.empty((F, H), np.uint16), np.empty((H, F), np.uint16)
+        _normal_bf16_into(w1, seed, 1000 + 3 * e + 0, WEIGHT_STD)
+        _normal_bf16_into(w3, seed, 1000 + 3 * e + 1, WEIGHT_STD)
+        _normal_bf16_into(w2, seed, 1000 + 3 * e + 2, WEIGHT_STD)
         return w1, w3, w2
     if kind == "identity":
         # W1 = W3 = [I_H; 0] (F x H), W2 = s_e [I_H 0] (H x F), s_e = 2^-(e mod 4).
@@ -268,8 +293,19 @@ def make_workload(
         w1 = np.empty((E_l, F, H), np.uint16)
         w3 = np.empty((E_l, F, H), np.uint16)
         w2 = np.empty((E_l, H, F), np.uint16)
-        for i in range(E_l):
-            w1[i], w3[i], w2[i] = _expert_weights(seed, lo + i, H, F, weights, i)
+        if weights == "identity":
+            for i in range(E_l):
+                w1[i], w3[i], w2[i] = _expert_weights(seed, lo + i, H, F, weights, i)
+        else:
+            _normal_weights_into(w1, w3, w2, seed, lo)
+            if weights == "zero_w1":
+                w1[:] = 0
+            elif weights == "zero_w3":
+                w3[:] = 0
+            elif weights == "zero_w2":
+                w2[:] = 0
+            elif weights != "normal":
+                raise ValueError(f"unknown weight kind {weights!r}")
 
     return Workload(
         name=name, H=H, F=F, E_t=E_t, k=k, R=R, T_r=T, E_l=E_l, self_rank=owner, seed=seed,
