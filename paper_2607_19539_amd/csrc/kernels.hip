@@ -183,26 +183,56 @@ __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const uint8_
   bf16x8 a0[4], b0[4], a1[4], b1[4];
   read_half(0, 0, a0, b0);
 
-  // Steady state.  Each stage: read the second half while the first half's MFMAs issue;
-  // then, with every read of this stage issued and returned, a barrier makes stage ks+1
-  // visible and frees this stage's slot for stage ks+4; the next stage's first half is read
-  // while the second half's MFMAs issue.  Reads stay one half ahead of the MFMAs and the
-  // DMA four stages ahead, so neither LDS nor global latency sits on the MFMA path.  The last
-  // three stages are peeled so each wait count is a constant on a straight path.
+  // Steady state.  Each stage: the first half's 16 MFMAs issue with the second half's eight
+  // fragment reads threaded between them; a barrier then makes stage ks+1 visible and frees
+  // this stage's slot; the second half's MFMAs issue with the eight DMAs of stage ks+4 and the
+  // next stage's first-half reads threaded between them.  Interleaving keeps the matrix pipe
+  // busy while the wave issues memory instructions (one wave per SIMD has no other wave to
+  // cover them), reads stay one half ahead of the MFMAs and the DMA four stages ahead.  The
+  // last three stages are peeled so each wait count is a constant on a straight path.
+  auto read_frag = [&](int ks, int kk, int q, bf16x8& dst) {
+    const uint8_t* cur = lds + (ks & (kStages - 1)) * kStageBytes;
+    const uint32_t coff = ((uint32_t)(2 * kk + lk) ^ lsw) << 4;
+    dst = q < 4 ? *(const bf16x8*)(cur + a_row + q * 32 * kRowBytes + coff)
+                : *(const bf16x8*)(cur + kOperandBytes + b_row + (q - 4) * 32 * kRowBytes + coff);
+  };
+  auto dma_one = [&](int ks, int q) {
+    const uint32_t st = lds0 + (uint32_t)(ks & (kStages - 1)) * kStageBytes;
+    if (q < kDmaPerThread)
+      dma16(wbase + ks * kRowBytes, woff[q], st + q * 1024);
+    else
+      dma16(xbase + ks * kRowBytes, xoff[q - kDmaPerThread], st + kOperandBytes + (q - kDmaPerThread) * 1024);
+  };
+  auto mfma = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4], int q) {
+    acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[q >> 2], fb[q & 3], acc[q >> 2][q & 3], 0, 0, 0);
+  };
   auto stage = [&](int ks, auto vm_after) {
-    read_half(ks, 1, a1, b1);
-    __builtin_amdgcn_sched_barrier(0);
-    mma_half(a0, b0);
-    __builtin_amdgcn_sched_barrier(0);
     constexpr int vm = decltype(vm_after)::value;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      mfma(a0, b0, q);
+      if (q < 8) read_frag(ks, 1, q, q < 4 ? a1[q] : b1[q - 4]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if constexpr (vm >= 0) {
       wait_vm_and_barrier<vm>();  // stage ks+1 has landed; slot ks % 4 is free
-      if (ks + kStages < nk) issue(ks + kStages);
-      read_half(ks + 1, 0, a0, b0);
+      // A uniform test per DMA: two unrolled copies of this loop (with and without DMAs)
+      // double the live ranges and spill.
+      const bool more = ks + kStages < nk;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        mfma(a1, b1, q);
+        if (q < 8) {
+          if (more) dma_one(ks + kStages, q);
+        } else {
+          read_frag(ks + 1, 0, q - 8, q < 12 ? a0[q - 8] : b0[q - 12]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      mma_half(a1, b1);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_barrier(0);
-    mma_half(a1, b1);
-    __builtin_amdgcn_sched_barrier(0);
   };
   int ks = 0;
   for (; ks + 3 < nk; ++ks) stage(ks, std::integral_constant<int, 2 * per_stage>{});
@@ -379,15 +409,16 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
       // kSplit parts: all parts read back (this part's too: the same values, and no branch
       // that would serialize the loads), 4 blocks of kSplit parts in flight per step.
       const uint64_t* src = parts + tid;
+      constexpr int kGroup = kSplit == 3 ? 2 : 4;  // keeps 4*kGroup*kSplit loaded floats live
 #pragma unroll 1
-      for (int b0 = 0; b0 < 64; b0 += 4) {
-        float4 v[4][kSplit];
+      for (int b0 = 0; b0 < 64; b0 += kGroup) {
+        float4 v[kGroup][kSplit];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < kGroup; ++u)
 #pragma unroll
           for (int p = 0; p < kSplit; ++p) v[u][p] = part_block(src, p, b0 + u);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < kGroup; ++u) {
           float4 s = v[u][0];
 #pragma unroll
           for (int p = 1; p < kSplit; ++p) {

@@ -1,0 +1,65 @@
+"""Register and scratch budget of the gfx950 kernels, read from the compiler's code-object
+metadata (no GPU needed).
+
+A producer wave holds 256 accumulation registers plus its vector registers; in a shared-CU
+run two consumer waves must fit beside it on each SIMD (512 registers), and no kernel may
+spill to scratch (a spill in the MFMA loop costs an order of magnitude).
+"""
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "paper_2607_19539_amd", "csrc", "kernels.hip")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+SIMD_REGISTERS = 512
+CONSUMER_WAVES_BESIDE_PRODUCER = 2
+
+
+@pytest.fixture(scope="module")
+def kernels(tmp_path_factory):
+    if not os.path.exists(HIPCC):
+        pytest.skip("hipcc not available")
+    out = tmp_path_factory.mktemp("dev") / "kernels.s"
+    subprocess.run([HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-x", "hip", "--cuda-device-only",
+                    "-S", SRC, f"-I{os.path.join(ROOT, 'include')}", "-o", str(out),
+                    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"],
+                   check=True, capture_output=True)
+    meta = out.read_text().split("amdhsa.kernels:", 1)[1]
+    found = {}
+    for block in re.split(r"\n  - ", meta)[1:]:
+        fields = dict(re.findall(r"^\s*\.(\w+):\s+(\S+)", block, re.M))
+        if "name" in fields:
+            found[fields["name"]] = fields
+    return found
+
+
+def by_name(kernels, fragment):
+    hits = {n: f for n, f in kernels.items() if fragment in n}
+    assert hits, fragment
+    return hits
+
+
+def test_no_kernel_spills(kernels):
+    for name, f in kernels.items():
+        assert int(f["private_segment_fixed_size"]) == 0, name
+        assert int(f["vgpr_spill_count"]) == 0, name
+
+
+def test_consumer_fits_beside_a_producer_wave(kernels):
+    (cons,) = by_name(kernels, "consumer_kernel").values()
+    budget = SIMD_REGISTERS - CONSUMER_WAVES_BESIDE_PRODUCER * int(cons["vgpr_count"])
+    # The launches taken by default (split 1 to 4 parts) must leave that room.
+    for name, f in by_name(kernels, "producer_kernel").items():
+        split = int(re.search(r"ILb[01]ELi(\d+)E", name).group(1))
+        if split in (1, 2, 3, 4):
+            assert int(f["vgpr_count"]) <= budget, (name, f["vgpr_count"], budget)
+        assert int(f["agpr_count"]) == 256, name
+
+
+def test_every_split_variant_is_instantiated(kernels):
+    names = set(by_name(kernels, "producer_kernel"))
+    for down, split in ((0, 1), (1, 1), (1, 2), (1, 3), (1, 4), (1, 0)):
+        assert any(f"ILb{down}ELi{split}E" in n for n in names), (down, split)
