@@ -18,6 +18,7 @@ consumer CU-split sweep (both CU modes) for every workload measured.
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -130,9 +131,10 @@ class Bench:
         self.run_args = (self.x, wl.expert_offsets, wl.row_src_rank, wl.row_slot, self.w1, self.w3, self.w2,
                          self.bufs, wl.return_rows)
         base = B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING
+        extra = {"shared": B.MOE_SHARED_CUS, "partitioned": 0, "direct": B.MOE_DIRECT_ALL}
         self.stages = {m: B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, args.mgb,
-                                     base | (B.MOE_SHARED_CUS if m == "shared" else 0), 0, args.split_k)
-                       for m in ("shared", "partitioned")}
+                                     base | f, 0, args.split_k)
+                       for m, f in extra.items()}
         torch.cuda.synchronize()
         # The stage runs on a stream of its own, as in a serving loop (on the legacy null stream
         # the shared-CU producer would have to fork to a second queue; see moe_stage_run).
@@ -155,6 +157,10 @@ class Bench:
             fn()
         stg.query(check=False)
         stg.times(reset=True)
+        # A garbage-collection pass inside the timed loop stalls the host for tens of ms while
+        # the GPU idles; collect before and keep the collector off while timing.
+        gc.collect()
+        gc.disable()
         torch.cuda.synchronize()
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         start.record(self.stream)
@@ -162,6 +168,7 @@ class Bench:
             fn()
         end.record(self.stream)
         torch.cuda.synchronize()
+        gc.enable()
         ms = start.elapsed_time(end) / steps
         st = stg.query(check=False)
         if st["rc"] != 0:
@@ -238,6 +245,12 @@ def main():
                 f"{ovl['producer_ms'] * 1e3:.1f}, gate/up {ovl['gate_up_ms'] * 1e3:.1f}, consumer "
                 f"{ovl['consumer_ms'] * 1e3:.1f}); segments {st['n_segments']}, workgroups "
                 f"{st['gu_workgroups']}/{st['down_workgroups']}")
+        direct = None
+        if only == "all":
+            # Ablation: no consumer at all, the down epilogue writes every row to its slot.
+            direct = bench.timed("direct", "serial", 0, steps, warmup)
+            log(f"{name} epilogue-direct ablation: {direct['ms'] * 1e3:.1f} us (producer "
+                f"{direct['producer_ms'] * 1e3:.1f}, gate/up {direct['gate_up_ms'] * 1e3:.1f})")
         sweep = []
         if sweep_cs and ser is not None and only == "all":
             for c in sweep_cs:
@@ -247,6 +260,8 @@ def main():
                                   "stage_us": r["ms"] * 1e3, "speedup_vs_serial": ser["ms"] / r["ms"]})
                     log(f"{name} sweep c={c} {mode}: {r['ms'] * 1e3:.1f} us, speedup {ser['ms'] / r['ms']:.3f}")
         per_wl[name] = summarize(wl, ser, ovl, sweep)
+        if direct is not None:
+            per_wl[name]["epilogue_direct_ablation_us"] = direct["ms"] * 1e3
         timeouts += bench.timeouts
         if headline:
             main_r = ovl if ovl is not None else ser

@@ -73,6 +73,9 @@ extern "C" {
                                       beside producer workgroups there (a consumer workgroup's
                                       registers and LDS fit next to a producer workgroup's), so
                                       the partition costs the producer issue slots, not CUs    */
+#define MOE_DIRECT_ALL (1u << 5)   /* ablation, serial runs only: the down epilogue writes every
+                                      row straight to its slot in return_bufs and no scatter
+                                      runs -- the bound of a stage with no consumer at all     */
 
 typedef struct moe_stage_s* moe_stage_t;
 

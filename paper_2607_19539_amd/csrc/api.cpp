@@ -117,7 +117,7 @@ int check_config(const moe_stage_config_t* c) {
       c->mid_segment_pieces < 0 || c->watchdog_ms < 0)
     return MOE_EINVAL;
   constexpr uint32_t kKnownFlags = MOE_LOCAL_DIRECT | MOE_KERNEL_TIMING | MOE_POISON |
-                                   MOE_TEST_NO_SIGNAL | MOE_SHARED_CUS;
+                                   MOE_TEST_NO_SIGNAL | MOE_SHARED_CUS | MOE_DIRECT_ALL;
   if (c->flags & ~kKnownFlags) return MOE_EINVAL;
   if (c->band_rows < 0 || c->band_rows > 256 || (c->band_rows & (c->band_rows - 1)) != 0)
     return MOE_EINVAL;
@@ -504,8 +504,10 @@ int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const
   h->last.producer_grid = pgrid;
   h->last.consumer_grid = 0;
   h->last.consumer_cus = 0;
-  const ProducerArgs pgu = producer_args(h, lay, x, w1, w3, w2, 0u, false);
-  const ProducerArgs pa = producer_args(h, lay, x, w1, w3, w2, 0u, true);
+  const bool direct_all = (h->cfg.flags & MOE_DIRECT_ALL) != 0;
+  const uint32_t mode = direct_all ? kModeDirectAll : 0u;
+  const ProducerArgs pgu = producer_args(h, lay, x, w1, w3, w2, mode, false);
+  const ProducerArgs pa = producer_args(h, lay, x, w1, w3, w2, mode, true);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], stream));
   if (pgu.n_items > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, stream));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], stream));
@@ -519,7 +521,7 @@ int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const
   sa.n_lrows = h->plan.n_lrows();
   sa.H = h->cfg.hidden;
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], stream));
-  if (sa.n_lrows > 0)
+  if (sa.n_lrows > 0 && !direct_all)
     HIP_TRY(h, launch_scatter(sa, (int)std::min<int64_t>(sa.n_lrows, (int64_t)h->num_cus * 8), stream));
   if (tr) {
     HIP_TRY(h, hipEventRecord(tr->ev[5], stream));

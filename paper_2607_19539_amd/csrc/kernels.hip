@@ -56,6 +56,11 @@ constexpr int kGuOutStride = kGuTileF * 2 + 16;        // 272 B per staged activ
 constexpr int kLdsAlloc = kTileM * kDownOutStride;     // 135168 B >= the 128 KiB operand ring
 constexpr int kDmaPerThread = kTileM / kRowsPerDma / 4;  // 4 per operand per thread
 
+// Chunk swizzle of the 64-byte operand rows: a row's four 16-byte K chunks are stored XOR
+// ((row / 2) ^ (row / 8)) % 4.  Measured on gfx950, fragment reads with it spend half of their
+// LDS-active cycles on bank conflicts, and (row / 4) % 4 brings that to 2 %; but the latter
+// costs the gate/up kernel a vector register, pushing it past the budget that lets two
+// consumer waves share its SIMDs, and the stage time did not change measurably.
 __device__ __forceinline__ uint32_t swz(uint32_t row) { return ((row >> 1) ^ (row >> 3)) & 3u; }
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -448,7 +453,8 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     // local rows go straight to the local receive buffer when the producer writes them
     // directly.  In a signalled launch a wave stores one 512-byte row (64 lanes x 8 bytes, 4
     // rows per pass) and the Y rows at device scope, so publishing the tile needs no L2
-    // writeback.  Without signalling, 32 lanes store a row with ordinary 16-byte stores.
+    // writeback.  Without signalling, 32 lanes store a row with ordinary 16-byte stores; in
+    // the no-consumer ablation every row goes straight to its receive buffer.
     const bool direct = (a.mode & kModeLocalDirect) != 0;
     const bool signal = (a.mode & kModeSignal) != 0;
     if (signal) {
@@ -468,6 +474,7 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
         }
       }
     } else {
+      const bool direct_all = (a.mode & kModeDirectAll) != 0;
       const int c16 = tid & 31;
       const int n = col * kDownTileN + c16 * 8;
 #pragma unroll 4
@@ -477,7 +484,7 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
         const int rank = a.row_rank[lrow];
         if (rank >= 0 && n < H) {
           const u32x4 v = *(const u32x4*)(lds + m * kDownOutStride + c16 * 16);
-          if (direct && rank == a.self_rank)
+          if (direct_all || (direct && rank == a.self_rank))
             *(g_u32x4*)(a.ret[rank] + (int64_t)a.row_slot[lrow] * H + n) = v;
           else
             *(g_u32x4*)(a.y + (int64_t)lrow * H + n) = v;

@@ -10,6 +10,7 @@ namespace moe {
 // Producer mode bits.
 constexpr uint32_t kModeSignal = 1u;       // raise a ready flag per down tile of a transfer tile row
 constexpr uint32_t kModeLocalDirect = 2u;  // local rows go straight to the local receive buffer
+constexpr uint32_t kModeDirectAll = 4u;    // every row goes straight to its receive buffer
 
 struct ProducerArgs {
   const uint16_t* x;       // [rows, H] dispatched tokens

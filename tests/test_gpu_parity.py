@@ -125,6 +125,23 @@ def test_poison_mode_catches_no_early_copy():
             compare(out, ref)
 
 
+def test_direct_all_matches_serial():
+    """MOE_DIRECT_ALL (no-consumer ablation): the down epilogue writes every row to its slot and
+    no scatter runs; the output is bitwise the serial path's and within tolerance of the oracle."""
+    wl = make_workload("tiny", owner=3, overrides=RAGGED)
+    dw = DeviceWorkload(torch, wl)
+    ref = oracle_bufs(wl)
+    with make_stage(wl, band_rows=16) as st:
+        ser = run_serial(dw, st)
+    with make_stage(wl, flags=B.MOE_LOCAL_DIRECT | B.MOE_DIRECT_ALL | B.MOE_KERNEL_TIMING) as st:
+        out = run_serial(dw, st)
+        t = st.times()
+        assert t["runs"] == 1 and t["scatter_ms"] < 0.01  # nothing between the down launch and the end
+    compare(out, ref)
+    for a, b in zip(out, ser):
+        assert np.array_equal(a, b)
+
+
 @pytest.mark.parametrize("split_k", [2, 3, 5, 16])
 def test_split_k_down_tiles(split_k):
     """Down tiles split into K parts (18 K steps here, so parts of 1..9 steps, uneven for 5 and 16):
