@@ -190,3 +190,46 @@ int moe_oracle_run(int32_t hidden, int32_t ffn, int32_t num_local_experts, int32
   free(row_expert);
   return OR_OK;
 }
+
+/*
+ * Weighted combine on a source rank (paper Section 2.1, step 5: once the expert outputs are
+ * back, each rank reduces the k outputs of every token it sent, weighted by the router's gate
+ * values).  For token t of this rank:
+ *     out[t, :] = bf16_rne( sum_{j = 0..k-1} gate[t*k + j] * recv[slot[t*k + j], :] ),
+ * the sum in fp32 over j ascending, each term an fp32 product followed by an fp32 add (built
+ * without contraction).  recv is the rank's receive buffer [recv_rows, H] bf16.
+ * Returns -1 for bad sizes or null pointers, -2 if a slot is outside [0, recv_rows); then
+ * nothing is written.
+ */
+int moe_oracle_combine(int32_t hidden, int32_t k, int64_t tokens, int64_t recv_rows, const uint16_t* recv,
+                       const int32_t* slot, const float* gate, uint16_t* out, int32_t nthreads) {
+  if (hidden <= 0 || k <= 0 || tokens < 0 || recv_rows < 0) return OR_EINVAL;
+  if (tokens > 0 && (!recv || !slot || !gate || !out)) return OR_EINVAL;
+  for (int64_t i = 0; i < tokens * k; ++i)
+    if (slot[i] < 0 || slot[i] >= recv_rows) return OR_EROUTING;
+  const int64_t H = hidden;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(static)
+#endif
+  for (int64_t t = 0; t < tokens; ++t) {
+    for (int64_t h = 0; h < H; ++h) {
+      float acc = 0.0f;
+      for (int32_t j = 0; j < k; ++j) {
+#if ORACLE_MUTATION == 7
+        const int32_t s = slot[t * k];  /* planted: every term reads the first choice's row */
+#else
+        const int32_t s = slot[t * k + j];
+#endif
+#if ORACLE_MUTATION == 6
+        const float term = widen_bf16(recv[s * H + h]);  /* planted: gate weight dropped */
+#else
+        const float term = gate[t * k + j] * widen_bf16(recv[s * H + h]);
+#endif
+        acc = acc + term;
+      }
+      out[t * H + h] = round_bf16(acc);
+    }
+  }
+  return OR_OK;
+}

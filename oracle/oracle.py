@@ -25,7 +25,8 @@ EINVAL, EROUTING = -1, -2
 
 def build(out: str = LIB, mutation: int = 0) -> str:
     """Compile the oracle into a shared library (portable x86-64 code, OpenMP)."""
-    cmd = ["gcc", "-O3", "-std=c11", "-fopenmp", "-fPIC", "-shared", f"-DORACLE_MUTATION={int(mutation)}",
+    cmd = ["gcc", "-O3", "-std=c11", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
+           f"-DORACLE_MUTATION={int(mutation)}",
            SRC, "-o", out + ".tmp", "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(out + ".tmp", out)
@@ -48,6 +49,8 @@ class Oracle:
         self.lib.moe_oracle_run.restype = ctypes.c_int
         self.lib.moe_oracle_validate.argtypes = [i32, i32, i32, i32, i32, i64, vp, vp, vp, vp]
         self.lib.moe_oracle_validate.restype = ctypes.c_int
+        self.lib.moe_oracle_combine.argtypes = [i32, i32, i64, i64, vp, vp, vp, vp, i32]
+        self.lib.moe_oracle_combine.restype = ctypes.c_int
 
     @staticmethod
     def _p(a: Optional[np.ndarray]):
@@ -84,6 +87,20 @@ class Oracle:
         rr = np.ascontiguousarray(return_rows, np.int64)
         return self.lib.moe_oracle_validate(H, F, E_l, R, self_rank, rows, self._p(off), self._p(src),
                                             self._p(slot), self._p(rr))
+
+    def combine(self, recv: np.ndarray, slot: np.ndarray, gate: np.ndarray, out: np.ndarray,
+                num_threads: int = 0) -> int:
+        """Weighted combine of one source rank: ``recv`` [recv_rows, H] u16, ``slot`` [T, k] i32,
+        ``gate`` [T, k] f32; writes ``out`` [T, H] u16 (bf16 bits)."""
+        recv = np.ascontiguousarray(recv, np.uint16)
+        slot = np.ascontiguousarray(slot, np.int32)
+        gate = np.ascontiguousarray(gate, np.float32)
+        if out.dtype != np.uint16 or not out.flags.c_contiguous:
+            raise ValueError("out must be a C-contiguous uint16 array")
+        T, k = slot.shape
+        return self.lib.moe_oracle_combine(int(recv.shape[1]), int(k), int(T), int(recv.shape[0]),
+                                           self._p(recv), self._p(slot), self._p(gate), self._p(out),
+                                           int(num_threads))
 
     def run_workload(self, wl, return_bufs: Sequence[np.ndarray], num_threads: int = 0) -> int:
         """Convenience: run on a ``Workload`` from the synthetic generator."""

@@ -106,6 +106,7 @@ class Workload:
     return_rows: np.ndarray           # [R] i64, receive-buffer rows per source rank (= T_r * k)
     topk_experts: np.ndarray          # [R, T_r, k] i32 global expert ids
     gates: np.ndarray                 # [R, T_r, k] f32 gate weights
+    slots: Optional[np.ndarray] = None  # [R, T_r, k] i32 receive slot of each (source, token, choice)
     x_src: List[np.ndarray] = field(default_factory=list)  # per source rank [T_r, H] u16 (optional)
 
     @property
@@ -314,5 +315,5 @@ def make_workload(
         row_token=t_all.astype(np.int32), row_j=j_all.astype(np.int32),
         w1=w1, w3=w3, w2=w2,
         return_rows=np.full(R, T * k, np.int64),
-        topk_experts=order, gates=gates, x_src=x_src,
+        topk_experts=order, gates=gates, slots=slots, x_src=x_src,
     )
