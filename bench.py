@@ -182,6 +182,34 @@ class Bench:
                 "scatter_ms": tm["scatter_ms"] / runs}
 
 
+    def timed_combine(self, steps, warmup):
+        """The weighted combine of this rank's own tokens (k returned rows each) from its receive
+        buffer: HBM-bound, timed with events on the stream it runs on."""
+        torch, B, wl = self.torch, self.B, self.wl
+        r = wl.self_rank
+        slot = torch.from_numpy(np.ascontiguousarray(wl.slots[r]).astype(np.int32)).cuda()
+        gate = torch.from_numpy(np.ascontiguousarray(wl.gates[r]).astype(np.float32)).cuda()
+        out = torch.empty((wl.T_r, wl.H), dtype=torch.int16, device="cuda")
+        recv = self.bufs[r]
+        fn = lambda: B.moe_combine(recv, slot, gate, out, stream=self.stream)
+        for _ in range(warmup):
+            fn()
+        gc.collect()
+        gc.disable()
+        torch.cuda.synchronize()
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(self.stream)
+        for _ in range(steps):
+            fn()
+        end.record(self.stream)
+        torch.cuda.synchronize()
+        gc.enable()
+        us = start.elapsed_time(end) / steps * 1e3
+        nbytes = 2.0 * wl.H * wl.T_r * (wl.k + 1) + 8.0 * wl.T_r * wl.k
+        return {"us": us, "tokens": wl.T_r, "k": wl.k, "bytes": nbytes,
+                "GBps": nbytes / (us * 1e-6) / 1e9, "frac_of_hbm_peak": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+
+
 def summarize(wl, ser, ovl, sweep):
     """Per-workload figures: stage times, producer launches, throughput against the bf16 peak."""
     flops = wl.flops()
@@ -260,6 +288,9 @@ def main():
                                   "stage_us": r["ms"] * 1e3, "speedup_vs_serial": ser["ms"] / r["ms"]})
                     log(f"{name} sweep c={c} {mode}: {r['ms'] * 1e3:.1f} us, speedup {ser['ms'] / r['ms']:.3f}")
         per_wl[name] = summarize(wl, ser, ovl, sweep)
+        comb = bench.timed_combine(max(steps, 20), max(warmup, 5))
+        per_wl[name]["combine"] = comb
+        log(f"{name} combine ({wl.T_r} tokens, k={wl.k}): {comb['us']:.1f} us, {comb['GBps']:.0f} GB/s")
         if direct is not None:
             per_wl[name]["epilogue_direct_ablation_us"] = direct["ms"] * 1e3
         timeouts += bench.timeouts

@@ -197,6 +197,33 @@ const char* moe_stage_last_error(moe_stage_t h);
 /* Waits for outstanding work, then frees the handle and everything it owns. */
 int moe_stage_destroy(moe_stage_t h);
 
+/*
+ * Weighted combine on a source rank (paper Section 2.1, step 5: after the
+ * return transfer, the rank that sent a token reduces the token's k expert
+ * outputs, weighted by the router's gate values).  Stateless, needs no handle:
+ *
+ *   out[t, :] = bf16_rne( sum_{j = 0..k-1} gate[t*k + j] * recv[slot[t*k + j], :] )
+ *
+ * summed in fp32 in ascending j, each term a rounded fp32 product followed by a
+ * rounded fp32 add (no fused multiply-add), starting from +0.
+ *   recv       device, [recv_rows, hidden] bf16 row-major: this rank's receive
+ *              buffer, as filled by every owner's moe_stage_run / _run_serial;
+ *   slot       device, [tokens, k] int32: receive slot of choice j of token t;
+ *   gate       device, [tokens, k] fp32 gate weights;
+ *   out        device, [tokens, hidden] bf16 row-major, written in full;
+ *   bad_slots  optional device uint32: incremented once per slot outside
+ *              [0, recv_rows) (the term is skipped and the output still written);
+ *              the caller zeroes it.
+ * hidden must be a multiple of 8 and <= 65536, recv and out 16-byte aligned.  The
+ * buffers stay owned by the caller; the call only enqueues a kernel on `stream`
+ * (a hipStream_t; NULL = null stream) and returns without waiting.  Errors
+ * (MOE_EINVAL, MOE_EUNSUPPORTED, MOE_EHIP) enqueue nothing; the message is
+ * moe_stage_last_error(NULL).
+ */
+int moe_combine(const void* recv, int64_t recv_rows, int32_t hidden, const int32_t* slot,
+                const float* gate, int64_t tokens, int32_t k, void* out, uint32_t* bad_slots,
+                void* stream);
+
 /* ---------------------------------------------------------------------------
  * Host-only plan inspection (no GPU needed).  Builds exactly the plan that
  * moe_stage_run would use for these arguments and lets the caller read its

@@ -25,7 +25,7 @@ ERROR_NAMES = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EROUTING", -3: "MOE_ECAPA
 
 EXPORTED = ["moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query", "moe_stage_times",
             "moe_stage_last_error", "moe_stage_destroy", "moe_plan_build", "moe_plan_info", "moe_plan_copy",
-            "moe_plan_free"]
+            "moe_plan_free", "moe_combine"]
 
 
 class moe_stage_config_t(ctypes.Structure):
@@ -91,7 +91,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.moe_plan_copy.restype = ctypes.c_int64
     lib.moe_plan_free.argtypes = [vp]
     lib.moe_plan_free.restype = None
-    for name in ("moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query",
+    lib.moe_combine.argtypes = [vp, i64, i32, vp, vp, i64, i32, vp, vp, vp]
+    for name in ("moe_combine", "moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query",
                  "moe_stage_times", "moe_stage_destroy", "moe_plan_build", "moe_plan_info"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -190,6 +191,28 @@ def moe_stage_run_serial(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w
     rc = load().moe_stage_run_serial(h, *args, _stream_ptr(stream))
     del keep
     return _check(rc, h)
+
+
+def moe_combine(recv, slot, gate, out, bad_slots=None, stream=None) -> int:
+    """Weighted combine of one source rank on the device.
+
+    ``recv`` [recv_rows, H] and ``out`` [T, H] are 2-byte device tensors (bf16 bits),
+    ``slot`` [T, k] int32 and ``gate`` [T, k] float32 device tensors, ``bad_slots`` an
+    optional one-element int32/uint32 device tensor that counts out-of-range slots."""
+    if recv.dim() != 2 or out.dim() != 2 or slot.dim() != 2 or gate.shape != slot.shape:
+        raise ValueError("recv [rows, H], out [T, H], slot and gate [T, k] expected")
+    if recv.element_size() != 2 or out.element_size() != 2:
+        raise ValueError("recv and out must hold 2-byte elements (bf16 bits)")
+    import torch
+    if slot.dtype != torch.int32 or gate.dtype != torch.float32:
+        raise ValueError("slot must be int32 and gate float32")
+    T, k = slot.shape
+    if out.shape[0] != T or out.shape[1] != recv.shape[1]:
+        raise ValueError("out must be [T, H] with the receive buffer's H")
+    bad = None if bad_slots is None else _dev_ptr(bad_slots)
+    rc = load().moe_combine(_dev_ptr(recv), int(recv.shape[0]), int(recv.shape[1]), _dev_ptr(slot),
+                            _dev_ptr(gate), int(T), int(k), _dev_ptr(out), bad, _stream_ptr(stream))
+    return _check(rc)
 
 
 def moe_stage_query(h, check: bool = True) -> dict:

@@ -611,6 +611,37 @@ int moe_stage_destroy(moe_stage_t h) {
   return MOE_OK;
 }
 
+// ----------------------------------------------------------------- weighted combine
+int moe_combine(const void* recv, int64_t recv_rows, int32_t hidden, const int32_t* slot,
+                const float* gate, int64_t tokens, int32_t k, void* out, uint32_t* bad_slots,
+                void* stream) {
+  if (hidden <= 0 || k <= 0 || tokens < 0 || recv_rows < 0)
+    return set_err(nullptr, MOE_EINVAL, "moe_combine: hidden and k must be positive, sizes >= 0");
+  if (tokens == 0) return MOE_OK;
+  if (!slot || !gate || !out || (recv_rows > 0 && !recv))
+    return set_err(nullptr, MOE_EINVAL, "moe_combine: null pointer");
+  if (hidden % 8 || hidden > 65536)
+    return set_err(nullptr, MOE_EUNSUPPORTED, "moe_combine: hidden must be a multiple of 8, <= 65536");
+  if (((uintptr_t)recv | (uintptr_t)out) & 15)
+    return set_err(nullptr, MOE_EUNSUPPORTED, "moe_combine: recv and out must be 16-byte aligned");
+  if (recv_rows > INT32_MAX)
+    return set_err(nullptr, MOE_EUNSUPPORTED, "moe_combine: recv_rows must fit a 32-bit slot");
+  CombineArgs a{};
+  a.recv = (const uint16_t*)recv;
+  a.slot = slot;
+  a.gate = gate;
+  a.out = (uint16_t*)out;
+  a.bad_slots = bad_slots;
+  a.recv_rows = recv_rows;
+  a.tokens = tokens;
+  a.k = k;
+  a.H = hidden;
+  const hipError_t e = launch_combine(a, (hipStream_t)stream);
+  if (e != hipSuccess)
+    return set_err(nullptr, MOE_EHIP, std::string("moe_combine launch: ") + hipGetErrorString(e));
+  return MOE_OK;
+}
+
 // ----------------------------------------------------------------- plan inspection
 struct moe_plan_s {
   Plan plan;

@@ -66,7 +66,19 @@ struct InitArgs {
   int32_t n_arrivals;
 };
 
+struct CombineArgs {
+  const uint16_t* recv;    // [recv_rows, H] receive buffer of this source rank
+  const int32_t* slot;     // [tokens, k] receive slot of each choice
+  const float* gate;       // [tokens, k] gate weights
+  uint16_t* out;           // [tokens, H]
+  uint32_t* bad_slots;     // optional: incremented once per out-of-range slot
+  int64_t recv_rows, tokens;
+  int32_t k, H;
+};
+
 hipError_t launch_init(const InitArgs& a, hipStream_t s);
+// Gate-weighted sum of each token's k returned rows (16-byte vectors, fp32 sum, bf16 out).
+hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 // Gate/up tiles (down = false) or down-projection tiles with ready flags (down = true).
 hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream_t s);
 hipError_t launch_consumer(const ConsumerArgs& a, int grid, hipStream_t s);

@@ -75,3 +75,17 @@ def test_create_rejects_bad_config_before_touching_the_device():
         with pytest.raises(B.MoeError) as ei:
             B.moe_stage_create(cfg)
         assert ei.value.code == code
+
+
+def test_combine_checks_arguments_before_touching_the_device():
+    lib = B.load()
+    p = 4096  # an aligned stand-in address; no call below reaches the device
+    assert lib.moe_combine(None, 0, 64, None, None, 0, 2, None, None, None) == B.MOE_OK   # no tokens
+    assert lib.moe_combine(p, 8, 0, p, p, 4, 2, p, None, None) == B.MOE_EINVAL           # hidden 0
+    assert lib.moe_combine(p, 8, 64, p, p, 4, 0, p, None, None) == B.MOE_EINVAL          # k 0
+    assert lib.moe_combine(p, 8, 64, None, p, 4, 2, p, None, None) == B.MOE_EINVAL       # null slot
+    assert lib.moe_combine(None, 8, 64, p, p, 4, 2, p, None, None) == B.MOE_EINVAL       # null recv
+    assert lib.moe_combine(p, 8, 12, p, p, 4, 2, p, None, None) == B.MOE_EUNSUPPORTED    # H % 8
+    assert lib.moe_combine(p + 8, 8, 64, p, p, 4, 2, p, None, None) == B.MOE_EUNSUPPORTED  # alignment
+    assert lib.moe_combine(p, 2 ** 31, 64, p, p, 4, 2, p, None, None) == B.MOE_EUNSUPPORTED
+    assert "moe_combine" in B.moe_stage_last_error(None)

@@ -12,7 +12,8 @@ import subprocess
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-SRC = os.path.join(ROOT, "paper_2607_19539_amd", "csrc", "kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2607_19539_amd", "csrc")
+SOURCES = ["kernels.hip", "combine.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SIMD_REGISTERS = 512
 CONSUMER_WAVES_BESIDE_PRODUCER = 2
@@ -22,17 +23,18 @@ CONSUMER_WAVES_BESIDE_PRODUCER = 2
 def kernels(tmp_path_factory):
     if not os.path.exists(HIPCC):
         pytest.skip("hipcc not available")
-    out = tmp_path_factory.mktemp("dev") / "kernels.s"
-    subprocess.run([HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-x", "hip", "--cuda-device-only",
-                    "-S", SRC, f"-I{os.path.join(ROOT, 'include')}", "-o", str(out),
-                    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"],
-                   check=True, capture_output=True)
-    meta = out.read_text().split("amdhsa.kernels:", 1)[1]
     found = {}
-    for block in re.split(r"\n  - ", meta)[1:]:
-        fields = dict(re.findall(r"^\s*\.(\w+):\s+(\S+)", block, re.M))
-        if "name" in fields:
-            found[fields["name"]] = fields
+    for src in SOURCES:
+        out = tmp_path_factory.mktemp("dev") / (src + ".s")
+        subprocess.run([HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-x", "hip", "--cuda-device-only",
+                        "-S", os.path.join(CSRC, src), f"-I{os.path.join(ROOT, 'include')}", "-o", str(out),
+                        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"],
+                       check=True, capture_output=True)
+        meta = out.read_text().split("amdhsa.kernels:", 1)[1]
+        for block in re.split(r"\n  - ", meta)[1:]:
+            fields = dict(re.findall(r"^\s*\.(\w+):\s+(\S+)", block, re.M))
+            if "name" in fields:
+                found[fields["name"]] = fields
     return found
 
 
@@ -63,3 +65,8 @@ def test_every_split_variant_is_instantiated(kernels):
     names = set(by_name(kernels, "producer_kernel"))
     for down, split in ((0, 1), (1, 1), (1, 2), (1, 3), (1, 4), (1, 0)):
         assert any(f"ILb{down}ELi{split}E" in n for n in names), (down, split)
+
+
+def test_combine_variants_present(kernels):
+    names = set(by_name(kernels, "combine_kernel"))
+    assert len(names) == 3, names
