@@ -55,8 +55,8 @@ extern "C" {
 #define MOE_ECAPACITY (-3)    /* rows > max_rows, or the plan exceeds the handle's workspaces   */
 #define MOE_EHIP (-4)         /* a HIP runtime call failed (message names it)                  */
 #define MOE_ETIMEOUT (-5)     /* a bounded device wait expired; sticky until the next query   */
-#define MOE_EUNSUPPORTED (-6) /* hidden/ffn not multiples of 64, hidden > 65536, cu_split out
-                                 of range                                                      */
+#define MOE_EUNSUPPORTED (-6) /* hidden/ffn not multiples of 64, hidden > 65536, max_rows >=
+                                 2^24, cu_split out of range                                   */
 
 /* Config flags */
 #define MOE_LOCAL_DIRECT (1u << 0) /* overlapped run: rows whose source is self_rank are written
@@ -85,7 +85,7 @@ typedef struct {
   int32_t num_local_experts; /* E_l >= 1                                                      */
   int32_t num_ranks;         /* R >= 1 source ranks                                           */
   int32_t self_rank;         /* 0 <= self_rank < R; rows from it are local (Section 3.2.1)    */
-  int32_t max_rows;          /* capacity of one run; sizes the workspaces                     */
+  int32_t max_rows;          /* capacity of one run (< 2^24); sizes the workspaces            */
   int32_t band_rows;         /* tb_M of the remote-owner-aligned layout (Section 3.2.1): each
                                 remote owner group is padded to a multiple of it, so every
                                 band of band_rows rows has one destination.  Power of two in
@@ -97,7 +97,7 @@ typedef struct {
                                 coalesce x pieces.  >= 1; 0 means 1.                         */
   uint32_t flags;            /* MOE_* flags above                                            */
   int32_t watchdog_ms;       /* bound on every device spin-wait; 0 = 2000 ms                  */
-  int32_t down_split_k;      /* K parts per down-projection tile, 1..16 and <= ffn / 32: each
+  int32_t down_split_k;      /* K parts per down-projection tile, 1..16 and <= ffn / 64: each
                                 part accumulates one contiguous K range in fp32 and the part
                                 that finishes last adds the parts in part order and writes the
                                 tile.  Fixed per handle, so results do not depend on the

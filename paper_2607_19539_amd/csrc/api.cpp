@@ -124,7 +124,8 @@ int check_config(const moe_stage_config_t* c) {
   if (c->down_split_k < 0 || c->down_split_k > kMaxSplitK ||
       (c->ffn > 0 && c->down_split_k > c->ffn / kTileK))
     return MOE_EINVAL;
-  if (c->hidden % 64 != 0 || c->ffn % 64 != 0 || c->hidden > kMaxDownColTiles * kDownTileN)
+  if (c->hidden % 64 != 0 || c->ffn % 64 != 0 || c->hidden > kMaxDownColTiles * kDownTileN ||
+      c->max_rows >= (1 << 24))
     return MOE_EUNSUPPORTED;
   return MOE_OK;
 }

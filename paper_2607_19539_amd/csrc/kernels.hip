@@ -34,34 +34,37 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // compiler cannot infer its address space and would emit flat accesses.
 typedef __attribute__((address_space(1))) u32x4 g_u32x4;
 
-// Operand tiles in LDS: 256 rows x 32 k (bf16) = 16 KiB per operand, 64 bytes per row,
-// weight tile then token tile per stage, four stages in a ring (128 KiB).  Global
-// memory is copied straight into LDS with global_load_lds_dwordx4 (no register
-// staging), three K-steps ahead of the MFMAs.  A DMA instruction writes 64 lanes x 16
-// bytes contiguously, i.e. 16 rows, so each lane fetches the 16-byte chunk that
-// belongs at its slot: chunk c of row r sits at physical chunk c ^ g(r).  g spreads the
-// 32 rows that one MFMA operand read touches over all banks, for 8-lane (32-bank) and
-// 16-lane (64-bank) phases alike.
-constexpr int kRowBytes = kTileK * 2;                  // 64
-constexpr int kOperandBytes = kTileM * kRowBytes;      // 16 KiB
-constexpr int kStageBytes = 2 * kOperandBytes;         // 32 KiB
-constexpr int kStages = 4;
-constexpr int kLdsBytes = kStages * kStageBytes;       // 128 KiB (operand ring)
-constexpr int kRowsPerDma = 64 * 16 / kRowBytes;       // 16 rows per DMA instruction
+// Operand blocks in LDS: 256 rows x 64 k (bf16) = 32 KiB, 128 bytes per row -- one whole
+// cache line of the row-major operand, so every line a K step touches is used in full (with
+// 64-byte rows each line is fetched twice, and the load path then streams about 0.6x as many
+// useful bytes per clock).  A K step needs a weight block and a token block; a ring of five
+// blocks (all 160 KiB of LDS) keeps one and a half K steps of loads in flight.  Global
+// memory is copied straight into LDS with global_load_lds_dwordx4 (no register staging).
+// A DMA instruction writes 64 lanes x 16 bytes contiguously, i.e. 8 rows, so each lane
+// fetches the 16-byte chunk that belongs at its slot: chunk c of row r sits at physical
+// chunk c ^ swz(r).
+constexpr int kRowBytes = kTileK * 2;                  // 128
+constexpr int kBlockBytes = kTileM * kRowBytes;        // 32 KiB: one operand of one K step
+constexpr int kRingBlocks = 5;
+constexpr int kLdsBytes = kRingBlocks * kBlockBytes;   // 160 KiB: the whole LDS of a CU
+constexpr int kRowsPerDma = 64 * 16 / kRowBytes;       // 8 rows per DMA instruction
+constexpr int kDmaPerThread = kTileM / kRowsPerDma / 4;  // 8 per operand block per thread
 // Epilogue staging: the finished tile goes through LDS (free once the pipeline drains) so
 // that global stores are whole 16-byte chunks of contiguous rows.  Rows are padded by 16
 // bytes so the 32 lanes writing one column of 32 rows hit distinct banks.
 constexpr int kDownOutStride = kDownTileN * 2 + 16;    // 528 B per staged output row
 constexpr int kGuOutStride = kGuTileF * 2 + 16;        // 272 B per staged activation row
-constexpr int kLdsAlloc = kTileM * kDownOutStride;     // 135168 B >= the 128 KiB operand ring
-constexpr int kDmaPerThread = kTileM / kRowsPerDma / 4;  // 4 per operand per thread
+// Two words past both staging areas carry the next work item and the split-K verdict
+// between the waves; the operand ring overwrites them, so they are used only outside it.
+constexpr int kSharedWords = kLdsBytes - 16;
+static_assert(kTileM * kDownOutStride <= kSharedWords, "down staging overlaps the shared words");
+static_assert(kTileM * kGuOutStride <= kSharedWords, "gate/up staging overlaps the shared words");
 
-// Chunk swizzle of the 64-byte operand rows: a row's four 16-byte K chunks are stored XOR
-// ((row / 2) ^ (row / 8)) % 4.  Measured on gfx950, fragment reads with it spend half of their
-// LDS-active cycles on bank conflicts, and (row / 4) % 4 brings that to 2 %; but the latter
-// costs the gate/up kernel a vector register, pushing it past the budget that lets two
-// consumer waves share its SIMDs, and the stage time did not change measurably.
-__device__ __forceinline__ uint32_t swz(uint32_t row) { return ((row >> 1) ^ (row >> 3)) & 3u; }
+// Chunk swizzle of the 128-byte operand rows: chunk c of row r is stored at c ^ ((r / 2) % 8).
+// A fragment read (ds_read_b128) is served 16 lanes at a time; those lanes read one chunk
+// column of 16 consecutive rows, and with 64 four-byte banks (256 bytes) even and odd rows
+// fall in opposite bank halves, so the XOR spreads the 16 reads over all 16 bank groups.
+__device__ __forceinline__ uint32_t swz(uint32_t row) { return (row >> 1) & 7u; }
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
@@ -120,21 +123,53 @@ __device__ __forceinline__ void wait_vm_and_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Rows of one operand as a DMA source.  Instruction i of a wave fetches the 8 rows starting at
+// g_i = min(g0 + 8i, gmax) from the wave-uniform address base + g_i * stride; each lane adds
+// lane_off[i % 2]: its row (lane / 8) times the stride plus its swizzled 16-byte chunk (the
+// swizzle of rows wave*64 + i*8 + lane/8 depends on i only through i % 2).  H and F are
+// multiples of 64, so an 8-row group lies wholly inside or wholly past the operand's last
+// row, and clamping the group start keeps every read in bounds.
+struct DmaRows {
+  const uint8_t* base;
+  uint32_t stride;
+  int32_t g0, gmax;
+  uint32_t lane_off[2];
+  __device__ __forceinline__ const uint8_t* rows(int i) const {
+    return base + (uint64_t)(uint32_t)min(g0 + 8 * i, gmax) * stride;
+  }
+};
+
+// Lane offset of row lane/8 with its swizzled chunk, for even (p = 0) or odd (p = 1) DMA
+// instructions: the tile row is wave*64 + i*8 + lane/8, whose swizzle is (4*(i%2) + lane/16) % 8.
+__device__ __forceinline__ uint32_t dma_lane_off(int lane, int p, uint32_t stride) {
+  const uint32_t r = (uint32_t)lane >> 3;
+  return r * stride + (((uint32_t)(lane & 7) ^ ((4u * p + (r >> 1)) & 7u)) << 4);
+}
+
 // ---------------------------------------------------------------------------
 // One 256x256 output tile: acc[i][j] holds D[n][m] for the wave's 128x128
 // quadrant, n = wn*128 + i*32 + 8*(r/4) + 4*(lane/32) + r%4, m = wm*128 + j*32 + lane%32.
-// wbase / xbase are wave-uniform byte bases of the weight / token operand; woff[i] /
-// xoff[i] are this lane's byte offsets of the row it fetches for DMA instruction i
-// (operand-tile row (wave*4 + i)*16 + lane/4), including its swizzled 16-byte chunk.
+// DMA instruction i of a wave fills operand-tile rows wave*64 + i*8 .. +7 (w for the weight
+// tile, x for the token tile); with kGatherX the token rows are gathered, xoff[i] being this
+// lane's byte offset from x.base for instruction i.
+//
+// Block b of the ring holds the weights (b even) or tokens (b odd) of K step b/2, in slot
+// b % 5.  Prologue: blocks 0-3 in flight.  K step ks runs four 16-deep MFMA sub-steps; each
+// sub-step's 16 MFMAs issue with the next sub-step's 8 fragment reads threaded between them,
+// and with the DMAs of the blocks whose slots are free: block 2ks+4 during sub-step 0 (its
+// slot held K step ks-1's tokens), block 2ks+5 during sub-step 3, after the barrier that
+// ends every wave's reads of step ks.  That barrier also waits for step ks+1's blocks, with
+// only block 2ks+4 allowed in flight.  The last two K steps are peeled so each wait count
+// is a constant on a straight path.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const uint8_t* wbase, const uint8_t* xbase,
-                                         const uint32_t (&woff)[kDmaPerThread],
+template <bool kGatherX>
+__device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const DmaRows& w, const DmaRows& x,
                                          const uint32_t (&xoff)[kDmaPerThread], int K, f32x16 (&acc)[4][4]) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave & 1, wm = wave >> 1;
   const int lr = lane & 31, lk = lane >> 5;
-  const uint32_t lsw = swz(lr);
+  const uint32_t lsw = swz(lr);  // rows wn*128 + i*32 + lr share lr's swizzle
   const uint32_t a_row = (uint32_t)(wn * 128 + lr) * kRowBytes;
   const uint32_t b_row = (uint32_t)(wm * 128 + lr) * kRowBytes;
   const uint32_t dma_off = (uint32_t)wave * kDmaPerThread * 1024;
@@ -146,104 +181,96 @@ __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const uint8_
 
   const int nk = K / kTileK;
   const uint32_t lds0 = lds_addr(lds) + dma_off;
-  auto issue = [&](int ks) {
-    const uint32_t st = lds0 + (uint32_t)(ks & (kStages - 1)) * kStageBytes;
-    const uint8_t* wb = wbase + ks * kRowBytes;  // wave-uniform: scalar base + 32-bit lane offset
-    const uint8_t* xb = xbase + ks * kRowBytes;
-#pragma unroll
-    for (int i = 0; i < kDmaPerThread; ++i) dma16(wb, woff[i], st + i * 1024);
-#pragma unroll
-    for (int i = 0; i < kDmaPerThread; ++i) dma16(xb, xoff[i], st + kOperandBytes + i * 1024);
+  auto slot = [](int blk) { return (uint32_t)(blk % kRingBlocks) * kBlockBytes; };
+  auto dma_w = [&](int ks, int q) {
+    dma16(w.rows(q) + ks * kRowBytes, w.lane_off[q & 1], lds0 + slot(2 * ks) + q * 1024);
   };
-  // Fragments of one 16-deep K half of stage ks: 4 weight and 4 token fragments per lane.
-  auto read_half = [&](int ks, int kk, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
-    const uint8_t* cur = lds + (ks & (kStages - 1)) * kStageBytes;
-    const uint32_t coff = ((uint32_t)(2 * kk + lk) ^ lsw) << 4;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) fa[i] = *(const bf16x8*)(cur + a_row + i * 32 * kRowBytes + coff);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8*)(cur + kOperandBytes + b_row + j * 32 * kRowBytes + coff);
-  };
-  auto mma_half = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-  };
-
-  // Prologue: four stages in flight, stage 0 visible, its first half read.
-#pragma unroll
-  for (int ks = 0; ks < kStages; ++ks)
-    if (ks < nk) issue(ks);
-  constexpr int per_stage = 2 * kDmaPerThread;
-  if (nk >= 4)
-    wait_vm_and_barrier<3 * per_stage>();
-  else if (nk == 3)
-    wait_vm_and_barrier<2 * per_stage>();
-  else if (nk == 2)
-    wait_vm_and_barrier<per_stage>();
-  else
-    wait_vm_and_barrier<0>();
-  bf16x8 a0[4], b0[4], a1[4], b1[4];
-  read_half(0, 0, a0, b0);
-
-  // Steady state.  Each stage: the first half's 16 MFMAs issue with the second half's eight
-  // fragment reads threaded between them; a barrier then makes stage ks+1 visible and frees
-  // this stage's slot; the second half's MFMAs issue with the eight DMAs of stage ks+4 and the
-  // next stage's first-half reads threaded between them.  Interleaving keeps the matrix pipe
-  // busy while the wave issues memory instructions (one wave per SIMD has no other wave to
-  // cover them), reads stay one half ahead of the MFMAs and the DMA four stages ahead.  The
-  // last three stages are peeled so each wait count is a constant on a straight path.
-  auto read_frag = [&](int ks, int kk, int q, bf16x8& dst) {
-    const uint8_t* cur = lds + (ks & (kStages - 1)) * kStageBytes;
-    const uint32_t coff = ((uint32_t)(2 * kk + lk) ^ lsw) << 4;
-    dst = q < 4 ? *(const bf16x8*)(cur + a_row + q * 32 * kRowBytes + coff)
-                : *(const bf16x8*)(cur + kOperandBytes + b_row + (q - 4) * 32 * kRowBytes + coff);
-  };
-  auto dma_one = [&](int ks, int q) {
-    const uint32_t st = lds0 + (uint32_t)(ks & (kStages - 1)) * kStageBytes;
-    if (q < kDmaPerThread)
-      dma16(wbase + ks * kRowBytes, woff[q], st + q * 1024);
+  auto dma_x = [&](int ks, int q) {
+    if constexpr (kGatherX)
+      dma16(x.base + ks * kRowBytes, xoff[q], lds0 + slot(2 * ks + 1) + q * 1024);
     else
-      dma16(xbase + ks * kRowBytes, xoff[q - kDmaPerThread], st + kOperandBytes + (q - kDmaPerThread) * 1024);
+      dma16(x.rows(q) + ks * kRowBytes, x.lane_off[q & 1], lds0 + slot(2 * ks + 1) + q * 1024);
+  };
+  // Fragment q of sub-step kk of K step ks: q < 4 weight rows, else token rows.  The lane
+  // reads logical chunk 2kk + lk of its row, stored at chunk (2kk + lk) ^ lsw = (lk ^ lsw) ^ 2kk;
+  // slot and row offsets are multiples of 128, so the sub-step enters as an XOR of bits 5-6
+  // of one per-operand base and the 32-row block as an immediate offset.
+  const uint32_t a_lane = a_row + (((uint32_t)lk ^ lsw) << 4);
+  const uint32_t b_lane = b_row + (((uint32_t)lk ^ lsw) << 4);
+  auto read_frag = [&](int ks, int kk, int q, bf16x8& dst) {
+    const uint32_t base = q < 4 ? a_lane + slot(2 * ks) : b_lane + slot(2 * ks + 1);
+    dst = *(const bf16x8*)(lds + ((base ^ ((uint32_t)kk << 5)) + (q & 3) * 32 * kRowBytes));
   };
   auto mfma = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4], int q) {
     acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[q >> 2], fb[q & 3], acc[q >> 2][q & 3], 0, 0, 0);
   };
-  auto stage = [&](int ks, auto vm_after) {
-    constexpr int vm = decltype(vm_after)::value;
+
+  // Prologue: K steps 0 and 1 in flight, step 0 visible, its first sub-step read.
+#pragma unroll
+  for (int q = 0; q < kDmaPerThread; ++q) dma_w(0, q);
+#pragma unroll
+  for (int q = 0; q < kDmaPerThread; ++q) dma_x(0, q);
+  if (nk > 1) {
+#pragma unroll
+    for (int q = 0; q < kDmaPerThread; ++q) dma_w(1, q);
+#pragma unroll
+    for (int q = 0; q < kDmaPerThread; ++q) dma_x(1, q);
+    wait_vm_and_barrier<2 * kDmaPerThread>();
+  } else {
+    wait_vm_and_barrier<0>();
+  }
+  bf16x8 a0[4], b0[4], a1[4], b1[4];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) read_frag(0, 0, q, q < 4 ? a0[q] : b0[q - 4]);
+
+  // kind 0: steady step (DMAs, then wait with one block in flight); 1: next to last (no
+  // DMAs, wait for everything); 2: last step (no wait, nothing to read ahead).
+  auto step = [&](int ks, auto kind) {
+    constexpr int kd = decltype(kind)::value;
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       mfma(a0, b0, q);
-      if (q < 8) read_frag(ks, 1, q, q < 4 ? a1[q] : b1[q - 4]);
+      if (q & 1)
+        read_frag(ks, 1, q >> 1, (q >> 1) < 4 ? a1[q >> 1] : b1[(q >> 1) - 4]);
+      else if constexpr (kd == 0)
+        dma_w(ks + 2, q >> 1);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if constexpr (vm >= 0) {
-      wait_vm_and_barrier<vm>();  // stage ks+1 has landed; slot ks % 4 is free
-      // A uniform test per DMA: two unrolled copies of this loop (with and without DMAs)
-      // double the live ranges and spill.
-      const bool more = ks + kStages < nk;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      mfma(a1, b1, q);
+      if (q < 8) read_frag(ks, 2, q, q < 4 ? a0[q] : b0[q - 4]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      mfma(a0, b0, q);
+      if (q < 8) read_frag(ks, 3, q, q < 4 ? a1[q] : b1[q - 4]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (kd < 2) {
+      wait_vm_and_barrier<kd == 0 ? kDmaPerThread : 0>();  // step ks+1 visible, step ks's slots free
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         mfma(a1, b1, q);
-        if (q < 8) {
-          if (more) dma_one(ks + kStages, q);
-        } else {
-          read_frag(ks + 1, 0, q - 8, q < 12 ? a0[q - 8] : b0[q - 12]);
-        }
+        if (q & 1)
+          read_frag(ks + 1, 0, q >> 1, (q >> 1) < 4 ? a0[q >> 1] : b0[(q >> 1) - 4]);
+        else if constexpr (kd == 0)
+          dma_x(ks + 2, q >> 1);
         __builtin_amdgcn_sched_barrier(0);
       }
     } else {
-      mma_half(a1, b1);
-      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        mfma(a1, b1, q);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   };
   int ks = 0;
-  for (; ks + 3 < nk; ++ks) stage(ks, std::integral_constant<int, 2 * per_stage>{});
-  if (ks + 2 < nk) stage(ks++, std::integral_constant<int, per_stage>{});
-  if (ks + 1 < nk) stage(ks++, std::integral_constant<int, 0>{});
-  stage(ks, std::integral_constant<int, -1>{});
+  for (; ks + 2 < nk; ++ks) step(ks, std::integral_constant<int, 0>{});
+  if (ks + 1 < nk) step(ks++, std::integral_constant<int, 1>{});
+  step(ks, std::integral_constant<int, 2>{});
   // All waves are done reading LDS before the epilogue or the next tile reuses it.
   wait_vm_and_barrier<0>();
 }
@@ -256,7 +283,7 @@ __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const uint8_
 // count lets the reduction issue the loads of several blocks of every part at once.
 template <bool down, int kSplit>
 __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t item, uint8_t* lds,
-                                              uint32_t* s_last) {
+                                              uint32_t* words) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave: keeps bases scalar
   const int wn = wave & 1, wm = wave >> 1;
@@ -267,38 +294,47 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
   const TileRow tr = a.tile_rows[t];
   const int64_t H = a.H, F = a.F;
   const int e = tr.expert, lrow0 = tr.lrow0;
-  // Operand rows this lane fetches: row n_i = (wave*4 + i)*16 + lane/4 of each 256-row tile.
-  // Tensors stay below 4 GiB per expert/operand, so per-lane offsets fit in 32 bits and the
-  // bases are wave-uniform (scalar registers).
-  const uint8_t* wbase;
-  const uint8_t* xbase;
-  uint32_t woff[kDmaPerThread], xoff[kDmaPerThread];
-  const uint32_t lrow4 = (uint32_t)lane >> 2;
+  // Operand rows: DMA instruction i of a wave fills tile rows wave*64 + i*8 .. +7.  Tensors
+  // stay below 4 GiB per expert/operand, so per-lane offsets fit in 32 bits and the bases are
+  // wave-uniform (scalar registers).
+  DmaRows w, x;
+  uint32_t xoff[kDmaPerThread];
   if constexpr (!down) {
     // Waves 0 and 2 fetch gate rows (W1), waves 1 and 3 the matching up rows (W3): tile rows
     // 0..63 / 128..191 are gate features, 64..127 / 192..255 the same features' up rows, so
     // each wave's MFMA quadrant holds gate and up of the same 64 features.
-    wbase = (const uint8_t*)((wave & 1) ? a.w3 : a.w1) + (uint64_t)e * F * H * 2;
-    xbase = (const uint8_t*)a.x;
+    const uint32_t stride = (uint32_t)H * 2;
+    w.base = (const uint8_t*)((wave & 1) ? a.w3 : a.w1) + (uint64_t)e * F * H * 2;
+    w.stride = stride;
+    w.g0 = col * kGuTileF + (wave >> 1) * 64;
+    w.gmax = (int)F - kRowsPerDma;
+    w.lane_off[0] = dma_lane_off(lane, 0, stride);
+    w.lane_off[1] = dma_lane_off(lane, 1, stride);
+    // Token rows are gathered from the dispatched rows through row_x.
+    x.base = (const uint8_t*)a.x;
+    const uint32_t r = (uint32_t)lane >> 3;
 #pragma unroll
     for (int i = 0; i < kDmaPerThread; ++i) {
-      const uint32_t n = (uint32_t)(wave * kDmaPerThread + i) * kRowsPerDma + lrow4;
-      const uint32_t ch = ((uint32_t)(lane & 3) ^ swz(n)) * 16;
-      const int f = min(col * kGuTileF + (wave >> 1) * 64 + i * kRowsPerDma + (int)lrow4, (int)F - 1);
-      woff[i] = (uint32_t)f * (uint32_t)H * 2 + ch;
-      xoff[i] = (uint32_t)a.row_x[lrow0 + n] * (uint32_t)H * 2 + ch;
+      const uint32_t n = (uint32_t)(wave * kDmaPerThread + i) * kRowsPerDma + r;
+      // 24-bit multiply (rows < 2^24, stride <= 2^17): a 32-bit result, where a full multiply-add
+      // would produce register pairs whose high halves stay allocated.
+      xoff[i] = __umul24((uint32_t)a.row_x[lrow0 + n], stride) + (((uint32_t)(lane & 7) ^ swz(n)) << 4);
     }
   } else {
-    wbase = (const uint8_t*)a.w2 + (uint64_t)e * H * F * 2;
-    xbase = (const uint8_t*)a.hws + (uint64_t)lrow0 * F * 2;
-#pragma unroll
-    for (int i = 0; i < kDmaPerThread; ++i) {
-      const uint32_t n = (uint32_t)(wave * kDmaPerThread + i) * kRowsPerDma + lrow4;
-      const uint32_t ch = ((uint32_t)(lane & 3) ^ swz(n)) * 16;
-      const int hcol = min(col * kDownTileN + (int)n, (int)H - 1);
-      woff[i] = (uint32_t)hcol * (uint32_t)F * 2 + ch;
-      xoff[i] = n * (uint32_t)F * 2 + ch;
-    }
+    const uint32_t stride = (uint32_t)F * 2;
+    w.base = (const uint8_t*)a.w2 + (uint64_t)e * H * F * 2;
+    w.stride = stride;
+    w.g0 = col * kDownTileN + wave * 64;
+    w.gmax = (int)H - kRowsPerDma;
+    w.lane_off[0] = dma_lane_off(lane, 0, stride);
+    w.lane_off[1] = dma_lane_off(lane, 1, stride);
+    // Token rows are the tile row's own activation rows, contiguous in the workspace.
+    x.base = (const uint8_t*)a.hws + (uint64_t)lrow0 * F * 2;
+    x.stride = stride;
+    x.g0 = wave * 64;
+    x.gmax = kTileM - kRowsPerDma;
+    x.lane_off[0] = w.lane_off[0];
+    x.lane_off[1] = w.lane_off[1];
   }
 
   // K range of this item: all of it, or one of split_k near-equal runs of K steps.
@@ -312,7 +348,9 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     klen = (s1 - s0) * kTileK;
   }
   f32x16 acc[4][4];
-  tile_mma(lds, wbase + kbeg * 2, xbase + kbeg * 2, woff, xoff, klen, acc);
+  w.base += kbeg * 2;
+  x.base += kbeg * 2;
+  tile_mma<!down>(lds, w, x, xoff, klen, acc);
 
   if constexpr (!down) {
     // Gated activation a = bf16(silu(g) * u): lane values -> LDS tile [256 rows][128 features].
@@ -373,10 +411,10 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
       if (tid == 0) {
         const uint32_t prev =
             __hip_atomic_fetch_add(&a.arrivals[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        *s_last = (prev + 1 == (uint32_t)S) ? 1u : 0u;
+        words[1] = (prev + 1 == (uint32_t)S) ? 1u : 0u;
       }
       __syncthreads();
-      if (*s_last == 0) return;  // another part finishes the tile
+      if (words[1] == 0) return;  // another part finishes the tile
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
     // Down-projection output: lane values -> LDS tile [256 rows][256 hidden columns].
@@ -505,23 +543,24 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
 // workgroups are resident.
 template <bool down, int kSplit>
 __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerArgs a) {
-  static_assert(kLdsAlloc >= kLdsBytes, "staging must fit the LDS allocation");
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsAlloc];
-  __shared__ uint32_t s_next, s_last;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsBytes];
+  uint32_t* words = (uint32_t*)(lds + kSharedWords);  // [0] next item, [1] split-K verdict
   const int tid = threadIdx.x;
   if (tid == 0) {
-    s_next = atomicAdd(a.claim, 1u);
-    if (s_next < (uint32_t)a.n_items) atomicAdd(a.active, 1u);
+    words[0] = atomicAdd(a.claim, 1u);
+    if (words[0] < (uint32_t)a.n_items) atomicAdd(a.active, 1u);
   }
   __syncthreads();
-  uint32_t cur = __builtin_amdgcn_readfirstlane(s_next);  // uniform: item fields stay scalar
+  uint32_t cur = __builtin_amdgcn_readfirstlane(words[0]);  // uniform: item fields stay scalar
   while (cur < (uint32_t)a.n_items) {
+    __syncthreads();  // every wave has read the word before the operand ring overwrites it
+    // Claim the next item now; thread 0 holds its index while this one runs and passes it
+    // on through LDS once the operand ring is no longer in use.
+    const uint32_t next = tid == 0 ? atomicAdd(a.claim, 1u) : 0u;
+    producer_item<down, kSplit>(a, a.items[cur], lds, words);
+    if (tid == 0) words[0] = next;
     __syncthreads();
-    // Claim the next item now; its index is read after this one finishes.
-    if (tid == 0) s_next = atomicAdd(a.claim, 1u);
-    producer_item<down, kSplit>(a, a.items[cur], lds, &s_last);
-    __syncthreads();
-    cur = __builtin_amdgcn_readfirstlane(s_next);
+    cur = __builtin_amdgcn_readfirstlane(words[0]);
   }
 }
 

@@ -87,9 +87,9 @@ hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s);
 int producer_blocks_per_cu();
 constexpr int kProducerThreads = 256;
 constexpr int kConsumerThreads = 256;
-constexpr int kCopyUnroll = 5;  // 16-byte vectors per consumer thread and copy chunk
-// Consumer waves per SIMD the register budget must allow: at most 512 / 7 = 72 VGPRs each, so
-// two consumer waves fit beside one producer wave (about 368 of the 512 registers).
-constexpr int kConsumerMinWaves = 7;
+constexpr int kCopyUnroll = 4;  // 16-byte vectors per consumer thread and copy chunk
+// Consumer waves per SIMD the register budget must allow: at most 512 / 8 = 64 VGPRs each, so
+// two consumer waves fit beside one producer wave of up to 384 of the 512 registers.
+constexpr int kConsumerMinWaves = 8;
 
 }  // namespace moe

@@ -15,7 +15,7 @@ namespace moe {
 constexpr int kTileM = 256;
 constexpr int kGuTileF = 128;
 constexpr int kDownTileN = 256;
-constexpr int kTileK = 32;
+constexpr int kTileK = 64;
 
 // Work-item encoding: bit 31 = down tile, bits 30..12 = tile row.  A gate/up item keeps its
 // column tile in bits 11..0.  A down item keeps its column tile in bits 11..4 and, in bits

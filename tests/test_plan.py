@@ -248,8 +248,9 @@ def test_validation_codes_via_plan():
     assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, wl.R, wl.rows)) == B.MOE_EINVAL
     assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, 0, wl.rows, band_rows=48)) == B.MOE_EINVAL
     assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, 0, wl.rows, split_k=17)) == B.MOE_EINVAL
-    assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, 0, wl.rows, split_k=wl.F // 32 + 1)) == B.MOE_EINVAL
+    assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, 0, wl.rows, split_k=wl.F // 64 + 1)) == B.MOE_EINVAL
     assert code(c=cfg_for(65536 + 64, wl.F, wl.E_l, wl.R, 0, wl.rows)) == B.MOE_EUNSUPPORTED
+    assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, 0, 1 << 24)) == B.MOE_EUNSUPPORTED
 
 
 @pytest.mark.parametrize("ffn,want", [(512, 1), (1408, 1), (2048, 1), (6144, 2), (9216, 3), (14336, 4), (32768, 4)])
