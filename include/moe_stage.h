@@ -245,16 +245,19 @@ typedef struct {
  *   MOE_PLAN_TILE_ROWS  int32 [n_tile_rows][4]: expert, first logical row, valid rows, has_remote
  *   MOE_PLAN_ITEMS      uint32 [n_items]: bit 31 = down tile, bits 30..12 tile row; gate/up
  *                       items: bits 11..0 column tile; down items: bits 11..4 column tile,
- *                       bits 3..0 K part (the parts of a tile are adjacent, in part order);
- *                       all gate/up tiles (first launch) precede all down items
+ *                       bits 3..0 K part; all gate/up tiles (first launch) precede all down
+ *                       items, and each launch's items are its 8 per-XCD queues in turn
  *   MOE_PLAN_ROW_X      int32 [n_logical_rows]: dispatched_x row feeding each logical row
  *                       (padding rows repeat a valid row of the same expert)
  *   MOE_PLAN_ROW_RANK   int32 [n_logical_rows]: source rank, -1 for padding
  *   MOE_PLAN_ROW_SLOT   int32 [n_logical_rows]: receive slot, -1 for padding
  *   MOE_PLAN_SEGMENTS   int32 [n_segments][8]: dst rank, rows, first logical row, first slot,
- *                       first flag, flag count, last schedule position it waits for, tile-row
- *                       pieces of its group it covers
+ *                       first flag, flag count, latest queue position (within its XCD queue)
+ *                       of the down items it waits for, tile-row pieces of its group it covers
  *   MOE_PLAN_GROUPS     int32 [n_groups][4]: expert, first logical row, rows, source rank
+ *   MOE_PLAN_QUEUES     int32 [2][9]: per launch (gate/up, then down), queue x of the XCD x
+ *                       workgroups is that launch's items [q[x], q[x+1]); a workgroup whose
+ *                       queue is empty continues with the following queues
  */
 #define MOE_PLAN_TILE_ROWS 0
 #define MOE_PLAN_ITEMS 1
@@ -263,6 +266,7 @@ typedef struct {
 #define MOE_PLAN_ROW_SLOT 4
 #define MOE_PLAN_SEGMENTS 5
 #define MOE_PLAN_GROUPS 6
+#define MOE_PLAN_QUEUES 7
 
 /* `overlapped` selects the plan of moe_stage_run (1) or moe_stage_run_serial (0). */
 int moe_plan_build(const moe_stage_config_t* cfg, int64_t rows, const int32_t* expert_offsets,

@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(PKG, "_lib", "libmoe_stage.so")
 
 MOE_OK, MOE_EINVAL, MOE_EROUTING, MOE_ECAPACITY, MOE_EHIP, MOE_ETIMEOUT, MOE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 MOE_LOCAL_DIRECT, MOE_KERNEL_TIMING, MOE_POISON, MOE_TEST_NO_SIGNAL, MOE_SHARED_CUS, MOE_DIRECT_ALL = 1, 2, 4, 8, 16, 32
-MOE_PLAN_TILE_ROWS, MOE_PLAN_ITEMS, MOE_PLAN_ROW_X, MOE_PLAN_ROW_RANK, MOE_PLAN_ROW_SLOT, MOE_PLAN_SEGMENTS, MOE_PLAN_GROUPS = range(7)
+(MOE_PLAN_TILE_ROWS, MOE_PLAN_ITEMS, MOE_PLAN_ROW_X, MOE_PLAN_ROW_RANK, MOE_PLAN_ROW_SLOT, MOE_PLAN_SEGMENTS,
+ MOE_PLAN_GROUPS, MOE_PLAN_QUEUES) = range(8)
 ERROR_NAMES = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EROUTING", -3: "MOE_ECAPACITY", -4: "MOE_EHIP",
                -5: "MOE_ETIMEOUT", -6: "MOE_EUNSUPPORTED"}
 
@@ -254,7 +255,8 @@ def moe_plan_build(cfg: moe_stage_config_t, expert_offsets, row_src_rank, row_sl
                                       ("row_rank", MOE_PLAN_ROW_RANK, np.int32, 1),
                                       ("row_slot", MOE_PLAN_ROW_SLOT, np.int32, 1),
                                       ("segments", MOE_PLAN_SEGMENTS, np.int32, 8),
-                                      ("groups", MOE_PLAN_GROUPS, np.int32, 4)):
+                                      ("groups", MOE_PLAN_GROUPS, np.int32, 4),
+                                      ("queues", MOE_PLAN_QUEUES, np.int32, 9)):
             need = lib.moe_plan_copy(p, which, None, 0)
             arr = np.empty(need // np.dtype(dt).itemsize, dt)
             if need:

@@ -132,7 +132,7 @@ int check_config(const moe_stage_config_t* c) {
 
 // Byte layout of the device plan blob.
 struct BlobLayout {
-  size_t tile_rows, items, row_x, row_rank, row_slot, segs, ret, total;
+  size_t tile_rows, items, queues, row_x, row_rank, row_slot, segs, ret, total;
 };
 
 BlobLayout blob_layout(int64_t n_tr, int64_t n_items, int64_t n_lrows, int64_t n_segs, int32_t R) {
@@ -140,6 +140,7 @@ BlobLayout blob_layout(int64_t n_tr, int64_t n_items, int64_t n_lrows, int64_t n
   size_t o = 0;
   b.tile_rows = o; o = align256(o + sizeof(TileRow) * (size_t)n_tr);
   b.items = o;     o = align256(o + sizeof(uint32_t) * (size_t)n_items);
+  b.queues = o;    o = align256(o + sizeof(int32_t) * 2 * (kXcds + 1));
   b.row_x = o;     o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
   b.row_rank = o;  o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
   b.row_slot = o;  o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
@@ -190,6 +191,8 @@ int prepare(moe_stage_s* h, bool overlapped, const void* x,
   uint8_t* hs = h->h_stage[si];
   memcpy(hs + lay->tile_rows, P.tile_rows.data(), sizeof(TileRow) * P.tile_rows.size());
   memcpy(hs + lay->items, P.items.data(), sizeof(uint32_t) * P.items.size());
+  memcpy(hs + lay->queues, P.gu_queue.data(), sizeof(int32_t) * (kXcds + 1));
+  memcpy(hs + lay->queues + sizeof(int32_t) * (kXcds + 1), P.down_queue.data(), sizeof(int32_t) * (kXcds + 1));
   memcpy(hs + lay->row_x, P.row_x.data(), sizeof(int32_t) * P.row_x.size());
   memcpy(hs + lay->row_rank, P.row_rank.data(), sizeof(int32_t) * P.row_rank.size());
   memcpy(hs + lay->row_slot, P.row_slot.data(), sizeof(int32_t) * P.row_slot.size());
@@ -237,7 +240,8 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
   a.tile_rows = (const TileRow*)(h->d_plan + lay.tile_rows);
   a.items = (const uint32_t*)(h->d_plan + lay.items) + (down ? P.n_gu : 0);
   a.n_items = down ? P.n_down : P.n_gu;
-  a.claim = down ? &h->ctr->down_next : &h->ctr->gu_next;
+  a.queue = (const int32_t*)(h->d_plan + lay.queues) + (down ? kXcds + 1 : 0);
+  a.claim = down ? h->ctr->down_next : h->ctr->gu_next;
   a.active = down ? &h->ctr->down_active : &h->ctr->gu_active;
   a.row_x = (const int32_t*)(h->d_plan + lay.row_x);
   a.row_rank = (const int32_t*)(h->d_plan + lay.row_rank);
@@ -647,6 +651,7 @@ int moe_combine(const void* recv, int64_t recv_rows, int32_t hidden, const int32
 struct moe_plan_s {
   Plan plan;
   int32_t band_rows = 0;
+  int32_t queues[2 * (kXcds + 1)] = {};  // gate/up then down queue offsets
 };
 
 int moe_plan_build(const moe_stage_config_t* cfg, int64_t rows, const int32_t* off,
@@ -669,6 +674,8 @@ int moe_plan_build(const moe_stage_config_t* cfg, int64_t rows, const int32_t* o
     return set_err(nullptr, rc, msg);
   }
   p->band_rows = overlapped ? c.band_rows : 1;
+  std::copy(p->plan.gu_queue.begin(), p->plan.gu_queue.end(), p->queues);
+  std::copy(p->plan.down_queue.begin(), p->plan.down_queue.end(), p->queues + kXcds + 1);
   *out = p;
   return MOE_OK;
 }
@@ -707,6 +714,7 @@ int64_t moe_plan_copy(moe_plan_t p, int32_t which, void* dst, int64_t bytes) {
     case MOE_PLAN_ROW_SLOT: src = P.row_slot.data(); need = sizeof(int32_t) * P.row_slot.size(); break;
     case MOE_PLAN_SEGMENTS: src = P.segs.data(); need = sizeof(Segment) * P.segs.size(); break;
     case MOE_PLAN_GROUPS: src = P.groups.data(); need = sizeof(Group) * P.groups.size(); break;
+    case MOE_PLAN_QUEUES: src = p->queues; need = sizeof p->queues; break;
     default: return MOE_EINVAL;
   }
   if (!dst) return need;

@@ -538,7 +538,25 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
   }
 }
 
-// Persistent producer: every workgroup claims items from this launch's queue until it is
+// The XCD (accelerator die) this wave runs on: hardware register XCC_ID, bits 3:0.
+__device__ __forceinline__ uint32_t xcc_id() {
+  constexpr int kHwRegXccId = 20;
+  return (uint32_t)__builtin_amdgcn_s_getreg(kHwRegXccId | (0 << 6) | ((4 - 1) << 11)) & (kXcds - 1);
+}
+
+// Claims the next item of this launch: from queue q (initially the workgroup's own XCD's),
+// moving on to the next queue whenever one is empty.  Returns a.n_items once all are empty.
+__device__ __forceinline__ uint32_t claim_item(const ProducerArgs& a, uint32_t& q) {
+  for (int tries = 0; tries < kXcds; ++tries) {
+    const uint32_t i = atomicAdd(&a.claim[q], 1u);
+    const int32_t q0 = a.queue[q], q1 = a.queue[q + 1];
+    if (i < (uint32_t)(q1 - q0)) return (uint32_t)q0 + i;
+    q = (q + 1) & (kXcds - 1);
+  }
+  return (uint32_t)a.n_items;
+}
+
+// Persistent producer: every workgroup claims items from this launch's queues until they are
 // empty.  Nothing inside waits on another workgroup, so progress never depends on which
 // workgroups are resident.
 template <bool down, int kSplit>
@@ -546,8 +564,9 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
   __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsBytes];
   uint32_t* words = (uint32_t*)(lds + kSharedWords);  // [0] next item, [1] split-K verdict
   const int tid = threadIdx.x;
+  uint32_t q = xcc_id();  // meaningful in thread 0, which does the claiming
   if (tid == 0) {
-    words[0] = atomicAdd(a.claim, 1u);
+    words[0] = claim_item(a, q);
     if (words[0] < (uint32_t)a.n_items) atomicAdd(a.active, 1u);
   }
   __syncthreads();
@@ -556,7 +575,7 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
     __syncthreads();  // every wave has read the word before the operand ring overwrites it
     // Claim the next item now; thread 0 holds its index while this one runs and passes it
     // on through LDS once the operand ring is no longer in use.
-    const uint32_t next = tid == 0 ? atomicAdd(a.claim, 1u) : 0u;
+    const uint32_t next = tid == 0 ? claim_item(a, q) : 0u;
     producer_item<down, kSplit>(a, a.items[cur], lds, words);
     if (tid == 0) words[0] = next;
     __syncthreads();
@@ -666,8 +685,10 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   if (i == 0) {
-    a.ctr->gu_next = 0;
-    a.ctr->down_next = 0;
+    for (int x = 0; x < kXcds; ++x) {
+      a.ctr->gu_next[x] = 0;
+      a.ctr->down_next[x] = 0;
+    }
     a.ctr->seg_next = 0;
     a.ctr->gu_active = 0;
     a.ctr->down_active = 0;

@@ -22,7 +22,8 @@ struct ProducerArgs {
   const TileRow* tile_rows;
   const uint32_t* items;   // this launch's work items (all gate/up or all down tiles)
   int32_t n_items;
-  uint32_t* claim;         // queue head of this launch
+  const int32_t* queue;    // [kXcds + 1]: XCD x's queue is items [queue[x], queue[x+1])
+  uint32_t* claim;         // [kXcds] queue heads of this launch
   uint32_t* active;        // count of workgroups that claimed work in this launch
   const int32_t* row_x;    // [n_lrows]
   const int32_t* row_rank; // [n_lrows], -1 = padding

@@ -204,34 +204,62 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
     for (int32_t t = 0; t < n_tr; ++t) order.push_back(t);
   }
 
-  // Band groups: up to band_group consecutive tile rows of one expert (and of one class,
-  // remote or local) sweep the gate/up columns together, so each weight slice is fetched
-  // once per group rather than once per tile row.
-  const int32_t G = std::max<int32_t>(p.band_group, 1);
-  for (int32_t a = 0; a < n_tr;) {
-    int32_t b = a + 1;
-    while (b < n_tr && b - a < G && P.tile_rows[order[b]].expert == P.tile_rows[order[a]].expert &&
-           P.tile_rows[order[b]].has_remote == P.tile_rows[order[a]].has_remote)
-      ++b;
-    for (int32_t j = 0; j < P.gu_per_row; ++j)
-      for (int32_t q = a; q < b; ++q) P.items.push_back(gu_item(order[q], j));
-    a = b;
+  // Per-XCD work queues.  Each XCD has its own L2, and an item streams two operand panels
+  // (a token or activation panel of its tile row and a weight panel of its column) through
+  // it.  So every tile row's items are dealt to the XCDs in 8 contiguous slices -- gate/up
+  // feature tiles, down (K part, column tile) pairs -- and each XCD's queue takes its slice of
+  // a small group of consecutive tile rows (one expert, one class) at a time, columns outer,
+  // rows inner.  The XCD's workgroups then run a block of about 4 rows x 8 columns together
+  // and share each panel through L2; queues follow the schedule order, so tile rows still
+  // finish in that order, each slice being 1/8 of every row's work.  A workgroup whose queue
+  // is empty takes items from the next XCD's queue.
+  auto row_groups = [&](int32_t g) {
+    std::vector<std::pair<int32_t, int32_t>> out;
+    g = std::max<int32_t>(g, 1);
+    for (int32_t a = 0; a < n_tr;) {
+      int32_t b = a + 1;
+      while (b < n_tr && b - a < g && P.tile_rows[order[b]].expert == P.tile_rows[order[a]].expert &&
+             P.tile_rows[order[b]].has_remote == P.tile_rows[order[a]].has_remote)
+        ++b;
+      out.emplace_back(a, b);
+      a = b;
+    }
+    return out;
+  };
+  auto slice = [](int32_t n, int32_t x) { return std::make_pair(x * n / kXcds, (x + 1) * n / kXcds); };
+
+  const auto gu_groups = row_groups(p.gu_group);
+  for (int32_t x = 0; x < kXcds; ++x) {
+    P.gu_queue[x] = (int32_t)P.items.size();
+    const auto cols = slice(P.gu_per_row, x);
+    for (const auto& g : gu_groups)
+      for (int32_t j = cols.first; j < cols.second; ++j)
+        for (int32_t q = g.first; q < g.second; ++q) P.items.push_back(gu_item(order[q], j));
   }
   P.n_gu = (int32_t)P.items.size();
+  P.gu_queue[kXcds] = P.n_gu;
 
   // Down tiles, the signaling GEMM of Section 3.3.1, run after every gate/up tile (a separate
-  // launch on the producer stream).  They follow the remote-first order tile row by tile
-  // row, so the first segments become ready as early as possible; the K parts of one tile
-  // are adjacent, so they run side by side and the tile is ready after 1/split_k of its
-  // sequential time.  A tile is ready once its last part is done.
+  // launch on the producer stream).  A tile is ready once all its K parts are done; its
+  // position in the run is taken as the latest queue position of its parts.
   std::vector<int32_t> pos_of_down((size_t)n_tr * P.down_per_row, -1);
-  for (int32_t q = 0; q < n_tr; ++q)
-    for (int32_t n = 0; n < P.down_per_row; ++n) {
-      const int32_t t = order[q];
-      for (int32_t part = 0; part < p.split_k; ++part) P.items.push_back(down_item(t, n, part));
-      pos_of_down[(size_t)t * P.down_per_row + n] = (int32_t)P.items.size() - 1;
-    }
+  const auto down_groups = row_groups(p.down_group);
+  const int32_t pairs = P.down_per_row * p.split_k;  // (part, column) pairs, part-major
+  for (int32_t x = 0; x < kXcds; ++x) {
+    const int32_t q0 = (int32_t)P.items.size();
+    P.down_queue[x] = q0 - P.n_gu;
+    const auto prs = slice(pairs, x);
+    for (const auto& g : down_groups)
+      for (int32_t pc = prs.first; pc < prs.second; ++pc)
+        for (int32_t q = g.first; q < g.second; ++q) {
+          const int32_t t = order[q], part = pc / P.down_per_row, n = pc % P.down_per_row;
+          P.items.push_back(down_item(t, n, part));
+          int32_t& pos = pos_of_down[(size_t)t * P.down_per_row + n];
+          pos = std::max(pos, (int32_t)P.items.size() - 1 - q0);
+        }
+  }
   P.n_down = (int32_t)P.items.size() - P.n_gu;
+  P.down_queue[kXcds] = P.n_down;
 
   // Combine plan (Section 3.2.3) and segment composition (Section 3.3.2).  A row is ready
   // when the down tiles of its 256-row tile row are, so each owner group is cut at tile-row

@@ -9,6 +9,7 @@
 #pragma once
 #include <stdint.h>
 
+#include <array>
 #include <string>
 #include <vector>
 
@@ -22,7 +23,8 @@ struct PlanParams {
   int32_t mid_pieces = 1;     // x (mgb): tile-row pieces per middle segment
   bool local_direct = true;   // local rows need no transfer
   bool overlapped = true;     // false: plan of the non-overlapped baseline
-  int32_t band_group = 8;     // tile rows that sweep the weight columns together
+  int32_t gu_group = 4;       // tile rows an XCD sweeps its gate/up columns for together
+  int32_t down_group = 4;     // tile rows an XCD sweeps its down (part, column) slice for together
   int32_t split_k = 1;        // K parts per down tile (1..kMaxSplitK)
 };
 
@@ -36,6 +38,9 @@ struct Plan {
   std::vector<Group> groups;
   int64_t n_valid = 0, n_band_pad = 0, n_remote = 0;
   int32_t n_gu = 0, n_down = 0;
+  // Per-XCD work queues of each launch: queue x holds items [q[x], q[x+1]) of that launch
+  // (offsets from the launch's first item).
+  std::array<int32_t, kXcds + 1> gu_queue{}, down_queue{};
   int64_t n_lrows() const { return (int64_t)row_x.size(); }
 };
 

@@ -60,19 +60,22 @@ struct Group {
   int32_t dst_rank;    // the source rank the rows return to
 };
 
+// MI355X has 8 XCDs (accelerator dies), each with its own L2; the workgroups of a launch are
+// dealt to them round-robin.  Each producer launch keeps one work queue per XCD.
+constexpr int kXcds = 8;
+
 // Device-side counters of one run; the queue heads are zeroed by the init kernel.
 struct RunCounters {
-  uint32_t gu_next;         // gate/up work queue head
-  uint32_t seg_next;        // consumer segment queue head
-  uint32_t timeouts;        // bounded waits that expired; NOT reset per run (cleared by a query)
-  uint32_t timeout_where;   // bit 0 = consumer flag wait, bit 1 = producer dependency wait
-  uint64_t poll_iters;      // consumer poll iterations
-  uint64_t wait_ticks;      // consumer wait time, 100 MHz ticks
-  uint32_t down_next;       // down-projection work queue head
-  uint32_t gu_active;       // gate/up workgroups that claimed at least one tile
-  uint32_t down_active;     // down workgroups that claimed at least one tile
-  uint32_t pad0;
-  uint64_t pad[2];
+  uint32_t gu_next[kXcds];    // gate/up work queue heads, one per XCD
+  uint32_t down_next[kXcds];  // down-projection work queue heads
+  uint32_t seg_next;          // consumer segment queue head
+  uint32_t timeouts;          // bounded waits that expired; NOT reset per run (cleared by a query)
+  uint32_t timeout_where;     // bit 0 = consumer flag wait, bit 1 = producer dependency wait
+  uint32_t gu_active;         // gate/up workgroups that claimed at least one tile
+  uint32_t down_active;       // down workgroups that claimed at least one tile
+  uint32_t pad0[3];
+  uint64_t poll_iters;        // consumer poll iterations
+  uint64_t wait_ticks;        // consumer wait time, 100 MHz ticks
 };
 
 }  // namespace moe

@@ -78,11 +78,30 @@ def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True,
     assert len(gu_pos) == n_tr * (info["gu_tiles_per_row"] + info["down_tiles_per_row"] * S)
     assert info["n_down_items"] == n_tr * info["down_tiles_per_row"] * S
     # two launches: every gate/up tile precedes every down item
-    assert np.all(down[:info["n_gu_items"]] == 0) and np.all(down[info["n_gu_items"]:] == 1)
-    # the K parts of a down tile are adjacent and in part order
-    dn = slice(info["n_gu_items"], None)
-    assert np.array_equal(part[dn], np.tile(np.arange(S), len(part[dn]) // S))
-    assert np.all(t[dn][::S, None] == t[dn].reshape(-1, S)) and np.all(col[dn][::S, None] == col[dn].reshape(-1, S))
+    n_gu = info["n_gu_items"]
+    assert np.all(down[:n_gu] == 0) and np.all(down[n_gu:] == 1)
+    # each launch's items are 8 per-XCD queues; every tile row's items are dealt over them in
+    # slices of near-equal size, and the queues take tile rows in one common order
+    qs = p["queues"]
+    assert qs.shape == (2, 9)
+    qpos = np.empty(len(down), np.int64)   # position of each item within its queue
+    for li, (lo, n) in enumerate(((0, n_gu), (n_gu, info["n_down_items"]))):
+        q = qs[li]
+        assert q[0] == 0 and q[8] == n and np.all(np.diff(q) >= 0)
+        lists = []
+        counts = np.zeros((8, n_tr), int)
+        for x in range(8):
+            ts = t[lo + q[x]:lo + q[x + 1]]
+            qpos[lo + q[x]:lo + q[x + 1]] = np.arange(q[x + 1] - q[x])
+            np.add.at(counts[x], ts, 1)
+            seen = list(dict.fromkeys(ts.tolist()))
+            lists.append(seen)
+        assert np.all(counts.max(axis=0) - counts.min(axis=0) <= 1)
+        ref = max(lists, key=len)
+        rank_in_ref = {tt: i for i, tt in enumerate(ref)}
+        for seen in lists:
+            assert all(tt in rank_in_ref for tt in seen)
+            assert [rank_in_ref[tt] for tt in seen] == sorted(rank_in_ref[tt] for tt in seen)
     if not overlapped:
         assert info["n_band_padding"] == 0 and info["n_segments"] == 0
         return
@@ -128,7 +147,8 @@ def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True,
         t0, t1 = y0 // TILE_M, (y0 + nrows - 1) // TILE_M
         dpr = info["down_tiles_per_row"]
         assert fb == t0 * dpr and fc == (t1 - t0 + 1) * dpr
-        assert rp == max(gu_pos[(1, ti, n, S - 1)] for ti in range(t0, t1 + 1) for n in range(dpr))
+        assert rp == max(qpos[gu_pos[(1, ti, n, k)]] for ti in range(t0, t1 + 1) for n in range(dpr)
+                         for k in range(S))
         assert 1 <= nb <= max(mgb, 1)
     need = valid & ((rank != self_rank) | (not local_direct))
     assert np.array_equal(covered, need.astype(int))
@@ -154,11 +174,14 @@ def test_golden_schedule_example():
     check_plan(p, off, src, slot, me, R, tb, 1)
     assert p["tile_rows"][:, 0].tolist() == g["expected_tile_row_experts"]
     down, t, col, _ = decode(p["items"])
-    order = []
-    for ti in t[down == 0]:
-        if ti not in order:
-            order.append(int(ti))
-    assert order == g["expected_tile_row_order"]
+    # every non-empty down queue takes the tile rows in the schedule order
+    q = p["queues"][1]
+    dn = t[down == 1]
+    filled = [x for x in range(8) if q[x + 1] > q[x]]
+    assert filled
+    for x in filled:
+        order = list(dict.fromkeys(dn[q[x]:q[x + 1]].tolist()))
+        assert order == g["expected_tile_row_order"]
     pg = p["groups"]
     for e_glob, want in g["expected_remote_bands"].items():
         e = glob.index(int(e_glob))
