@@ -584,84 +584,81 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
 }
 
 // ---------------------------------------------------------------------------
-// Consumer: claim segments in ready order; wave 0 polls the segment's flags
-// (one flag per lane, all lanes must read the current epoch), then the whole
-// workgroup copies rows * H bf16 with 16-byte loads and stores.
+// Consumer: every wave works alone.  It claims a copy unit -- a quarter of a segment, taken
+// in the segments' ready order, so the four quarters of a segment go to four waves at once
+// -- polls the segment's flags (one flag per lane; all must show the current epoch), then
+// copies its quarter with 16-byte loads and stores.  The kernel uses no LDS, so in a
+// shared-CU run its workgroups never keep a producer workgroup (which takes all of LDS)
+// off a compute unit.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_kernel(ConsumerArgs a) {
-  __shared__ int32_t s_seg;
-  __shared__ uint32_t s_abort;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x & 63;
   uint64_t polls = 0, waited = 0;
   for (;;) {
-    if (tid == 0) {
-      s_seg = (int32_t)atomicAdd(&a.ctr->seg_next, 1u);
-      s_abort = 0;
-    }
-    __syncthreads();
-    const int32_t s = s_seg;
+    uint32_t unit = 0;
+    if (lane == 0) unit = atomicAdd(&a.ctr->seg_next, 1u);
+    unit = __builtin_amdgcn_readfirstlane(unit);  // every lane is active here
+    const int32_t s = (int32_t)(unit / kCopyParts);
+    const int32_t part = (int32_t)(unit % kCopyParts);
     if (s >= a.n_segs) break;
     const Segment sg = a.segs[s];
-    if (wave == 0) {
-      const uint64_t t0 = ticks();
-      bool expired = false;
-      for (int base = 0; base < sg.flag_count && !expired; base += 64) {
-        const bool mine = base + lane < sg.flag_count;
-        const uint32_t* fp = a.flags + sg.flag_begin + base + lane;
-        for (;;) {
-          const uint32_t v =
-              mine ? __hip_atomic_load(fp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : a.epoch;
-          if (__all(v == a.epoch)) break;
-          ++polls;
-          if (ticks() - t0 > a.watchdog_ticks) {
-            expired = true;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
+    const uint64_t t0 = ticks();
+    bool expired = false;
+    for (int base = 0; base < sg.flag_count && !expired; base += 64) {
+      const bool mine = base + lane < sg.flag_count;
+      const uint32_t* fp = a.flags + sg.flag_begin + base + lane;
+      for (;;) {
+        const uint32_t v =
+            mine ? __hip_atomic_load(fp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : a.epoch;
+        if (__all(v == a.epoch)) break;
+        ++polls;
+        if (ticks() - t0 > a.watchdog_ticks) {
+          expired = true;
+          break;
         }
+        __builtin_amdgcn_s_sleep(1);
       }
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      waited += ticks() - t0;
-      if (expired && lane == 0) s_abort = 1;
     }
-    __syncthreads();
-    if (s_abort) {
-      if (tid == 0) {
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    waited += ticks() - t0;
+    if (expired) {
+      if (lane == 0) {
         __hip_atomic_fetch_add(&a.ctr->timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_fetch_or(&a.ctr->timeout_where, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       break;
     }
-    // The segment is contiguous on both sides: a flat 16-byte-vector copy in chunks of
-    // kCopyUnroll vectors per thread, double-buffered: the next chunk's loads are in flight
-    // while the current chunk is stored, so neither load nor store latency is exposed per
-    // chunk.  The last chunk re-reads itself as its "next" (in bounds) instead of branching,
-    // which would drain every outstanding access.
-    const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H);
-    g_u32x4* dst = (g_u32x4*)(a.ret[sg.dst_rank] + (int64_t)sg.slot0 * a.H);
+    // The segment is contiguous on both sides: this wave's quarter is a flat run of 16-byte
+    // vectors, copied in chunks of kCopyUnroll vectors per lane, double-buffered: the next
+    // chunk's loads are in flight while the current chunk is stored.  The last chunk re-reads
+    // itself as its "next" (in bounds) instead of branching, which would drain every
+    // outstanding access.
     const int64_t n16 = (int64_t)sg.rows * a.H / 8;
+    const int64_t i0 = n16 * part / kCopyParts, i1 = n16 * (part + 1) / kCopyParts;
+    const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H) + i0;
+    g_u32x4* dst = (g_u32x4*)(a.ret[sg.dst_rank] + (int64_t)sg.slot0 * a.H) + i0;
+    const int64_t n = i1 - i0;
     constexpr int kU = kCopyUnroll;
-    constexpr int64_t kStep = (int64_t)kU * kConsumerThreads;
-    const int64_t nfull = n16 / kStep;
+    constexpr int64_t kStep = (int64_t)kU * 64;
+    const int64_t nfull = n / kStep;
     if (nfull > 0) {
       u32x4 cur[kU], nxt[kU];
 #pragma unroll
-      for (int u = 0; u < kU; ++u) cur[u] = src[tid + u * kConsumerThreads];
+      for (int u = 0; u < kU; ++u) cur[u] = src[lane + u * 64];
       for (int64_t c = 0; c < nfull; ++c) {
-        const int64_t base = c * kStep + tid;
-        const int64_t next = (c + 1 < nfull ? c + 1 : c) * kStep + tid;
+        const int64_t base = c * kStep + lane;
+        const int64_t next = (c + 1 < nfull ? c + 1 : c) * kStep + lane;
 #pragma unroll
-        for (int u = 0; u < kU; ++u) nxt[u] = src[next + u * kConsumerThreads];
+        for (int u = 0; u < kU; ++u) nxt[u] = src[next + u * 64];
 #pragma unroll
-        for (int u = 0; u < kU; ++u) dst[base + u * kConsumerThreads] = cur[u];
+        for (int u = 0; u < kU; ++u) dst[base + u * 64] = cur[u];
 #pragma unroll
         for (int u = 0; u < kU; ++u) cur[u] = nxt[u];
       }
     }
-    for (int64_t i = nfull * kStep + tid; i < n16; i += kConsumerThreads) dst[i] = src[i];
-    __syncthreads();
+    for (int64_t i = nfull * kStep + lane; i < n; i += 64) dst[i] = src[i];
   }
-  if (wave == 0 && lane == 0 && (polls || waited)) {
+  if (lane == 0 && (polls || waited)) {
     atomicAdd((unsigned long long*)&a.ctr->poll_iters, (unsigned long long)polls);
     atomicAdd((unsigned long long*)&a.ctr->wait_ticks, (unsigned long long)waited);
   }

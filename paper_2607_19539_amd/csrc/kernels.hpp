@@ -88,7 +88,8 @@ hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s);
 int producer_blocks_per_cu();
 constexpr int kProducerThreads = 256;
 constexpr int kConsumerThreads = 256;
-constexpr int kCopyUnroll = 4;  // 16-byte vectors per consumer thread and copy chunk
+constexpr int kCopyUnroll = 4;  // 16-byte vectors per consumer lane and copy chunk
+constexpr int kCopyParts = 4;   // consumer copy units (one wave each) per segment
 // Consumer waves per SIMD the register budget must allow: at most 512 / 8 = 64 VGPRs each, so
 // two consumer waves fit beside one producer wave of up to 384 of the 512 registers.
 constexpr int kConsumerMinWaves = 8;

@@ -68,7 +68,7 @@ constexpr int kXcds = 8;
 struct RunCounters {
   uint32_t gu_next[kXcds];    // gate/up work queue heads, one per XCD
   uint32_t down_next[kXcds];  // down-projection work queue heads
-  uint32_t seg_next;          // consumer segment queue head
+  uint32_t seg_next;          // consumer copy-unit queue head
   uint32_t timeouts;          // bounded waits that expired; NOT reset per run (cleared by a query)
   uint32_t timeout_where;     // bit 0 = consumer flag wait, bit 1 = producer dependency wait
   uint32_t gu_active;         // gate/up workgroups that claimed at least one tile

@@ -72,3 +72,12 @@ def test_every_split_variant_is_instantiated(kernels):
 def test_combine_variants_present(kernels):
     names = set(by_name(kernels, "combine_kernel"))
     assert len(names) == 3, names
+
+
+def test_consumer_leaves_lds_to_the_producer(kernels):
+    """A producer workgroup takes all of a CU's LDS; a consumer workgroup holding any LDS would
+    keep producer workgroups off the compute units the two are meant to share."""
+    (cons,) = by_name(kernels, "consumer_kernel").values()
+    assert int(cons["group_segment_fixed_size"]) == 0
+    for name, f in by_name(kernels, "producer_kernel").items():
+        assert int(f["group_segment_fixed_size"]) == 160 * 1024, name
