@@ -97,13 +97,17 @@ typedef struct {
                                 coalesce x pieces.  >= 1; 0 means 1.                         */
   uint32_t flags;            /* MOE_* flags above                                            */
   int32_t watchdog_ms;       /* bound on every device spin-wait; 0 = 2000 ms                  */
-  int32_t down_split_k;      /* K parts per down-projection tile, 1..16 and <= ffn / 64: each
-                                part accumulates one contiguous K range in fp32 and the part
-                                that finishes last adds the parts in part order and writes the
-                                tile.  Fixed per handle, so results do not depend on the
-                                schedule or the path.  0 picks a default from ffn (long
-                                down-projection tiles are split so their last round fills the
-                                GPU).                                                         */
+  int32_t down_split_k;      /* K parts per down-projection tile, 0..16 and <= ffn / 64.  A
+                                split tile's parts each accumulate one contiguous K range in
+                                fp32; the part that finishes last adds them in part order and
+                                writes the tile.  Nonzero: every tile is split so.  0 (default):
+                                only the tile rows holding the last, partly filled round of 256
+                                down tiles are split, into as many parts as fill that round (at
+                                most 16), so the launch's tail keeps every compute unit busy
+                                for at most 256 fp32 partial tiles of traffic.  Which rows are
+                                split depends on the routing only, never on the launch: with
+                                band_rows = 1 the serial and overlapped runs of a routing give
+                                identical bits.                                               */
 } moe_stage_config_t;
 
 /* Statistics of the most recent run (moe_stage_query). */
@@ -115,8 +119,8 @@ typedef struct {
   int32_t n_tile_rows;      /* 256-row GEMM tile rows                                        */
   int32_t n_groups;         /* owner groups: (local expert, source rank) row groups          */
   int32_t n_gu_items;       /* gate/up tiles                                                */
-  int32_t n_down_items;     /* down-projection work items: tiles x split_k parts (each tile
-                               raises one ready flag when its last part is done)             */
+  int32_t n_down_items;     /* down-projection work items: one per part of each tile (each
+                               tile raises one ready flag when its last part is done)        */
   int32_t n_segments;       /* transfer segments issued by the consumer                      */
   int32_t producer_grid;    /* persistent producer workgroups launched                      */
   int32_t consumer_grid;    /* persistent consumer workgroups launched                      */
@@ -132,8 +136,8 @@ typedef struct {
                                run's gate/up launch (fewer than producer_grid means some
                                were not resident while the queue still held work)            */
   int32_t down_workgroups;  /* the same for the down-projection launch                       */
-  int32_t split_k;          /* K parts per down-projection tile in effect                    */
-  int32_t reserved;
+  int32_t split_k;          /* K parts of each split down-projection tile (1: none split)    */
+  int32_t split_rows;       /* tile rows whose down-projection tiles are split               */
 } moe_stage_stats_t;
 
 /* Accumulated kernel times (MOE_KERNEL_TIMING), milliseconds, over runs since the last reset. */
@@ -236,13 +240,14 @@ typedef struct {
   int32_t gu_tiles_per_row;   /* gate/up tiles per tile row (ffn / 128, rounded up)          */
   int32_t down_tiles_per_row; /* down tiles per tile row (hidden / 256, rounded up)          */
   int32_t tile_m, band_rows;
-  int32_t split_k;            /* K parts per down tile                                        */
-  int32_t reserved;
+  int32_t split_k;            /* K parts of each split down tile (1: none split)             */
+  int32_t split_rows;         /* tile rows whose down tiles are split                         */
   int64_t n_logical_rows, n_valid, n_band_padding, n_remote_rows;
 } moe_plan_info_t;
 
 /* Tables readable with moe_plan_copy:
- *   MOE_PLAN_TILE_ROWS  int32 [n_tile_rows][4]: expert, first logical row, valid rows, has_remote
+ *   MOE_PLAN_TILE_ROWS  int32 [n_tile_rows][6]: expert, first logical row, valid rows,
+ *                       has_remote, K parts of its down tiles, first fp32 partial tile (-1)
  *   MOE_PLAN_ITEMS      uint32 [n_items]: bit 31 = down tile, bits 30..12 tile row; gate/up
  *                       items: bits 11..0 column tile; down items: bits 11..4 column tile,
  *                       bits 3..0 K part; all gate/up tiles (first launch) precede all down

@@ -44,7 +44,7 @@ class moe_stage_stats_t(ctypes.Structure):
                 ("timeout", ctypes.c_int32),
                 ("plan_us", ctypes.c_double), ("poll_iters", ctypes.c_uint64), ("wait_ticks", ctypes.c_uint64),
                 ("gu_workgroups", ctypes.c_int32), ("down_workgroups", ctypes.c_int32),
-                ("split_k", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("split_k", ctypes.c_int32), ("split_rows", ctypes.c_int32)]
 
 
 class moe_stage_times_t(ctypes.Structure):
@@ -57,7 +57,7 @@ class moe_plan_info_t(ctypes.Structure):
                 ("n_down_items", ctypes.c_int32), ("n_segments", ctypes.c_int32), ("n_groups", ctypes.c_int32),
                 ("gu_tiles_per_row", ctypes.c_int32), ("down_tiles_per_row", ctypes.c_int32),
                 ("tile_m", ctypes.c_int32), ("band_rows", ctypes.c_int32), ("split_k", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("n_logical_rows", ctypes.c_int64),
+                ("split_rows", ctypes.c_int32), ("n_logical_rows", ctypes.c_int64),
                 ("n_valid", ctypes.c_int64), ("n_band_padding", ctypes.c_int64), ("n_remote_rows", ctypes.c_int64)]
 
 
@@ -249,7 +249,7 @@ def moe_plan_build(cfg: moe_stage_config_t, expert_offsets, row_src_rank, row_sl
         info = moe_plan_info_t()
         _check(lib.moe_plan_info(p, ctypes.byref(info)))
         out = {"info": _struct_dict(info)}
-        for key, which, dt, width in (("tile_rows", MOE_PLAN_TILE_ROWS, np.int32, 4),
+        for key, which, dt, width in (("tile_rows", MOE_PLAN_TILE_ROWS, np.int32, 6),
                                       ("items", MOE_PLAN_ITEMS, np.uint32, 1),
                                       ("row_x", MOE_PLAN_ROW_X, np.int32, 1),
                                       ("row_rank", MOE_PLAN_ROW_RANK, np.int32, 1),

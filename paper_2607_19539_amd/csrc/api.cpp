@@ -106,7 +106,7 @@ PlanParams params_of(const moe_stage_config_t& c, bool overlapped) {
   p.mid_pieces = std::max(c.mid_segment_pieces, 1);
   p.local_direct = (c.flags & MOE_LOCAL_DIRECT) != 0;
   p.overlapped = overlapped;
-  p.split_k = c.down_split_k > 0 ? c.down_split_k : default_split_k(c.ffn);
+  p.split_k = c.down_split_k;
   return p;
 }
 
@@ -223,7 +223,8 @@ int prepare(moe_stage_s* h, bool overlapped, const void* x,
   st.n_gu_items = P.n_gu;
   st.n_down_items = P.n_down;
   st.n_segments = (int32_t)P.segs.size();
-  st.split_k = P.p.split_k;
+  st.split_k = P.tail_split;
+  st.split_rows = P.n_split_rows;
   return MOE_OK;
 }
 
@@ -330,7 +331,6 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   h->cfg = *cfg;
   if (h->cfg.mid_segment_pieces == 0) h->cfg.mid_segment_pieces = 1;
   if (h->cfg.band_rows == 0) h->cfg.band_rows = 1;
-  if (h->cfg.down_split_k == 0) h->cfg.down_split_k = default_split_k(cfg->ffn);
   auto bail = [&](int code) {
     moe_stage_destroy(h);
     return code;
@@ -355,7 +355,10 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   h->down_per_row = (cfg->hidden + kDownTileN - 1) / kDownTileN;
   const int gu_per_row = (cfg->ffn + kGuTileF - 1) / kGuTileF;
   const int32_t S = h->cfg.down_split_k;
-  const int64_t max_items = (int64_t)h->max_tile_rows * (gu_per_row + (int64_t)h->down_per_row * S);
+  // Down items: one per part of every tile (uniform split), or one per tile plus at most one
+  // round of parts for the split tail rows (default).
+  const int64_t max_items = (int64_t)h->max_tile_rows * (gu_per_row + (int64_t)h->down_per_row * std::max(S, 1)) +
+                            (S == 0 ? kRoundTiles : 0);
   const BlobLayout lay =
       blob_layout(h->max_tile_rows, max_items, h->max_lrows, h->max_lrows, cfg->num_ranks);
   h->plan_cap = lay.total;
@@ -370,9 +373,9 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   const size_t hws_bytes = (size_t)h->max_lrows * cfg->ffn * 2;
   const size_t y_bytes = (size_t)h->max_lrows * cfg->hidden * 2;
   const size_t flag_bytes = (size_t)h->max_tile_rows * h->down_per_row * 4;
-  // One fp32 partial tile (256 threads x 256 accumulators) per K part of every down tile.
+  // One fp32 partial tile (256 threads x 256 accumulators) per K part of a split down tile.
   const size_t part_bytes =
-      S > 1 ? (size_t)h->max_tile_rows * h->down_per_row * S * kProducerThreads * 256 * 4 : 0;
+      (size_t)max_partial_tiles(S, h->max_tile_rows, h->down_per_row) * kProducerThreads * 256 * 4;
   if ((part_bytes && !try_hip(hipMalloc(&h->partials, part_bytes), "hipMalloc(partials)")) ||
       !try_hip(hipMalloc(&h->arrivals, flag_bytes), "hipMalloc(arrivals)") ||
       !try_hip(hipMemset(h->arrivals, 0, flag_bytes), "hipMemset(arrivals)") ||
@@ -693,7 +696,8 @@ int moe_plan_info(moe_plan_t p, moe_plan_info_t* o) {
   o->down_tiles_per_row = P.down_per_row;
   o->tile_m = kTileM;
   o->band_rows = p->band_rows;
-  o->split_k = P.p.split_k;
+  o->split_k = P.tail_split;
+  o->split_rows = P.n_split_rows;
   o->n_logical_rows = P.n_lrows();
   o->n_valid = P.n_valid;
   o->n_band_padding = P.n_band_pad;

@@ -278,7 +278,7 @@ __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const DmaRow
 // One work item; `down` selects a down-projection tile (otherwise a fused gate/up tile).
 // Each kind is its own instantiation so the register allocator sees one straight path.
 // One work item.  kSplit (down tiles only) selects the K-part count at compile time: 1 = whole
-// tiles, 2..4 = that many parts, 0 = any count read from the arguments.  A kernel holding
+// tiles, 2..4 = that many parts, 0 = the count of the item's tile row.  A kernel holding
 // both epilogues would keep copies of the accumulators live across the branch, and a fixed
 // count lets the reduction issue the loads of several blocks of every part at once.
 template <bool down, int kSplit>
@@ -340,7 +340,7 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
   // K range of this item: all of it, or one of split_k near-equal runs of K steps.
   int kbeg = 0, klen = down ? (int)F : (int)H;
   constexpr bool split = kSplit != 1;
-  const int S = kSplit == 0 ? a.split_k : kSplit;
+  const int S = kSplit == 0 ? tr.split : kSplit;
   if (split) {
     const int nk = (int)F / kTileK;
     const int s0 = part * nk / S, s1 = (part + 1) * nk / S;
@@ -394,8 +394,9 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     constexpr int kPartU64 = kProducerThreads * 128;  // 8-byte elements per part tile
     const uint64_t* parts = nullptr;
     if constexpr (split) {
-      parts = (const uint64_t*)a.partials + (size_t)tile * S * kPartU64;
-      uint64_t* mine = (uint64_t*)a.partials + ((size_t)tile * S + part) * kPartU64 + tid;
+      const size_t first = (size_t)tr.part_base + (size_t)col * S;  // this tile's part 0
+      parts = (const uint64_t*)a.partials + first * kPartU64;
+      uint64_t* mine = (uint64_t*)a.partials + (first + part) * kPartU64 + tid;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -434,19 +435,41 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
                     __uint_as_float((uint32_t)hi), __uint_as_float((uint32_t)(hi >> 32))};
     };
     if constexpr (kSplit == 0) {
-      // Any part count: blocks b = (i*4 + j)*4 + q indexed at run time, every part read back.
+      // Any part count: 2 blocks at a time, their parts read back 4 at a time with every
+      // load of a round issued together (a part past the count re-reads the last part and
+      // is not added), and added in part order.
       const uint64_t* src = parts + tid;
+      constexpr int kB = 2, kP = 4;
 #pragma unroll 1
-      for (int b = 0; b < 64; ++b) {
-        float4 s = part_block(src, 0, b);
-        for (int p = 1; p < S; ++p) {
-          const float4 v = part_block(src, p, b);
-          s.x += v.x;
-          s.y += v.y;
-          s.z += v.z;
-          s.w += v.w;
+      for (int b0 = 0; b0 < 64; b0 += kB) {
+        float4 acc4[kB];
+#pragma unroll 1
+        for (int p0 = 0; p0 < S; p0 += kP) {
+          float4 v[kB][kP];
+#pragma unroll
+          for (int u = 0; u < kB; ++u)
+#pragma unroll
+            for (int pp = 0; pp < kP; ++pp) v[u][pp] = part_block(src, min(p0 + pp, S - 1), b0 + u);
+#pragma unroll
+          for (int u = 0; u < kB; ++u)
+#pragma unroll
+            for (int pp = 0; pp < kP; ++pp) {
+              const int p = p0 + pp;
+              if (p == 0) {
+                acc4[u] = v[u][pp];
+              } else if (p < S) {
+                acc4[u].x += v[u][pp].x;
+                acc4[u].y += v[u][pp].y;
+                acc4[u].z += v[u][pp].z;
+                acc4[u].w += v[u][pp].w;
+              }
+            }
         }
-        stage_out(b >> 4, (b >> 2) & 3, b & 3, s);
+#pragma unroll
+        for (int u = 0; u < kB; ++u) {
+          const int b = b0 + u;
+          stage_out(b >> 4, (b >> 2) & 3, b & 3, acc4[u]);
+        }
       }
     } else if constexpr (split) {
       // kSplit parts: all parts read back (this part's too: the same values, and no branch
@@ -576,7 +599,17 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
     // Claim the next item now; thread 0 holds its index while this one runs and passes it
     // on through LDS once the operand ring is no longer in use.
     const uint32_t next = tid == 0 ? claim_item(a, q) : 0u;
-    producer_item<down, kSplit>(a, a.items[cur], lds, words);
+    const uint32_t item = a.items[cur];
+    if constexpr (kSplit < 0) {
+      // Split per tile row: whole tiles take the plain epilogue, split rows the part path.
+      const int t = (int)((item >> kItemRowShift) & (uint32_t)(kMaxTileRows - 1));
+      if (a.tile_rows[t].split == 1)
+        producer_item<down, 1>(a, item, lds, words);
+      else
+        producer_item<down, 0>(a, item, lds, words);
+    } else {
+      producer_item<down, kSplit>(a, item, lds, words);
+    }
     if (tid == 0) words[0] = next;
     __syncthreads();
     cur = __builtin_amdgcn_readfirstlane(words[0]);
@@ -710,6 +743,8 @@ hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream
   const dim3 g(grid), b(kProducerThreads);
   if (!down)
     hipLaunchKernelGGL((producer_kernel<false, 1>), g, b, 0, s, a);
+  else if (a.split_k == 0)
+    hipLaunchKernelGGL((producer_kernel<true, -1>), g, b, 0, s, a);
   else if (a.split_k == 1)
     hipLaunchKernelGGL((producer_kernel<true, 1>), g, b, 0, s, a);
   else if (a.split_k == 2)

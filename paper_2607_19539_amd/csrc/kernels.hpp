@@ -33,8 +33,8 @@ struct ProducerArgs {
   uint32_t epoch;
   int32_t H, F, self_rank, down_per_row;
   uint32_t mode;
-  int32_t split_k;         // K parts per down tile
-  float* partials;         // [tiles][split_k][256 threads x 256] fp32 part sums (split_k > 1)
+  int32_t split_k;         // K parts of every down tile; 0 = per tile row (TileRow::split)
+  float* partials;         // fp32 part tiles (256 threads x 256) from TileRow::part_base on
   uint32_t* arrivals;      // [tiles] parts finished this run (zeroed by the init kernel)
 };
 

@@ -30,7 +30,10 @@ int64_t max_logical_rows(int64_t max_rows, int32_t E_l, int32_t R, int32_t band_
   return max_rows + (int64_t)E_l * ((int64_t)(R - 1) * (tb - 1) + kTileM - 1);
 }
 
-int32_t default_split_k(int32_t ffn) { return std::max(1, std::min(4, ffn / 3072)); }
+int64_t max_partial_tiles(int32_t split_k, int64_t max_tile_rows, int32_t down_per_row) {
+  if (split_k == 0) return kRoundTiles;
+  return split_k > 1 ? max_tile_rows * down_per_row * split_k : 0;
+}
 
 int validate_routing(const PlanParams& p, int64_t rows, const int32_t* off, const int32_t* src,
                      const int32_t* slot, const int64_t* return_rows, std::string* err) {
@@ -95,15 +98,14 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
   P.gu_per_row = (p.F + kGuTileF - 1) / kGuTileF;
   P.down_per_row = (p.H + kDownTileN - 1) / kDownTileN;
 
-  // The baseline uses the conventional expert-contiguous layout: no alignment padding.
+  // The baseline uses no alignment padding.  Both paths order an expert's rows by owner
+  // group (Section 3.2.1, Algorithm 1): remote ranks in ascending order first, the local
+  // rank last; with the default tb_M = 1 the two layouts, and so every tile, coincide.
   const int32_t tb = p.overlapped ? std::max<int32_t>(p.band_rows, 1) : 1;
-
-  // Owner-group order inside an expert (Section 3.2.1, Algorithm 1): remote ranks in
-  // ascending order first, the local rank last.
   std::vector<int32_t> rank_order;
   for (int r = 0; r < p.R; ++r)
-    if (!p.overlapped || r != p.self) rank_order.push_back(r);
-  if (p.overlapped) rank_order.push_back(p.self);
+    if (r != p.self) rank_order.push_back(r);
+  rank_order.push_back(p.self);
 
   std::vector<int32_t> tr_begin(p.E_l, 0), tr_end(p.E_l, 0), remote_bands(p.E_l, 0);
   std::vector<int64_t> bucket_start(p.R + 1);
@@ -141,10 +143,8 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
         P.row_slot.push_back(slot[i]);
       }
       if (r != p.self) P.n_remote += n;
-      if (p.overlapped) {
-        P.groups.push_back(Group{e, (int32_t)pos, (int32_t)n, r});
-        if (r != p.self) remote_bands[e] += (int32_t)((n + tb - 1) / tb);
-      }
+      if (p.overlapped) P.groups.push_back(Group{e, (int32_t)pos, (int32_t)n, r});
+      if (r != p.self) remote_bands[e] += (int32_t)((n + tb - 1) / tb);
       pos += n;
       if (p.overlapped && r != p.self) {
         // Zero-row padding up to the next band boundary (Algorithm 1): the next group then
@@ -168,7 +168,7 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
       P.row_slot.push_back(-1);
     }
     for (int64_t t0 = base; t0 < end; t0 += kTileM) {
-      TileRow tr{e, (int32_t)t0, 0, 0};
+      TileRow tr{e, (int32_t)t0, 0, 0, 1, -1};
       for (int64_t q = t0; q < t0 + kTileM; ++q) {
         if (P.row_rank[q] >= 0) ++tr.nvalid;
         if (P.row_rank[q] >= 0 && P.row_rank[q] != p.self) tr.has_remote = 1;
@@ -181,15 +181,15 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
   if (n_tr >= kMaxTileRows) return fail(err, -3, "too many tile rows");
   if (P.gu_per_row >= kMaxColTiles || P.down_per_row > kMaxDownColTiles)
     return fail(err, -6, "hidden or ffn too large for the work-item encoding");
-  if (p.split_k < 1 || p.split_k > kMaxSplitK || p.split_k > p.F / kTileK)
+  if (p.split_k < 0 || p.split_k > kMaxSplitK || p.split_k > p.F / kTileK)
     return fail(err, -1, "split_k out of range");
 
-  // Remote-first tile schedule (Section 3.2.2): rule (ii) experts by remote band count
-  // (bands of tb_M rows, so remote rows when tb_M = 1), descending, ties by expert id;
-  // rule (i) every tile row holding remote rows before any tile row of only local rows.
+  // Remote-first tile schedule (Section 3.2.2), for both paths: rule (ii) experts by remote
+  // band count (bands of tb_M rows, so remote rows when tb_M = 1), descending, ties by expert
+  // id; rule (i) every tile row holding remote rows before any tile row of only local rows.
   std::vector<int32_t> order;
   order.reserve(n_tr);
-  if (p.overlapped) {
+  {
     std::vector<int32_t> experts(p.E_l);
     std::iota(experts.begin(), experts.end(), 0);
     std::stable_sort(experts.begin(), experts.end(),
@@ -200,25 +200,59 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
     for (int32_t e = 0; e < p.E_l; ++e)
       for (int32_t t = tr_begin[e]; t < tr_end[e]; ++t)
         if (!P.tile_rows[t].has_remote) order.push_back(t);
-  } else {
-    for (int32_t t = 0; t < n_tr; ++t) order.push_back(t);
+  }
+
+  // K parts per down tile.  An explicit split_k splits every tile.  By default only the
+  // tile rows at the end of the schedule are split: the down tiles fill whole rounds of
+  // kRoundTiles, and the tile rows holding the remainder -- the last, partly filled round --
+  // are split into as many parts as that round has room for, so it runs full instead of
+  // leaving most compute units idle, while the added fp32 partial traffic stays within one
+  // round's worth of tiles.  The choice depends on the tile count only, never on the path or
+  // the launch, so a given routing always gets the same parts.
+  const int32_t nk = p.F / kTileK;
+  P.tail_split = 1;
+  P.n_split_rows = 0;
+  if (p.split_k > 0) {
+    P.tail_split = p.split_k;
+    P.n_split_rows = p.split_k > 1 ? n_tr : 0;
+  } else if (n_tr > 0) {
+    const int64_t n_tiles = (int64_t)n_tr * P.down_per_row;
+    const int64_t rem = n_tiles % kRoundTiles;
+    if (rem > 0) {
+      const int32_t rows = (int32_t)((rem + P.down_per_row - 1) / P.down_per_row);
+      const int64_t s = kRoundTiles / ((int64_t)rows * P.down_per_row);
+      const int32_t S = (int32_t)std::min<int64_t>(std::min<int64_t>(s, kMaxSplitK), nk);
+      if (S > 1) {
+        P.tail_split = S;
+        P.n_split_rows = rows;
+      }
+    }
+  }
+  P.n_partials = 0;
+  for (int32_t q = n_tr - P.n_split_rows; q < n_tr; ++q) {
+    TileRow& tr = P.tile_rows[order[q]];
+    tr.split = P.tail_split;
+    tr.part_base = P.n_partials;
+    P.n_partials += P.down_per_row * P.tail_split;
   }
 
   // Per-XCD work queues.  Each XCD has its own L2, and an item streams two operand panels
   // (a token or activation panel of its tile row and a weight panel of its column) through
-  // it.  So every tile row's items are dealt to the XCDs in 8 contiguous slices -- gate/up
-  // feature tiles, down (K part, column tile) pairs -- and each XCD's queue takes its slice of
-  // a small group of consecutive tile rows (one expert, one class) at a time, columns outer,
-  // rows inner.  The XCD's workgroups then run a block of about 4 rows x 8 columns together
-  // and share each panel through L2; queues follow the schedule order, so tile rows still
-  // finish in that order, each slice being 1/8 of every row's work.  A workgroup whose queue
-  // is empty takes items from the next XCD's queue.
-  auto row_groups = [&](int32_t g) {
+  // it.  The work is cut into blocks: a row group (up to 4 consecutive tile rows of one
+  // expert and one class) times one of gc slices of its columns -- gate/up feature tiles,
+  // down (K part, column tile) pairs -- with gc the largest of 8, 4, 2, 1 that leaves at
+  // least 8 columns per slice.  Blocks are dealt round-robin to the XCD queues in schedule
+  // order, and each queue walks its blocks columns outer, rows inner, so an XCD's
+  // workgroups run about 4 rows x 8 columns together and share every panel through L2,
+  // while all queues advance through the schedule at the same pace and tile rows still
+  // finish in schedule order.  A workgroup whose queue is empty takes items from the next
+  // XCD's queue.
+  auto row_groups = [&](int32_t g, int32_t a0, int32_t a1) {
     std::vector<std::pair<int32_t, int32_t>> out;
     g = std::max<int32_t>(g, 1);
-    for (int32_t a = 0; a < n_tr;) {
+    for (int32_t a = a0; a < a1;) {
       int32_t b = a + 1;
-      while (b < n_tr && b - a < g && P.tile_rows[order[b]].expert == P.tile_rows[order[a]].expert &&
+      while (b < a1 && b - a < g && P.tile_rows[order[b]].expert == P.tile_rows[order[a]].expert &&
              P.tile_rows[order[b]].has_remote == P.tile_rows[order[a]].has_remote)
         ++b;
       out.emplace_back(a, b);
@@ -226,15 +260,24 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
     }
     return out;
   };
-  auto slice = [](int32_t n, int32_t x) { return std::make_pair(x * n / kXcds, (x + 1) * n / kXcds); };
+  // Queue x's share of `groups` whose tile rows each hold `cols` columns: push(q, column).
+  // Blocks (row group, column slice) are numbered group-major and dealt round-robin.
+  auto deal = [](int32_t x, const std::vector<std::pair<int32_t, int32_t>>& groups, int32_t cols,
+                 auto&& push) {
+    int32_t gc = kXcds;
+    while (gc > 1 && cols < 8 * gc) gc /= 2;
+    for (size_t gi = 0; gi < groups.size(); ++gi)
+      for (int32_t cs = 0; cs < gc; ++cs) {
+        if ((int32_t)((gi * (size_t)gc + (size_t)cs) % kXcds) != x) continue;
+        for (int32_t c = cs * cols / gc; c < (cs + 1) * cols / gc; ++c)
+          for (int32_t q = groups[gi].first; q < groups[gi].second; ++q) push(q, c);
+      }
+  };
 
-  const auto gu_groups = row_groups(p.gu_group);
+  const auto gu_groups = row_groups(p.gu_group, 0, n_tr);
   for (int32_t x = 0; x < kXcds; ++x) {
     P.gu_queue[x] = (int32_t)P.items.size();
-    const auto cols = slice(P.gu_per_row, x);
-    for (const auto& g : gu_groups)
-      for (int32_t j = cols.first; j < cols.second; ++j)
-        for (int32_t q = g.first; q < g.second; ++q) P.items.push_back(gu_item(order[q], j));
+    deal(x, gu_groups, P.gu_per_row, [&](int32_t q, int32_t j) { P.items.push_back(gu_item(order[q], j)); });
   }
   P.n_gu = (int32_t)P.items.size();
   P.gu_queue[kXcds] = P.n_gu;
@@ -243,20 +286,20 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
   // launch on the producer stream).  A tile is ready once all its K parts are done; its
   // position in the run is taken as the latest queue position of its parts.
   std::vector<int32_t> pos_of_down((size_t)n_tr * P.down_per_row, -1);
-  const auto down_groups = row_groups(p.down_group);
-  const int32_t pairs = P.down_per_row * p.split_k;  // (part, column) pairs, part-major
+  const int32_t n_whole = n_tr - P.n_split_rows;  // whole-tile rows first, split rows last
+  const auto whole_groups = row_groups(p.down_group, 0, n_whole);
+  const auto split_groups = row_groups(p.down_group, n_whole, n_tr);
   for (int32_t x = 0; x < kXcds; ++x) {
     const int32_t q0 = (int32_t)P.items.size();
     P.down_queue[x] = q0 - P.n_gu;
-    const auto prs = slice(pairs, x);
-    for (const auto& g : down_groups)
-      for (int32_t pc = prs.first; pc < prs.second; ++pc)
-        for (int32_t q = g.first; q < g.second; ++q) {
-          const int32_t t = order[q], part = pc / P.down_per_row, n = pc % P.down_per_row;
-          P.items.push_back(down_item(t, n, part));
-          int32_t& pos = pos_of_down[(size_t)t * P.down_per_row + n];
-          pos = std::max(pos, (int32_t)P.items.size() - 1 - q0);
-        }
+    auto push = [&](int32_t q, int32_t pc) {  // pc: (part, column) pair, part-major
+      const int32_t t = order[q], part = pc / P.down_per_row, n = pc % P.down_per_row;
+      P.items.push_back(down_item(t, n, part));
+      int32_t& pos = pos_of_down[(size_t)t * P.down_per_row + n];
+      pos = std::max(pos, (int32_t)P.items.size() - 1 - q0);
+    };
+    deal(x, whole_groups, P.down_per_row, push);
+    deal(x, split_groups, P.down_per_row * P.tail_split, push);
   }
   P.n_down = (int32_t)P.items.size() - P.n_gu;
   P.down_queue[kXcds] = P.n_down;

@@ -25,7 +25,7 @@ struct PlanParams {
   bool overlapped = true;     // false: plan of the non-overlapped baseline
   int32_t gu_group = 4;       // tile rows an XCD sweeps its gate/up columns for together
   int32_t down_group = 4;     // tile rows an XCD sweeps its down (part, column) slice for together
-  int32_t split_k = 1;        // K parts per down tile (1..kMaxSplitK)
+  int32_t split_k = 0;        // K parts of every down tile (1..kMaxSplitK); 0 = split the tail
 };
 
 struct Plan {
@@ -38,6 +38,9 @@ struct Plan {
   std::vector<Group> groups;
   int64_t n_valid = 0, n_band_pad = 0, n_remote = 0;
   int32_t n_gu = 0, n_down = 0;
+  int32_t tail_split = 1;     // K parts of the split tile rows (split_k when uniform)
+  int32_t n_split_rows = 0;   // tile rows whose down tiles are split
+  int32_t n_partials = 0;     // fp32 partial tiles the run uses
   // Per-XCD work queues of each launch: queue x holds items [q[x], q[x+1]) of that launch
   // (offsets from the launch's first item).
   std::array<int32_t, kXcds + 1> gu_queue{}, down_queue{};
@@ -59,10 +62,8 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* expert_offsets,
 int64_t max_logical_rows(int64_t max_rows, int32_t E_l, int32_t R, int32_t band_rows);
 
 
-// Default K parts per down tile: one per 3072 of ffn, at most 4.  A down tile is
-// 2 * 256 * 256 * ffn flops; long tiles make the last, partly filled round of the down launch
-// expensive, and splitting them shrinks that round while the added fp32 partial traffic
-// (about 7/4 x 256 KiB per tile at 4 parts) stays small next to the operand traffic.
-int32_t default_split_k(int32_t ffn);
+// fp32 partial tiles a run may need: uniform splitting keeps one per part of every down tile;
+// the default tail split keeps at most one round's worth (kRoundTiles).
+int64_t max_partial_tiles(int32_t split_k, int64_t max_tile_rows, int32_t down_per_row);
 
 }  // namespace moe

@@ -32,12 +32,17 @@ constexpr int32_t kMaxTileRows = 1 << 19;
 constexpr int32_t kMaxColTiles = 1 << 12;
 constexpr int32_t kMaxDownColTiles = 1 << 8;
 constexpr int32_t kMaxSplitK = 16;
+// Down tiles the producer runs at once on MI355X (one workgroup per compute unit).  The
+// default split (see build_plan) fills the last, partly occupied round of that many tiles.
+constexpr int32_t kRoundTiles = 256;
 
 struct TileRow {
   int32_t expert;      // local expert index
   int32_t lrow0;       // first logical row (multiple of kTileM)
   int32_t nvalid;      // routed (non-padding) rows in this tile row
   int32_t has_remote;  // 1 if any row returns to another rank
+  int32_t split;       // K parts of each of its down tiles (1 = whole tiles)
+  int32_t part_base;   // first fp32 partial tile of its parts (split > 1), else -1
 };
 
 struct Segment {

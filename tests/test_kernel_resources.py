@@ -57,15 +57,16 @@ def test_consumer_fits_beside_a_producer_wave(kernels):
     budget = SIMD_REGISTERS - CONSUMER_WAVES_BESIDE_PRODUCER * cons_alloc
     # The launches taken by default (split 1 to 4 parts) must leave that room.
     for name, f in by_name(kernels, "producer_kernel").items():
-        split = int(re.search(r"ILb[01]ELi(\d+)E", name).group(1))
-        if split in (1, 2, 3, 4):
+        tag = re.search(r"ILb[01]ELi(n?\d+)E", name).group(1)
+        split = -int(tag[1:]) if tag.startswith("n") else int(tag)
+        if split in (-1, 1, 2, 3, 4):
             assert int(f["vgpr_count"]) <= budget, (name, f["vgpr_count"], budget)
         assert int(f["agpr_count"]) == 256, name
 
 
 def test_every_split_variant_is_instantiated(kernels):
     names = set(by_name(kernels, "producer_kernel"))
-    for down, split in ((0, 1), (1, 1), (1, 2), (1, 3), (1, 4), (1, 0)):
+    for down, split in ((0, 1), (1, 1), (1, 2), (1, 3), (1, 4), (1, 0), (1, "n1")):
         assert any(f"ILb{down}ELi{split}E" in n for n in names), (down, split)
 
 

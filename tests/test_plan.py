@@ -61,22 +61,33 @@ def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True,
     e_of_row = np.searchsorted(off, np.arange(rows), side="right") - 1
     tr = p["tile_rows"]
     assert np.all(tr[:, 1] % TILE_M == 0)
-    for t, (e, l0, nvalid, has_remote) in enumerate(tr):
+    for t, (e, l0, nvalid, has_remote, *_split) in enumerate(tr):
         seg = slice(l0, l0 + TILE_M)
         assert np.all(e_of_row[rx[seg]] == e)
         assert nvalid == valid[seg].sum()
         assert has_remote == int(np.any(valid[seg] & (rank[seg] != self_rank)))
     # items: each gate/up tile and each K part of each down tile exactly once
     down, t, col, part = decode(p["items"])
-    S = info["split_k"]
     n_tr = len(tr)
+    dpr = info["down_tiles_per_row"]
+    # K parts per tile row: one split count for the split rows, 1 elsewhere; the split rows'
+    # partial tiles are numbered consecutively
+    splits = tr[:, 4]
+    assert set(np.unique(splits).tolist()) <= {1, info["split_k"]}
+    assert int(np.sum(splits > 1)) == info["split_rows"]
+    split_rows = np.flatnonzero(splits > 1)
+    bases = sorted(int(b) for b in tr[split_rows, 5])
+    assert bases == [i * dpr * info["split_k"] for i in range(len(split_rows))]
+    assert np.all(tr[splits == 1, 5] == -1)
     gu_pos = {}
     for pos, (d, ti, c, k) in enumerate(zip(down, t, col, part)):
         key = (d, ti, c, k)
         assert key not in gu_pos
         gu_pos[key] = pos
-    assert len(gu_pos) == n_tr * (info["gu_tiles_per_row"] + info["down_tiles_per_row"] * S)
-    assert info["n_down_items"] == n_tr * info["down_tiles_per_row"] * S
+    assert info["n_down_items"] == int(np.sum(splits)) * dpr
+    assert len(gu_pos) == n_tr * info["gu_tiles_per_row"] + info["n_down_items"]
+    for (d, ti, c, k) in gu_pos:
+        assert k < (splits[ti] if d else 1)
     # two launches: every gate/up tile precedes every down item
     n_gu = info["n_gu_items"]
     assert np.all(down[:n_gu] == 0) and np.all(down[n_gu:] == 1)
@@ -96,12 +107,32 @@ def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True,
             np.add.at(counts[x], ts, 1)
             seen = list(dict.fromkeys(ts.tolist()))
             lists.append(seen)
-        assert np.all(counts.max(axis=0) - counts.min(axis=0) <= 1)
-        ref = max(lists, key=len)
-        rank_in_ref = {tt: i for i, tt in enumerate(ref)}
+        for ti in range(n_tr):   # the queues holding a tile row share it near-evenly
+            nz = counts[:, ti][counts[:, ti] > 0]
+            assert len(nz) == 0 or nz.max() - nz.min() <= 1
+        # one schedule order explains every queue: the precedences the queues show are acyclic
+        after = {tt: set() for tt in range(n_tr)}
         for seen in lists:
-            assert all(tt in rank_in_ref for tt in seen)
-            assert [rank_in_ref[tt] for tt in seen] == sorted(rank_in_ref[tt] for tt in seen)
+            for a_, b_ in zip(seen, seen[1:]):
+                after[a_].add(b_)
+        indeg = {tt: 0 for tt in range(n_tr)}
+        for a_ in after:
+            for b_ in after[a_]:
+                indeg[b_] += 1
+        ready = [tt for tt in range(n_tr) if indeg[tt] == 0]
+        done = 0
+        while ready:
+            a_ = ready.pop()
+            done += 1
+            for b_ in after[a_]:
+                indeg[b_] -= 1
+                if indeg[b_] == 0:
+                    ready.append(b_)
+        assert done == n_tr, "queues take tile rows in contradicting orders"
+        # remote-first: within a queue no tile row holding remote rows follows a local-only one
+        for seen in lists:
+            hr = [int(tr[tt, 3]) for tt in seen]
+            assert hr == sorted(hr, reverse=True)
     if not overlapped:
         assert info["n_band_padding"] == 0 and info["n_segments"] == 0
         return
@@ -145,10 +176,9 @@ def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True,
         assert np.array_equal(lslot[y0:y0 + nrows], s0 + np.arange(nrows))
         covered[y0:y0 + nrows] += 1
         t0, t1 = y0 // TILE_M, (y0 + nrows - 1) // TILE_M
-        dpr = info["down_tiles_per_row"]
         assert fb == t0 * dpr and fc == (t1 - t0 + 1) * dpr
         assert rp == max(qpos[gu_pos[(1, ti, n, k)]] for ti in range(t0, t1 + 1) for n in range(dpr)
-                         for k in range(S))
+                         for k in range(splits[ti]))
         assert 1 <= nb <= max(mgb, 1)
     need = valid & ((rank != self_rank) | (not local_direct))
     assert np.array_equal(covered, need.astype(int))
@@ -174,14 +204,17 @@ def test_golden_schedule_example():
     check_plan(p, off, src, slot, me, R, tb, 1)
     assert p["tile_rows"][:, 0].tolist() == g["expected_tile_row_experts"]
     down, t, col, _ = decode(p["items"])
-    # every non-empty down queue takes the tile rows in the schedule order
+    # every down queue takes its tile rows in the schedule order, and together they take all
     q = p["queues"][1]
     dn = t[down == 1]
-    filled = [x for x in range(8) if q[x + 1] > q[x]]
-    assert filled
-    for x in filled:
+    want = g["expected_tile_row_order"]
+    rank_of = {tt: i for i, tt in enumerate(want)}
+    seen = set()
+    for x in range(8):
         order = list(dict.fromkeys(dn[q[x]:q[x + 1]].tolist()))
-        assert order == g["expected_tile_row_order"]
+        assert [rank_of[tt] for tt in order] == sorted(rank_of[tt] for tt in order)
+        seen |= set(order)
+    assert seen == set(want)
     pg = p["groups"]
     for e_glob, want in g["expected_remote_bands"].items():
         e = glob.index(int(e_glob))
@@ -276,14 +309,54 @@ def test_validation_codes_via_plan():
     assert code(c=cfg_for(wl.H, wl.F, wl.E_l, wl.R, 0, 1 << 24)) == B.MOE_EUNSUPPORTED
 
 
-@pytest.mark.parametrize("ffn,want", [(512, 1), (1408, 1), (2048, 1), (6144, 2), (9216, 3), (14336, 4), (32768, 4)])
-def test_default_split_k(ffn, want):
-    """Default K parts per down tile: one per 3072 of ffn, between 1 and 4."""
-    off = np.array([0, 4], np.int32)
-    p = B.moe_plan_build(cfg_for(256, ffn, 1, 1, 0, 4), off, np.zeros(4, np.int32),
-                         np.arange(4, dtype=np.int32), np.array([4], np.int64))
-    assert p["info"]["split_k"] == want
-    assert p["info"]["n_down_items"] == want
+def _tail_case(H, F, tile_rows_per_expert, E_l=1, split_k=0, overlapped=True):
+    """A routing whose experts each fill exactly `tile_rows_per_expert` 256-row tile rows."""
+    n = 256 * tile_rows_per_expert
+    off = np.arange(E_l + 1, dtype=np.int32) * n
+    rows = int(off[-1])
+    return B.moe_plan_build(cfg_for(H, F, E_l, 1, 0, rows, 1, split_k=split_k), off,
+                            np.zeros(rows, np.int32), np.arange(rows, dtype=np.int32),
+                            np.array([rows], np.int64), overlapped=overlapped)
+
+
+@pytest.mark.parametrize("H,F,rows_per_expert,E_l,want_rows,want_split", [
+    (4096, 14336, 16, 2, 0, 1),      # 32 tile rows x 16 tiles = 512: two full rounds
+    (4096, 14336, 33, 1, 1, 16),     # 33 x 16 = 528 tiles: the last row's 16 tiles split 16 ways
+    (4096, 2048, 33, 1, 1, 16),
+    (4096, 512, 33, 1, 1, 8),        # capped at the 8 K steps of ffn 512
+    (7168, 2048, 127, 1, 0, 1),      # 127 x 28 = 3556: the last round is 89 % full, no split
+    (2048, 1408, 3, 1, 3, 10),       # 24 tiles in all: 256 // 24 = 10 parts
+    (256, 512, 1, 1, 1, 8),          # one tile: as many parts as K steps (8)
+])
+def test_default_split_fills_the_last_round(H, F, rows_per_expert, E_l, want_rows, want_split):
+    """Default split: only the tile rows of the last, partly filled round of 256 down tiles
+    are split, into as many parts as that round has room for (at most 16 and ffn/64)."""
+    p = _tail_case(H, F, rows_per_expert, E_l)
+    info = p["info"]
+    assert info["split_rows"] == want_rows and info["split_k"] == want_split
+    tr = p["tile_rows"]
+    dpr = info["down_tiles_per_row"]
+    assert int(np.sum(tr[:, 4] > 1)) == want_rows
+    assert int(np.sum(tr[:, 4] > 1)) * dpr * info["split_k"] <= 256
+    # the split rows are the last rows of the schedule: their items end every down queue
+    down, t, _, part = decode(p["items"])
+    q = p["queues"][1]
+    dn_t, dn_part = t[down == 1], part[down == 1]
+    split_set = set(np.flatnonzero(tr[:, 4] > 1).tolist())
+    for x in range(8):
+        ts = dn_t[q[x]:q[x + 1]].tolist()
+        flags = [tt in split_set for tt in ts]
+        assert flags == sorted(flags)   # whole-tile items first, then split items
+    # serial and overlapped plans split the same rows (same layout and order at tb_M = 1)
+    ps = _tail_case(H, F, rows_per_expert, E_l, overlapped=False)
+    assert np.array_equal(ps["tile_rows"], tr)
+
+
+def test_explicit_split_splits_every_tile():
+    p = _tail_case(4096, 14336, 3, 1, split_k=3)
+    assert p["info"]["split_k"] == 3 and p["info"]["split_rows"] == 3
+    assert np.all(p["tile_rows"][:, 4] == 3)
+    assert p["info"]["n_down_items"] == 3 * 16 * 3
 
 
 def test_split_k_part_ranges_cover_k():
