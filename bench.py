@@ -210,6 +210,14 @@ class Bench:
                 "GBps": nbytes / (us * 1e-6) / 1e9, "frac_of_hbm_peak": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
 
 
+def down_kernel_name(split_k, st):
+    """Instantiation the down launch runs: whole tiles with split tail rows by default."""
+    if split_k == 0:
+        return (f"moe::producer_kernel<true, -1> (down launch: whole tiles, last {st['split_rows']} "
+                f"tile rows split {st['split_k']} ways)")
+    return f"moe::producer_kernel<true, {split_k if split_k <= 4 else 0}> (down launch, {split_k} K parts)"
+
+
 def summarize(wl, ser, ovl, sweep):
     """Per-workload figures: stage times, producer launches, throughput against the bf16 peak."""
     flops = wl.flops()
@@ -309,6 +317,7 @@ def main():
                              "cu_split": args.cu_split, "consumer_cus": st.get("consumer_cus", 0),
                              "cu_mode": args.mode, "band_rows": args.band_rows or 1,
                              "mid_segment_pieces": args.mgb, "down_split_k": st["split_k"],
+                             "down_split_rows": st["split_rows"],
                              "padding_rows": int(st["n_logical_rows"] - st["n_valid"]),
                              "plan_us": round(st["plan_us"], 1), "seed": args.seed}
             # Dominant kernel: the gate/up launch of the producer (4*H*F flops per routed row, two
@@ -327,7 +336,7 @@ def main():
             out["roofline_down"] = {"bound": "mfma", "achieved": dn_flops / (dn_ms * 1e-3) / 1e12,
                                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                                     "frac": dn_flops / (dn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
-                                    "kernel": f"moe::producer_kernel<true, {st['split_k']}> (down launch)",
+                                    "kernel": down_kernel_name(args.split_k, st),
                                     "flops_per_launch": dn_flops, "launch_us": dn_ms * 1e3}
             prod = wl.flops() / (main_r["producer_ms"] * 1e-3) / 1e12
             out["producer"] = {"us": main_r["producer_ms"] * 1e3, "tflops": prod, "frac": prod / PEAK_BF16_TFLOPS}
