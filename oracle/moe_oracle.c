@@ -14,7 +14,9 @@
  *     y = W2_e * bf16( silu(W1_e x) (.) (W3_e x) ),   silu(g) = g / (1 + e^-g),
  * and for every routed row i of local expert e:
  *     return_bufs[src[i]][slot[i], :] = bf16_rne(y_i).
- * Nothing else in the return buffers is written.  The row layout, tile
+ * Nothing else in the return buffers is written.  moe_oracle_combine adds the
+ * step after (Section 2.1, step 5): each source rank's gate-weighted sum of
+ * its tokens' returned rows.  The row layout, tile
  * schedule, segments and overlap of the paper's method (Section 3) change
  * only when and where rows are computed, never their values, so the oracle
  * has none of them.
