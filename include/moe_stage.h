@@ -262,7 +262,9 @@ typedef struct {
  *   MOE_PLAN_GROUPS     int32 [n_groups][4]: expert, first logical row, rows, source rank
  *   MOE_PLAN_QUEUES     int32 [2][9]: per launch (gate/up, then down), queue x of the XCD x
  *                       workgroups is that launch's items [q[x], q[x+1]); a workgroup whose
- *                       queue is empty continues with the following queues
+ *                       queue is empty continues with the following queues.  The queues are
+ *                       the launch's item sequence in schedule order dealt round-robin in
+ *                       chunks of 32 items (queue x holds chunks x, x + 8, ...)
  */
 #define MOE_PLAN_TILE_ROWS 0
 #define MOE_PLAN_ITEMS 1

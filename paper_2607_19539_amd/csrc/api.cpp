@@ -237,6 +237,7 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
   a.w3 = (const uint16_t*)w3;
   a.w2 = (const uint16_t*)w2;
   a.hws = h->hws;
+  a.hws_rows = h->max_lrows;
   a.y = h->y;
   a.tile_rows = (const TileRow*)(h->d_plan + lay.tile_rows);
   a.items = (const uint32_t*)(h->d_plan + lay.items) + (down ? P.n_gu : 0);

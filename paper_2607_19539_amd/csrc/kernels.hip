@@ -134,6 +134,7 @@ struct DmaRows {
   uint32_t stride;
   int32_t g0, gmax;
   uint32_t lane_off[2];
+  uint32_t step;  // bytes from one K step of a row to the next (128 when rows are K-contiguous)
   __device__ __forceinline__ const uint8_t* rows(int i) const {
     return base + (uint64_t)(uint32_t)min(g0 + 8 * i, gmax) * stride;
   }
@@ -183,13 +184,13 @@ __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const DmaRow
   const uint32_t lds0 = lds_addr(lds) + dma_off;
   auto slot = [](int blk) { return (uint32_t)(blk % kRingBlocks) * kBlockBytes; };
   auto dma_w = [&](int ks, int q) {
-    dma16(w.rows(q) + ks * kRowBytes, w.lane_off[q & 1], lds0 + slot(2 * ks) + q * 1024);
+    dma16(w.rows(q) + (size_t)ks * w.step, w.lane_off[q & 1], lds0 + slot(2 * ks) + q * 1024);
   };
   auto dma_x = [&](int ks, int q) {
     if constexpr (kGatherX)
-      dma16(x.base + ks * kRowBytes, xoff[q], lds0 + slot(2 * ks + 1) + q * 1024);
+      dma16(x.base + (size_t)ks * x.step, xoff[q], lds0 + slot(2 * ks + 1) + q * 1024);
     else
-      dma16(x.rows(q) + ks * kRowBytes, x.lane_off[q & 1], lds0 + slot(2 * ks + 1) + q * 1024);
+      dma16(x.rows(q) + (size_t)ks * x.step, x.lane_off[q & 1], lds0 + slot(2 * ks + 1) + q * 1024);
   };
   // Fragment q of sub-step kk of K step ks: q < 4 weight rows, else token rows.  The lane
   // reads logical chunk 2kk + lk of its row, stored at chunk (2kk + lk) ^ lsw = (lk ^ lsw) ^ 2kk;
@@ -310,8 +311,10 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     w.gmax = (int)F - kRowsPerDma;
     w.lane_off[0] = dma_lane_off(lane, 0, stride);
     w.lane_off[1] = dma_lane_off(lane, 1, stride);
+    w.step = kRowBytes;
     // Token rows are gathered from the dispatched rows through row_x.
     x.base = (const uint8_t*)a.x;
+    x.step = kRowBytes;
     const uint32_t r = (uint32_t)lane >> 3;
 #pragma unroll
     for (int i = 0; i < kDmaPerThread; ++i) {
@@ -328,13 +331,16 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     w.gmax = (int)H - kRowsPerDma;
     w.lane_off[0] = dma_lane_off(lane, 0, stride);
     w.lane_off[1] = dma_lane_off(lane, 1, stride);
-    // Token rows are the tile row's own activation rows, contiguous in the workspace.
-    x.base = (const uint8_t*)a.hws + (uint64_t)lrow0 * F * 2;
-    x.stride = stride;
+    w.step = kRowBytes;
+    // Token rows are the tile row's own activation rows in the K-blocked workspace: the 256
+    // rows' 64 features of one K step are one contiguous 32 KiB block.
+    x.base = (const uint8_t*)a.hws + (uint64_t)lrow0 * kRowBytes;
+    x.stride = kRowBytes;
     x.g0 = wave * 64;
     x.gmax = kTileM - kRowsPerDma;
-    x.lane_off[0] = w.lane_off[0];
-    x.lane_off[1] = w.lane_off[1];
+    x.lane_off[0] = dma_lane_off(lane, 0, kRowBytes);
+    x.lane_off[1] = dma_lane_off(lane, 1, kRowBytes);
+    x.step = (uint32_t)a.hws_rows * kRowBytes;
   }
 
   // K range of this item: all of it, or one of split_k near-equal runs of K steps.
@@ -348,8 +354,8 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     klen = (s1 - s0) * kTileK;
   }
   f32x16 acc[4][4];
-  w.base += kbeg * 2;
-  x.base += kbeg * 2;
+  w.base += (size_t)(kbeg / kTileK) * w.step;
+  x.base += (size_t)(kbeg / kTileK) * x.step;
   tile_mma<!down>(lds, w, x, xoff, klen, acc);
 
   if constexpr (!down) {
@@ -374,15 +380,17 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
         }
     }
     __syncthreads();
-    // 16 threads store one 256-byte activation row; 16 rows per pass.
+    // 16 threads store one row's 128 features: 8 threads per 64-feature K block of the
+    // workspace [F / 64][hws_rows][64], so consecutive rows fill contiguous 128-byte runs.
     const int c16 = tid & 15;
     const int f = col * kGuTileF + c16 * 8;
+    uint16_t* blk = a.hws + ((size_t)(f / kTileK) * a.hws_rows) * kTileK + (f % kTileK);
 #pragma unroll 4
     for (int p = 0; p < kTileM / 16; ++p) {
       const int m = p * 16 + (tid >> 4);
       const int lrow = lrow0 + m;
       if (a.row_rank[lrow] >= 0 && f < F)  // padding rows are never read back
-        *(u32x4*)(a.hws + (int64_t)lrow * F + f) = *(const u32x4*)(lds + m * kGuOutStride + c16 * 16);
+        *(u32x4*)(blk + (size_t)lrow * kTileK) = *(const u32x4*)(lds + m * kGuOutStride + c16 * 16);
     }
   } else {
     // Split K: every part stores its fp32 accumulators (in register order, so each thread

@@ -17,7 +17,8 @@ struct ProducerArgs {
   const uint16_t* w1;      // [E_l, F, H]
   const uint16_t* w3;      // [E_l, F, H]
   const uint16_t* w2;      // [E_l, H, F]
-  uint16_t* hws;           // [n_lrows, F] gated activation (workspace)
+  uint16_t* hws;           // [F / 64][hws_rows][64] gated activation (workspace, K-blocked)
+  int64_t hws_rows;        // rows per K block of the workspace (the handle's row capacity)
   uint16_t* y;             // [n_lrows, H] staged output (workspace)
   const TileRow* tile_rows;
   const uint32_t* items;   // this launch's work items (all gate/up or all down tiles)

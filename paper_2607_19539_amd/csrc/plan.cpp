@@ -238,15 +238,15 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
 
   // Per-XCD work queues.  Each XCD has its own L2, and an item streams two operand panels
   // (a token or activation panel of its tile row and a weight panel of its column) through
-  // it.  The work is cut into blocks: a row group (up to 4 consecutive tile rows of one
-  // expert and one class) times one of gc slices of its columns -- gate/up feature tiles,
-  // down (K part, column tile) pairs -- with gc the largest of 8, 4, 2, 1 that leaves at
-  // least 8 columns per slice.  Blocks are dealt round-robin to the XCD queues in schedule
-  // order, and each queue walks its blocks columns outer, rows inner, so an XCD's
-  // workgroups run about 4 rows x 8 columns together and share every panel through L2,
-  // while all queues advance through the schedule at the same pace and tile rows still
-  // finish in schedule order.  A workgroup whose queue is empty takes items from the next
-  // XCD's queue.
+  // it.  Each launch's items are laid out in schedule order as blocks: a row group (up to 4
+  // consecutive tile rows of one expert and one class) times a slice of its columns -- gate/up
+  // feature tiles, down (K part, column tile) pairs -- wide enough for about 32 items, columns
+  // outer and rows inner.  That sequence is cut into chunks of 32 items dealt round-robin to
+  // the XCD queues, so every queue holds the same work to within one chunk (whatever the
+  // row-group sizes) and advances through the schedule at the same pace (tile rows still
+  // finish in schedule order), and an XCD's 32 CUs run about 4 rows x 8 columns at once,
+  // sharing every panel through L2.  A workgroup whose queue is empty takes items from the
+  // next XCD's queue.
   auto row_groups = [&](int32_t g, int32_t a0, int32_t a1) {
     std::vector<std::pair<int32_t, int32_t>> out;
     g = std::max<int32_t>(g, 1);
@@ -260,25 +260,30 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
     }
     return out;
   };
-  // Queue x's share of `groups` whose tile rows each hold `cols` columns: push(q, column).
-  // Blocks (row group, column slice) are numbered group-major and dealt round-robin.
-  auto deal = [](int32_t x, const std::vector<std::pair<int32_t, int32_t>>& groups, int32_t cols,
-                 auto&& push) {
-    int32_t gc = kXcds;
-    while (gc > 1 && cols < 8 * gc) gc /= 2;
-    for (size_t gi = 0; gi < groups.size(); ++gi)
-      for (int32_t cs = 0; cs < gc; ++cs) {
-        if ((int32_t)((gi * (size_t)gc + (size_t)cs) % kXcds) != x) continue;
-        for (int32_t c = cs * cols / gc; c < (cs + 1) * cols / gc; ++c)
-          for (int32_t q = groups[gi].first; q < groups[gi].second; ++q) push(q, c);
-      }
+  // Appends the blocks of `groups` (tile rows of `cols` columns each) to `seq` as (q, column).
+  auto blocks = [&](const std::vector<std::pair<int32_t, int32_t>>& groups, int32_t cols,
+                    std::vector<std::pair<int32_t, int32_t>>* seq) {
+    for (const auto& g : groups) {
+      const int32_t w = std::max<int32_t>(1, kQueueChunk / (g.second - g.first));
+      for (int32_t c0 = 0; c0 < cols; c0 += w)
+        for (int32_t c = c0; c < std::min(cols, c0 + w); ++c)
+          for (int32_t q = g.first; q < g.second; ++q) seq->emplace_back(q, c);
+    }
   };
+  // Deals `seq` to the XCD queues in chunks of kQueueChunk items, round-robin: queue x gets
+  // chunks x, x + 8, ...; calls begin_queue(x) and push(q, column) queue by queue.
+  auto deal = [&](const std::vector<std::pair<int32_t, int32_t>>& seq, auto&& begin_queue, auto&& push) {
+    for (int32_t x = 0; x < kXcds; ++x) {
+      begin_queue(x);
+      for (size_t c0 = (size_t)x * kQueueChunk; c0 < seq.size(); c0 += (size_t)kXcds * kQueueChunk)
+        for (size_t i = c0; i < std::min(seq.size(), c0 + kQueueChunk); ++i) push(seq[i].first, seq[i].second);
+    }
+  };
+  std::vector<std::pair<int32_t, int32_t>> seq;
 
-  const auto gu_groups = row_groups(p.gu_group, 0, n_tr);
-  for (int32_t x = 0; x < kXcds; ++x) {
-    P.gu_queue[x] = (int32_t)P.items.size();
-    deal(x, gu_groups, P.gu_per_row, [&](int32_t q, int32_t j) { P.items.push_back(gu_item(order[q], j)); });
-  }
+  blocks(row_groups(p.gu_group, 0, n_tr), P.gu_per_row, &seq);
+  deal(seq, [&](int32_t x) { P.gu_queue[x] = (int32_t)P.items.size(); },
+       [&](int32_t q, int32_t j) { P.items.push_back(gu_item(order[q], j)); });
   P.n_gu = (int32_t)P.items.size();
   P.gu_queue[kXcds] = P.n_gu;
 
@@ -287,20 +292,21 @@ int build_plan(const PlanParams& p, int64_t rows, const int32_t* off, const int3
   // position in the run is taken as the latest queue position of its parts.
   std::vector<int32_t> pos_of_down((size_t)n_tr * P.down_per_row, -1);
   const int32_t n_whole = n_tr - P.n_split_rows;  // whole-tile rows first, split rows last
-  const auto whole_groups = row_groups(p.down_group, 0, n_whole);
-  const auto split_groups = row_groups(p.down_group, n_whole, n_tr);
-  for (int32_t x = 0; x < kXcds; ++x) {
-    const int32_t q0 = (int32_t)P.items.size();
-    P.down_queue[x] = q0 - P.n_gu;
-    auto push = [&](int32_t q, int32_t pc) {  // pc: (part, column) pair, part-major
-      const int32_t t = order[q], part = pc / P.down_per_row, n = pc % P.down_per_row;
-      P.items.push_back(down_item(t, n, part));
-      int32_t& pos = pos_of_down[(size_t)t * P.down_per_row + n];
-      pos = std::max(pos, (int32_t)P.items.size() - 1 - q0);
-    };
-    deal(x, whole_groups, P.down_per_row, push);
-    deal(x, split_groups, P.down_per_row * P.tail_split, push);
-  }
+  seq.clear();
+  blocks(row_groups(p.down_group, 0, n_whole), P.down_per_row, &seq);
+  blocks(row_groups(p.down_group, n_whole, n_tr), P.down_per_row * P.tail_split, &seq);
+  int32_t q0 = 0;
+  deal(seq,
+       [&](int32_t x) {
+         q0 = (int32_t)P.items.size();
+         P.down_queue[x] = q0 - P.n_gu;
+       },
+       [&](int32_t q, int32_t pc) {  // pc: (part, column) pair, part-major
+         const int32_t t = order[q], part = pc / P.down_per_row, n = pc % P.down_per_row;
+         P.items.push_back(down_item(t, n, part));
+         int32_t& pos = pos_of_down[(size_t)t * P.down_per_row + n];
+         pos = std::max(pos, (int32_t)P.items.size() - 1 - q0);
+       });
   P.n_down = (int32_t)P.items.size() - P.n_gu;
   P.down_queue[kXcds] = P.n_down;
 

@@ -68,6 +68,8 @@ struct Group {
 // MI355X has 8 XCDs (accelerator dies), each with its own L2; the workgroups of a launch are
 // dealt to them round-robin.  Each producer launch keeps one work queue per XCD.
 constexpr int kXcds = 8;
+// Items per chunk when a launch's item sequence is dealt round-robin to the XCD queues.
+constexpr int kQueueChunk = 32;
 
 // Device-side counters of one run; the queue heads are zeroed by the init kernel.
 struct RunCounters {

@@ -47,6 +47,22 @@ def decode(items):
     return down.astype(int), t.astype(int), col.astype(int), part.astype(int)
 
 
+def schedule_order(p, launch):
+    """Tile rows in order of first appearance in a launch's item sequence, restored from its
+    per-XCD queues by interleaving their 32-item chunks round-robin (queue x holds chunks x,
+    x + 8, ... of the sequence)."""
+    down, t, _, _ = decode(p["items"])
+    lo = 0 if launch == 0 else p["info"]["n_gu_items"]
+    q = p["queues"][launch]
+    chunks = [[t[lo + c:lo + min(c + 32, q[x + 1])] for c in range(q[x], q[x + 1], 32)] for x in range(8)]
+    seq = []
+    for c in range(max((len(ch) for ch in chunks), default=0)):
+        for x in range(8):
+            if c < len(chunks[x]):
+                seq.extend(chunks[x][c].tolist())
+    return list(dict.fromkeys(seq))
+
+
 def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True, local_direct=True):
     info = p["info"]
     rows = int(off[-1])
@@ -91,48 +107,29 @@ def check_plan(p, off, src, slot, self_rank, R, band_rows, mgb, overlapped=True,
     # two launches: every gate/up tile precedes every down item
     n_gu = info["n_gu_items"]
     assert np.all(down[:n_gu] == 0) and np.all(down[n_gu:] == 1)
-    # each launch's items are 8 per-XCD queues; every tile row's items are dealt over them in
-    # slices of near-equal size, and the queues take tile rows in one common order
+    # each launch's items are 8 per-XCD queues of near-equal size, which take tile rows in one
+    # common order
     qs = p["queues"]
     assert qs.shape == (2, 9)
     qpos = np.empty(len(down), np.int64)   # position of each item within its queue
+    sched_of = []
     for li, (lo, n) in enumerate(((0, n_gu), (n_gu, info["n_down_items"]))):
         q = qs[li]
         assert q[0] == 0 and q[8] == n and np.all(np.diff(q) >= 0)
-        lists = []
-        counts = np.zeros((8, n_tr), int)
         for x in range(8):
-            ts = t[lo + q[x]:lo + q[x + 1]]
             qpos[lo + q[x]:lo + q[x + 1]] = np.arange(q[x + 1] - q[x])
-            np.add.at(counts[x], ts, 1)
-            seen = list(dict.fromkeys(ts.tolist()))
-            lists.append(seen)
-        for ti in range(n_tr):   # the queues holding a tile row share it near-evenly
-            nz = counts[:, ti][counts[:, ti] > 0]
-            assert len(nz) == 0 or nz.max() - nz.min() <= 1
-        # one schedule order explains every queue: the precedences the queues show are acyclic
-        after = {tt: set() for tt in range(n_tr)}
-        for seen in lists:
-            for a_, b_ in zip(seen, seen[1:]):
-                after[a_].add(b_)
-        indeg = {tt: 0 for tt in range(n_tr)}
-        for a_ in after:
-            for b_ in after[a_]:
-                indeg[b_] += 1
-        ready = [tt for tt in range(n_tr) if indeg[tt] == 0]
-        done = 0
-        while ready:
-            a_ = ready.pop()
-            done += 1
-            for b_ in after[a_]:
-                indeg[b_] -= 1
-                if indeg[b_] == 0:
-                    ready.append(b_)
-        assert done == n_tr, "queues take tile rows in contradicting orders"
-        # remote-first: within a queue no tile row holding remote rows follows a local-only one
-        for seen in lists:
-            hr = [int(tr[tt, 3]) for tt in seen]
-            assert hr == sorted(hr, reverse=True)
+        sizes = np.diff(q)   # chunks of 32 items are dealt round-robin: sizes within one chunk
+        assert sizes.max() - sizes.min() <= 32
+        # the launch's sequence, restored from its queues, takes tile rows in schedule order:
+        # remote-first, and the same order in both launches
+        sched = schedule_order(p, li)
+        assert sorted(sched) == list(range(n_tr)) or n == 0
+        hr = [int(tr[tt, 3]) for tt in sched]
+        assert hr == sorted(hr, reverse=True)
+        sched_of.append(sched)
+    if n_gu and info["n_down_items"]:
+        assert sched_of[0] == sched_of[1]
+
     if not overlapped:
         assert info["n_band_padding"] == 0 and info["n_segments"] == 0
         return
@@ -203,18 +200,9 @@ def test_golden_schedule_example():
     p = B.moe_plan_build(cfg, off, src, slot, rr)
     check_plan(p, off, src, slot, me, R, tb, 1)
     assert p["tile_rows"][:, 0].tolist() == g["expected_tile_row_experts"]
-    down, t, col, _ = decode(p["items"])
-    # every down queue takes its tile rows in the schedule order, and together they take all
-    q = p["queues"][1]
-    dn = t[down == 1]
-    want = g["expected_tile_row_order"]
-    rank_of = {tt: i for i, tt in enumerate(want)}
-    seen = set()
-    for x in range(8):
-        order = list(dict.fromkeys(dn[q[x]:q[x + 1]].tolist()))
-        assert [rank_of[tt] for tt in order] == sorted(rank_of[tt] for tt in order)
-        seen |= set(order)
-    assert seen == set(want)
+    # both launches take the tile rows in the schedule order of the prose example
+    assert schedule_order(p, 0) == g["expected_tile_row_order"]
+    assert schedule_order(p, 1) == g["expected_tile_row_order"]
     pg = p["groups"]
     for e_glob, want in g["expected_remote_bands"].items():
         e = glob.index(int(e_glob))
