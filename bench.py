@@ -68,7 +68,9 @@ def parse():
     ap.add_argument("--band-rows", type=int, default=0, help="tb_M of the row layout (0 = 1, no alignment)")
     ap.add_argument("--split-k", type=int, default=0, help="K parts per down tile (0 = library default)")
     ap.add_argument("--mgb", type=int, default=1, help="tile-row pieces per middle transfer segment")
-    ap.add_argument("--sweep", default="4,8,16,32",
+    ap.add_argument("--copy-curve", default="8,16,32,64,128",
+                    help="consumer CU counts for the consumer-only copy ceiling ('' to skip)")
+    ap.add_argument("--sweep", default="8,16,24,32",
                     help="CU splits for the overlap-speedup sweep, both modes ('' = none)")
     ap.add_argument("--only", choices=["all", "serial", "overlapped"], default="all",
                     help="run only one path of the headline workload (counter collection)")
@@ -130,16 +132,27 @@ class Bench:
         self.bufs = [torch.zeros((int(n), wl.H), dtype=torch.int16, device="cuda") for n in wl.return_rows]
         self.run_args = (self.x, wl.expert_offsets, wl.row_src_rank, wl.row_slot, self.w1, self.w3, self.w2,
                          self.bufs, wl.return_rows)
-        base = B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING
+        self.base_flags = B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING
         extra = {"shared": B.MOE_SHARED_CUS, "partitioned": 0, "direct": B.MOE_DIRECT_ALL}
-        self.stages = {m: B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, args.mgb,
-                                     base | f, 0, args.split_k)
-                       for m, f in extra.items()}
+        self.stages = {m: self.make_stage(f, args.mgb) for m, f in extra.items()}
         torch.cuda.synchronize()
         # The stage runs on a stream of its own, as in a serving loop (on the legacy null stream
         # the shared-CU producer would have to fork to a second queue; see moe_stage_run).
         self.stream = torch.cuda.Stream()
         self.timeouts = []
+
+    def make_stage(self, flags, mgb):
+        wl, args = self.wl, self.args
+        return self.B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, mgb,
+                               self.base_flags | flags, 0, args.split_k)
+
+    def stage(self, mode, mgb):
+        """Handle of a CU mode and mid-segment piece count (created on first use)."""
+        key = mode if mgb == self.args.mgb else f"{mode}:mgb{mgb}"
+        if key not in self.stages:
+            f = {"shared": self.B.MOE_SHARED_CUS, "partitioned": 0}[mode]
+            self.stages[key] = self.make_stage(f, mgb)
+        return key
 
     def close(self):
         for s in self.stages.values():
@@ -162,14 +175,17 @@ class Bench:
         gc.collect()
         gc.disable()
         torch.cuda.synchronize()
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        start.record(self.stream)
-        for _ in range(steps):
+        # One event between consecutive steps: the whole loop's time gives the mean, the
+        # per-step differences its spread (an event between steps costs no GPU time).
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        ev[0].record(self.stream)
+        for i in range(steps):
             fn()
-        end.record(self.stream)
+            ev[i + 1].record(self.stream)
         torch.cuda.synchronize()
         gc.enable()
-        ms = start.elapsed_time(end) / steps
+        ms = ev[0].elapsed_time(ev[steps]) / steps
+        per_step = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)])
         st = stg.query(check=False)
         if st["rc"] != 0:
             msg = self.B.moe_stage_last_error(stg.h)
@@ -179,7 +195,35 @@ class Bench:
         runs = max(tm["runs"], 1)
         return {"ms": ms, "stats": st, "producer_ms": tm["producer_ms"] / runs,
                 "gate_up_ms": tm["gate_up_ms"] / runs, "consumer_ms": tm["consumer_ms"] / runs,
-                "scatter_ms": tm["scatter_ms"] / runs}
+                "scatter_ms": tm["scatter_ms"] / runs,
+                "p10_ms": float(np.percentile(per_step, 10)), "p50_ms": float(np.median(per_step)),
+                "p90_ms": float(np.percentile(per_step, 90))}
+
+    def copy_curve(self, splits, steps, warmup):
+        """Consumer copy rate with no producer work (every flag published up front), per
+        consumer CU count: the ceiling a c-CU consumer can reach on this workload's segments."""
+        torch, B = self.torch, self.B
+        stg = self.make_stage(B.MOE_SHARED_CUS | B.MOE_TEST_CONSUMER_ONLY, self.args.mgb)
+        out = []
+        try:
+            for c in splits:
+                fn = lambda: stg.run(*self.run_args, cu_split=c, stream=self.stream)
+                for _ in range(warmup):
+                    fn()
+                torch.cuda.synchronize()
+                stg.times(reset=True)
+                for _ in range(steps):
+                    fn()
+                torch.cuda.synchronize()
+                st = stg.query(check=False)
+                tm = stg.times(reset=True)
+                us = tm["consumer_ms"] / max(tm["runs"], 1) * 1e3
+                nbytes = 4.0 * self.wl.H * st["n_remote_rows"]
+                out.append({"cu_split": c, "consumer_cus": st["consumer_cus"], "us": us,
+                            "bytes": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9, "rc": st["rc"]})
+        finally:
+            stg.close()
+        return out
 
 
     def timed_combine(self, steps, warmup):
@@ -228,6 +272,8 @@ def summarize(wl, ser, ovl, sweep):
         gu = r["gate_up_ms"]
         dn = r["producer_ms"] - gu
         out[key] = {"stage_us": r["ms"] * 1e3, "tflops": flops / (r["ms"] * 1e-3) / 1e12,
+                    "step_us_p10_p50_p90": [round(r["p10_ms"] * 1e3, 1), round(r["p50_ms"] * 1e3, 1),
+                                            round(r["p90_ms"] * 1e3, 1)],
                     "producer_us": r["producer_ms"] * 1e3, "gate_up_us": gu * 1e3, "down_us": dn * 1e3,
                     "producer_frac_of_peak": flops / (r["producer_ms"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
         if key == "serial":
@@ -289,15 +335,30 @@ def main():
                 f"{direct['producer_ms'] * 1e3:.1f}, gate/up {direct['gate_up_ms'] * 1e3:.1f})")
         sweep = []
         if sweep_cs and ser is not None and only == "all":
-            for c in sweep_cs:
-                for mode in ("shared", "partitioned"):
-                    r = bench.timed(mode, "overlapped", c, max(steps // 2, 5), max(warmup // 2, 3))
-                    sweep.append({"cu_split": c, "cu_mode": mode, "consumer_cus": r["stats"]["consumer_cus"],
-                                  "stage_us": r["ms"] * 1e3, "speedup_vs_serial": ser["ms"] / r["ms"]})
-                    log(f"{name} sweep c={c} {mode}: {r['ms'] * 1e3:.1f} us, speedup {ser['ms'] / r['ms']:.3f}")
+            for mgb in (1, 2):
+                for c in sweep_cs:
+                    for mode in ("shared", "partitioned"):
+                        key = bench.stage(mode, mgb)
+                        r = bench.timed(key, "overlapped", c, max(steps // 2, 5), max(warmup // 2, 3))
+                        sweep.append({"cu_split": c, "cu_mode": mode, "mgb": mgb,
+                                      "consumer_cus": r["stats"]["consumer_cus"],
+                                      "segments": r["stats"]["n_segments"], "stage_us": r["ms"] * 1e3,
+                                      "speedup_vs_serial": ser["ms"] / r["ms"]})
+                        log(f"{name} sweep c={c} {mode} mgb={mgb}: {r['ms'] * 1e3:.1f} us, "
+                            f"speedup {ser['ms'] / r['ms']:.3f}")
         per_wl[name] = summarize(wl, ser, ovl, sweep)
+        if only == "all" and args.copy_curve:
+            curve = bench.copy_curve([int(v) for v in args.copy_curve.split(",")], 10, 3)
+            per_wl_curve = curve
+            for r in curve:
+                log(f"{name} consumer copy ceiling c={r['cu_split']} ({r['consumer_cus']} CUs): "
+                    f"{r['us']:.1f} us, {r['GBps']:.0f} GB/s")
+        else:
+            per_wl_curve = None
         comb = bench.timed_combine(max(steps, 20), max(warmup, 5))
         per_wl[name]["combine"] = comb
+        if per_wl_curve is not None:
+            per_wl[name]["consumer_copy_ceiling"] = per_wl_curve
         log(f"{name} combine ({wl.T_r} tokens, k={wl.k}): {comb['us']:.1f} us, {comb['GBps']:.0f} GB/s")
         if direct is not None:
             per_wl[name]["epilogue_direct_ablation_us"] = direct["ms"] * 1e3

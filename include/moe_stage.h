@@ -68,6 +68,11 @@ extern "C" {
 #define MOE_TEST_NO_SIGNAL (1u << 3) /* testing aid: the producer raises no ready flags, so every
                                        consumer wait runs into watchdog_ms and the run reports
                                        MOE_ETIMEOUT; the kernels still exit normally            */
+#define MOE_TEST_CONSUMER_ONLY (1u << 6) /* measurement aid: moe_stage_run launches no producer
+                                       work; the run's reset publishes every ready flag, so the
+                                       consumer copies the staged output (whatever it holds) at
+                                       the rate its cu_split compute units allow.  The receive
+                                       buffers then hold no results                            */
 #define MOE_SHARED_CUS (1u << 4)   /* overlapped run: the producer keeps every compute unit and
                                       the consumer, still confined to its cu_split units, runs
                                       beside producer workgroups there (a consumer workgroup's

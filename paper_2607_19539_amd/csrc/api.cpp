@@ -117,7 +117,8 @@ int check_config(const moe_stage_config_t* c) {
       c->mid_segment_pieces < 0 || c->watchdog_ms < 0)
     return MOE_EINVAL;
   constexpr uint32_t kKnownFlags = MOE_LOCAL_DIRECT | MOE_KERNEL_TIMING | MOE_POISON |
-                                   MOE_TEST_NO_SIGNAL | MOE_SHARED_CUS | MOE_DIRECT_ALL;
+                                   MOE_TEST_NO_SIGNAL | MOE_SHARED_CUS | MOE_DIRECT_ALL |
+                                   MOE_TEST_CONSUMER_ONLY;
   if (c->flags & ~kKnownFlags) return MOE_EINVAL;
   if (c->band_rows < 0 || c->band_rows > 256 || (c->band_rows & (c->band_rows - 1)) != 0)
     return MOE_EINVAL;
@@ -210,9 +211,14 @@ int prepare(moe_stage_s* h, bool overlapped, const void* x,
     ia.poison = h->y;
     ia.poison_elems = P.n_lrows() * c.hidden;
   }
+  const uint32_t epoch = h->epoch + 1 == 0 ? 1 : h->epoch + 1;  // flags hold the epoch of the run that set them
+  if (overlapped && (c.flags & MOE_TEST_CONSUMER_ONLY)) {
+    ia.publish = h->flags;
+    ia.n_publish = ia.n_arrivals;
+    ia.epoch = epoch;
+  }
   HIP_TRY(h, launch_init(ia, stream));
-
-  h->epoch = h->epoch + 1 == 0 ? 1 : h->epoch + 1;  // flags hold the epoch of the run that set them
+  h->epoch = epoch;
   moe_stage_stats_t& st = h->last;
   st.n_valid = P.n_valid;
   st.n_logical_rows = P.n_lrows();
@@ -477,9 +483,10 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
   HIP_TRY(h, hipEventRecord(h->ev_join_c, h->s_cons));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], ps));
-  if (pgu.n_items > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, ps));
+  const bool producer = !(h->cfg.flags & MOE_TEST_CONSUMER_ONLY);
+  if (producer && pgu.n_items > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, ps));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], ps));
-  if (pdn.n_items > 0) HIP_TRY(h, launch_producer(pdn, true, pgrid, ps));
+  if (producer && pdn.n_items > 0) HIP_TRY(h, launch_producer(pdn, true, pgrid, ps));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], ps));
   if (!on_caller) {
     HIP_TRY(h, hipEventRecord(h->ev_join_p, h->s_prod));

@@ -734,6 +734,8 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
     a.ctr->wait_ticks = 0;
   }
   for (int64_t j = i; j < a.n_arrivals; j += stride) a.arrivals[j] = 0;
+  if (a.publish)
+    for (int64_t j = i; j < a.n_publish; j += stride) a.publish[j] = a.epoch;
   if (a.poison) {
     const u32x4 nan = {0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};
     for (int64_t j = i; j < a.poison_elems / 8; j += stride) ((u32x4*)a.poison)[j] = nan;

@@ -66,6 +66,9 @@ struct InitArgs {
   int64_t poison_elems;    // multiple of 8
   uint32_t* arrivals;      // split-K arrival counters to zero
   int32_t n_arrivals;
+  uint32_t* publish;       // optional: ready flags to set to `epoch` (consumer-only measurement)
+  int32_t n_publish;
+  uint32_t epoch;
 };
 
 struct CombineArgs {

@@ -264,3 +264,22 @@ def test_repeated_runs_reuse_flags_across_epochs():
         out = dw.host_bufs()
         st.query()
     compare(out, ref)
+
+
+def test_consumer_only_copies_staged_rows():
+    """MOE_TEST_CONSUMER_ONLY (copy-ceiling measurement): no producer work, every flag published
+    by the run's reset, so the consumer copies the staged output -- zeros on a fresh handle --
+    into every remote slot and leaves local slots (written by the producer otherwise) alone."""
+    wl = make_workload("tiny", owner=2, overrides=RAGGED)
+    dw = DeviceWorkload(torch, wl)
+    with make_stage(wl, flags=B.MOE_LOCAL_DIRECT | B.MOE_SHARED_CUS | B.MOE_TEST_CONSUMER_ONLY) as st:
+        out, stats = run_overlapped(dw, st, cu_split=8)
+        assert stats["timeout"] == 0 and stats["n_segments"] > 0
+    for r, b in enumerate(out):
+        mine = wl.row_slot[wl.row_src_rank == r]
+        if r == wl.self_rank:
+            assert np.all(b[mine] == SENTINEL)
+        else:
+            assert np.all(b[mine] == 0)
+        other = np.setdiff1d(np.arange(b.shape[0]), mine)
+        assert np.all(b[other] == SENTINEL)
