@@ -46,6 +46,9 @@ DESCRIPTIONS = {
     "fine": "fine: H2048 F1408, 64 experts top-6, 4 source ranks x 8192 tokens, 16 local experts",
     "large_fine": "large_fine: H7168 F2048, 256 experts top-8, 8 source ranks x 4096 tokens, 32 local experts",
 }
+for _e in (4, 8, 16, 32, 64):
+    DESCRIPTIONS[f"layer_e{_e}"] = (f"layer_e{_e}: H1024 F4096, {4 * _e} experts top-2, 4 source ranks x 8192 tokens, "
+                                    f"{_e} local experts (expert-count sweep)")
 
 
 def log(msg):
@@ -72,6 +75,8 @@ def parse():
                     help="consumer CU counts for the consumer-only copy ceiling ('' to skip)")
     ap.add_argument("--sweep", default="8,16,24,32",
                     help="CU splits for the overlap-speedup sweep, both modes ('' = none)")
+    ap.add_argument("--esweep", default="4,8,16,32,64",
+                    help="experts per rank for the single-layer expert-count sweep ('' to skip)")
     ap.add_argument("--only", choices=["all", "serial", "overlapped"], default="all",
                     help="run only one path of the headline workload (counter collection)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -287,7 +292,49 @@ def summarize(wl, ser, ovl, sweep):
     return out
 
 
+def expert_count_sweep(torch, B, make_workload, args, counts, timeouts):
+    """Single-layer sweep over experts per rank (paper Section 4.2.2): serial and overlapped
+    stage times, the split the adaptive selector (cu_split = 0) settles on, and the overlap
+    ratio -- the share of the consumer's stand-alone copy time hidden behind the producer:
+    1 - (overlapped stage - serial producer) / consumer-only copy time, clamped to [0, 1]."""
+    rows = []
+    for E in counts:
+        name = f"layer_e{E}"
+        log(f"generating workload {name} seed {args.seed}")
+        wl = make_workload(name, seed=args.seed)
+        bench = Bench(torch, B, wl, args)
+        steps, warmup = max(args.steps // 2, 10), max(args.warmup // 2, 5)
+        ser = bench.timed("shared", "serial", 0, steps, warmup)
+        # Let the adaptive selector finish measuring its candidates before timing.
+        stg = bench.stages["shared"]
+        for i in range(160):
+            stg.run(*bench.run_args, cu_split=0, stream=bench.stream)
+            if i % 4 == 3:
+                torch.cuda.synchronize()
+                if stg.query(check=False)["auto_cu_split"] > 0:
+                    break
+        ovl = bench.timed("shared", "overlapped", 0, steps, warmup)
+        st = ovl["stats"]
+        c = st["consumer_cus"]
+        curve = bench.copy_curve([c], 10, 3)[0]
+        t_o, t_p, t_c = ovl["ms"] * 1e3, ser["producer_ms"] * 1e3, curve["us"]
+        ratio = min(max(1.0 - (t_o - t_p) / t_c, 0.0), 1.0) if t_c > 0 else None
+        rows.append({"experts_per_rank": E, "routed_rows": wl.rows, "serial_us": ser["ms"] * 1e3,
+                     "overlapped_us": t_o, "speedup": ser["ms"] / ovl["ms"], "serial_producer_us": t_p,
+                     "consumer_only_copy_us": t_c, "overlap_ratio": ratio,
+                     "auto_cu_split": st["auto_cu_split"], "consumer_cus": c,
+                     "tflops_overlapped": wl.flops() / (ovl["ms"] * 1e-3) / 1e12})
+        log(f"{name}: serial {ser['ms'] * 1e3:.1f} us, overlapped {t_o:.1f} us (auto c={st['auto_cu_split']}), "
+            f"speedup {ser['ms'] / ovl['ms']:.3f}, overlap ratio {ratio if ratio is None else round(ratio, 3)}")
+        timeouts += bench.timeouts
+        bench.close()
+        del bench, wl
+        torch.cuda.empty_cache()
+    return rows
+
+
 def main():
+    t_start = time.time()
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only: the return all-to-all is modelled by "
@@ -414,7 +461,11 @@ def main():
         del bench, wl
         torch.cuda.empty_cache()
     out["workloads"] = per_wl
+    if args.esweep and args.only == "all":
+        out["expert_count_sweep"] = expert_count_sweep(torch, B, make_workload, args,
+                                                       [int(v) for v in args.esweep.split(",")], timeouts)
     out["watchdog_timeouts"] = timeouts
+    log(f"done in {time.time() - t_start:.0f} s")
     print(json.dumps(out), flush=True)
 
 

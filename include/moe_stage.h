@@ -143,6 +143,9 @@ typedef struct {
   int32_t down_workgroups;  /* the same for the down-projection launch                       */
   int32_t split_k;          /* K parts of each split down-projection tile (1: none split)    */
   int32_t split_rows;       /* tile rows whose down-projection tiles are split               */
+  int32_t auto_cu_split;    /* cu_split = 0 runs: the split the selector settled on, 0 while
+                               it is still measuring candidates; -1 for other runs          */
+  int32_t reserved;
 } moe_stage_stats_t;
 
 /* Accumulated kernel times (MOE_KERNEL_TIMING), milliseconds, over runs since the last reset. */
@@ -172,7 +175,11 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out);
  * on `stream` under MOE_SHARED_CUS when `stream` is not the legacy null stream
  * (whose launches would wait for the polling consumer).
  *
- * cu_split: compute units for the consumer, 1 <= cu_split <= CUs - XCDs.  Workgroups
+ * cu_split: compute units for the consumer, 1 <= cu_split <= CUs - XCDs, or 0 to let the
+ * handle choose (a runtime-adaptive selector, the paper's Section 5 future work): it measures
+ * the stage time of its own runs at consumer splits of 8, 16, 32 and 64 CUs, three finished
+ * runs each and one candidate after another, then keeps the fastest (stats: auto_cu_split).
+ * Results do not depend on the split.  Workgroups
  * are dealt round-robin over the XCDs (8 on MI355X) and a CU-masked queue must own
  * CUs on each of them, so the split is rounded up to a multiple of the XCD count
  * (the stats report the effective value); the producer gets every other CU, or every

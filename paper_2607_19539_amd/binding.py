@@ -45,7 +45,8 @@ class moe_stage_stats_t(ctypes.Structure):
                 ("timeout", ctypes.c_int32),
                 ("plan_us", ctypes.c_double), ("poll_iters", ctypes.c_uint64), ("wait_ticks", ctypes.c_uint64),
                 ("gu_workgroups", ctypes.c_int32), ("down_workgroups", ctypes.c_int32),
-                ("split_k", ctypes.c_int32), ("split_rows", ctypes.c_int32)]
+                ("split_k", ctypes.c_int32), ("split_rows", ctypes.c_int32),
+                ("auto_cu_split", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class moe_stage_times_t(ctypes.Structure):

@@ -30,6 +30,23 @@ thread_local std::string g_create_error;
 
 constexpr int kTimingRing = 512;
 
+// Adaptive CU split (cu_split = 0): the consumer sizes tried, the completed runs measured for
+// each, and the event pairs kept in flight for the measurements.
+constexpr int kAutoSplits[] = {8, 16, 32, 64};
+constexpr int kNumAutoSplits = sizeof(kAutoSplits) / sizeof(kAutoSplits[0]);
+constexpr int kAutoSamples = 3;
+constexpr int kAutoRing = 8;
+
+struct AutoSplit {
+  int cand = 0;     // candidate being measured
+  int chosen = -1;  // index of the split in use once every candidate is measured
+  std::vector<float> ms[kNumAutoSplits];
+  hipEvent_t ev[kAutoRing][2] = {};
+  int ev_cand[kAutoRing] = {};
+  bool busy[kAutoRing] = {};
+  int next = 0;
+};
+
 struct TimingRec {
   hipEvent_t ev[7];  // 0 stage start, 1 producer start, 2 producer end, 3 consumer start,
                      // 4 consumer end / scatter start, 5 stage end / scatter end, 6 gate/up end
@@ -63,6 +80,14 @@ struct moe_stage_s {
   int stage_idx = 0;
   uint32_t epoch = 0;
 
+  // CU-masked queues per consumer split, kept once made (switching splits then costs no queue
+  // teardown); s_cons / s_prod are the current split's pair.  With shared CUs the producer's
+  // queue covers every CU whatever the split, so all entries share one.
+  struct SplitQueues {
+    int c;
+    hipStream_t cons, prod;
+  };
+  std::vector<SplitQueues> queues;
   int cached_split = -1;
   hipStream_t s_cons = nullptr, s_prod = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join_c = nullptr, ev_join_p = nullptr, ev_done = nullptr;
@@ -72,6 +97,7 @@ struct moe_stage_s {
 
   std::vector<TimingRec> ring;
   int ring_next = 0, ring_count = 0;
+  AutoSplit autos;
 
   Plan plan;
   std::string err;
@@ -301,6 +327,40 @@ void make_masks(int num_cus, int n_xcd, int c, bool shared, std::vector<uint32_t
   }
 }
 
+// Adaptive split: collects the stage times of finished measured runs (never waits).
+void harvest_auto(moe_stage_s* h) {
+  AutoSplit& a = h->autos;
+  for (int i = 0; i < kAutoRing; ++i) {
+    if (!a.busy[i] || hipEventQuery(a.ev[i][1]) != hipSuccess) continue;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, a.ev[i][0], a.ev[i][1]) == hipSuccess) a.ms[a.ev_cand[i]].push_back(ms);
+    a.busy[i] = false;
+  }
+}
+
+// The split of the next auto run: candidates are measured one after another (kAutoSamples
+// finished runs each, so the CU-masked queue is rebuilt only once per candidate), then the one
+// with the lowest median stage time is kept.  Returns the candidate index.
+int pick_auto(moe_stage_s* h) {
+  AutoSplit& a = h->autos;
+  if (a.chosen >= 0) return a.chosen;
+  while (a.cand < kNumAutoSplits &&
+         ((int)a.ms[a.cand].size() >= kAutoSamples || kAutoSplits[a.cand] > h->num_cus - h->n_xcd))
+    ++a.cand;
+  if (a.cand < kNumAutoSplits) return a.cand;
+  float best = 0.f;
+  for (int c = 0; c < kNumAutoSplits; ++c) {
+    auto v = a.ms[c];
+    if (v.empty()) continue;
+    std::nth_element(v.begin(), v.begin() + v.size() / 2, v.end());
+    if (a.chosen < 0 || v[v.size() / 2] < best) {
+      a.chosen = c;
+      best = v[v.size() / 2];
+    }
+  }
+  return a.chosen >= 0 ? a.chosen : 0;
+}
+
 // Consumer CUs actually reserved for a requested split: a multiple of the XCD count.
 int effective_split(const moe_stage_s* h, int c) {
   const int n = h->n_xcd;
@@ -309,20 +369,48 @@ int effective_split(const moe_stage_s* h, int c) {
 
 int ensure_streams(moe_stage_s* h, int c) {
   if (h->cached_split == c) return MOE_OK;
-  if (h->s_cons) {
-    HIP_TRY(h, hipStreamSynchronize(h->s_cons));
-    HIP_TRY(h, hipStreamSynchronize(h->s_prod));
-    HIP_TRY(h, hipStreamDestroy(h->s_cons));
-    HIP_TRY(h, hipStreamDestroy(h->s_prod));
-    h->s_cons = h->s_prod = nullptr;
-    h->cached_split = -1;
-  }
+  const bool shared = (h->cfg.flags & MOE_SHARED_CUS) != 0;
+  for (const auto& q : h->queues)
+    if (q.c == c) {
+      h->s_cons = q.cons;
+      h->s_prod = q.prod;
+      h->cached_split = c;
+      return MOE_OK;
+    }
   std::vector<uint32_t> mc, mp;
-  make_masks(h->num_cus, h->n_xcd, c, (h->cfg.flags & MOE_SHARED_CUS) != 0, &mc, &mp);
-  HIP_TRY(h, hipExtStreamCreateWithCUMask(&h->s_cons, (uint32_t)mc.size(), mc.data()));
-  HIP_TRY(h, hipExtStreamCreateWithCUMask(&h->s_prod, (uint32_t)mp.size(), mp.data()));
+  make_masks(h->num_cus, h->n_xcd, c, shared, &mc, &mp);
+  moe_stage_s::SplitQueues q{c, nullptr, nullptr};
+  HIP_TRY(h, hipExtStreamCreateWithCUMask(&q.cons, (uint32_t)mc.size(), mc.data()));
+  if (shared && !h->queues.empty()) {
+    q.prod = h->queues.front().prod;
+  } else if (hipExtStreamCreateWithCUMask(&q.prod, (uint32_t)mp.size(), mp.data()) != hipSuccess) {
+    (void)hipStreamDestroy(q.cons);
+    return set_err(h, MOE_EHIP, "hipExtStreamCreateWithCUMask(producer)");
+  }
+  h->queues.push_back(q);
+  h->s_cons = q.cons;
+  h->s_prod = q.prod;
   h->cached_split = c;
   return MOE_OK;
+}
+
+// Releases the queues of every split but the current one (once the adaptive selector has
+// settled, so idle queues do not stay with the device).
+void release_other_queues(moe_stage_s* h) {
+  std::vector<moe_stage_s::SplitQueues> keep;
+  for (const auto& q : h->queues) {
+    if (q.c == h->cached_split) {
+      keep.push_back(q);
+      continue;
+    }
+    (void)hipStreamSynchronize(q.cons);
+    (void)hipStreamDestroy(q.cons);
+    if (q.prod != h->s_prod) {
+      (void)hipStreamSynchronize(q.prod);
+      (void)hipStreamDestroy(q.prod);
+    }
+  }
+  h->queues.swap(keep);
 }
 
 }  // namespace
@@ -412,6 +500,10 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       !try_hip(hipEventCreateWithFlags(&h->ev_join_p, kSyncEv), "hipEventCreate") ||
       !try_hip(hipEventCreateWithFlags(&h->ev_done, kSyncEv), "hipEventCreate"))
     return bail(MOE_EHIP);
+  for (auto& pair : h->autos.ev)
+    for (auto& ev : pair)
+      if (!try_hip(hipEventCreateWithFlags(&ev, hipEventReleaseToDevice), "hipEventCreate"))
+        return bail(MOE_EHIP);
   if (h->cfg.flags & MOE_KERNEL_TIMING) {
     h->ring.resize(kTimingRing);
     for (auto& r : h->ring)
@@ -429,8 +521,16 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
                   void* const* ret, const int64_t* return_rows, int32_t cu_split, void* stream_) {
   if (!h) return MOE_EINVAL;
   hipStream_t stream = (hipStream_t)stream_;
+  const bool autosplit = cu_split == 0;
+  int auto_cand = -1, auto_slot = -1;
+  if (autosplit) {
+    harvest_auto(h);
+    auto_cand = pick_auto(h);
+    cu_split = kAutoSplits[auto_cand];
+    if (!h->autos.busy[h->autos.next]) auto_slot = h->autos.next;  // else: this run is not measured
+  }
   if (cu_split < 1 || cu_split > h->num_cus - h->n_xcd)
-    return set_err(h, MOE_EUNSUPPORTED, "cu_split must be in [1, compute units - XCDs]");
+    return set_err(h, MOE_EUNSUPPORTED, "cu_split must be in [0, compute units - XCDs]");
   const int c_eff = effective_split(h, cu_split);
   const bool shared = (h->cfg.flags & MOE_SHARED_CUS) != 0;
   const int pgrid = (shared ? h->num_cus : h->num_cus - c_eff) * h->producer_bpc;
@@ -439,9 +539,11 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   const int cgrid = c_eff * (shared ? 2 : 6);
   int rc = ensure_streams(h, c_eff);
   if (rc) return rc;
+  if (autosplit && h->autos.chosen >= 0 && h->queues.size() > 1) release_other_queues(h);
   BlobLayout lay{};
   TimingRec* tr = timing_slot(h);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[0], stream));
+  if (auto_slot >= 0) HIP_TRY(h, hipEventRecord(h->autos.ev[auto_slot][0], stream));
   rc = prepare(h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
   if (rc) {
     if (tr) h->ring_next = (h->ring_next + kTimingRing - 1) % kTimingRing, --h->ring_count;
@@ -498,6 +600,13 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
     tr->kind = 0;
   }
   HIP_TRY(h, hipEventRecord(h->ev_done, stream));
+  if (auto_slot >= 0) {
+    HIP_TRY(h, hipEventRecord(h->autos.ev[auto_slot][1], stream));
+    h->autos.busy[auto_slot] = true;
+    h->autos.ev_cand[auto_slot] = auto_cand;
+    h->autos.next = (auto_slot + 1) % kAutoRing;
+  }
+  h->last.auto_cu_split = autosplit ? (h->autos.chosen >= 0 ? kAutoSplits[h->autos.chosen] : 0) : -1;
   h->ran = true;
   h->counters_pending = true;
   return MOE_OK;
@@ -519,6 +628,7 @@ int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const
   }
   h->last.producer_grid = pgrid;
   h->last.consumer_grid = 0;
+  h->last.auto_cu_split = -1;
   h->last.consumer_cus = 0;
   const bool direct_all = (h->cfg.flags & MOE_DIRECT_ALL) != 0;
   const uint32_t mode = direct_all ? kModeDirectAll : 0u;
@@ -616,8 +726,15 @@ int moe_stage_destroy(moe_stage_t h) {
   for (hipEvent_t ev : {h->stage_free[0], h->stage_free[1], h->ev_fork, h->ev_join_c, h->ev_join_p,
                         h->ev_done})
     if (ev) (void)hipEventDestroy(ev);
-  if (h->s_cons) (void)hipStreamDestroy(h->s_cons);
-  if (h->s_prod) (void)hipStreamDestroy(h->s_prod);
+  for (auto& pair : h->autos.ev)
+    for (hipEvent_t ev : pair)
+      if (ev) (void)hipEventDestroy(ev);
+  hipStream_t shared_prod = nullptr;
+  for (const auto& q : h->queues) {
+    (void)hipStreamDestroy(q.cons);
+    if (q.prod && q.prod != shared_prod) (void)hipStreamDestroy(q.prod);
+    if (h->cfg.flags & MOE_SHARED_CUS) shared_prod = q.prod;
+  }
   for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->ctr, (void*)h->d_plan,
                   (void*)h->partials, (void*)h->arrivals})
     if (p) (void)hipFree(p);

@@ -18,7 +18,12 @@ mixtral         4096  14336  8     2   4   4096   2     U(0,1) iid
 mixtral_zipf    4096  14336  8     2   4   4096   2     Gumbel-top-k, p_e~(e+1)^-1.2
 fine            2048  1408   64    6   4   8192   16    N(0,1) + b_e, b_e~N(0,1)
 large_fine      7168  2048   256   8   8   4096   32    U(0,1) iid
+layer_e<E>      1024  4096   4E    2   4   8192   E     U(0,1) iid, E in 4..64
 ==============  ====  =====  ====  ==  ==  =====  ====  ============================
+
+The ``layer_e<E>`` family is the single-layer expert-count sweep of Section 4.2.2
+(one MoE block, 16 x 512 tokens per rank, top-2, model width 1024, E experts per
+rank); the paper states no FFN width, and the usual 4x width is taken.
 
 Conventions (see the dispatch description in Section 3.2.3, "non-overlapping
 offsets per peer across experts"):
@@ -54,6 +59,8 @@ CONFIGS: Dict[str, dict] = {
     "fine": dict(H=2048, F=1408, E_t=64, k=6, R=4, T_r=8192, E_l=16, router="normal_bias"),
     "large_fine": dict(H=7168, F=2048, E_t=256, k=8, R=8, T_r=4096, E_l=32, router="uniform"),
 }
+for _e in (4, 8, 16, 32, 64):
+    CONFIGS[f"layer_e{_e}"] = dict(H=1024, F=4096, E_t=4 * _e, k=2, R=4, T_r=8192, E_l=_e, router="uniform")
 
 ZIPF_S = 1.2
 WEIGHT_STD = 0.02

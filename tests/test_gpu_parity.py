@@ -246,9 +246,10 @@ def test_invalid_routing_enqueues_nothing():
             st.run(dw.x, wl.expert_offsets, bad_src, bad, dw.w1, dw.w3, dw.w2, dw.bufs, dw.return_rows,
                    cu_split=4)
         assert ei.value.code == B.MOE_EROUTING
-        with pytest.raises(B.MoeError) as ei:
-            st.run(*dw.args(), cu_split=0)
-        assert ei.value.code == B.MOE_EUNSUPPORTED
+        for bad_split in (-1, 10 ** 6):   # 0 asks for the adaptive selector, negative is invalid
+            with pytest.raises(B.MoeError) as ei:
+                st.run(*dw.args(), cu_split=bad_split)
+            assert ei.value.code == B.MOE_EUNSUPPORTED
     for b in dw.host_bufs():
         assert np.all(b == SENTINEL)
 
@@ -283,3 +284,27 @@ def test_consumer_only_copies_staged_rows():
             assert np.all(b[mine] == 0)
         other = np.setdiff1d(np.arange(b.shape[0]), mine)
         assert np.all(b[other] == SENTINEL)
+
+
+def test_auto_cu_split_settles_and_keeps_results():
+    """cu_split = 0: the handle measures its own runs at several consumer splits, settles on
+    one, and the output stays bitwise that of a fixed split (results never depend on it)."""
+    wl = make_workload("tiny", owner=0, overrides=RAGGED)
+    dw = DeviceWorkload(torch, wl)
+    ref = oracle_bufs(wl)
+    with make_stage(wl, flags=B.MOE_LOCAL_DIRECT | B.MOE_SHARED_CUS) as st:
+        fixed, _ = run_overlapped(dw, st, cu_split=8)
+    compare(fixed, ref)
+    seen = set()
+    with make_stage(wl, flags=B.MOE_LOCAL_DIRECT | B.MOE_SHARED_CUS) as st:
+        for i in range(16):
+            out, stats = run_overlapped(dw, st, cu_split=0)   # synchronises: every run measured
+            seen.add(stats["consumer_cus"])
+            for a, b in zip(out, fixed):
+                assert np.array_equal(a, b)
+        assert stats["auto_cu_split"] in (8, 16, 32, 64)
+        assert stats["consumer_cus"] == stats["auto_cu_split"]
+    assert seen >= {8, 16, 32, 64}
+    with make_stage(wl) as st:
+        st.run_serial(*dw.args())
+        assert st.query()["auto_cu_split"] == -1
