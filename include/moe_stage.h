@@ -134,7 +134,8 @@ typedef struct {
                                MOE_SHARED_CUS the producer runs on them too                  */
   int32_t timeout;          /* 1 if a device wait hit the watchdog in any run since the last
                                query (sticky across runs)                                    */
-  double plan_us;           /* host time to validate and build the plan                      */
+  double plan_us;           /* host time to validate and build the plan (device-built plans:
+                               to enqueue the planner)                                       */
   uint64_t poll_iters;      /* consumer flag-poll iterations summed over segments            */
   uint64_t wait_ticks;      /* consumer time spent waiting for flags (100 MHz ticks)         */
   int32_t gu_workgroups;    /* producer workgroups that claimed at least one tile in the last
@@ -200,8 +201,42 @@ int moe_stage_run_serial(moe_stage_t h, const void* dispatched_x, const int32_t*
                          const void* w3, const void* w2, void* const* return_bufs,
                          const int64_t* return_rows, void* stream);
 
+/*
+ * The same two runs with the plan built on the GPU (paper Section 3.2, Algorithm 1: layout,
+ * schedule and combine plan; Section 3.3.2: segments) from routing already in device memory:
+ *   expert_offsets  device int32 [num_local_experts + 1]
+ *   row_src_rank    device int32 [rows]  (rows = expert_offsets[num_local_experts])
+ *   row_slot        device int32 [rows]
+ * return_bufs and return_rows stay host arrays (the receive buffers' places and sizes).  A few
+ * small kernels on `stream` validate the routing and write the plan tables; the producer and
+ * consumer read their counts from device memory, so nothing waits for the host between the
+ * routing and the stage.  The tables are identical to those the host builder makes for the same
+ * routing (moe_stage_plan_copy reads them back).
+ *
+ * Precondition: the order a dispatch all-to-all delivers rows in -- within each expert, the
+ * rows of one source rank are contiguous and their slots ascend (source ranks may come in any
+ * order).  The host-planned entry points accept any order.
+ *
+ * Errors: argument errors (null pointers, negative return_rows) return at once and enqueue
+ * nothing.  Routing errors (the host path's MOE_EROUTING and MOE_ECAPACITY cases, and routing
+ * that breaks the precondition) are found on the device: the run then does no work, writes
+ * nothing to return_bufs, and the next moe_stage_query returns the code (the message names the
+ * first offending row).  Workspaces are sized at create; no run allocates memory.
+ */
+int moe_stage_run_devplan(moe_stage_t h, const void* dispatched_x, const int32_t* expert_offsets,
+                          const int32_t* row_src_rank, const int32_t* row_slot, const void* w1,
+                          const void* w3, const void* w2, void* const* return_bufs,
+                          const int64_t* return_rows, int32_t cu_split, void* stream);
+int moe_stage_run_serial_devplan(moe_stage_t h, const void* dispatched_x,
+                                 const int32_t* expert_offsets, const int32_t* row_src_rank,
+                                 const int32_t* row_slot, const void* w1, const void* w3,
+                                 const void* w2, void* const* return_bufs,
+                                 const int64_t* return_rows, void* stream);
+
 /* Statistics of the last run; synchronizes with it.  Returns MOE_ETIMEOUT (once) if any run
- * since the previous query had a device wait expire; its outputs are then incomplete. */
+ * since the previous query had a device wait expire; its outputs are then incomplete.  After a
+ * device-planned run it returns the planner's routing error (once), if any; its plan counts
+ * come from the device.  plan_us is the host time spent building (or enqueueing) the plan. */
 int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out);
 
 /* Kernel times accumulated since the last reset (needs MOE_KERNEL_TIMING); synchronizes. */
@@ -296,6 +331,11 @@ int moe_plan_info(moe_plan_t p, moe_plan_info_t* out);
  * dst is NULL, else MOE_OK or MOE_EINVAL when bytes is too small. */
 int64_t moe_plan_copy(moe_plan_t p, int32_t which, void* dst, int64_t bytes);
 void moe_plan_free(moe_plan_t p);
+
+/* The plan of a handle's last run (host- or device-built), read back from device memory in
+ * the layouts above; both synchronize with that run.  MOE_EINVAL before the first run. */
+int moe_stage_plan_info(moe_stage_t h, moe_plan_info_t* out);
+int64_t moe_stage_plan_copy(moe_stage_t h, int32_t which, void* dst, int64_t bytes);
 
 #ifdef __cplusplus
 }

@@ -27,7 +27,8 @@ ERROR_NAMES = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EROUTING", -3: "MOE_ECAPA
 
 EXPORTED = ["moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query", "moe_stage_times",
             "moe_stage_last_error", "moe_stage_destroy", "moe_plan_build", "moe_plan_info", "moe_plan_copy",
-            "moe_plan_free", "moe_combine"]
+            "moe_plan_free", "moe_combine", "moe_stage_run_devplan", "moe_stage_run_serial_devplan",
+            "moe_stage_plan_info", "moe_stage_plan_copy"]
 
 
 class moe_stage_config_t(ctypes.Structure):
@@ -95,6 +96,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.moe_plan_free.argtypes = [vp]
     lib.moe_plan_free.restype = None
     lib.moe_combine.argtypes = [vp, i64, i32, vp, vp, i64, i32, vp, vp, vp]
+    lib.moe_stage_run_devplan.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp]
+    lib.moe_stage_run_serial_devplan.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.moe_stage_plan_info.argtypes = [vp, ctypes.POINTER(moe_plan_info_t)]
+    lib.moe_stage_plan_copy.argtypes = [vp, i32, vp, i64]
+    lib.moe_stage_plan_copy.restype = ctypes.c_int64
     for name in ("moe_combine", "moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query",
                  "moe_stage_times", "moe_stage_destroy", "moe_plan_build", "moe_plan_info"):
         getattr(lib, name).restype = ctypes.c_int
@@ -196,6 +202,36 @@ def moe_stage_run_serial(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w
     return _check(rc, h)
 
 
+def _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows):
+    import torch
+    for name, t in (("expert_offsets", expert_offsets), ("row_src_rank", row_src_rank), ("row_slot", row_slot)):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.int32:
+            raise ValueError(f"{name} must be an int32 device tensor")
+    rr = _host_i64(return_rows if return_rows is not None else [b.shape[0] for b in return_bufs])
+    ptrs = (ctypes.c_void_p * len(return_bufs))(*[_dev_ptr(b) for b in return_bufs])
+    keep = (rr, ptrs)
+    args = [_dev_ptr(x), _dev_ptr(expert_offsets), _dev_ptr(row_src_rank), _dev_ptr(row_slot),
+            _dev_ptr(w1), _dev_ptr(w3), _dev_ptr(w2), ctypes.cast(ptrs, ctypes.c_void_p), _np_ptr(rr)]
+    return args, keep
+
+
+def moe_stage_run_devplan(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs: Sequence,
+                          return_rows=None, cu_split: int = 8, stream=None) -> int:
+    """moe_stage_run with the routing (int32 device tensors) planned on the device."""
+    args, keep = _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows)
+    rc = load().moe_stage_run_devplan(h, *args, int(cu_split), _stream_ptr(stream))
+    del keep
+    return _check(rc, h)
+
+
+def moe_stage_run_serial_devplan(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2,
+                                 return_bufs: Sequence, return_rows=None, stream=None) -> int:
+    args, keep = _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows)
+    rc = load().moe_stage_run_serial_devplan(h, *args, _stream_ptr(stream))
+    del keep
+    return _check(rc, h)
+
+
 def moe_combine(recv, slot, gate, out, bad_slots=None, stream=None) -> int:
     """Weighted combine of one source rank on the device.
 
@@ -248,25 +284,36 @@ def moe_plan_build(cfg: moe_stage_config_t, expert_offsets, row_src_rank, row_sl
     _check(lib.moe_plan_build(ctypes.byref(cfg), rows, _np_ptr(off), _np_ptr(src), _np_ptr(slot), _np_ptr(rr),
                               int(bool(overlapped)), ctypes.byref(p)))
     try:
-        info = moe_plan_info_t()
-        _check(lib.moe_plan_info(p, ctypes.byref(info)))
-        out = {"info": _struct_dict(info)}
-        for key, which, dt, width in (("tile_rows", MOE_PLAN_TILE_ROWS, np.int32, 6),
-                                      ("items", MOE_PLAN_ITEMS, np.uint32, 1),
-                                      ("row_x", MOE_PLAN_ROW_X, np.int32, 1),
-                                      ("row_rank", MOE_PLAN_ROW_RANK, np.int32, 1),
-                                      ("row_slot", MOE_PLAN_ROW_SLOT, np.int32, 1),
-                                      ("segments", MOE_PLAN_SEGMENTS, np.int32, 8),
-                                      ("groups", MOE_PLAN_GROUPS, np.int32, 4),
-                                      ("queues", MOE_PLAN_QUEUES, np.int32, 9)):
-            need = lib.moe_plan_copy(p, which, None, 0)
-            arr = np.empty(need // np.dtype(dt).itemsize, dt)
-            if need:
-                _check(lib.moe_plan_copy(p, which, _np_ptr(arr), need))
-            out[key] = arr.reshape(-1, width) if width > 1 else arr
-        return out
+        return _read_plan(lambda o: lib.moe_plan_info(p, o), lambda w, d, n: lib.moe_plan_copy(p, w, d, n))
     finally:
         lib.moe_plan_free(p)
+
+
+_PLAN_TABLES = (("tile_rows", MOE_PLAN_TILE_ROWS, np.int32, 6), ("items", MOE_PLAN_ITEMS, np.uint32, 1),
+                ("row_x", MOE_PLAN_ROW_X, np.int32, 1), ("row_rank", MOE_PLAN_ROW_RANK, np.int32, 1),
+                ("row_slot", MOE_PLAN_ROW_SLOT, np.int32, 1), ("segments", MOE_PLAN_SEGMENTS, np.int32, 8),
+                ("groups", MOE_PLAN_GROUPS, np.int32, 4), ("queues", MOE_PLAN_QUEUES, np.int32, 9))
+
+
+def _read_plan(info_fn, copy_fn, h=None) -> dict:
+    info = moe_plan_info_t()
+    _check(info_fn(ctypes.byref(info)), h)
+    out = {"info": _struct_dict(info)}
+    for key, which, dt, width in _PLAN_TABLES:
+        need = copy_fn(which, None, 0)
+        if need < 0:
+            _check(int(need), h)
+        arr = np.empty(need // np.dtype(dt).itemsize, dt)
+        if need:
+            _check(int(copy_fn(which, _np_ptr(arr), need)), h)
+        out[key] = arr.reshape(-1, width) if width > 1 else arr
+    return out
+
+
+def moe_stage_plan(h) -> dict:
+    """The plan of the handle's last run, read back from the device (same tables as moe_plan_build)."""
+    lib = load()
+    return _read_plan(lambda o: lib.moe_stage_plan_info(h, o), lambda w, d, n: lib.moe_stage_plan_copy(h, w, d, n), h)
 
 
 # ----------------------------------------------------------------------------- convenience wrapper
@@ -289,6 +336,19 @@ class MoeStage:
                    stream=None):
         return moe_stage_run_serial(self.h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs,
                                     return_rows, stream)
+
+    def run_devplan(self, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows=None,
+                    cu_split=8, stream=None):
+        return moe_stage_run_devplan(self.h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs,
+                                     return_rows, cu_split, stream)
+
+    def run_serial_devplan(self, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs,
+                           return_rows=None, stream=None):
+        return moe_stage_run_serial_devplan(self.h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2,
+                                            return_bufs, return_rows, stream)
+
+    def plan(self) -> dict:
+        return moe_stage_plan(self.h)
 
     def query(self, check=True) -> dict:
         return moe_stage_query(self.h, check)

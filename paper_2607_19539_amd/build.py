@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "libmoe_stage.so")
-SOURCES = ["kernels.hip", "combine.hip", "plan.cpp", "api.cpp"]
+SOURCES = ["kernels.hip", "combine.hip", "plan_device.hip", "plan.cpp", "api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # -packed-fp32-ops: never emit packed fp32 VALU ops (v_pk_add/mul/fma_f32).

@@ -21,6 +21,7 @@
 #include "../../include/moe_stage.h"
 #include "kernels.hpp"
 #include "plan.hpp"
+#include "plan_device.hpp"
 
 using namespace moe;
 
@@ -55,6 +56,30 @@ struct TimingRec {
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
+// Byte layout of the device plan blob.  The host builder packs it to the plan's own sizes;
+// the device builder writes into the layout of the handle's capacity.
+struct BlobLayout {
+  size_t hdr, tile_rows, items, queues, row_x, row_rank, row_slot, segs, groups, ret, total;
+};
+
+BlobLayout blob_layout(int64_t n_tr, int64_t n_items, int64_t n_lrows, int64_t n_segs, int64_t n_groups,
+                       int32_t R) {
+  BlobLayout b{};
+  size_t o = 0;
+  b.hdr = o;       o = align256(o + sizeof(PlanHeader));
+  b.tile_rows = o; o = align256(o + sizeof(TileRow) * (size_t)n_tr);
+  b.items = o;     o = align256(o + sizeof(uint32_t) * (size_t)n_items);
+  b.queues = o;    o = align256(o + sizeof(int32_t) * 2 * (kXcds + 1));
+  b.row_x = o;     o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
+  b.row_rank = o;  o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
+  b.row_slot = o;  o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
+  b.segs = o;      o = align256(o + sizeof(Segment) * (size_t)n_segs);
+  b.groups = o;    o = align256(o + sizeof(Group) * (size_t)n_groups);
+  b.ret = o;       o = align256(o + (sizeof(void*) + sizeof(int64_t)) * (size_t)R);  // pointers, then rows
+  b.total = o;
+  return b;
+}
+
 }  // namespace
 
 struct moe_stage_s {
@@ -75,6 +100,14 @@ struct moe_stage_s {
   RunCounters* ctr = nullptr;
   uint8_t* d_plan = nullptr;
   size_t plan_cap = 0;
+  BlobLayout cap_lay{};   // the blob at the handle's capacity (device-built plans)
+  BlobLayout last_lay{};  // the blob of the last run
+  void* dev_ws = nullptr; // device planner scratch
+  DevPlanWs ws{};
+  bool last_dev = false;         // the last run's plan was built on the device
+  bool last_overlapped = false;
+  bool dev_hdr_pending = false;  // its header has not been read back yet
+  int32_t dev_status = 0, dev_bad_row = 0;
   uint8_t* h_stage[2] = {nullptr, nullptr};
   hipEvent_t stage_free[2] = {nullptr, nullptr};
   int stage_idx = 0;
@@ -157,85 +190,23 @@ int check_config(const moe_stage_config_t* c) {
   return MOE_OK;
 }
 
-// Byte layout of the device plan blob.
-struct BlobLayout {
-  size_t tile_rows, items, queues, row_x, row_rank, row_slot, segs, ret, total;
-};
-
-BlobLayout blob_layout(int64_t n_tr, int64_t n_items, int64_t n_lrows, int64_t n_segs, int32_t R) {
-  BlobLayout b{};
-  size_t o = 0;
-  b.tile_rows = o; o = align256(o + sizeof(TileRow) * (size_t)n_tr);
-  b.items = o;     o = align256(o + sizeof(uint32_t) * (size_t)n_items);
-  b.queues = o;    o = align256(o + sizeof(int32_t) * 2 * (kXcds + 1));
-  b.row_x = o;     o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
-  b.row_rank = o;  o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
-  b.row_slot = o;  o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
-  b.segs = o;      o = align256(o + sizeof(Segment) * (size_t)n_segs);
-  b.ret = o;       o = align256(o + sizeof(void*) * (size_t)R);
-  b.total = o;
-  return b;
-}
-
 uint64_t watchdog_ticks(const moe_stage_s* h) {
   const int ms = h->cfg.watchdog_ms > 0 ? h->cfg.watchdog_ms : 2000;
   return (uint64_t)ms * 100000ull;  // wall clock runs at 100 MHz
 }
 
-// Validates and builds the plan, uploads it and resets the run counters, all on `stream`.
-int prepare(moe_stage_s* h, bool overlapped, const void* x,
-            const int32_t* off, const int32_t* src, const int32_t* slot, const void* w1,
-            const void* w3, const void* w2, void* const* ret, const int64_t* return_rows,
-            hipStream_t stream, BlobLayout* lay) {
-  const auto t0 = std::chrono::steady_clock::now();
+// Resets the run counters on `stream` (and, before a device-built plan, the planner's scratch
+// and header), and advances the flag epoch.
+int enqueue_init(moe_stage_s* h, bool overlapped, bool dev, int32_t n_tile_rows, int64_t n_lrows,
+                 hipStream_t stream) {
   const moe_stage_config_t& c = h->cfg;
-  if (!off || !return_rows || !ret) return set_err(h, MOE_EINVAL, "null routing or buffer array");
-  const int64_t rows = off[c.num_local_experts];
-  if (rows < 0) return set_err(h, MOE_EROUTING, "expert_offsets[E_l] < 0");
-  if (rows > c.max_rows)
-    return set_err(h, MOE_ECAPACITY, "rows " + std::to_string(rows) + " > max_rows " +
-                                         std::to_string(c.max_rows));
-  if (rows > 0 && (!x || !w1 || !w3 || !w2)) return set_err(h, MOE_EINVAL, "null tensor pointer");
-  for (int r = 0; r < c.num_ranks; ++r)
-    if (!ret[r] && return_rows[r] > 0) return set_err(h, MOE_EINVAL, "null return buffer");
-
-  std::string msg;
-  int rc = build_plan(params_of(c, overlapped), rows, off, src, slot, return_rows, &h->plan, &msg);
-  if (rc) return set_err(h, rc, msg);
-  const Plan& P = h->plan;
-  if (P.n_lrows() > h->max_lrows || (int64_t)P.tile_rows.size() > h->max_tile_rows)
-    return set_err(h, MOE_ECAPACITY, "plan exceeds the handle's workspaces");
-  *lay = blob_layout((int64_t)P.tile_rows.size(), (int64_t)P.items.size(), P.n_lrows(),
-                     (int64_t)P.segs.size(), c.num_ranks);
-  if (lay->total > h->plan_cap) return set_err(h, MOE_ECAPACITY, "plan exceeds the plan buffer");
-
-  h->last.plan_us =
-      std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
-  // Stage into pinned memory (wait until the copy that last used this half finished).
-  const int si = h->stage_idx;
-  h->stage_idx ^= 1;
-  HIP_TRY(h, hipEventSynchronize(h->stage_free[si]));
-  uint8_t* hs = h->h_stage[si];
-  memcpy(hs + lay->tile_rows, P.tile_rows.data(), sizeof(TileRow) * P.tile_rows.size());
-  memcpy(hs + lay->items, P.items.data(), sizeof(uint32_t) * P.items.size());
-  memcpy(hs + lay->queues, P.gu_queue.data(), sizeof(int32_t) * (kXcds + 1));
-  memcpy(hs + lay->queues + sizeof(int32_t) * (kXcds + 1), P.down_queue.data(), sizeof(int32_t) * (kXcds + 1));
-  memcpy(hs + lay->row_x, P.row_x.data(), sizeof(int32_t) * P.row_x.size());
-  memcpy(hs + lay->row_rank, P.row_rank.data(), sizeof(int32_t) * P.row_rank.size());
-  memcpy(hs + lay->row_slot, P.row_slot.data(), sizeof(int32_t) * P.row_slot.size());
-  memcpy(hs + lay->segs, P.segs.data(), sizeof(Segment) * P.segs.size());
-  memcpy(hs + lay->ret, ret, sizeof(void*) * (size_t)c.num_ranks);
-
-  HIP_TRY(h, hipMemcpyAsync(h->d_plan, hs, lay->total, hipMemcpyHostToDevice, stream));
-  HIP_TRY(h, hipEventRecord(h->stage_free[si], stream));
-
   InitArgs ia{};
   ia.ctr = h->ctr;
   ia.arrivals = h->arrivals;
-  ia.n_arrivals = (int32_t)P.tile_rows.size() * P.down_per_row;
+  ia.n_arrivals = n_tile_rows * h->down_per_row;
   if (c.flags & MOE_POISON) {
     ia.poison = h->y;
-    ia.poison_elems = P.n_lrows() * c.hidden;
+    ia.poison_elems = n_lrows * c.hidden;
   }
   const uint32_t epoch = h->epoch + 1 == 0 ? 1 : h->epoch + 1;  // flags hold the epoch of the run that set them
   if (overlapped && (c.flags & MOE_TEST_CONSUMER_ONLY)) {
@@ -243,8 +214,101 @@ int prepare(moe_stage_s* h, bool overlapped, const void* x,
     ia.n_publish = ia.n_arrivals;
     ia.epoch = epoch;
   }
+  if (dev) {
+    ia.fill_ones = (uint32_t*)h->ws.run_lo;
+    ia.n_fill_ones = h->ws.fill_words;
+    ia.plan_hdr = (PlanHeader*)(h->d_plan + h->cap_lay.hdr);
+  }
   HIP_TRY(h, launch_init(ia, stream));
   h->epoch = epoch;
+  return MOE_OK;
+}
+
+// Host arguments both planners check before anything is enqueued.
+int check_run_args(moe_stage_s* h, const void* const* ret, const int64_t* return_rows) {
+  if (!return_rows || !ret) return set_err(h, MOE_EINVAL, "null receive-buffer array");
+  for (int r = 0; r < h->cfg.num_ranks; ++r) {
+    if (return_rows[r] < 0) return set_err(h, MOE_EINVAL, "return_rows[" + std::to_string(r) + "] < 0");
+    if (!ret[r] && return_rows[r] > 0) return set_err(h, MOE_EINVAL, "null return buffer");
+  }
+  return MOE_OK;
+}
+
+// Validates and builds the plan on the host, uploads it and resets the run counters, all on
+// `stream`.
+int prepare(moe_stage_s* h, bool overlapped, const void* x,
+            const int32_t* off, const int32_t* src, const int32_t* slot, const void* w1,
+            const void* w3, const void* w2, void* const* ret, const int64_t* return_rows,
+            hipStream_t stream, BlobLayout* lay) {
+  const auto t0 = std::chrono::steady_clock::now();
+  const moe_stage_config_t& c = h->cfg;
+  if (!off) return set_err(h, MOE_EINVAL, "null routing array");
+  int rc = check_run_args(h, ret, return_rows);
+  if (rc) return rc;
+  const int64_t rows = off[c.num_local_experts];
+  if (rows < 0) return set_err(h, MOE_EROUTING, "expert_offsets[E_l] < 0");
+  if (rows > c.max_rows)
+    return set_err(h, MOE_ECAPACITY, "rows " + std::to_string(rows) + " > max_rows " +
+                                         std::to_string(c.max_rows));
+  if (rows > 0 && (!x || !w1 || !w3 || !w2)) return set_err(h, MOE_EINVAL, "null tensor pointer");
+
+  std::string msg;
+  rc = build_plan(params_of(c, overlapped), rows, off, src, slot, return_rows, &h->plan, &msg);
+  if (rc) return set_err(h, rc, msg);
+  const Plan& P = h->plan;
+  if (P.n_lrows() > h->max_lrows || (int64_t)P.tile_rows.size() > h->max_tile_rows)
+    return set_err(h, MOE_ECAPACITY, "plan exceeds the handle's workspaces");
+  *lay = blob_layout((int64_t)P.tile_rows.size(), (int64_t)P.items.size(), P.n_lrows(),
+                     (int64_t)P.segs.size(), (int64_t)P.groups.size(), c.num_ranks);
+  if (lay->total > h->plan_cap) return set_err(h, MOE_ECAPACITY, "plan exceeds the plan buffer");
+
+  h->last.plan_us =
+      std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+  PlanHeader hd{};
+  hd.bad_row = INT32_MAX;
+  hd.n_tile_rows = (int32_t)P.tile_rows.size();
+  hd.n_groups = hd.n_groups_all = (int32_t)P.groups.size();
+  hd.n_gu = P.n_gu;
+  hd.n_down = P.n_down;
+  hd.n_segs = (int32_t)P.segs.size();
+  hd.tail_split = P.tail_split;
+  hd.n_split_rows = P.n_split_rows;
+  hd.n_partials = P.n_partials;
+  hd.n_valid = P.n_valid;
+  hd.n_lrows = P.n_lrows();
+  hd.n_band_pad = P.n_band_pad;
+  hd.n_remote = P.n_remote;
+  // The kernels index the whole item table: the down queues follow the gate/up items.
+  int32_t queues[2 * (kXcds + 1)];
+  for (int x = 0; x <= kXcds; ++x) {
+    queues[x] = P.gu_queue[x];
+    queues[kXcds + 1 + x] = P.n_gu + P.down_queue[x];
+  }
+  // Stage into pinned memory (wait until the copy that last used this half finished).
+  const int si = h->stage_idx;
+  h->stage_idx ^= 1;
+  HIP_TRY(h, hipEventSynchronize(h->stage_free[si]));
+  uint8_t* hs = h->h_stage[si];
+  memcpy(hs + lay->hdr, &hd, sizeof hd);
+  memcpy(hs + lay->tile_rows, P.tile_rows.data(), sizeof(TileRow) * P.tile_rows.size());
+  memcpy(hs + lay->items, P.items.data(), sizeof(uint32_t) * P.items.size());
+  memcpy(hs + lay->queues, queues, sizeof queues);
+  memcpy(hs + lay->row_x, P.row_x.data(), sizeof(int32_t) * P.row_x.size());
+  memcpy(hs + lay->row_rank, P.row_rank.data(), sizeof(int32_t) * P.row_rank.size());
+  memcpy(hs + lay->row_slot, P.row_slot.data(), sizeof(int32_t) * P.row_slot.size());
+  memcpy(hs + lay->segs, P.segs.data(), sizeof(Segment) * P.segs.size());
+  memcpy(hs + lay->groups, P.groups.data(), sizeof(Group) * P.groups.size());
+  memcpy(hs + lay->ret, ret, sizeof(void*) * (size_t)c.num_ranks);
+  memcpy(hs + lay->ret + sizeof(void*) * (size_t)c.num_ranks, return_rows, sizeof(int64_t) * (size_t)c.num_ranks);
+
+  HIP_TRY(h, hipMemcpyAsync(h->d_plan, hs, lay->total, hipMemcpyHostToDevice, stream));
+  HIP_TRY(h, hipEventRecord(h->stage_free[si], stream));
+  rc = enqueue_init(h, overlapped, false, (int32_t)P.tile_rows.size(), P.n_lrows(), stream);
+  if (rc) return rc;
+  h->last_lay = *lay;
+  h->last_dev = false;
+  h->dev_hdr_pending = false;
+  h->last_overlapped = overlapped;
   moe_stage_stats_t& st = h->last;
   st.n_valid = P.n_valid;
   st.n_logical_rows = P.n_lrows();
@@ -260,9 +324,79 @@ int prepare(moe_stage_s* h, bool overlapped, const void* x,
   return MOE_OK;
 }
 
+// Enqueues the device planner on `stream` for routing already in device memory: only the
+// receive-buffer pointers and sizes go up from the host.  Routing errors are found on the
+// device; the plan is then empty and moe_stage_query reports them.
+int prepare_device(moe_stage_s* h, bool overlapped, const void* x, const int32_t* off,
+                   const int32_t* src, const int32_t* slot, const void* w1, const void* w3,
+                   const void* w2, void* const* ret, const int64_t* return_rows, hipStream_t stream,
+                   BlobLayout* lay) {
+  const auto t0 = std::chrono::steady_clock::now();
+  const moe_stage_config_t& c = h->cfg;
+  if (!off || !src || !slot) return set_err(h, MOE_EINVAL, "null routing array");
+  if (!x || !w1 || !w3 || !w2) return set_err(h, MOE_EINVAL, "null tensor pointer");
+  int rc = check_run_args(h, ret, return_rows);
+  if (rc) return rc;
+  const int32_t gu_per_row = (c.ffn + kGuTileF - 1) / kGuTileF;
+  if (gu_per_row >= kMaxColTiles || h->down_per_row > kMaxDownColTiles)
+    return set_err(h, MOE_EUNSUPPORTED, "hidden or ffn too large for the work-item encoding");
+  *lay = h->cap_lay;
+  const size_t R = (size_t)c.num_ranks;
+  const int si = h->stage_idx;
+  h->stage_idx ^= 1;
+  HIP_TRY(h, hipEventSynchronize(h->stage_free[si]));
+  uint8_t* hs = h->h_stage[si];
+  memcpy(hs, ret, sizeof(void*) * R);
+  memcpy(hs + sizeof(void*) * R, return_rows, sizeof(int64_t) * R);
+  HIP_TRY(h, hipMemcpyAsync(h->d_plan + lay->ret, hs, (sizeof(void*) + sizeof(int64_t)) * R,
+                            hipMemcpyHostToDevice, stream));
+  HIP_TRY(h, hipEventRecord(h->stage_free[si], stream));
+  rc = enqueue_init(h, overlapped, true, h->max_tile_rows, h->max_lrows, stream);
+  if (rc) return rc;
+
+  DevPlanArgs a{};
+  a.off = off;
+  a.src = src;
+  a.slot = slot;
+  a.return_rows = (const int64_t*)(h->d_plan + lay->ret + sizeof(void*) * R);
+  a.E_l = c.num_local_experts;
+  a.R = c.num_ranks;
+  a.self = c.self_rank;
+  a.tb = std::max(c.band_rows, 1);
+  a.mid_pieces = std::max(c.mid_segment_pieces, 1);
+  const PlanParams pp;
+  a.gu_group = pp.gu_group;
+  a.down_group = pp.down_group;
+  a.split_k = c.down_split_k;
+  a.gu_per_row = gu_per_row;
+  a.down_per_row = h->down_per_row;
+  a.nk = c.ffn / kTileK;
+  a.overlapped = overlapped ? 1 : 0;
+  a.local_direct = (c.flags & MOE_LOCAL_DIRECT) ? 1 : 0;
+  a.max_rows = c.max_rows;
+  a.max_tile_rows = h->max_tile_rows;
+  a.hdr = (PlanHeader*)(h->d_plan + lay->hdr);
+  a.tile_rows = (TileRow*)(h->d_plan + lay->tile_rows);
+  a.items = (uint32_t*)(h->d_plan + lay->items);
+  a.queues = (int32_t*)(h->d_plan + lay->queues);
+  a.row_x = (int32_t*)(h->d_plan + lay->row_x);
+  a.row_rank = (int32_t*)(h->d_plan + lay->row_rank);
+  a.row_slot = (int32_t*)(h->d_plan + lay->row_slot);
+  a.segs = (Segment*)(h->d_plan + lay->segs);
+  a.groups = (Group*)(h->d_plan + lay->groups);
+  a.ws = h->ws;
+  HIP_TRY(h, launch_devplan(a, h->num_cus, stream));
+  h->last.plan_us =
+      std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+  h->last_lay = *lay;
+  h->last_dev = true;
+  h->dev_hdr_pending = true;
+  h->last_overlapped = overlapped;
+  return MOE_OK;
+}
+
 ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x, const void* w1,
                            const void* w3, const void* w2, uint32_t mode, bool down) {
-  const Plan& P = h->plan;
   ProducerArgs a{};
   a.x = (const uint16_t*)x;
   a.w1 = (const uint16_t*)w1;
@@ -272,8 +406,7 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
   a.hws_rows = h->max_lrows;
   a.y = h->y;
   a.tile_rows = (const TileRow*)(h->d_plan + lay.tile_rows);
-  a.items = (const uint32_t*)(h->d_plan + lay.items) + (down ? P.n_gu : 0);
-  a.n_items = down ? P.n_down : P.n_gu;
+  a.items = (const uint32_t*)(h->d_plan + lay.items);
   a.queue = (const int32_t*)(h->d_plan + lay.queues) + (down ? kXcds + 1 : 0);
   a.claim = down ? h->ctr->down_next : h->ctr->gu_next;
   a.active = down ? &h->ctr->down_active : &h->ctr->gu_active;
@@ -286,9 +419,9 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
   a.H = h->cfg.hidden;
   a.F = h->cfg.ffn;
   a.self_rank = h->cfg.self_rank;
-  a.down_per_row = P.down_per_row;
+  a.down_per_row = h->down_per_row;
   a.mode = mode;
-  a.split_k = P.p.split_k;
+  a.split_k = h->cfg.down_split_k;
   a.partials = h->partials;
   a.arrivals = h->arrivals;
   return a;
@@ -454,9 +587,12 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   // round of parts for the split tail rows (default).
   const int64_t max_items = (int64_t)h->max_tile_rows * (gu_per_row + (int64_t)h->down_per_row * std::max(S, 1)) +
                             (S == 0 ? kRoundTiles : 0);
-  const BlobLayout lay =
-      blob_layout(h->max_tile_rows, max_items, h->max_lrows, h->max_lrows, cfg->num_ranks);
-  h->plan_cap = lay.total;
+  // Segments: at most one per routed row.  Groups: one per (local expert, source rank).
+  h->cap_lay = blob_layout(h->max_tile_rows, max_items, h->max_lrows, h->max_lrows,
+                           (int64_t)cfg->num_local_experts * cfg->num_ranks, cfg->num_ranks);
+  h->plan_cap = h->cap_lay.total;
+  const size_t ws_bytes = devplan_ws_bytes(cfg->num_local_experts, cfg->num_ranks, cfg->max_rows,
+                                           h->max_tile_rows, h->down_per_row, h->max_lrows, max_items);
 
   auto try_hip = [&](hipError_t err, const char* what) {
     if (err != hipSuccess) {
@@ -479,6 +615,7 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       !try_hip(hipMalloc(&h->flags, flag_bytes), "hipMalloc(flags)") ||
       !try_hip(hipMalloc(&h->ctr, sizeof(RunCounters)), "hipMalloc(counters)") ||
       !try_hip(hipMalloc(&h->d_plan, h->plan_cap), "hipMalloc(plan)") ||
+      !try_hip(hipMalloc(&h->dev_ws, ws_bytes), "hipMalloc(planner scratch)") ||
       !try_hip(hipHostMalloc(&h->h_stage[0], h->plan_cap, hipHostMallocDefault), "hipHostMalloc") ||
       !try_hip(hipHostMalloc(&h->h_stage[1], h->plan_cap, hipHostMallocDefault), "hipHostMalloc") ||
       !try_hip(hipMemset(h->hws, 0, hws_bytes), "hipMemset(hws)") ||
@@ -486,6 +623,8 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       !try_hip(hipMemset(h->flags, 0, flag_bytes), "hipMemset(flags)") ||
       !try_hip(hipMemset(h->ctr, 0, sizeof(RunCounters)), "hipMemset(counters)"))
     return bail(MOE_EHIP);
+  h->ws = devplan_ws_carve(h->dev_ws, cfg->num_local_experts, cfg->num_ranks, cfg->max_rows,
+                           h->max_tile_rows, h->down_per_row, h->max_lrows, max_items);
   // Every event here orders work on this device or marks completion for the host; none
   // publishes device writes to the host (results are read through the caller's own copies),
   // so a device-scope release suffices and no system-scope cache writeback sits between
@@ -516,9 +655,10 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   return MOE_OK;
 }
 
-int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_t* src,
-                  const int32_t* slot, const void* w1, const void* w3, const void* w2,
-                  void* const* ret, const int64_t* return_rows, int32_t cu_split, void* stream_) {
+static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t* off,
+                          const int32_t* src, const int32_t* slot, const void* w1, const void* w3,
+                          const void* w2, void* const* ret, const int64_t* return_rows,
+                          int32_t cu_split, void* stream_) {
   if (!h) return MOE_EINVAL;
   hipStream_t stream = (hipStream_t)stream_;
   const bool autosplit = cu_split == 0;
@@ -544,7 +684,8 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   TimingRec* tr = timing_slot(h);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[0], stream));
   if (auto_slot >= 0) HIP_TRY(h, hipEventRecord(h->autos.ev[auto_slot][0], stream));
-  rc = prepare(h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
+  rc = dev ? prepare_device(h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay)
+           : prepare(h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
   if (rc) {
     if (tr) h->ring_next = (h->ring_next + kTimingRing - 1) % kTimingRing, --h->ring_count;
     return rc;
@@ -560,7 +701,7 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   ca.y = h->y;
   ca.ret = pgu.ret;
   ca.segs = (const Segment*)(h->d_plan + lay.segs);
-  ca.n_segs = (int32_t)h->plan.segs.size();
+  ca.n_segs = &((const PlanHeader*)(h->d_plan + lay.hdr))->n_segs;
   ca.flags = h->flags;
   ca.epoch = h->epoch;
   ca.H = h->cfg.hidden;
@@ -581,14 +722,17 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   HIP_TRY(h, hipStreamWaitEvent(h->s_cons, h->ev_fork, 0));
   if (!on_caller) HIP_TRY(h, hipStreamWaitEvent(h->s_prod, h->ev_fork, 0));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[3], h->s_cons));
-  if (ca.n_segs > 0) HIP_TRY(h, launch_consumer(ca, cgrid, h->s_cons));
+  // A host-built plan's counts are known here, so empty launches are skipped; a device-built
+  // plan's kernels read them and return at once when there is nothing to do.
+  const bool known = !dev;
+  if (!known || !h->plan.segs.empty()) HIP_TRY(h, launch_consumer(ca, cgrid, h->s_cons));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
   HIP_TRY(h, hipEventRecord(h->ev_join_c, h->s_cons));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], ps));
   const bool producer = !(h->cfg.flags & MOE_TEST_CONSUMER_ONLY);
-  if (producer && pgu.n_items > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, ps));
+  if (producer && (!known || h->plan.n_gu > 0)) HIP_TRY(h, launch_producer(pgu, false, pgrid, ps));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], ps));
-  if (producer && pdn.n_items > 0) HIP_TRY(h, launch_producer(pdn, true, pgrid, ps));
+  if (producer && (!known || h->plan.n_down > 0)) HIP_TRY(h, launch_producer(pdn, true, pgrid, ps));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], ps));
   if (!on_caller) {
     HIP_TRY(h, hipEventRecord(h->ev_join_p, h->s_prod));
@@ -612,16 +756,17 @@ int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_
   return MOE_OK;
 }
 
-int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const int32_t* src,
-                         const int32_t* slot, const void* w1, const void* w3, const void* w2,
-                         void* const* ret, const int64_t* return_rows, void* stream_) {
+static int run_serial(moe_stage_t h, bool dev, const void* x, const int32_t* off,
+                      const int32_t* src, const int32_t* slot, const void* w1, const void* w3,
+                      const void* w2, void* const* ret, const int64_t* return_rows, void* stream_) {
   if (!h) return MOE_EINVAL;
   hipStream_t stream = (hipStream_t)stream_;
   const int pgrid = h->num_cus * h->producer_bpc;
   BlobLayout lay{};
   TimingRec* tr = timing_slot(h);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[0], stream));
-  int rc = prepare(h, false, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
+  int rc = dev ? prepare_device(h, false, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay)
+               : prepare(h, false, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
   if (rc) {
     if (tr) h->ring_next = (h->ring_next + kTimingRing - 1) % kTimingRing, --h->ring_count;
     return rc;
@@ -635,20 +780,22 @@ int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const
   const ProducerArgs pgu = producer_args(h, lay, x, w1, w3, w2, mode, false);
   const ProducerArgs pa = producer_args(h, lay, x, w1, w3, w2, mode, true);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], stream));
-  if (pgu.n_items > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, stream));
+  const bool known = !dev;
+  if (!known || h->plan.n_gu > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, stream));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], stream));
-  if (pa.n_items > 0) HIP_TRY(h, launch_producer(pa, true, pgrid, stream));
+  if (!known || h->plan.n_down > 0) HIP_TRY(h, launch_producer(pa, true, pgrid, stream));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], stream));
   ScatterArgs sa{};
   sa.y = h->y;
   sa.ret = pa.ret;
   sa.row_rank = pa.row_rank;
   sa.row_slot = pa.row_slot;
-  sa.n_lrows = h->plan.n_lrows();
+  sa.n_lrows = &((const PlanHeader*)(h->d_plan + lay.hdr))->n_lrows;
   sa.H = h->cfg.hidden;
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], stream));
-  if (sa.n_lrows > 0 && !direct_all)
-    HIP_TRY(h, launch_scatter(sa, (int)std::min<int64_t>(sa.n_lrows, (int64_t)h->num_cus * 8), stream));
+  const int64_t scatter_rows = known ? h->plan.n_lrows() : h->max_lrows;
+  if (scatter_rows > 0 && !direct_all)
+    HIP_TRY(h, launch_scatter(sa, (int)std::min<int64_t>(scatter_rows, (int64_t)h->num_cus * 8), stream));
   if (tr) {
     HIP_TRY(h, hipEventRecord(tr->ev[5], stream));
     tr->kind = 1;
@@ -657,6 +804,32 @@ int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const
   h->ran = true;
   h->counters_pending = true;
   return MOE_OK;
+}
+
+int moe_stage_run(moe_stage_t h, const void* x, const int32_t* off, const int32_t* src,
+                  const int32_t* slot, const void* w1, const void* w3, const void* w2,
+                  void* const* ret, const int64_t* return_rows, int32_t cu_split, void* stream) {
+  return run_overlapped(h, false, x, off, src, slot, w1, w3, w2, ret, return_rows, cu_split, stream);
+}
+
+int moe_stage_run_serial(moe_stage_t h, const void* x, const int32_t* off, const int32_t* src,
+                         const int32_t* slot, const void* w1, const void* w3, const void* w2,
+                         void* const* ret, const int64_t* return_rows, void* stream) {
+  return run_serial(h, false, x, off, src, slot, w1, w3, w2, ret, return_rows, stream);
+}
+
+int moe_stage_run_devplan(moe_stage_t h, const void* x, const int32_t* off, const int32_t* src,
+                          const int32_t* slot, const void* w1, const void* w3, const void* w2,
+                          void* const* ret, const int64_t* return_rows, int32_t cu_split,
+                          void* stream) {
+  return run_overlapped(h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, cu_split, stream);
+}
+
+int moe_stage_run_serial_devplan(moe_stage_t h, const void* x, const int32_t* off,
+                                 const int32_t* src, const int32_t* slot, const void* w1,
+                                 const void* w3, const void* w2, void* const* ret,
+                                 const int64_t* return_rows, void* stream) {
+  return run_serial(h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, stream);
 }
 
 int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
@@ -678,7 +851,34 @@ int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
       HIP_TRY(h, hipMemcpy(&h->ctr->timeouts, zero, sizeof zero, hipMemcpyHostToDevice));
     }
   }
+  if (h->dev_hdr_pending) {  // a device-built plan: its counts and verdict are on the device
+    h->dev_hdr_pending = false;
+    PlanHeader hd{};
+    HIP_TRY(h, hipMemcpy(&hd, h->d_plan + h->last_lay.hdr, sizeof hd, hipMemcpyDeviceToHost));
+    moe_stage_stats_t& st = h->last;
+    st.n_valid = hd.n_valid;
+    st.n_logical_rows = hd.n_lrows;
+    st.n_band_padding = hd.n_band_pad;
+    st.n_remote_rows = hd.n_remote;
+    st.n_tile_rows = hd.n_tile_rows;
+    st.n_groups = hd.n_groups;
+    st.n_gu_items = hd.n_gu;
+    st.n_down_items = hd.n_down;
+    st.n_segments = hd.n_segs;
+    st.split_k = hd.tail_split;
+    st.split_rows = hd.n_split_rows;
+    h->dev_status = hd.status;
+    h->dev_bad_row = hd.bad_row;
+  }
   *out = h->last;
+  if (h->dev_status) {
+    const int code = h->dev_status;
+    h->dev_status = 0;
+    std::string what = code == MOE_ECAPACITY ? "rows > max_rows, or the plan exceeds the handle's workspaces"
+                                             : "invalid routing";
+    if (h->dev_bad_row != INT32_MAX && code == MOE_EROUTING) what += " at row " + std::to_string(h->dev_bad_row);
+    return set_err(h, code, "device plan: " + what + "; the run did no work");
+  }
   if (h->last.timeout) {
     h->last.timeout = 0;
     return set_err(h, MOE_ETIMEOUT,
@@ -715,6 +915,68 @@ int moe_stage_times(moe_stage_t h, int32_t reset, moe_stage_times_t* out) {
   return MOE_OK;
 }
 
+// The last run's plan as the kernels saw it, read back from the device blob.
+static int read_header(moe_stage_t h, PlanHeader* hd) {
+  if (!h->ran) return set_err(h, MOE_EINVAL, "no run yet");
+  HIP_TRY(h, hipEventSynchronize(h->ev_done));
+  HIP_TRY(h, hipMemcpy(hd, h->d_plan + h->last_lay.hdr, sizeof *hd, hipMemcpyDeviceToHost));
+  return MOE_OK;
+}
+
+int moe_stage_plan_info(moe_stage_t h, moe_plan_info_t* o) {
+  if (!h || !o) return MOE_EINVAL;
+  PlanHeader hd{};
+  int rc = read_header(h, &hd);
+  if (rc) return rc;
+  *o = moe_plan_info_t{};
+  o->n_tile_rows = hd.n_tile_rows;
+  o->n_items = hd.n_gu + hd.n_down;
+  o->n_gu_items = hd.n_gu;
+  o->n_down_items = hd.n_down;
+  o->n_segments = hd.n_segs;
+  o->n_groups = hd.n_groups;
+  o->gu_tiles_per_row = (h->cfg.ffn + kGuTileF - 1) / kGuTileF;
+  o->down_tiles_per_row = h->down_per_row;
+  o->tile_m = kTileM;
+  o->band_rows = h->last_overlapped ? h->cfg.band_rows : 1;
+  o->split_k = hd.tail_split;
+  o->split_rows = hd.n_split_rows;
+  o->n_logical_rows = hd.n_lrows;
+  o->n_valid = hd.n_valid;
+  o->n_band_padding = hd.n_band_pad;
+  o->n_remote_rows = hd.n_remote;
+  return MOE_OK;
+}
+
+int64_t moe_stage_plan_copy(moe_stage_t h, int32_t which, void* dst, int64_t bytes) {
+  if (!h) return MOE_EINVAL;
+  PlanHeader hd{};
+  int rc = read_header(h, &hd);
+  if (rc) return rc;
+  const BlobLayout& L = h->last_lay;
+  size_t off = 0;
+  int64_t need = 0;
+  switch (which) {
+    case MOE_PLAN_TILE_ROWS: off = L.tile_rows; need = (int64_t)sizeof(TileRow) * hd.n_tile_rows; break;
+    case MOE_PLAN_ITEMS: off = L.items; need = 4 * ((int64_t)hd.n_gu + hd.n_down); break;
+    case MOE_PLAN_ROW_X: off = L.row_x; need = 4 * hd.n_lrows; break;
+    case MOE_PLAN_ROW_RANK: off = L.row_rank; need = 4 * hd.n_lrows; break;
+    case MOE_PLAN_ROW_SLOT: off = L.row_slot; need = 4 * hd.n_lrows; break;
+    case MOE_PLAN_SEGMENTS: off = L.segs; need = (int64_t)sizeof(Segment) * hd.n_segs; break;
+    case MOE_PLAN_GROUPS: off = L.groups; need = (int64_t)sizeof(Group) * hd.n_groups; break;
+    case MOE_PLAN_QUEUES: off = L.queues; need = 4 * 2 * (kXcds + 1); break;
+    default: return set_err(h, MOE_EINVAL, "unknown plan table");
+  }
+  if (!dst) return need;
+  if (bytes < need) return set_err(h, MOE_EINVAL, "destination too small");
+  if (need) HIP_TRY(h, hipMemcpy(dst, h->d_plan + off, (size_t)need, hipMemcpyDeviceToHost));
+  if (which == MOE_PLAN_QUEUES) {  // the blob's down queues index the whole item table
+    int32_t* q = (int32_t*)dst;
+    for (int x = 0; x <= kXcds; ++x) q[kXcds + 1 + x] -= hd.n_gu;
+  }
+  return MOE_OK;
+}
+
 const char* moe_stage_last_error(moe_stage_t h) { return h ? h->err.c_str() : g_create_error.c_str(); }
 
 int moe_stage_destroy(moe_stage_t h) {
@@ -736,7 +998,7 @@ int moe_stage_destroy(moe_stage_t h) {
     if (h->cfg.flags & MOE_SHARED_CUS) shared_prod = q.prod;
   }
   for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->ctr, (void*)h->d_plan,
-                  (void*)h->partials, (void*)h->arrivals})
+                  (void*)h->partials, (void*)h->arrivals, h->dev_ws})
     if (p) (void)hipFree(p);
   for (uint8_t* p : h->h_stage)
     if (p) (void)hipHostFree(p);

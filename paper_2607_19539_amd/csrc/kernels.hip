@@ -19,6 +19,7 @@
 // the token tile is the B operand, so every lane ends up holding 4
 // consecutive output features of one token row and stores 8 bytes at a time.
 #include <hip/hip_runtime.h>
+#include <limits.h>
 #include <stdint.h>
 
 #include <type_traits>
@@ -576,15 +577,15 @@ __device__ __forceinline__ uint32_t xcc_id() {
 }
 
 // Claims the next item of this launch: from queue q (initially the workgroup's own XCD's),
-// moving on to the next queue whenever one is empty.  Returns a.n_items once all are empty.
-__device__ __forceinline__ uint32_t claim_item(const ProducerArgs& a, uint32_t& q) {
+// moving on to the next queue whenever one is empty.  Returns `end` once all are empty.
+__device__ __forceinline__ uint32_t claim_item(const ProducerArgs& a, uint32_t& q, uint32_t end) {
   for (int tries = 0; tries < kXcds; ++tries) {
     const uint32_t i = atomicAdd(&a.claim[q], 1u);
     const int32_t q0 = a.queue[q], q1 = a.queue[q + 1];
     if (i < (uint32_t)(q1 - q0)) return (uint32_t)q0 + i;
     q = (q + 1) & (kXcds - 1);
   }
-  return (uint32_t)a.n_items;
+  return end;
 }
 
 // Persistent producer: every workgroup claims items from this launch's queues until they are
@@ -596,17 +597,18 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
   uint32_t* words = (uint32_t*)(lds + kSharedWords);  // [0] next item, [1] split-K verdict
   const int tid = threadIdx.x;
   uint32_t q = xcc_id();  // meaningful in thread 0, which does the claiming
+  const uint32_t end = (uint32_t)a.queue[kXcds];
   if (tid == 0) {
-    words[0] = claim_item(a, q);
-    if (words[0] < (uint32_t)a.n_items) atomicAdd(a.active, 1u);
+    words[0] = claim_item(a, q, end);
+    if (words[0] < end) atomicAdd(a.active, 1u);
   }
   __syncthreads();
   uint32_t cur = __builtin_amdgcn_readfirstlane(words[0]);  // uniform: item fields stay scalar
-  while (cur < (uint32_t)a.n_items) {
+  while (cur < end) {
     __syncthreads();  // every wave has read the word before the operand ring overwrites it
     // Claim the next item now; thread 0 holds its index while this one runs and passes it
     // on through LDS once the operand ring is no longer in use.
-    const uint32_t next = tid == 0 ? claim_item(a, q) : 0u;
+    const uint32_t next = tid == 0 ? claim_item(a, q, end) : 0u;
     const uint32_t item = a.items[cur];
     if constexpr (kSplit < 0) {
       // Split per tile row: whole tiles take the plain epilogue, split rows the part path.
@@ -634,6 +636,7 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_kernel(ConsumerArgs a) {
   const int lane = threadIdx.x & 63;
+  const int32_t n_segs = *a.n_segs;
   uint64_t polls = 0, waited = 0;
   for (;;) {
     uint32_t unit = 0;
@@ -641,7 +644,7 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
     unit = __builtin_amdgcn_readfirstlane(unit);  // every lane is active here
     const int32_t s = (int32_t)(unit / kCopyParts);
     const int32_t part = (int32_t)(unit % kCopyParts);
-    if (s >= a.n_segs) break;
+    if (s >= n_segs) break;
     const Segment sg = a.segs[s];
     const uint64_t t0 = ticks();
     bool expired = false;
@@ -710,7 +713,8 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
   const int64_t per_row = a.H / 8;
-  for (int64_t r = blockIdx.x; r < a.n_lrows; r += gridDim.x) {
+  const int64_t n_lrows = *a.n_lrows;
+  for (int64_t r = blockIdx.x; r < n_lrows; r += gridDim.x) {
     const int rank = a.row_rank[r];
     if (rank < 0) continue;
     const u32x4* src = (const u32x4*)(a.y + r * a.H);
@@ -732,7 +736,14 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
     a.ctr->down_active = 0;
     a.ctr->poll_iters = 0;
     a.ctr->wait_ticks = 0;
+    if (a.plan_hdr) {
+      a.plan_hdr->status = 0;
+      a.plan_hdr->bad_row = INT_MAX;
+      a.plan_hdr->ticket = 0;
+    }
   }
+  if (a.fill_ones)
+    for (int64_t j = i; j < a.n_fill_ones; j += stride) a.fill_ones[j] = ~0u;
   for (int64_t j = i; j < a.n_arrivals; j += stride) a.arrivals[j] = 0;
   if (a.publish)
     for (int64_t j = i; j < a.n_publish; j += stride) a.publish[j] = a.epoch;
@@ -744,7 +755,7 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
 
 hipError_t launch_init(const InitArgs& a, hipStream_t s) {
   int grid = 64;
-  if (a.poison) grid = 1024;
+  if (a.poison || a.n_fill_ones > (1 << 18)) grid = 1024;
   hipLaunchKernelGGL(init_kernel, dim3(grid), dim3(256), 0, s, a);
   return hipGetLastError();
 }

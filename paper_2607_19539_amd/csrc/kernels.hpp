@@ -21,9 +21,9 @@ struct ProducerArgs {
   int64_t hws_rows;        // rows per K block of the workspace (the handle's row capacity)
   uint16_t* y;             // [n_lrows, H] staged output (workspace)
   const TileRow* tile_rows;
-  const uint32_t* items;   // this launch's work items (all gate/up or all down tiles)
-  int32_t n_items;
-  const int32_t* queue;    // [kXcds + 1]: XCD x's queue is items [queue[x], queue[x+1])
+  const uint32_t* items;   // every work item of the run (gate/up tiles, then down items)
+  const int32_t* queue;    // [kXcds + 1] of this launch: XCD x's queue is items
+                           // [queue[x], queue[x+1]); queue[kXcds] ends the launch's items
   uint32_t* claim;         // [kXcds] queue heads of this launch
   uint32_t* active;        // count of workgroups that claimed work in this launch
   const int32_t* row_x;    // [n_lrows]
@@ -43,7 +43,7 @@ struct ConsumerArgs {
   const uint16_t* y;
   uint16_t* const* ret;
   const Segment* segs;
-  int32_t n_segs;
+  const int32_t* n_segs;   // device: segments of the plan
   const uint32_t* flags;
   uint32_t epoch;
   int32_t H;
@@ -56,7 +56,7 @@ struct ScatterArgs {
   uint16_t* const* ret;
   const int32_t* row_rank;
   const int32_t* row_slot;
-  int64_t n_lrows;
+  const int64_t* n_lrows;  // device: logical rows of the plan
   int32_t H;
 };
 
@@ -69,6 +69,9 @@ struct InitArgs {
   uint32_t* publish;       // optional: ready flags to set to `epoch` (consumer-only measurement)
   int32_t n_publish;
   uint32_t epoch;
+  uint32_t* fill_ones;     // optional: words to set to all-ones bits (device planner scratch)
+  int64_t n_fill_ones;
+  PlanHeader* plan_hdr;    // optional: header the device planner fills; reset to no error
 };
 
 struct CombineArgs {

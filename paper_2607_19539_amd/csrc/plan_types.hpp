@@ -71,6 +71,27 @@ constexpr int kXcds = 8;
 // Items per chunk when a launch's item sequence is dealt round-robin to the XCD queues.
 constexpr int kQueueChunk = 32;
 
+// Counts of a plan in device memory, written by whichever side built it (the host uploads
+// it with the tables; the device planner writes it itself).  The kernels take their item,
+// segment and row counts from here, so a plan built on the device needs no host round trip.
+struct PlanHeader {
+  int32_t status;        // 0, or the MOE_E* code the device planner found (then the plan is empty)
+  int32_t bad_row;       // first routing row that failed validation (INT32_MAX if none)
+  int32_t n_tile_rows;
+  int32_t n_groups;      // owner groups reported (overlapped plans only)
+  int32_t n_gu;          // gate/up items
+  int32_t n_down;        // down items
+  int32_t n_segs;        // transfer segments
+  int32_t tail_split;    // K parts of each split down tile
+  int32_t n_split_rows;
+  int32_t n_partials;
+  int32_t down_qmax;     // longest down queue (device planner)
+  uint32_t ticket;       // device planner: workgroups of the fill kernel that finished
+  int32_t n_groups_all;  // device planner: owner groups of the layout, any plan kind
+  int32_t reserved;
+  int64_t n_valid, n_lrows, n_band_pad, n_remote;
+};
+
 // Device-side counters of one run; the queue heads are zeroed by the init kernel.
 struct RunCounters {
   uint32_t gu_next[kXcds];    // gate/up work queue heads, one per XCD
