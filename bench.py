@@ -137,6 +137,10 @@ class Bench:
         self.bufs = [torch.zeros((int(n), wl.H), dtype=torch.int16, device="cuda") for n in wl.return_rows]
         self.run_args = (self.x, wl.expert_offsets, wl.row_src_rank, wl.row_slot, self.w1, self.w3, self.w2,
                          self.bufs, wl.return_rows)
+        # The same routing resident on the device, for the device-planned runs.
+        d_routing = [torch.from_numpy(np.ascontiguousarray(a, np.int32)).cuda()
+                     for a in (wl.expert_offsets, wl.row_src_rank, wl.row_slot)]
+        self.dev_run_args = (self.x, *d_routing, self.w1, self.w3, self.w2, self.bufs, wl.return_rows)
         self.base_flags = B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING
         extra = {"shared": B.MOE_SHARED_CUS, "partitioned": 0, "direct": B.MOE_DIRECT_ALL}
         self.stages = {m: self.make_stage(f, args.mgb) for m, f in extra.items()}
@@ -164,13 +168,16 @@ class Bench:
             s.close()
         self.torch.cuda.synchronize()
 
-    def timed(self, mode, path, cu_split, steps, warmup):
-        """W untimed steps, then exactly `steps` timed steps bracketed by device synchronisation."""
+    def timed(self, mode, path, cu_split, steps, warmup, device_plan=False):
+        """W untimed steps, then exactly `steps` timed steps bracketed by device synchronisation.
+        device_plan: the routing is on the device and the plan is built there."""
         torch, stg = self.torch, self.stages[mode]
         if path == "serial":
-            fn = lambda: stg.run_serial(*self.run_args, stream=self.stream)
+            fn = ((lambda: stg.run_serial_devplan(*self.dev_run_args, stream=self.stream)) if device_plan else
+                  (lambda: stg.run_serial(*self.run_args, stream=self.stream)))
         else:
-            fn = lambda: stg.run(*self.run_args, cu_split=cu_split, stream=self.stream)
+            fn = ((lambda: stg.run_devplan(*self.dev_run_args, cu_split=cu_split, stream=self.stream))
+                  if device_plan else (lambda: stg.run(*self.run_args, cu_split=cu_split, stream=self.stream)))
         for _ in range(warmup):
             fn()
         stg.query(check=False)
@@ -200,7 +207,7 @@ class Bench:
         runs = max(tm["runs"], 1)
         return {"ms": ms, "stats": st, "producer_ms": tm["producer_ms"] / runs,
                 "gate_up_ms": tm["gate_up_ms"] / runs, "consumer_ms": tm["consumer_ms"] / runs,
-                "scatter_ms": tm["scatter_ms"] / runs,
+                "scatter_ms": tm["scatter_ms"] / runs, "plan_ms": tm["plan_ms"] / runs,
                 "p10_ms": float(np.percentile(per_step, 10)), "p50_ms": float(np.median(per_step)),
                 "p90_ms": float(np.percentile(per_step, 90))}
 
@@ -374,6 +381,13 @@ def main():
                 f"{ovl['producer_ms'] * 1e3:.1f}, gate/up {ovl['gate_up_ms'] * 1e3:.1f}, consumer "
                 f"{ovl['consumer_ms'] * 1e3:.1f}); segments {st['n_segments']}, workgroups "
                 f"{st['gu_workgroups']}/{st['down_workgroups']}")
+        dplan = None
+        if only == "all" and ovl is not None:
+            # The same overlapped stage with the plan built on the GPU from device-resident routing.
+            dplan = bench.timed(args.mode, "overlapped", args.cu_split, steps, warmup, device_plan=True)
+            log(f"{name} overlapped, device-built plan: {dplan['ms'] * 1e3:.1f} us (planner on the GPU "
+                f"{dplan['plan_ms'] * 1e3:.1f} us; host-built plan: {ovl['stats']['plan_us']:.1f} us on the host, "
+                f"upload {ovl['plan_ms'] * 1e3:.1f} us on the GPU)")
         direct = None
         if only == "all":
             # Ablation: no consumer at all, the down epilogue writes every row to its slot.
@@ -409,6 +423,11 @@ def main():
         log(f"{name} combine ({wl.T_r} tokens, k={wl.k}): {comb['us']:.1f} us, {comb['GBps']:.0f} GB/s")
         if direct is not None:
             per_wl[name]["epilogue_direct_ablation_us"] = direct["ms"] * 1e3
+        if dplan is not None:
+            per_wl[name]["device_plan"] = {
+                "stage_us": dplan["ms"] * 1e3, "planner_gpu_us": dplan["plan_ms"] * 1e3,
+                "host_plan_host_us": ovl["stats"]["plan_us"], "host_plan_upload_gpu_us": ovl["plan_ms"] * 1e3,
+                "host_planned_stage_us": ovl["ms"] * 1e3}
         timeouts += bench.timeouts
         if headline:
             main_r = ovl if ovl is not None else ser

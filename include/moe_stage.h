@@ -73,6 +73,9 @@ extern "C" {
                                        consumer copies the staged output (whatever it holds) at
                                        the rate its cu_split compute units allow.  The receive
                                        buffers then hold no results                            */
+#define MOE_TEST_PLAN_NO_LDS (1u << 7) /* testing aid: the device planner keeps every table in
+                                       device memory even where it fits in LDS, so the path taken
+                                       by very large configurations is exercised on small ones */
 #define MOE_SHARED_CUS (1u << 4)   /* overlapped run: the producer keeps every compute unit and
                                       the consumer, still confined to its cu_split units, runs
                                       beside producer workgroups there (a consumer workgroup's
@@ -157,6 +160,8 @@ typedef struct {
   double gate_up_ms;   /* gate/up launch                                                 */
   double consumer_ms;  /* consumer kernel (overlapped runs)                              */
   double scatter_ms;   /* scatter kernel (serial runs)                                   */
+  double plan_ms;      /* stage start until the plan is on the device and the counters are
+                          reset: the upload of a host-built plan, or the device planner    */
 } moe_stage_times_t;
 
 /* Creates a handle and its device workspaces on the current HIP device. */

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(PKG, "_lib", "libmoe_stage.so")
 
 MOE_OK, MOE_EINVAL, MOE_EROUTING, MOE_ECAPACITY, MOE_EHIP, MOE_ETIMEOUT, MOE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 (MOE_LOCAL_DIRECT, MOE_KERNEL_TIMING, MOE_POISON, MOE_TEST_NO_SIGNAL, MOE_SHARED_CUS, MOE_DIRECT_ALL,
- MOE_TEST_CONSUMER_ONLY) = 1, 2, 4, 8, 16, 32, 64
+ MOE_TEST_CONSUMER_ONLY, MOE_TEST_PLAN_NO_LDS) = 1, 2, 4, 8, 16, 32, 64, 128
 (MOE_PLAN_TILE_ROWS, MOE_PLAN_ITEMS, MOE_PLAN_ROW_X, MOE_PLAN_ROW_RANK, MOE_PLAN_ROW_SLOT, MOE_PLAN_SEGMENTS,
  MOE_PLAN_GROUPS, MOE_PLAN_QUEUES) = range(8)
 ERROR_NAMES = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EROUTING", -3: "MOE_ECAPACITY", -4: "MOE_EHIP",
@@ -52,7 +52,8 @@ class moe_stage_stats_t(ctypes.Structure):
 
 class moe_stage_times_t(ctypes.Structure):
     _fields_ = [("runs", ctypes.c_int32), ("stage_ms", ctypes.c_double), ("producer_ms", ctypes.c_double),
-                ("gate_up_ms", ctypes.c_double), ("consumer_ms", ctypes.c_double), ("scatter_ms", ctypes.c_double)]
+                ("gate_up_ms", ctypes.c_double), ("consumer_ms", ctypes.c_double), ("scatter_ms", ctypes.c_double),
+                ("plan_ms", ctypes.c_double)]
 
 
 class moe_plan_info_t(ctypes.Structure):

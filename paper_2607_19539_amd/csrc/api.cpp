@@ -49,8 +49,9 @@ struct AutoSplit {
 };
 
 struct TimingRec {
-  hipEvent_t ev[7];  // 0 stage start, 1 producer start, 2 producer end, 3 consumer start,
-                     // 4 consumer end / scatter start, 5 stage end / scatter end, 6 gate/up end
+  hipEvent_t ev[8];  // 0 stage start, 1 producer start, 2 producer end, 3 consumer start,
+                     // 4 consumer end / scatter start, 5 stage end / scatter end, 6 gate/up end,
+                     // 7 plan ready (upload or device planner, and the counter reset, done)
   int kind = -1;     // 0 overlapped, 1 serial
 };
 
@@ -103,6 +104,7 @@ struct moe_stage_s {
   BlobLayout cap_lay{};   // the blob at the handle's capacity (device-built plans)
   BlobLayout last_lay{};  // the blob of the last run
   void* dev_ws = nullptr; // device planner scratch
+  int64_t max_items = 0;
   DevPlanWs ws{};
   bool last_dev = false;         // the last run's plan was built on the device
   bool last_overlapped = false;
@@ -177,7 +179,7 @@ int check_config(const moe_stage_config_t* c) {
     return MOE_EINVAL;
   constexpr uint32_t kKnownFlags = MOE_LOCAL_DIRECT | MOE_KERNEL_TIMING | MOE_POISON |
                                    MOE_TEST_NO_SIGNAL | MOE_SHARED_CUS | MOE_DIRECT_ALL |
-                                   MOE_TEST_CONSUMER_ONLY;
+                                   MOE_TEST_CONSUMER_ONLY | MOE_TEST_PLAN_NO_LDS;
   if (c->flags & ~kKnownFlags) return MOE_EINVAL;
   if (c->band_rows < 0 || c->band_rows > 256 || (c->band_rows & (c->band_rows - 1)) != 0)
     return MOE_EINVAL;
@@ -373,6 +375,7 @@ int prepare_device(moe_stage_s* h, bool overlapped, const void* x, const int32_t
   a.nk = c.ffn / kTileK;
   a.overlapped = overlapped ? 1 : 0;
   a.local_direct = (c.flags & MOE_LOCAL_DIRECT) ? 1 : 0;
+  a.no_lds = (c.flags & MOE_TEST_PLAN_NO_LDS) ? 1 : 0;
   a.max_rows = c.max_rows;
   a.max_tile_rows = h->max_tile_rows;
   a.hdr = (PlanHeader*)(h->d_plan + lay->hdr);
@@ -385,7 +388,7 @@ int prepare_device(moe_stage_s* h, bool overlapped, const void* x, const int32_t
   a.segs = (Segment*)(h->d_plan + lay->segs);
   a.groups = (Group*)(h->d_plan + lay->groups);
   a.ws = h->ws;
-  HIP_TRY(h, launch_devplan(a, h->num_cus, stream));
+  HIP_TRY(h, launch_devplan(a, h->max_items, h->num_cus, stream));
   h->last.plan_us =
       std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
   h->last_lay = *lay;
@@ -587,6 +590,7 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   // round of parts for the split tail rows (default).
   const int64_t max_items = (int64_t)h->max_tile_rows * (gu_per_row + (int64_t)h->down_per_row * std::max(S, 1)) +
                             (S == 0 ? kRoundTiles : 0);
+  h->max_items = max_items;
   // Segments: at most one per routed row.  Groups: one per (local expert, source rank).
   h->cap_lay = blob_layout(h->max_tile_rows, max_items, h->max_lrows, h->max_lrows,
                            (int64_t)cfg->num_local_experts * cfg->num_ranks, cfg->num_ranks);
@@ -690,6 +694,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
     if (tr) h->ring_next = (h->ring_next + kTimingRing - 1) % kTimingRing, --h->ring_count;
     return rc;
   }
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[7], stream));
   h->last.producer_grid = pgrid;
   h->last.consumer_grid = cgrid;
   h->last.consumer_cus = c_eff;
@@ -771,6 +776,7 @@ static int run_serial(moe_stage_t h, bool dev, const void* x, const int32_t* off
     if (tr) h->ring_next = (h->ring_next + kTimingRing - 1) % kTimingRing, --h->ring_count;
     return rc;
   }
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[7], stream));
   h->last.producer_grid = pgrid;
   h->last.consumer_grid = 0;
   h->last.auto_cu_split = -1;
@@ -902,6 +908,8 @@ int moe_stage_times(moe_stage_t h, int32_t reset, moe_stage_times_t* out) {
     out->producer_ms += ms;
     HIP_TRY(h, hipEventElapsedTime(&ms, r.ev[1], r.ev[6]));
     out->gate_up_ms += ms;
+    HIP_TRY(h, hipEventElapsedTime(&ms, r.ev[0], r.ev[7]));
+    out->plan_ms += ms;
     if (r.kind == 0) {
       HIP_TRY(h, hipEventElapsedTime(&ms, r.ev[3], r.ev[4]));
       out->consumer_ms += ms;

@@ -739,7 +739,6 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
     if (a.plan_hdr) {
       a.plan_hdr->status = 0;
       a.plan_hdr->bad_row = INT_MAX;
-      a.plan_hdr->ticket = 0;
     }
   }
   if (a.fill_ones)

@@ -2,7 +2,7 @@
 //
 // The host builder (plan.cpp) walks the routing serially.  Here the same plan -- layout,
 // schedule, work queues and combine plan (paper Section 3.2, Algorithm 1; segment
-// composition of Section 3.3.2) -- comes from five kernels in stream order:
+// composition of Section 3.3.2) -- comes from four kernels in stream order:
 //
 //   rows    grid over dispatched rows: validates the routing and records, per (expert, source
 //           rank), the run of rows it occupies (a histogram by run bounds: the dispatch order
@@ -13,17 +13,21 @@
 //           remote-first schedule (experts by remote band count, descending), the tail split,
 //           each schedule position's row group and the per-XCD queue bounds -- all closed forms
 //           of the host's greedy walks.
-//   fill    grid: every work item straight to its queue slot; the row tables; per logical row,
-//           whether a transfer segment starts or ends there; segment starts counted per tile
-//           row, and the last workgroup to finish scans the counts.
-//   segs    grid: each segment's fields from its first and last rows.
-//   sort    one workgroup: rows, flags and ready position of every segment, then a stable
-//           counting sort by ready position (the order the consumer claims them in).
+//   fill    grid: every work item straight to its queue slot; the row tables; per tile row, the
+//           logical rows where transfer segments start and end, compacted into short lists.
+//   segs    one workgroup: prefix sums of the per-tile-row counts pair the k-th start with the
+//           k-th end; each segment's fields and ready position; then a stable counting sort by
+//           ready position (the order the consumer claims them in).
 //
-// Every step reproduces the host's tables exactly for routing in dispatch order.
+// Every step reproduces the host's tables exactly for routing in dispatch order.  The
+// single-workgroup kernels keep their tables in LDS when they fit, and need only workgroup
+// barriers between phases: every wave of a workgroup shares one compute unit, whose vector
+// cache is coherent for it, so no device-scope fence (an L2 write-back on this chip) is paid.
 #include <hip/hip_runtime.h>
 #include <limits.h>
 #include <stdint.h>
+
+#include <algorithm>
 
 #include "../../include/moe_stage.h"
 #include "plan_device.hpp"
@@ -37,35 +41,51 @@ static_assert(kBlk == kTileM, "the fill and segment kernels give each tile row o
 
 __device__ __forceinline__ int32_t round_up_i(int32_t v, int32_t m) { return (v + m - 1) / m * m; }
 
-// Global writes of this workgroup are complete and visible to every wave of it after this
-// (device-scope fence, so L1 lines read earlier are dropped), then a barrier.
-__device__ __forceinline__ void wg_sync() {
-  __threadfence();
+// Inclusive prefix sum of x over a workgroup of kThreads threads: a shuffle scan within each
+// 64-lane wave, then one over the wave totals.  `sh` holds kThreads / 64 ints of LDS; *total
+// gets the workgroup's sum.  Every thread must call it.
+template <int kThreads>
+__device__ __forceinline__ int32_t wg_incl_scan(int32_t x, int32_t* sh, int32_t* total) {
+  constexpr int kWaves = kThreads / 64;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  for (int d = 1; d < 64; d <<= 1) {
+    const int32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) sh[wv] = x;
   __syncthreads();
+  if (wv == 0) {
+    int32_t t = lane < kWaves ? sh[lane] : 0;
+    for (int d = 1; d < kWaves; d <<= 1) {
+      const int32_t y = __shfl_up(t, d, 64);
+      if (lane >= d) t += y;
+    }
+    if (lane < kWaves) sh[lane] = t;
+  }
+  __syncthreads();
+  const int32_t r = x + (wv ? sh[wv - 1] : 0);
+  *total = sh[kWaves - 1];
+  __syncthreads();  // sh may be reused at once
+  return r;
 }
 
-// Exclusive prefix sum of v[0, n) in place by one workgroup of kThreads threads (global memory,
-// LDS scratch `sh` of kThreads ints); returns the total, the same in every thread.
-template <int kThreads>
+// Exclusive prefix sum of v[0, n) in place by one workgroup of kThreads threads (v in LDS or
+// global memory); returns the total, the same in every thread.
+// kAtomicIn: v was last written by atomics; read it with device-coherent loads.
+template <int kThreads, bool kAtomicIn = false>
 __device__ int32_t wg_scan(int32_t* v, int32_t n, int32_t* sh) {
   const int tid = threadIdx.x;
   int32_t carry = 0;
   for (int32_t c0 = 0; c0 < n; c0 += kThreads) {
     const int32_t i = c0 + tid;
-    const int32_t x = i < n ? v[i] : 0;
-    sh[tid] = x;
-    __syncthreads();
-    for (int d = 1; d < kThreads; d <<= 1) {
-      const int32_t y = tid >= d ? sh[tid - d] : 0;
-      __syncthreads();
-      sh[tid] += y;
-      __syncthreads();
-    }
-    if (i < n) v[i] = carry + sh[tid] - x;
-    carry += sh[kThreads - 1];
-    __syncthreads();
+    int32_t x = 0;
+    if (i < n) x = kAtomicIn ? __hip_atomic_load(&v[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : v[i];
+    int32_t tot;
+    const int32_t incl = wg_incl_scan<kThreads>(x, sh, &tot);
+    if (i < n) v[i] = carry + incl - x;
+    carry += tot;
   }
-  wg_sync();
+  __syncthreads();
   return carry;
 }
 
@@ -118,17 +138,32 @@ __device__ void write_empty(const DevPlanArgs& a) {
 // ---------------------------------------------------------------------------------------------
 // rows: validation and the per-(expert, rank) runs.
 // ---------------------------------------------------------------------------------------------
+constexpr int kLdsOffsets = 4096;  // expert offsets staged in LDS up to this many experts
+constexpr int kLdsRanks = 1024;    // receive-buffer sizes staged in LDS up to this many ranks
+
 __global__ __launch_bounds__(kBlk) void plan_rows_kernel(DevPlanArgs a) {
-  const int32_t rows = a.off[a.E_l];
+  __shared__ int32_t off_lds[kLdsOffsets + 1];
+  __shared__ int64_t rr_lds[kLdsRanks];
+  const bool in_lds = !a.no_lds && a.E_l <= kLdsOffsets;
+  const bool rr_in_lds = !a.no_lds && a.R <= kLdsRanks;
+  const int32_t* off = in_lds ? off_lds : a.off;
+  const int64_t* rrows = rr_in_lds ? rr_lds : a.return_rows;
   int bad_off = 0;
-  for (int e = threadIdx.x; e < a.E_l; e += kBlk) bad_off |= a.off[e] > a.off[e + 1];
+  for (int e = threadIdx.x; e <= a.E_l; e += kBlk) {
+    const int32_t v = a.off[e];
+    if (in_lds) off_lds[e] = v;
+    if (e < a.E_l) bad_off |= v > a.off[e + 1];
+  }
+  if (rr_in_lds)
+    for (int r = threadIdx.x; r < a.R; r += kBlk) rr_lds[r] = a.return_rows[r];
   bad_off = __syncthreads_or(bad_off);
+  const int32_t rows = off[a.E_l];
   int32_t code = 0;
   if (rows < 0)
     code = MOE_EROUTING;
   else if (rows > a.max_rows)
     code = MOE_ECAPACITY;
-  else if (a.off[0] != 0 || bad_off)
+  else if (off[0] != 0 || bad_off)
     code = MOE_EROUTING;
   if (code) {
     if (blockIdx.x == 0 && threadIdx.x == 0) a.hdr->status = code;
@@ -136,14 +171,16 @@ __global__ __launch_bounds__(kBlk) void plan_rows_kernel(DevPlanArgs a) {
   }
   const int32_t R = a.R;
   for (int32_t i = blockIdx.x * kBlk + threadIdx.x; i < rows; i += gridDim.x * kBlk) {
-    const int32_t e = range_of(a.off, a.E_l, i);
-    const int32_t lo = a.off[e], hi = a.off[e + 1];
-    const int32_t r = a.src[i], s = a.slot[i];
-    bool bad = r < 0 || r >= R || s < 0 || (int64_t)s >= a.return_rows[r];
+    // Neighbours are loaded with the row itself (clamped indices), so one round trip serves all.
+    const int32_t ip = i > 0 ? i - 1 : i, in = i + 1 < rows ? i + 1 : i;
+    const int32_t r = a.src[i], s = a.slot[i], r_prev = a.src[ip], r_next = a.src[in], s_prev = a.slot[ip];
+    const int32_t e = range_of(off, a.E_l, i);
+    const int32_t lo = off[e], hi = off[e + 1];
+    bool bad = r < 0 || r >= R || s < 0 || (int64_t)s >= rrows[r];
     if (!bad) {
-      const bool first = i == lo || a.src[i - 1] != r;
-      const bool last = i == hi - 1 || a.src[i + 1] != r;
-      if (!first && a.slot[i - 1] >= s) bad = true;  // slots ascend within a rank's run
+      const bool first = i == lo || r_prev != r;
+      const bool last = i == hi - 1 || r_next != r;
+      if (!first && s_prev >= s) bad = true;  // slots ascend within a rank's run
       if (first && atomicCAS(&a.ws.run_lo[e * R + r], -1, i) != -1) bad = true;  // a second run
       if (last) a.ws.run_hi[e * R + r] = i + 1;
       if (seen_insert(a.ws.seen, a.ws.seen_cap, ((uint64_t)r << 32) | (uint32_t)s)) bad = true;
@@ -158,8 +195,13 @@ __global__ __launch_bounds__(kBlk) void plan_rows_kernel(DevPlanArgs a) {
 // ---------------------------------------------------------------------------------------------
 // layout: one workgroup.
 // ---------------------------------------------------------------------------------------------
+constexpr int kLdsExperts = 1024;  // per-expert tables in LDS up to this many experts
+constexpr int kLdsGroups = 2048;   // group table in LDS up to this many (expert, rank) pairs
+
 __global__ __launch_bounds__(kWg) void plan_layout_kernel(DevPlanArgs a) {
   __shared__ int32_t sh[kWg];
+  __shared__ int32_t ex_lds[7 * kLdsExperts];
+  __shared__ int32_t g_lds[3 * kLdsGroups];
   __shared__ unsigned long long s_pad, s_remote;
   PlanHeader* H = a.hdr;
   const int tid = threadIdx.x;
@@ -168,10 +210,24 @@ __global__ __launch_bounds__(kWg) void plan_layout_kernel(DevPlanArgs a) {
     return;
   }
   if (tid == 0) s_pad = s_remote = 0;
-  __syncthreads();
   const int32_t E_l = a.E_l, R = a.R, self = a.self;
   const int32_t tb = a.overlapped ? a.tb : 1;
   const DevPlanWs& w = a.ws;
+  // Per-expert and group tables: LDS when they fit, else the global scratch (generic pointers,
+  // so the code is the same either way).
+  const bool ex_in_lds = !a.no_lds && E_l <= kLdsExperts;
+  int32_t* ex_ntr = ex_in_lds ? ex_lds : w.ex_ntr;
+  int32_t* ex_ng = ex_in_lds ? ex_lds + kLdsExperts : w.ex_ng;
+  int32_t* ex_hr = ex_in_lds ? ex_lds + 2 * kLdsExperts : w.ex_hr;
+  int32_t* ex_bands = ex_in_lds ? ex_lds + 3 * kLdsExperts : w.ex_bands;
+  int32_t* ex_roff = ex_in_lds ? ex_lds + 4 * kLdsExperts : w.ex_roff;
+  int32_t* ex_loff = ex_in_lds ? ex_lds + 5 * kLdsExperts : w.ex_loff;
+  int32_t* tmp = ex_in_lds ? ex_lds + 6 * kLdsExperts : w.tmp;
+  const bool g_in_lds = !a.no_lds && (int64_t)E_l * R <= kLdsGroups;
+  int32_t* gl_lrow0 = g_in_lds ? g_lds : w.g_lrow0;
+  int32_t* gl_rows = g_in_lds ? g_lds + kLdsGroups : w.g_rows;
+  int32_t* gl_dst = g_in_lds ? g_lds + 2 * kLdsGroups : w.g_dst;
+  __syncthreads();
 
   // Per expert: its owner groups in rank order, band padding after each remote group (only
   // in the overlapped layout), its extent in tile rows, and its schedule key.
@@ -196,18 +252,18 @@ __global__ __launch_bounds__(kWg) void plan_layout_kernel(DevPlanArgs a) {
         }
       }
     }
-    w.ex_ntr[e] = round_up_i(pos, kTileM) / kTileM;
+    ex_ntr[e] = round_up_i(pos, kTileM) / kTileM;
     // Remote rows precede local ones, and padding never fills a whole tile row, so the tile
     // rows holding remote rows are the expert's first ones, through the last remote row's.
-    w.ex_hr[e] = remote_end > 0 ? (remote_end - 1) / kTileM + 1 : 0;
-    w.ex_bands[e] = bands;
-    w.ex_ng[e] = ng;
+    ex_hr[e] = remote_end > 0 ? (remote_end - 1) / kTileM + 1 : 0;
+    ex_bands[e] = bands;
+    ex_ng[e] = ng;
     if (pad_e) atomicAdd(&s_pad, (unsigned long long)pad_e);
     if (remote_e) atomicAdd(&s_remote, (unsigned long long)remote_e);
   }
-  wg_sync();
-  const int32_t n_tr = wg_scan<kWg>(w.ex_ntr, E_l, sh);   // ex_ntr: first tile row of each expert
-  const int32_t n_grp = wg_scan<kWg>(w.ex_ng, E_l, sh);   // ex_ng: first group of each expert
+  __syncthreads();
+  const int32_t n_tr = wg_scan<kWg>(ex_ntr, E_l, sh);   // ex_ntr: first tile row of each expert
+  const int32_t n_grp = wg_scan<kWg>(ex_ng, E_l, sh);   // ex_ng: first group of each expert
   if (n_tr > a.max_tile_rows || n_tr >= kMaxTileRows) {
     if (tid == 0) H->status = MOE_ECAPACITY;
     write_empty(a);
@@ -218,29 +274,28 @@ __global__ __launch_bounds__(kWg) void plan_layout_kernel(DevPlanArgs a) {
   // id, each contributing its remote tile rows; then every expert's local-only tile rows in
   // expert order.  tmp[rank] takes each expert's remote tile-row count for the prefix sum.
   for (int32_t e = tid; e < E_l; e += kWg) {
-    const int32_t b = w.ex_bands[e];
+    const int32_t b = ex_bands[e];
     int32_t rank = 0;
     for (int32_t f = 0; f < E_l; ++f) {
-      const int32_t c = w.ex_bands[f];
+      const int32_t c = ex_bands[f];
       rank += (c > b) || (c == b && f < e);
     }
-    w.tmp[rank] = w.ex_hr[e];
-    w.ex_roff[e] = rank;
+    tmp[rank] = ex_hr[e];
+    ex_roff[e] = rank;
+    const int32_t ntr_e = (e + 1 < E_l ? ex_ntr[e + 1] : n_tr) - ex_ntr[e];
+    ex_loff[e] = ntr_e - ex_hr[e];
   }
-  wg_sync();
-  const int32_t n_hr = wg_scan<kWg>(w.tmp, E_l, sh);
-  for (int32_t e = tid; e < E_l; e += kWg) {
-    w.ex_roff[e] = w.tmp[w.ex_roff[e]];
-    const int32_t ntr_e = (e + 1 < E_l ? w.ex_ntr[e + 1] : n_tr) - w.ex_ntr[e];
-    w.ex_loff[e] = ntr_e - w.ex_hr[e];
-  }
-  wg_sync();
-  wg_scan<kWg>(w.ex_loff, E_l, sh);  // + n_hr: first local-only position of each expert
+  __syncthreads();
+  const int32_t n_hr = wg_scan<kWg>(tmp, E_l, sh);
+  wg_scan<kWg>(ex_loff, E_l, sh);  // + n_hr: first local-only position of each expert
+  for (int32_t e = tid; e < E_l; e += kWg) ex_roff[e] = tmp[ex_roff[e]];
 
-  // Owner groups with their places in the padded layout.
+  // Owner groups with their places in the padded layout (the fill kernel reads the global
+  // copies of the group table and of each expert's first group).
   for (int32_t e = tid; e < E_l; e += kWg) {
-    const int32_t base = w.ex_ntr[e] * kTileM;
-    int32_t g = w.ex_ng[e], pos = base;
+    const int32_t base = ex_ntr[e] * kTileM;
+    int32_t g = ex_ng[e], pos = base;
+    if (ex_in_lds) w.ex_ng[e] = g;
     for (int32_t j = 0; j < R; ++j) {
       const int32_t r = rank_at(j, R, self);
       const int32_t lo = w.run_lo[e * R + r];
@@ -250,44 +305,16 @@ __global__ __launch_bounds__(kWg) void plan_layout_kernel(DevPlanArgs a) {
       w.g_rows[g] = n;
       w.g_dst[g] = r;
       w.g_src0[g] = lo;
+      if (g_in_lds) {
+        gl_lrow0[g] = pos;
+        gl_rows[g] = n;
+        gl_dst[g] = r;
+      }
       if (a.overlapped) a.groups[g] = Group{e, pos, n, r};
       ++g;
       pos += n;
       if (a.overlapped && r != self) pos = base + round_up_i(pos - base, tb);
     }
-  }
-  wg_sync();
-
-  // Tile rows and the schedule.  ga_gu/gb_gu first hold each position's class run: the
-  // expert's remote or local-only tile rows, consecutive in the schedule.
-  for (int32_t t = tid; t < n_tr; t += kWg) {
-    const int32_t e = range_of(w.ex_ntr, E_l, t);
-    const int32_t j = t - w.ex_ntr[e], hr = w.ex_hr[e];
-    const int32_t ntr_e = (e + 1 < E_l ? w.ex_ntr[e + 1] : n_tr) - w.ex_ntr[e];
-    const int32_t t0 = t * kTileM;
-    int32_t nvalid = 0, has_remote = 0;
-    const int32_t g1 = e + 1 < E_l ? w.ex_ng[e + 1] : n_grp;
-    for (int32_t g = w.ex_ng[e]; g < g1; ++g) {
-      const int32_t lo = max(t0, w.g_lrow0[g]), hi = min(t0 + kTileM, w.g_lrow0[g] + w.g_rows[g]);
-      if (hi > lo) {
-        nvalid += hi - lo;
-        if (w.g_dst[g] != self) has_remote = 1;
-      }
-    }
-    int32_t cs, ce, q;
-    if (j < hr) {
-      cs = w.ex_roff[e];
-      ce = cs + hr;
-      q = cs + j;
-    } else {
-      cs = n_hr + w.ex_loff[e];
-      ce = cs + (ntr_e - hr);
-      q = cs + (j - hr);
-    }
-    w.order[q] = t;
-    w.ga_gu[q] = cs;
-    w.gb_gu[q] = ce;
-    a.tile_rows[t] = TileRow{e, t0, nvalid, has_remote, 1, -1};
   }
 
   // K parts of the down tiles: an explicit split_k splits every tile row; by default the tile
@@ -311,17 +338,43 @@ __global__ __launch_bounds__(kWg) void plan_layout_kernel(DevPlanArgs a) {
     }
   }
   const int32_t n_whole = n_tr - n_split;
-  wg_sync();
+  __syncthreads();
 
-  // Row groups (the host's greedy walk in closed form): within a class run [cs, ce), clipped
-  // to the range [a0, a1) being grouped, groups of g positions start at max(cs, a0).
+  // Tile rows, their schedule positions and row groups.  A position's class run [cs, ce) is
+  // its expert's remote (or local-only) tile rows, consecutive in the schedule; the host's
+  // greedy grouping in closed form: within the run, clipped to the range [a0, a1) being
+  // grouped, groups of g positions start at max(cs, a0).
   const int32_t ggu = max(a.gu_group, 1), gdn = max(a.down_group, 1);
-  for (int32_t q = tid; q < n_tr; q += kWg) {
-    const int32_t cs = w.ga_gu[q], ce = w.gb_gu[q];
+  for (int32_t t = tid; t < n_tr; t += kWg) {
+    const int32_t e = range_of(ex_ntr, E_l, t);
+    const int32_t j = t - ex_ntr[e], hr = ex_hr[e];
+    const int32_t ntr_e = (e + 1 < E_l ? ex_ntr[e + 1] : n_tr) - ex_ntr[e];
+    const int32_t t0 = t * kTileM;
+    int32_t nvalid = 0, has_remote = 0;
+    const int32_t g1 = e + 1 < E_l ? ex_ng[e + 1] : n_grp;
+    for (int32_t g = ex_ng[e]; g < g1; ++g) {
+      const int32_t L0 = gl_lrow0[g];
+      const int32_t lo = max(t0, L0), hi = min(t0 + kTileM, L0 + gl_rows[g]);
+      if (hi > lo) {
+        nvalid += hi - lo;
+        if (gl_dst[g] != self) has_remote = 1;
+      }
+    }
+    int32_t cs, ce, q;
+    if (j < hr) {
+      cs = ex_roff[e];
+      ce = cs + hr;
+      q = cs + j;
+    } else {
+      cs = n_hr + ex_loff[e];
+      ce = cs + (ntr_e - hr);
+      q = cs + (j - hr);
+    }
+    w.order[q] = t;
     {
       const int32_t A = cs + (q - cs) / ggu * ggu;
       w.ga_gu[q] = A;
-      w.gb_gu[q] = min(A + ggu, min(ce, n_tr));
+      w.gb_gu[q] = min(A + ggu, ce);
     }
     {
       const int32_t a0 = q < n_whole ? 0 : n_whole, a1 = q < n_whole ? n_whole : n_tr;
@@ -330,13 +383,10 @@ __global__ __launch_bounds__(kWg) void plan_layout_kernel(DevPlanArgs a) {
       w.ga_dn[q] = A;
       w.gb_dn[q] = min(A + gdn, min(ce, a1));
     }
-    if (q >= n_whole) {
-      TileRow* tr = &a.tile_rows[w.order[q]];
-      tr->split = S;
-      tr->part_base = (q - n_whole) * dpr * S;
-    }
+    const bool split = q >= n_whole;
+    a.tile_rows[t] = TileRow{e, t0, nvalid, has_remote, split ? S : 1, split ? (q - n_whole) * dpr * S : -1};
+    for (int32_t n = 0; n < dpr; ++n) w.pos_of_down[t * dpr + n] = -1;
   }
-  for (int32_t i = tid; i < n_tr * dpr; i += kWg) w.pos_of_down[i] = -1;
 
   // Queue bounds: each launch's item sequence dealt round-robin to the XCD queues in chunks of
   // kQueueChunk items (queue x holds chunks x, x + kXcds, ...).  Absolute item indices.
@@ -378,8 +428,7 @@ __global__ __launch_bounds__(kWg) void plan_layout_kernel(DevPlanArgs a) {
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlk) void plan_fill_kernel(DevPlanArgs a) {
   __shared__ int32_t sh[kBlk];
-  __shared__ int s_last;
-  PlanHeader* H = a.hdr;
+  const PlanHeader* H = a.hdr;
   if (H->status != 0) return;
   const DevPlanWs& w = a.ws;
   const int32_t n_tr = H->n_tile_rows, n_gu = H->n_gu, n_down = H->n_down;
@@ -423,8 +472,9 @@ __global__ __launch_bounds__(kBlk) void plan_fill_kernel(DevPlanArgs a) {
   // tile-row boundaries into k pieces; its first and last pieces are one chunk each and the
   // middle ones coalesce mid_pieces at a time; a slot gap also starts a segment.
   const int32_t xm = max(a.mid_pieces, 1);
+  const int tid = threadIdx.x;
   for (int32_t t = blockIdx.x; t < n_tr; t += gridDim.x) {
-    const int32_t q = t * kTileM + threadIdx.x;
+    const int32_t q = t * kTileM + tid;
     const int32_t e = a.tile_rows[t].expert;
     const int32_t g1 = e + 1 < a.E_l ? w.ex_ng[e + 1] : n_grp;
     int32_t g = -1;
@@ -433,7 +483,7 @@ __global__ __launch_bounds__(kBlk) void plan_fill_kernel(DevPlanArgs a) {
         g = k;
         break;
       }
-    uint32_t flag = 0;
+    int32_t start = 0, end = 0, np = 1;
     if (g >= 0) {
       const int32_t L0 = w.g_lrow0[g], L1 = L0 + w.g_rows[g];
       const int32_t i = w.g_src0[g] + (q - L0);
@@ -444,104 +494,89 @@ __global__ __launch_bounds__(kBlk) void plan_fill_kernel(DevPlanArgs a) {
       if (a.overlapped && (r != a.self || !a.local_direct)) {
         const int32_t first_t = L0 / kTileM, k = (L1 - 1) / kTileM - first_t + 1, b = t - first_t;
         auto chunk_start = [&](int32_t pb) { return pb == 0 || k <= 2 || pb == k - 1 || (pb - 1) % xm == 0; };
-        const bool start = q == L0 || (q % kTileM == 0 && chunk_start(b)) || (int64_t)a.slot[i - 1] + 1 != sl;
-        const bool end = q == L1 - 1 || ((q + 1) % kTileM == 0 && chunk_start(b + 1)) ||
-                         (int64_t)a.slot[i + 1] != (int64_t)sl + 1;
-        int32_t np = 1;
+        start = q == L0 || (q % kTileM == 0 && chunk_start(b)) || (int64_t)a.slot[i - 1] + 1 != sl;
+        end = q == L1 - 1 || ((q + 1) % kTileM == 0 && chunk_start(b + 1)) ||
+              (int64_t)a.slot[i + 1] != (int64_t)sl + 1;
         if (k > 2 && b > 0 && b < k - 1) {
           const int32_t cb = 1 + (b - 1) / xm * xm;
           np = min(cb + xm, k - 1) - cb;
         }
-        flag = (start ? 1u : 0u) | (end ? 2u : 0u) | ((uint32_t)np << 8);
       }
     } else {
       a.row_x[q] = a.off[e];
       a.row_rank[q] = -1;
       a.row_slot[q] = -1;
     }
-    w.row_flag[q] = flag;
-    const int cnt = __syncthreads_count(flag & 1u);
-    if (threadIdx.x == 0) w.blk_cnt[t] = cnt;
-  }
-
-  // The last workgroup to finish turns the per-tile-row counts into segment offsets.
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = atomicAdd(&H->ticket, 1u) == gridDim.x - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  const int32_t total = wg_scan<kBlk>(w.blk_cnt, n_tr, sh);
-  if (threadIdx.x == 0) {
-    H->n_segs = total;
-    H->ticket = 0;
+    // Compact this tile row's segment starts and ends (counts packed in one scan).
+    const int32_t v = start | (end << 16);
+    int32_t tot;
+    const int32_t ex = wg_incl_scan<kBlk>(v, sh, &tot) - v;
+    if (start) {
+      w.start_q[t * kTileM + (ex & 0xFFFF)] = q;
+      w.start_np[t * kTileM + (ex & 0xFFFF)] = np;
+    }
+    if (end) w.end_q[t * kTileM + (ex >> 16)] = q + 1;
+    if (tid == 0) {
+      w.cnt_s[t] = tot & 0xFFFF;
+      w.cnt_e[t] = tot >> 16;
+    }
   }
 }
 
 // ---------------------------------------------------------------------------------------------
-// segs: each segment's first-row fields and its end, in layout order.
+// segs: one workgroup pairs starts with ends, finishes each segment, and orders them by ready
+// position, stably.
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlk) void plan_segs_kernel(DevPlanArgs a) {
-  __shared__ int32_t sh[kBlk];
-  const PlanHeader* H = a.hdr;
-  if (H->status != 0 || H->n_segs == 0) return;
-  const DevPlanWs& w = a.ws;
-  const int32_t n_tr = H->n_tile_rows;
-  const int tid = threadIdx.x;
-  for (int32_t t = blockIdx.x; t < n_tr; t += gridDim.x) {
-    const int32_t q = t * kTileM + tid;
-    const uint32_t f = w.row_flag[q];
-    const int32_t st = (int32_t)(f & 1u);
-    sh[tid] = st;
-    __syncthreads();
-    for (int d = 1; d < kBlk; d <<= 1) {
-      const int32_t y = tid >= d ? sh[tid - d] : 0;
-      __syncthreads();
-      sh[tid] += y;
-      __syncthreads();
-    }
-    const int32_t incl = w.blk_cnt[t] + sh[tid];  // segment starts up to and including q
-    if (st) {
-      Segment sg{};
-      sg.dst_rank = a.row_rank[q];
-      sg.y_row0 = q;
-      sg.slot0 = a.row_slot[q];
-      sg.npieces = (int32_t)(f >> 8);
-      w.seg_tmp[incl - 1] = sg;
-    }
-    if (f & 2u) w.seg_end[incl - 1] = q + 1;
-    __syncthreads();
-  }
-}
+constexpr int kLdsTileRows = 4096;  // per-tile-row counts in LDS up to this many tile rows
+constexpr int kLdsHist = 8192;      // ready-position histogram in LDS up to this many positions
 
-// ---------------------------------------------------------------------------------------------
-// sort: finish each segment, then order them by ready position, stably.
-// ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kWg) void plan_sort_kernel(DevPlanArgs a) {
+__global__ __launch_bounds__(kWg) void plan_segs_kernel(DevPlanArgs a) {
   __shared__ int32_t sh[kWg];
-  const PlanHeader* H = a.hdr;
-  if (H->status != 0 || H->n_segs == 0) return;
+  __shared__ int32_t cnt_lds[2 * kLdsTileRows];
+  __shared__ int32_t hist_lds[kLdsHist];
+  PlanHeader* H = a.hdr;
+  if (H->status != 0) return;
   const DevPlanWs& w = a.ws;
-  const int32_t n = H->n_segs, K = H->down_qmax, dpr = a.down_per_row;
+  const int32_t n_tr = H->n_tile_rows, K = H->down_qmax, dpr = a.down_per_row;
   const int tid = threadIdx.x;
-  for (int32_t i = tid; i < K; i += kWg) w.hist[i] = 0;
-  wg_sync();
-  for (int32_t i = tid; i < n; i += kWg) {
-    Segment sg = w.seg_tmp[i];
-    const int32_t end = w.seg_end[i];
-    sg.rows = end - sg.y_row0;
-    const int32_t t0 = sg.y_row0 / kTileM, t1 = (end - 1) / kTileM;
+  const bool c_in_lds = !a.no_lds && n_tr <= kLdsTileRows;
+  int32_t* cs = c_in_lds ? cnt_lds : w.cnt_s;
+  int32_t* ce = c_in_lds ? cnt_lds + kLdsTileRows : w.cnt_e;
+  if (c_in_lds)
+    for (int32_t t = tid; t < n_tr; t += kWg) {
+      cs[t] = w.cnt_s[t];
+      ce[t] = w.cnt_e[t];
+    }
+  __syncthreads();
+  const int32_t n = wg_scan<kWg>(cs, n_tr, sh);
+  wg_scan<kWg>(ce, n_tr, sh);  // the k-th end closes the k-th start's segment
+  if (tid == 0) H->n_segs = n;
+  if (n == 0) return;
+  int32_t* hist = !a.no_lds && K <= kLdsHist ? hist_lds : w.hist;
+  for (int32_t i = tid; i < K; i += kWg) hist[i] = 0;
+  __syncthreads();
+  for (int32_t k = tid; k < n; k += kWg) {
+    const int32_t ts = range_of(cs, n_tr, k), te = range_of(ce, n_tr, k);
+    const int32_t js = ts * kTileM + (k - cs[ts]);
+    const int32_t q0 = w.start_q[js], q1 = w.end_q[te * kTileM + (k - ce[te])];
+    Segment sg;
+    sg.dst_rank = a.row_rank[q0];
+    sg.rows = q1 - q0;
+    sg.y_row0 = q0;
+    sg.slot0 = a.row_slot[q0];
+    const int32_t t0 = q0 / kTileM, t1 = (q1 - 1) / kTileM;
     sg.flag_begin = t0 * dpr;
     sg.flag_count = (t1 - t0 + 1) * dpr;
     int32_t rp = 0;
     for (int32_t f = sg.flag_begin; f < sg.flag_begin + sg.flag_count; ++f) rp = max(rp, w.pos_of_down[f]);
     sg.ready_pos = rp;
-    w.seg_tmp[i] = sg;
-    w.seg_key[i] = rp;
-    atomicAdd(&w.hist[rp], 1);
+    sg.npieces = w.start_np[js];
+    w.seg_tmp[k] = sg;
+    w.seg_key[k] = rp;
+    atomicAdd(&hist[rp], 1);
   }
-  wg_sync();
-  wg_scan<kWg>(w.hist, K, sh);
+  __syncthreads();
+  wg_scan<kWg, true>(hist, K, sh);
   // Stable placement, kWg segments at a time: a segment goes after every earlier one with
   // the same ready position.
   for (int32_t c0 = 0; c0 < n; c0 += kWg) {
@@ -553,21 +588,21 @@ __global__ __launch_bounds__(kWg) void plan_sort_kernel(DevPlanArgs a) {
     if (i < n) {
       int32_t rank = 0;
       for (int j = 0; j < tid; ++j) rank += sh[j] == k;
-      dest = w.hist[k] + rank;
+      dest = __hip_atomic_load(&hist[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + rank;
     }
-    wg_sync();
+    __syncthreads();
     if (i < n) {
       a.segs[dest] = w.seg_tmp[i];
-      atomicAdd(&w.hist[k], 1);
+      atomicAdd(&hist[k], 1);
     }
-    wg_sync();
+    __syncthreads();
   }
 }
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t run_lo, run_hi, seen, ex, g, order, ga, pod, row_flag, blk, seg_end, seg_tmp, seg_key, hist, total;
+  size_t run_lo, run_hi, seen, ex, g, order, ga, pod, lists, cnt, seg_tmp, seg_key, hist, total;
   int64_t seen_cap;
 };
 
@@ -590,9 +625,8 @@ WsLayout ws_layout(int32_t E_l, int32_t R, int32_t max_rows, int32_t max_tile_ro
   L.order = o;    o = align256(o + 4 * (size_t)max_tile_rows);
   L.ga = o;       o = align256(o + 4 * 4 * (size_t)max_tile_rows);
   L.pod = o;      o = align256(o + 4 * (size_t)max_tile_rows * dpr);
-  L.row_flag = o; o = align256(o + 4 * (size_t)max_lrows);
-  L.blk = o;      o = align256(o + 4 * (size_t)max_tile_rows);
-  L.seg_end = o;  o = align256(o + 4 * (size_t)max_lrows);
+  L.lists = o;    o = align256(o + 4 * 3 * (size_t)max_lrows);
+  L.cnt = o;      o = align256(o + 4 * 2 * (size_t)max_tile_rows);
   L.seg_tmp = o;  o = align256(o + sizeof(Segment) * (size_t)max_lrows);
   L.seg_key = o;  o = align256(o + 4 * (size_t)max_lrows);
   L.hist = o;     o = align256(o + 4 * (size_t)(max_items + 1));
@@ -638,24 +672,28 @@ DevPlanWs devplan_ws_carve(void* base_, int32_t E_l, int32_t R, int32_t max_rows
   w.ga_dn = ga + 2 * (size_t)max_tile_rows;
   w.gb_dn = ga + 3 * (size_t)max_tile_rows;
   w.pos_of_down = (int32_t*)(b + L.pod);
-  w.row_flag = (uint32_t*)(b + L.row_flag);
-  w.blk_cnt = (int32_t*)(b + L.blk);
-  w.seg_end = (int32_t*)(b + L.seg_end);
+  int32_t* lists = (int32_t*)(b + L.lists);
+  w.start_q = lists;
+  w.start_np = lists + max_lrows;
+  w.end_q = lists + 2 * max_lrows;
+  w.cnt_s = (int32_t*)(b + L.cnt);
+  w.cnt_e = w.cnt_s + max_tile_rows;
   w.seg_tmp = (Segment*)(b + L.seg_tmp);
   w.seg_key = (int32_t*)(b + L.seg_key);
   w.hist = (int32_t*)(b + L.hist);
   return w;
 }
 
-hipError_t launch_devplan(const DevPlanArgs& a, int num_cus, hipStream_t s) {
-  const int wide = std::max(num_cus, 1) * 4;
+hipError_t launch_devplan(const DevPlanArgs& a, int64_t max_items, int num_cus, hipStream_t s) {
+  const int64_t wide = (int64_t)std::max(num_cus, 1) * 4;
   const int rows_grid = (int)std::max<int64_t>(1, std::min<int64_t>(wide, ((int64_t)a.max_rows + kBlk - 1) / kBlk));
-  const int tr_grid = std::max(1, std::min(wide, a.max_tile_rows));
+  // The fill kernel: a workgroup per tile row, and enough threads for the work items.
+  const int fill_grid = (int)std::max<int64_t>(
+      1, std::min<int64_t>(wide, std::max<int64_t>(a.max_tile_rows, (max_items + kBlk - 1) / kBlk)));
   hipLaunchKernelGGL(plan_rows_kernel, dim3(rows_grid), dim3(kBlk), 0, s, a);
   hipLaunchKernelGGL(plan_layout_kernel, dim3(1), dim3(kWg), 0, s, a);
-  hipLaunchKernelGGL(plan_fill_kernel, dim3(wide), dim3(kBlk), 0, s, a);
-  hipLaunchKernelGGL(plan_segs_kernel, dim3(tr_grid), dim3(kBlk), 0, s, a);
-  hipLaunchKernelGGL(plan_sort_kernel, dim3(1), dim3(kWg), 0, s, a);
+  hipLaunchKernelGGL(plan_fill_kernel, dim3(fill_grid), dim3(kBlk), 0, s, a);
+  if (a.overlapped) hipLaunchKernelGGL(plan_segs_kernel, dim3(1), dim3(kWg), 0, s, a);
   return hipGetLastError();
 }
 

@@ -41,9 +41,11 @@ struct DevPlanWs {
   int32_t* ga_dn;         //   down launch
   int32_t* gb_dn;
   int32_t* pos_of_down;   // [max_tile_rows * down_per_row] latest queue position of a tile's parts
-  uint32_t* row_flag;     // [max_lrows] bit 0 segment start, bit 1 segment end, bits 8.. pieces
-  int32_t* blk_cnt;       // [max_lrows / 256] segment starts per 256-row block
-  int32_t* seg_end;       // [max_lrows] one past each segment's last logical row
+  int32_t* start_q;       // [max_tile_rows][256] per tile row: logical rows where segments start,
+  int32_t* start_np;      //   the tile-row pieces each one's chunk covers,
+  int32_t* end_q;         //   and one past the rows where segments end
+  int32_t* cnt_s;         // [max_tile_rows] segment starts per tile row (then their prefix sums)
+  int32_t* cnt_e;         // [max_tile_rows] segment ends per tile row (then their prefix sums)
   Segment* seg_tmp;       // [max_lrows] segments in layout order
   int32_t* seg_key;       // [max_lrows] ready position of each
   int32_t* hist;          // [max_items + 1] ready-position counts, then offsets
@@ -57,6 +59,7 @@ struct DevPlanArgs {
   int32_t E_l, R, self, tb, mid_pieces, gu_group, down_group, split_k;
   int32_t gu_per_row, down_per_row, nk;
   int32_t overlapped, local_direct;
+  int32_t no_lds;         // keep every table in device memory (testing the large-size path)
   int32_t max_rows, max_tile_rows;
   PlanHeader* hdr;
   TileRow* tile_rows;
@@ -77,7 +80,7 @@ DevPlanWs devplan_ws_carve(void* base, int32_t E_l, int32_t R, int32_t max_rows,
                            int32_t down_per_row, int64_t max_lrows, int64_t max_items);
 
 // Enqueues the planner kernels on `s`.  The init kernel must already have filled the
-// all-ones range of the scratch and reset the header (status 0, bad_row INT32_MAX, ticket 0).
-hipError_t launch_devplan(const DevPlanArgs& a, int num_cus, hipStream_t s);
+// all-ones range of the scratch and reset the header (status 0, bad_row INT32_MAX).
+hipError_t launch_devplan(const DevPlanArgs& a, int64_t max_items, int num_cus, hipStream_t s);
 
 }  // namespace moe

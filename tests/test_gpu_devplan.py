@@ -22,6 +22,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 TABLES = ("tile_rows", "items", "row_x", "row_rank", "row_slot", "segments", "groups", "queues")
+NO_LDS = B.MOE_TEST_PLAN_NO_LDS
 
 
 def _bf16_rand(shape, seed, scale=0.05):
@@ -129,6 +130,8 @@ def test_workload_plans_match_host(name):
     c = Case.from_workload(make_workload(name, weights=None), seed=3)
     check_both_paths(c, overlapped=True, cu_split=32)
     check_both_paths(c, overlapped=False)
+    # the planner's device-memory path (taken by configurations too large for its LDS tables)
+    check_both_paths(c, overlapped=True, cu_split=32, flags=B.MOE_LOCAL_DIRECT | NO_LDS)
 
 
 RAGGED = dict(H=320, F=576, E_t=8, k=2, R=4, T_r=512, E_l=2)
@@ -137,6 +140,7 @@ RAGGED = dict(H=320, F=576, E_t=8, k=2, R=4, T_r=512, E_l=2)
 @pytest.mark.parametrize("band_rows,mgb,flags,split_k", [
     (0, 1, B.MOE_LOCAL_DIRECT, 0), (16, 3, B.MOE_LOCAL_DIRECT, 0), (256, 2, 0, 0), (1, 1, 0, 3),
     (64, 4, B.MOE_LOCAL_DIRECT, 1), (32, 1, B.MOE_LOCAL_DIRECT | B.MOE_SHARED_CUS, 2),
+    (0, 1, B.MOE_LOCAL_DIRECT | NO_LDS, 0), (16, 3, NO_LDS, 2),
 ])
 @pytest.mark.parametrize("owner", [0, 3])
 def test_config_matrix(band_rows, mgb, flags, split_k, owner):
@@ -221,7 +225,7 @@ def test_random_routings(seed):
     c, rng = random_case(seed)
     band = int(rng.choice([0, 1, 8, 64, 256]))
     mgb = int(rng.integers(1, 4))
-    flags = int(rng.choice([0, B.MOE_LOCAL_DIRECT]))
+    flags = int(rng.choice([0, B.MOE_LOCAL_DIRECT])) | (NO_LDS if seed % 2 else 0)
     split_k = int(rng.choice([0, 0, 1, 2]))
     max_rows = c.rows + int(rng.choice([0, 1, 1000]))
     log(f"devplan random seed={seed} E_l={c.E_l} R={c.R} rows={c.rows} tb={band} mgb={mgb} flags={flags} "
