@@ -144,23 +144,29 @@ class Bench:
         self.base_flags = B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING
         extra = {"shared": B.MOE_SHARED_CUS, "partitioned": 0, "direct": B.MOE_DIRECT_ALL}
         self.stages = {m: self.make_stage(f, args.mgb) for m, f in extra.items()}
+        # The same CU modes without per-kernel events: the events a timed handle records inside
+        # every run (eight on two queues) cost the overlapped stage ~1%, so the stage time is
+        # taken from these, and kernel durations from the timed handles.
+        for m in ("shared", "partitioned"):
+            self.stages[m + ":plain"] = self.make_stage(extra[m], args.mgb, timing=False)
         torch.cuda.synchronize()
         # The stage runs on a stream of its own, as in a serving loop (on the legacy null stream
         # the shared-CU producer would have to fork to a second queue; see moe_stage_run).
         self.stream = torch.cuda.Stream()
         self.timeouts = []
 
-    def make_stage(self, flags, mgb):
+    def make_stage(self, flags, mgb, timing=True):
         wl, args = self.wl, self.args
+        base = self.base_flags if timing else self.base_flags & ~self.B.MOE_KERNEL_TIMING
         return self.B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, mgb,
-                               self.base_flags | flags, 0, args.split_k)
+                               base | flags, 0, args.split_k)
 
     def stage(self, mode, mgb):
-        """Handle of a CU mode and mid-segment piece count (created on first use)."""
-        key = mode if mgb == self.args.mgb else f"{mode}:mgb{mgb}"
+        """Event-free handle of a CU mode and mid-segment piece count (created on first use)."""
+        key = f"{mode}:plain" if mgb == self.args.mgb else f"{mode}:mgb{mgb}:plain"
         if key not in self.stages:
             f = {"shared": self.B.MOE_SHARED_CUS, "partitioned": 0}[mode]
-            self.stages[key] = self.make_stage(f, mgb)
+            self.stages[key] = self.make_stage(f, mgb, timing=False)
         return key
 
     def close(self):
@@ -181,7 +187,8 @@ class Bench:
         for _ in range(warmup):
             fn()
         stg.query(check=False)
-        stg.times(reset=True)
+        if stg.cfg.flags & self.B.MOE_KERNEL_TIMING:
+            stg.times(reset=True)
         # A garbage-collection pass inside the timed loop stalls the host for tens of ms while
         # the GPU idles; collect before and keep the collector off while timing.
         gc.collect()
@@ -203,7 +210,8 @@ class Bench:
             msg = self.B.moe_stage_last_error(stg.h)
             log(f"ERROR: {msg} -- timing invalid")
             self.timeouts.append(msg)
-        tm = stg.times(reset=True)
+        tm = stg.times(reset=True) if stg.cfg.flags & self.B.MOE_KERNEL_TIMING else {
+            "runs": 0, "producer_ms": 0.0, "gate_up_ms": 0.0, "consumer_ms": 0.0, "scatter_ms": 0.0, "plan_ms": 0.0}
         runs = max(tm["runs"], 1)
         return {"ms": ms, "stats": st, "producer_ms": tm["producer_ms"] / runs,
                 "gate_up_ms": tm["gate_up_ms"] / runs, "consumer_ms": tm["consumer_ms"] / runs,
@@ -274,6 +282,15 @@ def down_kernel_name(split_k, st):
     return f"moe::producer_kernel<true, {split_k if split_k <= 4 else 0}> (down launch, {split_k} K parts)"
 
 
+def with_plain_times(timed_r, plain_r):
+    """Kernel durations and stats from the event-timed handle, stage times from the plain one."""
+    r = dict(timed_r)
+    r["ms_with_kernel_events"] = timed_r["ms"]
+    for k in ("ms", "p10_ms", "p50_ms", "p90_ms"):
+        r[k] = plain_r[k]
+    return r
+
+
 def summarize(wl, ser, ovl, sweep):
     """Per-workload figures: stage times, producer launches, throughput against the bf16 peak."""
     flops = wl.flops()
@@ -284,6 +301,7 @@ def summarize(wl, ser, ovl, sweep):
         gu = r["gate_up_ms"]
         dn = r["producer_ms"] - gu
         out[key] = {"stage_us": r["ms"] * 1e3, "tflops": flops / (r["ms"] * 1e-3) / 1e12,
+                    "stage_us_with_kernel_events": r.get("ms_with_kernel_events", r["ms"]) * 1e3,
                     "step_us_p10_p50_p90": [round(r["p10_ms"] * 1e3, 1), round(r["p50_ms"] * 1e3, 1),
                                             round(r["p90_ms"] * 1e3, 1)],
                     "producer_us": r["producer_ms"] * 1e3, "gate_up_us": gu * 1e3, "down_us": dn * 1e3,
@@ -370,12 +388,15 @@ def main():
                                                                     max(args.warmup // 2, 5))
         only = args.only if headline else "all"
         ser = ovl = None
+        ser_plain = ovl_plain = None
         if only in ("all", "serial"):
-            ser = bench.timed(args.mode, "serial", 0, steps, warmup)
+            ser_plain = bench.timed(args.mode + ":plain", "serial", 0, steps, warmup)
+            ser = with_plain_times(bench.timed(args.mode, "serial", 0, steps, warmup), ser_plain)
             log(f"{name} serial: {ser['ms'] * 1e3:.1f} us (producer {ser['producer_ms'] * 1e3:.1f}, gate/up "
                 f"{ser['gate_up_ms'] * 1e3:.1f}, scatter {ser['scatter_ms'] * 1e3:.1f})")
         if only in ("all", "overlapped"):
-            ovl = bench.timed(args.mode, "overlapped", args.cu_split, steps, warmup)
+            ovl_plain = bench.timed(args.mode + ":plain", "overlapped", args.cu_split, steps, warmup)
+            ovl = with_plain_times(bench.timed(args.mode, "overlapped", args.cu_split, steps, warmup), ovl_plain)
             st = ovl["stats"]
             log(f"{name} overlapped ({args.mode}, c={args.cu_split}): {ovl['ms'] * 1e3:.1f} us (producer "
                 f"{ovl['producer_ms'] * 1e3:.1f}, gate/up {ovl['gate_up_ms'] * 1e3:.1f}, consumer "
@@ -384,7 +405,10 @@ def main():
         dplan = None
         if only == "all" and ovl is not None:
             # The same overlapped stage with the plan built on the GPU from device-resident routing.
-            dplan = bench.timed(args.mode, "overlapped", args.cu_split, steps, warmup, device_plan=True)
+            dplan_plain = bench.timed(args.mode + ":plain", "overlapped", args.cu_split, steps, warmup,
+                                      device_plan=True)
+            dplan = with_plain_times(bench.timed(args.mode, "overlapped", args.cu_split, steps, warmup,
+                                                 device_plan=True), dplan_plain)
             log(f"{name} overlapped, device-built plan: {dplan['ms'] * 1e3:.1f} us (planner on the GPU "
                 f"{dplan['plan_ms'] * 1e3:.1f} us; host-built plan: {ovl['stats']['plan_us']:.1f} us on the host, "
                 f"upload {ovl['plan_ms'] * 1e3:.1f} us on the GPU)")

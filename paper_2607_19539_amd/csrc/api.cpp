@@ -115,14 +115,19 @@ struct moe_stage_s {
   int stage_idx = 0;
   uint32_t epoch = 0;
 
-  // CU-masked queues per consumer split, kept once made (switching splits then costs no queue
-  // teardown); s_cons / s_prod are the current split's pair.  With shared CUs the producer's
-  // queue covers every CU whatever the split, so all entries share one.
+  // CU-masked queues of the consumer split in use (and, while the adaptive selector measures,
+  // of each candidate, so a switch costs no queue teardown); s_cons / s_prod are the current
+  // split's pair.  Partitioned runs give each split a producer queue on the complementary
+  // mask; with shared CUs one every-CU producer queue serves every split, made only when a
+  // run needs it (a caller on the legacy null stream).  Every hardware queue a process keeps
+  // costs: past a few dozen the scheduler time-slices them and every kernel slows down, so a
+  // manual split keeps only its own pair.
   struct SplitQueues {
     int c;
-    hipStream_t cons, prod;
+    hipStream_t cons, prod;  // prod: partitioned runs only
   };
   std::vector<SplitQueues> queues;
+  hipStream_t shared_prod = nullptr;
   int cached_split = -1;
   hipStream_t s_cons = nullptr, s_prod = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join_c = nullptr, ev_join_p = nullptr, ev_done = nullptr;
@@ -503,50 +508,58 @@ int effective_split(const moe_stage_s* h, int c) {
   return std::min((c + n - 1) / n * n, h->num_cus - n);
 }
 
-int ensure_streams(moe_stage_s* h, int c) {
-  if (h->cached_split == c) return MOE_OK;
-  const bool shared = (h->cfg.flags & MOE_SHARED_CUS) != 0;
-  for (const auto& q : h->queues)
-    if (q.c == c) {
-      h->s_cons = q.cons;
-      h->s_prod = q.prod;
-      h->cached_split = c;
-      return MOE_OK;
-    }
-  std::vector<uint32_t> mc, mp;
-  make_masks(h->num_cus, h->n_xcd, c, shared, &mc, &mp);
-  moe_stage_s::SplitQueues q{c, nullptr, nullptr};
-  HIP_TRY(h, hipExtStreamCreateWithCUMask(&q.cons, (uint32_t)mc.size(), mc.data()));
-  if (shared && !h->queues.empty()) {
-    q.prod = h->queues.front().prod;
-  } else if (hipExtStreamCreateWithCUMask(&q.prod, (uint32_t)mp.size(), mp.data()) != hipSuccess) {
-    (void)hipStreamDestroy(q.cons);
-    return set_err(h, MOE_EHIP, "hipExtStreamCreateWithCUMask(producer)");
+void destroy_split(moe_stage_s::SplitQueues& q) {
+  (void)hipStreamSynchronize(q.cons);
+  (void)hipStreamDestroy(q.cons);
+  if (q.prod) {
+    (void)hipStreamSynchronize(q.prod);
+    (void)hipStreamDestroy(q.prod);
   }
-  h->queues.push_back(q);
-  h->s_cons = q.cons;
-  h->s_prod = q.prod;
-  h->cached_split = c;
-  return MOE_OK;
 }
 
-// Releases the queues of every split but the current one (once the adaptive selector has
-// settled, so idle queues do not stay with the device).
-void release_other_queues(moe_stage_s* h) {
-  std::vector<moe_stage_s::SplitQueues> keep;
-  for (const auto& q : h->queues) {
-    if (q.c == h->cached_split) {
-      keep.push_back(q);
-      continue;
-    }
-    (void)hipStreamSynchronize(q.cons);
-    (void)hipStreamDestroy(q.cons);
-    if (q.prod != h->s_prod) {
-      (void)hipStreamSynchronize(q.prod);
-      (void)hipStreamDestroy(q.prod);
-    }
+// Releases the queues of every split but `keep` (waiting for work still on them).
+void release_other_queues(moe_stage_s* h, int keep) {
+  std::vector<moe_stage_s::SplitQueues> kept;
+  for (auto& q : h->queues) {
+    if (q.c == keep)
+      kept.push_back(q);
+    else
+      destroy_split(q);
   }
-  h->queues.swap(keep);
+  h->queues.swap(kept);
+  if (h->cached_split != keep) h->cached_split = -1;
+}
+
+// Makes the consumer queue of split c (and its producer queue where the run needs one)
+// current.  keep_others: leave other splits' queues alive (the adaptive selector's candidates).
+int ensure_streams(moe_stage_s* h, int c, bool need_prod, bool keep_others) {
+  const bool shared = (h->cfg.flags & MOE_SHARED_CUS) != 0;
+  if (!keep_others && (h->queues.size() > 1 || (h->queues.size() == 1 && h->queues[0].c != c)))
+    release_other_queues(h, c);
+  moe_stage_s::SplitQueues* cur = nullptr;
+  for (auto& q : h->queues)
+    if (q.c == c) cur = &q;
+  if (!cur) {
+    std::vector<uint32_t> mc, mp;
+    make_masks(h->num_cus, h->n_xcd, c, shared, &mc, &mp);
+    moe_stage_s::SplitQueues q{c, nullptr, nullptr};
+    HIP_TRY(h, hipExtStreamCreateWithCUMask(&q.cons, (uint32_t)mc.size(), mc.data()));
+    if (!shared && hipExtStreamCreateWithCUMask(&q.prod, (uint32_t)mp.size(), mp.data()) != hipSuccess) {
+      (void)hipStreamDestroy(q.cons);
+      return set_err(h, MOE_EHIP, "hipExtStreamCreateWithCUMask(producer)");
+    }
+    h->queues.push_back(q);
+    cur = &h->queues.back();
+  }
+  if (shared && need_prod && !h->shared_prod) {
+    std::vector<uint32_t> mc, mp;
+    make_masks(h->num_cus, h->n_xcd, c, true, &mc, &mp);
+    HIP_TRY(h, hipExtStreamCreateWithCUMask(&h->shared_prod, (uint32_t)mp.size(), mp.data()));
+  }
+  h->s_cons = cur->cons;
+  h->s_prod = shared ? h->shared_prod : cur->prod;
+  h->cached_split = c;
+  return MOE_OK;
 }
 
 }  // namespace
@@ -681,9 +694,11 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   // Consumer workgroups per CU: two beside a producer workgroup (their registers fill what a
   // producer wave leaves free), six when the consumer owns its CUs.
   const int cgrid = c_eff * (shared ? 2 : 6);
-  int rc = ensure_streams(h, c_eff);
+  const bool legacy = stream == nullptr || stream == hipStreamLegacy;
+  const bool on_caller = shared && !legacy;
+  // The adaptive selector keeps its candidates' queues until it has settled.
+  int rc = ensure_streams(h, c_eff, !on_caller, autosplit && h->autos.chosen < 0);
   if (rc) return rc;
-  if (autosplit && h->autos.chosen >= 0 && h->queues.size() > 1) release_other_queues(h);
   BlobLayout lay{};
   TimingRec* tr = timing_slot(h);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[0], stream));
@@ -720,8 +735,6 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   // the legacy null stream, whose launches wait for all earlier work on blocking streams,
   // the still-polling consumer included: that would be a cycle, so the producer then forks
   // to the handle's own stream like the partitioned launch.
-  const bool legacy = stream == nullptr || stream == hipStreamLegacy;
-  const bool on_caller = shared && !legacy;
   hipStream_t ps = on_caller ? stream : h->s_prod;
   HIP_TRY(h, hipEventRecord(h->ev_fork, stream));
   HIP_TRY(h, hipStreamWaitEvent(h->s_cons, h->ev_fork, 0));
@@ -999,12 +1012,11 @@ int moe_stage_destroy(moe_stage_t h) {
   for (auto& pair : h->autos.ev)
     for (hipEvent_t ev : pair)
       if (ev) (void)hipEventDestroy(ev);
-  hipStream_t shared_prod = nullptr;
   for (const auto& q : h->queues) {
     (void)hipStreamDestroy(q.cons);
-    if (q.prod && q.prod != shared_prod) (void)hipStreamDestroy(q.prod);
-    if (h->cfg.flags & MOE_SHARED_CUS) shared_prod = q.prod;
+    if (q.prod) (void)hipStreamDestroy(q.prod);
   }
+  if (h->shared_prod) (void)hipStreamDestroy(h->shared_prod);
   for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->ctr, (void*)h->d_plan,
                   (void*)h->partials, (void*)h->arrivals, h->dev_ws})
     if (p) (void)hipFree(p);
