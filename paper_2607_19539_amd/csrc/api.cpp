@@ -435,6 +435,13 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
   return a;
 }
 
+TailArgs tail_args(moe_stage_s* h, const BlobLayout& lay, const ProducerArgs& down) {
+  TailArgs t{};
+  t.p = down;
+  t.n_tile_rows = &((const PlanHeader*)(h->d_plan + lay.hdr))->n_tile_rows;
+  return t;
+}
+
 TimingRec* timing_slot(moe_stage_s* h) {
   if (!(h->cfg.flags & MOE_KERNEL_TIMING)) return nullptr;
   TimingRec* r = &h->ring[h->ring_next];
@@ -715,6 +722,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   h->last.consumer_cus = c_eff;
   uint32_t mode = (h->cfg.flags & MOE_TEST_NO_SIGNAL) ? 0u : kModeSignal;
   if (h->cfg.flags & MOE_LOCAL_DIRECT) mode |= kModeLocalDirect;
+  if (h->cfg.down_split_k == 0) mode |= kModeDeferTail;
   const ProducerArgs pgu = producer_args(h, lay, x, w1, w3, w2, mode, false);
   const ProducerArgs pdn = producer_args(h, lay, x, w1, w3, w2, mode, true);
   ConsumerArgs ca{};
@@ -751,6 +759,8 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   if (producer && (!known || h->plan.n_gu > 0)) HIP_TRY(h, launch_producer(pgu, false, pgrid, ps));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], ps));
   if (producer && (!known || h->plan.n_down > 0)) HIP_TRY(h, launch_producer(pdn, true, pgrid, ps));
+  if (producer && (pdn.mode & kModeDeferTail) && (!known || h->plan.n_split_rows > 0))
+    HIP_TRY(h, launch_tail(tail_args(h, lay, pdn), h->num_cus, ps));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], ps));
   if (!on_caller) {
     HIP_TRY(h, hipEventRecord(h->ev_join_p, h->s_prod));
@@ -795,7 +805,7 @@ static int run_serial(moe_stage_t h, bool dev, const void* x, const int32_t* off
   h->last.auto_cu_split = -1;
   h->last.consumer_cus = 0;
   const bool direct_all = (h->cfg.flags & MOE_DIRECT_ALL) != 0;
-  const uint32_t mode = direct_all ? kModeDirectAll : 0u;
+  const uint32_t mode = (direct_all ? kModeDirectAll : 0u) | (h->cfg.down_split_k == 0 ? kModeDeferTail : 0u);
   const ProducerArgs pgu = producer_args(h, lay, x, w1, w3, w2, mode, false);
   const ProducerArgs pa = producer_args(h, lay, x, w1, w3, w2, mode, true);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], stream));
@@ -803,6 +813,8 @@ static int run_serial(moe_stage_t h, bool dev, const void* x, const int32_t* off
   if (!known || h->plan.n_gu > 0) HIP_TRY(h, launch_producer(pgu, false, pgrid, stream));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], stream));
   if (!known || h->plan.n_down > 0) HIP_TRY(h, launch_producer(pa, true, pgrid, stream));
+  if ((pa.mode & kModeDeferTail) && (!known || h->plan.n_split_rows > 0))
+    HIP_TRY(h, launch_tail(tail_args(h, lay, pa), h->num_cus, stream));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], stream));
   ScatterArgs sa{};
   sa.y = h->y;

@@ -417,6 +417,7 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
             store8_device(mine + (2 * b) * kProducerThreads, pack_f32x2(d[4 * q], d[4 * q + 1]));
             store8_device(mine + (2 * b + 1) * kProducerThreads, pack_f32x2(d[4 * q + 2], d[4 * q + 3]));
           }
+      if (kSplit == 0 && (a.mode & kModeDeferTail)) return;  // the tail kernel adds the parts
       wait_vm_and_barrier<0>();  // every wave's part stores have reached the coherence point
       if (tid == 0) {
         const uint32_t prev =
@@ -627,6 +628,81 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
 }
 
 // ---------------------------------------------------------------------------
+// Tail: the split tile rows of a kModeDeferTail down launch.  Their parts only stored fp32
+// partials; here kTailSlices workgroups per tile each add the parts of 4 of the 64 accumulator
+// blocks -- in part order, from part 0, exactly the sums the last-arriving part would form --
+// and store those outputs where the down epilogue would (Y at device scope, or the local
+// receive buffer).  The last slice of a tile to finish raises its flag.  Thread tid takes the
+// positions producer thread tid held, so its loads are the 8-byte words that thread stored.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kProducerThreads) void tail_kernel(TailArgs ta) {
+  const ProducerArgs& a = ta.p;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn = wave & 1, wm = wave >> 1, lr = lane & 31, lk = lane >> 5;
+  const int dpr = a.down_per_row;
+  const int64_t H = a.H;
+  const int64_t n_pairs = (int64_t)*ta.n_tile_rows * dpr * kTailSlices;
+  const bool direct = (a.mode & kModeLocalDirect) != 0;
+  const bool signal = (a.mode & kModeSignal) != 0;
+  const bool direct_all = (a.mode & kModeDirectAll) != 0;
+  constexpr int kPartU64 = kProducerThreads * 128;
+  constexpr int kBlocks = 64 / kTailSlices;
+  // The parts were stored by the previous launch, at the coherence point.
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  for (int64_t pr = blockIdx.x; pr < n_pairs; pr += gridDim.x) {
+    const int t = (int)(pr / (dpr * kTailSlices));
+    const int col = (int)(pr / kTailSlices % dpr), slice = (int)(pr % kTailSlices);
+    const TileRow tr = a.tile_rows[t];
+    if (tr.split <= 1) continue;  // a whole tile: finished by the down launch
+    const int S = tr.split;
+    const uint64_t* src = (const uint64_t*)a.partials + ((size_t)tr.part_base + (size_t)col * S) * kPartU64 + tid;
+#pragma unroll
+    for (int u = 0; u < kBlocks; ++u) {
+      const int b = slice * kBlocks + u;
+      const int i = b >> 4, j = (b >> 2) & 3, q = b & 3;
+      float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+#pragma unroll 4
+      for (int p = 0; p < S; ++p) {
+        const uint64_t lo = src[(size_t)p * kPartU64 + (2 * b) * kProducerThreads];
+        const uint64_t hi = src[(size_t)p * kPartU64 + (2 * b + 1) * kProducerThreads];
+        const float v0 = __uint_as_float((uint32_t)lo), v1 = __uint_as_float((uint32_t)(lo >> 32));
+        const float v2 = __uint_as_float((uint32_t)hi), v3 = __uint_as_float((uint32_t)(hi >> 32));
+        if (p == 0) {
+          s0 = v0, s1 = v1, s2 = v2, s3 = v3;
+        } else {
+          s0 += v0, s1 += v1, s2 += v2, s3 += v3;
+        }
+      }
+      const int m = wm * 128 + j * 32 + lr;
+      const int n = col * kDownTileN + wn * 128 + i * 32 + 8 * q + 4 * lk;
+      const int lrow = tr.lrow0 + m;
+      const int rank = a.row_rank[lrow];
+      if (rank >= 0 && n < H) {
+        const uint64_t v = (uint64_t)pack_bf16x2(s0, s1) | ((uint64_t)pack_bf16x2(s2, s3) << 32);
+        if (direct_all || (direct && rank == a.self_rank))
+          *(__attribute__((address_space(1))) uint64_t*)(a.ret[rank] + (int64_t)a.row_slot[lrow] * H + n) = v;
+        else if (signal)
+          store8_device(a.y + (int64_t)lrow * H + n, v);
+        else
+          *(__attribute__((address_space(1))) uint64_t*)(a.y + (int64_t)lrow * H + n) = v;
+      }
+    }
+    if (signal && (tr.has_remote || !direct)) {
+      // Every wave's stores have completed before the slice counts itself in; the slice that
+      // completes the tile raises the flag.
+      wait_vm_and_barrier<0>();
+      if (tid == 0) {
+        const int tile = t * dpr + col;
+        const uint32_t prev =
+            __hip_atomic_fetch_add(&a.arrivals[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (prev + 1 == (uint32_t)kTailSlices)
+          __hip_atomic_store(&a.flags[tile], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Consumer: every wave works alone.  It claims a copy unit -- a quarter of a segment, taken
 // in the segments' ready order, so the four quarters of a segment go to four waves at once
 // -- polls the segment's flags (one flag per lane; all must show the current epoch), then
@@ -780,6 +856,11 @@ hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream
 
 hipError_t launch_consumer(const ConsumerArgs& a, int grid, hipStream_t s) {
   hipLaunchKernelGGL(consumer_kernel, dim3(grid), dim3(kConsumerThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_tail(const TailArgs& a, int grid, hipStream_t s) {
+  hipLaunchKernelGGL(tail_kernel, dim3(grid), dim3(kProducerThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -11,6 +11,8 @@ namespace moe {
 constexpr uint32_t kModeSignal = 1u;       // raise a ready flag per down tile of a transfer tile row
 constexpr uint32_t kModeLocalDirect = 2u;  // local rows go straight to the local receive buffer
 constexpr uint32_t kModeDirectAll = 4u;    // every row goes straight to its receive buffer
+constexpr uint32_t kModeDeferTail = 8u;    // split tail tiles: parts only store their partials; the
+                                           // tail kernel after the launch adds them and writes the tiles
 
 struct ProducerArgs {
   const uint16_t* x;       // [rows, H] dispatched tokens
@@ -37,6 +39,14 @@ struct ProducerArgs {
   int32_t split_k;         // K parts of every down tile; 0 = per tile row (TileRow::split)
   float* partials;         // fp32 part tiles (256 threads x 256) from TileRow::part_base on
   uint32_t* arrivals;      // [tiles] parts finished this run (zeroed by the init kernel)
+};
+
+// The tail kernel: finishes the split down tiles after the down launch.  Reads the plan's tile
+// rows and its partials; writes the tiles' rows exactly as the down epilogue would and raises
+// their flags.
+struct TailArgs {
+  ProducerArgs p;             // the down launch's arguments (mode, outputs, flags, partials)
+  const int32_t* n_tile_rows; // device: tile rows of the plan
 };
 
 struct ConsumerArgs {
@@ -90,6 +100,8 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 // Gate/up tiles (down = false) or down-projection tiles with ready flags (down = true).
 hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream_t s);
 hipError_t launch_consumer(const ConsumerArgs& a, int grid, hipStream_t s);
+// Split tail tiles of a kModeDeferTail down launch: kTailSlices workgroups per tile.
+hipError_t launch_tail(const TailArgs& a, int grid, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s);
 // Resident producer workgroups per compute unit.
 int producer_blocks_per_cu();
@@ -97,6 +109,7 @@ constexpr int kProducerThreads = 256;
 constexpr int kConsumerThreads = 256;
 constexpr int kCopyUnroll = 4;  // 16-byte vectors per consumer lane and copy chunk
 constexpr int kCopyParts = 4;   // consumer copy units (one wave each) per segment
+constexpr int kTailSlices = 16; // workgroups sharing one split tile's reduction
 // Consumer waves per SIMD the register budget must allow: at most 512 / 8 = 64 VGPRs each, so
 // two consumer waves fit beside one producer wave of up to 384 of the 512 registers.
 constexpr int kConsumerMinWaves = 8;
