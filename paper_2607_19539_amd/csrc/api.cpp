@@ -60,7 +60,7 @@ size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 // Byte layout of the device plan blob.  The host builder packs it to the plan's own sizes;
 // the device builder writes into the layout of the handle's capacity.
 struct BlobLayout {
-  size_t hdr, tile_rows, items, queues, row_x, row_rank, row_slot, segs, groups, ret, total;
+  size_t hdr, tile_rows, items, queues, row_x, row_rank, row_slot, segs, groups, tail, ret, total;
 };
 
 BlobLayout blob_layout(int64_t n_tr, int64_t n_items, int64_t n_lrows, int64_t n_segs, int64_t n_groups,
@@ -76,6 +76,7 @@ BlobLayout blob_layout(int64_t n_tr, int64_t n_items, int64_t n_lrows, int64_t n
   b.row_slot = o;  o = align256(o + sizeof(int32_t) * (size_t)n_lrows);
   b.segs = o;      o = align256(o + sizeof(Segment) * (size_t)n_segs);
   b.groups = o;    o = align256(o + sizeof(Group) * (size_t)n_groups);
+  b.tail = o;      o = align256(o + sizeof(int32_t) * (size_t)kMaxTailRows);  // split tile rows (default split)
   b.ret = o;       o = align256(o + (sizeof(void*) + sizeof(int64_t)) * (size_t)R);  // pointers, then rows
   b.total = o;
   return b;
@@ -305,6 +306,11 @@ int prepare(moe_stage_s* h, bool overlapped, const void* x,
   memcpy(hs + lay->row_slot, P.row_slot.data(), sizeof(int32_t) * P.row_slot.size());
   memcpy(hs + lay->segs, P.segs.data(), sizeof(Segment) * P.segs.size());
   memcpy(hs + lay->groups, P.groups.data(), sizeof(Group) * P.groups.size());
+  if (c.down_split_k == 0) {  // the tail kernel's list of split tile rows, in schedule order
+    int32_t* tail = (int32_t*)(hs + lay->tail);
+    for (size_t t = 0; t < P.tile_rows.size(); ++t)
+      if (P.tile_rows[t].split > 1) tail[P.tile_rows[t].part_base / (P.down_per_row * P.tail_split)] = (int32_t)t;
+  }
   memcpy(hs + lay->ret, ret, sizeof(void*) * (size_t)c.num_ranks);
   memcpy(hs + lay->ret + sizeof(void*) * (size_t)c.num_ranks, return_rows, sizeof(int64_t) * (size_t)c.num_ranks);
 
@@ -392,6 +398,7 @@ int prepare_device(moe_stage_s* h, bool overlapped, const void* x, const int32_t
   a.row_slot = (int32_t*)(h->d_plan + lay->row_slot);
   a.segs = (Segment*)(h->d_plan + lay->segs);
   a.groups = (Group*)(h->d_plan + lay->groups);
+  a.tail_rows = (int32_t*)(h->d_plan + lay->tail);
   a.ws = h->ws;
   HIP_TRY(h, launch_devplan(a, h->max_items, h->num_cus, stream));
   h->last.plan_us =
@@ -438,7 +445,8 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
 TailArgs tail_args(moe_stage_s* h, const BlobLayout& lay, const ProducerArgs& down) {
   TailArgs t{};
   t.p = down;
-  t.n_tile_rows = &((const PlanHeader*)(h->d_plan + lay.hdr))->n_tile_rows;
+  t.tail_rows = (const int32_t*)(h->d_plan + lay.tail);
+  t.n_split_rows = &((const PlanHeader*)(h->d_plan + lay.hdr))->n_split_rows;
   return t;
 }
 
@@ -760,7 +768,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], ps));
   if (producer && (!known || h->plan.n_down > 0)) HIP_TRY(h, launch_producer(pdn, true, pgrid, ps));
   if (producer && (pdn.mode & kModeDeferTail) && (!known || h->plan.n_split_rows > 0))
-    HIP_TRY(h, launch_tail(tail_args(h, lay, pdn), h->num_cus, ps));
+    HIP_TRY(h, launch_tail(tail_args(h, lay, pdn), kTailGrid, ps));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], ps));
   if (!on_caller) {
     HIP_TRY(h, hipEventRecord(h->ev_join_p, h->s_prod));
@@ -814,7 +822,7 @@ static int run_serial(moe_stage_t h, bool dev, const void* x, const int32_t* off
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], stream));
   if (!known || h->plan.n_down > 0) HIP_TRY(h, launch_producer(pa, true, pgrid, stream));
   if ((pa.mode & kModeDeferTail) && (!known || h->plan.n_split_rows > 0))
-    HIP_TRY(h, launch_tail(tail_args(h, lay, pa), h->num_cus, stream));
+    HIP_TRY(h, launch_tail(tail_args(h, lay, pa), kTailGrid, stream));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], stream));
   ScatterArgs sa{};
   sa.y = h->y;

@@ -629,11 +629,12 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
 
 // ---------------------------------------------------------------------------
 // Tail: the split tile rows of a kModeDeferTail down launch.  Their parts only stored fp32
-// partials; here kTailSlices workgroups per tile each add the parts of 4 of the 64 accumulator
-// blocks -- in part order, from part 0, exactly the sums the last-arriving part would form --
-// and store those outputs where the down epilogue would (Y at device scope, or the local
-// receive buffer).  The last slice of a tile to finish raises its flag.  Thread tid takes the
-// positions producer thread tid held, so its loads are the 8-byte words that thread stored.
+// partials; here each workgroup pass takes one of a tile's 64 accumulator blocks, issues the
+// loads of all its parts at once, adds them in part order from part 0 -- exactly the sums the
+// last-arriving part would form -- and stores those outputs where the down epilogue would (Y
+// at device scope, or the local receive buffer).  The last of a tile's 64 passes raises its
+// flag.  Thread tid takes the positions producer thread tid held, so its loads are the 8-byte
+// words that thread stored.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kProducerThreads) void tail_kernel(TailArgs ta) {
   const ProducerArgs& a = ta.p;
@@ -641,61 +642,63 @@ __global__ __launch_bounds__(kProducerThreads) void tail_kernel(TailArgs ta) {
   const int wn = wave & 1, wm = wave >> 1, lr = lane & 31, lk = lane >> 5;
   const int dpr = a.down_per_row;
   const int64_t H = a.H;
-  const int64_t n_pairs = (int64_t)*ta.n_tile_rows * dpr * kTailSlices;
+  constexpr int kBlocks = 64;
+  const int64_t n_pass = (int64_t)*ta.n_split_rows * dpr * kBlocks;
   const bool direct = (a.mode & kModeLocalDirect) != 0;
   const bool signal = (a.mode & kModeSignal) != 0;
   const bool direct_all = (a.mode & kModeDirectAll) != 0;
   constexpr int kPartU64 = kProducerThreads * 128;
-  constexpr int kBlocks = 64 / kTailSlices;
-  // The parts were stored by the previous launch, at the coherence point.
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  for (int64_t pr = blockIdx.x; pr < n_pairs; pr += gridDim.x) {
-    const int t = (int)(pr / (dpr * kTailSlices));
-    const int col = (int)(pr / kTailSlices % dpr), slice = (int)(pr % kTailSlices);
+  // The parts were stored by the previous launch at the coherence point; the launch's own
+  // acquire makes them visible, so no fence (an L2 invalidate per workgroup) is needed here.
+  for (int64_t pr = blockIdx.x; pr < n_pass; pr += gridDim.x) {
+    const int t = ta.tail_rows[pr / (dpr * kBlocks)];
+    const int col = (int)(pr / kBlocks % dpr), b = (int)(pr % kBlocks);
     const TileRow tr = a.tile_rows[t];
-    if (tr.split <= 1) continue;  // a whole tile: finished by the down launch
     const int S = tr.split;
-    const uint64_t* src = (const uint64_t*)a.partials + ((size_t)tr.part_base + (size_t)col * S) * kPartU64 + tid;
+    const uint64_t* src = (const uint64_t*)a.partials + ((size_t)tr.part_base + (size_t)col * S) * kPartU64 +
+                          (2 * b) * kProducerThreads + tid;
+    // Every part's two words in flight together (a part past the count re-reads the last one
+    // and is not added).
+    uint64_t lo[kMaxSplitK], hi[kMaxSplitK];
 #pragma unroll
-    for (int u = 0; u < kBlocks; ++u) {
-      const int b = slice * kBlocks + u;
-      const int i = b >> 4, j = (b >> 2) & 3, q = b & 3;
-      float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-#pragma unroll 4
-      for (int p = 0; p < S; ++p) {
-        const uint64_t lo = src[(size_t)p * kPartU64 + (2 * b) * kProducerThreads];
-        const uint64_t hi = src[(size_t)p * kPartU64 + (2 * b + 1) * kProducerThreads];
-        const float v0 = __uint_as_float((uint32_t)lo), v1 = __uint_as_float((uint32_t)(lo >> 32));
-        const float v2 = __uint_as_float((uint32_t)hi), v3 = __uint_as_float((uint32_t)(hi >> 32));
-        if (p == 0) {
-          s0 = v0, s1 = v1, s2 = v2, s3 = v3;
-        } else {
-          s0 += v0, s1 += v1, s2 += v2, s3 += v3;
-        }
+    for (int p = 0; p < kMaxSplitK; ++p) {
+      const size_t o = (size_t)min(p, S - 1) * kPartU64;
+      lo[p] = src[o];
+      hi[p] = src[o + kProducerThreads];
+    }
+    float s0 = __uint_as_float((uint32_t)lo[0]), s1 = __uint_as_float((uint32_t)(lo[0] >> 32));
+    float s2 = __uint_as_float((uint32_t)hi[0]), s3 = __uint_as_float((uint32_t)(hi[0] >> 32));
+#pragma unroll
+    for (int p = 1; p < kMaxSplitK; ++p)
+      if (p < S) {
+        s0 += __uint_as_float((uint32_t)lo[p]);
+        s1 += __uint_as_float((uint32_t)(lo[p] >> 32));
+        s2 += __uint_as_float((uint32_t)hi[p]);
+        s3 += __uint_as_float((uint32_t)(hi[p] >> 32));
       }
-      const int m = wm * 128 + j * 32 + lr;
-      const int n = col * kDownTileN + wn * 128 + i * 32 + 8 * q + 4 * lk;
-      const int lrow = tr.lrow0 + m;
-      const int rank = a.row_rank[lrow];
-      if (rank >= 0 && n < H) {
-        const uint64_t v = (uint64_t)pack_bf16x2(s0, s1) | ((uint64_t)pack_bf16x2(s2, s3) << 32);
-        if (direct_all || (direct && rank == a.self_rank))
-          *(__attribute__((address_space(1))) uint64_t*)(a.ret[rank] + (int64_t)a.row_slot[lrow] * H + n) = v;
-        else if (signal)
-          store8_device(a.y + (int64_t)lrow * H + n, v);
-        else
-          *(__attribute__((address_space(1))) uint64_t*)(a.y + (int64_t)lrow * H + n) = v;
-      }
+    const int i = b >> 4, j = (b >> 2) & 3, q = b & 3;
+    const int m = wm * 128 + j * 32 + lr;
+    const int n = col * kDownTileN + wn * 128 + i * 32 + 8 * q + 4 * lk;
+    const int lrow = tr.lrow0 + m;
+    const int rank = a.row_rank[lrow];
+    if (rank >= 0 && n < H) {
+      const uint64_t v = (uint64_t)pack_bf16x2(s0, s1) | ((uint64_t)pack_bf16x2(s2, s3) << 32);
+      if (direct_all || (direct && rank == a.self_rank))
+        *(__attribute__((address_space(1))) uint64_t*)(a.ret[rank] + (int64_t)a.row_slot[lrow] * H + n) = v;
+      else if (signal)
+        store8_device(a.y + (int64_t)lrow * H + n, v);
+      else
+        *(__attribute__((address_space(1))) uint64_t*)(a.y + (int64_t)lrow * H + n) = v;
     }
     if (signal && (tr.has_remote || !direct)) {
-      // Every wave's stores have completed before the slice counts itself in; the slice that
+      // Every wave's stores have completed before the pass counts itself in; the pass that
       // completes the tile raises the flag.
       wait_vm_and_barrier<0>();
       if (tid == 0) {
         const int tile = t * dpr + col;
         const uint32_t prev =
             __hip_atomic_fetch_add(&a.arrivals[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (prev + 1 == (uint32_t)kTailSlices)
+        if (prev + 1 == (uint32_t)kBlocks)
           __hip_atomic_store(&a.flags[tile], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }

@@ -45,8 +45,9 @@ struct ProducerArgs {
 // rows and its partials; writes the tiles' rows exactly as the down epilogue would and raises
 // their flags.
 struct TailArgs {
-  ProducerArgs p;             // the down launch's arguments (mode, outputs, flags, partials)
-  const int32_t* n_tile_rows; // device: tile rows of the plan
+  ProducerArgs p;              // the down launch's arguments (mode, outputs, flags, partials)
+  const int32_t* tail_rows;    // device: the split tile rows, in schedule order
+  const int32_t* n_split_rows; // device: how many
 };
 
 struct ConsumerArgs {
@@ -100,7 +101,7 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 // Gate/up tiles (down = false) or down-projection tiles with ready flags (down = true).
 hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream_t s);
 hipError_t launch_consumer(const ConsumerArgs& a, int grid, hipStream_t s);
-// Split tail tiles of a kModeDeferTail down launch: kTailSlices workgroups per tile.
+// Split tail tiles of a kModeDeferTail down launch: one accumulator block of one tile per pass.
 hipError_t launch_tail(const TailArgs& a, int grid, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s);
 // Resident producer workgroups per compute unit.
@@ -109,7 +110,7 @@ constexpr int kProducerThreads = 256;
 constexpr int kConsumerThreads = 256;
 constexpr int kCopyUnroll = 4;  // 16-byte vectors per consumer lane and copy chunk
 constexpr int kCopyParts = 4;   // consumer copy units (one wave each) per segment
-constexpr int kTailSlices = 16; // workgroups sharing one split tile's reduction
+constexpr int kTailGrid = 1024; // tail kernel workgroups (one pass each on the usual tail)
 // Consumer waves per SIMD the register budget must allow: at most 512 / 8 = 64 VGPRs each, so
 // two consumer waves fit beside one producer wave of up to 384 of the 512 registers.
 constexpr int kConsumerMinWaves = 8;

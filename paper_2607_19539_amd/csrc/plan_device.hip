@@ -385,6 +385,7 @@ __global__ __launch_bounds__(kWg) void plan_layout_kernel(DevPlanArgs a) {
     }
     const bool split = q >= n_whole;
     a.tile_rows[t] = TileRow{e, t0, nvalid, has_remote, split ? S : 1, split ? (q - n_whole) * dpr * S : -1};
+    if (split && a.split_k == 0) a.tail_rows[q - n_whole] = t;
     for (int32_t n = 0; n < dpr; ++n) w.pos_of_down[t * dpr + n] = -1;
   }
 

@@ -70,6 +70,7 @@ struct DevPlanArgs {
   int32_t* row_slot;
   Segment* segs;
   Group* groups;
+  int32_t* tail_rows;     // [kMaxTailRows] split tile rows of the default tail split, schedule order
   DevPlanWs ws;
 };
 

@@ -35,6 +35,9 @@ constexpr int32_t kMaxSplitK = 16;
 // Down tiles the producer runs at once on MI355X (one workgroup per compute unit).  The
 // default split (see build_plan) fills the last, partly occupied round of that many tiles.
 constexpr int32_t kRoundTiles = 256;
+// Split tile rows the default tail split can produce: each has at least two parts of its
+// down_per_row tiles within one round.
+constexpr int32_t kMaxTailRows = kRoundTiles / 2;
 
 struct TileRow {
   int32_t expert;      // local expert index
