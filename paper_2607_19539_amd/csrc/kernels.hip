@@ -597,6 +597,9 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
   __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsBytes];
   uint32_t* words = (uint32_t*)(lds + kSharedWords);  // [0] next item, [1] split-K verdict
   const int tid = threadIdx.x;
+  // Where consumer waves share a SIMD with this wave (shared CUs), the producer's instructions
+  // issue first: its workgroups are the stage's critical path, the consumer's copies are not.
+  __builtin_amdgcn_s_setprio(3);
   uint32_t q = xcc_id();  // meaningful in thread 0, which does the claiming
   const uint32_t end = (uint32_t)a.queue[kXcds];
   if (tid == 0) {
@@ -638,6 +641,7 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kProducerThreads) void tail_kernel(TailArgs ta) {
   const ProducerArgs& a = ta.p;
+  __builtin_amdgcn_s_setprio(3);  // ahead of consumer waves on shared CUs, like the producer
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wn = wave & 1, wm = wave >> 1, lr = lane & 31, lk = lane >> 5;
   const int dpr = a.down_per_row;
