@@ -79,6 +79,7 @@ def parse():
                     help="experts per rank for the single-layer expert-count sweep ('' to skip)")
     ap.add_argument("--only", choices=["all", "serial", "overlapped"], default="all",
                     help="run only one path of the headline workload (counter collection)")
+    ap.add_argument("--esweep-child", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     return ap.parse_args()
@@ -370,6 +371,14 @@ def main():
     from paper_2607_19539_amd.workload import make_workload
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.esweep_child:
+        # The expert-count sweep alone, in a process of its own: handles, queues and allocations
+        # of the earlier workloads do not carry over into its timings.
+        torch.cuda.set_device(0)
+        timeouts = []
+        rows = expert_count_sweep(torch, B, make_workload, args, [int(v) for v in args.esweep.split(",")], timeouts)
+        print(json.dumps({"expert_count_sweep": rows, "watchdog_timeouts": timeouts}), flush=True)
+        return
     torch.cuda.set_device(0)
     sweep_cs = [int(v) for v in args.sweep.split(",") if v]
     names = [args.workload] + [w for w in args.extra_workloads.split(",") if w and w != args.workload]
@@ -505,8 +514,19 @@ def main():
         torch.cuda.empty_cache()
     out["workloads"] = per_wl
     if args.esweep and args.only == "all":
-        out["expert_count_sweep"] = expert_count_sweep(torch, B, make_workload, args,
-                                                       [int(v) for v in args.esweep.split(",")], timeouts)
+        import subprocess
+        cmd = [sys.executable, "-u", os.path.abspath(__file__), "--esweep-child", "--esweep", args.esweep,
+               "--steps", str(args.steps), "--warmup", str(args.warmup), "--seed", str(args.seed),
+               "--band-rows", str(args.band_rows), "--split-k", str(args.split_k), "--mgb", str(args.mgb)]
+        child = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)  # progress lines pass through stderr
+        lines = [l for l in child.stdout.splitlines() if l.startswith("{")]
+        if child.returncode != 0 or not lines:
+            log(f"ERROR: expert-count sweep exited with {child.returncode}")
+            timeouts.append(f"expert-count sweep exited with {child.returncode}")
+        else:
+            res = json.loads(lines[-1])
+            out["expert_count_sweep"] = res["expert_count_sweep"]
+            timeouts += res["watchdog_timeouts"]
     out["watchdog_timeouts"] = timeouts
     log(f"done in {time.time() - t_start:.0f} s")
     print(json.dumps(out), flush=True)
