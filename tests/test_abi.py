@@ -89,3 +89,29 @@ def test_combine_checks_arguments_before_touching_the_device():
     assert lib.moe_combine(p + 8, 8, 64, p, p, 4, 2, p, None, None) == B.MOE_EUNSUPPORTED  # alignment
     assert lib.moe_combine(p, 2 ** 31, 64, p, p, 4, 2, p, None, None) == B.MOE_EUNSUPPORTED
     assert "moe_combine" in B.moe_stage_last_error(None)
+
+
+def test_handle_entry_points_reject_a_null_handle():
+    """Every handle entry point checks its handle before anything else (no device needed)."""
+    lib = B.load()
+    st = B.moe_stage_stats_t()
+    tm = B.moe_stage_times_t()
+    info = B.moe_plan_info_t()
+    null10 = [None] * 9
+    assert lib.moe_stage_run(None, *null10, 8, None) == B.MOE_EINVAL
+    assert lib.moe_stage_run_serial(None, *null10, None) == B.MOE_EINVAL
+    assert lib.moe_stage_run_devplan(None, *null10, 8, None) == B.MOE_EINVAL
+    assert lib.moe_stage_run_serial_devplan(None, *null10, None) == B.MOE_EINVAL
+    assert lib.moe_stage_query(None, ctypes.byref(st)) == B.MOE_EINVAL
+    assert lib.moe_stage_times(None, 0, ctypes.byref(tm)) == B.MOE_EINVAL
+    assert lib.moe_stage_plan_info(None, ctypes.byref(info)) == B.MOE_EINVAL
+    assert lib.moe_stage_plan_copy(None, B.MOE_PLAN_ITEMS, None, 0) == B.MOE_EINVAL
+    assert lib.moe_stage_destroy(None) == B.MOE_EINVAL
+
+
+def test_device_plan_flag_is_a_known_config_flag():
+    """MOE_TEST_PLAN_NO_LDS passes configuration checks (the host planner ignores it)."""
+    wl_cfg = B.make_config(256, 512, 2, 4, 0, 128, flags=B.MOE_LOCAL_DIRECT | B.MOE_TEST_PLAN_NO_LDS)
+    off = [0, 1, 2]
+    p = B.moe_plan_build(wl_cfg, off, [1, 2], [0, 0], [4, 4, 4, 4])
+    assert p["info"]["n_valid"] == 2
