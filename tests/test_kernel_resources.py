@@ -13,7 +13,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2607_19539_amd", "csrc")
-SOURCES = ["kernels.hip", "combine.hip"]
+SOURCES = ["kernels.hip", "combine.hip", "plan_device.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SIMD_REGISTERS = 512
 CONSUMER_WAVES_BESIDE_PRODUCER = 2
@@ -27,7 +27,7 @@ def kernels(tmp_path_factory):
     for src in SOURCES:
         out = tmp_path_factory.mktemp("dev") / (src + ".s")
         subprocess.run([HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-x", "hip", "--cuda-device-only",
-                        "-S", os.path.join(CSRC, src), f"-I{os.path.join(ROOT, 'include')}", "-o", str(out),
+                        "-S", os.path.join(CSRC, src), f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}", "-o", str(out),
                         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"],
                        check=True, capture_output=True)
         meta = out.read_text().split("amdhsa.kernels:", 1)[1]
@@ -82,3 +82,24 @@ def test_consumer_leaves_lds_to_the_producer(kernels):
     assert int(cons["group_segment_fixed_size"]) == 0
     for name, f in by_name(kernels, "producer_kernel").items():
         assert int(f["group_segment_fixed_size"]) == 160 * 1024, name
+
+
+def test_tail_kernel_fits_beside_a_producer_wave(kernels):
+    """The tail kernel runs while the consumer polls on shared CUs: it holds no LDS (so no
+    workgroup waits for LDS it holds) and at most 128 vector registers per wave."""
+    (tail,) = by_name(kernels, "tail_kernel").values()
+    assert int(tail["group_segment_fixed_size"]) == 0
+    assert int(tail["vgpr_count"]) <= 128
+
+
+def test_device_planner_kernels_present_and_small(kernels):
+    """The four planner kernels: single-workgroup ones stay within the 160 KiB of LDS a workgroup
+    may hold on gfx950, grid ones use little."""
+    names = {n.split("_kernel")[0].rsplit("plan_", 1)[1]: f for n, f in by_name(kernels, "plan_").items()
+             if "_kernel" in n}
+    assert set(names) == {"rows", "layout", "fill", "segs"}, names
+    for part, f in names.items():
+        lds = int(f["group_segment_fixed_size"])
+        assert lds <= 160 * 1024, (part, lds)
+        if part in ("rows", "fill"):
+            assert lds <= 32 * 1024, (part, lds)
