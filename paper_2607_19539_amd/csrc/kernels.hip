@@ -392,12 +392,15 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     const int c16 = tid & 15;
     const int f = col * kGuTileF + c16 * 8;
     uint16_t* blk = a.hws + ((size_t)(f / kTileK) * a.hws_rows) * kTileK + (f % kTileK);
+    // Padding rows are stored too: they gather a valid token row, so their activations are
+    // finite, and the down launch only uses them for padding outputs it never stores -- no
+    // per-row lookup sits between the staged tile and its stores.
+    if (f < F) {
 #pragma unroll 4
-    for (int p = 0; p < kTileM / 16; ++p) {
-      const int m = p * 16 + (tid >> 4);
-      const int lrow = lrow0 + m;
-      if (a.row_rank[lrow] >= 0 && f < F)  // padding rows are never read back
-        *(u32x4*)(blk + (size_t)lrow * kTileK) = *(const u32x4*)(lds + m * kGuOutStride + c16 * 16);
+      for (int p = 0; p < kTileM / 16; ++p) {
+        const int m = p * 16 + (tid >> 4);
+        *(u32x4*)(blk + (size_t)(lrow0 + m) * kTileK) = *(const u32x4*)(lds + m * kGuOutStride + c16 * 16);
+      }
     }
   } else {
     // Split K: every part stores its fp32 accumulators (in register order, so each thread
