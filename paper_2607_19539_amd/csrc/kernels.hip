@@ -59,6 +59,9 @@ constexpr int kGuOutStride = kGuTileF * 2 + 16;        // 272 B per staged activ
 // between the waves; the operand ring overwrites them, so they are used only outside it.
 constexpr int kSharedWords = kLdsBytes - 16;
 static_assert(kTileM * kDownOutStride <= kSharedWords, "down staging overlaps the shared words");
+// Down epilogue: each tile row's (rank, slot) pairs, right past the staged output tile.
+constexpr int kDownRowInfo = kTileM * kDownOutStride;
+static_assert(kDownRowInfo + kTileM * 8 <= kSharedWords, "row info overlaps the shared words");
 static_assert(kTileM * kGuOutStride <= kSharedWords, "gate/up staging overlaps the shared words");
 
 // Chunk swizzle of the 128-byte operand rows: chunk c of row r is stored at c ^ ((r / 2) % 8).
@@ -437,6 +440,11 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
       if (words[1] == 0) return;  // another part finishes the tile
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
+    // Each row's rank and slot for the stores below: one row per thread, loaded now so the
+    // loads overlap the staging, and put in LDS past the staged tile.
+    static_assert(kProducerThreads == kTileM, "one row per thread");
+    const int my_rank = a.row_rank[lrow0 + tid], my_slot = a.row_slot[lrow0 + tid];
+    int32_t* rinfo = (int32_t*)(lds + kDownRowInfo);
     // Down-projection output: lane values -> LDS tile [256 rows][256 hidden columns].
     auto stage_out = [&](int i, int j, int q, float4 s) {
       const int m = wm * 128 + j * 32 + lr;
@@ -528,6 +536,8 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
             __builtin_amdgcn_sched_barrier(0);  // block by block (see above)
           }
     }
+    rinfo[2 * tid] = my_rank;
+    rinfo[2 * tid + 1] = my_slot;
     __syncthreads();
     // Rows returning to another rank go to the staged output Y (the consumer moves them);
     // local rows go straight to the local receive buffer when the producer writes them
@@ -544,11 +554,11 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
       for (int p = 0; p < kTileM / 4; ++p) {
         const int m = p * 4 + (tid >> 6);
         const int lrow = lrow0 + m;
-        const int rank = a.row_rank[lrow];
+        const int rank = rinfo[2 * m];
         if (rank >= 0 && n < H) {
           const uint64_t v = *(const uint64_t*)(lds + m * kDownOutStride + c8 * 8);
           if (direct && rank == a.self_rank)
-            *(__attribute__((address_space(1))) uint64_t*)(a.ret[rank] + (int64_t)a.row_slot[lrow] * H + n) = v;
+            *(__attribute__((address_space(1))) uint64_t*)(a.ret[rank] + (int64_t)rinfo[2 * m + 1] * H + n) = v;
           else
             store8_device(a.y + (int64_t)lrow * H + n, v);
         }
@@ -561,11 +571,11 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
       for (int p = 0; p < kTileM / 8; ++p) {
         const int m = p * 8 + (tid >> 5);
         const int lrow = lrow0 + m;
-        const int rank = a.row_rank[lrow];
+        const int rank = rinfo[2 * m];
         if (rank >= 0 && n < H) {
           const u32x4 v = *(const u32x4*)(lds + m * kDownOutStride + c16 * 16);
           if (direct_all || (direct && rank == a.self_rank))
-            *(g_u32x4*)(a.ret[rank] + (int64_t)a.row_slot[lrow] * H + n) = v;
+            *(g_u32x4*)(a.ret[rank] + (int64_t)rinfo[2 * m + 1] * H + n) = v;
           else
             *(g_u32x4*)(a.y + (int64_t)lrow * H + n) = v;
         }
