@@ -64,7 +64,7 @@ def parse():
     ap.add_argument("--extra-workloads", default="mixtral_zipf,fine,large_fine",
                     help="further workloads measured into 'workloads' ('' = none)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cu-split", type=int, default=32, help="consumer compute units")
+    ap.add_argument("--cu-split", type=int, default=248, help="consumer compute units")
     ap.add_argument("--mode", choices=["shared", "partitioned"], default="shared",
                     help="shared: the producer keeps every CU and the consumer runs beside it on its "
                          "cu_split CUs; partitioned: the consumer's CUs are reserved for it")
@@ -73,8 +73,9 @@ def parse():
     ap.add_argument("--mgb", type=int, default=1, help="tile-row pieces per middle transfer segment")
     ap.add_argument("--copy-curve", default="8,16,32,64,128",
                     help="consumer CU counts for the consumer-only copy ceiling ('' to skip)")
-    ap.add_argument("--sweep", default="8,16,24,32",
-                    help="CU splits for the overlap-speedup sweep, both modes ('' = none)")
+    ap.add_argument("--sweep", default="8,16,32,64,128,248",
+                    help="CU splits for the overlap-speedup sweep: shared CUs at each, a reserved "
+                         "partition at those up to 64 ('' = none)")
     ap.add_argument("--esweep", default="4,8,16,32,64",
                     help="experts per rank for the single-layer expert-count sweep ('' to skip)")
     ap.add_argument("--only", choices=["all", "serial", "overlapped"], default="all",
@@ -431,7 +432,7 @@ def main():
         if sweep_cs and ser is not None and only == "all":
             for mgb in (1, 2):
                 for c in sweep_cs:
-                    for mode in ("shared", "partitioned"):
+                    for mode in ("shared", "partitioned") if c <= 64 else ("shared",):
                         key = bench.stage(mode, mgb)
                         r = bench.timed(key, "overlapped", c, max(steps // 2, 5), max(warmup // 2, 3))
                         sweep.append({"cu_split": c, "cu_mode": mode, "mgb": mgb,

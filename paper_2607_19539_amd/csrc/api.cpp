@@ -33,8 +33,13 @@ constexpr int kTimingRing = 512;
 
 // Adaptive CU split (cu_split = 0): the consumer sizes tried, the completed runs measured for
 // each, and the event pairs kept in flight for the measurements.
-constexpr int kAutoSplits[] = {8, 16, 32, 64};
-constexpr int kNumAutoSplits = sizeof(kAutoSplits) / sizeof(kAutoSplits[0]);
+// With shared CUs the consumer's waves are best spread thinly over many compute units (each
+// slows the producer workgroup beside it); a reserved partition takes its CUs from the producer,
+// so it stays small.
+constexpr int kAutoSplitsShared[] = {32, 96, 160, 248};
+constexpr int kAutoSplitsPartitioned[] = {8, 16, 32, 64};
+constexpr int kNumAutoSplits = sizeof(kAutoSplitsShared) / sizeof(kAutoSplitsShared[0]);
+static_assert(sizeof(kAutoSplitsPartitioned) == sizeof(kAutoSplitsShared), "one candidate count");
 constexpr int kAutoSamples = 3;
 constexpr int kAutoRing = 8;
 
@@ -494,6 +499,10 @@ void harvest_auto(moe_stage_s* h) {
   }
 }
 
+int auto_split(const moe_stage_s* h, int i) {
+  return (h->cfg.flags & MOE_SHARED_CUS) ? kAutoSplitsShared[i] : kAutoSplitsPartitioned[i];
+}
+
 // The split of the next auto run: candidates are measured one after another (kAutoSamples
 // finished runs each, so the CU-masked queue is rebuilt only once per candidate), then the one
 // with the lowest median stage time is kept.  Returns the candidate index.
@@ -501,7 +510,7 @@ int pick_auto(moe_stage_s* h) {
   AutoSplit& a = h->autos;
   if (a.chosen >= 0) return a.chosen;
   while (a.cand < kNumAutoSplits &&
-         ((int)a.ms[a.cand].size() >= kAutoSamples || kAutoSplits[a.cand] > h->num_cus - h->n_xcd))
+         ((int)a.ms[a.cand].size() >= kAutoSamples || auto_split(h, a.cand) > h->num_cus - h->n_xcd))
     ++a.cand;
   if (a.cand < kNumAutoSplits) return a.cand;
   float best = 0.f;
@@ -698,7 +707,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   if (autosplit) {
     harvest_auto(h);
     auto_cand = pick_auto(h);
-    cu_split = kAutoSplits[auto_cand];
+    cu_split = auto_split(h, auto_cand);
     if (!h->autos.busy[h->autos.next]) auto_slot = h->autos.next;  // else: this run is not measured
   }
   if (cu_split < 1 || cu_split > h->num_cus - h->n_xcd)
@@ -786,7 +795,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
     h->autos.ev_cand[auto_slot] = auto_cand;
     h->autos.next = (auto_slot + 1) % kAutoRing;
   }
-  h->last.auto_cu_split = autosplit ? (h->autos.chosen >= 0 ? kAutoSplits[h->autos.chosen] : 0) : -1;
+  h->last.auto_cu_split = autosplit ? (h->autos.chosen >= 0 ? auto_split(h, h->autos.chosen) : 0) : -1;
   h->ran = true;
   h->counters_pending = true;
   return MOE_OK;

@@ -729,27 +729,35 @@ __global__ __launch_bounds__(kProducerThreads) void tail_kernel(TailArgs ta) {
 }
 
 // ---------------------------------------------------------------------------
-// Consumer: every wave works alone.  It claims a copy unit -- a quarter of a segment, taken
-// in the segments' ready order, so the four quarters of a segment go to four waves at once
-// -- polls the segment's flags (one flag per lane; all must show the current epoch), then
-// copies its quarter with 16-byte loads and stores.  The kernel uses no LDS, so in a
-// shared-CU run its workgroups never keep a producer workgroup (which takes all of LDS)
-// off a compute unit.
+// Consumer: every wave works alone.  It takes a copy unit -- a quarter of a segment, in the
+// segments' ready order -- polls the segment's flags (one flag per lane; all must show the
+// current epoch), then copies its quarter with 16-byte loads and stores.  The kernel uses no
+// LDS, so in a shared-CU run its workgroups never keep a producer workgroup (which takes all
+// of LDS) off a compute unit.  A copying wave slows the producer workgroup on its compute
+// unit, so the units are spread: the first ones go one per workgroup (the four quarters of a
+// segment to four workgroups), and a wide consumer grid puts about one copying wave on each
+// compute unit instead of four on each of a few.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_kernel(ConsumerArgs a) {
   const int lane = threadIdx.x & 63;
   const int32_t n_segs = *a.n_segs;
+  // A wave's first unit is fixed, (wave of its workgroup) x grid + workgroup; later units are
+  // claimed from the counter, after all the fixed ones.
+  const uint32_t n_waves = gridDim.x * (kConsumerThreads / 64);
+  uint32_t unit = (threadIdx.x >> 6) * gridDim.x + blockIdx.x;
   uint64_t polls = 0, waited = 0;
-  for (;;) {
-    uint32_t unit = 0;
-    if (lane == 0) unit = atomicAdd(&a.ctr->seg_next, 1u);
-    unit = __builtin_amdgcn_readfirstlane(unit);  // every lane is active here
+  for (bool first = true;; first = false) {
+    if (!first) {
+      if (lane == 0) unit = n_waves + atomicAdd(&a.ctr->seg_next, 1u);
+      unit = __builtin_amdgcn_readfirstlane(unit);  // every lane is active here
+    }
     const int32_t s = (int32_t)(unit / kCopyParts);
     const int32_t part = (int32_t)(unit % kCopyParts);
     if (s >= n_segs) break;
     const Segment sg = a.segs[s];
     const uint64_t t0 = ticks();
     bool expired = false;
+    uint32_t backoff = 1;
     for (int base = 0; base < sg.flag_count && !expired; base += 64) {
       const bool mine = base + lane < sg.flag_count;
       const uint32_t* fp = a.flags + sg.flag_begin + base + lane;
@@ -762,7 +770,10 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
           expired = true;
           break;
         }
-        __builtin_amdgcn_s_sleep(1);
+        // Exponential backoff: a wave that waits through the whole gate/up launch polls
+        // a few times per microsecond at most, instead of flooding L2 with flag loads.
+        for (uint32_t i = 0; i < backoff; ++i) __builtin_amdgcn_s_sleep(kPollSleep);
+        backoff = backoff < kPollBackoffMax ? 2 * backoff : kPollBackoffMax;
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");

@@ -110,6 +110,10 @@ constexpr int kProducerThreads = 256;
 constexpr int kConsumerThreads = 256;
 constexpr int kCopyUnroll = 4;  // 16-byte vectors per consumer lane and copy chunk
 constexpr int kCopyParts = 4;   // consumer copy units (one wave each) per segment
+// Consumer flag polls sleep kPollSleep x 64 cycles, doubling the count of sleeps per poll up to
+// kPollBackoffMax (about 2.5 us between polls at the loaded clock).
+constexpr int kPollSleep = 4;
+constexpr uint32_t kPollBackoffMax = 16;
 constexpr int kTailGrid = 1024; // tail kernel workgroups (one pass each on the usual tail)
 // Consumer waves per SIMD the register budget must allow: at most 512 / 8 = 64 VGPRs each, so
 // two consumer waves fit beside one producer wave of up to 384 of the 512 registers.

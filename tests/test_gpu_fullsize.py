@@ -14,7 +14,7 @@ from tests.gpu_helpers import DeviceWorkload, compare, log, make_stage, oracle_b
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
-BENCH_CU_SPLIT = 32
+BENCH_CU_SPLIT = 248
 BENCH_FLAGS = B.MOE_LOCAL_DIRECT | B.MOE_SHARED_CUS   # bench.py's default mode, on its own stream
 SAMPLE_ROWS = 24
 

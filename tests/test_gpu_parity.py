@@ -183,7 +183,7 @@ def test_shared_cus_matches_partitioned(local_direct):
     with make_stage(wl, band_rows=16, flags=base | B.MOE_SHARED_CUS | B.MOE_POISON) as st:
         # Null stream: the producer forks to the handle's stream.  Created stream: the
         # producer runs on it directly, beside the consumer's CU-masked stream.
-        for stream, split in ((None, 1), (None, 8), (side, 8), (side, 32)):
+        for stream, split in ((None, 1), (None, 8), (side, 8), (side, 32), (None, 248), (side, 248)):
             dw.fill()
             torch.cuda.synchronize()
             st.run(*dw.args(), cu_split=split, stream=stream)
@@ -302,8 +302,18 @@ def test_auto_cu_split_settles_and_keeps_results():
             seen.add(stats["consumer_cus"])
             for a, b in zip(out, fixed):
                 assert np.array_equal(a, b)
-        assert stats["auto_cu_split"] in (8, 16, 32, 64)
+        assert stats["auto_cu_split"] in (32, 96, 160, 248)
         assert stats["consumer_cus"] == stats["auto_cu_split"]
+    assert seen >= {32, 96, 160, 248}
+    # A reserved partition takes its CUs from the producer: the candidates stay small.
+    seen = set()
+    with make_stage(wl, flags=B.MOE_LOCAL_DIRECT) as st:
+        for i in range(16):
+            out, stats = run_overlapped(dw, st, cu_split=0)
+            seen.add(stats["consumer_cus"])
+            for a, b in zip(out, fixed):
+                assert np.array_equal(a, b)
+        assert stats["auto_cu_split"] in (8, 16, 32, 64)
     assert seen >= {8, 16, 32, 64}
     with make_stage(wl) as st:
         st.run_serial(*dw.args())
