@@ -47,6 +47,17 @@ def test_fullsize_sampled(name):
             want[wl.row_slot[wl.row_src_rank == r]] = True
             assert np.array_equal(written_mask(dw.bufs[r]), want), f"rank {r} placement"
         over = [b.clone() for b in dw.bufs]
+        # A narrow consumer: four copy units per segment, far more than its waves, so most
+        # units are claimed from the counter after each wave's fixed first one.
+        dw.fill()
+        torch.cuda.synchronize()
+        st.run(*dw.args(), cu_split=8, stream=side)
+        torch.cuda.synchronize()
+        narrow = st.query()
+        log(f"full-size {name}: c=8 units={4 * narrow['n_segments']} consumer waves={4 * narrow['consumer_grid']}")
+        assert narrow["timeout"] == 0
+        for a, b in zip(over, dw.bufs):
+            assert torch.equal(a, b), "consumer splits differ"
         dw.fill()
         torch.cuda.synchronize()
         st.run_serial(*dw.args(), stream=side)

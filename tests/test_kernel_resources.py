@@ -84,7 +84,7 @@ def test_consumer_leaves_lds_to_the_producer(kernels):
         assert int(f["group_segment_fixed_size"]) == 160 * 1024, name
 
 
-def test_tail_kernel_fits_beside_a_producer_wave(kernels):
+def test_tail_kernel_fits_beside_the_polling_consumer(kernels):
     """The tail kernel runs while the consumer polls on shared CUs: it holds no LDS (so no
     workgroup waits for LDS it holds) and at most 128 vector registers per wave."""
     (tail,) = by_name(kernels, "tail_kernel").values()
