@@ -287,6 +287,8 @@ int prepare(moe_stage_s* h, bool overlapped, const void* x,
   hd.tail_split = P.tail_split;
   hd.n_split_rows = P.n_split_rows;
   hd.n_partials = P.n_partials;
+  for (int x = 0; x < kXcds; ++x)
+    hd.down_qmax = std::max(hd.down_qmax, P.down_queue[x + 1] - P.down_queue[x]);
   hd.n_valid = P.n_valid;
   hd.n_lrows = P.n_lrows();
   hd.n_band_pad = P.n_band_pad;
@@ -747,6 +749,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   ca.ret = pgu.ret;
   ca.segs = (const Segment*)(h->d_plan + lay.segs);
   ca.n_segs = &((const PlanHeader*)(h->d_plan + lay.hdr))->n_segs;
+  ca.down_qmax = &((const PlanHeader*)(h->d_plan + lay.hdr))->down_qmax;
   ca.flags = h->flags;
   ca.epoch = h->epoch;
   ca.H = h->cfg.hidden;

@@ -729,14 +729,15 @@ __global__ __launch_bounds__(kProducerThreads) void tail_kernel(TailArgs ta) {
 }
 
 // ---------------------------------------------------------------------------
-// Consumer: every wave works alone.  It takes a copy unit -- a quarter of a segment, in the
-// segments' ready order -- polls the segment's flags (one flag per lane; all must show the
-// current epoch), then copies its quarter with 16-byte loads and stores.  The kernel uses no
+// Consumer: every wave works alone.  It takes a copy unit -- a quarter of a segment, or up to a
+// sixteenth of one that becomes ready in the down launch's last two rounds, in the segments'
+// ready order -- polls the segment's flags (one flag per lane; all must show the current
+// epoch), then copies its part with 16-byte loads and stores.  The kernel uses no
 // LDS, so in a shared-CU run its workgroups never keep a producer workgroup (which takes all
 // of LDS) off a compute unit.  A copying wave slows the producer workgroup on its compute
-// unit, so the units are spread: the first ones go one per workgroup (the four quarters of a
-// segment to four workgroups), and a wide consumer grid puts about one copying wave on each
-// compute unit instead of four on each of a few.
+// unit, so the units are spread: the first ones go one per workgroup (the parts of a segment to
+// different workgroups), and a wide consumer grid puts about one copying wave on each compute
+// unit instead of four on each of a few.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_kernel(ConsumerArgs a) {
   const int lane = threadIdx.x & 63;
@@ -745,15 +746,33 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
   // claimed from the counter, after all the fixed ones.
   const uint32_t n_waves = gridDim.x * (kConsumerThreads / 64);
   uint32_t unit = (threadIdx.x >> 6) * gridDim.x + blockIdx.x;
+  // Segments are in ready order: the first late one by binary search (uniform loads).
+  const int32_t late_from = *a.down_qmax - kLatePositions;
+  int32_t n_early = 0;
+  for (int32_t hi = n_segs; n_early < hi;) {
+    const int32_t mid = (n_early + hi) >> 1;
+    if (a.segs[mid].ready_pos < late_from)
+      n_early = mid + 1;
+    else
+      hi = mid;
+  }
+  // A late segment's units hold about 128 KiB of each 256-row piece: H / 256 of them, within
+  // [kCopyParts, kCopyPartsLate].
+  const int32_t late_parts = min(max(a.H / 256, kCopyParts), kCopyPartsLate);
+  const uint32_t early_units = (uint32_t)n_early * kCopyParts;
+  const uint32_t n_units = early_units + (uint32_t)(n_segs - n_early) * late_parts;
   uint64_t polls = 0, waited = 0;
   for (bool first = true;; first = false) {
     if (!first) {
       if (lane == 0) unit = n_waves + atomicAdd(&a.ctr->seg_next, 1u);
       unit = __builtin_amdgcn_readfirstlane(unit);  // every lane is active here
     }
-    const int32_t s = (int32_t)(unit / kCopyParts);
-    const int32_t part = (int32_t)(unit % kCopyParts);
-    if (s >= n_segs) break;
+    if (unit >= n_units) break;
+    const bool early = unit < early_units;
+    const uint32_t u = early ? unit : unit - early_units;
+    const int32_t parts = early ? kCopyParts : late_parts;
+    const int32_t s = early ? (int32_t)(u / kCopyParts) : n_early + (int32_t)(u / (uint32_t)late_parts);
+    const int32_t part = (int32_t)(u % (uint32_t)parts);
     const Segment sg = a.segs[s];
     const uint64_t t0 = ticks();
     bool expired = false;
@@ -785,13 +804,13 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
       }
       break;
     }
-    // The segment is contiguous on both sides: this wave's quarter is a flat run of 16-byte
+    // The segment is contiguous on both sides: this wave's part is a flat run of 16-byte
     // vectors, copied in chunks of kCopyUnroll vectors per lane, double-buffered: the next
     // chunk's loads are in flight while the current chunk is stored.  The last chunk re-reads
     // itself as its "next" (in bounds) instead of branching, which would drain every
     // outstanding access.
     const int64_t n16 = (int64_t)sg.rows * a.H / 8;
-    const int64_t i0 = n16 * part / kCopyParts, i1 = n16 * (part + 1) / kCopyParts;
+    const int64_t i0 = n16 * part / parts, i1 = n16 * (part + 1) / parts;
     const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H) + i0;
     g_u32x4* dst = (g_u32x4*)(a.ret[sg.dst_rank] + (int64_t)sg.slot0 * a.H) + i0;
     const int64_t n = i1 - i0;

@@ -55,6 +55,7 @@ struct ConsumerArgs {
   uint16_t* const* ret;
   const Segment* segs;
   const int32_t* n_segs;   // device: segments of the plan
+  const int32_t* down_qmax; // device: longest down queue, in items
   const uint32_t* flags;
   uint32_t epoch;
   int32_t H;
@@ -110,6 +111,12 @@ constexpr int kProducerThreads = 256;
 constexpr int kConsumerThreads = 256;
 constexpr int kCopyUnroll = 4;  // 16-byte vectors per consumer lane and copy chunk
 constexpr int kCopyParts = 4;   // consumer copy units (one wave each) per segment
+// Segments ready in the last kLatePositions positions of the down queues (two rounds of an
+// XCD's 32 compute units) are copied after most of the producer's work is done, some of them
+// after all of it: they take up to kCopyPartsLate units each, so more waves share the final
+// copies.
+constexpr int kCopyPartsLate = 16;
+constexpr int kLatePositions = 64;
 // Consumer flag polls sleep kPollSleep x 64 cycles, doubling the count of sleeps per poll up to
 // kPollBackoffMax (about 2.5 us between polls at the loaded clock).
 constexpr int kPollSleep = 4;

@@ -88,7 +88,7 @@ struct PlanHeader {
   int32_t tail_split;    // K parts of each split down tile
   int32_t n_split_rows;
   int32_t n_partials;
-  int32_t down_qmax;     // longest down queue (device planner)
+  int32_t down_qmax;     // longest down queue (items)
   int32_t n_groups_all;  // device planner: owner groups of the layout, any plan kind
   int32_t reserved[2];
   int64_t n_valid, n_lrows, n_band_pad, n_remote;
