@@ -756,11 +756,12 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
     else
       hi = mid;
   }
-  // A late segment's units hold about 128 KiB of each 256-row piece: H / 256 of them, within
-  // [kCopyParts, kCopyPartsLate].
-  const int32_t late_parts = min(max(a.H / 256, kCopyParts), kCopyPartsLate);
-  const uint32_t early_units = (uint32_t)n_early * kCopyParts;
-  const uint32_t n_units = early_units + (uint32_t)(n_segs - n_early) * late_parts;
+  // A late segment's units hold about 128 KiB of each 256-row piece: H / 256 of them rounded
+  // down to a power of two within [kCopyParts, kCopyPartsLate], so a part's range is a shift.
+  const int32_t late_shift =
+      min(max(31 - __builtin_clz((uint32_t)max(a.H / 256, 1)), kCopyPartsShift), kCopyPartsLateShift);
+  const uint32_t early_units = (uint32_t)n_early << kCopyPartsShift;
+  const uint32_t n_units = early_units + ((uint32_t)(n_segs - n_early) << late_shift);
   uint64_t polls = 0, waited = 0;
   for (bool first = true;; first = false) {
     if (!first) {
@@ -770,9 +771,9 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
     if (unit >= n_units) break;
     const bool early = unit < early_units;
     const uint32_t u = early ? unit : unit - early_units;
-    const int32_t parts = early ? kCopyParts : late_parts;
-    const int32_t s = early ? (int32_t)(u / kCopyParts) : n_early + (int32_t)(u / (uint32_t)late_parts);
-    const int32_t part = (int32_t)(u % (uint32_t)parts);
+    const int32_t shift = early ? kCopyPartsShift : late_shift;
+    const int32_t s = (early ? 0 : n_early) + (int32_t)(u >> shift);
+    const int32_t part = (int32_t)(u & ((1u << shift) - 1));
     const Segment sg = a.segs[s];
     const uint64_t t0 = ticks();
     bool expired = false;
@@ -810,7 +811,7 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
     // itself as its "next" (in bounds) instead of branching, which would drain every
     // outstanding access.
     const int64_t n16 = (int64_t)sg.rows * a.H / 8;
-    const int64_t i0 = n16 * part / parts, i1 = n16 * (part + 1) / parts;
+    const int64_t i0 = (n16 * part) >> shift, i1 = (n16 * (part + 1)) >> shift;
     const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H) + i0;
     g_u32x4* dst = (g_u32x4*)(a.ret[sg.dst_rank] + (int64_t)sg.slot0 * a.H) + i0;
     const int64_t n = i1 - i0;

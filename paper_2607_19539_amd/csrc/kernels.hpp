@@ -110,12 +110,14 @@ int producer_blocks_per_cu();
 constexpr int kProducerThreads = 256;
 constexpr int kConsumerThreads = 256;
 constexpr int kCopyUnroll = 4;  // 16-byte vectors per consumer lane and copy chunk
-constexpr int kCopyParts = 4;   // consumer copy units (one wave each) per segment
+constexpr int kCopyPartsShift = 2;
+constexpr int kCopyParts = 1 << kCopyPartsShift;  // consumer copy units (one wave each) per segment
 // Segments ready in the last kLatePositions positions of the down queues (two rounds of an
 // XCD's 32 compute units) are copied after most of the producer's work is done, some of them
 // after all of it: they take up to kCopyPartsLate units each, so more waves share the final
 // copies.
-constexpr int kCopyPartsLate = 16;
+constexpr int kCopyPartsLateShift = 4;
+constexpr int kCopyPartsLate = 1 << kCopyPartsLateShift;
 constexpr int kLatePositions = 64;
 // Consumer flag polls sleep kPollSleep x 64 cycles, doubling the count of sleeps per poll up to
 // kPollBackoffMax (about 2.5 us between polls at the loaded clock).
