@@ -47,7 +47,10 @@ struct AutoSplit {
   int cand = 0;     // candidate being measured
   int chosen = -1;  // index of the split in use once every candidate is measured
   std::vector<float> ms[kNumAutoSplits];
-  hipEvent_t ev[kAutoRing][2] = {};
+  // Per measured run: GPU wall-clock stamps at its start and after its join (pinned host
+  // memory, written by a one-thread kernel) and an event without timing that marks them done.
+  uint64_t* stamps = nullptr;  // [kAutoRing][2]
+  hipEvent_t done[kAutoRing] = {};
   int ev_cand[kAutoRing] = {};
   bool busy[kAutoRing] = {};
   int next = 0;
@@ -494,9 +497,10 @@ void make_masks(int num_cus, int n_xcd, int c, bool shared, std::vector<uint32_t
 void harvest_auto(moe_stage_s* h) {
   AutoSplit& a = h->autos;
   for (int i = 0; i < kAutoRing; ++i) {
-    if (!a.busy[i] || hipEventQuery(a.ev[i][1]) != hipSuccess) continue;
-    float ms = 0.f;
-    if (hipEventElapsedTime(&ms, a.ev[i][0], a.ev[i][1]) == hipSuccess) a.ms[a.ev_cand[i]].push_back(ms);
+    if (!a.busy[i] || hipEventQuery(a.done[i]) != hipSuccess) continue;
+    const volatile uint64_t* st = a.stamps + 2 * i;
+    const uint64_t t0 = st[0], t1 = st[1];
+    if (t1 > t0) a.ms[a.ev_cand[i]].push_back((float)((double)(t1 - t0) * 1e-5));  // 100 MHz ticks
     a.busy[i] = false;
   }
 }
@@ -505,20 +509,30 @@ int auto_split(const moe_stage_s* h, int i) {
   return (h->cfg.flags & MOE_SHARED_CUS) ? kAutoSplitsShared[i] : kAutoSplitsPartitioned[i];
 }
 
-// The split of the next auto run: candidates are measured one after another (kAutoSamples
-// finished runs each, so the CU-masked queue is rebuilt only once per candidate), then the one
-// with the lowest median stage time is kept.  Returns the candidate index.
+// The split of the next auto run: the candidates take turns, run by run, so each is measured
+// under the same conditions (the same CU-masked queues alive, the same GPU state) rather than
+// the last one beside the most queues; once each has 1 + kAutoSamples finished runs, the one
+// with the lowest median stage time over all but its first (a warm-up of its queue) is kept.
+// Returns the candidate index.
 int pick_auto(moe_stage_s* h) {
   AutoSplit& a = h->autos;
   if (a.chosen >= 0) return a.chosen;
-  while (a.cand < kNumAutoSplits &&
-         ((int)a.ms[a.cand].size() >= kAutoSamples || auto_split(h, a.cand) > h->num_cus - h->n_xcd))
-    ++a.cand;
-  if (a.cand < kNumAutoSplits) return a.cand;
+  auto valid = [&](int c) { return auto_split(h, c) <= h->num_cus - h->n_xcd; };
+  bool measured = true, any = false;
+  for (int c = 0; c < kNumAutoSplits; ++c) {
+    any |= valid(c);
+    if (valid(c) && (int)a.ms[c].size() < 1 + kAutoSamples) measured = false;
+  }
+  if (!any) return 0;  // no candidate fits this GPU: the run reports the split as unsupported
+  if (!measured) {
+    do a.cand = (a.cand + 1) % kNumAutoSplits;
+    while (!valid(a.cand));
+    return a.cand;
+  }
   float best = 0.f;
   for (int c = 0; c < kNumAutoSplits; ++c) {
-    auto v = a.ms[c];
-    if (v.empty()) continue;
+    if (!valid(c)) continue;
+    std::vector<float> v(a.ms[c].begin() + 1, a.ms[c].end());
     std::nth_element(v.begin(), v.begin() + v.size() / 2, v.end());
     if (a.chosen < 0 || v[v.size() / 2] < best) {
       a.chosen = c;
@@ -682,10 +696,12 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       !try_hip(hipEventCreateWithFlags(&h->ev_join_p, kSyncEv), "hipEventCreate") ||
       !try_hip(hipEventCreateWithFlags(&h->ev_done, kSyncEv), "hipEventCreate"))
     return bail(MOE_EHIP);
-  for (auto& pair : h->autos.ev)
-    for (auto& ev : pair)
-      if (!try_hip(hipEventCreateWithFlags(&ev, hipEventReleaseToDevice), "hipEventCreate"))
-        return bail(MOE_EHIP);
+  for (auto& ev : h->autos.done)
+    if (!try_hip(hipEventCreateWithFlags(&ev, kSyncEv), "hipEventCreate")) return bail(MOE_EHIP);
+  if (!try_hip(hipHostMalloc((void**)&h->autos.stamps, 2 * kAutoRing * sizeof(uint64_t),
+                             hipHostMallocCoherent | hipHostMallocMapped),
+               "hipHostMalloc"))
+    return bail(MOE_EHIP);
   if (h->cfg.flags & MOE_KERNEL_TIMING) {
     h->ring.resize(kTimingRing);
     for (auto& r : h->ring)
@@ -728,7 +744,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   BlobLayout lay{};
   TimingRec* tr = timing_slot(h);
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[0], stream));
-  if (auto_slot >= 0) HIP_TRY(h, hipEventRecord(h->autos.ev[auto_slot][0], stream));
+  if (auto_slot >= 0) HIP_TRY(h, launch_stamp(&h->autos.stamps[2 * auto_slot], stream));
   rc = dev ? prepare_device(h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay)
            : prepare(h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, stream, &lay);
   if (rc) {
@@ -793,7 +809,8 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   }
   HIP_TRY(h, hipEventRecord(h->ev_done, stream));
   if (auto_slot >= 0) {
-    HIP_TRY(h, hipEventRecord(h->autos.ev[auto_slot][1], stream));
+    HIP_TRY(h, launch_stamp(&h->autos.stamps[2 * auto_slot + 1], stream));
+    HIP_TRY(h, hipEventRecord(h->autos.done[auto_slot], stream));
     h->autos.busy[auto_slot] = true;
     h->autos.ev_cand[auto_slot] = auto_cand;
     h->autos.next = (auto_slot + 1) % kAutoRing;
@@ -1041,9 +1058,9 @@ int moe_stage_destroy(moe_stage_t h) {
   for (hipEvent_t ev : {h->stage_free[0], h->stage_free[1], h->ev_fork, h->ev_join_c, h->ev_join_p,
                         h->ev_done})
     if (ev) (void)hipEventDestroy(ev);
-  for (auto& pair : h->autos.ev)
-    for (hipEvent_t ev : pair)
-      if (ev) (void)hipEventDestroy(ev);
+  for (hipEvent_t ev : h->autos.done)
+    if (ev) (void)hipEventDestroy(ev);
+  if (h->autos.stamps) (void)hipHostFree(h->autos.stamps);
   for (const auto& q : h->queues) {
     (void)hipStreamDestroy(q.cons);
     if (q.prod) (void)hipStreamDestroy(q.prod);

@@ -921,6 +921,21 @@ hipError_t launch_tail(const TailArgs& a, int grid, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Writes the GPU's 100 MHz real-time counter to *dst (pinned host memory) when the stream
+// reaches it: the adaptive split times its candidates with a pair of these, not with timing
+// events recorded inside the runs it measures.
+__global__ void stamp_kernel(uint64_t* dst) {
+  if (threadIdx.x == 0) {
+    *dst = ticks();
+    __threadfence_system();
+  }
+}
+
+hipError_t launch_stamp(uint64_t* dst, hipStream_t s) {
+  hipLaunchKernelGGL(stamp_kernel, dim3(1), dim3(64), 0, s, dst);
+  return hipGetLastError();
+}
+
 hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s) {
   hipLaunchKernelGGL(scatter_kernel, dim3(grid), dim3(256), 0, s, a);
   return hipGetLastError();

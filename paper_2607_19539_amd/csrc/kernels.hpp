@@ -105,6 +105,8 @@ hipError_t launch_consumer(const ConsumerArgs& a, int grid, hipStream_t s);
 // Split tail tiles of a kModeDeferTail down launch: one accumulator block of one tile per pass.
 hipError_t launch_tail(const TailArgs& a, int grid, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s);
+// One 100 MHz real-time counter reading into *dst (host-visible memory) in stream order.
+hipError_t launch_stamp(uint64_t* dst, hipStream_t s);
 // Resident producer workgroups per compute unit.
 int producer_blocks_per_cu();
 constexpr int kProducerThreads = 256;

@@ -297,7 +297,7 @@ def test_auto_cu_split_settles_and_keeps_results():
     compare(fixed, ref)
     seen = set()
     with make_stage(wl, flags=B.MOE_LOCAL_DIRECT | B.MOE_SHARED_CUS) as st:
-        for i in range(16):
+        for i in range(20):
             out, stats = run_overlapped(dw, st, cu_split=0)   # synchronises: every run measured
             seen.add(stats["consumer_cus"])
             for a, b in zip(out, fixed):
@@ -308,7 +308,7 @@ def test_auto_cu_split_settles_and_keeps_results():
     # A reserved partition takes its CUs from the producer: the candidates stay small.
     seen = set()
     with make_stage(wl, flags=B.MOE_LOCAL_DIRECT) as st:
-        for i in range(16):
+        for i in range(20):
             out, stats = run_overlapped(dw, st, cu_split=0)
             seen.add(stats["consumer_cus"])
             for a, b in zip(out, fixed):
