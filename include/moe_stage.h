@@ -184,9 +184,9 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out);
  * cu_split: compute units for the consumer, 1 <= cu_split <= CUs - XCDs, or 0 to let the
  * handle choose (a runtime-adaptive selector, the paper's Section 5 future work): it measures
  * the stage time of its own runs at consumer splits of 32, 96, 160 and 248 CUs under
- * MOE_SHARED_CUS (8, 16, 32 and 64 without it), the candidates taking turns run by run until
- * each has four finished runs (the first a warm-up), skipping any above CUs - XCDs, then keeps
- * the one with the lowest median (stats: auto_cu_split).
+ * MOE_SHARED_CUS (8, 16, 32 and 64 without it), one after another and each with only its own
+ * CU-masked queue alive, four finished runs each (the first a warm-up), skipping any above
+ * CUs - XCDs, then keeps the one with the lowest median (stats: auto_cu_split).
  * Results do not depend on the split.  Workgroups
  * are dealt round-robin over the XCDs (8 on MI355X) and a CU-masked queue must own
  * CUs on each of them, so the split is rounded up to a multiple of the XCD count

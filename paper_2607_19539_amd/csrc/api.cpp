@@ -509,26 +509,21 @@ int auto_split(const moe_stage_s* h, int i) {
   return (h->cfg.flags & MOE_SHARED_CUS) ? kAutoSplitsShared[i] : kAutoSplitsPartitioned[i];
 }
 
-// The split of the next auto run: the candidates take turns, run by run, so each is measured
-// under the same conditions (the same CU-masked queues alive, the same GPU state) rather than
-// the last one beside the most queues; once each has 1 + kAutoSamples finished runs, the one
-// with the lowest median stage time over all but its first (a warm-up of its queue) is kept.
-// Returns the candidate index.
+// The split of the next auto run: the candidates are measured one after another, each alone
+// (its CU-masked queue is the only one the handle keeps, as in the steady state it is chosen
+// for: live queues of other splits slow the stage by amounts that differ from split to split),
+// 1 + kAutoSamples finished runs each; the one with the lowest median stage time over all but
+// its first (which pays for the new queue) is kept.  Returns the candidate index.
 int pick_auto(moe_stage_s* h) {
   AutoSplit& a = h->autos;
   if (a.chosen >= 0) return a.chosen;
   auto valid = [&](int c) { return auto_split(h, c) <= h->num_cus - h->n_xcd; };
-  bool measured = true, any = false;
-  for (int c = 0; c < kNumAutoSplits; ++c) {
-    any |= valid(c);
-    if (valid(c) && (int)a.ms[c].size() < 1 + kAutoSamples) measured = false;
-  }
+  bool any = false;
+  for (int c = 0; c < kNumAutoSplits; ++c) any |= valid(c);
   if (!any) return 0;  // no candidate fits this GPU: the run reports the split as unsupported
-  if (!measured) {
-    do a.cand = (a.cand + 1) % kNumAutoSplits;
-    while (!valid(a.cand));
-    return a.cand;
-  }
+  while (a.cand < kNumAutoSplits && (!valid(a.cand) || (int)a.ms[a.cand].size() >= 1 + kAutoSamples))
+    ++a.cand;
+  if (a.cand < kNumAutoSplits) return a.cand;
   float best = 0.f;
   for (int c = 0; c < kNumAutoSplits; ++c) {
     if (!valid(c)) continue;
@@ -571,7 +566,7 @@ void release_other_queues(moe_stage_s* h, int keep) {
 }
 
 // Makes the consumer queue of split c (and its producer queue where the run needs one)
-// current.  keep_others: leave other splits' queues alive (the adaptive selector's candidates).
+// current.  keep_others: leave other splits' queues alive.
 int ensure_streams(moe_stage_s* h, int c, bool need_prod, bool keep_others) {
   const bool shared = (h->cfg.flags & MOE_SHARED_CUS) != 0;
   if (!keep_others && (h->queues.size() > 1 || (h->queues.size() == 1 && h->queues[0].c != c)))
@@ -739,7 +734,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   const bool legacy = stream == nullptr || stream == hipStreamLegacy;
   const bool on_caller = shared && !legacy;
   // The adaptive selector keeps its candidates' queues until it has settled.
-  int rc = ensure_streams(h, c_eff, !on_caller, autosplit && h->autos.chosen < 0);
+  int rc = ensure_streams(h, c_eff, !on_caller, false);
   if (rc) return rc;
   BlobLayout lay{};
   TimingRec* tr = timing_slot(h);
