@@ -129,8 +129,8 @@ struct moe_stage_s {
   // split's pair.  Partitioned runs give each split a producer queue on the complementary
   // mask; with shared CUs one every-CU producer queue serves every split, made only when a
   // run needs it (a caller on the legacy null stream).  Every hardware queue a process keeps
-  // costs: past a few dozen the scheduler time-slices them and every kernel slows down, so a
-  // manual split keeps only its own pair.
+  // costs: past a few dozen the scheduler time-slices them and every kernel slows down, and even
+  // a few idle ones slow the stage, so a handle keeps only the current split's pair.
   struct SplitQueues {
     int c;
     hipStream_t cons, prod;  // prod: partitioned runs only
@@ -566,11 +566,10 @@ void release_other_queues(moe_stage_s* h, int keep) {
 }
 
 // Makes the consumer queue of split c (and its producer queue where the run needs one)
-// current.  keep_others: leave other splits' queues alive.
-int ensure_streams(moe_stage_s* h, int c, bool need_prod, bool keep_others) {
+// current, releasing every other split's queues: live CU-masked queues slow the stage.
+int ensure_streams(moe_stage_s* h, int c, bool need_prod) {
   const bool shared = (h->cfg.flags & MOE_SHARED_CUS) != 0;
-  if (!keep_others && (h->queues.size() > 1 || (h->queues.size() == 1 && h->queues[0].c != c)))
-    release_other_queues(h, c);
+  if (h->queues.size() > 1 || (h->queues.size() == 1 && h->queues[0].c != c)) release_other_queues(h, c);
   moe_stage_s::SplitQueues* cur = nullptr;
   for (auto& q : h->queues)
     if (q.c == c) cur = &q;
@@ -734,7 +733,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   const bool legacy = stream == nullptr || stream == hipStreamLegacy;
   const bool on_caller = shared && !legacy;
   // The adaptive selector keeps its candidates' queues until it has settled.
-  int rc = ensure_streams(h, c_eff, !on_caller, false);
+  int rc = ensure_streams(h, c_eff, !on_caller);
   if (rc) return rc;
   BlobLayout lay{};
   TimingRec* tr = timing_slot(h);
