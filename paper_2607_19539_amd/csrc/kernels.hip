@@ -790,8 +790,8 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
           expired = true;
           break;
         }
-        // Exponential backoff: a wave that waits through the whole gate/up launch polls
-        // a few times per microsecond at most, instead of flooding L2 with flag loads.
+        // Exponential backoff: a wave that waits through the whole gate/up launch settles at
+        // one poll every 2.5 us or so, instead of flooding L2 with flag loads.
         for (uint32_t i = 0; i < backoff; ++i) __builtin_amdgcn_s_sleep(kPollSleep);
         backoff = backoff < kPollBackoffMax ? 2 * backoff : kPollBackoffMax;
       }
