@@ -368,7 +368,7 @@ def main():
     t_start = time.time()
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the return all-to-all is modelled by "
+        print(json.dumps({"error": "the expert stage runs on one GPU: the return all-to-all is modelled by "
                                    "copies into per-source-rank buffers in local HBM; --gpus must be 1"}))
         sys.exit(2)
     import torch
