@@ -9,11 +9,17 @@ buffers) are resident in HBM before the timed region; the routing arrays are
 host inputs by design of the C ABI, so each step re-validates and re-uploads
 the plan.
 
-Prints one JSON line.  ``value`` is the stage's algorithmic bf16 throughput
-(6*H*F flops per routed row, padding excluded) in TFLOP/s on the headline
-workload; ``ms_per_step`` is its expert-stage time; ``overlap_speedup`` is
-serial time / overlapped time.  ``workloads`` holds the same figures and the
-consumer CU-split sweep (both CU modes) for every workload measured.
+The LAST stdout line is one compact JSON object (the headline: ``value`` is the
+stage's algorithmic bf16 throughput, 6*H*F flops per routed row, padding
+excluded, in TFLOP/s on the headline workload; ``ms_per_step`` its expert-stage
+time; ``overlap_speedup`` serial / overlapped; ``roofline`` the gate/up launch
+against the bf16 dense peak; ``cpu_baseline`` the CPU oracle).  Everything else
+-- per-workload serial / overlapped / device-planned / ablation timings, the
+consumer CU-split sweep in both CU modes and both segment sizes, the consumer
+copy ceiling, the overlap ratio and flag latencies from in-kernel timestamps,
+the compute units each kernel ran on, the band_rows = 256 layout and the
+expert-count sweep -- goes to the ``--detail-out`` JSON file, which earlier
+stdout lines name.
 """
 from __future__ import annotations
 
@@ -35,6 +41,7 @@ if ROOT not in sys.path:
 METRIC = "MoE expert-stage µs + bf16 MFMA TFLOP/s vs peak; overlap speedup vs serial"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA peak
 PEAK_HBM_GBS = 8000.0
+TICK_US = 0.01              # the GPU wall clock runs at 100 MHz
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_19539_amd", "csrc", "kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "producer_mixtral_traffic.md")
 
@@ -56,40 +63,56 @@ def log(msg):
 
 
 def parse():
-    ap = argparse.ArgumentParser(description=__doc__)
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=30)
+    ap.add_argument("--warm-s", type=float, default=1.5,
+                    help="warm-up time floor of the headline timings (after --warmup steps, runs continue until "
+                         "this many seconds have passed, so the clocks have settled whatever --warmup is)")
+    ap.add_argument("--warm-s-other", type=float, default=0.4, help="the same floor for every other timing")
     ap.add_argument("--workload", default="mixtral", choices=sorted(DESCRIPTIONS), help="headline workload")
-    ap.add_argument("--extra-workloads", default="mixtral_zipf,fine,large_fine",
-                    help="further workloads measured into 'workloads' ('' = none)")
+    ap.add_argument("--extra-workloads", default="tiny,mixtral_zipf,fine,large_fine",
+                    help="further workloads measured into the detail file ('' = none)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cu-split", type=int, default=248, help="consumer compute units")
+    ap.add_argument("--cu-split", type=int, default=248, help="consumer compute units of the headline path")
     ap.add_argument("--mode", choices=["shared", "partitioned"], default="shared",
                     help="shared: the producer keeps every CU and the consumer runs beside it on its "
                          "cu_split CUs; partitioned: the consumer's CUs are reserved for it")
     ap.add_argument("--band-rows", type=int, default=0, help="tb_M of the row layout (0 = 1, no alignment)")
     ap.add_argument("--split-k", type=int, default=0, help="K parts per down tile (0 = library default)")
     ap.add_argument("--mgb", type=int, default=1, help="tile-row pieces per middle transfer segment")
+    ap.add_argument("--small", default="8,16,24,32",
+                    help="small consumer partitions (paper's range): measured in both CU modes and mgb 1 and 2")
+    ap.add_argument("--sweep", default="64,128,248", help="further shared-CU splits of the sweep")
     ap.add_argument("--copy-curve", default="8,16,32,64,128",
                     help="consumer CU counts for the consumer-only copy ceiling ('' to skip)")
-    ap.add_argument("--sweep", default="8,16,32,64,128,248",
-                    help="CU splits for the overlap-speedup sweep: shared CUs at each, a reserved "
-                         "partition at those up to 64 ('' = none)")
     ap.add_argument("--esweep", default="4,8,16,32,64",
                     help="experts per rank for the single-layer expert-count sweep ('' to skip)")
     ap.add_argument("--only", choices=["all", "serial", "overlapped"], default="all",
-                    help="run only one path of the headline workload (counter collection)")
+                    help="time only one path of the headline workload (profiler runs)")
+    ap.add_argument("--detail-out", default=os.path.join("gpurun_out", "bench_detail.json"))
     ap.add_argument("--esweep-child", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     return ap.parse_args()
 
 
-def cpu_baseline(wl, target_s):
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, target_s, threads=None):
     """Time the CPU oracle on a bounded sample of the workload's routed rows."""
     from oracle import oracle as orc
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    if threads is None:
+        threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     o = orc.get()
 
     def run(n):
@@ -107,8 +130,9 @@ def cpu_baseline(wl, target_s):
     n, dt = run(n)
     flops = 6.0 * wl.H * wl.F * n
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} of {wl.rows} routed rows ({n / wl.rows:.1%}), {dt:.1f} s wall; full stage "
-                      f"would take ~{dt * wl.rows / n:.0f} s on these cores"}
+            "cpu_model": cpu_model(),
+            "sample": f"{n} of {wl.rows} routed rows ({n / wl.rows:.1%}) of {wl.name}, {dt:.1f} s wall; the full "
+                      f"stage would take ~{dt * wl.rows / n:.0f} s on these cores"}
 
 
 def stored_traffic():
@@ -126,8 +150,79 @@ def stored_traffic():
     return float(m_b.group(1)) if cur == m_h.group(1) else None
 
 
+def union_length(iv):
+    """Total length of the union of intervals [(a, b)], and the sorted disjoint pieces."""
+    pieces = []
+    for a, b in sorted(iv):
+        if pieces and a <= pieces[-1][1]:
+            pieces[-1][1] = max(pieces[-1][1], b)
+        else:
+            pieces.append([a, b])
+    return sum(b - a for a, b in pieces), pieces
+
+
+def cu_key(hw_id, xcc):
+    """A compute unit's identity from the HW_ID register (CU, shader array, shader engine) and XCD."""
+    return (int(xcc) & 0xF, (int(hw_id) >> 8) & 0xFF)
+
+
+def overlap_analysis(B, stg, wl):
+    """Overlap of the return copy with the expert compute (paper Section 4.2.2, Fig. 5b) from the
+    last run's in-kernel timestamps: the share of the consumer's busy time (the union of its copy
+    intervals) that lies inside the producer's span, the copy time left after the producer ended,
+    how long each segment waited after its last flag was raised before a wave saw it, and where
+    each kernel's workgroups ran."""
+    span = stg.records(B.MOE_RECORDS_SPAN)[0]
+    cp = stg.records(B.MOE_RECORDS_COPY)
+    wg = stg.records(B.MOE_RECORDS_PRODUCER)
+    tiles = stg.records(B.MOE_RECORDS_TILES)
+    segs = stg.plan()["segments"]          # dst, rows, y_row0, slot0, flag_begin, flag_count, ready_pos, npieces
+    p0, p1 = int(span["producer_start"]), int(span["producer_end"])
+    out = {"copy_units": int(span["copy_units"]), "recorded": int(len(cp))}
+    if len(cp) == 0 or p1 <= p0:
+        return out
+    busy, pieces = union_length(list(zip(cp["t_ready"].astype(np.int64), cp["t_done"].astype(np.int64))))
+    hidden = sum(max(0, min(b, p1) - max(a, p0)) for a, b in pieces)
+    t_end = int(cp["t_done"].max())
+    nbytes = 4.0 * wl.H * float(segs[:, 1].sum())
+    lag, deliver = [], []
+    for s in range(len(segs)):
+        m = cp["segment"] == s
+        if not m.any():
+            continue
+        fb, fc = int(segs[s, 4]), int(segs[s, 5])
+        t_flag = int(tiles[fb:fb + fc].max()) if fc else 0
+        if t_flag:
+            lag.append((int(cp["t_ready"][m].min()) - t_flag) * TICK_US)
+            deliver.append((int(cp["t_done"][m].max()) - t_flag) * TICK_US)
+    cons_cu = {cu_key(h, x) for h, x in zip(cp["hw_id"], cp["xcc_id"])}
+    grid = int(span["producer_grid"])
+    prod_cu = {cu_key(h, x) for h, x in zip(wg["hw_id"][grid:], wg["xcc_id"][grid:])}
+    per_cu = {}
+    for h, x in zip(wg["hw_id"][grid:], wg["xcc_id"][grid:]):
+        per_cu[cu_key(h, x)] = per_cu.get(cu_key(h, x), 0) + 1
+    out.update({
+        "producer_span_us": (p1 - p0) * TICK_US,
+        "consumer_busy_us": busy * TICK_US,
+        "overlap_ratio": hidden / busy if busy else None,
+        "exposed_copy_us": max(0, t_end - p1) * TICK_US,
+        "consumer_GBps_while_busy": nbytes / (busy * TICK_US * 1e-6) / 1e9 if busy else None,
+        "copy_bytes": nbytes,
+        "flag_to_copy_start_us_p50_p90_max": [round(float(np.percentile(lag, q)), 2) for q in (50, 90, 100)] if lag else None,
+        "flag_to_delivered_us_p50_p90_max": [round(float(np.percentile(deliver, q)), 2) for q in (50, 90, 100)]
+        if deliver else None,
+        "segments_timed": len(lag),
+        "consumer_cus_used": len(cons_cu),
+        "producer_down_cus_used": len(prod_cu),
+        "producer_down_workgroups_per_cu_max": max(per_cu.values()) if per_cu else 0,
+        "consumer_cus_shared_with_producer": len(cons_cu & prod_cu),
+    })
+    return out
+
+
 class Bench:
-    """One workload resident on the GPU, with a handle per CU mode on a dedicated stream."""
+    """One workload resident on the GPU.  Handles are created per measurement and closed right
+    after it: every live handle keeps CU-masked hardware queues, and idle queues slow the stage."""
 
     def __init__(self, torch, B, wl, args):
         self.torch, self.B, self.wl, self.args = torch, B, wl, args
@@ -139,97 +234,122 @@ class Bench:
         self.bufs = [torch.zeros((int(n), wl.H), dtype=torch.int16, device="cuda") for n in wl.return_rows]
         self.run_args = (self.x, wl.expert_offsets, wl.row_src_rank, wl.row_slot, self.w1, self.w3, self.w2,
                          self.bufs, wl.return_rows)
-        # The same routing resident on the device, for the device-planned runs.
         d_routing = [torch.from_numpy(np.ascontiguousarray(a, np.int32)).cuda()
                      for a in (wl.expert_offsets, wl.row_src_rank, wl.row_slot)]
         self.dev_run_args = (self.x, *d_routing, self.w1, self.w3, self.w2, self.bufs, wl.return_rows)
-        self.base_flags = B.MOE_LOCAL_DIRECT | B.MOE_KERNEL_TIMING
-        extra = {"shared": B.MOE_SHARED_CUS, "partitioned": 0, "direct": B.MOE_DIRECT_ALL}
-        self.stages = {m: self.make_stage(f, args.mgb) for m, f in extra.items()}
-        # The same CU modes without per-kernel events: the events a timed handle records inside
-        # every run (eight on two queues) cost the overlapped stage ~1%, so the stage time is
-        # taken from these, and kernel durations from the timed handles.
-        for m in ("shared", "partitioned"):
-            self.stages[m + ":plain"] = self.make_stage(extra[m], args.mgb, timing=False)
         torch.cuda.synchronize()
         # The stage runs on a stream of its own, as in a serving loop (on the legacy null stream
         # the shared-CU producer would have to fork to a second queue; see moe_stage_run).
         self.stream = torch.cuda.Stream()
         self.timeouts = []
 
-    def make_stage(self, flags, mgb, timing=True):
-        wl, args = self.wl, self.args
-        base = self.base_flags if timing else self.base_flags & ~self.B.MOE_KERNEL_TIMING
-        return self.B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows, args.band_rows, mgb,
-                               base | flags, 0, args.split_k)
+    def handle(self, mode, mgb=None, timing=False, extra=0, band_rows=None):
+        B, wl, args = self.B, self.wl, self.args
+        flags = B.MOE_LOCAL_DIRECT | extra | {"shared": B.MOE_SHARED_CUS, "partitioned": 0, "direct": B.MOE_DIRECT_ALL}[mode]
+        if timing:
+            flags |= B.MOE_KERNEL_TIMING
+        return B.MoeStage(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, wl.rows,
+                          args.band_rows if band_rows is None else band_rows, mgb or args.mgb, flags, 0, args.split_k)
 
-    def stage(self, mode, mgb):
-        """Event-free handle of a CU mode and mid-segment piece count (created on first use)."""
-        key = f"{mode}:plain" if mgb == self.args.mgb else f"{mode}:mgb{mgb}:plain"
-        if key not in self.stages:
-            f = {"shared": self.B.MOE_SHARED_CUS, "partitioned": 0}[mode]
-            self.stages[key] = self.make_stage(f, mgb, timing=False)
-        return key
-
-    def close(self):
-        for s in self.stages.values():
-            s.close()
-        self.torch.cuda.synchronize()
-
-    def timed(self, mode, path, cu_split, steps, warmup, device_plan=False):
-        """W untimed steps, then exactly `steps` timed steps bracketed by device synchronisation.
-        device_plan: the routing is on the device and the plan is built there."""
-        torch, stg = self.torch, self.stages[mode]
+    def fn(self, stg, path, cu_split, device_plan=False):
         if path == "serial":
-            fn = ((lambda: stg.run_serial_devplan(*self.dev_run_args, stream=self.stream)) if device_plan else
-                  (lambda: stg.run_serial(*self.run_args, stream=self.stream)))
-        else:
-            fn = ((lambda: stg.run_devplan(*self.dev_run_args, cu_split=cu_split, stream=self.stream))
-                  if device_plan else (lambda: stg.run(*self.run_args, cu_split=cu_split, stream=self.stream)))
-        for _ in range(warmup):
+            if device_plan:
+                return lambda: stg.run_serial_devplan(*self.dev_run_args, stream=self.stream)
+            return lambda: stg.run_serial(*self.run_args, stream=self.stream)
+        if device_plan:
+            return lambda: stg.run_devplan(*self.dev_run_args, cu_split=cu_split, stream=self.stream)
+        return lambda: stg.run(*self.run_args, cu_split=cu_split, stream=self.stream)
+
+    def timed(self, stg, fn, steps, warmup, warm_s):
+        """`warmup` untimed steps (continued until `warm_s` seconds have passed), then exactly
+        `steps` timed steps bracketed by device synchronisation, one event between consecutive
+        steps: the whole loop's time gives the mean, the per-step differences the median and
+        spread."""
+        torch = self.torch
+        t0 = time.perf_counter()
+        i = 0
+        while i < warmup or time.perf_counter() - t0 < warm_s:
             fn()
+            i += 1
+            if i % 16 == 0:
+                torch.cuda.synchronize()
         stg.query(check=False)
         if stg.cfg.flags & self.B.MOE_KERNEL_TIMING:
             stg.times(reset=True)
-        # A garbage-collection pass inside the timed loop stalls the host for tens of ms while
-        # the GPU idles; collect before and keep the collector off while timing.
+        # A garbage-collection pass inside the timed loop stalls the host while the GPU idles.
         gc.collect()
         gc.disable()
         torch.cuda.synchronize()
-        # One event between consecutive steps: the whole loop's time gives the mean, the
-        # per-step differences its spread (an event between steps costs no GPU time).
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
         ev[0].record(self.stream)
-        for i in range(steps):
+        for k in range(steps):
             fn()
-            ev[i + 1].record(self.stream)
+            ev[k + 1].record(self.stream)
         torch.cuda.synchronize()
         gc.enable()
-        ms = ev[0].elapsed_time(ev[steps]) / steps
-        per_step = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)])
+        per_step = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(steps)])
         st = stg.query(check=False)
         if st["rc"] != 0:
             msg = self.B.moe_stage_last_error(stg.h)
             log(f"ERROR: {msg} -- timing invalid")
             self.timeouts.append(msg)
-        tm = stg.times(reset=True) if stg.cfg.flags & self.B.MOE_KERNEL_TIMING else {
-            "runs": 0, "producer_ms": 0.0, "gate_up_ms": 0.0, "consumer_ms": 0.0, "scatter_ms": 0.0, "plan_ms": 0.0}
-        runs = max(tm["runs"], 1)
-        return {"ms": ms, "stats": st, "producer_ms": tm["producer_ms"] / runs,
-                "gate_up_ms": tm["gate_up_ms"] / runs, "consumer_ms": tm["consumer_ms"] / runs,
-                "scatter_ms": tm["scatter_ms"] / runs, "plan_ms": tm["plan_ms"] / runs,
-                "p10_ms": float(np.percentile(per_step, 10)), "p50_ms": float(np.median(per_step)),
-                "p90_ms": float(np.percentile(per_step, 90))}
+        r = {"ms": ev[0].elapsed_time(ev[steps]) / steps, "p10_ms": float(np.percentile(per_step, 10)),
+             "p50_ms": float(np.median(per_step)), "p90_ms": float(np.percentile(per_step, 90)),
+             "warmup_runs": i, "stats": st}
+        if stg.cfg.flags & self.B.MOE_KERNEL_TIMING:
+            tm = stg.times(reset=True)
+            runs = max(tm["runs"], 1)
+            for k in ("producer_ms", "gate_up_ms", "consumer_ms", "scatter_ms", "plan_ms"):
+                r[k] = tm[k] / runs
+        return r
 
-    def copy_curve(self, splits, steps, warmup):
-        """Consumer copy rate with no producer work (every flag published up front), per
-        consumer CU count: the ceiling a c-CU consumer can reach on this workload's segments."""
-        torch, B = self.torch, self.B
-        stg = self.make_stage(B.MOE_SHARED_CUS | B.MOE_TEST_CONSUMER_ONLY, self.args.mgb)
-        out = []
+    def measure(self, mode, path, cu_split, steps, warmup, warm_s, mgb=None, device_plan=False, band_rows=None):
+        """Stage time from a handle without per-kernel events (they cost the overlapped stage about
+        1 %), then kernel durations from an event-timed handle on the same configuration."""
+        stg = self.handle(mode, mgb, band_rows=band_rows)
         try:
-            for c in splits:
-                fn = lambda: stg.run(*self.run_args, cu_split=c, stream=self.stream)
+            plain = self.timed(stg, self.fn(stg, path, cu_split, device_plan), steps, warmup, warm_s)
+        finally:
+            stg.close()
+        stg = self.handle(mode, mgb, timing=True, band_rows=band_rows)
+        try:
+            ev = self.timed(stg, self.fn(stg, path, cu_split, device_plan), steps, warmup, warm_s)
+        finally:
+            stg.close()
+        r = dict(ev)
+        r["ms_with_kernel_events"] = ev["ms"]
+        for k in ("ms", "p10_ms", "p50_ms", "p90_ms", "warmup_runs"):
+            r[k] = plain[k]
+        return r
+
+    def plain(self, mode, path, cu_split, steps, warmup, warm_s, mgb=None):
+        stg = self.handle(mode, mgb)
+        try:
+            return self.timed(stg, self.fn(stg, path, cu_split), steps, warmup, warm_s)
+        finally:
+            stg.close()
+
+    def timestamps(self, mode, cu_split, warmup, warm_s, mgb=None):
+        """One timestamped overlapped run after warm-up: overlap ratio, flag latencies, placement."""
+        stg = self.handle(mode, mgb, extra=self.B.MOE_TIMESTAMPS)
+        try:
+            fn = self.fn(stg, "overlapped", cu_split)
+            self.timed(stg, fn, 5, warmup, warm_s)
+            fn()
+            stg.query(check=False)
+            return overlap_analysis(self.B, stg, self.wl)
+        finally:
+            stg.close()
+
+    def copy_curve(self, mode, splits, steps, warmup):
+        """Consumer copy rate with no producer work (every flag published up front), per consumer
+        CU count: the ceiling a c-CU consumer reaches on this workload's segments."""
+        torch, B = self.torch, self.B
+        out = []
+        for c in splits:
+            stg = self.handle(mode, timing=True, extra=B.MOE_TEST_CONSUMER_ONLY)
+            try:
+                fn = self.fn(stg, "overlapped", c)
                 for _ in range(warmup):
                     fn()
                 torch.cuda.synchronize()
@@ -239,14 +359,14 @@ class Bench:
                 torch.cuda.synchronize()
                 st = stg.query(check=False)
                 tm = stg.times(reset=True)
-                us = tm["consumer_ms"] / max(tm["runs"], 1) * 1e3
-                nbytes = 4.0 * self.wl.H * st["n_remote_rows"]
-                out.append({"cu_split": c, "consumer_cus": st["consumer_cus"], "us": us,
-                            "bytes": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9, "rc": st["rc"]})
-        finally:
-            stg.close()
+            finally:
+                stg.close()
+            us = tm["consumer_ms"] / max(tm["runs"], 1) * 1e3
+            nbytes = 4.0 * self.wl.H * st["n_remote_rows"]
+            out.append({"cu_split": c, "mode": mode, "consumer_cus": st["consumer_cus"], "units": st["copy_units"],
+                        "us": us, "bytes": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9,
+                        "frac_of_hbm_peak": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, "rc": st["rc"]})
         return out
-
 
     def timed_combine(self, steps, warmup):
         """The weighted combine of this rank's own tokens (k returned rows each) from its receive
@@ -284,84 +404,252 @@ def down_kernel_name(split_k, st):
     return f"moe::producer_kernel<true, {split_k if split_k <= 4 else 0}> (down launch, {split_k} K parts)"
 
 
-def with_plain_times(timed_r, plain_r):
-    """Kernel durations and stats from the event-timed handle, stage times from the plain one."""
-    r = dict(timed_r)
-    r["ms_with_kernel_events"] = timed_r["ms"]
-    for k in ("ms", "p10_ms", "p50_ms", "p90_ms"):
-        r[k] = plain_r[k]
-    return r
-
-
-def summarize(wl, ser, ovl, sweep):
-    """Per-workload figures: stage times, producer launches, throughput against the bf16 peak."""
+def path_summary(wl, r, serial):
     flops = wl.flops()
-    out = {"routed_rows": wl.rows, "gflop": flops / 1e9}
-    for key, r in (("serial", ser), ("overlapped", ovl)):
-        if r is None:
-            continue
-        gu = r["gate_up_ms"]
-        dn = r["producer_ms"] - gu
-        out[key] = {"stage_us": r["ms"] * 1e3, "tflops": flops / (r["ms"] * 1e-3) / 1e12,
-                    "stage_us_with_kernel_events": r.get("ms_with_kernel_events", r["ms"]) * 1e3,
-                    "step_us_p10_p50_p90": [round(r["p10_ms"] * 1e3, 1), round(r["p50_ms"] * 1e3, 1),
-                                            round(r["p90_ms"] * 1e3, 1)],
-                    "producer_us": r["producer_ms"] * 1e3, "gate_up_us": gu * 1e3, "down_us": dn * 1e3,
-                    "producer_frac_of_peak": flops / (r["producer_ms"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
-        if key == "serial":
-            out[key]["scatter_us"] = r["scatter_ms"] * 1e3
-        else:
-            out[key]["consumer_us"] = r["consumer_ms"] * 1e3
-    if ser is not None and ovl is not None:
-        out["overlap_speedup"] = ser["ms"] / ovl["ms"]
-    if sweep:
-        out["cu_split_sweep"] = sweep
+    gu = r["gate_up_ms"]
+    dn = r["producer_ms"] - gu
+    out = {"stage_us": r["ms"] * 1e3, "tflops": flops / (r["ms"] * 1e-3) / 1e12,
+           "stage_us_median": r["p50_ms"] * 1e3,
+           "stage_us_with_kernel_events": r["ms_with_kernel_events"] * 1e3,
+           "step_us_p10_p50_p90": [round(r["p10_ms"] * 1e3, 1), round(r["p50_ms"] * 1e3, 1), round(r["p90_ms"] * 1e3, 1)],
+           "warmup_runs": r["warmup_runs"],
+           "producer_us": r["producer_ms"] * 1e3, "gate_up_us": gu * 1e3, "down_us": dn * 1e3,
+           "gate_up_frac_of_peak": 4.0 * wl.H * wl.F * wl.rows / (gu * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+           "down_frac_of_peak": 2.0 * wl.H * wl.F * wl.rows / (dn * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+           "producer_frac_of_peak": flops / (r["producer_ms"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+           "workgroups_gate_up_down": [int(r["stats"]["gu_workgroups"]), int(r["stats"]["down_workgroups"])]}
+    if serial:
+        out["scatter_us"] = r["scatter_ms"] * 1e3
+    else:
+        out["consumer_us"] = r["consumer_ms"] * 1e3
+        out["copy_units"] = int(r["stats"]["copy_units"])
     return out
 
 
-def expert_count_sweep(torch, B, make_workload, args, counts, timeouts):
-    """Single-layer sweep over experts per rank (paper Section 4.2.2): serial and overlapped
-    stage times, the split the adaptive selector (cu_split = 0) settles on, and the overlap
-    ratio -- the share of the consumer's stand-alone copy time hidden behind the producer:
-    1 - (overlapped stage - serial producer) / consumer-only copy time, clamped to [0, 1]."""
+def measure_workload(torch, B, wl, args, headline):
+    """Every figure of one workload; returns (detail dict, raw results of the headline paths)."""
+    bench = Bench(torch, B, wl, args)
+    name = wl.name
+    steps = args.steps if headline else max(args.steps, 20)
+    warmup = args.warmup
+    warm_s = args.warm_s if headline else args.warm_s_other
+    wo = args.warm_s_other
+    d = {"description": DESCRIPTIONS[name], "routed_rows": wl.rows, "gflop": wl.flops() / 1e9}
+    only = args.only if headline else "all"
+    raw = {}
+    try:
+        ser = ovl = None
+        if only in ("all", "serial"):
+            ser = bench.measure(args.mode, "serial", 0, steps, warmup, warm_s)
+            d["serial"] = path_summary(wl, ser, True)
+            log(f"{name} serial: {ser['ms'] * 1e3:.1f} us (median {ser['p50_ms'] * 1e3:.1f}; producer "
+                f"{ser['producer_ms'] * 1e3:.1f}, gate/up {ser['gate_up_ms'] * 1e3:.1f}, scatter "
+                f"{ser['scatter_ms'] * 1e3:.1f})")
+        if only in ("all", "overlapped"):
+            ovl = bench.measure(args.mode, "overlapped", args.cu_split, steps, warmup, warm_s)
+            d["overlapped"] = path_summary(wl, ovl, False)
+            d["overlapped"]["config"] = {"cu_split": args.cu_split, "cu_mode": args.mode, "mgb": args.mgb,
+                                         "consumer_cus": int(ovl["stats"]["consumer_cus"])}
+            st = ovl["stats"]
+            log(f"{name} overlapped ({args.mode}, c={args.cu_split}): {ovl['ms'] * 1e3:.1f} us (median "
+                f"{ovl['p50_ms'] * 1e3:.1f}; producer {ovl['producer_ms'] * 1e3:.1f}, gate/up "
+                f"{ovl['gate_up_ms'] * 1e3:.1f}, consumer {ovl['consumer_ms'] * 1e3:.1f}); segments "
+                f"{st['n_segments']}, units {st['copy_units']}, workgroups {st['gu_workgroups']}/{st['down_workgroups']}")
+        raw = {"serial": ser, "overlapped": ovl}
+        if ser is not None and ovl is not None:
+            d["overlap_speedup"] = ser["ms"] / ovl["ms"]
+            d["overlap_speedup_median"] = ser["p50_ms"] / ovl["p50_ms"]
+        if only != "all":
+            return d, raw
+        ts = bench.timestamps(args.mode, args.cu_split, warmup, wo)
+        d["overlapped"]["timestamps"] = ts
+        raw["timestamps"] = ts
+        log(f"{name} timestamps: overlap ratio {ts.get('overlap_ratio')}, exposed copy {ts.get('exposed_copy_us')} us, "
+            f"flag->copy start p50/p90/max {ts.get('flag_to_copy_start_us_p50_p90_max')} us, consumer CUs "
+            f"{ts.get('consumer_cus_used')}, producer CUs {ts.get('producer_down_cus_used')}")
+        dp = bench.measure(args.mode, "overlapped", args.cu_split, steps, warmup, wo, device_plan=True)
+        d["device_plan"] = {"stage_us": dp["ms"] * 1e3, "planner_gpu_us": dp["plan_ms"] * 1e3,
+                            "host_plan_host_us": ovl["stats"]["plan_us"],
+                            "host_plan_upload_gpu_us": ovl["plan_ms"] * 1e3}
+        log(f"{name} overlapped, device-built plan: {dp['ms'] * 1e3:.1f} us (planner {dp['plan_ms'] * 1e3:.1f} us)")
+        direct = bench.measure("direct", "serial", 0, steps, warmup, wo)
+        d["epilogue_direct_ablation_us"] = direct["ms"] * 1e3
+        log(f"{name} epilogue-direct ablation: {direct['ms'] * 1e3:.1f} us")
+        # The paper's single-destination layout: every 256-row band belongs to one source rank.
+        b256 = bench.handle(args.mode, band_rows=256)
+        try:
+            r = bench.timed(b256, bench.fn(b256, "overlapped", args.cu_split), steps, warmup, wo)
+        finally:
+            b256.close()
+        d["band_rows_256"] = {"stage_us": r["ms"] * 1e3, "stage_us_median": r["p50_ms"] * 1e3,
+                              "padding_rows": int(r["stats"]["n_band_padding"]),
+                              "tile_rows": int(r["stats"]["n_tile_rows"]),
+                              "vs_default_band_rows": ovl["ms"] / r["ms"]}
+        log(f"{name} band_rows=256: {r['ms'] * 1e3:.1f} us, {r['stats']['n_band_padding']} padding rows, "
+            f"{r['stats']['n_tile_rows']} tile rows")
+        # Consumer CU-split sweep: the paper's small partitions in both CU modes and both segment
+        # sizes, and wider shared splits; the main configuration is re-measured first, so the sweep
+        # can be checked against it.
+        sweep = []
+        small = [int(v) for v in args.small.split(",") if v]
+        wide = [int(v) for v in args.sweep.split(",") if v]
+        points = [(args.cu_split, args.mode, args.mgb)]
+        points += [(c, m, g) for g in (1, 2) for c in small for m in ("shared", "partitioned")]
+        points += [(c, "shared", 1) for c in wide if (c, "shared", 1) not in points]
+        for c, m, g in points:
+            r = bench.plain(m, "overlapped", c, max(steps // 2, 20), warmup, wo, mgb=g)
+            sweep.append({"cu_split": c, "cu_mode": m, "mgb": g, "consumer_cus": int(r["stats"]["consumer_cus"]),
+                          "segments": int(r["stats"]["n_segments"]), "units": int(r["stats"]["copy_units"]),
+                          "stage_us": r["ms"] * 1e3, "stage_us_median": r["p50_ms"] * 1e3,
+                          "speedup_vs_serial": ser["ms"] / r["ms"],
+                          "speedup_vs_serial_median": ser["p50_ms"] / r["p50_ms"],
+                          "beats_serial": bool(r["p50_ms"] < ser["p50_ms"])})
+            log(f"{name} sweep c={c} {m} mgb={g}: {r['ms'] * 1e3:.1f} us (median {r['p50_ms'] * 1e3:.1f}), "
+                f"speedup {ser['ms'] / r['ms']:.3f}")
+        d["cu_split_sweep"] = sweep
+        d["sweep_main_agreement"] = sweep[0]["stage_us_median"] / (ovl["p50_ms"] * 1e3)
+        best = max(sweep, key=lambda x: x["speedup_vs_serial_median"])
+        d["best_sweep_point"] = {k: best[k] for k in ("cu_split", "cu_mode", "mgb", "stage_us_median",
+                                                      "speedup_vs_serial_median")}
+        smalls = [x for x in sweep if x["cu_split"] <= 32]
+        bs = max(smalls, key=lambda x: x["speedup_vs_serial_median"]) if smalls else None
+        if bs:
+            d["best_small_partition"] = {k: bs[k] for k in ("cu_split", "cu_mode", "mgb", "stage_us_median",
+                                                            "speedup_vs_serial_median")}
+            ts_small = bench.timestamps(bs["cu_mode"], bs["cu_split"], warmup, wo, mgb=bs["mgb"])
+            d["best_small_partition"]["timestamps"] = ts_small
+        if args.copy_curve:
+            cs = [int(v) for v in args.copy_curve.split(",")]
+            d["consumer_copy_ceiling"] = bench.copy_curve("partitioned", cs, 10, 3) + bench.copy_curve("shared", cs, 10, 3)
+            for r in d["consumer_copy_ceiling"]:
+                log(f"{name} consumer-only copy c={r['cu_split']} {r['mode']}: {r['us']:.1f} us, {r['GBps']:.0f} GB/s "
+                    f"({r['units']} units)")
+        d["combine"] = bench.timed_combine(max(steps, 20), max(warmup, 5))
+        log(f"{name} combine ({wl.T_r} tokens, k={wl.k}): {d['combine']['us']:.1f} us, {d['combine']['GBps']:.0f} GB/s")
+        return d, raw
+    finally:
+        if bench.timeouts:
+            d["watchdog"] = bench.timeouts
+        del bench
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+
+def expert_count_sweep(torch, B, make_workload, args, counts):
+    """Single-layer sweep over experts per rank (paper Section 4.2.2): serial and overlapped stage
+    times, the split the adaptive selector (cu_split = 0) settles on, and the overlap ratio from the
+    in-kernel timestamps of a run at that split (share of the consumer's copy time inside the
+    producer's span)."""
     rows = []
     for E in counts:
         name = f"layer_e{E}"
         log(f"generating workload {name} seed {args.seed}")
         wl = make_workload(name, seed=args.seed)
         bench = Bench(torch, B, wl, args)
-        steps, warmup = max(args.steps // 2, 10), max(args.warmup // 2, 5)
-        # Stage times and the selector run on a handle without per-kernel events (those events
-        # slow some consumer splits down, which would steer the selector); the event-timed
-        # handle gives only the serial producer time of the overlap ratio.
-        ser_t = bench.timed("shared", "serial", 0, steps, warmup)
-        ser = bench.timed("shared:plain", "serial", 0, steps, warmup)
-        # Let the adaptive selector finish measuring its candidates before timing.
-        stg = bench.stages["shared:plain"]
-        for i in range(160):
-            stg.run(*bench.run_args, cu_split=0, stream=bench.stream)
-            if i % 4 == 3:
-                torch.cuda.synchronize()
-                if stg.query(check=False)["auto_cu_split"] > 0:
-                    break
-        ovl = bench.timed("shared:plain", "overlapped", 0, steps, warmup)
-        st = ovl["stats"]
-        c = st["consumer_cus"]
-        curve = bench.copy_curve([c], 10, 3)[0]
-        t_o, t_p, t_c = ovl["ms"] * 1e3, ser_t["producer_ms"] * 1e3, curve["us"]
-        ratio = min(max(1.0 - (t_o - t_p) / t_c, 0.0), 1.0) if t_c > 0 else None
+        steps, warmup, wo = max(args.steps, 20), args.warmup, args.warm_s_other
+        ser = bench.plain("shared", "serial", 0, steps, warmup, wo)
+        stg = bench.handle("shared")
+        try:
+            # Let the adaptive selector finish measuring its candidates, then time it.
+            for i in range(200):
+                stg.run(*bench.run_args, cu_split=0, stream=bench.stream)
+                if i % 4 == 3:
+                    torch.cuda.synchronize()
+                    if stg.query(check=False)["auto_cu_split"] > 0:
+                        break
+            ovl = bench.timed(stg, bench.fn(stg, "overlapped", 0), steps, warmup, wo)
+        finally:
+            stg.close()
+        c = int(ovl["stats"]["auto_cu_split"])
+        ts = bench.timestamps("shared", c, warmup, wo)
         rows.append({"experts_per_rank": E, "routed_rows": wl.rows, "serial_us": ser["ms"] * 1e3,
-                     "overlapped_us": t_o, "speedup": ser["ms"] / ovl["ms"], "serial_producer_us": t_p,
-                     "consumer_only_copy_us": t_c, "overlap_ratio": ratio,
-                     "auto_cu_split": st["auto_cu_split"], "consumer_cus": c,
+                     "overlapped_us": ovl["ms"] * 1e3, "speedup": ser["ms"] / ovl["ms"],
+                     "speedup_median": ser["p50_ms"] / ovl["p50_ms"], "auto_cu_split": c,
+                     "overlap_ratio": ts.get("overlap_ratio"), "exposed_copy_us": ts.get("exposed_copy_us"),
+                     "consumer_busy_us": ts.get("consumer_busy_us"),
                      "tflops_overlapped": wl.flops() / (ovl["ms"] * 1e-3) / 1e12})
-        log(f"{name}: serial {ser['ms'] * 1e3:.1f} us, overlapped {t_o:.1f} us (auto c={st['auto_cu_split']}), "
-            f"speedup {ser['ms'] / ovl['ms']:.3f}, overlap ratio {ratio if ratio is None else round(ratio, 3)}")
-        timeouts += bench.timeouts
-        bench.close()
+        log(f"{name}: serial {ser['ms'] * 1e3:.1f} us, overlapped {ovl['ms'] * 1e3:.1f} us (auto c={c}), speedup "
+            f"{ser['ms'] / ovl['ms']:.3f}, overlap ratio {ts.get('overlap_ratio')}")
         del bench, wl
         torch.cuda.empty_cache()
     return rows
+
+
+def compact_line(args, detail, name, raw, wl):
+    """The headline object: what the metric asks for, well under 4 KB."""
+    d = detail["workloads"][name]
+    ser, ovl = raw.get("serial"), raw.get("overlapped")
+    main_r = ovl if ovl is not None else ser
+    st = main_r["stats"]
+    out = {"metric": METRIC, "value": wl.flops() / (main_r["ms"] * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": main_r["ms"], "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded generator, random-init weights N(0,0.02^2), activations N(0,1))"}
+    out["config"] = {"workload": DESCRIPTIONS[name], "routed_rows": wl.rows,
+                     "path": "overlapped" if ovl is not None else "serial",
+                     "cu_split": args.cu_split, "consumer_cus": int(st.get("consumer_cus", 0)), "cu_mode": args.mode,
+                     "band_rows": args.band_rows or 1, "mid_segment_pieces": args.mgb,
+                     "down_split_k": int(st["split_k"]), "down_split_rows": int(st["split_rows"]),
+                     "plan_us": round(st["plan_us"], 1), "seed": args.seed}
+    out["expert_stage_us"] = main_r["ms"] * 1e3
+    out["expert_stage_us_median"] = main_r["p50_ms"] * 1e3
+    if ser is not None:
+        out["serial_stage_us"] = ser["ms"] * 1e3
+        out["serial_stage_us_median"] = ser["p50_ms"] * 1e3
+    if ser is not None and ovl is not None:
+        out["overlap_speedup"] = ser["ms"] / ovl["ms"]
+        out["overlap_speedup_median"] = ser["p50_ms"] / ovl["p50_ms"]
+    # Dominant kernel: the producer's gate/up launch (4*H*F flops per routed row, two thirds of the
+    # stage), timed by HIP events the library records on the producer's own stream around every
+    # launch in the timed region.
+    gu_flops = 4.0 * wl.H * wl.F * wl.rows
+    gu_ms = main_r["gate_up_ms"]
+    ach = gu_flops / (gu_ms * 1e-3) / 1e12
+    out["roofline"] = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                       "frac": ach / PEAK_BF16_TFLOPS, "traffic": stored_traffic(),
+                       "kernel": "moe::producer_kernel<false, 1> (gate/up launch)",
+                       "flops_per_launch": gu_flops, "launch_us": gu_ms * 1e3}
+    dn_ms = main_r["producer_ms"] - gu_ms
+    dn = 2.0 * wl.H * wl.F * wl.rows / (dn_ms * 1e-3) / 1e12
+    out["roofline_down"] = {"bound": "mfma", "achieved": dn, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                            "frac": dn / PEAK_BF16_TFLOPS, "kernel": down_kernel_name(args.split_k, st),
+                            "launch_us": dn_ms * 1e3}
+    prod = wl.flops() / (main_r["producer_ms"] * 1e-3) / 1e12
+    out["producer"] = {"us": main_r["producer_ms"] * 1e3, "tflops": prod, "frac": prod / PEAK_BF16_TFLOPS}
+    ts = raw.get("timestamps") or {}
+    if ovl is not None:
+        out["consumer"] = {"us": ovl["consumer_ms"] * 1e3, "copy_bytes": ts.get("copy_bytes"),
+                           "units": int(st["copy_units"]),
+                           "busy_us": ts.get("consumer_busy_us"), "GBps_while_busy": ts.get("consumer_GBps_while_busy"),
+                           "overlap_ratio": ts.get("overlap_ratio"), "exposed_copy_us": ts.get("exposed_copy_us"),
+                           "flag_to_copy_start_us_p50_p90_max": ts.get("flag_to_copy_start_us_p50_p90_max"),
+                           "cus_used": ts.get("consumer_cus_used")}
+        cc = [r for r in d.get("consumer_copy_ceiling", []) if r["mode"] == "partitioned"]
+        if cc:
+            out["consumer"]["copy_ceiling_GBps_by_cus"] = {str(r["consumer_cus"]): round(r["GBps"]) for r in cc}
+    if "best_small_partition" in d:
+        b = d["best_small_partition"]
+        out["best_small_partition"] = {k: b[k] for k in ("cu_split", "cu_mode", "mgb", "speedup_vs_serial_median")}
+    if "sweep_main_agreement" in d:
+        out["sweep_main_agreement"] = round(d["sweep_main_agreement"], 4)
+    out["workloads"] = {}
+    for n, w in detail["workloads"].items():
+        s = {}
+        if "serial" in w:
+            s["serial_us"] = round(w["serial"]["stage_us"], 1)
+            s["gate_up_frac"] = round(w["serial"]["gate_up_frac_of_peak"], 3)
+        if "overlapped" in w:
+            s["overlapped_us"] = round(w["overlapped"]["stage_us"], 1)
+        if "overlap_speedup_median" in w:
+            s["speedup_median"] = round(w["overlap_speedup_median"], 3)
+        if "best_small_partition" in w:
+            s["best_small_c_speedup"] = round(w["best_small_partition"]["speedup_vs_serial_median"], 3)
+        out["workloads"][n] = s
+    if "cpu_baseline" in detail:
+        out["cpu_baseline"] = detail["cpu_baseline"]
+    out["watchdog_timeouts"] = len(detail.get("watchdog_timeouts", []))
+    out["detail"] = args.detail_out
+    return out
 
 
 def main():
@@ -376,165 +664,66 @@ def main():
     from paper_2607_19539_amd.workload import make_workload
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
     if args.esweep_child:
         # The expert-count sweep alone, in a process of its own: handles, queues and allocations
         # of the earlier workloads do not carry over into its timings.
-        torch.cuda.set_device(0)
-        timeouts = []
-        rows = expert_count_sweep(torch, B, make_workload, args, [int(v) for v in args.esweep.split(",")], timeouts)
-        print(json.dumps({"expert_count_sweep": rows, "watchdog_timeouts": timeouts}), flush=True)
+        rows = expert_count_sweep(torch, B, make_workload, args, [int(v) for v in args.esweep.split(",")])
+        print(json.dumps({"expert_count_sweep": rows}), flush=True)
         return
-    torch.cuda.set_device(0)
-    sweep_cs = [int(v) for v in args.sweep.split(",") if v]
     names = [args.workload] + [w for w in args.extra_workloads.split(",") if w and w != args.workload]
-    out = {"metric": METRIC, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-           "data": "synthetic (seeded generator, random-init weights N(0,0.02^2), activations N(0,1))"}
-    per_wl = {}
+    detail = {"metric": METRIC, "args": vars(args), "workloads": {}}
     timeouts = []
+    head_raw, head_wl = None, None
     for wi, name in enumerate(names):
         headline = wi == 0
         log(f"generating workload {name} seed {args.seed}")
         wl = make_workload(name, seed=args.seed)
         log(f"{name}: rows={wl.rows} H={wl.H} F={wl.F} E_l={wl.E_l} R={wl.R}")
-        bench = Bench(torch, B, wl, args)
-        steps, warmup = (args.steps, args.warmup) if headline else (max(args.steps // 2, 10),
-                                                                    max(args.warmup // 2, 5))
-        only = args.only if headline else "all"
-        ser = ovl = None
-        ser_plain = ovl_plain = None
-        if only in ("all", "serial"):
-            ser_plain = bench.timed(args.mode + ":plain", "serial", 0, steps, warmup)
-            ser = with_plain_times(bench.timed(args.mode, "serial", 0, steps, warmup), ser_plain)
-            log(f"{name} serial: {ser['ms'] * 1e3:.1f} us (producer {ser['producer_ms'] * 1e3:.1f}, gate/up "
-                f"{ser['gate_up_ms'] * 1e3:.1f}, scatter {ser['scatter_ms'] * 1e3:.1f})")
-        if only in ("all", "overlapped"):
-            ovl_plain = bench.timed(args.mode + ":plain", "overlapped", args.cu_split, steps, warmup)
-            ovl = with_plain_times(bench.timed(args.mode, "overlapped", args.cu_split, steps, warmup), ovl_plain)
-            st = ovl["stats"]
-            log(f"{name} overlapped ({args.mode}, c={args.cu_split}): {ovl['ms'] * 1e3:.1f} us (producer "
-                f"{ovl['producer_ms'] * 1e3:.1f}, gate/up {ovl['gate_up_ms'] * 1e3:.1f}, consumer "
-                f"{ovl['consumer_ms'] * 1e3:.1f}); segments {st['n_segments']}, workgroups "
-                f"{st['gu_workgroups']}/{st['down_workgroups']}")
-        dplan = None
-        if only == "all" and ovl is not None:
-            # The same overlapped stage with the plan built on the GPU from device-resident routing.
-            dplan_plain = bench.timed(args.mode + ":plain", "overlapped", args.cu_split, steps, warmup,
-                                      device_plan=True)
-            dplan = with_plain_times(bench.timed(args.mode, "overlapped", args.cu_split, steps, warmup,
-                                                 device_plan=True), dplan_plain)
-            log(f"{name} overlapped, device-built plan: {dplan['ms'] * 1e3:.1f} us (planner on the GPU "
-                f"{dplan['plan_ms'] * 1e3:.1f} us; host-built plan: {ovl['stats']['plan_us']:.1f} us on the host, "
-                f"upload {ovl['plan_ms'] * 1e3:.1f} us on the GPU)")
-        direct = None
-        if only == "all":
-            # Ablation: no consumer at all, the down epilogue writes every row to its slot.
-            direct = bench.timed("direct", "serial", 0, steps, warmup)
-            log(f"{name} epilogue-direct ablation: {direct['ms'] * 1e3:.1f} us (producer "
-                f"{direct['producer_ms'] * 1e3:.1f}, gate/up {direct['gate_up_ms'] * 1e3:.1f})")
-        sweep = []
-        if sweep_cs and ser is not None and only == "all":
-            for mgb in (1, 2):
-                for c in sweep_cs:
-                    for mode in ("shared", "partitioned") if c <= 64 else ("shared",):
-                        key = bench.stage(mode, mgb)
-                        r = bench.timed(key, "overlapped", c, max(steps // 2, 5), max(warmup // 2, 3))
-                        sweep.append({"cu_split": c, "cu_mode": mode, "mgb": mgb,
-                                      "consumer_cus": r["stats"]["consumer_cus"],
-                                      "segments": r["stats"]["n_segments"], "stage_us": r["ms"] * 1e3,
-                                      "speedup_vs_serial": ser["ms"] / r["ms"]})
-                        log(f"{name} sweep c={c} {mode} mgb={mgb}: {r['ms'] * 1e3:.1f} us, "
-                            f"speedup {ser['ms'] / r['ms']:.3f}")
-        per_wl[name] = summarize(wl, ser, ovl, sweep)
-        if only == "all" and args.copy_curve:
-            curve = bench.copy_curve([int(v) for v in args.copy_curve.split(",")], 10, 3)
-            per_wl_curve = curve
-            for r in curve:
-                log(f"{name} consumer copy ceiling c={r['cu_split']} ({r['consumer_cus']} CUs): "
-                    f"{r['us']:.1f} us, {r['GBps']:.0f} GB/s")
-        else:
-            per_wl_curve = None
-        comb = bench.timed_combine(max(steps, 20), max(warmup, 5))
-        per_wl[name]["combine"] = comb
-        if per_wl_curve is not None:
-            per_wl[name]["consumer_copy_ceiling"] = per_wl_curve
-        log(f"{name} combine ({wl.T_r} tokens, k={wl.k}): {comb['us']:.1f} us, {comb['GBps']:.0f} GB/s")
-        if direct is not None:
-            per_wl[name]["epilogue_direct_ablation_us"] = direct["ms"] * 1e3
-        if dplan is not None:
-            per_wl[name]["device_plan"] = {
-                "stage_us": dplan["ms"] * 1e3, "planner_gpu_us": dplan["plan_ms"] * 1e3,
-                "host_plan_host_us": ovl["stats"]["plan_us"], "host_plan_upload_gpu_us": ovl["plan_ms"] * 1e3,
-                "host_planned_stage_us": ovl["ms"] * 1e3}
-        timeouts += bench.timeouts
+        d, raw = measure_workload(torch, B, wl, args, headline)
+        detail["workloads"][name] = d
+        timeouts += d.get("watchdog", [])
         if headline:
-            main_r = ovl if ovl is not None else ser
-            st = main_r["stats"]
-            out["value"] = wl.flops() / (main_r["ms"] * 1e-3) / 1e12
-            out["ms_per_step"] = main_r["ms"]
-            out["expert_stage_us"] = main_r["ms"] * 1e3
-            if ser is not None:
-                out["serial_stage_us"] = ser["ms"] * 1e3
-            if ser is not None and ovl is not None:
-                out["overlap_speedup"] = ser["ms"] / ovl["ms"]
-            out["config"] = {"workload": DESCRIPTIONS[name], "routed_rows": wl.rows,
-                             "path": "overlapped" if ovl is not None else "serial",
-                             "cu_split": args.cu_split, "consumer_cus": st.get("consumer_cus", 0),
-                             "cu_mode": args.mode, "band_rows": args.band_rows or 1,
-                             "mid_segment_pieces": args.mgb, "down_split_k": st["split_k"],
-                             "down_split_rows": st["split_rows"],
-                             "padding_rows": int(st["n_logical_rows"] - st["n_valid"]),
-                             "plan_us": round(st["plan_us"], 1), "seed": args.seed}
-            # Dominant kernel: the gate/up launch of the producer (4*H*F flops per routed row, two
-            # thirds of the stage).  Its duration comes from HIP events the library records on the
-            # producer's own stream around every launch in the timed region.
-            gu_flops = 4.0 * wl.H * wl.F * wl.rows
-            gu_ms = main_r["gate_up_ms"]
-            achieved = gu_flops / (gu_ms * 1e-3) / 1e12
-            out["roofline"] = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                               "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                               "traffic": stored_traffic(),
-                               "kernel": "moe::producer_kernel<false, 1> (gate/up launch)",
-                               "flops_per_launch": gu_flops, "launch_us": gu_ms * 1e3}
-            dn_ms = main_r["producer_ms"] - gu_ms
-            dn_flops = 2.0 * wl.H * wl.F * wl.rows
-            out["roofline_down"] = {"bound": "mfma", "achieved": dn_flops / (dn_ms * 1e-3) / 1e12,
-                                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                                    "frac": dn_flops / (dn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
-                                    "kernel": down_kernel_name(args.split_k, st),
-                                    "flops_per_launch": dn_flops, "launch_us": dn_ms * 1e3}
-            prod = wl.flops() / (main_r["producer_ms"] * 1e-3) / 1e12
-            out["producer"] = {"us": main_r["producer_ms"] * 1e3, "tflops": prod, "frac": prod / PEAK_BF16_TFLOPS}
-            if ovl is not None:
-                cons_bytes = 4.0 * wl.H * st["n_remote_rows"]
-                out["consumer"] = {"us": ovl["consumer_ms"] * 1e3, "bytes": cons_bytes,
-                                   "busy_GBps_lower_bound": cons_bytes / (ovl["consumer_ms"] * 1e-3) / 1e9,
-                                   "flag_wait_us_summed": st["wait_ticks"] / 100.0,
-                                   "poll_iters": int(st["poll_iters"]), "segments": int(st["n_segments"])}
+            head_raw, head_wl = raw, wl
             if not args.no_cpu_baseline:
                 log("timing the CPU oracle on a bounded sample")
-                out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
-        bench.close()
-        del bench, wl
-        torch.cuda.empty_cache()
-    out["workloads"] = per_wl
+                detail["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+                log(f"cpu baseline: {detail['cpu_baseline']['value']:.4f} TFLOP/s on {detail['cpu_baseline']['cores']} "
+                    f"threads ({detail['cpu_baseline']['cpu_model']})")
+        else:
+            del wl
+        if name == "tiny" and not args.no_cpu_baseline:
+            # The tiny workload's whole stage on one host thread (it finishes in seconds).
+            tb = cpu_baseline(make_workload("tiny", seed=args.seed), 1e9, threads=1)
+            detail["cpu_baseline_tiny_1thread"] = tb
     if args.esweep and args.only == "all":
         import subprocess
         cmd = [sys.executable, "-u", os.path.abspath(__file__), "--esweep-child", "--esweep", args.esweep,
                "--steps", str(args.steps), "--warmup", str(args.warmup), "--seed", str(args.seed),
-               "--band-rows", str(args.band_rows), "--split-k", str(args.split_k), "--mgb", str(args.mgb)]
+               "--band-rows", str(args.band_rows), "--split-k", str(args.split_k), "--mgb", str(args.mgb),
+               "--warm-s-other", str(args.warm_s_other)]
         child = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)  # progress lines pass through stderr
         lines = [l for l in child.stdout.splitlines() if l.startswith("{")]
         if child.returncode != 0 or not lines:
             log(f"ERROR: expert-count sweep exited with {child.returncode}")
             timeouts.append(f"expert-count sweep exited with {child.returncode}")
         else:
-            res = json.loads(lines[-1])
-            out["expert_count_sweep"] = res["expert_count_sweep"]
-            timeouts += res["watchdog_timeouts"]
-    out["watchdog_timeouts"] = timeouts
+            detail["expert_count_sweep"] = json.loads(lines[-1])["expert_count_sweep"]
+    detail["watchdog_timeouts"] = timeouts
+    detail["elapsed_s"] = time.time() - t_start
+    line = compact_line(args, detail, names[0], head_raw, head_wl)
+    if "expert_count_sweep" in detail:
+        line["expert_count_sweep"] = [{"E": r["experts_per_rank"], "speedup": round(r["speedup_median"], 3),
+                                       "overlap_ratio": None if r["overlap_ratio"] is None else round(r["overlap_ratio"], 3),
+                                       "c": r["auto_cu_split"]} for r in detail["expert_count_sweep"]]
+    detail["headline"] = line
+    if args.detail_out:
+        os.makedirs(os.path.dirname(os.path.abspath(args.detail_out)), exist_ok=True)
+        with open(args.detail_out, "w") as f:
+            json.dump(detail, f, indent=1)
+        log(f"detail written to {args.detail_out}")
     log(f"done in {time.time() - t_start:.0f} s")
-    print(json.dumps(out), flush=True)
+    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":

@@ -56,7 +56,9 @@ extern "C" {
 #define MOE_EHIP (-4)         /* a HIP runtime call failed (message names it)                  */
 #define MOE_ETIMEOUT (-5)     /* a bounded device wait expired; sticky until the next query   */
 #define MOE_EUNSUPPORTED (-6) /* hidden/ffn not multiples of 64, hidden > 65536, max_rows >=
-                                 2^24, cu_split out of range                                   */
+                                 2^24, max_rows * hidden * 2 > 2^32 - 1 (gathered rows are
+                                 addressed with 32-bit offsets), a padded layout of more than
+                                 2^24 rows, cu_split out of range                              */
 
 /* Config flags */
 #define MOE_LOCAL_DIRECT (1u << 0) /* overlapped run: rows whose source is self_rank are written
@@ -81,6 +83,11 @@ extern "C" {
                                       beside producer workgroups there (a consumer workgroup's
                                       registers and LDS fit next to a producer workgroup's), so
                                       the partition costs the producer issue slots, not CUs    */
+#define MOE_TIMESTAMPS (1u << 8)   /* measurement: every run records, in 100 MHz wall-clock ticks,
+                                      when each producer workgroup started and ended and where it
+                                      ran, and when each consumer copy unit began polling, saw its
+                                      flags and finished its copy (moe_stage_records); the handle
+                                      allocates the record buffers at create                   */
 #define MOE_DIRECT_ALL (1u << 5)   /* ablation, serial runs only: the down epilogue writes every
                                       row straight to its slot in return_bufs and no scatter
                                       runs -- the bound of a stage with no consumer at all     */
@@ -93,7 +100,8 @@ typedef struct {
   int32_t num_local_experts; /* E_l >= 1                                                      */
   int32_t num_ranks;         /* R >= 1 source ranks                                           */
   int32_t self_rank;         /* 0 <= self_rank < R; rows from it are local (Section 3.2.1)    */
-  int32_t max_rows;          /* capacity of one run (< 2^24); sizes the workspaces            */
+  int32_t max_rows;          /* capacity of one run (< 2^24, and max_rows * hidden * 2 bytes
+                                < 4 GiB); sizes the workspaces                                */
   int32_t band_rows;         /* tb_M of the remote-owner-aligned layout (Section 3.2.1): each
                                 remote owner group is padded to a multiple of it, so every
                                 band of band_rows rows has one destination.  Power of two in
@@ -149,6 +157,11 @@ typedef struct {
   int32_t split_rows;       /* tile rows whose down-projection tiles are split               */
   int32_t auto_cu_split;    /* cu_split = 0 runs: the split the selector settled on, 0 while
                                it is still measuring candidates; -1 for other runs          */
+  int32_t timeout_segment;  /* with timeout = 1: the lowest segment (ready order, as in
+                               moe_stage_plan_copy(MOE_PLAN_SEGMENTS)) whose flag wait expired;
+                               -1 otherwise                                                  */
+  int32_t copy_units;       /* overlapped runs: consumer copy units (one wave each) the run's
+                               segments were cut into; 0 for serial runs                     */
   int32_t reserved;
 } moe_stage_stats_t;
 
@@ -248,6 +261,52 @@ int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out);
 
 /* Kernel times accumulated since the last reset (needs MOE_KERNEL_TIMING); synchronizes. */
 int moe_stage_times(moe_stage_t h, int32_t reset, moe_stage_times_t* out);
+
+/*
+ * Timing and placement records of the last run of a handle created with MOE_TIMESTAMPS
+ * (measurement of the overlap of paper Section 4.2.2 and of the compute-unit partition of
+ * Section 3.3.3).  Times are the GPU's 100 MHz wall clock.  `which` selects:
+ *   MOE_RECORDS_PRODUCER  moe_wg_record_t[2 * producer_grid]: the gate/up launch's workgroups
+ *                         (index = workgroup), then the down launch's;
+ *   MOE_RECORDS_COPY      moe_copy_record_t[min(copy_units, 2^18)]: one per consumer copy unit
+ *                         (overlapped runs; index = unit);
+ *   MOE_RECORDS_SPAN      moe_span_t: the producer's span (first gate/up workgroup start, last
+ *                         down or tail workgroup end) and the unit counts;
+ *   MOE_RECORDS_TILES     uint64_t[tile rows * down tiles per row]: when each down tile's ready
+ *                         flag was raised (index = tile row * down tiles per row + column tile;
+ *                         0 = no flag this run: local-only tile rows, serial runs).
+ * With dst == NULL returns the bytes needed; else copies them (bytes must be at least that) and
+ * returns MOE_OK.  Synchronizes with the last run.  MOE_EINVAL without MOE_TIMESTAMPS or a run.
+ */
+#define MOE_RECORDS_PRODUCER 0
+#define MOE_RECORDS_COPY 1
+#define MOE_RECORDS_SPAN 2
+#define MOE_RECORDS_TILES 3
+typedef struct {
+  uint32_t hw_id;   /* HW_ID register of the workgroup's first wave: wave slot [3:0], SIMD
+                       [5:4], compute unit [11:8], shader array [12], shader engine [15:13]   */
+  uint32_t xcc_id;  /* XCD (accelerator die)                                               */
+  int32_t launch;   /* 0 gate/up, 1 down                                                   */
+  int32_t items;    /* work items the workgroup ran                                        */
+  uint64_t t_start, t_end;
+} moe_wg_record_t;
+typedef struct {
+  int32_t segment;  /* segment index (ready order)                                         */
+  int32_t part;     /* copy unit within the segment                                        */
+  uint32_t hw_id;   /* HW_ID register of the copying wave (fields as above)                */
+  uint32_t xcc_id;
+  uint64_t t_poll;  /* the wave starts polling the segment's ready flags                   */
+  uint64_t t_ready; /* every flag seen and acquired: the copy starts                       */
+  uint64_t t_done;  /* the unit's stores have completed                                    */
+} moe_copy_record_t;
+typedef struct {
+  uint64_t producer_start, producer_end;
+  int32_t copy_units;     /* units of the last run (0 for serial runs)                      */
+  int32_t copy_recorded;  /* of them recorded                                               */
+  int32_t producer_grid;  /* workgroups per producer launch                                 */
+  int32_t reserved;
+} moe_span_t;
+int64_t moe_stage_records(moe_stage_t h, int32_t which, void* dst, int64_t bytes);
 
 /* Human-readable description of the handle's last error ("" if none).  Valid until the next call. */
 const char* moe_stage_last_error(moe_stage_t h);

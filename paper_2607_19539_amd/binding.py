@@ -8,9 +8,11 @@ GPU is present, calls fail loudly.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
-from typing import Optional, Sequence
+import sys
+from typing import Dict, Optional, Sequence
 
 import numpy as np
 
@@ -19,7 +21,8 @@ LIB_PATH = os.path.join(PKG, "_lib", "libmoe_stage.so")
 
 MOE_OK, MOE_EINVAL, MOE_EROUTING, MOE_ECAPACITY, MOE_EHIP, MOE_ETIMEOUT, MOE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 (MOE_LOCAL_DIRECT, MOE_KERNEL_TIMING, MOE_POISON, MOE_TEST_NO_SIGNAL, MOE_SHARED_CUS, MOE_DIRECT_ALL,
- MOE_TEST_CONSUMER_ONLY, MOE_TEST_PLAN_NO_LDS) = 1, 2, 4, 8, 16, 32, 64, 128
+ MOE_TEST_CONSUMER_ONLY, MOE_TEST_PLAN_NO_LDS, MOE_TIMESTAMPS) = 1, 2, 4, 8, 16, 32, 64, 128, 256
+MOE_RECORDS_PRODUCER, MOE_RECORDS_COPY, MOE_RECORDS_SPAN, MOE_RECORDS_TILES = 0, 1, 2, 3
 (MOE_PLAN_TILE_ROWS, MOE_PLAN_ITEMS, MOE_PLAN_ROW_X, MOE_PLAN_ROW_RANK, MOE_PLAN_ROW_SLOT, MOE_PLAN_SEGMENTS,
  MOE_PLAN_GROUPS, MOE_PLAN_QUEUES) = range(8)
 ERROR_NAMES = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EROUTING", -3: "MOE_ECAPACITY", -4: "MOE_EHIP",
@@ -28,7 +31,7 @@ ERROR_NAMES = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EROUTING", -3: "MOE_ECAPA
 EXPORTED = ["moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query", "moe_stage_times",
             "moe_stage_last_error", "moe_stage_destroy", "moe_plan_build", "moe_plan_info", "moe_plan_copy",
             "moe_plan_free", "moe_combine", "moe_stage_run_devplan", "moe_stage_run_serial_devplan",
-            "moe_stage_plan_info", "moe_stage_plan_copy"]
+            "moe_stage_plan_info", "moe_stage_plan_copy", "moe_stage_records"]
 
 
 class moe_stage_config_t(ctypes.Structure):
@@ -47,7 +50,25 @@ class moe_stage_stats_t(ctypes.Structure):
                 ("plan_us", ctypes.c_double), ("poll_iters", ctypes.c_uint64), ("wait_ticks", ctypes.c_uint64),
                 ("gu_workgroups", ctypes.c_int32), ("down_workgroups", ctypes.c_int32),
                 ("split_k", ctypes.c_int32), ("split_rows", ctypes.c_int32),
-                ("auto_cu_split", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("auto_cu_split", ctypes.c_int32), ("timeout_segment", ctypes.c_int32),
+                ("copy_units", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class moe_wg_record_t(ctypes.Structure):
+    _fields_ = [("hw_id", ctypes.c_uint32), ("xcc_id", ctypes.c_uint32), ("launch", ctypes.c_int32),
+                ("items", ctypes.c_int32), ("t_start", ctypes.c_uint64), ("t_end", ctypes.c_uint64)]
+
+
+class moe_copy_record_t(ctypes.Structure):
+    _fields_ = [("segment", ctypes.c_int32), ("part", ctypes.c_int32), ("hw_id", ctypes.c_uint32),
+                ("xcc_id", ctypes.c_uint32), ("t_poll", ctypes.c_uint64), ("t_ready", ctypes.c_uint64),
+                ("t_done", ctypes.c_uint64)]
+
+
+class moe_span_t(ctypes.Structure):
+    _fields_ = [("producer_start", ctypes.c_uint64), ("producer_end", ctypes.c_uint64),
+                ("copy_units", ctypes.c_int32), ("copy_recorded", ctypes.c_int32),
+                ("producer_grid", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class moe_stage_times_t(ctypes.Structure):
@@ -70,6 +91,21 @@ def _struct_dict(s) -> dict:
 
 
 _lib: Optional[ctypes.CDLL] = None
+# Live handles and their configurations: the run wrappers check buffer shapes against them, and
+# the exit hook destroys whatever is still alive while the HIP runtime is intact.
+_handles: Dict[int, moe_stage_config_t] = {}
+
+
+def _destroy_live_handles():
+    """Exit hook: destroy every live handle before the HIP runtime's own teardown.  Registered
+    after torch is imported, so it runs before torch's exit hooks (atexit runs last-in first-out);
+    a handle destroyed from a garbage-collector pass during interpreter finalization would tear
+    down its streams and pinned memory after the runtime has started unloading."""
+    lib = _lib
+    for h in list(_handles):
+        _handles.pop(h, None)
+        if lib is not None:
+            lib.moe_stage_destroy(h)
 
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -79,6 +115,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"HIP library not built: {path} (run `python -m paper_2607_19539_amd.build`)")
+    try:
+        import torch  # noqa: F401  (its exit hooks must be registered before ours)
+    except ImportError:
+        pass
+    atexit.register(_destroy_live_handles)
     lib = ctypes.CDLL(path)
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     lib.moe_stage_create.argtypes = [ctypes.POINTER(moe_stage_config_t), ctypes.POINTER(vp)]
@@ -102,6 +143,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.moe_stage_plan_info.argtypes = [vp, ctypes.POINTER(moe_plan_info_t)]
     lib.moe_stage_plan_copy.argtypes = [vp, i32, vp, i64]
     lib.moe_stage_plan_copy.restype = ctypes.c_int64
+    lib.moe_stage_records.argtypes = [vp, i32, vp, i64]
+    lib.moe_stage_records.restype = ctypes.c_int64
     for name in ("moe_combine", "moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query",
                  "moe_stage_times", "moe_stage_destroy", "moe_plan_build", "moe_plan_info"):
         getattr(lib, name).restype = ctypes.c_int
@@ -164,12 +207,66 @@ def _check(rc: int, h=None) -> int:
 def moe_stage_create(cfg: moe_stage_config_t) -> int:
     h = ctypes.c_void_p()
     _check(load().moe_stage_create(ctypes.byref(cfg), ctypes.byref(h)))
+    _handles[h.value] = moe_stage_config_t.from_buffer_copy(cfg)
     return h.value
 
 
-def _run_args(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows):
+def _shape(t):
+    """(shape, element size) of a tensor or array; None for a raw integer address or None."""
+    if t is None or isinstance(t, int):
+        return None
+    esize = t.element_size() if hasattr(t, "element_size") else t.itemsize
+    return tuple(int(d) for d in t.shape), int(esize)
+
+
+def validate_run_args(cfg, x, rows, n_routing, w1, w3, w2, return_bufs, return_rows):
+    """Checks that every buffer is as large as the call says, before anything reaches the library
+    (whose kernels would otherwise read or write past a short buffer).  ``rows`` is the routed-row
+    count (expert_offsets[E_l]; None when the routing lives on the device), ``n_routing`` the
+    lengths of (expert_offsets, row_src_rank, row_slot).  Raw integer addresses are not checked.
+    Raises ValueError."""
+    H, F, E, R = cfg.hidden, cfg.ffn, cfg.num_local_experts, cfg.num_ranks
+    n_off, n_src, n_slot = n_routing
+    if n_off != E + 1:
+        raise ValueError(f"expert_offsets must have num_local_experts + 1 = {E + 1} entries, not {n_off}")
+    if n_src != n_slot:
+        raise ValueError(f"row_src_rank ({n_src}) and row_slot ({n_slot}) differ in length")
+    if rows is not None and rows >= 0 and n_src != rows:
+        raise ValueError(f"row_src_rank and row_slot must have expert_offsets[-1] = {rows} entries, not {n_src}")
+    n_rows = n_src if rows is None else max(rows, 0)
+    for name, t, want in (("w1", w1, (E, F, H)), ("w3", w3, (E, F, H)), ("w2", w2, (E, H, F))):
+        sh = _shape(t)
+        if sh is not None and (sh[0] != want or sh[1] != 2):
+            raise ValueError(f"{name} must be [{', '.join(map(str, want))}] with 2-byte elements, got {sh[0]} "
+                             f"of {sh[1]}-byte elements")
+    sh = _shape(x)
+    if sh is not None and (len(sh[0]) != 2 or sh[0][1] != H or sh[0][0] < n_rows or sh[1] != 2):
+        raise ValueError(f"dispatched_x must be [>= {n_rows}, {H}] with 2-byte elements, got {sh[0]} of "
+                         f"{sh[1]}-byte elements")
+    if len(return_bufs) != R:
+        raise ValueError(f"return_bufs must hold num_ranks = {R} buffers, not {len(return_bufs)}")
+    if len(return_rows) != R:
+        raise ValueError(f"return_rows must hold num_ranks = {R} entries, not {len(return_rows)}")
+    for r, (b, n) in enumerate(zip(return_bufs, return_rows)):
+        sh = _shape(b)
+        if sh is not None and (len(sh[0]) != 2 or sh[0][1] != H or sh[0][0] < int(n) or sh[1] != 2):
+            raise ValueError(f"return_bufs[{r}] must be [>= return_rows[{r}] = {int(n)}, {H}] with 2-byte "
+                             f"elements, got {sh[0]} of {sh[1]}-byte elements")
+
+
+def _cfg_of(h) -> moe_stage_config_t:
+    cfg = _handles.get(h)
+    if cfg is None:
+        raise ValueError("not a live handle of this binding")
+    return cfg
+
+
+def _run_args(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows, cfg=None):
     off, src, slot = _host_i32(expert_offsets), _host_i32(row_src_rank), _host_i32(row_slot)
     rr = _host_i64(return_rows if return_rows is not None else [b.shape[0] for b in return_bufs])
+    if cfg is not None:
+        validate_run_args(cfg, x, int(off[-1]) if off.size else None, (off.size, src.size, slot.size),
+                          w1, w3, w2, return_bufs, rr)
     ptrs = (ctypes.c_void_p * len(return_bufs))(*[_dev_ptr(b) for b in return_bufs])
     keep = (off, src, slot, rr, ptrs)
     args = [_dev_ptr(x) if x is not None else None, _np_ptr(off), _np_ptr(src), _np_ptr(slot),
@@ -189,7 +286,8 @@ def _stream_ptr(stream) -> Optional[int]:
 
 def moe_stage_run(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs: Sequence,
                   return_rows=None, cu_split: int = 8, stream=None) -> int:
-    args, keep = _run_args(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows)
+    args, keep = _run_args(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows,
+                           _cfg_of(h))
     rc = load().moe_stage_run(h, *args, int(cu_split), _stream_ptr(stream))
     del keep
     return _check(rc, h)
@@ -197,18 +295,23 @@ def moe_stage_run(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, retu
 
 def moe_stage_run_serial(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs: Sequence,
                          return_rows=None, stream=None) -> int:
-    args, keep = _run_args(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows)
+    args, keep = _run_args(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows,
+                           _cfg_of(h))
     rc = load().moe_stage_run_serial(h, *args, _stream_ptr(stream))
     del keep
     return _check(rc, h)
 
 
-def _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows):
+def _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows, cfg=None):
     import torch
     for name, t in (("expert_offsets", expert_offsets), ("row_src_rank", row_src_rank), ("row_slot", row_slot)):
-        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.int32:
-            raise ValueError(f"{name} must be an int32 device tensor")
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.int32 or t.dim() != 1:
+            raise ValueError(f"{name} must be a one-dimensional int32 device tensor")
     rr = _host_i64(return_rows if return_rows is not None else [b.shape[0] for b in return_bufs])
+    if cfg is not None:
+        # The routed-row count lives on the device; the routing arrays' own lengths bound it.
+        validate_run_args(cfg, x, None, (expert_offsets.numel(), row_src_rank.numel(), row_slot.numel()),
+                          w1, w3, w2, return_bufs, rr)
     ptrs = (ctypes.c_void_p * len(return_bufs))(*[_dev_ptr(b) for b in return_bufs])
     keep = (rr, ptrs)
     args = [_dev_ptr(x), _dev_ptr(expert_offsets), _dev_ptr(row_src_rank), _dev_ptr(row_slot),
@@ -219,7 +322,8 @@ def _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_
 def moe_stage_run_devplan(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs: Sequence,
                           return_rows=None, cu_split: int = 8, stream=None) -> int:
     """moe_stage_run with the routing (int32 device tensors) planned on the device."""
-    args, keep = _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows)
+    args, keep = _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows,
+                               _cfg_of(h))
     rc = load().moe_stage_run_devplan(h, *args, int(cu_split), _stream_ptr(stream))
     del keep
     return _check(rc, h)
@@ -227,7 +331,8 @@ def moe_stage_run_devplan(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, 
 
 def moe_stage_run_serial_devplan(h, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2,
                                  return_bufs: Sequence, return_rows=None, stream=None) -> int:
-    args, keep = _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows)
+    args, keep = _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows,
+                               _cfg_of(h))
     rc = load().moe_stage_run_serial_devplan(h, *args, _stream_ptr(stream))
     del keep
     return _check(rc, h)
@@ -272,7 +377,28 @@ def moe_stage_times(h, reset: bool = False) -> dict:
 
 
 def moe_stage_destroy(h) -> int:
+    _handles.pop(h, None)
     return _check(load().moe_stage_destroy(h))
+
+
+def moe_stage_records(h, which: int) -> np.ndarray:
+    """Records of the handle's last run (MOE_TIMESTAMPS) as a numpy structured array (the span: a
+    one-element array)."""
+    lib = load()
+    ctype = {MOE_RECORDS_PRODUCER: moe_wg_record_t, MOE_RECORDS_COPY: moe_copy_record_t,
+             MOE_RECORDS_SPAN: moe_span_t, MOE_RECORDS_TILES: None}[which]
+    need = lib.moe_stage_records(h, int(which), None, 0)
+    if need < 0:
+        _check(int(need), h)
+    if ctype is None:
+        dt = np.dtype(np.uint64)
+    else:
+        dt = np.dtype([(n, np.dtype(t)) for n, t in ctype._fields_], align=True)
+        assert dt.itemsize == ctypes.sizeof(ctype)
+    out = np.zeros(need // dt.itemsize, dt)
+    if need:
+        _check(int(lib.moe_stage_records(h, int(which), _np_ptr(out), int(need))), h)
+    return out
 
 
 def moe_plan_build(cfg: moe_stage_config_t, expert_offsets, row_src_rank, row_slot, return_rows,
@@ -357,6 +483,9 @@ class MoeStage:
     def times(self, reset=False) -> dict:
         return moe_stage_times(self.h, reset)
 
+    def records(self, which) -> np.ndarray:
+        return moe_stage_records(self.h, which)
+
     def close(self):
         if self.h:
             moe_stage_destroy(self.h)
@@ -369,6 +498,9 @@ class MoeStage:
         self.close()
 
     def __del__(self):
+        # During interpreter finalization the exit hook has already destroyed live handles.
+        if sys.is_finalizing():
+            return
         try:
             self.close()
         except Exception:

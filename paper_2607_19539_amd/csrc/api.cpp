@@ -11,6 +11,7 @@
 #include <hip/hip_runtime.h>
 #include <hip/hip_ext.h>
 #include <stdint.h>
+#include <stddef.h>
 #include <string.h>
 
 #include <algorithm>
@@ -24,6 +25,11 @@
 #include "plan_device.hpp"
 
 using namespace moe;
+
+static_assert(sizeof(WgRecord) == sizeof(moe_wg_record_t) && offsetof(WgRecord, t_start) == offsetof(moe_wg_record_t, t_start),
+              "producer record layout");
+static_assert(sizeof(CopyRecord) == sizeof(moe_copy_record_t) && offsetof(CopyRecord, t_poll) == offsetof(moe_copy_record_t, t_poll),
+              "copy record layout");
 
 namespace {
 
@@ -108,6 +114,11 @@ struct moe_stage_s {
   float* partials = nullptr;
   uint32_t* arrivals = nullptr;
   RunCounters* ctr = nullptr;
+  WgRecord* wg_rec = nullptr;      // MOE_TIMESTAMPS: [2][num_cus * producer_bpc] per launch
+  CopyRecord* copy_rec = nullptr;  // MOE_TIMESTAMPS: [kMaxCopyRecords]
+  uint64_t* tile_ready = nullptr;  // MOE_TIMESTAMPS: [max_tile_rows * down_per_row] flag times
+  uint32_t* simd_waves = nullptr;  // consumer waves per SIMD beside the producer [kXcds * kSimdKeys]
+  int32_t last_tiles = 0;          // down tiles of the last run (tile rows x down_per_row)
   uint8_t* d_plan = nullptr;
   size_t plan_cap = 0;
   BlobLayout cap_lay{};   // the blob at the handle's capacity (device-built plans)
@@ -142,6 +153,7 @@ struct moe_stage_s {
   hipEvent_t ev_fork = nullptr, ev_join_c = nullptr, ev_join_p = nullptr, ev_done = nullptr;
   bool ran = false;
   bool counters_pending = false;  // the last run's device counters have not been read yet
+  uint64_t last_span[2] = {0, 0};  // producer span of the last timestamped run
   uint32_t last_timeouts = 0, last_timeout_where = 0;
 
   std::vector<TimingRec> ring;
@@ -193,7 +205,7 @@ int check_config(const moe_stage_config_t* c) {
     return MOE_EINVAL;
   constexpr uint32_t kKnownFlags = MOE_LOCAL_DIRECT | MOE_KERNEL_TIMING | MOE_POISON |
                                    MOE_TEST_NO_SIGNAL | MOE_SHARED_CUS | MOE_DIRECT_ALL |
-                                   MOE_TEST_CONSUMER_ONLY | MOE_TEST_PLAN_NO_LDS;
+                                   MOE_TEST_CONSUMER_ONLY | MOE_TEST_PLAN_NO_LDS | MOE_TIMESTAMPS;
   if (c->flags & ~kKnownFlags) return MOE_EINVAL;
   if (c->band_rows < 0 || c->band_rows > 256 || (c->band_rows & (c->band_rows - 1)) != 0)
     return MOE_EINVAL;
@@ -203,6 +215,14 @@ int check_config(const moe_stage_config_t* c) {
   if (c->hidden % 64 != 0 || c->ffn % 64 != 0 || c->hidden > kMaxDownColTiles * kDownTileN ||
       c->max_rows >= (1 << 24))
     return MOE_EUNSUPPORTED;
+  // The kernels address within one operand with 32-bit lane offsets: the gathered token rows of
+  // dispatched_x (row x 2*hidden bytes) and the K blocks of the activation workspace (its
+  // logical rows x 128 bytes).
+  if ((int64_t)c->max_rows * c->hidden * 2 > (int64_t)UINT32_MAX) return MOE_EUNSUPPORTED;
+  const int64_t tile_rows =
+      (max_logical_rows(c->max_rows, c->num_local_experts, c->num_ranks, std::max(c->band_rows, 1)) + kTileM - 1) /
+          kTileM + c->num_local_experts;
+  if (tile_rows > kMaxTileRows || tile_rows * kTileM * kTileK * 2 > (int64_t)UINT32_MAX) return MOE_EUNSUPPORTED;
   return MOE_OK;
 }
 
@@ -220,6 +240,9 @@ int enqueue_init(moe_stage_s* h, bool overlapped, bool dev, int32_t n_tile_rows,
   ia.ctr = h->ctr;
   ia.arrivals = h->arrivals;
   ia.n_arrivals = n_tile_rows * h->down_per_row;
+  ia.tile_ready = h->tile_ready;
+  h->last_tiles = ia.n_arrivals;
+  if (overlapped && (c.flags & MOE_SHARED_CUS)) ia.simd_waves = h->simd_waves;
   if (c.flags & MOE_POISON) {
     ia.poison = h->y;
     ia.poison_elems = n_lrows * c.hidden;
@@ -449,6 +472,11 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
   a.split_k = h->cfg.down_split_k;
   a.partials = h->partials;
   a.arrivals = h->arrivals;
+  if (h->wg_rec) {
+    a.wg_rec = h->wg_rec + (down ? (size_t)h->num_cus * h->producer_bpc : 0);
+    a.ctr = h->ctr;
+    a.tile_ready = h->tile_ready;
+  }
   return a;
 }
 
@@ -535,6 +563,21 @@ int pick_auto(moe_stage_s* h) {
     }
   }
   return a.chosen >= 0 ? a.chosen : 0;
+}
+
+// Copy units per segment (powers of two).  Beside the producer, few: a copying wave slows the
+// producer workgroup on its compute unit; segments ready in the down launch's last two rounds
+// take H / 256 units (about 128 KiB of each 256-row piece, 4..16).  On compute units of its own
+// the consumer cuts each 256-row piece into units of about 64 KiB (H / 128, 4..64), so its
+// waves copy in parallel whatever the segment count.
+void copy_units(int32_t H, bool shared, int32_t* early_shift, int32_t* late_shift) {
+  auto log2_floor = [](int32_t v) { return v > 1 ? 31 - __builtin_clz((uint32_t)v) : 0; };
+  if (shared) {
+    *early_shift = kCopyPartsShift;
+    *late_shift = std::min(std::max(log2_floor(H / 256), kCopyPartsShift), kCopyPartsLateShift);
+  } else {
+    *early_shift = *late_shift = std::min(std::max(log2_floor(H / 128), kCopyPartsShift), kCopyPartsOwnShift);
+  }
 }
 
 // Consumer CUs actually reserved for a requested split: a multiple of the XCD count.
@@ -665,6 +708,8 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       !try_hip(hipMalloc(&h->y, y_bytes), "hipMalloc(y)") ||
       !try_hip(hipMalloc(&h->flags, flag_bytes), "hipMalloc(flags)") ||
       !try_hip(hipMalloc(&h->ctr, sizeof(RunCounters)), "hipMalloc(counters)") ||
+      !try_hip(hipMalloc(&h->simd_waves, sizeof(uint32_t) * kXcds * kSimdKeys), "hipMalloc(counters)") ||
+      !try_hip(hipMemset(h->simd_waves, 0, sizeof(uint32_t) * kXcds * kSimdKeys), "hipMemset(counters)") ||
       !try_hip(hipMalloc(&h->d_plan, h->plan_cap), "hipMalloc(plan)") ||
       !try_hip(hipMalloc(&h->dev_ws, ws_bytes), "hipMalloc(planner scratch)") ||
       !try_hip(hipHostMalloc(&h->h_stage[0], h->plan_cap, hipHostMallocDefault), "hipHostMalloc") ||
@@ -672,8 +717,19 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       !try_hip(hipMemset(h->hws, 0, hws_bytes), "hipMemset(hws)") ||
       !try_hip(hipMemset(h->y, 0, y_bytes), "hipMemset(y)") ||
       !try_hip(hipMemset(h->flags, 0, flag_bytes), "hipMemset(flags)") ||
-      !try_hip(hipMemset(h->ctr, 0, sizeof(RunCounters)), "hipMemset(counters)"))
+      !try_hip(hipMemset(h->ctr, 0, sizeof(RunCounters)), "hipMemset(counters)") ||
+      !try_hip(hipMemset(&h->ctr->timeout_seg, 0xFF, sizeof(uint32_t)), "hipMemset(counters)"))
     return bail(MOE_EHIP);
+  if (cfg->flags & MOE_TIMESTAMPS) {
+    const size_t wg_bytes = 2 * (size_t)h->num_cus * h->producer_bpc * sizeof(WgRecord);
+    const size_t cp_bytes = (size_t)kMaxCopyRecords * sizeof(CopyRecord);
+    if (!try_hip(hipMalloc(&h->wg_rec, wg_bytes), "hipMalloc(records)") ||
+        !try_hip(hipMalloc(&h->copy_rec, cp_bytes), "hipMalloc(records)") ||
+        !try_hip(hipMalloc(&h->tile_ready, flag_bytes * 2), "hipMalloc(records)") ||
+        !try_hip(hipMemset(h->wg_rec, 0, wg_bytes), "hipMemset(records)") ||
+        !try_hip(hipMemset(h->copy_rec, 0, cp_bytes), "hipMemset(records)"))
+      return bail(MOE_EHIP);
+  }
   h->ws = devplan_ws_carve(h->dev_ws, cfg->num_local_experts, cfg->num_ranks, cfg->max_rows,
                            h->max_tile_rows, h->down_per_row, h->max_lrows, max_items);
   // Every event here orders work on this device or marks completion for the host; none
@@ -728,8 +784,9 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   const bool shared = (h->cfg.flags & MOE_SHARED_CUS) != 0;
   const int pgrid = (shared ? h->num_cus : h->num_cus - c_eff) * h->producer_bpc;
   // Consumer workgroups per CU: two beside a producer workgroup (their registers fill what a
-  // producer wave leaves free), six when the consumer owns its CUs.
-  const int cgrid = c_eff * (shared ? 2 : 6);
+  // producer wave leaves free), four of the wider variant when the consumer owns its CUs.
+  const bool own_cus = !shared;
+  const int cgrid = c_eff * (own_cus ? kConsumerOwnPerCu : 2);
   const bool legacy = stream == nullptr || stream == hipStreamLegacy;
   const bool on_caller = shared && !legacy;
   // The adaptive selector keeps its candidates' queues until it has settled.
@@ -765,6 +822,12 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   ca.H = h->cfg.hidden;
   ca.ctr = h->ctr;
   ca.watchdog_ticks = watchdog_ticks(h);
+  copy_units(h->cfg.hidden, !own_cus, &ca.early_shift, &ca.late_shift);
+  if (!own_cus) ca.simd_waves = h->simd_waves;
+  if (h->copy_rec) {
+    ca.rec = h->copy_rec;
+    ca.rec_cap = kMaxCopyRecords;
+  }
 
   // The consumer is released as soon as the init kernel has reset the queue heads: it only
   // reads segments of the uploaded plan and flags this run's down launch raises, so no event
@@ -781,7 +844,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   // A host-built plan's counts are known here, so empty launches are skipped; a device-built
   // plan's kernels read them and return at once when there is nothing to do.
   const bool known = !dev;
-  if (!known || !h->plan.segs.empty()) HIP_TRY(h, launch_consumer(ca, cgrid, h->s_cons));
+  if (!known || !h->plan.segs.empty()) HIP_TRY(h, launch_consumer(ca, own_cus, cgrid, h->s_cons));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
   HIP_TRY(h, hipEventRecord(h->ev_join_c, h->s_cons));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], ps));
@@ -894,8 +957,9 @@ int moe_stage_run_serial_devplan(moe_stage_t h, const void* x, const int32_t* of
   return run_serial(h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, stream);
 }
 
-int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
-  if (!h || !out) return MOE_EINVAL;
+// Waits for the last run and reads its device counters once (the watchdog reports stay in
+// h->last until a query returns them).
+static int sync_counters(moe_stage_t h) {
   if (h->ran) HIP_TRY(h, hipEventSynchronize(h->ev_done));
   if (h->counters_pending) {
     h->counters_pending = false;
@@ -906,13 +970,24 @@ int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
     h->last.gu_workgroups = (int32_t)c.gu_active;
     h->last.down_workgroups = (int32_t)c.down_active;
     h->last.timeout = c.timeouts ? 1 : 0;
+    h->last.timeout_segment = c.timeouts ? (int32_t)c.timeout_seg : -1;
+    h->last.copy_units = (int32_t)c.n_units;
     h->last_timeouts = c.timeouts;
     h->last_timeout_where = c.timeout_where;
+    h->last_span[0] = c.prod_t0;
+    h->last_span[1] = c.prod_t1;
     if (c.timeouts) {  // sticky across runs until reported here
-      const uint32_t zero[2] = {0, 0};
-      HIP_TRY(h, hipMemcpy(&h->ctr->timeouts, zero, sizeof zero, hipMemcpyHostToDevice));
+      const uint32_t reset[3] = {0, 0, UINT32_MAX};  // timeouts, timeout_where, timeout_seg
+      HIP_TRY(h, hipMemcpy(&h->ctr->timeouts, reset, sizeof reset, hipMemcpyHostToDevice));
     }
   }
+  return MOE_OK;
+}
+
+int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
+  if (!h || !out) return MOE_EINVAL;
+  const int rc = sync_counters(h);
+  if (rc) return rc;
   if (h->dev_hdr_pending) {  // a device-built plan: its counts and verdict are on the device
     h->dev_hdr_pending = false;
     PlanHeader hd{};
@@ -945,7 +1020,8 @@ int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
     h->last.timeout = 0;
     return set_err(h, MOE_ETIMEOUT,
                    std::to_string(h->last_timeouts) + " device wait(s) hit the watchdog since the last query (" +
-                       ((h->last_timeout_where & 1) ? "consumer flag wait" : "") + ")");
+                       ((h->last_timeout_where & 1) ? "consumer flag wait" : "") + ", first at segment " +
+                       std::to_string(h->last.timeout_segment) + ")");
   }
   return MOE_OK;
 }
@@ -1041,6 +1117,44 @@ int64_t moe_stage_plan_copy(moe_stage_t h, int32_t which, void* dst, int64_t byt
   return MOE_OK;
 }
 
+int64_t moe_stage_records(moe_stage_t h, int32_t which, void* dst, int64_t bytes) {
+  if (!h) return MOE_EINVAL;
+  if (!(h->cfg.flags & MOE_TIMESTAMPS)) return set_err(h, MOE_EINVAL, "MOE_TIMESTAMPS not set");
+  if (!h->ran) return set_err(h, MOE_EINVAL, "no run yet");
+  const int rc = sync_counters(h);
+  if (rc) return rc;
+  const int32_t recorded = std::min<int32_t>(h->last.copy_units, (int32_t)kMaxCopyRecords);
+  int64_t need = 0;
+  switch (which) {
+    case MOE_RECORDS_PRODUCER: need = 2 * (int64_t)h->last.producer_grid * (int64_t)sizeof(WgRecord); break;
+    case MOE_RECORDS_COPY: need = (int64_t)recorded * (int64_t)sizeof(CopyRecord); break;
+    case MOE_RECORDS_SPAN: need = (int64_t)sizeof(moe_span_t); break;
+    case MOE_RECORDS_TILES: need = (int64_t)h->last_tiles * (int64_t)sizeof(uint64_t); break;
+    default: return set_err(h, MOE_EINVAL, "unknown record kind");
+  }
+  if (!dst) return need;
+  if (bytes < need) return set_err(h, MOE_EINVAL, "destination too small");
+  if (which == MOE_RECORDS_PRODUCER) {
+    const size_t per = (size_t)h->last.producer_grid * sizeof(WgRecord);
+    const size_t stride = (size_t)h->num_cus * h->producer_bpc;
+    HIP_TRY(h, hipMemcpy(dst, h->wg_rec, per, hipMemcpyDeviceToHost));
+    HIP_TRY(h, hipMemcpy((uint8_t*)dst + per, h->wg_rec + stride, per, hipMemcpyDeviceToHost));
+  } else if (which == MOE_RECORDS_COPY) {
+    if (need) HIP_TRY(h, hipMemcpy(dst, h->copy_rec, (size_t)need, hipMemcpyDeviceToHost));
+  } else if (which == MOE_RECORDS_TILES) {
+    if (need) HIP_TRY(h, hipMemcpy(dst, h->tile_ready, (size_t)need, hipMemcpyDeviceToHost));
+  } else {
+    moe_span_t sp{};
+    sp.producer_start = h->last_span[0];
+    sp.producer_end = h->last_span[1];
+    sp.copy_units = h->last.copy_units;
+    sp.copy_recorded = recorded;
+    sp.producer_grid = h->last.producer_grid;
+    memcpy(dst, &sp, sizeof sp);
+  }
+  return MOE_OK;
+}
+
 const char* moe_stage_last_error(moe_stage_t h) { return h ? h->err.c_str() : g_create_error.c_str(); }
 
 int moe_stage_destroy(moe_stage_t h) {
@@ -1061,7 +1175,8 @@ int moe_stage_destroy(moe_stage_t h) {
   }
   if (h->shared_prod) (void)hipStreamDestroy(h->shared_prod);
   for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->ctr, (void*)h->d_plan,
-                  (void*)h->partials, (void*)h->arrivals, h->dev_ws})
+                  (void*)h->partials, (void*)h->arrivals, h->dev_ws, (void*)h->wg_rec, (void*)h->copy_rec,
+                  (void*)h->tile_ready, (void*)h->simd_waves})
     if (p) (void)hipFree(p);
   for (uint8_t* p : h->h_stage)
     if (p) (void)hipHostFree(p);

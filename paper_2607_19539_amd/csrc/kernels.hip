@@ -585,7 +585,10 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     // before wave 0 raises the flag; a plain barrier does not wait for other waves' stores.
     wait_vm_and_barrier<0>();
     if (signal && (tr.has_remote || !direct)) {
-      if (tid == 0) __hip_atomic_store(&a.flags[tile], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (tid == 0) {
+        if (a.tile_ready) a.tile_ready[tile] = ticks();
+        __hip_atomic_store(&a.flags[tile], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   }
 }
@@ -594,6 +597,12 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
 __device__ __forceinline__ uint32_t xcc_id() {
   constexpr int kHwRegXccId = 20;
   return (uint32_t)__builtin_amdgcn_s_getreg(kHwRegXccId | (0 << 6) | ((4 - 1) << 11)) & (kXcds - 1);
+}
+
+// The wave's HW_ID register: wave slot, SIMD, compute unit, shader array and shader engine.
+__device__ __forceinline__ uint32_t hw_id() {
+  constexpr int kHwRegHwId = 4;
+  return (uint32_t)__builtin_amdgcn_s_getreg(kHwRegHwId | (0 << 6) | ((32 - 1) << 11));
 }
 
 // Claims the next item of this launch: from queue q (initially the workgroup's own XCD's),
@@ -621,13 +630,16 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
   __builtin_amdgcn_s_setprio(3);
   uint32_t q = xcc_id();  // meaningful in thread 0, which does the claiming
   const uint32_t end = (uint32_t)a.queue[kXcds];
+  const uint64_t t_start = ticks();
   if (tid == 0) {
     words[0] = claim_item(a, q, end);
     if (words[0] < end) atomicAdd(a.active, 1u);
   }
   __syncthreads();
   uint32_t cur = __builtin_amdgcn_readfirstlane(words[0]);  // uniform: item fields stay scalar
+  int32_t n_items = 0;
   while (cur < end) {
+    ++n_items;
     __syncthreads();  // every wave has read the word before the operand ring overwrites it
     // Claim the next item now; thread 0 holds its index while this one runs and passes it
     // on through LDS once the operand ring is no longer in use.
@@ -646,6 +658,22 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
     if (tid == 0) words[0] = next;
     __syncthreads();
     cur = __builtin_amdgcn_readfirstlane(words[0]);
+  }
+  if (a.wg_rec && tid == 0) {  // timestamped runs: where and when this workgroup ran
+    // The last item is done (a signalled down item has also waited for its stores).
+    const uint64_t t_end = ticks();
+    WgRecord r;
+    r.hw_id = hw_id();
+    r.xcc_id = xcc_id();
+    r.launch = down ? 1 : 0;
+    r.items = n_items;
+    r.t_start = t_start;
+    r.t_end = t_end;
+    a.wg_rec[blockIdx.x] = r;
+    if (down)
+      __hip_atomic_fetch_max(&a.ctr->prod_t1, t_end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      __hip_atomic_fetch_min(&a.ctr->prod_t0, t_start, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -721,31 +749,83 @@ __global__ __launch_bounds__(kProducerThreads) void tail_kernel(TailArgs ta) {
         const int tile = t * dpr + col;
         const uint32_t prev =
             __hip_atomic_fetch_add(&a.arrivals[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (prev + 1 == (uint32_t)kBlocks)
+        if (prev + 1 == (uint32_t)kBlocks) {
+          if (a.tile_ready) a.tile_ready[tile] = ticks();
           __hip_atomic_store(&a.flags[tile], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
       }
     }
+  }
+  if (a.wg_rec && n_pass > 0) {  // timestamped runs: the producer ends with its last tail pass
+    wait_vm_and_barrier<0>();
+    if (tid == 0) __hip_atomic_fetch_max(&a.ctr->prod_t1, ticks(), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
 // ---------------------------------------------------------------------------
-// Consumer: every wave works alone.  It takes a copy unit -- a quarter of a segment, or up to a
-// sixteenth of one that becomes ready in the down launch's last two rounds, in the segments'
-// ready order -- polls the segment's flags (one flag per lane; all must show the current
-// epoch), then copies its part with 16-byte loads and stores.  The kernel uses no
-// LDS, so in a shared-CU run its workgroups never keep a producer workgroup (which takes all
-// of LDS) off a compute unit.  A copying wave slows the producer workgroup on its compute
-// unit, so the units are spread: the first ones go one per workgroup (the parts of a segment to
-// different workgroups), and a wide consumer grid puts about one copying wave on each compute
-// unit instead of four on each of a few.
+// Consumer: every wave works alone.  It claims a copy unit -- one of a segment's 2^shift equal
+// parts, in the segments' ready order -- polls the segment's flags (one flag per lane; all
+// must show the current epoch), then copies its part with 16-byte loads and stores.  The
+// kernel uses no LDS, so in a shared-CU run its workgroups never keep a producer workgroup
+// (which takes all of LDS) off a compute unit.
+//
+// kOwn = false (beside the producer): at most 64 VGPRs per wave, so two consumer waves fit
+// beside a producer wave on a SIMD, and at most kMaxConsumerWavesPerSimd consumer waves stay on
+// a SIMD: a wave that finds more already there exits at once, so consumer waves that happened to
+// pile onto one compute unit before the producer arrived never keep a producer workgroup off it.
+// A copying wave slows the producer workgroup on its compute unit, so the units are spread: the
+// first tickets are dealt transposed (ticket 4b + w to unit w x grid + b), so the waves of one
+// workgroup, which claim together, take parts of different segments, about one copying wave
+// per compute unit.  kOwn = true (compute units of its own): up to 128 VGPRs, twice the data in
+// flight per wave.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_kernel(ConsumerArgs a) {
+
+// Copies n 16-byte vectors from src to dst, kU per lane per chunk, with two register buffers in
+// turn so one chunk's loads are in flight while the other's stores issue.
+template <int kU>
+__device__ __forceinline__ void copy_vectors(const u32x4* __restrict__ src, g_u32x4* __restrict__ dst, int64_t n,
+                                             int lane) {
+  constexpr int64_t kStep = (int64_t)kU * 64;
+  const int64_t nfull = n / kStep;
+  u32x4 a[kU], b[kU];
+  auto load = [&](u32x4 (&r)[kU], int64_t c) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) r[u] = src[c * kStep + lane + u * 64];
+  };
+  auto store = [&](const u32x4 (&r)[kU], int64_t c) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) dst[c * kStep + lane + u * 64] = r[u];
+  };
+  if (nfull > 0) {
+    load(a, 0);
+    int64_t c = 0;
+    for (; c + 1 < nfull; c += 2) {
+      load(b, c + 1);
+      store(a, c);
+      if (c + 2 < nfull) load(a, c + 2);
+      store(b, c + 1);
+    }
+    if (c < nfull) store(a, c);
+  }
+  for (int64_t i = nfull * kStep + lane; i < n; i += 64) dst[i] = src[i];
+}
+
+template <bool kOwn>
+__global__ __launch_bounds__(kConsumerThreads, kOwn ? kConsumerOwnMinWaves : kConsumerMinWaves)
+void consumer_kernel(ConsumerArgs a) {
   const int lane = threadIdx.x & 63;
+  if (!kOwn && a.simd_waves) {
+    // hw_id: SIMD [5:4], compute unit [11:8], shader array [12], shader engine [15:13].
+    uint32_t before = 0;
+    if (lane == 0) {
+      const uint32_t h = hw_id();
+      const uint32_t key = ((((h >> 13) & 7u) * 2 + ((h >> 12) & 1u)) * 16 + ((h >> 8) & 15u)) * 4 + ((h >> 4) & 3u);
+      before = atomicAdd(&a.simd_waves[xcc_id() * kSimdKeys + key], 1u);
+    }
+    if (__builtin_amdgcn_readfirstlane(before) >= (uint32_t)kMaxConsumerWavesPerSimd) return;
+  }
   const int32_t n_segs = *a.n_segs;
-  // A wave's first unit is fixed, (wave of its workgroup) x grid + workgroup; later units are
-  // claimed from the counter, after all the fixed ones.
   const uint32_t n_waves = gridDim.x * (kConsumerThreads / 64);
-  uint32_t unit = (threadIdx.x >> 6) * gridDim.x + blockIdx.x;
   // Segments are in ready order: the first late one by binary search (uniform loads).
   const int32_t late_from = *a.down_qmax - kLatePositions;
   int32_t n_early = 0;
@@ -756,22 +836,22 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
     else
       hi = mid;
   }
-  // A late segment's units hold about 128 KiB of each 256-row piece: H / 256 of them rounded
-  // down to a power of two within [kCopyParts, kCopyPartsLate], so a part's range is a shift.
-  const int32_t late_shift =
-      min(max(31 - __builtin_clz((uint32_t)max(a.H / 256, 1)), kCopyPartsShift), kCopyPartsLateShift);
-  const uint32_t early_units = (uint32_t)n_early << kCopyPartsShift;
+  const int32_t early_shift = a.early_shift, late_shift = a.late_shift;
+  const uint32_t early_units = (uint32_t)n_early << early_shift;
   const uint32_t n_units = early_units + ((uint32_t)(n_segs - n_early) << late_shift);
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.ctr->n_units = n_units;
+  const uint32_t last_ticket = max(n_waves, n_units);
   uint64_t polls = 0, waited = 0;
-  for (bool first = true;; first = false) {
-    if (!first) {
-      if (lane == 0) unit = n_waves + atomicAdd(&a.ctr->seg_next, 1u);
-      unit = __builtin_amdgcn_readfirstlane(unit);  // every lane is active here
-    }
-    if (unit >= n_units) break;
+  for (;;) {
+    uint32_t t = 0;
+    if (lane == 0) t = atomicAdd(&a.ctr->seg_next, 1u);
+    t = __builtin_amdgcn_readfirstlane(t);  // every lane is active here
+    if (t >= last_ticket) break;
+    const uint32_t unit = t < n_waves ? (t % (kConsumerThreads / 64)) * gridDim.x + t / (kConsumerThreads / 64) : t;
+    if (unit >= n_units) continue;
     const bool early = unit < early_units;
     const uint32_t u = early ? unit : unit - early_units;
-    const int32_t shift = early ? kCopyPartsShift : late_shift;
+    const int32_t shift = early ? early_shift : late_shift;
     const int32_t s = (early ? 0 : n_early) + (int32_t)(u >> shift);
     const int32_t part = (int32_t)(u & ((1u << shift) - 1));
     const Segment sg = a.segs[s];
@@ -797,43 +877,38 @@ __global__ __launch_bounds__(kConsumerThreads, kConsumerMinWaves) void consumer_
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    waited += ticks() - t0;
+    const uint64_t t_ready = ticks();
+    waited += t_ready - t0;
     if (expired) {
       if (lane == 0) {
         __hip_atomic_fetch_add(&a.ctr->timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_fetch_or(&a.ctr->timeout_where, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_min(&a.ctr->timeout_seg, (uint32_t)s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       break;
     }
-    // The segment is contiguous on both sides: this wave's part is a flat run of 16-byte
-    // vectors, copied in chunks of kCopyUnroll vectors per lane, double-buffered: the next
-    // chunk's loads are in flight while the current chunk is stored.  The last chunk re-reads
-    // itself as its "next" (in bounds) instead of branching, which would drain every
-    // outstanding access.
+    // The segment is contiguous on both sides: this wave's part is a flat run of 16-byte vectors.
     const int64_t n16 = (int64_t)sg.rows * a.H / 8;
     const int64_t i0 = (n16 * part) >> shift, i1 = (n16 * (part + 1)) >> shift;
     const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H) + i0;
     g_u32x4* dst = (g_u32x4*)(a.ret[sg.dst_rank] + (int64_t)sg.slot0 * a.H) + i0;
-    const int64_t n = i1 - i0;
-    constexpr int kU = kCopyUnroll;
-    constexpr int64_t kStep = (int64_t)kU * 64;
-    const int64_t nfull = n / kStep;
-    if (nfull > 0) {
-      u32x4 cur[kU], nxt[kU];
-#pragma unroll
-      for (int u = 0; u < kU; ++u) cur[u] = src[lane + u * 64];
-      for (int64_t c = 0; c < nfull; ++c) {
-        const int64_t base = c * kStep + lane;
-        const int64_t next = (c + 1 < nfull ? c + 1 : c) * kStep + lane;
-#pragma unroll
-        for (int u = 0; u < kU; ++u) nxt[u] = src[next + u * 64];
-#pragma unroll
-        for (int u = 0; u < kU; ++u) dst[base + u * 64] = cur[u];
-#pragma unroll
-        for (int u = 0; u < kU; ++u) cur[u] = nxt[u];
+    copy_vectors<kOwn ? kCopyUnrollOwn : kCopyUnroll>(src, dst, i1 - i0, lane);
+    if (a.rec && unit < a.rec_cap) {
+      // Timestamped runs: the unit ends when its stores have completed.
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      const uint64_t t_done = ticks();
+      if (lane == 0) {
+        CopyRecord r;
+        r.segment = s;
+        r.part = part;
+        r.hw_id = hw_id();
+        r.xcc_id = xcc_id();
+        r.t_poll = t0;
+        r.t_ready = t_ready;
+        r.t_done = t_done;
+        a.rec[unit] = r;
       }
     }
-    for (int64_t i = nfull * kStep + lane; i < n; i += 64) dst[i] = src[i];
   }
   if (lane == 0 && (polls || waited)) {
     atomicAdd((unsigned long long*)&a.ctr->poll_iters, (unsigned long long)polls);
@@ -869,6 +944,9 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
     a.ctr->down_active = 0;
     a.ctr->poll_iters = 0;
     a.ctr->wait_ticks = 0;
+    a.ctr->n_units = 0;
+    a.ctr->prod_t0 = ~0ull;
+    a.ctr->prod_t1 = 0;
     if (a.plan_hdr) {
       a.plan_hdr->status = 0;
       a.plan_hdr->bad_row = INT_MAX;
@@ -877,6 +955,10 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
   if (a.fill_ones)
     for (int64_t j = i; j < a.n_fill_ones; j += stride) a.fill_ones[j] = ~0u;
   for (int64_t j = i; j < a.n_arrivals; j += stride) a.arrivals[j] = 0;
+  if (a.tile_ready)
+    for (int64_t j = i; j < a.n_arrivals; j += stride) a.tile_ready[j] = 0;
+  if (a.simd_waves)
+    for (int64_t j = i; j < kXcds * kSimdKeys; j += stride) a.simd_waves[j] = 0;
   if (a.publish)
     for (int64_t j = i; j < a.n_publish; j += stride) a.publish[j] = a.epoch;
   if (a.poison) {
@@ -911,8 +993,11 @@ hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream
   return hipGetLastError();
 }
 
-hipError_t launch_consumer(const ConsumerArgs& a, int grid, hipStream_t s) {
-  hipLaunchKernelGGL(consumer_kernel, dim3(grid), dim3(kConsumerThreads), 0, s, a);
+hipError_t launch_consumer(const ConsumerArgs& a, bool own_cus, int grid, hipStream_t s) {
+  if (own_cus)
+    hipLaunchKernelGGL(consumer_kernel<true>, dim3(grid), dim3(kConsumerThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(consumer_kernel<false>, dim3(grid), dim3(kConsumerThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -14,6 +14,26 @@ constexpr uint32_t kModeDirectAll = 4u;    // every row goes straight to its rec
 constexpr uint32_t kModeDeferTail = 8u;    // split tail tiles: parts only store their partials; the
                                            // tail kernel after the launch adds them and writes the tiles
 
+// Timestamped runs: one record per producer workgroup of each launch (where it ran, how many
+// items it took, when it started and ended; 100 MHz wall clock) and one per consumer copy unit.
+struct WgRecord {
+  uint32_t hw_id;   // HW_ID register of wave 0 (wave, SIMD, CU, shader array and engine ids)
+  uint32_t xcc_id;  // XCD the workgroup ran on
+  int32_t launch;   // 0 gate/up, 1 down
+  int32_t items;    // work items it ran
+  uint64_t t_start, t_end;
+};
+struct CopyRecord {
+  int32_t segment;  // segment index (ready order)
+  int32_t part;     // copy unit within the segment
+  uint32_t hw_id;   // HW_ID register of the copying wave
+  uint32_t xcc_id;
+  uint64_t t_poll;  // the wave starts polling the segment's flags
+  uint64_t t_ready; // every flag seen, acquire done: the copy starts
+  uint64_t t_done;  // the wave's copy stores have completed
+};
+static_assert(sizeof(WgRecord) == 32 && sizeof(CopyRecord) == 40, "record layouts are part of the ABI");
+
 struct ProducerArgs {
   const uint16_t* x;       // [rows, H] dispatched tokens
   const uint16_t* w1;      // [E_l, F, H]
@@ -39,6 +59,9 @@ struct ProducerArgs {
   int32_t split_k;         // K parts of every down tile; 0 = per tile row (TileRow::split)
   float* partials;         // fp32 part tiles (256 threads x 256) from TileRow::part_base on
   uint32_t* arrivals;      // [tiles] parts finished this run (zeroed by the init kernel)
+  WgRecord* wg_rec;        // timestamped runs: [grid] records of this launch, else null
+  RunCounters* ctr;        // timestamped runs: the producer span (prod_t0 / prod_t1)
+  uint64_t* tile_ready;    // timestamped runs: [tiles] when each down tile's flag was raised
 };
 
 // The tail kernel: finishes the split down tiles after the down launch.  Reads the plan's tile
@@ -59,8 +82,14 @@ struct ConsumerArgs {
   const uint32_t* flags;
   uint32_t epoch;
   int32_t H;
+  // Copy units per segment, as powers of two: segments ready before the down launch's last two
+  // rounds take 2^early_shift units, later ones 2^late_shift.
+  int32_t early_shift, late_shift;
   RunCounters* ctr;
   uint64_t watchdog_ticks;
+  CopyRecord* rec;         // timestamped runs: one record per copy unit below rec_cap, else null
+  uint32_t rec_cap;
+  uint32_t* simd_waves;    // beside the producer: [kXcds * kSimdKeys] consumer waves per SIMD
 };
 
 struct ScatterArgs {
@@ -78,6 +107,8 @@ struct InitArgs {
   int64_t poison_elems;    // multiple of 8
   uint32_t* arrivals;      // split-K arrival counters to zero
   int32_t n_arrivals;
+  uint64_t* tile_ready;    // optional: per-tile flag times to zero (as many as arrivals)
+  uint32_t* simd_waves;    // optional: consumer per-SIMD wave counts to zero
   uint32_t* publish;       // optional: ready flags to set to `epoch` (consumer-only measurement)
   int32_t n_publish;
   uint32_t epoch;
@@ -85,6 +116,7 @@ struct InitArgs {
   int64_t n_fill_ones;
   PlanHeader* plan_hdr;    // optional: header the device planner fills; reset to no error
 };
+
 
 struct CombineArgs {
   const uint16_t* recv;    // [recv_rows, H] receive buffer of this source rank
@@ -101,7 +133,8 @@ hipError_t launch_init(const InitArgs& a, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 // Gate/up tiles (down = false) or down-projection tiles with ready flags (down = true).
 hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream_t s);
-hipError_t launch_consumer(const ConsumerArgs& a, int grid, hipStream_t s);
+// own_cus: the consumer has its compute units to itself (a reserved partition, or no producer).
+hipError_t launch_consumer(const ConsumerArgs& a, bool own_cus, int grid, hipStream_t s);
 // Split tail tiles of a kModeDeferTail down launch: one accumulator block of one tile per pass.
 hipError_t launch_tail(const TailArgs& a, int grid, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s);
@@ -111,16 +144,23 @@ hipError_t launch_stamp(uint64_t* dst, hipStream_t s);
 int producer_blocks_per_cu();
 constexpr int kProducerThreads = 256;
 constexpr int kConsumerThreads = 256;
-constexpr int kCopyUnroll = 4;  // 16-byte vectors per consumer lane and copy chunk
+// 16-byte vectors per consumer lane and copy chunk (two chunks in flight): beside the producer,
+// within 64 VGPRs; on compute units of its own, within 128.
+constexpr int kCopyUnroll = 5;
+constexpr int kCopyUnrollOwn = 12;
+// Consumer copy units (one wave each) per segment, as a power of two.  Beside the producer
+// (shared compute units) a copying wave slows the producer workgroup on its compute unit, so
+// segments take few units (kCopyPartsShift) until the last two rounds of the down queues
+// (kLatePositions positions: two rounds of an XCD's 32 compute units), after which little
+// producer work is left and the last segments take up to kCopyPartsLateShift units each.  On
+// compute units of its own the consumer cuts every segment into units of about 64 KiB (at
+// most kCopyPartsOwnShift), so its waves copy in parallel whatever the segment count.
 constexpr int kCopyPartsShift = 2;
-constexpr int kCopyParts = 1 << kCopyPartsShift;  // consumer copy units (one wave each) per segment
-// Segments ready in the last kLatePositions positions of the down queues (two rounds of an
-// XCD's 32 compute units) are copied after most of the producer's work is done, some of them
-// after all of it: they take up to kCopyPartsLate units each, so more waves share the final
-// copies.
 constexpr int kCopyPartsLateShift = 4;
-constexpr int kCopyPartsLate = 1 << kCopyPartsLateShift;
+constexpr int kCopyPartsOwnShift = 6;
 constexpr int kLatePositions = 64;
+// Copy records a timestamped handle keeps per run (units past it are not recorded).
+constexpr uint32_t kMaxCopyRecords = 1u << 18;
 // Consumer flag polls sleep kPollSleep x 64 cycles, doubling the count of sleeps per poll up to
 // kPollBackoffMax (about 2.5 us between polls at the loaded clock).
 constexpr int kPollSleep = 4;
@@ -129,5 +169,12 @@ constexpr int kTailGrid = 1024; // tail kernel workgroups (one pass each on the 
 // Consumer waves per SIMD the register budget must allow: at most 512 / 8 = 64 VGPRs each, so
 // two consumer waves fit beside one producer wave of up to 384 of the 512 registers.
 constexpr int kConsumerMinWaves = 8;
+// Consumer waves a SIMD keeps beside the producer (the register budget above), counted per SIMD
+// key (shader engine, shader array, compute unit, SIMD) of each XCD.
+constexpr int kMaxConsumerWavesPerSimd = 2;
+constexpr int kSimdKeys = 1024;
+// On compute units of its own: up to 128 VGPRs, four waves per SIMD (four workgroups per CU).
+constexpr int kConsumerOwnMinWaves = 4;
+constexpr int kConsumerOwnPerCu = 4;
 
 }  // namespace moe

@@ -99,13 +99,19 @@ struct RunCounters {
   uint32_t gu_next[kXcds];    // gate/up work queue heads, one per XCD
   uint32_t down_next[kXcds];  // down-projection work queue heads
   uint32_t seg_next;          // consumer copy-unit queue head
-  uint32_t timeouts;          // bounded waits that expired; NOT reset per run (cleared by a query)
-  uint32_t timeout_where;     // bit 0 = consumer flag wait, bit 1 = producer dependency wait
+  // Watchdog reports, NOT reset per run (a query reads and clears them, so they are sticky):
+  uint32_t timeouts;          // bounded waits that expired
+  uint32_t timeout_where;     // bit 0 = consumer flag wait
+  uint32_t timeout_seg;       // lowest segment (ready order) whose wait expired; UINT32_MAX if none
   uint32_t gu_active;         // gate/up workgroups that claimed at least one tile
   uint32_t down_active;       // down workgroups that claimed at least one tile
-  uint32_t pad0[3];
+  uint32_t n_units;           // consumer copy units of the run (written by the consumer)
+  uint32_t pad0;
   uint64_t poll_iters;        // consumer poll iterations
   uint64_t wait_ticks;        // consumer wait time, 100 MHz ticks
+  // Timestamped runs only (100 MHz wall clock): first gate/up workgroup start and last
+  // producer (down or tail) workgroup end.
+  uint64_t prod_t0, prod_t1;
 };
 
 }  // namespace moe

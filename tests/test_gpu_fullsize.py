@@ -1,22 +1,27 @@
 """Full-size GPU parity at the workload sizes the benchmark uses, in its launch configuration.
 
-The oracle computes a seeded sample of routed rows one by one; placement (every
-routed slot written, nothing else touched) and serial == overlapped bitwise are
-checked on every row, since they hold at any size.
+Placement (every routed slot written, nothing else touched) and bitwise equality across
+consumer splits, CU modes and the serial path hold at any size and are checked on every row.
+Values are checked against the oracle, row by row, on a stratified sample drawn from the
+plan the GPU ran: at least one routed row of every 256-row tile row, of every (expert,
+source rank) owner group (so every local expert's weights and the local-direct rows), every
+row of the first split tile row (the K-split tail, whose parts a tail kernel adds), and
+random rows on top.  Each sampled row is checked on all hidden columns, so every 256-column
+down tile is covered.
 """
 import numpy as np
 import pytest
 
 from paper_2607_19539_amd import binding as B
 from paper_2607_19539_amd.workload import make_workload
-from tests.gpu_helpers import DeviceWorkload, compare, log, make_stage, oracle_bufs, SENTINEL
+from tests.gpu_helpers import DeviceWorkload, compare, log, make_stage, SENTINEL
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 BENCH_CU_SPLIT = 248
 BENCH_FLAGS = B.MOE_LOCAL_DIRECT | B.MOE_SHARED_CUS   # bench.py's default mode, on its own stream
-SAMPLE_ROWS = 24
+RANDOM_ROWS = 24
 
 
 def written_mask(buf_dev):
@@ -24,9 +29,62 @@ def written_mask(buf_dev):
     return (~(buf_dev == s).all(dim=1)).cpu().numpy()
 
 
+def stratified_rows(wl, plan, seed=3):
+    """Dispatched-row indices of the value sample, and how many each stratum contributed."""
+    g = np.random.default_rng(seed)
+    tr = plan["tile_rows"]            # expert, lrow0, nvalid, has_remote, split, part_base
+    row_x, row_rank = plan["row_x"], plan["row_rank"]
+    picked = set()
+    counts = {"tile_rows": 0, "groups": 0, "split_tail_rows": 0, "local_rows": 0, "random": 0}
+    for t in range(len(tr)):
+        l0 = int(tr[t, 1])
+        valid = np.nonzero(row_rank[l0:l0 + 256] >= 0)[0]
+        if len(valid):
+            picked.add(int(row_x[l0 + int(g.choice(valid))]))
+            counts["tile_rows"] += 1
+    split = [t for t in range(len(tr)) if int(tr[t, 4]) > 1]
+    if split:
+        l0 = int(tr[split[0], 1])
+        for lr in range(l0, l0 + 256):
+            if row_rank[lr] >= 0:
+                picked.add(int(row_x[lr]))
+                counts["split_tail_rows"] += 1
+    e_of = np.searchsorted(wl.expert_offsets, np.arange(wl.rows), side="right") - 1
+    for e in range(wl.E_l):
+        for r in range(wl.R):
+            rows = np.nonzero((e_of == e) & (wl.row_src_rank == r))[0]
+            if len(rows):
+                picked.add(int(g.choice(rows)))
+                counts["groups"] += 1
+                counts["local_rows"] += int(r == wl.self_rank)
+    for i in g.choice(wl.rows, size=min(RANDOM_ROWS, wl.rows), replace=False):
+        picked.add(int(i))
+        counts["random"] += 1
+    return np.array(sorted(picked), np.int64), counts, len(split)
+
+
+def compact_oracle(wl, idx):
+    """Oracle outputs of the rows `idx` with each source rank's slots renumbered densely (the
+    oracle computes every row on its own, so the values are those of the full stage)."""
+    from oracle import oracle as orc
+    sub = wl.subset(idx)
+    slot = np.empty(sub.rows, np.int32)
+    rows = np.zeros(wl.R, np.int64)
+    for r in range(wl.R):
+        m = np.nonzero(sub.row_src_rank == r)[0]
+        order = m[np.argsort(sub.row_slot[m], kind="stable")]
+        slot[order] = np.arange(len(order), dtype=np.int32)
+        rows[r] = len(order)
+    bufs = [np.full((int(n), wl.H), SENTINEL, np.uint16) for n in rows]
+    rc = orc.get().run(wl.H, wl.F, wl.E_l, wl.R, wl.self_rank, sub.dispatched_x, sub.expert_offsets,
+                       sub.row_src_rank, slot, wl.w1, wl.w3, wl.w2, bufs, rows, 0)
+    assert rc == 0, rc
+    return sub, slot, bufs
+
+
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("name", ["mixtral", "mixtral_zipf", "fine", "large_fine"])
-def test_fullsize_sampled(name):
+@pytest.mark.parametrize("name", ["mixtral", "mixtral_zipf", "fine", "large_fine", "layer_e4", "layer_e64"])
+def test_fullsize_stratified(name):
     log(f"full-size {name}: generating")
     wl = make_workload(name)
     log(f"full-size {name}: rows={wl.rows}")
@@ -38,8 +96,10 @@ def test_fullsize_sampled(name):
         st.run(*dw.args(), cu_split=BENCH_CU_SPLIT, stream=side)
         torch.cuda.synchronize()
         stats = st.query()
-        log(f"full-size {name}: overlapped done, segments={stats['n_segments']} tiles={stats['n_tile_rows']} "
-            f"split_k={stats['split_k']} workgroups={stats['gu_workgroups']}/{stats['down_workgroups']}")
+        plan = st.plan()
+        log(f"full-size {name}: overlapped done, segments={stats['n_segments']} units={stats['copy_units']} "
+            f"tiles={stats['n_tile_rows']} split_k={stats['split_k']} workgroups={stats['gu_workgroups']}/"
+            f"{stats['down_workgroups']}")
         assert stats["timeout"] == 0
         # placement on every row: exactly the routed slots are written
         for r in range(wl.R):
@@ -47,14 +107,14 @@ def test_fullsize_sampled(name):
             want[wl.row_slot[wl.row_src_rank == r]] = True
             assert np.array_equal(written_mask(dw.bufs[r]), want), f"rank {r} placement"
         over = [b.clone() for b in dw.bufs]
-        # A narrow consumer: four copy units per segment, far more than its waves, so most
-        # units are claimed from the counter after each wave's fixed first one.
+        # A narrow consumer beside the producer: most units are claimed from the counter after
+        # each wave's fixed first one.
         dw.fill()
         torch.cuda.synchronize()
         st.run(*dw.args(), cu_split=8, stream=side)
         torch.cuda.synchronize()
         narrow = st.query()
-        log(f"full-size {name}: c=8 units={4 * narrow['n_segments']} consumer waves={4 * narrow['consumer_grid']}")
+        log(f"full-size {name}: c=8 shared units={narrow['copy_units']} consumer waves={4 * narrow['consumer_grid']}")
         assert narrow["timeout"] == 0
         for a, b in zip(over, dw.bufs):
             assert torch.equal(a, b), "consumer splits differ"
@@ -65,17 +125,30 @@ def test_fullsize_sampled(name):
         st.query()
         for a, b in zip(over, dw.bufs):
             assert torch.equal(a, b), "serial and overlapped differ"
-        del over
-    # values on a seeded sample of rows, against the oracle row by row
-    sub = wl.sample(SAMPLE_ROWS, seed=3)
-    ref = oracle_bufs(sub)
+    # The consumer on compute units of its own cuts segments into ~64 KiB units.
+    with make_stage(wl, flags=B.MOE_LOCAL_DIRECT) as st:
+        dw.fill()
+        torch.cuda.synchronize()
+        st.run(*dw.args(), cu_split=32, stream=side)
+        torch.cuda.synchronize()
+        part = st.query()
+        log(f"full-size {name}: c=32 partitioned units={part['copy_units']} segments={part['n_segments']}")
+        assert part["timeout"] == 0
+        for a, b in zip(over, dw.bufs):
+            assert torch.equal(a, b), "partitioned consumer differs"
+    del over
+    idx, counts, n_split = stratified_rows(wl, plan)
+    log(f"full-size {name}: value sample {len(idx)} rows: {counts} ({n_split} split tile rows in the plan)")
+    assert counts["tile_rows"] == int((plan["tile_rows"][:, 2] > 0).sum())
+    assert n_split == 0 or counts["split_tail_rows"] > 0
+    sub, slot, ref = compact_oracle(wl, idx)
     got = []
     for r in range(wl.R):
-        g = np.full((int(wl.return_rows[r]), wl.H), SENTINEL, np.uint16)
-        slots = sub.row_slot[sub.row_src_rank == r]
-        if len(slots):
-            idx = torch.from_numpy(slots.astype(np.int64)).to("cuda")
-            g[slots] = dw.bufs[r].index_select(0, idx).cpu().numpy().view(np.uint16)
+        m = np.nonzero(sub.row_src_rank == r)[0]
+        g = np.full((len(m), wl.H), SENTINEL, np.uint16)
+        if len(m):
+            rows = torch.from_numpy(sub.row_slot[m].astype(np.int64)).to("cuda")
+            g[slot[m]] = dw.bufs[r].index_select(0, rows).cpu().numpy().view(np.uint16)
         got.append(g)
     worst, worst_rel = compare(got, ref)
     log(f"full-size {name}: sampled max scaled err {worst:.2e}, max row rel-L2 {worst_rel:.2e}")
@@ -84,17 +157,22 @@ def test_fullsize_sampled(name):
 @pytest.mark.timeout(300)
 def test_watchdog_expiry_is_reported():
     """With ready flags suppressed from the host, the consumer's bounded wait expires, the
-    kernels exit, the run reports MOE_ETIMEOUT, and the next run on a fresh handle is correct."""
+    kernels exit, the run reports MOE_ETIMEOUT with the first segment that expired, and the next
+    run on a fresh handle is correct."""
+    from tests.gpu_helpers import oracle_bufs
     wl = make_workload("tiny", owner=1)
     dw = DeviceWorkload(torch, wl)
     with make_stage(wl, flags=B.MOE_LOCAL_DIRECT | B.MOE_TEST_NO_SIGNAL, watchdog_ms=20) as st:
         st.run(*dw.args(), cu_split=8)
         q = st.query(check=False)
         assert q["rc"] == B.MOE_ETIMEOUT and q["timeout"] == 1
-        assert st.query()["timeout"] == 0   # reported once
+        assert 0 <= q["timeout_segment"] < q["n_segments"]
+        assert "segment" in B.moe_stage_last_error(st.h)
+        q2 = st.query()
+        assert q2["timeout"] == 0   # reported once
     ref = oracle_bufs(wl)
     with make_stage(wl) as st:
         dw.fill()
         st.run(*dw.args(), cu_split=8)
-        st.query()
+        assert st.query()["timeout_segment"] == -1
     compare(dw.host_bufs(), ref)

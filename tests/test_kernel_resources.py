@@ -51,7 +51,11 @@ def test_no_kernel_spills(kernels):
 
 
 def test_consumer_fits_beside_a_producer_wave(kernels):
-    (cons,) = by_name(kernels, "consumer_kernel").values()
+    """The shared-CU consumer variant (kOwn = false) leaves a producer wave its registers; the
+    variant for compute units of its own keeps four waves per SIMD."""
+    (cons,) = by_name(kernels, "consumer_kernelILb0E").values()
+    (own,) = by_name(kernels, "consumer_kernelILb1E").values()
+    assert int(own["vgpr_count"]) <= 128
     granule = 8  # registers are allocated to a wave in blocks of 8
     cons_alloc = -(-int(cons["vgpr_count"]) // granule) * granule
     budget = SIMD_REGISTERS - CONSUMER_WAVES_BESIDE_PRODUCER * cons_alloc
@@ -78,8 +82,8 @@ def test_combine_variants_present(kernels):
 def test_consumer_leaves_lds_to_the_producer(kernels):
     """A producer workgroup takes all of a CU's LDS; a consumer workgroup holding any LDS would
     keep producer workgroups off the compute units the two are meant to share."""
-    (cons,) = by_name(kernels, "consumer_kernel").values()
-    assert int(cons["group_segment_fixed_size"]) == 0
+    for cons in by_name(kernels, "consumer_kernel").values():
+        assert int(cons["group_segment_fixed_size"]) == 0
     for name, f in by_name(kernels, "producer_kernel").items():
         assert int(f["group_segment_fixed_size"]) == 160 * 1024, name
 
