@@ -253,6 +253,31 @@ int moe_stage_run_serial_devplan(moe_stage_t h, const void* dispatched_x,
                                  const void* w2, void* const* return_bufs,
                                  const int64_t* return_rows, void* stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): the non-overlapped run of
+ * moe_stage_run_serial_devplan without a handle.  Arguments are those of
+ * moe_stage_run_serial_devplan with the configuration in place of the handle (routing in device
+ * memory, in the order a dispatch all-to-all delivers it).  Every workspace (activations, staged
+ * output, K-part partials, counters, plan tables, planner scratch) lives in one fixed device
+ * array of MOE_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs on until the
+ * process ends; the call allocates nothing: no hipMalloc, hipFree, stream, event or pinned host
+ * memory.  It enqueues on `stream` (a hipStream_t; NULL = null stream) and returns; the two
+ * receive-buffer tables go up with hipMemcpyAsync from the caller's host arrays.  Every call on
+ * a GPU shares that GPU's array and leaves its contents behind (each run's kernels reset what
+ * must start at zero): calls that overlap on one GPU -- on different streams, or from different
+ * threads -- race and must not be made.  Errors: MOE_ECAPACITY when the configuration's
+ * workspaces (sized by max_rows as for moe_stage_create) exceed the array, the other codes as
+ * for moe_stage_run_serial_devplan; routing errors found on the device leave return_bufs
+ * untouched.  The message is moe_stage_last_error(NULL).  Results are bit-identical to
+ * moe_stage_run_serial_devplan on a handle of the same configuration.
+ */
+#define MOE_STATIC_SCRATCH_BYTES (64u * 1024u * 1024u)
+int moe_stage_run_serial_static(const moe_stage_config_t* cfg, const void* dispatched_x,
+                                const int32_t* expert_offsets, const int32_t* row_src_rank,
+                                const int32_t* row_slot, const void* w1, const void* w3, const void* w2,
+                                void* const* return_bufs, const int64_t* return_rows, void* stream);
+
 /* Statistics of the last run; synchronizes with it.  Returns MOE_ETIMEOUT (once) if any run
  * since the previous query had a device wait expire; its outputs are then incomplete.  After a
  * device-planned run it returns the planner's routing error (once), if any; its plan counts

@@ -31,7 +31,8 @@ ERROR_NAMES = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EROUTING", -3: "MOE_ECAPA
 EXPORTED = ["moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query", "moe_stage_times",
             "moe_stage_last_error", "moe_stage_destroy", "moe_plan_build", "moe_plan_info", "moe_plan_copy",
             "moe_plan_free", "moe_combine", "moe_stage_run_devplan", "moe_stage_run_serial_devplan",
-            "moe_stage_plan_info", "moe_stage_plan_copy", "moe_stage_records"]
+            "moe_stage_plan_info", "moe_stage_plan_copy", "moe_stage_records", "moe_stage_run_serial_static"]
+MOE_STATIC_SCRATCH_BYTES = 64 * 1024 * 1024
 
 
 class moe_stage_config_t(ctypes.Structure):
@@ -143,6 +144,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.moe_stage_plan_info.argtypes = [vp, ctypes.POINTER(moe_plan_info_t)]
     lib.moe_stage_plan_copy.argtypes = [vp, i32, vp, i64]
     lib.moe_stage_plan_copy.restype = ctypes.c_int64
+    lib.moe_stage_run_serial_static.argtypes = [ctypes.POINTER(moe_stage_config_t), vp, vp, vp, vp, vp, vp, vp, vp,
+                                                vp, vp]
+    lib.moe_stage_run_serial_static.restype = ctypes.c_int
     lib.moe_stage_records.argtypes = [vp, i32, vp, i64]
     lib.moe_stage_records.restype = ctypes.c_int64
     for name in ("moe_combine", "moe_stage_create", "moe_stage_run", "moe_stage_run_serial", "moe_stage_query",
@@ -336,6 +340,17 @@ def moe_stage_run_serial_devplan(h, x, expert_offsets, row_src_rank, row_slot, w
     rc = load().moe_stage_run_serial_devplan(h, *args, _stream_ptr(stream))
     del keep
     return _check(rc, h)
+
+
+def moe_stage_run_serial_static(cfg: moe_stage_config_t, x, expert_offsets, row_src_rank, row_slot, w1, w3, w2,
+                                return_bufs: Sequence, return_rows=None, stream=None) -> int:
+    """moe_stage_run_serial_devplan without a handle: every workspace in the library's fixed
+    per-GPU array (no allocation); routing as int32 device tensors."""
+    args, keep = _run_args_dev(x, expert_offsets, row_src_rank, row_slot, w1, w3, w2, return_bufs, return_rows,
+                               cfg)
+    rc = load().moe_stage_run_serial_static(ctypes.byref(cfg), *args, _stream_ptr(stream))
+    del keep
+    return _check(rc)
 
 
 def moe_combine(recv, slot, gate, out, bad_slots=None, stream=None) -> int:

@@ -29,7 +29,8 @@ def build(verbose: bool = False) -> str:
         objs = []
         for src in SOURCES:
             obj = os.path.join(tmp, src + ".o")
-            lang = ["-x", "hip"] if src.endswith(".hip") else []
+            # api.cpp holds the no-allocation entry point's device array, so it is HIP source too.
+            lang = ["-x", "hip"] if src.endswith(".hip") or src == "api.cpp" else []
             cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
             _run(cmd, verbose)
             objs.append(obj)

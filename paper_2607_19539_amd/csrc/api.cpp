@@ -16,6 +16,7 @@
 
 #include <algorithm>
 #include <chrono>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -388,15 +389,21 @@ int prepare_device(moe_stage_s* h, bool overlapped, const void* x, const int32_t
     return set_err(h, MOE_EUNSUPPORTED, "hidden or ffn too large for the work-item encoding");
   *lay = h->cap_lay;
   const size_t R = (size_t)c.num_ranks;
-  const int si = h->stage_idx;
-  h->stage_idx ^= 1;
-  HIP_TRY(h, hipEventSynchronize(h->stage_free[si]));
-  uint8_t* hs = h->h_stage[si];
-  memcpy(hs, ret, sizeof(void*) * R);
-  memcpy(hs + sizeof(void*) * R, return_rows, sizeof(int64_t) * R);
-  HIP_TRY(h, hipMemcpyAsync(h->d_plan + lay->ret, hs, (sizeof(void*) + sizeof(int64_t)) * R,
-                            hipMemcpyHostToDevice, stream));
-  HIP_TRY(h, hipEventRecord(h->stage_free[si], stream));
+  if (h->h_stage[0]) {
+    const int si = h->stage_idx;
+    h->stage_idx ^= 1;
+    HIP_TRY(h, hipEventSynchronize(h->stage_free[si]));
+    uint8_t* hs = h->h_stage[si];
+    memcpy(hs, ret, sizeof(void*) * R);
+    memcpy(hs + sizeof(void*) * R, return_rows, sizeof(int64_t) * R);
+    HIP_TRY(h, hipMemcpyAsync(h->d_plan + lay->ret, hs, (sizeof(void*) + sizeof(int64_t)) * R,
+                              hipMemcpyHostToDevice, stream));
+    HIP_TRY(h, hipEventRecord(h->stage_free[si], stream));
+  } else {  // a handle without pinned staging (the no-allocation entry point): pageable copies
+    HIP_TRY(h, hipMemcpyAsync(h->d_plan + lay->ret, ret, sizeof(void*) * R, hipMemcpyHostToDevice, stream));
+    HIP_TRY(h, hipMemcpyAsync(h->d_plan + lay->ret + sizeof(void*) * R, return_rows, sizeof(int64_t) * R,
+                              hipMemcpyHostToDevice, stream));
+  }
   rc = enqueue_init(h, overlapped, true, h->max_tile_rows, h->max_lrows, stream);
   if (rc) return rc;
 
@@ -639,6 +646,39 @@ int ensure_streams(moe_stage_s* h, int c, bool need_prod) {
   return MOE_OK;
 }
 
+// Workspace sizes of a handle (its configuration set): the capacities every run fits in.
+struct WsBytes {
+  size_t hws, y, flags, partials, planner;
+};
+
+WsBytes size_workspaces(moe_stage_s* h) {
+  const moe_stage_config_t& c = h->cfg;
+  h->max_lrows = max_logical_rows(c.max_rows, c.num_local_experts, c.num_ranks, c.band_rows);
+  h->max_tile_rows = (int32_t)((h->max_lrows + kTileM - 1) / kTileM) + c.num_local_experts;
+  h->max_lrows = (int64_t)h->max_tile_rows * kTileM;
+  h->down_per_row = (c.hidden + kDownTileN - 1) / kDownTileN;
+  const int gu_per_row = (c.ffn + kGuTileF - 1) / kGuTileF;
+  const int32_t S = c.down_split_k;
+  // Down items: one per part of every tile (uniform split), or one per tile plus at most one
+  // round of parts for the split tail rows (default).
+  h->max_items = (int64_t)h->max_tile_rows * (gu_per_row + (int64_t)h->down_per_row * std::max(S, 1)) +
+                 (S == 0 ? kRoundTiles : 0);
+  // Segments: at most one per routed row.  Groups: one per (local expert, source rank).
+  h->cap_lay = blob_layout(h->max_tile_rows, h->max_items, h->max_lrows, h->max_lrows,
+                           (int64_t)c.num_local_experts * c.num_ranks, c.num_ranks);
+  h->plan_cap = h->cap_lay.total;
+  WsBytes b;
+  b.planner = devplan_ws_bytes(c.num_local_experts, c.num_ranks, c.max_rows, h->max_tile_rows, h->down_per_row,
+                               h->max_lrows, h->max_items);
+  b.hws = (size_t)h->max_lrows * c.ffn * 2;
+  b.y = (size_t)h->max_lrows * c.hidden * 2;
+  b.flags = (size_t)h->max_tile_rows * h->down_per_row * 4;
+  // One fp32 partial tile (256 threads x 256 accumulators) per K part of a split down tile.
+  b.partials = (size_t)max_partial_tiles(S, h->max_tile_rows, h->down_per_row, c.ffn / kTileK) * kProducerThreads *
+               256 * 4;
+  return b;
+}
+
 }  // namespace
 
 extern "C" {
@@ -669,24 +709,9 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       h->n_xcd < 1 || h->num_cus % h->n_xcd != 0)
     h->n_xcd = 1;
   h->producer_bpc = producer_blocks_per_cu();
-  h->max_lrows = max_logical_rows(cfg->max_rows, cfg->num_local_experts, cfg->num_ranks,
-                                  h->cfg.band_rows);
-  h->max_tile_rows = (int32_t)((h->max_lrows + kTileM - 1) / kTileM) + cfg->num_local_experts;
-  h->max_lrows = (int64_t)h->max_tile_rows * kTileM;
-  h->down_per_row = (cfg->hidden + kDownTileN - 1) / kDownTileN;
-  const int gu_per_row = (cfg->ffn + kGuTileF - 1) / kGuTileF;
-  const int32_t S = h->cfg.down_split_k;
-  // Down items: one per part of every tile (uniform split), or one per tile plus at most one
-  // round of parts for the split tail rows (default).
-  const int64_t max_items = (int64_t)h->max_tile_rows * (gu_per_row + (int64_t)h->down_per_row * std::max(S, 1)) +
-                            (S == 0 ? kRoundTiles : 0);
-  h->max_items = max_items;
-  // Segments: at most one per routed row.  Groups: one per (local expert, source rank).
-  h->cap_lay = blob_layout(h->max_tile_rows, max_items, h->max_lrows, h->max_lrows,
-                           (int64_t)cfg->num_local_experts * cfg->num_ranks, cfg->num_ranks);
-  h->plan_cap = h->cap_lay.total;
-  const size_t ws_bytes = devplan_ws_bytes(cfg->num_local_experts, cfg->num_ranks, cfg->max_rows,
-                                           h->max_tile_rows, h->down_per_row, h->max_lrows, max_items);
+  const WsBytes wb = size_workspaces(h);
+  const size_t ws_bytes = wb.planner, hws_bytes = wb.hws, y_bytes = wb.y, flag_bytes = wb.flags,
+               part_bytes = wb.partials;
 
   auto try_hip = [&](hipError_t err, const char* what) {
     if (err != hipSuccess) {
@@ -695,12 +720,6 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
     }
     return true;
   };
-  const size_t hws_bytes = (size_t)h->max_lrows * cfg->ffn * 2;
-  const size_t y_bytes = (size_t)h->max_lrows * cfg->hidden * 2;
-  const size_t flag_bytes = (size_t)h->max_tile_rows * h->down_per_row * 4;
-  // One fp32 partial tile (256 threads x 256 accumulators) per K part of a split down tile.
-  const size_t part_bytes =
-      (size_t)max_partial_tiles(S, h->max_tile_rows, h->down_per_row) * kProducerThreads * 256 * 4;
   if ((part_bytes && !try_hip(hipMalloc(&h->partials, part_bytes), "hipMalloc(partials)")) ||
       !try_hip(hipMalloc(&h->arrivals, flag_bytes), "hipMalloc(arrivals)") ||
       !try_hip(hipMemset(h->arrivals, 0, flag_bytes), "hipMemset(arrivals)") ||
@@ -731,7 +750,7 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       return bail(MOE_EHIP);
   }
   h->ws = devplan_ws_carve(h->dev_ws, cfg->num_local_experts, cfg->num_ranks, cfg->max_rows,
-                           h->max_tile_rows, h->down_per_row, h->max_lrows, max_items);
+                           h->max_tile_rows, h->down_per_row, h->max_lrows, h->max_items);
   // Every event here orders work on this device or marks completion for the host; none
   // publishes device writes to the host (results are read through the caller's own copies),
   // so a device-scope release suffices and no system-scope cache writeback sits between
@@ -925,7 +944,7 @@ static int run_serial(moe_stage_t h, bool dev, const void* x, const int32_t* off
     HIP_TRY(h, hipEventRecord(tr->ev[5], stream));
     tr->kind = 1;
   }
-  HIP_TRY(h, hipEventRecord(h->ev_done, stream));
+  if (h->ev_done) HIP_TRY(h, hipEventRecord(h->ev_done, stream));
   h->ran = true;
   h->counters_pending = true;
   return MOE_OK;
@@ -1213,6 +1232,77 @@ int moe_combine(const void* recv, int64_t recv_rows, int32_t hidden, const int32
   if (e != hipSuccess)
     return set_err(nullptr, MOE_EHIP, std::string("moe_combine launch: ") + hipGetErrorString(e));
   return MOE_OK;
+}
+
+// ----------------------------------------------------------------- no-allocation entry point
+// Every workspace of moe_stage_run_serial_static lives in one fixed array per GPU.  In host code
+// `scratch` only names the symbol: its device address comes from hipGetSymbolAddress, looked up
+// once per device with that device current, and only that address is passed to kernels.
+static __device__ __align__(256) uint8_t scratch[MOE_STATIC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t* g_scratch[kMaxDevices] = {};
+
+int scratch_of_device(int dev, uint8_t** out) {
+  if (dev < 0 || dev >= kMaxDevices) return set_err(nullptr, MOE_EUNSUPPORTED, "device index beyond 64");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return set_err(nullptr, MOE_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch[dev] = (uint8_t*)p;
+  }
+  *out = g_scratch[dev];
+  return MOE_OK;
+}
+}  // namespace
+
+int moe_stage_run_serial_static(const moe_stage_config_t* cfg, const void* x, const int32_t* off,
+                                const int32_t* src, const int32_t* slot, const void* w1, const void* w3,
+                                const void* w2, void* const* ret, const int64_t* return_rows, void* stream) {
+  int rc = check_config(cfg);
+  if (rc) return set_err(nullptr, rc, "moe_stage_run_serial_static: invalid configuration");
+  moe_stage_s h;  // a handle view over the scratch array: no streams, events or pinned staging
+  h.cfg = *cfg;
+  if (h.cfg.mid_segment_pieces == 0) h.cfg.mid_segment_pieces = 1;
+  if (h.cfg.band_rows == 0) h.cfg.band_rows = 1;
+  h.cfg.flags &= ~(uint32_t)MOE_KERNEL_TIMING;
+  if (hipGetDevice(&h.device) != hipSuccess ||
+      hipDeviceGetAttribute(&h.num_cus, hipDeviceAttributeMultiprocessorCount, h.device) != hipSuccess)
+    return set_err(nullptr, MOE_EHIP, "moe_stage_run_serial_static: no HIP device");
+  h.producer_bpc = producer_blocks_per_cu();
+  const WsBytes wb = size_workspaces(&h);
+  size_t off_b = 0;
+  auto carve = [&](size_t bytes) {
+    const size_t at = off_b;
+    off_b = align256(off_b + bytes);
+    return at;
+  };
+  const size_t o_hws = carve(wb.hws), o_y = carve(wb.y), o_arr = carve(wb.flags), o_part = carve(wb.partials),
+               o_ctr = carve(sizeof(RunCounters)), o_plan = carve(h.plan_cap), o_ws = carve(wb.planner);
+  if (off_b > (size_t)MOE_STATIC_SCRATCH_BYTES)
+    return set_err(nullptr, MOE_ECAPACITY,
+                   "moe_stage_run_serial_static: the configuration needs " + std::to_string(off_b) +
+                       " bytes of workspace, more than the " + std::to_string((size_t)MOE_STATIC_SCRATCH_BYTES) +
+                       " of the static array");
+  uint8_t* base = nullptr;
+  rc = scratch_of_device(h.device, &base);
+  if (rc) return rc;
+  h.hws = (uint16_t*)(base + o_hws);
+  h.y = (uint16_t*)(base + o_y);
+  h.arrivals = (uint32_t*)(base + o_arr);
+  h.partials = wb.partials ? (float*)(base + o_part) : nullptr;
+  h.ctr = (RunCounters*)(base + o_ctr);
+  h.d_plan = base + o_plan;
+  h.dev_ws = base + o_ws;
+  h.ws = devplan_ws_carve(h.dev_ws, h.cfg.num_local_experts, h.cfg.num_ranks, h.cfg.max_rows, h.max_tile_rows,
+                          h.down_per_row, h.max_lrows, h.max_items);
+  rc = run_serial(&h, true, x, off, src, slot, w1, w3, w2, ret, return_rows, stream);
+  if (rc) g_create_error = "moe_stage_run_serial_static: " + h.err;
+  return rc;
 }
 
 // ----------------------------------------------------------------- plan inspection

@@ -30,8 +30,11 @@ int64_t max_logical_rows(int64_t max_rows, int32_t E_l, int32_t R, int32_t band_
   return max_rows + (int64_t)E_l * ((int64_t)(R - 1) * (tb - 1) + kTileM - 1);
 }
 
-int64_t max_partial_tiles(int32_t split_k, int64_t max_tile_rows, int32_t down_per_row) {
-  if (split_k == 0) return kRoundTiles;
+int64_t max_partial_tiles(int32_t split_k, int64_t max_tile_rows, int32_t down_per_row, int32_t nk) {
+  // The default tail split keeps at most one round of tiles' parts, and no more parts than the
+  // tile rows have tiles times the parts a tile can take.
+  if (split_k == 0)
+    return std::min<int64_t>(kRoundTiles, max_tile_rows * down_per_row * std::min<int32_t>(kMaxSplitK, nk));
   return split_k > 1 ? max_tile_rows * down_per_row * split_k : 0;
 }
 

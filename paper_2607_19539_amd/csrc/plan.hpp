@@ -63,7 +63,7 @@ int64_t max_logical_rows(int64_t max_rows, int32_t E_l, int32_t R, int32_t band_
 
 
 // fp32 partial tiles a run may need: uniform splitting keeps one per part of every down tile;
-// the default tail split keeps at most one round's worth (kRoundTiles).
-int64_t max_partial_tiles(int32_t split_k, int64_t max_tile_rows, int32_t down_per_row);
+// the default tail split keeps at most one round's worth (kRoundTiles).  nk = ffn / 64.
+int64_t max_partial_tiles(int32_t split_k, int64_t max_tile_rows, int32_t down_per_row, int32_t nk);
 
 }  // namespace moe
