@@ -89,8 +89,9 @@ def parse():
                     help="consumer CU counts for the consumer-only copy ceiling ('' to skip)")
     ap.add_argument("--esweep", default="4,8,16,32,64",
                     help="experts per rank for the single-layer expert-count sweep ('' to skip)")
-    ap.add_argument("--only", choices=["all", "serial", "overlapped"], default="all",
-                    help="time only one path of the headline workload (profiler runs)")
+    ap.add_argument("--only", choices=["all", "serial", "overlapped", "copy"], default="all",
+                    help="time only one path of the headline workload, or only its consumer-only copy "
+                         "curve (profiler runs)")
     ap.add_argument("--detail-out", default=os.path.join("gpurun_out", "bench_detail.json"))
     ap.add_argument("--esweep-child", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -438,6 +439,12 @@ def measure_workload(torch, B, wl, args, headline):
     only = args.only if headline else "all"
     raw = {}
     try:
+        if only == "copy":
+            cs = [int(v) for v in args.copy_curve.split(",")]
+            d["consumer_copy_ceiling"] = bench.copy_curve("partitioned", cs, 10, 3) + bench.copy_curve("shared", cs, 10, 3)
+            for r in d["consumer_copy_ceiling"]:
+                log(f"{name} consumer-only copy c={r['cu_split']} {r['mode']}: {r['us']:.1f} us, {r['GBps']:.0f} GB/s")
+            return d, raw
         ser = ovl = None
         if only in ("all", "serial"):
             ser = bench.measure(args.mode, "serial", 0, steps, warmup, warm_s)
@@ -580,6 +587,9 @@ def compact_line(args, detail, name, raw, wl):
     d = detail["workloads"][name]
     ser, ovl = raw.get("serial"), raw.get("overlapped")
     main_r = ovl if ovl is not None else ser
+    if main_r is None:
+        return {"metric": METRIC, "value": None, "unit": "TFLOP/s", "n_gpus": 1, "note": f"--only {args.only}",
+                "detail": args.detail_out}
     st = main_r["stats"]
     out = {"metric": METRIC, "value": wl.flops() / (main_r["ms"] * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": main_r["ms"], "higher_is_better": True,

@@ -512,9 +512,10 @@ class MoeStage:
     def __exit__(self, *exc):
         self.close()
 
-    def __del__(self):
-        # During interpreter finalization the exit hook has already destroyed live handles.
-        if sys.is_finalizing():
+    def __del__(self, _finalizing=sys.is_finalizing):
+        # During interpreter finalization the exit hook has already destroyed live handles (and
+        # module globals may already be gone, hence the bound default).
+        if _finalizing():
             return
         try:
             self.close()
