@@ -75,7 +75,8 @@ def parse():
     ap.add_argument("--extra-workloads", default="tiny,mixtral_zipf,fine,large_fine",
                     help="further workloads measured into the detail file ('' = none)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cu-split", type=int, default=248, help="consumer compute units of the headline path")
+    ap.add_argument("--cu-split", type=int, default=32,
+                    help="consumer compute units of the headline path (a small partition, 12.5 %% of the GPU)")
     ap.add_argument("--mode", choices=["shared", "partitioned"], default="shared",
                     help="shared: the producer keeps every CU and the consumer runs beside it on its "
                          "cu_split CUs; partitioned: the consumer's CUs are reserved for it")
@@ -344,11 +345,14 @@ class Bench:
 
     def copy_curve(self, mode, splits, steps, warmup):
         """Consumer copy rate with no producer work (every flag published up front), per consumer
-        CU count: the ceiling a c-CU consumer reaches on this workload's segments."""
+        CU count: the ceiling a c-CU consumer reaches on this workload's segments.  mode "plain":
+        a plain grid-stride copy of the same segments on the same compute units, the rate those
+        compute units reach with no protocol (the c-CU copy ceiling)."""
         torch, B = self.torch, self.B
         out = []
         for c in splits:
-            stg = self.handle(mode, timing=True, extra=B.MOE_TEST_CONSUMER_ONLY)
+            extra = B.MOE_TEST_CONSUMER_ONLY | (B.MOE_TEST_PLAIN_COPY if mode == "plain" else 0)
+            stg = self.handle("partitioned" if mode == "plain" else mode, timing=True, extra=extra)
             try:
                 fn = self.fn(stg, "overlapped", c)
                 for _ in range(warmup):
@@ -441,7 +445,8 @@ def measure_workload(torch, B, wl, args, headline):
     try:
         if only == "copy":
             cs = [int(v) for v in args.copy_curve.split(",")]
-            d["consumer_copy_ceiling"] = bench.copy_curve("partitioned", cs, 10, 3) + bench.copy_curve("shared", cs, 10, 3)
+            d["consumer_copy_ceiling"] = (bench.copy_curve("partitioned", cs, 10, 3) + bench.copy_curve("shared", cs, 10, 3)
+                                          + bench.copy_curve("plain", cs, 10, 3))
             for r in d["consumer_copy_ceiling"]:
                 log(f"{name} consumer-only copy c={r['cu_split']} {r['mode']}: {r['us']:.1f} us, {r['GBps']:.0f} GB/s")
             return d, raw
@@ -527,7 +532,8 @@ def measure_workload(torch, B, wl, args, headline):
             d["best_small_partition"]["timestamps"] = ts_small
         if args.copy_curve:
             cs = [int(v) for v in args.copy_curve.split(",")]
-            d["consumer_copy_ceiling"] = bench.copy_curve("partitioned", cs, 10, 3) + bench.copy_curve("shared", cs, 10, 3)
+            d["consumer_copy_ceiling"] = (bench.copy_curve("partitioned", cs, 10, 3) + bench.copy_curve("shared", cs, 10, 3)
+                                          + bench.copy_curve("plain", cs, 10, 3))
             for r in d["consumer_copy_ceiling"]:
                 log(f"{name} consumer-only copy c={r['cu_split']} {r['mode']}: {r['us']:.1f} us, {r['GBps']:.0f} GB/s "
                     f"({r['units']} units)")
@@ -634,9 +640,10 @@ def compact_line(args, detail, name, raw, wl):
                            "overlap_ratio": ts.get("overlap_ratio"), "exposed_copy_us": ts.get("exposed_copy_us"),
                            "flag_to_copy_start_us_p50_p90_max": ts.get("flag_to_copy_start_us_p50_p90_max"),
                            "cus_used": ts.get("consumer_cus_used")}
-        cc = [r for r in d.get("consumer_copy_ceiling", []) if r["mode"] == "partitioned"]
-        if cc:
-            out["consumer"]["copy_ceiling_GBps_by_cus"] = {str(r["consumer_cus"]): round(r["GBps"]) for r in cc}
+        for mode, key in (("partitioned", "copy_alone_GBps_by_cus"), ("plain", "plain_copy_GBps_by_cus")):
+            cc = [r for r in d.get("consumer_copy_ceiling", []) if r["mode"] == mode]
+            if cc:
+                out["consumer"][key] = {str(r["consumer_cus"]): round(r["GBps"]) for r in cc}
     if "best_small_partition" in d:
         b = d["best_small_partition"]
         out["best_small_partition"] = {k: b[k] for k in ("cu_split", "cu_mode", "mgb", "speedup_vs_serial_median")}

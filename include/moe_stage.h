@@ -75,6 +75,13 @@ extern "C" {
                                        consumer copies the staged output (whatever it holds) at
                                        the rate its cu_split compute units allow.  The receive
                                        buffers then hold no results                            */
+#define MOE_TEST_PLAIN_COPY (1u << 9) /* measurement aid, with MOE_TEST_CONSUMER_ONLY and a
+                                       host-built plan: instead of the consumer, a flat grid-stride
+                                       copy of as many bytes as the segments hold (8 vectors in
+                                       flight per lane, no flags, no copy units) from the staged
+                                       output into return_bufs[0] runs on the same cu_split compute
+                                       units: the copy ceiling of those compute units.  It overwrites
+                                       return_bufs[0]                                            */
 #define MOE_TEST_PLAN_NO_LDS (1u << 7) /* testing aid: the device planner keeps every table in
                                        device memory even where it fits in LDS, so the path taken
                                        by very large configurations is exercised on small ones */
@@ -196,7 +203,7 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out);
  *
  * cu_split: compute units for the consumer, 1 <= cu_split <= CUs - XCDs, or 0 to let the
  * handle choose (a runtime-adaptive selector, the paper's Section 5 future work): it measures
- * the stage time of its own runs at consumer splits of 32, 96, 160 and 248 CUs under
+ * the stage time of its own runs at consumer splits of 16, 32, 64 and 248 CUs under
  * MOE_SHARED_CUS (8, 16, 32 and 64 without it), one after another and each with only its own
  * CU-masked queue alive, four finished runs each (the first a warm-up), skipping any above
  * CUs - XCDs, then keeps the one with the lowest median (stats: auto_cu_split).

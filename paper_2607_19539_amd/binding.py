@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(PKG, "_lib", "libmoe_stage.so")
 MOE_OK, MOE_EINVAL, MOE_EROUTING, MOE_ECAPACITY, MOE_EHIP, MOE_ETIMEOUT, MOE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 (MOE_LOCAL_DIRECT, MOE_KERNEL_TIMING, MOE_POISON, MOE_TEST_NO_SIGNAL, MOE_SHARED_CUS, MOE_DIRECT_ALL,
  MOE_TEST_CONSUMER_ONLY, MOE_TEST_PLAN_NO_LDS, MOE_TIMESTAMPS) = 1, 2, 4, 8, 16, 32, 64, 128, 256
+MOE_TEST_PLAIN_COPY = 512
 MOE_RECORDS_PRODUCER, MOE_RECORDS_COPY, MOE_RECORDS_SPAN, MOE_RECORDS_TILES = 0, 1, 2, 3
 (MOE_PLAN_TILE_ROWS, MOE_PLAN_ITEMS, MOE_PLAN_ROW_X, MOE_PLAN_ROW_RANK, MOE_PLAN_ROW_SLOT, MOE_PLAN_SEGMENTS,
  MOE_PLAN_GROUPS, MOE_PLAN_QUEUES) = range(8)

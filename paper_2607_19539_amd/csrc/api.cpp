@@ -43,7 +43,7 @@ constexpr int kTimingRing = 512;
 // With shared CUs the consumer's waves are best spread thinly over many compute units (each
 // slows the producer workgroup beside it); a reserved partition takes its CUs from the producer,
 // so it stays small.
-constexpr int kAutoSplitsShared[] = {32, 96, 160, 248};
+constexpr int kAutoSplitsShared[] = {16, 32, 64, 248};
 constexpr int kAutoSplitsPartitioned[] = {8, 16, 32, 64};
 constexpr int kNumAutoSplits = sizeof(kAutoSplitsShared) / sizeof(kAutoSplitsShared[0]);
 static_assert(sizeof(kAutoSplitsPartitioned) == sizeof(kAutoSplitsShared), "one candidate count");
@@ -206,7 +206,8 @@ int check_config(const moe_stage_config_t* c) {
     return MOE_EINVAL;
   constexpr uint32_t kKnownFlags = MOE_LOCAL_DIRECT | MOE_KERNEL_TIMING | MOE_POISON |
                                    MOE_TEST_NO_SIGNAL | MOE_SHARED_CUS | MOE_DIRECT_ALL |
-                                   MOE_TEST_CONSUMER_ONLY | MOE_TEST_PLAN_NO_LDS | MOE_TIMESTAMPS;
+                                   MOE_TEST_CONSUMER_ONLY | MOE_TEST_PLAN_NO_LDS | MOE_TIMESTAMPS |
+                                   MOE_TEST_PLAIN_COPY;
   if (c->flags & ~kKnownFlags) return MOE_EINVAL;
   if (c->band_rows < 0 || c->band_rows > 256 || (c->band_rows & (c->band_rows - 1)) != 0)
     return MOE_EINVAL;
@@ -505,26 +506,23 @@ TimingRec* timing_slot(moe_stage_s* h) {
 
 // CU masks for the consumer/producer partition.  Workgroups of a launch are dealt
 // round-robin to the XCDs, so a queue must own CUs on every XCD, and an even split keeps
-// the per-XCD share symmetric: the consumer gets m = c / n_xcd CUs on each XCD.  The mask
-// bit b = i * (cus_per_xcd + 1) + j (XCD i, j < m) lands on XCD i whether the driver maps
-// bit b to XCD (b mod n_xcd) or to XCD (b / cus_per_xcd).  The producer gets the complement,
-// or every CU when `shared`.
+// the per-XCD share symmetric: the consumer gets m = c / n_xcd CUs on each XCD.  Mask bit b
+// selects compute unit b / n_xcd of XCD b mod n_xcd, and consecutive compute units of an XCD
+// sit in different shader engines (both read from the placement records on MI355X), so the first
+// c bits give the consumer m compute units on every XCD spread over its shader engines.  (Bits
+// (cus_per_xcd + 1) * i + j, j < m, which also land on every XCD, put all m of an XCD's compute
+// units in one shader engine for m <= 8, whose shared path to L2 held a 16- to 64-CU copy at
+// the same 1.5 TB/s.)  The producer gets the complement, or every CU when `shared`.
 void make_masks(int num_cus, int n_xcd, int c, bool shared, std::vector<uint32_t>* mc,
                 std::vector<uint32_t>* mp) {
+  (void)n_xcd;
   const int words = (num_cus + 31) / 32;
   mc->assign(words, 0);
   mp->assign(words, 0);
-  std::vector<char> is_c(num_cus, 0);
-  const int per = num_cus / n_xcd, m = c / n_xcd;
-  if (per % n_xcd == 0 && m <= per - n_xcd + 1) {
-    for (int i = 0; i < n_xcd; ++i)
-      for (int j = 0; j < m; ++j) is_c[i * (per + 1) + j] = 1;
-  } else {
-    for (int b = 0; b < c; ++b) is_c[b] = 1;  // interleaved numbering: bits 0..c-1 cover every XCD
-  }
   for (int cu = 0; cu < num_cus; ++cu) {
-    if (is_c[cu]) (*mc)[cu / 32] |= 1u << (cu % 32);
-    if (shared || !is_c[cu]) (*mp)[cu / 32] |= 1u << (cu % 32);
+    const bool is_c = cu < c;
+    if (is_c) (*mc)[cu / 32] |= 1u << (cu % 32);
+    if (shared || !is_c) (*mp)[cu / 32] |= 1u << (cu % 32);
   }
 }
 
@@ -863,7 +861,17 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   // A host-built plan's counts are known here, so empty launches are skipped; a device-built
   // plan's kernels read them and return at once when there is nothing to do.
   const bool known = !dev;
-  if (!known || !h->plan.segs.empty()) HIP_TRY(h, launch_consumer(ca, own_cus, cgrid, h->s_cons));
+  const bool plain = (h->cfg.flags & MOE_TEST_CONSUMER_ONLY) && (h->cfg.flags & MOE_TEST_PLAIN_COPY);
+  if (plain && known) {
+    // As many rows as the segments hold, bounded by the staged output and the first receive buffer.
+    int64_t rows = 0;
+    for (const Segment& sg : h->plan.segs) rows += sg.rows;
+    rows = std::min<int64_t>(std::min<int64_t>(rows, return_rows[0]), h->max_lrows);
+    ca.plain_n16 = rows * h->cfg.hidden / 8;
+    if (ca.plain_n16 > 0) HIP_TRY(h, launch_plain_copy(ca, c_eff * kConsumerOwnPerCu, h->s_cons));
+  } else if (!known || !h->plan.segs.empty()) {
+    HIP_TRY(h, launch_consumer(ca, own_cus, cgrid, h->s_cons));
+  }
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
   HIP_TRY(h, hipEventRecord(h->ev_join_c, h->s_cons));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], ps));

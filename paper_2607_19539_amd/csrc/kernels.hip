@@ -917,6 +917,33 @@ void consumer_kernel(ConsumerArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Measurement aid: as many bytes as the consumer's segments hold, copied from the staged
+// output into the first receive buffer by a plain grid-stride loop, 8 vectors in flight per
+// lane -- what the same compute units reach on a flat copy of the same size, with no protocol.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kConsumerThreads) void plain_copy_kernel(ConsumerArgs a) {
+  const int64_t stride = (int64_t)gridDim.x * kConsumerThreads;
+  const int64_t n = a.plain_n16;
+  const u32x4* src = (const u32x4*)a.y;
+  g_u32x4* dst = (g_u32x4*)a.ret[0];
+  constexpr int kU = 8;
+  for (int64_t i = (int64_t)blockIdx.x * kConsumerThreads + threadIdx.x; i < n; i += kU * stride) {
+    u32x4 v[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      if (i + u * stride < n) v[u] = src[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      if (i + u * stride < n) dst[i + u * stride] = v[u];
+  }
+}
+
+hipError_t launch_plain_copy(const ConsumerArgs& a, int grid, hipStream_t s) {
+  hipLaunchKernelGGL(plain_copy_kernel, dim3(grid), dim3(kConsumerThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Baseline bulk return: every routed row of the staged output to its slot.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
@@ -959,8 +986,12 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
     for (int64_t j = i; j < a.n_arrivals; j += stride) a.tile_ready[j] = 0;
   if (a.simd_waves)
     for (int64_t j = i; j < kXcds * kSimdKeys; j += stride) a.simd_waves[j] = 0;
+  // Published flags are stored as the producer raises them (relaxed, agent scope): a plain store
+  // would sit in this XCD's L2, and the consumer's polls on other XCDs would not see it until the
+  // line is written back.
   if (a.publish)
-    for (int64_t j = i; j < a.n_publish; j += stride) a.publish[j] = a.epoch;
+    for (int64_t j = i; j < a.n_publish; j += stride)
+      __hip_atomic_store(&a.publish[j], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (a.poison) {
     const u32x4 nan = {0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};
     for (int64_t j = i; j < a.poison_elems / 8; j += stride) ((u32x4*)a.poison)[j] = nan;

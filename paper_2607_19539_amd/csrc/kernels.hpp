@@ -90,6 +90,7 @@ struct ConsumerArgs {
   CopyRecord* rec;         // timestamped runs: one record per copy unit below rec_cap, else null
   uint32_t rec_cap;
   uint32_t* simd_waves;    // beside the producer: [kXcds * kSimdKeys] consumer waves per SIMD
+  int64_t plain_n16;       // plain-copy measurement: 16-byte vectors to copy into ret[0]
 };
 
 struct ScatterArgs {
@@ -135,6 +136,9 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream_t s);
 // own_cus: the consumer has its compute units to itself (a reserved partition, or no producer).
 hipError_t launch_consumer(const ConsumerArgs& a, bool own_cus, int grid, hipStream_t s);
+// Measurement aid: a flat grid-stride copy of plain_n16 vectors from the staged output into the
+// first receive buffer (no flags, no copy units).
+hipError_t launch_plain_copy(const ConsumerArgs& a, int grid, hipStream_t s);
 // Split tail tiles of a kModeDeferTail down launch: one accumulator block of one tile per pass.
 hipError_t launch_tail(const TailArgs& a, int grid, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs& a, int grid, hipStream_t s);

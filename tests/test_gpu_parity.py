@@ -302,9 +302,9 @@ def test_auto_cu_split_settles_and_keeps_results():
             seen.add(stats["consumer_cus"])
             for a, b in zip(out, fixed):
                 assert np.array_equal(a, b)
-        assert stats["auto_cu_split"] in (32, 96, 160, 248)
+        assert stats["auto_cu_split"] in (16, 32, 64, 248)
         assert stats["consumer_cus"] == stats["auto_cu_split"]
-    assert seen >= {32, 96, 160, 248}
+    assert seen >= {16, 32, 64, 248}
     # A reserved partition takes its CUs from the producer: the candidates stay small.
     seen = set()
     with make_stage(wl, flags=B.MOE_LOCAL_DIRECT) as st:

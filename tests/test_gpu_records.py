@@ -98,8 +98,11 @@ def test_consumer_stays_on_its_compute_units(mode):
     cons = cu_keys(cp["hw_id"], cp["xcc_id"])
     prod = cu_keys(wg["hw_id"][grid:], wg["xcc_id"][grid:]) | cu_keys(wg["hw_id"][:grid], wg["xcc_id"][:grid])
     per_xcd = np.bincount([k[0] for k in cons], minlength=8)
-    log(f"{mode}: consumer_cus={stats['consumer_cus']} used={len(cons)} per XCD {per_xcd.tolist()}; producer "
-        f"grid={grid} CUs={len(prod)} shared={len(cons & prod)}")
+    se = {}
+    for x, key in cons:
+        se.setdefault(x, set()).add(key >> 5)       # shader engine (HW_ID bits 15:13)
+    log(f"{mode}: consumer_cus={stats['consumer_cus']} used={len(cons)} per XCD {per_xcd.tolist()}; shader engines "
+        f"per XCD {[len(se.get(x, ())) for x in range(8)]}; producer grid={grid} CUs={len(prod)} shared={len(cons & prod)}")
     assert len(cons) <= stats["consumer_cus"]
     if mode == "partitioned":
         assert grid == 256 - stats["consumer_cus"]
