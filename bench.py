@@ -168,6 +168,26 @@ def cu_key(hw_id, xcc):
     return (int(xcc) & 0xF, (int(hw_id) >> 8) & 0xFF)
 
 
+def producer_clocks(wg, grid, cons_cu=None):
+    """Mean shader clock (GHz) of each producer launch from its workgroups' records: cycles over
+    wall-clock ticks, summed over the workgroups that took work.  With a consumer CU set, the
+    down launch's figure is also split into workgroups on those compute units and the rest."""
+    out = {}
+    for name, sl in (("gate_up", slice(0, grid)), ("down", slice(grid, 2 * grid))):
+        w = wg[sl]
+        w = w[w["items"] > 0]
+        dt = (w["t_end"].astype(np.int64) - w["t_start"].astype(np.int64)).sum()
+        out[name] = round(float(w["cycles"].astype(np.float64).sum() / dt / TICK_US * 1e-3), 3) if dt > 0 else None
+    if cons_cu:
+        w = wg[grid:2 * grid]
+        w = w[w["items"] > 0]
+        on = np.array([cu_key(h, x) in cons_cu for h, x in zip(w["hw_id"], w["xcc_id"])], bool)
+        for key, m in (("down_on_consumer_cus", on), ("down_elsewhere", ~on)):
+            dt = (w["t_end"][m].astype(np.int64) - w["t_start"][m].astype(np.int64)).sum()
+            out[key] = round(float(w["cycles"][m].astype(np.float64).sum() / dt / TICK_US * 1e-3), 3) if dt > 0 else None
+    return out
+
+
 def overlap_analysis(B, stg, wl):
     """Overlap of the return copy with the expert compute (paper Section 4.2.2, Fig. 5b) from the
     last run's in-kernel timestamps: the share of the consumer's busy time (the union of its copy
@@ -197,7 +217,8 @@ def overlap_analysis(B, stg, wl):
         if t_flag:
             lag.append((int(cp["t_ready"][m].min()) - t_flag) * TICK_US)
             deliver.append((int(cp["t_done"][m].max()) - t_flag) * TICK_US)
-    cons_cu = {cu_key(h, x) for h, x in zip(cp["hw_id"], cp["xcc_id"])}
+    own = cp["source"] == 0
+    cons_cu = {cu_key(h, x) for h, x in zip(cp["hw_id"][own], cp["xcc_id"][own])}
     grid = int(span["producer_grid"])
     prod_cu = {cu_key(h, x) for h, x in zip(wg["hw_id"][grid:], wg["xcc_id"][grid:])}
     per_cu = {}
@@ -214,10 +235,12 @@ def overlap_analysis(B, stg, wl):
         "flag_to_delivered_us_p50_p90_max": [round(float(np.percentile(deliver, q)), 2) for q in (50, 90, 100)]
         if deliver else None,
         "segments_timed": len(lag),
+        "units_drained": int((~own).sum()),
         "consumer_cus_used": len(cons_cu),
         "producer_down_cus_used": len(prod_cu),
         "producer_down_workgroups_per_cu_max": max(per_cu.values()) if per_cu else 0,
         "consumer_cus_shared_with_producer": len(cons_cu & prod_cu),
+        "producer_clock_GHz": producer_clocks(wg, grid, cons_cu),
     })
     return out
 
@@ -331,14 +354,19 @@ class Bench:
         finally:
             stg.close()
 
-    def timestamps(self, mode, cu_split, warmup, warm_s, mgb=None):
-        """One timestamped overlapped run after warm-up: overlap ratio, flag latencies, placement."""
+    def timestamps(self, mode, cu_split, warmup, warm_s, mgb=None, path="overlapped"):
+        """One timestamped run after warm-up: for the overlapped path the overlap ratio, flag
+        latencies and placement, for the serial path the producer's clocks."""
         stg = self.handle(mode, mgb, extra=self.B.MOE_TIMESTAMPS)
         try:
-            fn = self.fn(stg, "overlapped", cu_split)
+            fn = self.fn(stg, path, cu_split)
             self.timed(stg, fn, 5, warmup, warm_s)
             fn()
             stg.query(check=False)
+            if path == "serial":
+                span = stg.records(self.B.MOE_RECORDS_SPAN)[0]
+                return {"producer_clock_GHz": producer_clocks(stg.records(self.B.MOE_RECORDS_PRODUCER),
+                                                              int(span["producer_grid"]))}
             return overlap_analysis(self.B, stg, self.wl)
         finally:
             stg.close()
@@ -476,6 +504,10 @@ def measure_workload(torch, B, wl, args, headline):
         ts = bench.timestamps(args.mode, args.cu_split, warmup, wo)
         d["overlapped"]["timestamps"] = ts
         raw["timestamps"] = ts
+        ts_ser = bench.timestamps(args.mode, 0, warmup, wo, path="serial")
+        d["serial"]["producer_clock_GHz"] = ts_ser["producer_clock_GHz"]
+        raw["serial_clock"] = ts_ser["producer_clock_GHz"]
+        log(f"{name} producer clock GHz: serial {ts_ser['producer_clock_GHz']}, overlapped {ts.get('producer_clock_GHz')}")
         log(f"{name} timestamps: overlap ratio {ts.get('overlap_ratio')}, exposed copy {ts.get('exposed_copy_us')} us, "
             f"flag->copy start p50/p90/max {ts.get('flag_to_copy_start_us_p50_p90_max')} us, consumer CUs "
             f"{ts.get('consumer_cus_used')}, producer CUs {ts.get('producer_down_cus_used')}")
@@ -633,6 +665,9 @@ def compact_line(args, detail, name, raw, wl):
     prod = wl.flops() / (main_r["producer_ms"] * 1e-3) / 1e12
     out["producer"] = {"us": main_r["producer_ms"] * 1e3, "tflops": prod, "frac": prod / PEAK_BF16_TFLOPS}
     ts = raw.get("timestamps") or {}
+    if raw.get("serial_clock") or ts.get("producer_clock_GHz"):
+        # Mean shader clock of the gate/up and down launches, from the workgroups' cycle counts.
+        out["producer"]["clock_GHz"] = {"serial": raw.get("serial_clock"), "overlapped": ts.get("producer_clock_GHz")}
     if ovl is not None:
         out["consumer"] = {"us": ovl["consumer_ms"] * 1e3, "copy_bytes": ts.get("copy_bytes"),
                            "units": int(st["copy_units"]),

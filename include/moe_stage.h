@@ -199,10 +199,14 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out);
  * stream) and later work on `stream` sees the results.  The consumer runs on a
  * CU-masked stream of the handle; the producer runs on another one, or directly
  * on `stream` under MOE_SHARED_CUS when `stream` is not the legacy null stream
- * (whose launches would wait for the polling consumer).
+ * (whose launches would wait for the polling consumer).  A drain launch follows
+ * the producer in its stream: it copies the units the consumer has not claimed
+ * when the producer ends, on the producer's compute units, and waits (bounded by
+ * the watchdog) until every consumer wave has finished, so the stage ends with it.
  *
  * cu_split: compute units for the consumer, 1 <= cu_split <= CUs - XCDs, or 0 to let the
- * handle choose (a runtime-adaptive selector, the paper's Section 5 future work): it measures
+ * handle choose (a runtime-adaptive selector, the future work of paper Sections 4.3.4
+ * and 6): it measures
  * the stage time of its own runs at consumer splits of 16, 32, 64 and 248 CUs under
  * MOE_SHARED_CUS (8, 16, 32 and 64 without it), one after another and each with only its own
  * CU-masked queue alive, four finished runs each (the first a warm-up), skipping any above
@@ -321,6 +325,8 @@ typedef struct {
   int32_t launch;   /* 0 gate/up, 1 down                                                   */
   int32_t items;    /* work items the workgroup ran                                        */
   uint64_t t_start, t_end;
+  uint64_t cycles;  /* shader clock cycles that passed between t_start and t_end: the
+                       workgroup's mean clock is cycles / (t_end - t_start) x 100 MHz          */
 } moe_wg_record_t;
 typedef struct {
   int32_t segment;  /* segment index (ready order)                                         */
@@ -330,6 +336,9 @@ typedef struct {
   uint64_t t_poll;  /* the wave starts polling the segment's ready flags                   */
   uint64_t t_ready; /* every flag seen and acquired: the copy starts                       */
   uint64_t t_done;  /* the unit's stores have completed                                    */
+  int32_t source;   /* 0: copied by the consumer launch; 1: by the drain launch that follows
+                       the producer (units still unclaimed when the producer ended)          */
+  int32_t reserved;
 } moe_copy_record_t;
 typedef struct {
   uint64_t producer_start, producer_end;

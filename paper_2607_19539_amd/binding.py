@@ -58,13 +58,14 @@ class moe_stage_stats_t(ctypes.Structure):
 
 class moe_wg_record_t(ctypes.Structure):
     _fields_ = [("hw_id", ctypes.c_uint32), ("xcc_id", ctypes.c_uint32), ("launch", ctypes.c_int32),
-                ("items", ctypes.c_int32), ("t_start", ctypes.c_uint64), ("t_end", ctypes.c_uint64)]
+                ("items", ctypes.c_int32), ("t_start", ctypes.c_uint64), ("t_end", ctypes.c_uint64),
+                ("cycles", ctypes.c_uint64)]
 
 
 class moe_copy_record_t(ctypes.Structure):
     _fields_ = [("segment", ctypes.c_int32), ("part", ctypes.c_int32), ("hw_id", ctypes.c_uint32),
                 ("xcc_id", ctypes.c_uint32), ("t_poll", ctypes.c_uint64), ("t_ready", ctypes.c_uint64),
-                ("t_done", ctypes.c_uint64)]
+                ("t_done", ctypes.c_uint64), ("source", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class moe_span_t(ctypes.Structure):

@@ -27,7 +27,8 @@
 
 using namespace moe;
 
-static_assert(sizeof(WgRecord) == sizeof(moe_wg_record_t) && offsetof(WgRecord, t_start) == offsetof(moe_wg_record_t, t_start),
+static_assert(sizeof(WgRecord) == sizeof(moe_wg_record_t) && offsetof(WgRecord, t_start) == offsetof(moe_wg_record_t, t_start) &&
+                  offsetof(WgRecord, cycles) == offsetof(moe_wg_record_t, cycles),
               "producer record layout");
 static_assert(sizeof(CopyRecord) == sizeof(moe_copy_record_t) && offsetof(CopyRecord, t_poll) == offsetof(moe_copy_record_t, t_poll),
               "copy record layout");
@@ -862,6 +863,15 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   // plan's kernels read them and return at once when there is nothing to do.
   const bool known = !dev;
   const bool plain = (h->cfg.flags & MOE_TEST_CONSUMER_ONLY) && (h->cfg.flags & MOE_TEST_PLAIN_COPY);
+  const bool producer = !(h->cfg.flags & MOE_TEST_CONSUMER_ONLY);
+  // With a producer, the run ends with a drain launch in the producer's stream: it copies the
+  // units the consumer has not claimed by then on the producer's compute units and waits for the
+  // consumer's last wave, so the caller's stream needs no event from the consumer's queue.
+  const bool drain = producer && (!known || !h->plan.segs.empty());
+  if (drain) {
+    ca.role = kRoleCounted;
+    ca.map_grid = (uint32_t)cgrid;
+  }
   if (plain && known) {
     // As many rows as the segments hold, bounded by the staged output and the first receive buffer.
     int64_t rows = 0;
@@ -875,18 +885,24 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
   HIP_TRY(h, hipEventRecord(h->ev_join_c, h->s_cons));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], ps));
-  const bool producer = !(h->cfg.flags & MOE_TEST_CONSUMER_ONLY);
   if (producer && (!known || h->plan.n_gu > 0)) HIP_TRY(h, launch_producer(pgu, false, pgrid, ps));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], ps));
   if (producer && (!known || h->plan.n_down > 0)) HIP_TRY(h, launch_producer(pdn, true, pgrid, ps));
   if (producer && (pdn.mode & kModeDeferTail) && (!known || h->plan.n_split_rows > 0))
     HIP_TRY(h, launch_tail(tail_args(h, lay, pdn), kTailGrid, ps));
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[2], ps));
+  if (drain) {
+    ConsumerArgs da = ca;
+    da.role = kRoleDrain;
+    da.simd_waves = nullptr;
+    da.exit_waves = (uint32_t)cgrid * (kConsumerThreads / 64);
+    HIP_TRY(h, launch_drain(da, shared ? h->num_cus : h->num_cus - c_eff, ps));
+  }
   if (!on_caller) {
     HIP_TRY(h, hipEventRecord(h->ev_join_p, h->s_prod));
     HIP_TRY(h, hipStreamWaitEvent(stream, h->ev_join_p, 0));
   }
-  HIP_TRY(h, hipStreamWaitEvent(stream, h->ev_join_c, 0));
+  if (!drain) HIP_TRY(h, hipStreamWaitEvent(stream, h->ev_join_c, 0));
   if (tr) {
     HIP_TRY(h, hipEventRecord(tr->ev[5], stream));
     tr->kind = 0;
@@ -1047,7 +1063,9 @@ int moe_stage_query(moe_stage_t h, moe_stage_stats_t* out) {
     h->last.timeout = 0;
     return set_err(h, MOE_ETIMEOUT,
                    std::to_string(h->last_timeouts) + " device wait(s) hit the watchdog since the last query (" +
-                       ((h->last_timeout_where & 1) ? "consumer flag wait" : "") + ", first at segment " +
+                       ((h->last_timeout_where & 1) ? "consumer flag wait" : "") +
+                       ((h->last_timeout_where & 3) == 3 ? ", " : "") +
+                       ((h->last_timeout_where & 2) ? "end-of-stage wait for the consumer" : "") + ", first at segment " +
                        std::to_string(h->last.timeout_segment) + ")");
   }
   return MOE_OK;

@@ -631,6 +631,7 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
   uint32_t q = xcc_id();  // meaningful in thread 0, which does the claiming
   const uint32_t end = (uint32_t)a.queue[kXcds];
   const uint64_t t_start = ticks();
+  const uint64_t c_start = clock64();
   if (tid == 0) {
     words[0] = claim_item(a, q, end);
     if (words[0] < end) atomicAdd(a.active, 1u);
@@ -662,6 +663,7 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
   if (a.wg_rec && tid == 0) {  // timestamped runs: where and when this workgroup ran
     // The last item is done (a signalled down item has also waited for its stores).
     const uint64_t t_end = ticks();
+    const uint64_t c_end = clock64();
     WgRecord r;
     r.hw_id = hw_id();
     r.xcc_id = xcc_id();
@@ -669,6 +671,7 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
     r.items = n_items;
     r.t_start = t_start;
     r.t_end = t_end;
+    r.cycles = c_end - c_start;
     a.wg_rec[blockIdx.x] = r;
     if (down)
       __hip_atomic_fetch_max(&a.ctr->prod_t1, t_end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -810,22 +813,12 @@ __device__ __forceinline__ void copy_vectors(const u32x4* __restrict__ src, g_u3
   for (int64_t i = nfull * kStep + lane; i < n; i += 64) dst[i] = src[i];
 }
 
+// The ticket loop of one wave: claim a copy unit, wait for its segment's flags, copy its part.
 template <bool kOwn>
-__global__ __launch_bounds__(kConsumerThreads, kOwn ? kConsumerOwnMinWaves : kConsumerMinWaves)
-void consumer_kernel(ConsumerArgs a) {
-  const int lane = threadIdx.x & 63;
-  if (!kOwn && a.simd_waves) {
-    // hw_id: SIMD [5:4], compute unit [11:8], shader array [12], shader engine [15:13].
-    uint32_t before = 0;
-    if (lane == 0) {
-      const uint32_t h = hw_id();
-      const uint32_t key = ((((h >> 13) & 7u) * 2 + ((h >> 12) & 1u)) * 16 + ((h >> 8) & 15u)) * 4 + ((h >> 4) & 3u);
-      before = atomicAdd(&a.simd_waves[xcc_id() * kSimdKeys + key], 1u);
-    }
-    if (__builtin_amdgcn_readfirstlane(before) >= (uint32_t)kMaxConsumerWavesPerSimd) return;
-  }
+__device__ __forceinline__ void consume_units(const ConsumerArgs& a, int lane) {
   const int32_t n_segs = *a.n_segs;
-  const uint32_t n_waves = gridDim.x * (kConsumerThreads / 64);
+  const uint32_t map_grid = a.map_grid ? a.map_grid : gridDim.x;
+  const uint32_t n_waves = map_grid * (kConsumerThreads / 64);
   // Segments are in ready order: the first late one by binary search (uniform loads).
   const int32_t late_from = *a.down_qmax - kLatePositions;
   int32_t n_early = 0;
@@ -841,13 +834,14 @@ void consumer_kernel(ConsumerArgs a) {
   const uint32_t n_units = early_units + ((uint32_t)(n_segs - n_early) << late_shift);
   if (blockIdx.x == 0 && threadIdx.x == 0) a.ctr->n_units = n_units;
   const uint32_t last_ticket = max(n_waves, n_units);
-  uint64_t polls = 0, waited = 0;
+  uint32_t polls = 0;
+  uint64_t waited = 0;
   for (;;) {
     uint32_t t = 0;
     if (lane == 0) t = atomicAdd(&a.ctr->seg_next, 1u);
     t = __builtin_amdgcn_readfirstlane(t);  // every lane is active here
     if (t >= last_ticket) break;
-    const uint32_t unit = t < n_waves ? (t % (kConsumerThreads / 64)) * gridDim.x + t / (kConsumerThreads / 64) : t;
+    const uint32_t unit = t < n_waves ? (t % (kConsumerThreads / 64)) * map_grid + t / (kConsumerThreads / 64) : t;
     if (unit >= n_units) continue;
     const bool early = unit < early_units;
     const uint32_t u = early ? unit : unit - early_units;
@@ -897,22 +891,81 @@ void consumer_kernel(ConsumerArgs a) {
       // Timestamped runs: the unit ends when its stores have completed.
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       const uint64_t t_done = ticks();
-      if (lane == 0) {
-        CopyRecord r;
-        r.segment = s;
-        r.part = part;
-        r.hw_id = hw_id();
-        r.xcc_id = xcc_id();
-        r.t_poll = t0;
-        r.t_ready = t_ready;
-        r.t_done = t_done;
-        a.rec[unit] = r;
+      // One dword of the record per lane: a whole record in lane 0 would hold twelve
+      // registers at once, past this variant's budget.
+      constexpr int kWords = (int)(sizeof(CopyRecord) / 4);
+      if (lane < kWords) {
+        const uint32_t source = kOwn && a.role == kRoleDrain ? 1u : 0u;  // the drain is a kOwn launch
+        uint32_t w = 0;
+        switch (lane) {
+          case 0: w = (uint32_t)s; break;
+          case 1: w = (uint32_t)part; break;
+          case 2: w = hw_id(); break;
+          case 3: w = xcc_id(); break;
+          case 4: w = (uint32_t)t0; break;
+          case 5: w = (uint32_t)(t0 >> 32); break;
+          case 6: w = (uint32_t)t_ready; break;
+          case 7: w = (uint32_t)(t_ready >> 32); break;
+          case 8: w = (uint32_t)t_done; break;
+          case 9: w = (uint32_t)(t_done >> 32); break;
+          case 10: w = source; break;
+          default: break;
+        }
+        reinterpret_cast<uint32_t*>(a.rec + unit)[lane] = w;
       }
     }
   }
   if (lane == 0 && (polls || waited)) {
     atomicAdd((unsigned long long*)&a.ctr->poll_iters, (unsigned long long)polls);
     atomicAdd((unsigned long long*)&a.ctr->wait_ticks, (unsigned long long)waited);
+  }
+}
+
+// A counted consumer wave's exit: its copies are complete and written back from its XCD's L2
+// before the count rises, so the drain launch's end covers them.
+__device__ __forceinline__ void count_exit(const ConsumerArgs& a, int lane) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  if (lane == 0) __hip_atomic_fetch_add(&a.ctr->cons_exit, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <bool kOwn>
+__global__ __launch_bounds__(kConsumerThreads, kOwn ? kConsumerOwnMinWaves : kConsumerMinWaves)
+void consumer_kernel(ConsumerArgs a) {
+  const int lane = threadIdx.x & 63;
+  if (!kOwn && a.simd_waves) {
+    // hw_id: SIMD [5:4], compute unit [11:8], shader array [12], shader engine [15:13].
+    uint32_t before = 0;
+    if (lane == 0) {
+      const uint32_t h = hw_id();
+      const uint32_t key = ((((h >> 13) & 7u) * 2 + ((h >> 12) & 1u)) * 16 + ((h >> 8) & 15u)) * 4 + ((h >> 4) & 3u);
+      before = atomicAdd(&a.simd_waves[xcc_id() * kSimdKeys + key], 1u);
+    }
+    if (__builtin_amdgcn_readfirstlane(before) >= (uint32_t)kMaxConsumerWavesPerSimd) {
+      if (a.role == kRoleCounted) count_exit(a, lane);
+      return;
+    }
+  }
+  consume_units<kOwn>(a, lane);
+  if (a.role == kRoleCounted) {
+    count_exit(a, lane);
+  } else if (kOwn && a.role == kRoleDrain && blockIdx.x == 0 && threadIdx.x < 64) {
+    // Every ticket is claimed; the consumer's waves still copying finish on their own (each
+    // unit's flags are raised, the producer having ended), and waves not yet started find no
+    // ticket left.  The wait is bounded like every flag wait.
+    const uint64_t t0 = ticks();
+    uint32_t backoff = 1;
+    while (__hip_atomic_load(&a.ctr->cons_exit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < a.exit_waves) {
+      if (ticks() - t0 > a.watchdog_ticks) {
+        if (lane == 0) {
+          __hip_atomic_fetch_add(&a.ctr->timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_fetch_or(&a.ctr->timeout_where, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        break;
+      }
+      for (uint32_t i = 0; i < backoff; ++i) __builtin_amdgcn_s_sleep(1);
+      backoff = backoff < 8 ? 2 * backoff : 8;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
 }
 
@@ -972,6 +1025,7 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
     a.ctr->poll_iters = 0;
     a.ctr->wait_ticks = 0;
     a.ctr->n_units = 0;
+    a.ctr->cons_exit = 0;
     a.ctr->prod_t0 = ~0ull;
     a.ctr->prod_t1 = 0;
     if (a.plan_hdr) {
@@ -1021,6 +1075,11 @@ hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream
     hipLaunchKernelGGL((producer_kernel<true, 4>), g, b, 0, s, a);
   else
     hipLaunchKernelGGL((producer_kernel<true, 0>), g, b, 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_drain(const ConsumerArgs& a, int grid, hipStream_t s) {
+  hipLaunchKernelGGL(consumer_kernel<true>, dim3(grid), dim3(kConsumerThreads), 0, s, a);
   return hipGetLastError();
 }
 

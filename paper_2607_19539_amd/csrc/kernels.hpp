@@ -22,6 +22,7 @@ struct WgRecord {
   int32_t launch;   // 0 gate/up, 1 down
   int32_t items;    // work items it ran
   uint64_t t_start, t_end;
+  uint64_t cycles;  // shader clock cycles of wave 0 between t_start and t_end
 };
 struct CopyRecord {
   int32_t segment;  // segment index (ready order)
@@ -31,8 +32,10 @@ struct CopyRecord {
   uint64_t t_poll;  // the wave starts polling the segment's flags
   uint64_t t_ready; // every flag seen, acquire done: the copy starts
   uint64_t t_done;  // the wave's copy stores have completed
+  int32_t source;   // 0 the consumer launch, 1 the drain launch
+  int32_t reserved;
 };
-static_assert(sizeof(WgRecord) == 32 && sizeof(CopyRecord) == 40, "record layouts are part of the ABI");
+static_assert(sizeof(WgRecord) == 40 && sizeof(CopyRecord) == 48, "record layouts are part of the ABI");
 
 struct ProducerArgs {
   const uint16_t* x;       // [rows, H] dispatched tokens
@@ -91,7 +94,19 @@ struct ConsumerArgs {
   uint32_t rec_cap;
   uint32_t* simd_waves;    // beside the producer: [kXcds * kSimdKeys] consumer waves per SIMD
   int64_t plain_n16;       // plain-copy measurement: 16-byte vectors to copy into ret[0]
+  // Ticket dealing: tickets below 4 x map_grid go transposed to the waves of the consumer launch
+  // of map_grid workgroups (0: this launch's grid), so the drain deals them like the consumer.
+  uint32_t map_grid;
+  int32_t role;            // kRoleConsumer, kRoleCounted or kRoleDrain
+  uint32_t exit_waves;     // drain: consumer waves whose exit it waits for
 };
+// Consumer launch roles.  A counted consumer's waves each add one to ctr->cons_exit once their
+// stores are written back; a drain launch (after the producer, in its stream) claims the copy
+// units still unclaimed, then waits until every consumer wave has counted its exit, so the end
+// of the drain is the end of every copy of the run.
+constexpr int32_t kRoleConsumer = 0;
+constexpr int32_t kRoleCounted = 1;
+constexpr int32_t kRoleDrain = 2;
 
 struct ScatterArgs {
   const uint16_t* y;
@@ -136,6 +151,9 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream_t s);
 // own_cus: the consumer has its compute units to itself (a reserved partition, or no producer).
 hipError_t launch_consumer(const ConsumerArgs& a, bool own_cus, int grid, hipStream_t s);
+// After the producer, in its stream: the copy units the consumer has not claimed yet, on the
+// producer's compute units, and the wait for the consumer's last wave.
+hipError_t launch_drain(const ConsumerArgs& a, int grid, hipStream_t s);
 // Measurement aid: a flat grid-stride copy of plain_n16 vectors from the staged output into the
 // first receive buffer (no flags, no copy units).
 hipError_t launch_plain_copy(const ConsumerArgs& a, int grid, hipStream_t s);
@@ -150,7 +168,7 @@ constexpr int kProducerThreads = 256;
 constexpr int kConsumerThreads = 256;
 // 16-byte vectors per consumer lane and copy chunk (two chunks in flight): beside the producer,
 // within 64 VGPRs; on compute units of its own, within 128.
-constexpr int kCopyUnroll = 5;
+constexpr int kCopyUnroll = 4;
 constexpr int kCopyUnrollOwn = 12;
 // Consumer copy units (one wave each) per segment, as a power of two.  Beside the producer
 // (shared compute units) a copying wave slows the producer workgroup on its compute unit, so

@@ -106,7 +106,7 @@ struct RunCounters {
   uint32_t gu_active;         // gate/up workgroups that claimed at least one tile
   uint32_t down_active;       // down workgroups that claimed at least one tile
   uint32_t n_units;           // consumer copy units of the run (written by the consumer)
-  uint32_t pad0;
+  uint32_t cons_exit;         // consumer waves done (runs that end with a drain launch)
   uint64_t poll_iters;        // consumer poll iterations
   uint64_t wait_ticks;        // consumer wait time, 100 MHz ticks
   // Timestamped runs only (100 MHz wall clock): first gate/up workgroup start and last

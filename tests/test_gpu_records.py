@@ -52,6 +52,11 @@ def check_protocol(rec):
     pairs = set(zip(cp["segment"].tolist(), cp["part"].tolist()))
     assert len(pairs) == len(cp)
     assert np.all(cp["t_poll"] <= cp["t_ready"]) and np.all(cp["t_ready"] <= cp["t_done"])
+    assert set(np.unique(cp["source"]).tolist()) <= {0, 1}
+    # the drain launch starts after the producer's last launch: its units start copying after it ended
+    dr = cp["source"] == 1
+    if dr.any():
+        assert int(cp["t_ready"][dr].min()) + SKEW_TICKS >= int(span["producer_end"])
     # a unit starts after every flag of its segment was raised
     for s in range(len(segs)):
         fb, fc = int(segs[s, 4]), int(segs[s, 5])
@@ -95,13 +100,16 @@ def test_consumer_stays_on_its_compute_units(mode):
     check_protocol(rec)
     stats, cp, wg = rec["stats"], rec["copy"], rec["wg"]
     grid = int(rec["span"]["producer_grid"])
+    drained = int((cp["source"] == 1).sum())
+    cp = cp[cp["source"] == 0]        # units the drain copied after the producer ran anywhere
     cons = cu_keys(cp["hw_id"], cp["xcc_id"])
     prod = cu_keys(wg["hw_id"][grid:], wg["xcc_id"][grid:]) | cu_keys(wg["hw_id"][:grid], wg["xcc_id"][:grid])
     per_xcd = np.bincount([k[0] for k in cons], minlength=8)
     se = {}
     for x, key in cons:
         se.setdefault(x, set()).add(key >> 5)       # shader engine (HW_ID bits 15:13)
-    log(f"{mode}: consumer_cus={stats['consumer_cus']} used={len(cons)} per XCD {per_xcd.tolist()}; shader engines "
+    log(f"{mode}: units={len(rec['copy'])} drained={drained}; consumer_cus={stats['consumer_cus']} used={len(cons)} "
+        f"per XCD {per_xcd.tolist()}; shader engines "
         f"per XCD {[len(se.get(x, ())) for x in range(8)]}; producer grid={grid} CUs={len(prod)} shared={len(cons & prod)}")
     assert len(cons) <= stats["consumer_cus"]
     if mode == "partitioned":
