@@ -55,9 +55,12 @@ constexpr int kDmaPerThread = kTileM / kRowsPerDma / 4;  // 8 per operand block 
 // bytes so the 32 lanes writing one column of 32 rows hit distinct banks.
 constexpr int kDownOutStride = kDownTileN * 2 + 16;    // 528 B per staged output row
 constexpr int kGuOutStride = kGuTileF * 2 + 16;        // 272 B per staged activation row
-// Two words past both staging areas carry the next work item and the split-K verdict
-// between the waves; the operand ring overwrites them, so they are used only outside it.
-constexpr int kSharedWords = kLdsBytes - 16;
+// Words past both staging areas carry the next work item (its queue position, item word and
+// tile row) and the split-K verdict between the waves; the operand ring overwrites them, so
+// they are used only while the ring is idle (the epilogue and the item boundary).
+constexpr int kSharedWords = kLdsBytes - 48;
+constexpr int kWordPos = 0, kWordSplit = 1, kWordItem = 2, kWordTileRow = 3;  // tile row: 6 words
+static_assert((kWordTileRow + 6) * 4 <= kLdsBytes - kSharedWords, "shared words");
 static_assert(kTileM * kDownOutStride <= kSharedWords, "down staging overlaps the shared words");
 // Down epilogue: each tile row's (rank, slot) pairs, right past the staged output tile.
 constexpr int kDownRowInfo = kTileM * kDownOutStride;
@@ -292,9 +295,14 @@ __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const DmaRow
 // tiles, 2..4 = that many parts, 0 = the count of the item's tile row.  A kernel holding
 // both epilogues would keep copies of the accumulators live across the branch, and a fixed
 // count lets the reduction issue the loads of several blocks of every part at once.
-template <bool down, int kSplit>
-__device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t item, uint8_t* lds,
-                                              uint32_t* words) {
+//
+// `hook()` runs once the epilogue has staged the tile (not on the paths that return early):
+// thread 0 fetches the next item's descriptor there, and the stores that follow hide part of
+// the load latency.  (Branching there while the accumulators are still live, right after the
+// K loop, made the compiler spill them.)
+template <bool down, int kSplit, class Hook>
+__device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t item, const TileRow& tr,
+                                              uint8_t* lds, uint32_t* words, Hook&& hook) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave: keeps bases scalar
   const int wn = wave & 1, wm = wave >> 1;
@@ -302,7 +310,6 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
   const int t = (int)((item >> kItemRowShift) & (uint32_t)(kMaxTileRows - 1));
   const int col = down ? (int)((item >> kDownColShift) & kDownColMask) : (int)(item & kItemColMask);
   const int part = down ? (int)(item & kDownPartMask) : 0;
-  const TileRow tr = a.tile_rows[t];
   const int64_t H = a.H, F = a.F;
   const int e = tr.expert, lrow0 = tr.lrow0;
   // Operand rows: DMA instruction i of a wave fills tile rows wave*64 + i*8 .. +7.  Tensors
@@ -333,6 +340,12 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
       // would produce register pairs whose high halves stay allocated.
       xoff[i] = __umul24((uint32_t)a.row_x[lrow0 + n], stride) + (((uint32_t)(lane & 7) ^ swz(n)) << 4);
     }
+    // The offsets are complete before the first operand DMA.  The compiler counts only its own
+    // loads, not the DMAs: had it waited for each offset just before its token DMA, each of
+    // those waits would also have drained the weight DMAs issued in between, serialising the
+    // prologue into three memory latencies instead of two.
+#pragma unroll
+    for (int i = 0; i < kDmaPerThread; ++i) asm volatile("" ::"v"(xoff[i]));
   } else {
     const uint32_t stride = (uint32_t)F * 2;
     w.base = (const uint8_t*)a.w2 + (uint64_t)e * H * F * 2;
@@ -390,6 +403,7 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
         }
     }
     __syncthreads();
+    hook();
     // 16 threads store one row's 128 features: 8 threads per 64-feature K block of the
     // workspace [F / 64][hws_rows][64], so consecutive rows fill contiguous 128-byte runs.
     const int c16 = tid & 15;
@@ -434,10 +448,10 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
       if (tid == 0) {
         const uint32_t prev =
             __hip_atomic_fetch_add(&a.arrivals[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        words[1] = (prev + 1 == (uint32_t)S) ? 1u : 0u;
+        words[kWordSplit] = (prev + 1 == (uint32_t)S) ? 1u : 0u;
       }
       __syncthreads();
-      if (words[1] == 0) return;  // another part finishes the tile
+      if (words[kWordSplit] == 0) return;  // another part finishes the tile
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
     // Each row's rank and slot for the stores below: one row per thread, loaded now so the
@@ -539,6 +553,7 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     rinfo[2 * tid] = my_rank;
     rinfo[2 * tid + 1] = my_slot;
     __syncthreads();
+    hook();
     // Rows returning to another rank go to the staged output Y (the consumer moves them);
     // local rows go straight to the local receive buffer when the producer writes them
     // directly.  In a signalled launch a wave stores one 512-byte row (64 lanes x 8 bytes, 4
@@ -607,8 +622,10 @@ __device__ __forceinline__ uint32_t hw_id() {
 
 // Claims the next item of this launch: from queue q (initially the workgroup's own XCD's),
 // moving on to the next queue whenever one is empty.  Returns `end` once all are empty.
-__device__ __forceinline__ uint32_t claim_item(const ProducerArgs& a, uint32_t& q, uint32_t end) {
-  for (int tries = 0; tries < kXcds; ++tries) {
+// Claims the next item from queue q, then from the following queues once q is empty; `tries`
+// queues are tried in all.  Returns the item's position in a.items, or `end`.
+__device__ __forceinline__ uint32_t claim_item(const ProducerArgs& a, uint32_t& q, uint32_t end, int tries = kXcds) {
+  for (; tries > 0; --tries) {
     const uint32_t i = atomicAdd(&a.claim[q], 1u);
     const int32_t q0 = a.queue[q], q1 = a.queue[q + 1];
     if (i < (uint32_t)(q1 - q0)) return (uint32_t)q0 + i;
@@ -617,48 +634,126 @@ __device__ __forceinline__ uint32_t claim_item(const ProducerArgs& a, uint32_t& 
   return end;
 }
 
+// The next work item as thread 0 learns it while the current one runs: the claim is issued
+// when the item starts, and resolved once the epilogue has staged the tile, where the item
+// word and the tile row are loaded too; the next item then starts with its descriptor at hand.
+struct NextItem {
+  uint32_t q;       // queue claimed from
+  uint32_t ticket;  // the claim's position in queue q (in flight until resolved)
+  int32_t q0, q1;   // queue q's bounds
+  uint32_t pos;     // position of the next item in a.items, or end
+  uint32_t item;
+  TileRow tr;
+  bool done;        // pos, item and tr are known
+};
+
+__device__ __forceinline__ void next_claim(const ProducerArgs& a, NextItem& n) {
+  n.ticket = atomicAdd(&a.claim[n.q], 1u);
+  n.q0 = a.queue[n.q];
+  n.q1 = a.queue[n.q + 1];
+  n.done = false;
+}
+
+__device__ __forceinline__ uint32_t item_tile_row(uint32_t item) {
+  return (item >> kItemRowShift) & (uint32_t)(kMaxTileRows - 1);
+}
+
+// Resolves the claim (the other queues in turn if queue q ran dry) and loads the descriptor.
+__device__ __forceinline__ void next_resolve(const ProducerArgs& a, NextItem& n, uint32_t end) {
+  if (n.done) return;
+  if (n.ticket < (uint32_t)(n.q1 - n.q0)) {
+    n.pos = (uint32_t)n.q0 + n.ticket;
+  } else {
+    n.q = (n.q + 1) & (kXcds - 1);
+    n.pos = claim_item(a, n.q, end, kXcds - 1);
+  }
+  if (n.pos < end) {
+    n.item = a.items[n.pos];
+    n.tr = a.tile_rows[item_tile_row(n.item)];
+  }
+  n.done = true;
+}
+
+// Thread 0 hands the next item over through the shared words (the ring is idle).
+__device__ __forceinline__ void next_publish(const ProducerArgs& a, NextItem& n, uint32_t end, uint32_t* words) {
+  next_resolve(a, n, end);
+  words[kWordPos] = n.pos;
+  if (n.pos < end) {
+    words[kWordItem] = n.item;
+    words[kWordTileRow + 0] = (uint32_t)n.tr.expert;
+    words[kWordTileRow + 1] = (uint32_t)n.tr.lrow0;
+    words[kWordTileRow + 2] = (uint32_t)n.tr.nvalid;
+    words[kWordTileRow + 3] = (uint32_t)n.tr.has_remote;
+    words[kWordTileRow + 4] = (uint32_t)n.tr.split;
+    words[kWordTileRow + 5] = (uint32_t)n.tr.part_base;
+  }
+}
+
+// Every thread reads the published item (uniform values, kept in scalar registers).
+__device__ __forceinline__ uint32_t read_item(const uint32_t* words, uint32_t& item, TileRow& tr) {
+  const uint32_t pos = __builtin_amdgcn_readfirstlane(words[kWordPos]);
+  item = __builtin_amdgcn_readfirstlane(words[kWordItem]);
+  tr.expert = __builtin_amdgcn_readfirstlane((int)words[kWordTileRow + 0]);
+  tr.lrow0 = __builtin_amdgcn_readfirstlane((int)words[kWordTileRow + 1]);
+  tr.nvalid = __builtin_amdgcn_readfirstlane((int)words[kWordTileRow + 2]);
+  tr.has_remote = __builtin_amdgcn_readfirstlane((int)words[kWordTileRow + 3]);
+  tr.split = __builtin_amdgcn_readfirstlane((int)words[kWordTileRow + 4]);
+  tr.part_base = __builtin_amdgcn_readfirstlane((int)words[kWordTileRow + 5]);
+  return pos;
+}
+
 // Persistent producer: every workgroup claims items from this launch's queues until they are
 // empty.  Nothing inside waits on another workgroup, so progress never depends on which
 // workgroups are resident.
 template <bool down, int kSplit>
 __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsBytes];
-  uint32_t* words = (uint32_t*)(lds + kSharedWords);  // [0] next item, [1] split-K verdict
+  uint32_t* words = (uint32_t*)(lds + kSharedWords);
   const int tid = threadIdx.x;
   // Where consumer waves share a SIMD with this wave (shared CUs), the producer's instructions
   // issue first: its workgroups are the stage's critical path, the consumer's copies are not.
   __builtin_amdgcn_s_setprio(3);
-  uint32_t q = xcc_id();  // meaningful in thread 0, which does the claiming
   const uint32_t end = (uint32_t)a.queue[kXcds];
   const uint64_t t_start = ticks();
   const uint64_t c_start = clock64();
+  NextItem nx;  // meaningful in thread 0, which does the claiming
   if (tid == 0) {
-    words[0] = claim_item(a, q, end);
-    if (words[0] < end) atomicAdd(a.active, 1u);
+    nx.q = xcc_id();
+    nx.pos = claim_item(a, nx.q, end);
+    if (nx.pos < end) {
+      atomicAdd(a.active, 1u);
+      nx.item = a.items[nx.pos];
+      nx.tr = a.tile_rows[item_tile_row(nx.item)];
+    }
+    nx.done = true;
+    next_publish(a, nx, end, words);
   }
   __syncthreads();
-  uint32_t cur = __builtin_amdgcn_readfirstlane(words[0]);  // uniform: item fields stay scalar
+  uint32_t item;
+  TileRow tr;
+  uint32_t cur = read_item(words, item, tr);
   int32_t n_items = 0;
   while (cur < end) {
     ++n_items;
-    __syncthreads();  // every wave has read the word before the operand ring overwrites it
-    // Claim the next item now; thread 0 holds its index while this one runs and passes it
-    // on through LDS once the operand ring is no longer in use.
-    const uint32_t next = tid == 0 ? claim_item(a, q, end) : 0u;
-    const uint32_t item = a.items[cur];
+    __syncthreads();  // every wave has read the words before the operand ring overwrites them
+    // Claim the next item now; thread 0 resolves the claim and fetches the item's descriptor
+    // during the epilogue, and passes it on through LDS at the end.
+    if (tid == 0) next_claim(a, nx);
+    auto hook = [&]() {
+      if (tid == 0) next_resolve(a, nx, end);
+    };
     if constexpr (kSplit < 0) {
       // Split per tile row: whole tiles take the plain epilogue, split rows the part path.
-      const int t = (int)((item >> kItemRowShift) & (uint32_t)(kMaxTileRows - 1));
-      if (a.tile_rows[t].split == 1)
-        producer_item<down, 1>(a, item, lds, words);
+      if (tr.split == 1)
+        producer_item<down, 1>(a, item, tr, lds, words, hook);
       else
-        producer_item<down, 0>(a, item, lds, words);
+        producer_item<down, 0>(a, item, tr, lds, words, hook);
     } else {
-      producer_item<down, kSplit>(a, item, lds, words);
+      producer_item<down, kSplit>(a, item, tr, lds, words, hook);
     }
-    if (tid == 0) words[0] = next;
+    if (tid == 0) next_publish(a, nx, end, words);
     __syncthreads();
-    cur = __builtin_amdgcn_readfirstlane(words[0]);
+    cur = read_item(words, item, tr);
   }
   if (a.wg_rec && tid == 0) {  // timestamped runs: where and when this workgroup ran
     // The last item is done (a signalled down item has also waited for its stores).

@@ -167,8 +167,9 @@ int producer_blocks_per_cu();
 constexpr int kProducerThreads = 256;
 constexpr int kConsumerThreads = 256;
 // 16-byte vectors per consumer lane and copy chunk (two chunks in flight): beside the producer,
-// within 64 VGPRs; on compute units of its own, within 128.
-constexpr int kCopyUnroll = 4;
+// within 56 VGPRs (two such waves and a producer wave of 136 VGPRs + 256 AGPRs fill a SIMD's
+// 512 registers); on compute units of its own, within 128.
+constexpr int kCopyUnroll = 3;
 constexpr int kCopyUnrollOwn = 12;
 // Consumer copy units (one wave each) per segment, as a power of two.  Beside the producer
 // (shared compute units) a copying wave slows the producer workgroup on its compute unit, so
@@ -188,8 +189,8 @@ constexpr uint32_t kMaxCopyRecords = 1u << 18;
 constexpr int kPollSleep = 4;
 constexpr uint32_t kPollBackoffMax = 16;
 constexpr int kTailGrid = 1024; // tail kernel workgroups (one pass each on the usual tail)
-// Consumer waves per SIMD the register budget must allow: at most 512 / 8 = 64 VGPRs each, so
-// two consumer waves fit beside one producer wave of up to 384 of the 512 registers.
+// Consumer waves per SIMD the register budget must allow: at most 512 / 8 = 64 VGPRs each (the
+// copy chunk keeps the kernel at 56, so two waves fit beside a producer wave of 392 registers).
 constexpr int kConsumerMinWaves = 8;
 // Consumer waves a SIMD keeps beside the producer (the register budget above), counted per SIMD
 // key (shader engine, shader array, compute unit, SIMD) of each XCD.
