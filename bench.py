@@ -83,8 +83,11 @@ def parse():
     ap.add_argument("--band-rows", type=int, default=0, help="tb_M of the row layout (0 = 1, no alignment)")
     ap.add_argument("--split-k", type=int, default=0, help="K parts per down tile (0 = library default)")
     ap.add_argument("--mgb", type=int, default=1, help="tile-row pieces per middle transfer segment")
-    ap.add_argument("--small", default="8,16,24,32",
-                    help="small consumer partitions (paper's range): measured in both CU modes and mgb 1 and 2")
+    ap.add_argument("--small", default="4,8,16,24,32",
+                    help="small consumer partitions (paper's range): measured in both CU modes and mgb 1 and 2 "
+                         "(a partition owns CUs on every XCD, so requests round up to multiples of 8)")
+    ap.add_argument("--grid", default="2,4,6,8,10,12,14,16,18,20,22,24,26,28,30,32",
+                    help="consumer CU requests of the large_fine shared-CU grid (the paper's consumer-CTA grid)")
     ap.add_argument("--sweep", default="64,128,248", help="further shared-CU splits of the sweep")
     ap.add_argument("--copy-curve", default="8,16,32,64,128",
                     help="consumer CU counts for the consumer-only copy ceiling ('' to skip)")
@@ -540,6 +543,9 @@ def measure_workload(torch, B, wl, args, headline):
         points = [(args.cu_split, args.mode, args.mgb)]
         points += [(c, m, g) for g in (1, 2) for c in small for m in ("shared", "partitioned")]
         points += [(c, "shared", 1) for c in wide if (c, "shared", 1) not in points]
+        if name == "large_fine":
+            grid = [int(v) for v in args.grid.split(",") if v]
+            points += [(c, "shared", 1) for c in grid if (c, "shared", 1) not in points]
         for c, m, g in points:
             r = bench.plain(m, "overlapped", c, max(steps // 2, 20), warmup, wo, mgb=g)
             sweep.append({"cu_split": c, "cu_mode": m, "mgb": g, "consumer_cus": int(r["stats"]["consumer_cus"]),

@@ -827,7 +827,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   uint32_t mode = (h->cfg.flags & MOE_TEST_NO_SIGNAL) ? 0u : kModeSignal;
   if (h->cfg.flags & MOE_LOCAL_DIRECT) mode |= kModeLocalDirect;
   if (h->cfg.down_split_k == 0) mode |= kModeDeferTail;
-  const ProducerArgs pgu = producer_args(h, lay, x, w1, w3, w2, mode, false);
+  ProducerArgs pgu = producer_args(h, lay, x, w1, w3, w2, mode, false);
   const ProducerArgs pdn = producer_args(h, lay, x, w1, w3, w2, mode, true);
   ConsumerArgs ca{};
   ca.y = h->y;
@@ -847,23 +847,33 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
     ca.rec_cap = kMaxCopyRecords;
   }
 
-  // The consumer is released as soon as the init kernel has reset the queue heads: it only
-  // reads segments of the uploaded plan and flags this run's down launch raises, so no event
-  // sits between the producer's two launches.  With shared CUs the producer stays on the
-  // caller's stream and follows the init kernel without a cross-queue hop -- unless that is
-  // the legacy null stream, whose launches wait for all earlier work on blocking streams,
-  // the still-polling consumer included: that would be a cycle, so the producer then forks
-  // to the handle's own stream like the partitioned launch.
+  // No event orders the consumer after this run's reset: the consumer launch waits for the run's
+  // epoch in the counters, which the gate/up launch publishes as it starts (it follows the init
+  // kernel), so the caller's stream carries no cross-queue packet (an event there stalled it
+  // ~6 us per run, a kernel of its own ~5 us).
+  // Its queue holds it behind the previous run's consumer, whose waves the previous drain saw
+  // leave before this run's reset.  Should the caller's stream hold back the reset past the
+  // watchdog, the consumer leaves without copying and the drain launch copies every unit.
+  // With shared CUs the producer stays on the caller's stream and is enqueued first, so the
+  // host's consumer launch overlaps the gate/up launch -- unless that stream is the legacy null
+  // stream, whose launches wait for all earlier work on blocking streams, the still-polling
+  // consumer included: that would be a cycle, so the producer then forks to the handle's own
+  // stream like the partitioned launch, after an event that orders it behind the reset.
   hipStream_t ps = on_caller ? stream : h->s_prod;
-  HIP_TRY(h, hipEventRecord(h->ev_fork, stream));
-  HIP_TRY(h, hipStreamWaitEvent(h->s_cons, h->ev_fork, 0));
-  if (!on_caller) HIP_TRY(h, hipStreamWaitEvent(h->s_prod, h->ev_fork, 0));
-  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[3], h->s_cons));
+  const bool producer = !(h->cfg.flags & MOE_TEST_CONSUMER_ONLY);
   // A host-built plan's counts are known here, so empty launches are skipped; a device-built
   // plan's kernels read them and return at once when there is nothing to do.
   const bool known = !dev;
+  const bool gu_launch = producer && (!known || h->plan.n_gu > 0);
+  if (gu_launch)
+    pgu.go_ctr = h->ctr;
+  else
+    HIP_TRY(h, launch_go(h->ctr, h->epoch, stream));
+  if (!on_caller) {
+    HIP_TRY(h, hipEventRecord(h->ev_fork, stream));
+    HIP_TRY(h, hipStreamWaitEvent(h->s_prod, h->ev_fork, 0));
+  }
   const bool plain = (h->cfg.flags & MOE_TEST_CONSUMER_ONLY) && (h->cfg.flags & MOE_TEST_PLAIN_COPY);
-  const bool producer = !(h->cfg.flags & MOE_TEST_CONSUMER_ONLY);
   // With a producer, the run ends with a drain launch in the producer's stream: it copies the
   // units the consumer has not claimed by then on the producer's compute units and waits for the
   // consumer's last wave, so the caller's stream needs no event from the consumer's queue.
@@ -872,6 +882,14 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
     ca.role = kRoleCounted;
     ca.map_grid = (uint32_t)cgrid;
   }
+  ca.wait_go = 1;
+  auto gate_up = [&]() -> int {
+    if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], ps));
+    if (gu_launch) HIP_TRY(h, launch_producer(pgu, false, pgrid, ps));
+    return MOE_OK;
+  };
+  if (on_caller && (rc = gate_up()) != MOE_OK) return rc;
+  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[3], h->s_cons));
   if (plain && known) {
     // As many rows as the segments hold, bounded by the staged output and the first receive buffer.
     int64_t rows = 0;
@@ -884,8 +902,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   }
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
   HIP_TRY(h, hipEventRecord(h->ev_join_c, h->s_cons));
-  if (tr) HIP_TRY(h, hipEventRecord(tr->ev[1], ps));
-  if (producer && (!known || h->plan.n_gu > 0)) HIP_TRY(h, launch_producer(pgu, false, pgrid, ps));
+  if (!on_caller && (rc = gate_up()) != MOE_OK) return rc;
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[6], ps));
   if (producer && (!known || h->plan.n_down > 0)) HIP_TRY(h, launch_producer(pdn, true, pgrid, ps));
   if (producer && (pdn.mode & kModeDeferTail) && (!known || h->plan.n_split_rows > 0))
@@ -894,6 +911,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   if (drain) {
     ConsumerArgs da = ca;
     da.role = kRoleDrain;
+    da.wait_go = 0;  // behind the producer in its stream, so behind the reset
     da.simd_waves = nullptr;
     da.exit_waves = (uint32_t)cgrid * (kConsumerThreads / 64);
     HIP_TRY(h, launch_drain(da, shared ? h->num_cus : h->num_cus - c_eff, ps));

@@ -713,6 +713,9 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
   // Where consumer waves share a SIMD with this wave (shared CUs), the producer's instructions
   // issue first: its workgroups are the stage's critical path, the consumer's copies are not.
   __builtin_amdgcn_s_setprio(3);
+  // The init kernel has finished (it precedes this launch in the stream): release the consumer.
+  if (!down && a.go_ctr && blockIdx.x == 0 && tid == 0)
+    __hip_atomic_store(&a.go_ctr->go, a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const uint32_t end = (uint32_t)a.queue[kXcds];
   const uint64_t t_start = ticks();
   const uint64_t c_start = clock64();
@@ -908,26 +911,39 @@ __device__ __forceinline__ void copy_vectors(const u32x4* __restrict__ src, g_u3
   for (int64_t i = nfull * kStep + lane; i < n; i += 64) dst[i] = src[i];
 }
 
-// The ticket loop of one wave: claim a copy unit, wait for its segment's flags, copy its part.
-template <bool kOwn>
-__device__ __forceinline__ void consume_units(const ConsumerArgs& a, int lane) {
+// The units of a run: segments in ready order, the first n_early (ready before the last round
+// of the down queues) cut into 2^early_shift units each, the others into 2^late_shift.
+struct UnitCounts {
+  int32_t n_early;
+  uint32_t early_units, n_units;
+};
+
+__device__ __forceinline__ UnitCounts unit_counts(const ConsumerArgs& a) {
   const int32_t n_segs = *a.n_segs;
-  const uint32_t map_grid = a.map_grid ? a.map_grid : gridDim.x;
-  const uint32_t n_waves = map_grid * (kConsumerThreads / 64);
   // Segments are in ready order: the first late one by binary search (uniform loads).
   const int32_t late_from = *a.down_qmax - kLatePositions;
-  int32_t n_early = 0;
-  for (int32_t hi = n_segs; n_early < hi;) {
-    const int32_t mid = (n_early + hi) >> 1;
+  UnitCounts u;
+  u.n_early = 0;
+  for (int32_t hi = n_segs; u.n_early < hi;) {
+    const int32_t mid = (u.n_early + hi) >> 1;
     if (a.segs[mid].ready_pos < late_from)
-      n_early = mid + 1;
+      u.n_early = mid + 1;
     else
       hi = mid;
   }
+  u.early_units = (uint32_t)u.n_early << a.early_shift;
+  u.n_units = u.early_units + ((uint32_t)(n_segs - u.n_early) << a.late_shift);
+  return u;
+}
+
+// The ticket loop of one wave: claim a copy unit, wait for its segment's flags, copy its part.
+template <bool kOwn>
+__device__ __forceinline__ void consume_units(const ConsumerArgs& a, const UnitCounts& uc, int lane) {
+  const uint32_t map_grid = a.map_grid ? a.map_grid : gridDim.x;
+  const uint32_t n_waves = map_grid * (kConsumerThreads / 64);
+  const int32_t n_early = uc.n_early;
   const int32_t early_shift = a.early_shift, late_shift = a.late_shift;
-  const uint32_t early_units = (uint32_t)n_early << early_shift;
-  const uint32_t n_units = early_units + ((uint32_t)(n_segs - n_early) << late_shift);
-  if (blockIdx.x == 0 && threadIdx.x == 0) a.ctr->n_units = n_units;
+  const uint32_t early_units = uc.early_units, n_units = uc.n_units;
   const uint32_t last_ticket = max(n_waves, n_units);
   uint32_t polls = 0;
   uint64_t waited = 0;
@@ -1027,6 +1043,28 @@ template <bool kOwn>
 __global__ __launch_bounds__(kConsumerThreads, kOwn ? kConsumerOwnMinWaves : kConsumerMinWaves)
 void consumer_kernel(ConsumerArgs a) {
   const int lane = threadIdx.x & 63;
+  if (a.wait_go) {
+    // Launched with no stream dependency on this run's reset: wait until the reset has
+    // published the run's epoch.  If that takes past the watchdog (the caller's stream still
+    // busy with earlier work), leave without claiming anything: the drain launch, which
+    // follows the producer in its stream, copies every unit, so this costs only the overlap.
+    const uint64_t t0 = ticks();
+    uint32_t backoff = 1;
+    bool go = true;
+    while (__hip_atomic_load(&a.ctr->go, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != a.epoch) {
+      if (ticks() - t0 > a.watchdog_ticks) {
+        go = false;
+        break;
+      }
+      for (uint32_t i = 0; i < backoff; ++i) __builtin_amdgcn_s_sleep(kPollSleep);
+      backoff = backoff < kPollBackoffMax ? 2 * backoff : kPollBackoffMax;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if (!go) {
+      if (a.role == kRoleCounted) count_exit(a, lane);
+      return;
+    }
+  }
   if (!kOwn && a.simd_waves) {
     // hw_id: SIMD [5:4], compute unit [11:8], shader array [12], shader engine [15:13].
     uint32_t before = 0;
@@ -1040,7 +1078,32 @@ void consumer_kernel(ConsumerArgs a) {
       return;
     }
   }
-  consume_units<kOwn>(a, lane);
+  UnitCounts uc;
+  bool tickets = true;
+  bool known = false;
+  if (kOwn && a.role == kRoleDrain) {
+    // The consumer has published the unit counts, so the drain skips the unit map (a chain of
+    // dependent loads); usually every ticket is taken too, and the drain leaves at once.
+    const uint64_t pub = __hip_atomic_load(&a.ctr->units_pub, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (pub != 0) {
+      uc.n_units = (uint32_t)(pub >> 32);
+      uc.early_units = (uint32_t)pub;
+      uc.n_early = (int32_t)(uc.early_units >> a.early_shift);
+      const uint32_t next = __hip_atomic_load(&a.ctr->seg_next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      tickets = next < max(a.map_grid * (kConsumerThreads / 64), uc.n_units);
+      known = true;
+    }
+  }
+  if (!known) {
+    uc = unit_counts(a);
+    if (!(kOwn && a.role == kRoleDrain) && blockIdx.x == 0 && threadIdx.x == 0) {
+      // Published at agent scope: the drain launch reads them from other XCDs.
+      __hip_atomic_store(&a.ctr->n_units, uc.n_units, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.ctr->units_pub, ((uint64_t)uc.n_units << 32) | uc.early_units, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  if (tickets) consume_units<kOwn>(a, uc, lane);
   if (a.role == kRoleCounted) {
     count_exit(a, lane);
   } else if (kOwn && a.role == kRoleDrain && blockIdx.x == 0 && threadIdx.x < 64) {
@@ -1121,6 +1184,7 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
     a.ctr->wait_ticks = 0;
     a.ctr->n_units = 0;
     a.ctr->cons_exit = 0;
+    a.ctr->units_pub = 0;
     a.ctr->prod_t0 = ~0ull;
     a.ctr->prod_t1 = 0;
     if (a.plan_hdr) {
@@ -1170,6 +1234,15 @@ hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream
     hipLaunchKernelGGL((producer_kernel<true, 4>), g, b, 0, s, a);
   else
     hipLaunchKernelGGL((producer_kernel<true, 0>), g, b, 0, s, a);
+  return hipGetLastError();
+}
+
+__global__ void go_kernel(RunCounters* ctr, uint32_t epoch) {
+  if (threadIdx.x == 0) __hip_atomic_store(&ctr->go, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+hipError_t launch_go(RunCounters* ctr, uint32_t epoch, hipStream_t s) {
+  hipLaunchKernelGGL(go_kernel, dim3(1), dim3(64), 0, s, ctr, epoch);
   return hipGetLastError();
 }
 

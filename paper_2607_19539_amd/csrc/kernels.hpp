@@ -65,6 +65,7 @@ struct ProducerArgs {
   WgRecord* wg_rec;        // timestamped runs: [grid] records of this launch, else null
   RunCounters* ctr;        // timestamped runs: the producer span (prod_t0 / prod_t1)
   uint64_t* tile_ready;    // timestamped runs: [tiles] when each down tile's flag was raised
+  RunCounters* go_ctr;     // gate/up launch of an overlapped run: publishes go = epoch as it starts
 };
 
 // The tail kernel: finishes the split down tiles after the down launch.  Reads the plan's tile
@@ -99,6 +100,7 @@ struct ConsumerArgs {
   uint32_t map_grid;
   int32_t role;            // kRoleConsumer, kRoleCounted or kRoleDrain
   uint32_t exit_waves;     // drain: consumer waves whose exit it waits for
+  uint32_t wait_go;        // 1: wait until ctr->go holds this run's epoch before anything else
 };
 // Consumer launch roles.  A counted consumer's waves each add one to ctr->cons_exit once their
 // stores are written back; a drain launch (after the producer, in its stream) claims the copy
@@ -154,6 +156,9 @@ hipError_t launch_consumer(const ConsumerArgs& a, bool own_cus, int grid, hipStr
 // After the producer, in its stream: the copy units the consumer has not claimed yet, on the
 // producer's compute units, and the wait for the consumer's last wave.
 hipError_t launch_drain(const ConsumerArgs& a, int grid, hipStream_t s);
+// One thread stores `epoch` into ctr->go (agent scope): the run's reset is complete (for runs
+// without a gate/up launch, which otherwise publishes it).
+hipError_t launch_go(RunCounters* ctr, uint32_t epoch, hipStream_t s);
 // Measurement aid: a flat grid-stride copy of plain_n16 vectors from the staged output into the
 // first receive buffer (no flags, no copy units).
 hipError_t launch_plain_copy(const ConsumerArgs& a, int grid, hipStream_t s);

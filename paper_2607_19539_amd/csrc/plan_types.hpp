@@ -107,6 +107,9 @@ struct RunCounters {
   uint32_t down_active;       // down workgroups that claimed at least one tile
   uint32_t n_units;           // consumer copy units of the run (written by the consumer)
   uint32_t cons_exit;         // consumer waves done (runs that end with a drain launch)
+  uint32_t go;                // epoch of the last run whose reset is complete (set after the
+                              // init kernel by a kernel of its own; the init kernel leaves it)
+  uint64_t units_pub;         // (copy units << 32) | early units, published by the consumer
   uint64_t poll_iters;        // consumer poll iterations
   uint64_t wait_ticks;        // consumer wait time, 100 MHz ticks
   // Timestamped runs only (100 MHz wall clock): first gate/up workgroup start and last
