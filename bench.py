@@ -244,8 +244,28 @@ def overlap_analysis(B, stg, wl):
         "producer_down_workgroups_per_cu_max": max(per_cu.values()) if per_cu else 0,
         "consumer_cus_shared_with_producer": len(cons_cu & prod_cu),
         "producer_clock_GHz": producer_clocks(wg, grid, cons_cu),
+        "down_end_spread": down_end_spread(wg, grid, cons_cu),
     })
     return out
+
+
+def down_end_spread(wg, grid, cons_cu):
+    """When the down launch's workgroups finished, relative to the launch's first start: the
+    median and the last, and the last among workgroups on the consumer's compute units and on
+    the others (the launch ends with its slowest workgroup)."""
+    w = wg[grid:2 * grid]
+    w = w[w["items"] > 0]
+    if len(w) == 0:
+        return None
+    t0 = int(w["t_start"].min())
+    end = (w["t_end"].astype(np.int64) - t0) * TICK_US
+    on = np.array([cu_key(h, x) in cons_cu for h, x in zip(w["hw_id"], w["xcc_id"])], bool)
+    r = {"median_end_us": round(float(np.median(end)), 1), "last_end_us": round(float(end.max()), 1)}
+    if on.any():
+        r["last_end_on_consumer_cus_us"] = round(float(end[on].max()), 1)
+    if (~on).any():
+        r["last_end_elsewhere_us"] = round(float(end[~on].max()), 1)
+    return r
 
 
 class Bench:
@@ -368,8 +388,9 @@ class Bench:
             stg.query(check=False)
             if path == "serial":
                 span = stg.records(self.B.MOE_RECORDS_SPAN)[0]
-                return {"producer_clock_GHz": producer_clocks(stg.records(self.B.MOE_RECORDS_PRODUCER),
-                                                              int(span["producer_grid"]))}
+                wg = stg.records(self.B.MOE_RECORDS_PRODUCER)
+                return {"producer_clock_GHz": producer_clocks(wg, int(span["producer_grid"])),
+                        "down_end_spread": down_end_spread(wg, int(span["producer_grid"]), set())}
             return overlap_analysis(self.B, stg, self.wl)
         finally:
             stg.close()
@@ -509,7 +530,11 @@ def measure_workload(torch, B, wl, args, headline):
         raw["timestamps"] = ts
         ts_ser = bench.timestamps(args.mode, 0, warmup, wo, path="serial")
         d["serial"]["producer_clock_GHz"] = ts_ser["producer_clock_GHz"]
+        d["serial"]["down_end_spread"] = ts_ser["down_end_spread"]
+        log(f"{name} down launch ends (median / last / last on consumer CUs / last elsewhere): serial "
+            f"{ts_ser['down_end_spread']}, overlapped {ts.get('down_end_spread')}")
         raw["serial_clock"] = ts_ser["producer_clock_GHz"]
+        raw["serial_end_spread"] = ts_ser["down_end_spread"]
         log(f"{name} producer clock GHz: serial {ts_ser['producer_clock_GHz']}, overlapped {ts.get('producer_clock_GHz')}")
         log(f"{name} timestamps: overlap ratio {ts.get('overlap_ratio')}, exposed copy {ts.get('exposed_copy_us')} us, "
             f"flag->copy start p50/p90/max {ts.get('flag_to_copy_start_us_p50_p90_max')} us, consumer CUs "
@@ -674,6 +699,8 @@ def compact_line(args, detail, name, raw, wl):
     if raw.get("serial_clock") or ts.get("producer_clock_GHz"):
         # Mean shader clock of the gate/up and down launches, from the workgroups' cycle counts.
         out["producer"]["clock_GHz"] = {"serial": raw.get("serial_clock"), "overlapped": ts.get("producer_clock_GHz")}
+        # When the down launch's workgroups finished (us after its start): median and last.
+        out["producer"]["down_end_us"] = {"serial": raw.get("serial_end_spread"), "overlapped": ts.get("down_end_spread")}
     if ovl is not None:
         out["consumer"] = {"us": ovl["consumer_ms"] * 1e3, "copy_bytes": ts.get("copy_bytes"),
                            "units": int(st["copy_units"]),

@@ -869,9 +869,12 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
     pgu.go_ctr = h->ctr;
   else
     HIP_TRY(h, launch_go(h->ctr, h->epoch, stream));
-  if (!on_caller) {
+  if (!on_caller || !producer) {
+    // The handle's producer stream follows the reset through an event; so does the consumer of
+    // the consumer-only measurement, whose timing then starts at the reset.
     HIP_TRY(h, hipEventRecord(h->ev_fork, stream));
-    HIP_TRY(h, hipStreamWaitEvent(h->s_prod, h->ev_fork, 0));
+    if (!on_caller) HIP_TRY(h, hipStreamWaitEvent(h->s_prod, h->ev_fork, 0));
+    if (!producer) HIP_TRY(h, hipStreamWaitEvent(h->s_cons, h->ev_fork, 0));
   }
   const bool plain = (h->cfg.flags & MOE_TEST_CONSUMER_ONLY) && (h->cfg.flags & MOE_TEST_PLAIN_COPY);
   // With a producer, the run ends with a drain launch in the producer's stream: it copies the
