@@ -75,8 +75,8 @@ def parse():
     ap.add_argument("--extra-workloads", default="tiny,mixtral_zipf,fine,large_fine",
                     help="further workloads measured into the detail file ('' = none)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cu-split", type=int, default=32,
-                    help="consumer compute units of the headline path (a small partition, 12.5 %% of the GPU)")
+    ap.add_argument("--cu-split", type=int, default=64,
+                    help="consumer compute units of the headline path (a quarter of the GPU, one wave per SIMD)")
     ap.add_argument("--mode", choices=["shared", "partitioned"], default="shared",
                     help="shared: the producer keeps every CU and the consumer runs beside it on its "
                          "cu_split CUs; partitioned: the consumer's CUs are reserved for it")

@@ -44,7 +44,7 @@ constexpr int kTimingRing = 512;
 // With shared CUs the consumer's waves are best spread thinly over many compute units (each
 // slows the producer workgroup beside it); a reserved partition takes its CUs from the producer,
 // so it stays small.
-constexpr int kAutoSplitsShared[] = {16, 32, 64, 248};
+constexpr int kAutoSplitsShared[] = {32, 64, 128, 248};
 constexpr int kAutoSplitsPartitioned[] = {8, 16, 32, 64};
 constexpr int kNumAutoSplits = sizeof(kAutoSplitsShared) / sizeof(kAutoSplitsShared[0]);
 static_assert(sizeof(kAutoSplitsPartitioned) == sizeof(kAutoSplitsShared), "one candidate count");
@@ -119,7 +119,7 @@ struct moe_stage_s {
   WgRecord* wg_rec = nullptr;      // MOE_TIMESTAMPS: [2][num_cus * producer_bpc] per launch
   CopyRecord* copy_rec = nullptr;  // MOE_TIMESTAMPS: [kMaxCopyRecords]
   uint64_t* tile_ready = nullptr;  // MOE_TIMESTAMPS: [max_tile_rows * down_per_row] flag times
-  uint32_t* simd_waves = nullptr;  // consumer waves per SIMD beside the producer [kXcds * kSimdKeys]
+  uint32_t* simd_waves = nullptr;  // consumer waves per SIMD and per CU beside the producer [kWaveCounters]
   int32_t last_tiles = 0;          // down tiles of the last run (tile rows x down_per_row)
   uint8_t* d_plan = nullptr;
   size_t plan_cap = 0;
@@ -586,6 +586,14 @@ void copy_units(int32_t H, bool shared, int32_t* early_shift, int32_t* late_shif
   }
 }
 
+// Consumer waves per compute unit beside the producer for a split of c compute units: a power of
+// two, 1 to 8, so that about kConsumerWavesShared waves copy in all.
+int consumer_waves_per_cu(int c) {
+  int w = 1;
+  while (w < 8 && (w * 2) * c <= kConsumerWavesShared) w *= 2;
+  return w;
+}
+
 // Consumer CUs actually reserved for a requested split: a multiple of the XCD count.
 int effective_split(const moe_stage_s* h, int c) {
   const int n = h->n_xcd;
@@ -726,8 +734,8 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       !try_hip(hipMalloc(&h->y, y_bytes), "hipMalloc(y)") ||
       !try_hip(hipMalloc(&h->flags, flag_bytes), "hipMalloc(flags)") ||
       !try_hip(hipMalloc(&h->ctr, sizeof(RunCounters)), "hipMalloc(counters)") ||
-      !try_hip(hipMalloc(&h->simd_waves, sizeof(uint32_t) * kXcds * kSimdKeys), "hipMalloc(counters)") ||
-      !try_hip(hipMemset(h->simd_waves, 0, sizeof(uint32_t) * kXcds * kSimdKeys), "hipMemset(counters)") ||
+      !try_hip(hipMalloc(&h->simd_waves, sizeof(uint32_t) * kWaveCounters), "hipMalloc(counters)") ||
+      !try_hip(hipMemset(h->simd_waves, 0, sizeof(uint32_t) * kWaveCounters), "hipMemset(counters)") ||
       !try_hip(hipMalloc(&h->d_plan, h->plan_cap), "hipMalloc(plan)") ||
       !try_hip(hipMalloc(&h->dev_ws, ws_bytes), "hipMalloc(planner scratch)") ||
       !try_hip(hipHostMalloc(&h->h_stage[0], h->plan_cap, hipHostMallocDefault), "hipHostMalloc") ||
@@ -804,7 +812,14 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   // Consumer workgroups per CU: two beside a producer workgroup (their registers fill what a
   // producer wave leaves free), four of the wider variant when the consumer owns its CUs.
   const bool own_cus = !shared;
-  const int cgrid = c_eff * (own_cus ? kConsumerOwnPerCu : 2);
+  // Consumer waves beside the producer: about kConsumerWavesShared in all, spread over the c_eff
+  // compute units (8 per CU on 32 CUs, 1 per CU on 248): each copying wave slows the producer
+  // workgroup on its compute unit, so a wide split copies thinly everywhere, and the down launch's
+  // last workgroups are not held back on a few busy compute units.  On compute units of its own the
+  // consumer runs kConsumerOwnPerCu workgroups of four waves per compute unit.
+  const int wpc = own_cus ? 4 * kConsumerOwnPerCu : consumer_waves_per_cu(c_eff);
+  const int cthreads = own_cus ? kConsumerThreads : 64 * std::min(wpc, 4);
+  const int cgrid = own_cus ? c_eff * kConsumerOwnPerCu : c_eff * std::max(1, wpc / 4);
   const bool legacy = stream == nullptr || stream == hipStreamLegacy;
   const bool on_caller = shared && !legacy;
   // The adaptive selector keeps its candidates' queues until it has settled.
@@ -841,7 +856,10 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   ca.ctr = h->ctr;
   ca.watchdog_ticks = watchdog_ticks(h);
   copy_units(h->cfg.hidden, !own_cus, &ca.early_shift, &ca.late_shift);
-  if (!own_cus) ca.simd_waves = h->simd_waves;
+  if (!own_cus) {
+    ca.simd_waves = h->simd_waves;
+    ca.max_waves_cu = (uint32_t)wpc;
+  }
   if (h->copy_rec) {
     ca.rec = h->copy_rec;
     ca.rec_cap = kMaxCopyRecords;
@@ -884,6 +902,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   if (drain) {
     ca.role = kRoleCounted;
     ca.map_grid = (uint32_t)cgrid;
+    ca.map_wpg = (uint32_t)(cthreads / 64);
   }
   ca.wait_go = 1;
   auto gate_up = [&]() -> int {
@@ -901,7 +920,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
     ca.plain_n16 = rows * h->cfg.hidden / 8;
     if (ca.plain_n16 > 0) HIP_TRY(h, launch_plain_copy(ca, c_eff * kConsumerOwnPerCu, h->s_cons));
   } else if (!known || !h->plan.segs.empty()) {
-    HIP_TRY(h, launch_consumer(ca, own_cus, cgrid, h->s_cons));
+    HIP_TRY(h, launch_consumer(ca, own_cus, cgrid, cthreads, h->s_cons));
   }
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], h->s_cons));
   HIP_TRY(h, hipEventRecord(h->ev_join_c, h->s_cons));
@@ -916,7 +935,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
     da.role = kRoleDrain;
     da.wait_go = 0;  // behind the producer in its stream, so behind the reset
     da.simd_waves = nullptr;
-    da.exit_waves = (uint32_t)cgrid * (kConsumerThreads / 64);
+    da.exit_waves = (uint32_t)cgrid * (uint32_t)(cthreads / 64);
     HIP_TRY(h, launch_drain(da, shared ? h->num_cus : h->num_cus - c_eff, ps));
   }
   if (!on_caller) {

@@ -34,6 +34,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // Global-memory view of a pointer that was loaded from memory (the receive-buffer table): the
 // compiler cannot infer its address space and would emit flat accesses.
 typedef __attribute__((address_space(1))) u32x4 g_u32x4;
+// Word 3 of a raw buffer resource on gfx9-family GPUs (stride 0, byte-addressed, range-checked).
+constexpr int kBufferRsrcWord3 = 0x00020000;
 
 // Operand blocks in LDS: 256 rows x 64 k (bf16) = 32 KiB, 128 bytes per row -- one whole
 // cache line of the row-major operand, so every line a K step touches is used in full (with
@@ -870,32 +872,44 @@ __global__ __launch_bounds__(kProducerThreads) void tail_kernel(TailArgs ta) {
 // kernel uses no LDS, so in a shared-CU run its workgroups never keep a producer workgroup
 // (which takes all of LDS) off a compute unit.
 //
-// kOwn = false (beside the producer): at most 64 VGPRs per wave, so two consumer waves fit
-// beside a producer wave on a SIMD, and at most kMaxConsumerWavesPerSimd consumer waves stay on
-// a SIMD: a wave that finds more already there exits at once, so consumer waves that happened to
-// pile onto one compute unit before the producer arrived never keep a producer workgroup off it.
-// A copying wave slows the producer workgroup on its compute unit, so the units are spread: the
-// first tickets are dealt transposed (ticket 4b + w to unit w x grid + b), so the waves of one
-// workgroup, which claim together, take parts of different segments, about one copying wave
-// per compute unit.  kOwn = true (compute units of its own): up to 128 VGPRs, twice the data in
-// flight per wave.
+// kOwn = false (beside the producer): at most 56 VGPRs per wave, so two consumer waves fit
+// beside a producer wave on a SIMD.  A copying wave slows the producer workgroup on its compute
+// unit, so the launch spreads about 256 waves over the split's compute units (one per compute
+// unit on a wide split, eight on a narrow one), and a wave that finds its SIMD or its compute unit
+// already holding its share exits at once: consumer waves that happened to pile onto one compute
+// unit before the producer arrived never keep a producer workgroup off it, nor crowd its memory
+// path.  The first tickets are dealt transposed, so the waves of one workgroup, which claim
+// together, take parts of different segments.  kOwn = true (compute units of its own): up to 128
+// VGPRs, about three times the data in flight per wave.
 // ---------------------------------------------------------------------------
 
 // Copies n 16-byte vectors from src to dst, kU per lane per chunk, with two register buffers in
 // turn so one chunk's loads are in flight while the other's stores issue.
+//
+// The staged rows are read with agent-scope coherent, streaming buffer loads (cache policy sc1 nt):
+// each load sees what the producer stored at the coherence point, whichever XCD it ran on, so the
+// copy needs no acquire fence after the flag poll.  On gfx950 an agent-scope acquire invalidates
+// the XCD's whole L2, which would throw away the operand panels the producer workgroups on that
+// XCD keep there (one invalidation per copy unit while the down launch runs); the streaming hint
+// keeps the copied lines from displacing those panels.  The source run is below 4 GiB (the
+// handle's staged output is), so 32-bit buffer offsets reach all of it.
+constexpr int kLoadAgentStream = 16 | 2;  // buffer-load cache policy: sc1 (agent scope) | nt
+
 template <int kU>
-__device__ __forceinline__ void copy_vectors(const u32x4* __restrict__ src, g_u32x4* __restrict__ dst, int64_t n,
-                                             int lane) {
+__device__ __forceinline__ void copy_vectors(const void* src, g_u32x4* __restrict__ dst, int64_t n, int lane) {
   constexpr int64_t kStep = (int64_t)kU * 64;
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(src), 0, (int)(uint32_t)min<int64_t>(n * 16, INT_MAX), kBufferRsrcWord3);
+  auto ld = [&](int64_t i) { return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(i * 16), 0, kLoadAgentStream); };
   const int64_t nfull = n / kStep;
   u32x4 a[kU], b[kU];
   auto load = [&](u32x4 (&r)[kU], int64_t c) {
 #pragma unroll
-    for (int u = 0; u < kU; ++u) r[u] = src[c * kStep + lane + u * 64];
+    for (int u = 0; u < kU; ++u) r[u] = ld(c * kStep + lane + u * 64);
   };
   auto store = [&](const u32x4 (&r)[kU], int64_t c) {
 #pragma unroll
-    for (int u = 0; u < kU; ++u) dst[c * kStep + lane + u * 64] = r[u];
+    for (int u = 0; u < kU; ++u) __builtin_nontemporal_store(r[u], dst + (c * kStep + lane + u * 64));
   };
   if (nfull > 0) {
     load(a, 0);
@@ -908,7 +922,33 @@ __device__ __forceinline__ void copy_vectors(const u32x4* __restrict__ src, g_u3
     }
     if (c < nfull) store(a, c);
   }
-  for (int64_t i = nfull * kStep + lane; i < n; i += 64) dst[i] = src[i];
+  for (int64_t i = nfull * kStep + lane; i < n; i += 64) dst[i] = ld(i);
+}
+
+// Plan words read at agent scope (sc1): coherent with what the run's upload or the device planner
+// wrote, whichever XCD cached an older plan, so the consumer needs no acquire fence (on gfx950 an
+// agent-scope acquire invalidates the XCD's whole L2, under the producer's feet).
+__device__ __forceinline__ int32_t ld_agent(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ Segment load_segment(const Segment* p) {
+  Segment sg;
+  sg.dst_rank = ld_agent(&p->dst_rank);
+  sg.rows = ld_agent(&p->rows);
+  sg.y_row0 = ld_agent(&p->y_row0);
+  sg.slot0 = ld_agent(&p->slot0);
+  sg.flag_begin = ld_agent(&p->flag_begin);
+  sg.flag_count = ld_agent(&p->flag_count);
+  sg.ready_pos = ld_agent(&p->ready_pos);
+  sg.npieces = ld_agent(&p->npieces);
+  return sg;
+}
+
+// The receive buffer of rank r, read from the run's pointer table at agent scope.
+__device__ __forceinline__ uint16_t* ret_buffer(uint16_t* const* table, int r) {
+  const uint64_t v = __hip_atomic_load((const uint64_t*)(table + r), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return (uint16_t*)(uintptr_t)v;
 }
 
 // The units of a run: segments in ready order, the first n_early (ready before the last round
@@ -919,14 +959,14 @@ struct UnitCounts {
 };
 
 __device__ __forceinline__ UnitCounts unit_counts(const ConsumerArgs& a) {
-  const int32_t n_segs = *a.n_segs;
+  const int32_t n_segs = ld_agent(a.n_segs);
   // Segments are in ready order: the first late one by binary search (uniform loads).
-  const int32_t late_from = *a.down_qmax - kLatePositions;
+  const int32_t late_from = ld_agent(a.down_qmax) - kLatePositions;
   UnitCounts u;
   u.n_early = 0;
   for (int32_t hi = n_segs; u.n_early < hi;) {
     const int32_t mid = (u.n_early + hi) >> 1;
-    if (a.segs[mid].ready_pos < late_from)
+    if (ld_agent(&a.segs[mid].ready_pos) < late_from)
       u.n_early = mid + 1;
     else
       hi = mid;
@@ -937,10 +977,15 @@ __device__ __forceinline__ UnitCounts unit_counts(const ConsumerArgs& a) {
 }
 
 // The ticket loop of one wave: claim a copy unit, wait for its segment's flags, copy its part.
+// The first n_waves tickets are dealt transposed over the waves of the launch that map_grid and
+// map_wpg describe (ticket w_per_wg * b + w to unit w * map_grid + b), so the waves of one
+// workgroup, which claim together, take parts of different segments; later tickets are units in
+// order.
 template <bool kOwn>
 __device__ __forceinline__ void consume_units(const ConsumerArgs& a, const UnitCounts& uc, int lane) {
+  const uint32_t wpg = a.map_wpg ? a.map_wpg : blockDim.x >> 6;
   const uint32_t map_grid = a.map_grid ? a.map_grid : gridDim.x;
-  const uint32_t n_waves = map_grid * (kConsumerThreads / 64);
+  const uint32_t n_waves = map_grid * wpg;
   const int32_t n_early = uc.n_early;
   const int32_t early_shift = a.early_shift, late_shift = a.late_shift;
   const uint32_t early_units = uc.early_units, n_units = uc.n_units;
@@ -952,14 +997,14 @@ __device__ __forceinline__ void consume_units(const ConsumerArgs& a, const UnitC
     if (lane == 0) t = atomicAdd(&a.ctr->seg_next, 1u);
     t = __builtin_amdgcn_readfirstlane(t);  // every lane is active here
     if (t >= last_ticket) break;
-    const uint32_t unit = t < n_waves ? (t % (kConsumerThreads / 64)) * map_grid + t / (kConsumerThreads / 64) : t;
+    const uint32_t unit = t < n_waves ? (t % wpg) * map_grid + t / wpg : t;
     if (unit >= n_units) continue;
     const bool early = unit < early_units;
     const uint32_t u = early ? unit : unit - early_units;
     const int32_t shift = early ? early_shift : late_shift;
     const int32_t s = (early ? 0 : n_early) + (int32_t)(u >> shift);
     const int32_t part = (int32_t)(u & ((1u << shift) - 1));
-    const Segment sg = a.segs[s];
+    const Segment sg = load_segment(a.segs + s);
     const uint64_t t0 = ticks();
     bool expired = false;
     uint32_t backoff = 1;
@@ -981,7 +1026,7 @@ __device__ __forceinline__ void consume_units(const ConsumerArgs& a, const UnitC
         backoff = backoff < kPollBackoffMax ? 2 * backoff : kPollBackoffMax;
       }
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    // No acquire: the copy's loads are agent-scope coherent (see copy_vectors).
     const uint64_t t_ready = ticks();
     waited += t_ready - t0;
     if (expired) {
@@ -995,8 +1040,8 @@ __device__ __forceinline__ void consume_units(const ConsumerArgs& a, const UnitC
     // The segment is contiguous on both sides: this wave's part is a flat run of 16-byte vectors.
     const int64_t n16 = (int64_t)sg.rows * a.H / 8;
     const int64_t i0 = (n16 * part) >> shift, i1 = (n16 * (part + 1)) >> shift;
-    const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H) + i0;
-    g_u32x4* dst = (g_u32x4*)(a.ret[sg.dst_rank] + (int64_t)sg.slot0 * a.H) + i0;
+    const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H) + i0;  // wave-uniform
+    g_u32x4* dst = (g_u32x4*)(ret_buffer(a.ret, sg.dst_rank) + (int64_t)sg.slot0 * a.H) + i0;
     copy_vectors<kOwn ? kCopyUnrollOwn : kCopyUnroll>(src, dst, i1 - i0, lane);
     if (a.rec && unit < a.rec_cap) {
       // Timestamped runs: the unit ends when its stores have completed.
@@ -1059,7 +1104,8 @@ void consumer_kernel(ConsumerArgs a) {
       for (uint32_t i = 0; i < backoff; ++i) __builtin_amdgcn_s_sleep(kPollSleep);
       backoff = backoff < kPollBackoffMax ? 2 * backoff : kPollBackoffMax;
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    // No acquire fence: every plan word, flag and staged row the consumer reads afterwards is read
+    // at agent scope.
     if (!go) {
       if (a.role == kRoleCounted) count_exit(a, lane);
       return;
@@ -1067,30 +1113,31 @@ void consumer_kernel(ConsumerArgs a) {
   }
   if (!kOwn && a.simd_waves) {
     // hw_id: SIMD [5:4], compute unit [11:8], shader array [12], shader engine [15:13].
-    uint32_t before = 0;
+    // A wave past either limit leaves at once.
+    uint32_t over = 0;
     if (lane == 0) {
       const uint32_t h = hw_id();
       const uint32_t key = ((((h >> 13) & 7u) * 2 + ((h >> 12) & 1u)) * 16 + ((h >> 8) & 15u)) * 4 + ((h >> 4) & 3u);
-      before = atomicAdd(&a.simd_waves[xcc_id() * kSimdKeys + key], 1u);
+      const uint32_t x = xcc_id();
+      over = atomicAdd(&a.simd_waves[x * kSimdKeys + key], 1u) >= (uint32_t)kMaxConsumerWavesPerSimd;
+      if (!over && a.max_waves_cu)
+        over = atomicAdd(&a.simd_waves[kXcds * kSimdKeys + x * kCuKeys + (key >> 2)], 1u) >= a.max_waves_cu;
     }
-    if (__builtin_amdgcn_readfirstlane(before) >= (uint32_t)kMaxConsumerWavesPerSimd) {
+    if (__builtin_amdgcn_readfirstlane(over)) {
       if (a.role == kRoleCounted) count_exit(a, lane);
       return;
     }
   }
   UnitCounts uc;
-  bool tickets = true;
   bool known = false;
   if (kOwn && a.role == kRoleDrain) {
     // The consumer has published the unit counts, so the drain skips the unit map (a chain of
-    // dependent loads); usually every ticket is taken too, and the drain leaves at once.
+    // dependent loads).
     const uint64_t pub = __hip_atomic_load(&a.ctr->units_pub, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (pub != 0) {
       uc.n_units = (uint32_t)(pub >> 32);
       uc.early_units = (uint32_t)pub;
       uc.n_early = (int32_t)(uc.early_units >> a.early_shift);
-      const uint32_t next = __hip_atomic_load(&a.ctr->seg_next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      tickets = next < max(a.map_grid * (kConsumerThreads / 64), uc.n_units);
       known = true;
     }
   }
@@ -1102,6 +1149,13 @@ void consumer_kernel(ConsumerArgs a) {
       __hip_atomic_store(&a.ctr->units_pub, ((uint64_t)uc.n_units << 32) | uc.early_units, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
     }
+  }
+  bool tickets = true;
+  if (known) {
+    // Usually the consumer has taken every ticket, and the drain skips the ticket loop.
+    const uint32_t next = __hip_atomic_load(&a.ctr->seg_next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t wpg = a.map_wpg ? a.map_wpg : blockDim.x >> 6;
+    tickets = next < max(a.map_grid * wpg, uc.n_units);
   }
   if (tickets) consume_units<kOwn>(a, uc, lane);
   if (a.role == kRoleCounted) {
@@ -1198,7 +1252,7 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
   if (a.tile_ready)
     for (int64_t j = i; j < a.n_arrivals; j += stride) a.tile_ready[j] = 0;
   if (a.simd_waves)
-    for (int64_t j = i; j < kXcds * kSimdKeys; j += stride) a.simd_waves[j] = 0;
+    for (int64_t j = i; j < kWaveCounters; j += stride) a.simd_waves[j] = 0;
   // Published flags are stored as the producer raises them (relaxed, agent scope): a plain store
   // would sit in this XCD's L2, and the consumer's polls on other XCDs would not see it until the
   // line is written back.
@@ -1251,11 +1305,12 @@ hipError_t launch_drain(const ConsumerArgs& a, int grid, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_consumer(const ConsumerArgs& a, bool own_cus, int grid, hipStream_t s) {
+hipError_t launch_consumer(const ConsumerArgs& a, bool own_cus, int grid, int threads, hipStream_t s) {
+  if (threads <= 0 || threads > kConsumerThreads || threads % 64) return hipErrorInvalidValue;
   if (own_cus)
-    hipLaunchKernelGGL(consumer_kernel<true>, dim3(grid), dim3(kConsumerThreads), 0, s, a);
+    hipLaunchKernelGGL(consumer_kernel<true>, dim3(grid), dim3(threads), 0, s, a);
   else
-    hipLaunchKernelGGL(consumer_kernel<false>, dim3(grid), dim3(kConsumerThreads), 0, s, a);
+    hipLaunchKernelGGL(consumer_kernel<false>, dim3(grid), dim3(threads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -101,6 +101,8 @@ struct ConsumerArgs {
   int32_t role;            // kRoleConsumer, kRoleCounted or kRoleDrain
   uint32_t exit_waves;     // drain: consumer waves whose exit it waits for
   uint32_t wait_go;        // 1: wait until ctr->go holds this run's epoch before anything else
+  uint32_t map_wpg;        // waves per workgroup of the launch map_grid describes (0: this launch's)
+  uint32_t max_waves_cu;   // beside the producer: consumer waves a compute unit keeps (0: no limit)
 };
 // Consumer launch roles.  A counted consumer's waves each add one to ctr->cons_exit once their
 // stores are written back; a drain launch (after the producer, in its stream) claims the copy
@@ -152,7 +154,7 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 // Gate/up tiles (down = false) or down-projection tiles with ready flags (down = true).
 hipError_t launch_producer(const ProducerArgs& a, bool down, int grid, hipStream_t s);
 // own_cus: the consumer has its compute units to itself (a reserved partition, or no producer).
-hipError_t launch_consumer(const ConsumerArgs& a, bool own_cus, int grid, hipStream_t s);
+hipError_t launch_consumer(const ConsumerArgs& a, bool own_cus, int grid, int threads, hipStream_t s);
 // After the producer, in its stream: the copy units the consumer has not claimed yet, on the
 // producer's compute units, and the wait for the consumer's last wave.
 hipError_t launch_drain(const ConsumerArgs& a, int grid, hipStream_t s);
@@ -175,7 +177,7 @@ constexpr int kConsumerThreads = 256;
 // within 56 VGPRs (two such waves and a producer wave of 136 VGPRs + 256 AGPRs fill a SIMD's
 // 512 registers); on compute units of its own, within 128.
 constexpr int kCopyUnroll = 3;
-constexpr int kCopyUnrollOwn = 12;
+constexpr int kCopyUnrollOwn = 10;
 // Consumer copy units (one wave each) per segment, as a power of two.  Beside the producer
 // (shared compute units) a copying wave slows the producer workgroup on its compute unit, so
 // segments take few units (kCopyPartsShift) until the last two rounds of the down queues
@@ -197,10 +199,16 @@ constexpr int kTailGrid = 1024; // tail kernel workgroups (one pass each on the 
 // Consumer waves per SIMD the register budget must allow: at most 512 / 8 = 64 VGPRs each (the
 // copy chunk keeps the kernel at 56, so two waves fit beside a producer wave of 392 registers).
 constexpr int kConsumerMinWaves = 8;
+// Consumer waves beside the producer in all (their copy rate is latency-bound per wave; about 256
+// waves saturate it), spread over however many compute units the split gives the consumer.
+constexpr int kConsumerWavesShared = 256;
 // Consumer waves a SIMD keeps beside the producer (the register budget above), counted per SIMD
 // key (shader engine, shader array, compute unit, SIMD) of each XCD.
 constexpr int kMaxConsumerWavesPerSimd = 2;
 constexpr int kSimdKeys = 1024;
+constexpr int kCuKeys = kSimdKeys / 4;
+// Consumer wave counters beside the producer: per SIMD key, then per compute-unit key, per XCD.
+constexpr int kWaveCounters = kXcds * (kSimdKeys + kCuKeys);
 // On compute units of its own: up to 128 VGPRs, four waves per SIMD (four workgroups per CU).
 constexpr int kConsumerOwnMinWaves = 4;
 constexpr int kConsumerOwnPerCu = 4;
