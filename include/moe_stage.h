@@ -207,7 +207,7 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out);
  * cu_split: compute units for the consumer, 1 <= cu_split <= CUs - XCDs, or 0 to let the
  * handle choose (a runtime-adaptive selector, the future work of paper Sections 4.3.4
  * and 6): it measures
- * the stage time of its own runs at consumer splits of 16, 32, 64 and 248 CUs under
+ * the stage time of its own runs at consumer splits of 32, 64, 128 and 248 CUs under
  * MOE_SHARED_CUS (8, 16, 32 and 64 without it), one after another and each with only its own
  * CU-masked queue alive, four finished runs each (the first a warm-up), skipping any above
  * CUs - XCDs, then keeps the one with the lowest median (stats: auto_cu_split).
@@ -215,7 +215,9 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out);
  * are dealt round-robin over the XCDs (8 on MI355X) and a CU-masked queue must own
  * CUs on each of them, so the split is rounded up to a multiple of the XCD count
  * (the stats report the effective value); the producer gets every other CU, or every
- * CU under MOE_SHARED_CUS.
+ * CU under MOE_SHARED_CUS.  Beside the producer (MOE_SHARED_CUS) the consumer runs about
+ * 256 waves spread over its cu_split CUs (8 per CU on 32 CUs, 1 per CU on 248); on CUs of
+ * its own it runs 16 waves per CU.
  */
 int moe_stage_run(moe_stage_t h, const void* dispatched_x, const int32_t* expert_offsets,
                   const int32_t* row_src_rank, const int32_t* row_slot, const void* w1,
