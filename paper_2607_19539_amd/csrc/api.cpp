@@ -586,6 +586,17 @@ void copy_units(int32_t H, bool shared, int32_t* early_shift, int32_t* late_shif
   }
 }
 
+// The copy units of a host-built plan, as the consumer counts them from the uploaded plan: the
+// segments ready before the last kLatePositions positions of the longest down queue take
+// 2^early_shift units each, the others 2^late_shift.
+int64_t host_copy_units(const Plan& P, int32_t early_shift, int32_t late_shift) {
+  int32_t qmax = 0;
+  for (int x = 0; x < kXcds; ++x) qmax = std::max(qmax, P.down_queue[x + 1] - P.down_queue[x]);
+  int64_t early = 0;
+  while (early < (int64_t)P.segs.size() && P.segs[early].ready_pos < qmax - kLatePositions) ++early;
+  return (early << early_shift) + (((int64_t)P.segs.size() - early) << late_shift);
+}
+
 // Consumer waves per compute unit beside the producer for a split of c compute units: a power of
 // two, 1 to 8, so that about kConsumerWavesShared waves copy in all.
 int consumer_waves_per_cu(int c) {
@@ -819,7 +830,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   // consumer runs kConsumerOwnPerCu workgroups of four waves per compute unit.
   const int wpc = own_cus ? 4 * kConsumerOwnPerCu : consumer_waves_per_cu(c_eff);
   const int cthreads = own_cus ? kConsumerThreads : 64 * std::min(wpc, 4);
-  const int cgrid = own_cus ? c_eff * kConsumerOwnPerCu : c_eff * std::max(1, wpc / 4);
+  int cgrid = own_cus ? c_eff * kConsumerOwnPerCu : c_eff * std::max(1, wpc / 4);
   const bool legacy = stream == nullptr || stream == hipStreamLegacy;
   const bool on_caller = shared && !legacy;
   // The adaptive selector keeps its candidates' queues until it has settled.
@@ -836,6 +847,17 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
     return rc;
   }
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[7], stream));
+  int32_t early_shift = 0, late_shift = 0;
+  copy_units(h->cfg.hidden, !own_cus, &early_shift, &late_shift);
+  // A host-built plan's copy units are known: launch no more consumer waves than there are units
+  // (a small stage's few units would otherwise send hundreds of waves claiming nothing), and a
+  // drain of about one workgroup per four units.
+  int dgrid = shared ? h->num_cus : h->num_cus - c_eff;
+  if (!dev) {
+    const int64_t units = host_copy_units(h->plan, early_shift, late_shift);
+    cgrid = (int)std::min<int64_t>(cgrid, std::max<int64_t>(1, (units + cthreads / 64 - 1) / (cthreads / 64)));
+    dgrid = (int)std::min<int64_t>(dgrid, std::max<int64_t>(h->n_xcd, (units + 3) / 4));
+  }
   h->last.producer_grid = pgrid;
   h->last.consumer_grid = cgrid;
   h->last.consumer_cus = c_eff;
@@ -855,7 +877,8 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   ca.H = h->cfg.hidden;
   ca.ctr = h->ctr;
   ca.watchdog_ticks = watchdog_ticks(h);
-  copy_units(h->cfg.hidden, !own_cus, &ca.early_shift, &ca.late_shift);
+  ca.early_shift = early_shift;
+  ca.late_shift = late_shift;
   if (!own_cus) {
     ca.simd_waves = h->simd_waves;
     ca.max_waves_cu = (uint32_t)wpc;
@@ -936,7 +959,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
     da.wait_go = 0;  // behind the producer in its stream, so behind the reset
     da.simd_waves = nullptr;
     da.exit_waves = (uint32_t)cgrid * (uint32_t)(cthreads / 64);
-    HIP_TRY(h, launch_drain(da, shared ? h->num_cus : h->num_cus - c_eff, ps));
+    HIP_TRY(h, launch_drain(da, dgrid, ps));
   }
   if (!on_caller) {
     HIP_TRY(h, hipEventRecord(h->ev_join_p, h->s_prod));
