@@ -19,7 +19,7 @@ from tests.gpu_helpers import DeviceWorkload, compare, log, make_stage, SENTINEL
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
-BENCH_CU_SPLIT = 32
+BENCH_CU_SPLIT = 64
 BENCH_FLAGS = B.MOE_LOCAL_DIRECT | B.MOE_SHARED_CUS   # bench.py's default mode, on its own stream
 RANDOM_ROWS = 24
 
@@ -107,15 +107,16 @@ def test_fullsize_stratified(name):
             want[wl.row_slot[wl.row_src_rank == r]] = True
             assert np.array_equal(written_mask(dw.bufs[r]), want), f"rank {r} placement"
         over = [b.clone() for b in dw.bufs]
-        # A narrow and a wide consumer beside the producer: with 8 CUs most units are claimed
-        # after each wave's first one, with 248 many waves find no unit left.
-        for c in (8, 248):
+        # Narrower and wider consumers beside the producer: with 8 CUs (eight waves each) most
+        # units are claimed after each wave's first one; with 248 (one wave each) many waves find
+        # no unit left.
+        for c in (8, 32, 248):
             dw.fill()
             torch.cuda.synchronize()
             st.run(*dw.args(), cu_split=c, stream=side)
             torch.cuda.synchronize()
             other = st.query()
-            log(f"full-size {name}: c={c} shared units={other['copy_units']} consumer waves={4 * other['consumer_grid']}")
+            log(f"full-size {name}: c={c} shared units={other['copy_units']} consumer workgroups={other['consumer_grid']}")
             assert other["timeout"] == 0
             for a, b in zip(over, dw.bufs):
                 assert torch.equal(a, b), f"consumer splits differ (c={c})"
