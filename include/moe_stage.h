@@ -54,7 +54,12 @@ extern "C" {
                               /* its receive buffer, or two rows with the same (rank, slot)     */
 #define MOE_ECAPACITY (-3)    /* rows > max_rows, or the plan exceeds the handle's workspaces   */
 #define MOE_EHIP (-4)         /* a HIP runtime call failed (message names it)                  */
-#define MOE_ETIMEOUT (-5)     /* a bounded device wait expired; sticky until the next query   */
+#define MOE_ETIMEOUT (-5)     /* a bounded device wait expired; sticky until the next query.
+                                 A consumer wave whose flag wait expires hands its copy unit to
+                                 the drain launch, which copies it after the producer, so an
+                                 overlapped run's output is still complete; the run took at least
+                                 watchdog_ms.  Only an expired wait of the drain itself (for the
+                                 consumer's last wave) can leave rows uncopied               */
 #define MOE_EUNSUPPORTED (-6) /* hidden/ffn not multiples of 64, hidden > 65536, max_rows >=
                                  2^24, max_rows * hidden * 2 > 2^32 - 1 (gathered rows are
                                  addressed with 32-bit offsets), a padded layout of more than
@@ -69,7 +74,8 @@ extern "C" {
                                        copy that races ahead of its data is detectable          */
 #define MOE_TEST_NO_SIGNAL (1u << 3) /* testing aid: the producer raises no ready flags, so every
                                        consumer wait runs into watchdog_ms and the run reports
-                                       MOE_ETIMEOUT; the kernels still exit normally            */
+                                       MOE_ETIMEOUT; the kernels still exit normally and the drain
+                                       launch copies every unit                                 */
 #define MOE_TEST_CONSUMER_ONLY (1u << 6) /* measurement aid: moe_stage_run launches no producer
                                        work; the run's reset publishes every ready flag, so the
                                        consumer copies the staged output (whatever it holds) at

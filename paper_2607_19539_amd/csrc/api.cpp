@@ -115,6 +115,7 @@ struct moe_stage_s {
   uint32_t* flags = nullptr;
   float* partials = nullptr;
   uint32_t* arrivals = nullptr;
+  uint32_t* abandoned = nullptr;   // [kMaxAbandoned] copy units a consumer wave gave up on
   RunCounters* ctr = nullptr;
   WgRecord* wg_rec = nullptr;      // MOE_TIMESTAMPS: [2][num_cus * producer_bpc] per launch
   CopyRecord* copy_rec = nullptr;  // MOE_TIMESTAMPS: [kMaxCopyRecords]
@@ -740,6 +741,7 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
   };
   if ((part_bytes && !try_hip(hipMalloc(&h->partials, part_bytes), "hipMalloc(partials)")) ||
       !try_hip(hipMalloc(&h->arrivals, flag_bytes), "hipMalloc(arrivals)") ||
+      !try_hip(hipMalloc(&h->abandoned, sizeof(uint32_t) * kMaxAbandoned), "hipMalloc(counters)") ||
       !try_hip(hipMemset(h->arrivals, 0, flag_bytes), "hipMemset(arrivals)") ||
       !try_hip(hipMalloc(&h->hws, hws_bytes), "hipMalloc(hws)") ||
       !try_hip(hipMalloc(&h->y, y_bytes), "hipMalloc(y)") ||
@@ -879,6 +881,8 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   ca.watchdog_ticks = watchdog_ticks(h);
   ca.early_shift = early_shift;
   ca.late_shift = late_shift;
+  ca.abandoned = h->abandoned;
+  ca.abandoned_cap = kMaxAbandoned;
   if (!own_cus) {
     ca.simd_waves = h->simd_waves;
     ca.max_waves_cu = (uint32_t)wpc;
@@ -1284,7 +1288,7 @@ int moe_stage_destroy(moe_stage_t h) {
   if (h->shared_prod) (void)hipStreamDestroy(h->shared_prod);
   for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->ctr, (void*)h->d_plan,
                   (void*)h->partials, (void*)h->arrivals, h->dev_ws, (void*)h->wg_rec, (void*)h->copy_rec,
-                  (void*)h->tile_ready, (void*)h->simd_waves})
+                  (void*)h->tile_ready, (void*)h->simd_waves, (void*)h->abandoned})
     if (p) (void)hipFree(p);
   for (uint8_t* p : h->h_stage)
     if (p) (void)hipHostFree(p);

@@ -976,6 +976,23 @@ __device__ __forceinline__ UnitCounts unit_counts(const ConsumerArgs& a) {
   return u;
 }
 
+// Copies unit `unit` with no flag wait (its rows are known complete).
+template <bool kOwn>
+__device__ __forceinline__ void copy_unit(const ConsumerArgs& a, const UnitCounts& uc, uint32_t unit, int lane) {
+  if (unit >= uc.n_units) return;
+  const bool early = unit < uc.early_units;
+  const uint32_t u = early ? unit : unit - uc.early_units;
+  const int32_t shift = early ? a.early_shift : a.late_shift;
+  const int32_t s = (early ? 0 : uc.n_early) + (int32_t)(u >> shift);
+  const int32_t part = (int32_t)(u & ((1u << shift) - 1));
+  const Segment sg = load_segment(a.segs + s);
+  const int64_t n16 = (int64_t)sg.rows * a.H / 8;
+  const int64_t i0 = (n16 * part) >> shift, i1 = (n16 * (part + 1)) >> shift;
+  const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H) + i0;
+  g_u32x4* dst = (g_u32x4*)(ret_buffer(a.ret, sg.dst_rank) + (int64_t)sg.slot0 * a.H) + i0;
+  copy_vectors<kOwn ? kCopyUnrollOwn : kCopyUnroll>(src, dst, i1 - i0, lane);
+}
+
 // The ticket loop of one wave: claim a copy unit, wait for its segment's flags, copy its part.
 // The first n_waves tickets are dealt transposed over the waves of the launch that map_grid and
 // map_wpg describe (ticket w_per_wg * b + w to unit w * map_grid + b), so the waves of one
@@ -1008,8 +1025,11 @@ __device__ __forceinline__ void consume_units(const ConsumerArgs& a, const UnitC
     const uint64_t t0 = ticks();
     bool expired = false;
     uint32_t backoff = 1;
-    for (int base = 0; base < sg.flag_count && !expired; base += 64) {
-      const bool mine = base + lane < sg.flag_count;
+    // The drain follows the producer and its tail kernel in their stream, so every row it copies
+    // is complete: it does not poll.
+    const int flag_count = (kOwn && a.role == kRoleDrain) ? 0 : sg.flag_count;
+    for (int base = 0; base < flag_count && !expired; base += 64) {
+      const bool mine = base + lane < flag_count;
       const uint32_t* fp = a.flags + sg.flag_begin + base + lane;
       for (;;) {
         const uint32_t v =
@@ -1030,10 +1050,17 @@ __device__ __forceinline__ void consume_units(const ConsumerArgs& a, const UnitC
     const uint64_t t_ready = ticks();
     waited += t_ready - t0;
     if (expired) {
+      // The wave gives up (the producer is not making progress beside it) and hands the unit to
+      // the drain launch, which copies it after the producer: the run is slow but complete.
       if (lane == 0) {
         __hip_atomic_fetch_add(&a.ctr->timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_fetch_or(&a.ctr->timeout_where, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_fetch_min(&a.ctr->timeout_seg, (uint32_t)s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (a.abandoned) {
+          const uint32_t k = __hip_atomic_fetch_add(&a.ctr->n_abandoned, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if (k < a.abandoned_cap)
+            __hip_atomic_store(&a.abandoned[k], unit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
       }
       break;
     }
@@ -1178,6 +1205,12 @@ void consumer_kernel(ConsumerArgs a) {
       backoff = backoff < 8 ? 2 * backoff : 8;
     }
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    // Units a consumer wave abandoned when its flag wait expired: every consumer wave has exited,
+    // so the list is complete, and the producer has finished, so the rows are.
+    const uint32_t n_ab = min(__hip_atomic_load(&a.ctr->n_abandoned, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+                              a.abandoned_cap);
+    for (uint32_t k = 0; a.abandoned && k < n_ab; ++k)
+      copy_unit<kOwn>(a, uc, __hip_atomic_load(&a.abandoned[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), lane);
   }
 }
 
@@ -1241,6 +1274,7 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
     a.ctr->units_pub = 0;
     a.ctr->prod_t0 = ~0ull;
     a.ctr->prod_t1 = 0;
+    a.ctr->n_abandoned = 0;
     if (a.plan_hdr) {
       a.plan_hdr->status = 0;
       a.plan_hdr->bad_row = INT_MAX;

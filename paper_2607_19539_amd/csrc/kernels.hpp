@@ -103,6 +103,8 @@ struct ConsumerArgs {
   uint32_t wait_go;        // 1: wait until ctr->go holds this run's epoch before anything else
   uint32_t map_wpg;        // waves per workgroup of the launch map_grid describes (0: this launch's)
   uint32_t max_waves_cu;   // beside the producer: consumer waves a compute unit keeps (0: no limit)
+  uint32_t* abandoned;     // [abandoned_cap] copy units whose flag wait expired, for the drain
+  uint32_t abandoned_cap;
 };
 // Consumer launch roles.  A counted consumer's waves each add one to ctr->cons_exit once their
 // stores are written back; a drain launch (after the producer, in its stream) claims the copy
@@ -212,5 +214,8 @@ constexpr int kWaveCounters = kXcds * (kSimdKeys + kCuKeys);
 // On compute units of its own: up to 128 VGPRs, four waves per SIMD (four workgroups per CU).
 constexpr int kConsumerOwnMinWaves = 4;
 constexpr int kConsumerOwnPerCu = 4;
+// Entries of the abandoned-unit list: a consumer wave abandons at most one unit (then exits), and a
+// launch has at most 16 waves on each of 256 compute units.
+constexpr uint32_t kMaxAbandoned = 4096;
 
 }  // namespace moe

@@ -115,6 +115,8 @@ struct RunCounters {
   // Timestamped runs only (100 MHz wall clock): first gate/up workgroup start and last
   // producer (down or tail) workgroup end.
   uint64_t prod_t0, prod_t1;
+  uint32_t n_abandoned;       // copy units whose flag wait expired (the drain copies them)
+  uint32_t pad_;
 };
 
 }  // namespace moe

@@ -160,19 +160,24 @@ def test_fullsize_stratified(name):
 def test_watchdog_expiry_is_reported():
     """With ready flags suppressed from the host, the consumer's bounded wait expires, the
     kernels exit, the run reports MOE_ETIMEOUT with the first segment that expired, and the next
-    run on a fresh handle is correct."""
+    run on a fresh handle is correct.  The expired run's output is complete too: each consumer
+    wave that gives up hands its unit to the drain launch, which copies it after the producer."""
     from tests.gpu_helpers import oracle_bufs
     wl = make_workload("tiny", owner=1)
     dw = DeviceWorkload(torch, wl)
-    with make_stage(wl, flags=B.MOE_LOCAL_DIRECT | B.MOE_TEST_NO_SIGNAL, watchdog_ms=20) as st:
-        st.run(*dw.args(), cu_split=8)
-        q = st.query(check=False)
-        assert q["rc"] == B.MOE_ETIMEOUT and q["timeout"] == 1
-        assert 0 <= q["timeout_segment"] < q["n_segments"]
-        assert "segment" in B.moe_stage_last_error(st.h)
-        q2 = st.query()
-        assert q2["timeout"] == 0   # reported once
     ref = oracle_bufs(wl)
+    for c, mode in ((8, B.MOE_SHARED_CUS), (64, B.MOE_SHARED_CUS), (16, 0)):
+        dw.fill()
+        with make_stage(wl, flags=B.MOE_LOCAL_DIRECT | B.MOE_TEST_NO_SIGNAL | mode, watchdog_ms=20) as st:
+            st.run(*dw.args(), cu_split=c)
+            q = st.query(check=False)
+            assert q["rc"] == B.MOE_ETIMEOUT and q["timeout"] == 1
+            assert 0 <= q["timeout_segment"] < q["n_segments"]
+            assert "segment" in B.moe_stage_last_error(st.h)
+            q2 = st.query()
+            assert q2["timeout"] == 0   # reported once
+        compare(dw.host_bufs(), ref)
+        log(f"watchdog: c={c} {'shared' if mode else 'partitioned'} expired run complete")
     with make_stage(wl) as st:
         dw.fill()
         st.run(*dw.args(), cu_split=8)
