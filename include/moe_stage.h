@@ -101,6 +101,13 @@ extern "C" {
                                       ran, and when each consumer copy unit began polling, saw its
                                       flags and finished its copy (moe_stage_records); the handle
                                       allocates the record buffers at create                   */
+#define MOE_WRITE_COUNTS (1u << 10) /* testing aid: every run counts, per logical row of its plan,
+                                      the 8-byte words stored into the receive buffers (by the down
+                                      epilogue, the tail kernel, the consumer, the drain or the
+                                      scatter), so a test can check that every routed row was
+                                      written exactly once and nothing else
+                                      (moe_stage_records, MOE_RECORDS_WRITES); the handle
+                                      allocates the counters at create                          */
 #define MOE_DIRECT_ALL (1u << 5)   /* ablation, serial runs only: the down epilogue writes every
                                       row straight to its slot in return_bufs and no scatter
                                       runs -- the bound of a stage with no consumer at all     */
@@ -319,13 +326,19 @@ int moe_stage_times(moe_stage_t h, int32_t reset, moe_stage_times_t* out);
  *   MOE_RECORDS_TILES     uint64_t[tile rows * down tiles per row]: when each down tile's ready
  *                         flag was raised (index = tile row * down tiles per row + column tile;
  *                         0 = no flag this run: local-only tile rows, serial runs).
+ *   MOE_RECORDS_WRITES    uint32_t[the handle's logical-row capacity]: with MOE_WRITE_COUNTS
+ *                         instead of MOE_TIMESTAMPS, the 8-byte words the last run stored into the
+ *                         receive buffers for each logical row of its plan (hidden / 4 for every
+ *                         routed row, 0 for padding rows and past the plan's rows).
  * With dst == NULL returns the bytes needed; else copies them (bytes must be at least that) and
- * returns MOE_OK.  Synchronizes with the last run.  MOE_EINVAL without MOE_TIMESTAMPS or a run.
+ * returns MOE_OK.  Synchronizes with the last run.  MOE_EINVAL without MOE_TIMESTAMPS (or, for
+ * MOE_RECORDS_WRITES, MOE_WRITE_COUNTS) or without a run.
  */
 #define MOE_RECORDS_PRODUCER 0
 #define MOE_RECORDS_COPY 1
 #define MOE_RECORDS_SPAN 2
 #define MOE_RECORDS_TILES 3
+#define MOE_RECORDS_WRITES 4
 typedef struct {
   uint32_t hw_id;   /* HW_ID register of the workgroup's first wave: wave slot [3:0], SIMD
                        [5:4], compute unit [11:8], shader array [12], shader engine [15:13]   */

@@ -22,8 +22,8 @@ LIB_PATH = os.path.join(PKG, "_lib", "libmoe_stage.so")
 MOE_OK, MOE_EINVAL, MOE_EROUTING, MOE_ECAPACITY, MOE_EHIP, MOE_ETIMEOUT, MOE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 (MOE_LOCAL_DIRECT, MOE_KERNEL_TIMING, MOE_POISON, MOE_TEST_NO_SIGNAL, MOE_SHARED_CUS, MOE_DIRECT_ALL,
  MOE_TEST_CONSUMER_ONLY, MOE_TEST_PLAN_NO_LDS, MOE_TIMESTAMPS) = 1, 2, 4, 8, 16, 32, 64, 128, 256
-MOE_TEST_PLAIN_COPY = 512
-MOE_RECORDS_PRODUCER, MOE_RECORDS_COPY, MOE_RECORDS_SPAN, MOE_RECORDS_TILES = 0, 1, 2, 3
+MOE_TEST_PLAIN_COPY, MOE_WRITE_COUNTS = 512, 1024
+MOE_RECORDS_PRODUCER, MOE_RECORDS_COPY, MOE_RECORDS_SPAN, MOE_RECORDS_TILES, MOE_RECORDS_WRITES = 0, 1, 2, 3, 4
 (MOE_PLAN_TILE_ROWS, MOE_PLAN_ITEMS, MOE_PLAN_ROW_X, MOE_PLAN_ROW_RANK, MOE_PLAN_ROW_SLOT, MOE_PLAN_SEGMENTS,
  MOE_PLAN_GROUPS, MOE_PLAN_QUEUES) = range(8)
 ERROR_NAMES = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EROUTING", -3: "MOE_ECAPACITY", -4: "MOE_EHIP",
@@ -403,12 +403,12 @@ def moe_stage_records(h, which: int) -> np.ndarray:
     one-element array)."""
     lib = load()
     ctype = {MOE_RECORDS_PRODUCER: moe_wg_record_t, MOE_RECORDS_COPY: moe_copy_record_t,
-             MOE_RECORDS_SPAN: moe_span_t, MOE_RECORDS_TILES: None}[which]
+             MOE_RECORDS_SPAN: moe_span_t, MOE_RECORDS_TILES: np.uint64, MOE_RECORDS_WRITES: np.uint32}[which]
     need = lib.moe_stage_records(h, int(which), None, 0)
     if need < 0:
         _check(int(need), h)
-    if ctype is None:
-        dt = np.dtype(np.uint64)
+    if ctype in (np.uint64, np.uint32):
+        dt = np.dtype(ctype)
     else:
         dt = np.dtype([(n, np.dtype(t)) for n, t in ctype._fields_], align=True)
         assert dt.itemsize == ctypes.sizeof(ctype)

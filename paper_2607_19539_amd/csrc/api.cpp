@@ -116,6 +116,7 @@ struct moe_stage_s {
   float* partials = nullptr;
   uint32_t* arrivals = nullptr;
   uint32_t* abandoned = nullptr;   // [kMaxAbandoned] copy units a consumer wave gave up on
+  uint32_t* wcount = nullptr;      // MOE_WRITE_COUNTS: [max logical rows] words stored per row
   RunCounters* ctr = nullptr;
   WgRecord* wg_rec = nullptr;      // MOE_TIMESTAMPS: [2][num_cus * producer_bpc] per launch
   CopyRecord* copy_rec = nullptr;  // MOE_TIMESTAMPS: [kMaxCopyRecords]
@@ -209,7 +210,7 @@ int check_config(const moe_stage_config_t* c) {
   constexpr uint32_t kKnownFlags = MOE_LOCAL_DIRECT | MOE_KERNEL_TIMING | MOE_POISON |
                                    MOE_TEST_NO_SIGNAL | MOE_SHARED_CUS | MOE_DIRECT_ALL |
                                    MOE_TEST_CONSUMER_ONLY | MOE_TEST_PLAN_NO_LDS | MOE_TIMESTAMPS |
-                                   MOE_TEST_PLAIN_COPY;
+                                   MOE_TEST_PLAIN_COPY | MOE_WRITE_COUNTS;
   if (c->flags & ~kKnownFlags) return MOE_EINVAL;
   if (c->band_rows < 0 || c->band_rows > 256 || (c->band_rows & (c->band_rows - 1)) != 0)
     return MOE_EINVAL;
@@ -246,6 +247,8 @@ int enqueue_init(moe_stage_s* h, bool overlapped, bool dev, int32_t n_tile_rows,
   ia.n_arrivals = n_tile_rows * h->down_per_row;
   ia.tile_ready = h->tile_ready;
   h->last_tiles = ia.n_arrivals;
+  ia.wcount = h->wcount;
+  ia.n_wcount = h->wcount ? h->max_lrows : 0;
   if (overlapped && (c.flags & MOE_SHARED_CUS)) ia.simd_waves = h->simd_waves;
   if (c.flags & MOE_POISON) {
     ia.poison = h->y;
@@ -482,6 +485,7 @@ ProducerArgs producer_args(moe_stage_s* h, const BlobLayout& lay, const void* x,
   a.split_k = h->cfg.down_split_k;
   a.partials = h->partials;
   a.arrivals = h->arrivals;
+  a.wcount = h->wcount;
   if (h->wg_rec) {
     a.wg_rec = h->wg_rec + (down ? (size_t)h->num_cus * h->producer_bpc : 0);
     a.ctr = h->ctr;
@@ -759,6 +763,10 @@ int moe_stage_create(const moe_stage_config_t* cfg, moe_stage_t* out) {
       !try_hip(hipMemset(h->ctr, 0, sizeof(RunCounters)), "hipMemset(counters)") ||
       !try_hip(hipMemset(&h->ctr->timeout_seg, 0xFF, sizeof(uint32_t)), "hipMemset(counters)"))
     return bail(MOE_EHIP);
+  if ((cfg->flags & MOE_WRITE_COUNTS) &&
+      (!try_hip(hipMalloc(&h->wcount, (size_t)h->max_lrows * 4), "hipMalloc(write counts)") ||
+       !try_hip(hipMemset(h->wcount, 0, (size_t)h->max_lrows * 4), "hipMemset(write counts)")))
+    return bail(MOE_EHIP);
   if (cfg->flags & MOE_TIMESTAMPS) {
     const size_t wg_bytes = 2 * (size_t)h->num_cus * h->producer_bpc * sizeof(WgRecord);
     const size_t cp_bytes = (size_t)kMaxCopyRecords * sizeof(CopyRecord);
@@ -883,6 +891,7 @@ static int run_overlapped(moe_stage_t h, bool dev, const void* x, const int32_t*
   ca.late_shift = late_shift;
   ca.abandoned = h->abandoned;
   ca.abandoned_cap = kMaxAbandoned;
+  ca.wcount = h->wcount;
   if (!own_cus) {
     ca.simd_waves = h->simd_waves;
     ca.max_waves_cu = (uint32_t)wpc;
@@ -1027,6 +1036,7 @@ static int run_serial(moe_stage_t h, bool dev, const void* x, const int32_t* off
   sa.row_slot = pa.row_slot;
   sa.n_lrows = &((const PlanHeader*)(h->d_plan + lay.hdr))->n_lrows;
   sa.H = h->cfg.hidden;
+  sa.wcount = h->wcount;
   if (tr) HIP_TRY(h, hipEventRecord(tr->ev[4], stream));
   const int64_t scatter_rows = known ? h->plan.n_lrows() : h->max_lrows;
   if (scatter_rows > 0 && !direct_all)
@@ -1231,6 +1241,17 @@ int64_t moe_stage_plan_copy(moe_stage_t h, int32_t which, void* dst, int64_t byt
 
 int64_t moe_stage_records(moe_stage_t h, int32_t which, void* dst, int64_t bytes) {
   if (!h) return MOE_EINVAL;
+  if (which == MOE_RECORDS_WRITES) {
+    if (!h->wcount) return set_err(h, MOE_EINVAL, "MOE_WRITE_COUNTS not set");
+    if (!h->ran) return set_err(h, MOE_EINVAL, "no run yet");
+    const int64_t need = h->max_lrows * 4;
+    if (!dst) return need;
+    if (bytes < need) return set_err(h, MOE_EINVAL, "destination too small");
+    const int rc = sync_counters(h);
+    if (rc) return rc;
+    HIP_TRY(h, hipMemcpy(dst, h->wcount, (size_t)need, hipMemcpyDeviceToHost));
+    return MOE_OK;
+  }
   if (!(h->cfg.flags & MOE_TIMESTAMPS)) return set_err(h, MOE_EINVAL, "MOE_TIMESTAMPS not set");
   if (!h->ran) return set_err(h, MOE_EINVAL, "no run yet");
   const int rc = sync_counters(h);
@@ -1288,7 +1309,7 @@ int moe_stage_destroy(moe_stage_t h) {
   if (h->shared_prod) (void)hipStreamDestroy(h->shared_prod);
   for (void* p : {(void*)h->hws, (void*)h->y, (void*)h->flags, (void*)h->ctr, (void*)h->d_plan,
                   (void*)h->partials, (void*)h->arrivals, h->dev_ws, (void*)h->wg_rec, (void*)h->copy_rec,
-                  (void*)h->tile_ready, (void*)h->simd_waves, (void*)h->abandoned})
+                  (void*)h->tile_ready, (void*)h->simd_waves, (void*)h->abandoned, (void*)h->wcount})
     if (p) (void)hipFree(p);
   for (uint8_t* p : h->h_stage)
     if (p) (void)hipHostFree(p);

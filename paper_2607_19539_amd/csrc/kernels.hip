@@ -114,6 +114,11 @@ __device__ __forceinline__ void store8_device(void* p, uint64_t v) {
   __hip_atomic_store((uint64_t*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// MOE_WRITE_COUNTS: counts `words` 8-byte words stored into the receive buffer for logical row lrow.
+__device__ __forceinline__ void count_words(uint32_t* wcount, int64_t lrow, uint32_t words) {
+  if (wcount) __hip_atomic_fetch_add(&wcount[lrow], words, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ uint64_t pack_f32x2(float lo, float hi) {
   return (uint64_t)__float_as_uint(lo) | ((uint64_t)__float_as_uint(hi) << 32);
 }
@@ -574,10 +579,12 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
         const int rank = rinfo[2 * m];
         if (rank >= 0 && n < H) {
           const uint64_t v = *(const uint64_t*)(lds + m * kDownOutStride + c8 * 8);
-          if (direct && rank == a.self_rank)
+          if (direct && rank == a.self_rank) {
             *(__attribute__((address_space(1))) uint64_t*)(a.ret[rank] + (int64_t)rinfo[2 * m + 1] * H + n) = v;
-          else
+            count_words(a.wcount, lrow, 1);
+          } else {
             store8_device(a.y + (int64_t)lrow * H + n, v);
+          }
         }
       }
     } else {
@@ -591,10 +598,12 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
         const int rank = rinfo[2 * m];
         if (rank >= 0 && n < H) {
           const u32x4 v = *(const u32x4*)(lds + m * kDownOutStride + c16 * 16);
-          if (direct_all || (direct && rank == a.self_rank))
+          if (direct_all || (direct && rank == a.self_rank)) {
             *(g_u32x4*)(a.ret[rank] + (int64_t)rinfo[2 * m + 1] * H + n) = v;
-          else
+            count_words(a.wcount, lrow, 2);
+          } else {
             *(g_u32x4*)(a.y + (int64_t)lrow * H + n) = v;
+          }
         }
       }
     }
@@ -837,9 +846,10 @@ __global__ __launch_bounds__(kProducerThreads) void tail_kernel(TailArgs ta) {
     const int rank = a.row_rank[lrow];
     if (rank >= 0 && n < H) {
       const uint64_t v = (uint64_t)pack_bf16x2(s0, s1) | ((uint64_t)pack_bf16x2(s2, s3) << 32);
-      if (direct_all || (direct && rank == a.self_rank))
+      if (direct_all || (direct && rank == a.self_rank)) {
         *(__attribute__((address_space(1))) uint64_t*)(a.ret[rank] + (int64_t)a.row_slot[lrow] * H + n) = v;
-      else if (signal)
+        count_words(a.wcount, lrow, 1);
+      } else if (signal)
         store8_device(a.y + (int64_t)lrow * H + n, v);
       else
         *(__attribute__((address_space(1))) uint64_t*)(a.y + (int64_t)lrow * H + n) = v;
@@ -976,8 +986,19 @@ __device__ __forceinline__ UnitCounts unit_counts(const ConsumerArgs& a) {
   return u;
 }
 
+// MOE_WRITE_COUNTS: a copied run of vectors [i0, i1) of a segment whose rows start at logical row
+// y_row0 counts, for each row it touches, the 8-byte words it wrote there.
+__device__ __forceinline__ void count_copy(uint32_t* wcount, int32_t y_row0, uint32_t per_row, uint32_t i0,
+                                           uint32_t i1, int lane) {
+  if (!wcount || i1 <= i0) return;
+  for (uint32_t r = i0 / per_row + (uint32_t)lane; r <= (i1 - 1) / per_row; r += 64) {
+    const uint32_t a = max(i0, r * per_row), b = min(i1, (r + 1) * per_row);
+    count_words(wcount, (int64_t)y_row0 + r, 2 * (b - a));
+  }
+}
+
 // Copies unit `unit` with no flag wait (its rows are known complete).
-template <bool kOwn>
+template <bool kOwn, bool kCount>
 __device__ __forceinline__ void copy_unit(const ConsumerArgs& a, const UnitCounts& uc, uint32_t unit, int lane) {
   if (unit >= uc.n_units) return;
   const bool early = unit < uc.early_units;
@@ -991,6 +1012,7 @@ __device__ __forceinline__ void copy_unit(const ConsumerArgs& a, const UnitCount
   const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H) + i0;
   g_u32x4* dst = (g_u32x4*)(ret_buffer(a.ret, sg.dst_rank) + (int64_t)sg.slot0 * a.H) + i0;
   copy_vectors<kOwn ? kCopyUnrollOwn : kCopyUnroll>(src, dst, i1 - i0, lane);
+  if constexpr (kCount) count_copy(a.wcount, sg.y_row0, (uint32_t)(a.H / 8), (uint32_t)i0, (uint32_t)i1, lane);
 }
 
 // The ticket loop of one wave: claim a copy unit, wait for its segment's flags, copy its part.
@@ -998,7 +1020,7 @@ __device__ __forceinline__ void copy_unit(const ConsumerArgs& a, const UnitCount
 // map_wpg describe (ticket w_per_wg * b + w to unit w * map_grid + b), so the waves of one
 // workgroup, which claim together, take parts of different segments; later tickets are units in
 // order.
-template <bool kOwn>
+template <bool kOwn, bool kCount>
 __device__ __forceinline__ void consume_units(const ConsumerArgs& a, const UnitCounts& uc, int lane) {
   const uint32_t wpg = a.map_wpg ? a.map_wpg : blockDim.x >> 6;
   const uint32_t map_grid = a.map_grid ? a.map_grid : gridDim.x;
@@ -1070,6 +1092,7 @@ __device__ __forceinline__ void consume_units(const ConsumerArgs& a, const UnitC
     const u32x4* src = (const u32x4*)(a.y + (int64_t)sg.y_row0 * a.H) + i0;  // wave-uniform
     g_u32x4* dst = (g_u32x4*)(ret_buffer(a.ret, sg.dst_rank) + (int64_t)sg.slot0 * a.H) + i0;
     copy_vectors<kOwn ? kCopyUnrollOwn : kCopyUnroll>(src, dst, i1 - i0, lane);
+    if constexpr (kCount) count_copy(a.wcount, sg.y_row0, (uint32_t)(a.H / 8), (uint32_t)i0, (uint32_t)i1, lane);
     if (a.rec && unit < a.rec_cap) {
       // Timestamped runs: the unit ends when its stores have completed.
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -1111,7 +1134,8 @@ __device__ __forceinline__ void count_exit(const ConsumerArgs& a, int lane) {
   if (lane == 0) __hip_atomic_fetch_add(&a.ctr->cons_exit, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <bool kOwn>
+// kCount: the MOE_WRITE_COUNTS variant, which also counts what it writes (outside the register budget).
+template <bool kOwn, bool kCount>
 __global__ __launch_bounds__(kConsumerThreads, kOwn ? kConsumerOwnMinWaves : kConsumerMinWaves)
 void consumer_kernel(ConsumerArgs a) {
   const int lane = threadIdx.x & 63;
@@ -1184,7 +1208,7 @@ void consumer_kernel(ConsumerArgs a) {
     const uint32_t wpg = a.map_wpg ? a.map_wpg : blockDim.x >> 6;
     tickets = next < max(a.map_grid * wpg, uc.n_units);
   }
-  if (tickets) consume_units<kOwn>(a, uc, lane);
+  if (tickets) consume_units<kOwn, kCount>(a, uc, lane);
   if (a.role == kRoleCounted) {
     count_exit(a, lane);
   } else if (kOwn && a.role == kRoleDrain && blockIdx.x == 0 && threadIdx.x < 64) {
@@ -1210,7 +1234,7 @@ void consumer_kernel(ConsumerArgs a) {
     const uint32_t n_ab = min(__hip_atomic_load(&a.ctr->n_abandoned, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
                               a.abandoned_cap);
     for (uint32_t k = 0; a.abandoned && k < n_ab; ++k)
-      copy_unit<kOwn>(a, uc, __hip_atomic_load(&a.abandoned[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), lane);
+      copy_unit<kOwn, kCount>(a, uc, __hip_atomic_load(&a.abandoned[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), lane);
   }
 }
 
@@ -1253,6 +1277,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
     const u32x4* src = (const u32x4*)(a.y + r * a.H);
     g_u32x4* dst = (g_u32x4*)(a.ret[rank] + (int64_t)a.row_slot[r] * a.H);
     for (int64_t i = threadIdx.x; i < per_row; i += blockDim.x) dst[i] = src[i];
+    if (threadIdx.x == 0) count_words(a.wcount, r, (uint32_t)(2 * per_row));
   }
 }
 
@@ -1283,6 +1308,8 @@ __global__ __launch_bounds__(256) void init_kernel(InitArgs a) {
   if (a.fill_ones)
     for (int64_t j = i; j < a.n_fill_ones; j += stride) a.fill_ones[j] = ~0u;
   for (int64_t j = i; j < a.n_arrivals; j += stride) a.arrivals[j] = 0;
+  if (a.wcount)
+    for (int64_t j = i; j < a.n_wcount; j += stride) a.wcount[j] = 0;
   if (a.tile_ready)
     for (int64_t j = i; j < a.n_arrivals; j += stride) a.tile_ready[j] = 0;
   if (a.simd_waves)
@@ -1335,16 +1362,24 @@ hipError_t launch_go(RunCounters* ctr, uint32_t epoch, hipStream_t s) {
 }
 
 hipError_t launch_drain(const ConsumerArgs& a, int grid, hipStream_t s) {
-  hipLaunchKernelGGL(consumer_kernel<true>, dim3(grid), dim3(kConsumerThreads), 0, s, a);
+  if (a.wcount)
+    hipLaunchKernelGGL((consumer_kernel<true, true>), dim3(grid), dim3(kConsumerThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((consumer_kernel<true, false>), dim3(grid), dim3(kConsumerThreads), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_consumer(const ConsumerArgs& a, bool own_cus, int grid, int threads, hipStream_t s) {
   if (threads <= 0 || threads > kConsumerThreads || threads % 64) return hipErrorInvalidValue;
-  if (own_cus)
-    hipLaunchKernelGGL(consumer_kernel<true>, dim3(grid), dim3(threads), 0, s, a);
+  const dim3 g(grid), b(threads);
+  if (own_cus && a.wcount)
+    hipLaunchKernelGGL((consumer_kernel<true, true>), g, b, 0, s, a);
+  else if (own_cus)
+    hipLaunchKernelGGL((consumer_kernel<true, false>), g, b, 0, s, a);
+  else if (a.wcount)
+    hipLaunchKernelGGL((consumer_kernel<false, true>), g, b, 0, s, a);
   else
-    hipLaunchKernelGGL(consumer_kernel<false>, dim3(grid), dim3(threads), 0, s, a);
+    hipLaunchKernelGGL((consumer_kernel<false, false>), g, b, 0, s, a);
   return hipGetLastError();
 }
 

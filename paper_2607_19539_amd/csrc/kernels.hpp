@@ -66,6 +66,7 @@ struct ProducerArgs {
   RunCounters* ctr;        // timestamped runs: the producer span (prod_t0 / prod_t1)
   uint64_t* tile_ready;    // timestamped runs: [tiles] when each down tile's flag was raised
   RunCounters* go_ctr;     // gate/up launch of an overlapped run: publishes go = epoch as it starts
+  uint32_t* wcount;        // MOE_WRITE_COUNTS: [logical rows] 8-byte words stored into receive buffers
 };
 
 // The tail kernel: finishes the split down tiles after the down launch.  Reads the plan's tile
@@ -105,6 +106,7 @@ struct ConsumerArgs {
   uint32_t max_waves_cu;   // beside the producer: consumer waves a compute unit keeps (0: no limit)
   uint32_t* abandoned;     // [abandoned_cap] copy units whose flag wait expired, for the drain
   uint32_t abandoned_cap;
+  uint32_t* wcount;        // MOE_WRITE_COUNTS: [logical rows] 8-byte words stored into receive buffers
 };
 // Consumer launch roles.  A counted consumer's waves each add one to ctr->cons_exit once their
 // stores are written back; a drain launch (after the producer, in its stream) claims the copy
@@ -121,6 +123,7 @@ struct ScatterArgs {
   const int32_t* row_slot;
   const int64_t* n_lrows;  // device: logical rows of the plan
   int32_t H;
+  uint32_t* wcount;        // MOE_WRITE_COUNTS: [logical rows] 8-byte words stored into receive buffers
 };
 
 struct InitArgs {
@@ -129,6 +132,8 @@ struct InitArgs {
   int64_t poison_elems;    // multiple of 8
   uint32_t* arrivals;      // split-K arrival counters to zero
   int32_t n_arrivals;
+  uint32_t* wcount;        // optional: write counts to zero
+  int64_t n_wcount;
   uint64_t* tile_ready;    // optional: per-tile flag times to zero (as many as arrivals)
   uint32_t* simd_waves;    // optional: consumer per-SIMD wave counts to zero
   uint32_t* publish;       // optional: ready flags to set to `epoch` (consumer-only measurement)

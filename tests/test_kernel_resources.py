@@ -53,8 +53,8 @@ def test_no_kernel_spills(kernels):
 def test_consumer_fits_beside_a_producer_wave(kernels):
     """The shared-CU consumer variant (kOwn = false) leaves a producer wave its registers; the
     variant for compute units of its own keeps four waves per SIMD."""
-    (cons,) = by_name(kernels, "consumer_kernelILb0E").values()
-    (own,) = by_name(kernels, "consumer_kernelILb1E").values()
+    (cons,) = by_name(kernels, "consumer_kernelILb0ELb0E").values()   # the MOE_WRITE_COUNTS
+    (own,) = by_name(kernels, "consumer_kernelILb1ELb0E").values()    # variants are outside it
     assert int(own["vgpr_count"]) <= 128
     granule = 8  # registers are allocated to a wave in blocks of 8
     cons_alloc = -(-int(cons["vgpr_count"]) // granule) * granule
