@@ -896,21 +896,22 @@ __global__ __launch_bounds__(kProducerThreads) void tail_kernel(TailArgs ta) {
 // Copies n 16-byte vectors from src to dst, kU per lane per chunk, with two register buffers in
 // turn so one chunk's loads are in flight while the other's stores issue.
 //
-// The staged rows are read with agent-scope coherent, streaming buffer loads (cache policy sc1 nt):
-// each load sees what the producer stored at the coherence point, whichever XCD it ran on, so the
-// copy needs no acquire fence after the flag poll.  On gfx950 an agent-scope acquire invalidates
-// the XCD's whole L2, which would throw away the operand panels the producer workgroups on that
-// XCD keep there (one invalidation per copy unit while the down launch runs); the streaming hint
-// keeps the copied lines from displacing those panels.  The source run is below 4 GiB (the
-// handle's staged output is), so 32-bit buffer offsets reach all of it.
-constexpr int kLoadAgentStream = 16 | 2;  // buffer-load cache policy: sc1 (agent scope) | nt
+// The staged rows are read with agent-scope coherent buffer loads (cache policy sc1): each load
+// sees what the producer stored at the coherence point, whichever XCD it ran on, so the copy needs
+// no acquire fence after the flag poll.  On gfx950 an agent-scope acquire invalidates the XCD's
+// whole L2, which would throw away the operand panels the producer workgroups on that XCD keep
+// there (one invalidation per copy unit while the down launch runs).  No streaming (nt) hint: rows
+// the producer has just written are often still in the memory-side cache, and an nt load of them
+// went slower (a 100 MB copy by 10-30 %) with no gain for the producer beside it.  The source run
+// is below 4 GiB (the handle's staged output is), so 32-bit buffer offsets reach all of it.
+constexpr int kLoadAgent = 16;  // buffer-load cache policy: sc1 (agent scope)
 
 template <int kU>
 __device__ __forceinline__ void copy_vectors(const void* src, g_u32x4* __restrict__ dst, int64_t n, int lane) {
   constexpr int64_t kStep = (int64_t)kU * 64;
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(src), 0, (int)(uint32_t)min<int64_t>(n * 16, INT_MAX), kBufferRsrcWord3);
-  auto ld = [&](int64_t i) { return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(i * 16), 0, kLoadAgentStream); };
+  auto ld = [&](int64_t i) { return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(i * 16), 0, kLoadAgent); };
   const int64_t nfull = n / kStep;
   u32x4 a[kU], b[kU];
   auto load = [&](u32x4 (&r)[kU], int64_t c) {
