@@ -609,8 +609,11 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
     }
     // Every wave's output stores have completed (the staged rows at the coherence point)
     // before wave 0 raises the flag; a plain barrier does not wait for other waves' stores.
-    wait_vm_and_barrier<0>();
+    // A tile that raises no flag does not wait: its stores drain under the next item's first
+    // operand loads (the staged tile in LDS is free once the loop's barrier has passed, every
+    // wave's LDS reads for its stores having returned).
     if (signal && (tr.has_remote || !direct)) {
+      wait_vm_and_barrier<0>();
       if (tid == 0) {
         if (a.tile_ready) a.tile_ready[tile] = ticks();
         __hip_atomic_store(&a.flags[tile], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -669,7 +672,18 @@ __device__ __forceinline__ uint32_t item_tile_row(uint32_t item) {
   return (item >> kItemRowShift) & (uint32_t)(kMaxTileRows - 1);
 }
 
+// A load through the scalar cache: the plan arrays are written before the launch and only read
+// during it.  Scalar loads count on lgkmcnt, so waiting for one does not also wait for the vector
+// stores issued before it (vmcnt counts loads and stores in issue order).
+template <class T>
+__device__ __forceinline__ T load_scalar(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)p;
+}
+
 // Resolves the claim (the other queues in turn if queue q ran dry) and loads the descriptor.
+// Thread 0 runs this while the epilogue's stores are in flight: the item word and the tile row
+// come through the scalar cache at a wave-uniform address, so the wait for them is not a wait
+// for those stores.
 __device__ __forceinline__ void next_resolve(const ProducerArgs& a, NextItem& n, uint32_t end) {
   if (n.done) return;
   if (n.ticket < (uint32_t)(n.q1 - n.q0)) {
@@ -678,9 +692,16 @@ __device__ __forceinline__ void next_resolve(const ProducerArgs& a, NextItem& n,
     n.q = (n.q + 1) & (kXcds - 1);
     n.pos = claim_item(a, n.q, end, kXcds - 1);
   }
+  n.pos = __builtin_amdgcn_readfirstlane(n.pos);  // thread 0's value: one lane is active
   if (n.pos < end) {
-    n.item = a.items[n.pos];
-    n.tr = a.tile_rows[item_tile_row(n.item)];
+    n.item = load_scalar(a.items + n.pos);
+    const int32_t* w = (const int32_t*)(a.tile_rows + item_tile_row(n.item));
+    n.tr.expert = load_scalar(w + 0);
+    n.tr.lrow0 = load_scalar(w + 1);
+    n.tr.nvalid = load_scalar(w + 2);
+    n.tr.has_remote = load_scalar(w + 3);
+    n.tr.split = load_scalar(w + 4);
+    n.tr.part_base = load_scalar(w + 5);
   }
   n.done = true;
 }
