@@ -749,6 +749,17 @@ def compact_line(args, detail, name, raw, wl):
     return out
 
 
+def short_floats(o):
+    """The headline line with every float kept to 6 significant digits (the line stays a few KB)."""
+    if isinstance(o, float):
+        return float(f"{o:.6g}")
+    if isinstance(o, dict):
+        return {k: short_floats(v) for k, v in o.items()}
+    if isinstance(o, list):
+        return [short_floats(v) for v in o]
+    return o
+
+
 def main():
     t_start = time.time()
     args = parse()
@@ -820,7 +831,7 @@ def main():
             json.dump(detail, f, indent=1)
         log(f"detail written to {args.detail_out}")
     log(f"done in {time.time() - t_start:.0f} s")
-    print(json.dumps(line), flush=True)
+    print(json.dumps(short_floats(line)), flush=True)
 
 
 if __name__ == "__main__":
