@@ -634,16 +634,52 @@ __device__ __forceinline__ uint32_t hw_id() {
   return (uint32_t)__builtin_amdgcn_s_getreg(kHwRegHwId | (0 << 6) | ((32 - 1) << 11));
 }
 
-// Claims the next item of this launch: from queue q (initially the workgroup's own XCD's),
-// moving on to the next queue whenever one is empty.  Returns `end` once all are empty.
-// Claims the next item from queue q, then from the following queues once q is empty; `tries`
-// queues are tried in all.  Returns the item's position in a.items, or `end`.
-__device__ __forceinline__ uint32_t claim_item(const ProducerArgs& a, uint32_t& q, uint32_t end, int tries = kXcds) {
-  for (; tries > 0; --tries) {
+// A load through the scalar cache: the plan arrays are written before the launch and only read
+// during it.  Scalar loads count on lgkmcnt, so waiting for one does not also wait for the vector
+// stores issued before it (vmcnt counts loads and stores in issue order).
+template <class T>
+__device__ __forceinline__ T load_scalar(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)p;
+}
+
+// Claims the next item of this launch (thread 0): from queue q first when try_q (the workgroup's
+// own XCD's queue, or the one it last took from), else from the first queue at or after q that
+// still holds items.  Returns the item's position in a.items, or `end` once every queue is empty.
+// The queues' claim counts are read together, one round trip, instead of one atomic per empty
+// queue in turn: at a launch's end every workgroup learns that all queues are empty in one round
+// trip, not eight.  Counts only grow, so a queue seen exhausted stays exhausted; each failed claim
+// exhausts one more queue, so the loop ends within kXcds + 1 passes.
+__device__ __forceinline__ uint32_t claim_item(const ProducerArgs& a, uint32_t& q, uint32_t end, bool try_q) {
+  if (try_q) {
     const uint32_t i = atomicAdd(&a.claim[q], 1u);
     const int32_t q0 = a.queue[q], q1 = a.queue[q + 1];
     if (i < (uint32_t)(q1 - q0)) return (uint32_t)q0 + i;
-    q = (q + 1) & (kXcds - 1);
+  }
+  int32_t bound[kXcds + 1];
+#pragma unroll
+  for (int x = 0; x <= kXcds; ++x) bound[x] = load_scalar(a.queue + x);
+  for (int pass = 0; pass <= kXcds; ++pass) {
+    uint32_t cnt[kXcds];
+#pragma unroll
+    for (int x = 0; x < kXcds; ++x) cnt[x] = __hip_atomic_load(&a.claim[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t open = 0;
+#pragma unroll
+    for (int x = 0; x < kXcds; ++x) open |= (cnt[x] < (uint32_t)(bound[x + 1] - bound[x]) ? 1u : 0u) << x;
+    if (open == 0) return end;
+    const uint32_t rot = ((open >> q) | (open << (kXcds - q))) & ((1u << kXcds) - 1);
+    const uint32_t x = (q + (uint32_t)__builtin_ctz(rot)) & (kXcds - 1);
+    int32_t x0 = bound[0], x1 = bound[1];
+#pragma unroll
+    for (int y = 1; y < kXcds; ++y)
+      if ((uint32_t)y == x) {
+        x0 = bound[y];
+        x1 = bound[y + 1];
+      }
+    const uint32_t i = atomicAdd(&a.claim[x], 1u);
+    if (i < (uint32_t)(x1 - x0)) {
+      q = x;
+      return (uint32_t)x0 + i;
+    }
   }
   return end;
 }
@@ -672,14 +708,6 @@ __device__ __forceinline__ uint32_t item_tile_row(uint32_t item) {
   return (item >> kItemRowShift) & (uint32_t)(kMaxTileRows - 1);
 }
 
-// A load through the scalar cache: the plan arrays are written before the launch and only read
-// during it.  Scalar loads count on lgkmcnt, so waiting for one does not also wait for the vector
-// stores issued before it (vmcnt counts loads and stores in issue order).
-template <class T>
-__device__ __forceinline__ T load_scalar(const T* p) {
-  return *(const __attribute__((address_space(4))) T*)p;
-}
-
 // Resolves the claim (the other queues in turn if queue q ran dry) and loads the descriptor.
 // Thread 0 runs this while the epilogue's stores are in flight: the item word and the tile row
 // come through the scalar cache at a wave-uniform address, so the wait for them is not a wait
@@ -689,8 +717,7 @@ __device__ __forceinline__ void next_resolve(const ProducerArgs& a, NextItem& n,
   if (n.ticket < (uint32_t)(n.q1 - n.q0)) {
     n.pos = (uint32_t)n.q0 + n.ticket;
   } else {
-    n.q = (n.q + 1) & (kXcds - 1);
-    n.pos = claim_item(a, n.q, end, kXcds - 1);
+    n.pos = claim_item(a, n.q, end, false);  // queue q ran dry: any queue that has items
   }
   n.pos = __builtin_amdgcn_readfirstlane(n.pos);  // thread 0's value: one lane is active
   if (n.pos < end) {
@@ -754,7 +781,7 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
   NextItem nx;  // meaningful in thread 0, which does the claiming
   if (tid == 0) {
     nx.q = xcc_id();
-    nx.pos = claim_item(a, nx.q, end);
+    nx.pos = claim_item(a, nx.q, end, true);
     if (nx.pos < end) {
       atomicAdd(a.active, 1u);
       nx.item = a.items[nx.pos];
