@@ -183,9 +183,10 @@ __device__ __forceinline__ uint32_t dma_lane_off(int lane, int p, uint32_t strid
 // only block 2ks+4 allowed in flight.  The last two K steps are peeled so each wait count
 // is a constant on a straight path.
 // ---------------------------------------------------------------------------
-template <bool kGatherX>
+template <bool kGatherX, class Late>
 __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const DmaRows& w, const DmaRows& x,
-                                         const uint32_t (&xoff)[kDmaPerThread], int K, f32x16 (&acc)[4][4]) {
+                                         const uint32_t (&xoff)[kDmaPerThread], int K, f32x16 (&acc)[4][4],
+                                         Late&& late) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave & 1, wm = wave >> 1;
@@ -290,6 +291,7 @@ __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const DmaRow
   };
   int ks = 0;
   for (; ks + 2 < nk; ++ks) step(ks, std::integral_constant<int, 0>{});
+  late();  // two K steps (or one) before the end
   if (ks + 1 < nk) step(ks++, std::integral_constant<int, 1>{});
   step(ks, std::integral_constant<int, 2>{});
   // All waves are done reading LDS before the epilogue or the next tile reuses it.
@@ -307,9 +309,9 @@ __device__ __forceinline__ void tile_mma(uint8_t* __restrict__ lds, const DmaRow
 // thread 0 fetches the next item's descriptor there, and the stores that follow hide part of
 // the load latency.  (Branching there while the accumulators are still live, right after the
 // K loop, made the compiler spill them.)
-template <bool down, int kSplit, class Hook>
+template <bool down, int kSplit, class Late, class Hook>
 __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t item, const TileRow& tr,
-                                              uint8_t* lds, uint32_t* words, Hook&& hook) {
+                                              uint8_t* lds, uint32_t* words, Late&& late, Hook&& hook) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave: keeps bases scalar
   const int wn = wave & 1, wm = wave >> 1;
@@ -386,7 +388,7 @@ __device__ __forceinline__ void producer_item(const ProducerArgs& a, uint32_t it
   f32x16 acc[4][4];
   w.base += (size_t)(kbeg / kTileK) * w.step;
   x.base += (size_t)(kbeg / kTileK) * x.step;
-  tile_mma<!down>(lds, w, x, xoff, klen, acc);
+  tile_mma<!down>(lds, w, x, xoff, klen, acc, late);
 
   if constexpr (!down) {
     // Gated activation a = bf16(silu(g) * u): lane values -> LDS tile [256 rows][128 features].
@@ -798,20 +800,24 @@ __global__ __launch_bounds__(kProducerThreads, 1) void producer_kernel(ProducerA
   while (cur < end) {
     ++n_items;
     __syncthreads();  // every wave has read the words before the operand ring overwrites them
-    // Claim the next item now; thread 0 resolves the claim and fetches the item's descriptor
-    // during the epilogue, and passes it on through LDS at the end.
-    if (tid == 0) next_claim(a, nx);
+    // Thread 0 claims the next item two K steps before this one ends, late enough that a
+    // workgroup slowed down (by consumer waves beside it) does not hold a claim on an item that
+    // another one could start sooner, and early enough that the claim has returned by the
+    // epilogue, where the item's descriptor is fetched; it is passed on through LDS at the end.
+    auto late = [&]() {
+      if (tid == 0) next_claim(a, nx);
+    };
     auto hook = [&]() {
       if (tid == 0) next_resolve(a, nx, end);
     };
     if constexpr (kSplit < 0) {
       // Split per tile row: whole tiles take the plain epilogue, split rows the part path.
       if (tr.split == 1)
-        producer_item<down, 1>(a, item, tr, lds, words, hook);
+        producer_item<down, 1>(a, item, tr, lds, words, late, hook);
       else
-        producer_item<down, 0>(a, item, tr, lds, words, hook);
+        producer_item<down, 0>(a, item, tr, lds, words, late, hook);
     } else {
-      producer_item<down, kSplit>(a, item, tr, lds, words, hook);
+      producer_item<down, kSplit>(a, item, tr, lds, words, late, hook);
     }
     if (tid == 0) next_publish(a, nx, end, words);
     __syncthreads();
